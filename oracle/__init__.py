@@ -1,0 +1,183 @@
+"""TEST INFRASTRUCTURE: the CPU oracle for one HARL search round.
+
+A ctypes wrapper over ``harl_oracle.c`` (plain C, fp64, optional OpenMP).  It computes, from the
+paper's definitions, what the HIP path must reproduce: per-program cost-model scores (GBDT over
+statement rows, summed per program), the actor/critic forward with its argmax action, and the
+top-K / running-heap selection.  Only ``tests/``, the package's ``smoke()`` check and
+``bench.py``'s ``cpu_baseline`` leg may import this package; the product path never does.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "harl_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "_liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+CFLAGS = ["-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-fno-fast-math", "-Wall", "-Wextra"]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into ``oracle/_liboracle.so`` (plain -O2, no fast-math)."""
+    global _lib
+    with _lock:
+        if force or not os.path.exists(_LIB_PATH):
+            tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+            subprocess.run(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+            os.replace(tmp, _LIB_PATH)
+            _lib = None
+    return _LIB_PATH
+
+
+def _bind(lib):
+    P = ctypes.c_void_p
+    i32, i64, dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    lib.oracle_score_round.argtypes = [i32, i32, P, P, P, P, P, P, P, dbl, i32, P, i64, i32,
+                                       P, i32, P, P, P, ctypes.c_int]
+    lib.oracle_policy_step.argtypes = [ctypes.c_int, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
+                                       P, i32, P, P, P, P, P, P, ctypes.c_int]
+    lib.oracle_topk.argtypes = [P, i64, i32, i64, P, P]
+    lib.oracle_merge.argtypes = [P, P, i32, P, i64, i64]
+    lib.oracle_max_threads.argtypes = []
+    lib.oracle_round_bf16.argtypes = [dbl]
+    lib.oracle_round_bf16.restype = dbl
+    for f in (lib.oracle_score_round, lib.oracle_policy_step, lib.oracle_topk,
+              lib.oracle_merge, lib.oracle_max_threads):
+        f.restype = ctypes.c_int
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build(force=True)
+        with _lock:
+            if _lib is None:
+                _lib = _bind(ctypes.CDLL(_LIB_PATH))
+    return _lib
+
+
+def use_library(path: str | None):
+    """Point this wrapper at another build of the oracle source (the tests use this to check that
+    their pins reject deliberately broken copies); ``None`` restores the default build."""
+    global _lib
+    with _lock:
+        _lib = None if path is None else _bind(ctypes.CDLL(path))
+
+
+def round_bf16(v: float) -> float:
+    """The oracle's fp64 -> bf16 rounding (nearest, ties to even), returned as a float."""
+    return float(_load().oracle_round_bf16(float(v)))
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def score_round(ens: dict, features: np.ndarray, prog_ptr: np.ndarray, n_rows: int | None = None,
+                threads: int = 0) -> dict:
+    """Cost-model scores of every program (GBDT per statement row, summed per program).
+
+    ``features`` is the feature-major matrix ``[n_features][ld]``.  Returns fp64 ``prog`` and
+    ``stmt`` scores, their fp32 roundings ``prog32`` / ``stmt32``, and ``scale`` (sum of |terms|
+    per program, the basis of the scale-relative tolerance).
+    """
+    lib = _load()
+    X = _c(features, np.float32)
+    ptr = _c(prog_ptr, np.int32)
+    n_prog = ptr.size - 1
+    n_rows = int(ptr[-1]) if n_rows is None else n_rows
+    arrs = dict(root=_c(ens["root"], np.int32), feature=_c(ens["feature"], np.int32),
+                threshold=_c(ens["threshold"], np.float32), left=_c(ens["left"], np.int32),
+                right=_c(ens["right"], np.int32), default_left=_c(ens["default_left"], np.uint8),
+                leaf_value=_c(ens["leaf_value"], np.float32))
+    prog = np.zeros(n_prog, dtype=np.float64)
+    stmt = np.zeros(n_rows, dtype=np.float64)
+    scale = np.zeros(n_prog, dtype=np.float64)
+    rc = lib.oracle_score_round(int(ens["n_trees"]), arrs["feature"].size, _p(arrs["root"]),
+                                _p(arrs["feature"]), _p(arrs["threshold"]), _p(arrs["left"]),
+                                _p(arrs["right"]), _p(arrs["default_left"]), _p(arrs["leaf_value"]),
+                                float(ens.get("base_score", 0.0)), int(ens["n_features"]), _p(X),
+                                X.shape[1], n_rows, _p(ptr), n_prog, _p(prog), _p(stmt), _p(scale),
+                                threads)
+    if rc != 0:
+        raise ValueError("oracle_score_round failed (%d): malformed input" % rc)
+    return dict(prog=prog, stmt=stmt, scale=scale, prog32=prog.astype(np.float32),
+                stmt32=stmt.astype(np.float32))
+
+
+def policy_step(pol: dict, states: np.ndarray, threads: int = 0, want_probs: bool = True) -> dict:
+    """Actor/critic forward for every state: action (lowest-index argmax of the logits), value,
+    logits, softmax probabilities and per-output tolerance scales (fp64)."""
+    lib = _load()
+    dt = 1 if pol["dtype"] == "bf16" else 0
+    wdt = np.uint16 if dt else np.float32
+    S, H1, H2, A = int(pol["s"]), int(pol["h1"]), int(pol["h2"]), int(pol["a"])
+    st = _c(states, wdt)
+    B = st.shape[0]
+    assert st.shape == (B, S)
+    w = {k: _c(pol[k], wdt) for k in ("w1", "w2", "wa", "wv")}
+    b = {k: _c(pol[k], np.float32) for k in ("b1", "b2", "ba", "bv")}
+    action = np.zeros(B, dtype=np.int32)
+    value = np.zeros(B, dtype=np.float64)
+    logits = np.zeros((B, A), dtype=np.float64)
+    probs = np.zeros((B, A), dtype=np.float64) if want_probs else None
+    lscale = np.zeros((B, A), dtype=np.float64)
+    vscale = np.zeros(B, dtype=np.float64)
+    rc = lib.oracle_policy_step(dt, S, H1, H2, A, _p(w["w1"]), _p(b["b1"]), _p(w["w2"]), _p(b["b2"]),
+                                _p(w["wa"]), _p(b["ba"]), _p(w["wv"]), _p(b["bv"]), _p(st), B,
+                                _p(action), _p(value), _p(logits), _p(probs), _p(lscale), _p(vscale),
+                                threads)
+    if rc != 0:
+        raise ValueError("oracle_policy_step failed (%d)" % rc)
+    return dict(action=action, value=value, logits=logits, probs=probs, logit_scale=lscale,
+                value_scale=vscale)
+
+
+def topk(score: np.ndarray, k: int, index_base: int = 0):
+    """The k best scores ranked by (score desc, index asc); returns (scores fp32, indices int64)."""
+    lib = _load()
+    s = _c(score, np.float32)
+    out_s = np.zeros(k, dtype=np.float32)
+    out_i = np.zeros(k, dtype=np.int64)
+    rc = lib.oracle_topk(_p(s), s.size, k, index_base, _p(out_s), _p(out_i))
+    if rc != 0:
+        raise ValueError("oracle_topk failed (%d)" % rc)
+    return out_s, out_i
+
+
+RESET_SCORE = np.float32(-np.inf)
+RESET_INDEX = np.int64(np.iinfo(np.int64).max)
+
+
+def reset(k: int):
+    """An empty running heap of capacity k: every slot (-inf, INT64_MAX)."""
+    return np.full(k, RESET_SCORE, dtype=np.float32), np.full(k, RESET_INDEX, dtype=np.int64)
+
+
+def merge(run_score: np.ndarray, run_index: np.ndarray, score: np.ndarray, index_base: int):
+    """running <- top-k(running U {(score[i], index_base + i)}); returns new (scores, indices)."""
+    lib = _load()
+    rs = np.array(run_score, dtype=np.float32, copy=True)
+    ri = np.array(run_index, dtype=np.int64, copy=True)
+    s = _c(score, np.float32)
+    rc = lib.oracle_merge(_p(rs), _p(ri), rs.size, _p(s), s.size, index_base)
+    if rc != 0:
+        raise ValueError("oracle_merge failed (%d)" % rc)
+    return rs, ri

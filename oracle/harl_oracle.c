@@ -1,0 +1,305 @@
+/*
+ * harl_oracle.c -- TEST INFRASTRUCTURE, not part of the product path.
+ *
+ * A plain, slow, obviously correct CPU implementation of one HARL search round's candidate
+ * evaluation, written from the paper (Zhang, He, Zhang: "HARL: Hierarchical Adaptive
+ * Reinforcement Learning Based Auto Scheduler for Neural Networks", ICPP'22):
+ *
+ *   oracle_score_round   cost-model prediction C(S') of every candidate (Algorithm 1, the reward
+ *                        step and the heap-insert step; Section 4.3; the cost model is XGBoost,
+ *                        Section 6.1 and Appendix A.2), here a GBDT applied to each statement's
+ *                        feature row and summed over the statements of a program;
+ *   oracle_policy_step   actor pi_theta(M|S) and critic V(S) forward (Algorithm 1, action
+ *                        selection; Eq. 6 for the critic's role; Section 4.3), a shared ReLU
+ *                        trunk with a linear actor head and a linear value head;
+ *   oracle_topk          "select top-K states from the heap H" (Algorithm 1, top-K phase;
+ *                        Section 4.3, Top-K Selection Phase): the K best predicted scores;
+ *   oracle_merge         the heap H accumulating candidates across steps (Algorithm 1).
+ *
+ * All arithmetic on scores and activations is fp64 over the given fp32 / bf16 input values.
+ * Nothing here is blocked, fused or reordered beyond the definitions.  Only tests/, the package's
+ * smoke check and bench.py's CPU-baseline leg may load this library; the HIP path shares no code
+ * with it.  Built with plain -O2 (never -ffast-math: NaN tests must survive).
+ *
+ * Readings where the paper is silent (each also listed in the design doc):
+ *   - a split sends x left iff x < threshold (strict), x == threshold goes right;
+ *   - only NaN is missing; a missing value follows the node's default direction;
+ *   - a program's score is base_score + the sum of its statements' scores;
+ *   - larger score is better; ranking is by (score desc, index asc); -0 ties +0; NaN ranks last;
+ *   - bf16 policies round the hidden activations h1, h2 to bf16 (nearest, ties to even) after
+ *     bias and ReLU; fp32 policies keep them exact (fp64 here);
+ *   - the action is the lowest index attaining the maximum logit; probabilities are the softmax
+ *     of the logits.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ENOMEM (-5)
+
+static void set_threads(int n_threads) {
+#ifdef _OPENMP
+    if (n_threads > 0) omp_set_num_threads(n_threads);
+#else
+    (void)n_threads;
+#endif
+}
+
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------------------------- */
+/* Cost model: GBDT over per-statement feature rows, summed per program                         */
+/* ------------------------------------------------------------------------------------------- */
+
+/* Walk one tree from its root for statement row r; return the reached leaf's node id, or -1 if the
+ * walk does not end within n_nodes steps or leaves the node range (a malformed tree). */
+static int64_t walk_tree(int32_t root, int32_t n_nodes, const int32_t *feature, const float *threshold,
+                         const int32_t *left, const int32_t *right, const uint8_t *default_left,
+                         const float *X, int64_t ld, int32_t n_features, int64_t r) {
+    int64_t n = root;
+    for (int32_t step = 0; step <= n_nodes; ++step) {
+        if (n < 0 || n >= n_nodes) return -1;
+        int32_t f = feature[n];
+        if (f < 0) return n;                       /* a leaf */
+        if (f >= n_features) return -1;
+        float v = X[(int64_t)f * ld + r];
+        if (isnan(v))
+            n = default_left[n] ? left[n] : right[n];
+        else
+            n = (v < threshold[n]) ? left[n] : right[n];
+    }
+    return -1;
+}
+
+/*
+ * For every program p and statement row r in [prog_ptr[p], prog_ptr[p+1]):
+ *     stmt[r]  = sum over trees t of leaf_t(x_r)                    (fp64)
+ *     prog[p]  = base_score + sum over its rows of stmt[r]          (fp64)
+ *     scale[p] = |base_score| + sum over its rows and trees of |leaf_t(x_r)|
+ * X is feature-major: feature f of row r is X[f*ld + r].  Outputs are fp64; stmt may be NULL.
+ * Returns 0, or -1 on a malformed input (bad prog_ptr, malformed tree).
+ */
+int oracle_score_round(int32_t n_trees, int32_t n_nodes, const int32_t *root, const int32_t *feature,
+                       const float *threshold, const int32_t *left, const int32_t *right,
+                       const uint8_t *default_left, const float *leaf_value, double base_score,
+                       int32_t n_features, const float *X, int64_t ld, int32_t n_rows,
+                       const int32_t *prog_ptr, int32_t n_prog,
+                       double *prog, double *stmt, double *scale, int n_threads) {
+    if (n_prog < 0 || n_rows < 0 || ld < n_rows || n_trees < 0) return ORACLE_EINVAL;
+    if (n_prog > 0 && (prog_ptr[0] != 0 || prog_ptr[n_prog] != n_rows)) return ORACLE_EINVAL;
+    for (int32_t p = 0; p < n_prog; ++p)
+        if (prog_ptr[p + 1] < prog_ptr[p]) return ORACLE_EINVAL;
+    set_threads(n_threads);
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : bad)
+    for (int32_t p = 0; p < n_prog; ++p) {
+        double acc = base_score, sc = fabs(base_score);
+        for (int64_t r = prog_ptr[p]; r < prog_ptr[p + 1]; ++r) {
+            double s = 0.0;
+            for (int32_t t = 0; t < n_trees; ++t) {
+                int64_t leaf = walk_tree(root[t], n_nodes, feature, threshold, left, right,
+                                         default_left, X, ld, n_features, r);
+                if (leaf < 0) { bad = 1; break; }
+                s += (double)leaf_value[leaf];
+                sc += fabs((double)leaf_value[leaf]);
+            }
+            if (stmt) stmt[r] = s;
+            acc += s;
+        }
+        prog[p] = acc;
+        if (scale) scale[p] = sc;
+    }
+    return bad ? ORACLE_EINVAL : ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------------------------- */
+/* Actor / critic forward                                                                       */
+/* ------------------------------------------------------------------------------------------- */
+
+/* Value of element i of a weight/state array stored as fp32 (dtype 0) or bf16 bits (dtype 1). */
+static double load_val(const void *base, int dtype, int64_t i) {
+    if (dtype == 0) return (double)((const float *)base)[i];
+    uint32_t bits = (uint32_t)((const uint16_t *)base)[i] << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+/* Round an fp64 value to the nearest bf16 value (ties to even), returned as fp64.  Works on the
+ * exact binary expansion: keep 8 significant bits (1 implicit + 7 stored) of the normalised
+ * value; subnormal bf16 values keep fewer bits, with the same rule. */
+static double round_to_bf16(double v) {
+    if (v == 0.0 || isnan(v) || isinf(v)) return v;
+    int e;
+    double m = frexp(fabs(v), &e);           /* |v| = m * 2^e, m in [0.5, 1) */
+    int keep = 8;                            /* significant bits of a normal bf16 */
+    int emin = -125;                         /* smallest normal bf16 is 2^-126 = 0.5 * 2^-125 */
+    if (e < emin) keep -= (emin - e);        /* subnormal range loses bits */
+    if (keep < 0) return copysign(0.0, v);
+    double scaled = ldexp(m, keep);          /* integer part holds the kept bits */
+    double fl = floor(scaled);
+    double frac = scaled - fl;
+    if (frac > 0.5 || (frac == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;
+    double r = ldexp(fl, e - keep);
+    if (r > 3.3895313892515355e38) r = INFINITY; /* beyond the largest finite bf16 */
+    return copysign(r, v);
+}
+
+/* Exported for the tests of the rounding rule itself. */
+double oracle_round_bf16(double v) { return round_to_bf16(v); }
+
+/*
+ * For each state b (row b of states[B][S]):
+ *     h1 = max(0, W1 s + b1),  h2 = max(0, W2 h1 + b2)     (bf16 policies: h rounded to bf16)
+ *     logits = Wa h2 + ba,     value = wv . h2 + bv
+ *     action = lowest i with logits[i] == max logits;  probs = softmax(logits)
+ * Weights are [out][in] row-major.  Scales (for tolerances) are sum_j |W_ij h_j| + |b_i|.
+ * logits/probs/logit_scale are [B][A]; any output but action and value may be NULL.
+ */
+int oracle_policy_step(int dtype, int32_t S, int32_t H1, int32_t H2, int32_t A,
+                       const void *w1, const float *b1, const void *w2, const float *b2,
+                       const void *wa, const float *ba, const void *wv, const float *bv,
+                       const void *states, int32_t B,
+                       int32_t *action, double *value, double *logits, double *probs,
+                       double *logit_scale, double *value_scale, int n_threads) {
+    if ((dtype != 0 && dtype != 1) || S <= 0 || H1 <= 0 || H2 <= 0 || A <= 0 || B < 0)
+        return ORACLE_EINVAL;
+    set_threads(n_threads);
+    int oom = 0;
+#pragma omp parallel reduction(| : oom)
+    {
+        double *h1 = (double *)malloc(sizeof(double) * (size_t)H1);
+        double *h2 = (double *)malloc(sizeof(double) * (size_t)H2);
+        double *z = (double *)malloc(sizeof(double) * (size_t)A);
+        if (!h1 || !h2 || !z) {
+            oom = 1;
+        } else {
+#pragma omp for schedule(static)
+            for (int32_t b = 0; b < B; ++b) {
+                for (int32_t i = 0; i < H1; ++i) {
+                    double acc = b1[i];
+                    for (int32_t j = 0; j < S; ++j)
+                        acc += load_val(w1, dtype, (int64_t)i * S + j) *
+                               load_val(states, dtype, (int64_t)b * S + j);
+                    acc = acc > 0.0 ? acc : 0.0;
+                    h1[i] = dtype == 1 ? round_to_bf16(acc) : acc;
+                }
+                for (int32_t i = 0; i < H2; ++i) {
+                    double acc = b2[i];
+                    for (int32_t j = 0; j < H1; ++j) acc += load_val(w2, dtype, (int64_t)i * H1 + j) * h1[j];
+                    acc = acc > 0.0 ? acc : 0.0;
+                    h2[i] = dtype == 1 ? round_to_bf16(acc) : acc;
+                }
+                int32_t best = 0;
+                for (int32_t i = 0; i < A; ++i) {
+                    double acc = ba[i], sc = fabs((double)ba[i]);
+                    for (int32_t j = 0; j < H2; ++j) {
+                        double t = load_val(wa, dtype, (int64_t)i * H2 + j) * h2[j];
+                        acc += t;
+                        sc += fabs(t);
+                    }
+                    z[i] = acc;
+                    if (logits) logits[(int64_t)b * A + i] = acc;
+                    if (logit_scale) logit_scale[(int64_t)b * A + i] = sc;
+                    if (acc > z[best]) best = i;      /* strict: the lowest index wins ties */
+                }
+                action[b] = best;
+                double v = bv[0], vs = fabs((double)bv[0]);
+                for (int32_t j = 0; j < H2; ++j) {
+                    double t = load_val(wv, dtype, j) * h2[j];
+                    v += t;
+                    vs += fabs(t);
+                }
+                value[b] = v;
+                if (value_scale) value_scale[b] = vs;
+                if (probs) {
+                    double m = z[best], sum = 0.0;
+                    for (int32_t i = 0; i < A; ++i) sum += exp(z[i] - m);
+                    for (int32_t i = 0; i < A; ++i) probs[(int64_t)b * A + i] = exp(z[i] - m) / sum;
+                }
+            }
+        }
+        free(h1);
+        free(h2);
+        free(z);
+    }
+    return oom ? ORACLE_ENOMEM : ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------------------------- */
+/* Top-K and the running heap                                                                   */
+/* ------------------------------------------------------------------------------------------- */
+
+typedef struct {
+    float score;
+    int64_t index;
+} cand_t;
+
+/* Ranking order: higher score first; NaN after every number; -0 and +0 equal; then lower index. */
+static int cand_cmp(const void *pa, const void *pb) {
+    const cand_t *a = (const cand_t *)pa, *b = (const cand_t *)pb;
+    int an = isnan(a->score), bn = isnan(b->score);
+    if (an != bn) return an ? 1 : -1;
+    if (!an) {
+        if (a->score > b->score) return -1;
+        if (a->score < b->score) return 1;
+    }
+    if (a->index < b->index) return -1;
+    if (a->index > b->index) return 1;
+    return 0;
+}
+
+/* The k best of n scores, ranked; candidate i carries index index_base + i.  Requires k <= n. */
+int oracle_topk(const float *score, int64_t n, int32_t k, int64_t index_base,
+                float *out_score, int64_t *out_index) {
+    if (n < 0 || k < 0 || k > n) return ORACLE_EINVAL;
+    cand_t *c = (cand_t *)malloc(sizeof(cand_t) * (size_t)(n > 0 ? n : 1));
+    if (!c) return ORACLE_ENOMEM;
+    for (int64_t i = 0; i < n; ++i) {
+        c[i].score = score[i];
+        c[i].index = index_base + i;
+    }
+    qsort(c, (size_t)n, sizeof(cand_t), cand_cmp);
+    for (int32_t i = 0; i < k; ++i) {
+        out_score[i] = c[i].score;
+        out_index[i] = c[i].index;
+    }
+    free(c);
+    return ORACLE_OK;
+}
+
+/* running <- the k best of (running's k entries) united with (n new scores, indices index_base+i). */
+int oracle_merge(float *run_score, int64_t *run_index, int32_t k,
+                 const float *score, int64_t n, int64_t index_base) {
+    if (n < 0 || k < 0) return ORACLE_EINVAL;
+    int64_t m = (int64_t)k + n;
+    cand_t *c = (cand_t *)malloc(sizeof(cand_t) * (size_t)(m > 0 ? m : 1));
+    if (!c) return ORACLE_ENOMEM;
+    for (int32_t i = 0; i < k; ++i) {
+        c[i].score = run_score[i];
+        c[i].index = run_index[i];
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        c[k + i].score = score[i];
+        c[k + i].index = index_base + i;
+    }
+    qsort(c, (size_t)m, sizeof(cand_t), cand_cmp);
+    for (int32_t i = 0; i < k; ++i) {
+        run_score[i] = c[i].score;
+        run_index[i] = c[i].index;
+    }
+    free(c);
+    return ORACLE_OK;
+}

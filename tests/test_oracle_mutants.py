@@ -1,0 +1,85 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case plants one mistake (a flipped comparison, a dropped term, a transposed operand, a wrong
+tie rule ...) in a private copy of the oracle source, builds it with gcc on the CPU, points the
+oracle wrapper at that build and checks that at least one pin fails.  The real oracle is restored
+afterwards."""
+from __future__ import annotations
+
+import os
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "harl_oracle.c")
+
+MUTANTS = {
+    "split_not_strict": ("(v < threshold[n])", "(v <= threshold[n])",
+                         [(pins.test_threshold_ties_and_missing, dict(thr=np.float32(1.5), dl=0))]),
+    "default_dir_swapped": ("default_left[n] ? left[n] : right[n]", "default_left[n] ? right[n] : left[n]",
+                            [(pins.test_all_missing_row_follows_default_bits, {})]),
+    "missing_not_detected": ("if (isnan(v))", "if (0)",
+                             [(pins.test_threshold_ties_and_missing, dict(thr=np.float32(1.5), dl=1))]),
+    "first_tree_dropped": ("for (int32_t t = 0; t < n_trees; ++t)", "for (int32_t t = 1; t < n_trees; ++t)",
+                           [(pins.test_tree_sums_match_path_predicates, dict(p_nan=0.0, depth=3))]),
+    "program_keeps_last_stmt": ("acc += s;", "acc = s;",
+                                [(pins.test_leafless_root_and_constant_leaves_closed_form, {})]),
+    "base_score_ignored": ("double acc = base_score, sc", "double acc = 0.0, sc",
+                           [(pins.test_base_score_and_empty_programs, {})]),
+    "layer2_bias_dropped": ("double acc = b2[i];", "double acc = 0.0;",
+                            [(pins.test_policy_matches_numpy_matmul, dict(dtype="f32"))]),
+    "relu_missing": ("acc = acc > 0.0 ? acc : 0.0;\n                    h1[i]", "h1[i]",
+                     [(pins.test_policy_matches_numpy_matmul, dict(dtype="f32"))]),
+    "w2_transposed": ("load_val(w2, dtype, (int64_t)i * H1 + j)", "load_val(w2, dtype, (int64_t)j * H2 + i)",
+                      [(pins.test_policy_matches_numpy_matmul, dict(dtype="f32"))]),
+    "argmax_last_tie": ("if (acc > z[best]) best = i;", "if (acc >= z[best]) best = i;",
+                        [(pins.test_policy_exact_integer_variant, dict(dtype="f32"))]),
+    "bf16_rounding_skipped": ("h2[i] = dtype == 1 ? round_to_bf16(acc) : acc;", "h2[i] = acc;",
+                              [(pins.test_policy_matches_numpy_matmul, dict(dtype="bf16"))]),
+    "bf16_ties_away": ("(frac == 0.5 && fmod(fl, 2.0) != 0.0)", "(frac == 0.5)",
+                       [(pins.test_bf16_rounding_rule, {})]),
+    "softmax_unnormalised": ("exp(z[i] - m) / sum", "exp(z[i] - m)",
+                             [(pins.test_softmax_invariants, {})]),
+    "topk_index_desc": ("if (a->index < b->index) return -1;\n    if (a->index > b->index) return 1;",
+                        "if (a->index < b->index) return 1;\n    if (a->index > b->index) return -1;",
+                        [(pins.test_topk_matches_lexsort, {})]),
+    "nan_ranked_first": ("if (an != bn) return an ? 1 : -1;", "if (an != bn) return an ? -1 : 1;",
+                         [(pins.test_topk_special_cases, {})]),
+    "merge_local_index": ("c[k + i].index = index_base + i;", "c[k + i].index = i;",
+                          [(pins.test_merge_equals_topk_of_union_in_any_order, {})]),
+}
+
+
+@pytest.fixture(scope="module")
+def workdir():
+    with tempfile.TemporaryDirectory(prefix="harl_mutants_") as d:
+        yield d
+    oracle.use_library(None)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_planted_mistake(name, workdir):
+    old, new, checks = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, "mutation site must be unique: %r" % old
+    path_c = os.path.join(workdir, name + ".c")
+    path_so = os.path.join(workdir, name + ".so")
+    with open(path_c, "w") as f:
+        f.write(src.replace(old, new))
+    subprocess.run(["gcc", *oracle.CFLAGS, path_c, "-o", path_so, "-lm"], check=True)
+    oracle.use_library(path_so)
+    try:
+        caught = 0
+        for fn, kw in checks:
+            try:
+                fn(**kw)
+            except (AssertionError, ValueError):
+                caught += 1
+        assert caught > 0, "planted mistake %s passed every pin" % name
+    finally:
+        oracle.use_library(None)

@@ -1,0 +1,355 @@
+"""Pins of the CPU oracle against things other than itself (brute force, closed forms, invariants,
+library routines).  Paper anchors: the cost model C scores every new schedule (Algorithm 1; the
+cost model is XGBoost, Section 6.1, Appendix A.2); the actor and critic act on the states
+(Algorithm 1; Section 4.3, Eq. 6); the top-K of the heap H are the K best predicted scores
+(Algorithm 1; Section 4.3, Top-K Selection Phase)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import gen_batch, gen_ensemble, gen_policy, gen_states, mini_config, get_config
+from synth.gen import bf16_bits_from_f32, f32_from_bf16_bits
+from tests import brute
+
+
+# ----------------------------------------------------------------------------------------------
+# tree routing and sums
+# ----------------------------------------------------------------------------------------------
+def _irregular_ensemble(rng, n_trees, n_features, max_depth, thr_pool):
+    """Random non-complete trees in the explicit node format (children ids, leaves feature -1)."""
+    feature, threshold, left, right, dl, leaf, root = [], [], [], [], [], [], []
+
+    def build(depth):
+        nid = len(feature)
+        feature.append(-1); threshold.append(0.0); left.append(-1); right.append(-1)
+        dl.append(0); leaf.append(0.0)
+        if depth < max_depth and (depth == 0 or rng.random() < 0.7):
+            feature[nid] = int(rng.integers(0, n_features))
+            threshold[nid] = float(rng.choice(thr_pool))
+            dl[nid] = int(rng.random() < 0.5)
+            left[nid] = build(depth + 1)
+            right[nid] = build(depth + 1)
+        else:
+            leaf[nid] = float(np.float32(rng.normal(0, 0.1)))
+        return nid
+
+    for _ in range(n_trees):
+        root.append(build(0))
+    return dict(n_trees=n_trees, n_features=n_features, max_depth=max_depth,
+                root=np.array(root, np.int32), feature=np.array(feature, np.int32),
+                threshold=np.array(threshold, np.float32), left=np.array(left, np.int32),
+                right=np.array(right, np.int32), default_left=np.array(dl, np.uint8),
+                leaf_value=np.array(leaf, np.float32), base_score=0.0)
+
+
+def _plant_threshold_rows(X, ens, n_rows, rng):
+    """Overwrite some feature values with exact thresholds and their fp32 neighbours so that
+    x == thr and x just below thr occur for many splits."""
+    internal = np.nonzero(ens["feature"] >= 0)[0]
+    for r in range(0, n_rows, 3):
+        for n in rng.choice(internal, size=min(6, internal.size), replace=False):
+            f, th = ens["feature"][n], np.float32(ens["threshold"][n])
+            X[f, r] = rng.choice([th, np.nextafter(th, np.float32(-np.inf)), np.nextafter(th, np.float32(np.inf))])
+
+
+@pytest.mark.parametrize("p_nan", [0.0, 0.2])
+@pytest.mark.parametrize("depth", [1, 3, 4])
+def test_tree_sums_match_path_predicates(p_nan, depth):
+    cfg = mini_config(depth=depth, p_nan=p_nan, n_trees=4, n_features=8, n_prog=60, s_max=6)
+    ens = gen_ensemble(cfg)
+    b = gen_batch(cfg)
+    X, n = b["features"].copy(), b["n_rows"]
+    _plant_threshold_rows(X, ens, n, np.random.default_rng(7))
+    got = oracle.score_round(ens, X, b["prog_ptr"])
+    want, n_true = brute.brute_stmt_scores(ens, X, n)
+    assert (n_true == 1).all(), "every (row, tree) must satisfy exactly one leaf predicate"
+    np.testing.assert_allclose(got["stmt"], want, rtol=0, atol=1e-12)
+
+
+def test_irregular_trees_match_path_predicates():
+    rng = np.random.default_rng(3)
+    cfg = mini_config(p_nan=0.15, n_features=6, n_prog=50)
+    b = gen_batch(cfg)
+    X, n = b["features"].copy(), b["n_rows"]
+    pool = np.unique(X[~np.isnan(X)])
+    ens = _irregular_ensemble(rng, n_trees=5, n_features=6, max_depth=5, thr_pool=pool)
+    got = oracle.score_round(ens, X, b["prog_ptr"])
+    want, n_true = brute.brute_stmt_scores(ens, X, n)
+    assert (n_true == 1).all()
+    np.testing.assert_allclose(got["stmt"], want, rtol=0, atol=1e-12)
+
+
+def _stump(feature, thr, dl, lv, rv, n_features):
+    return dict(n_trees=1, n_features=n_features, max_depth=1, root=np.array([0], np.int32),
+                feature=np.array([feature, -1, -1], np.int32),
+                threshold=np.array([thr, 0, 0], np.float32),
+                left=np.array([1, -1, -1], np.int32), right=np.array([2, -1, -1], np.int32),
+                default_left=np.array([dl, 0, 0], np.uint8),
+                leaf_value=np.array([0, lv, rv], np.float32), base_score=0.0)
+
+
+@pytest.mark.parametrize("thr", [np.float32(0.0), np.float32(1.5), np.float32(-2.25), np.float32(3.0e-3)])
+@pytest.mark.parametrize("dl", [0, 1])
+def test_threshold_ties_and_missing(thr, dl):
+    """x == thr goes right; the fp32 value just below goes left; -0 equals +0; NaN follows the
+    default direction; +-inf go to the sides their order says."""
+    L, R = 1.0, 2.0
+    below = np.nextafter(thr, np.float32(-np.inf))
+    above = np.nextafter(thr, np.float32(np.inf))
+    vals = [thr, below, above, np.float32(np.nan), np.float32(-np.inf), np.float32(np.inf)]
+    want = [R, L, R, L if dl else R, L, R]
+    if thr == 0:
+        vals.append(np.float32(-0.0)); want.append(R)
+    X = np.array([vals], dtype=np.float32)
+    ens = _stump(0, thr, dl, L, R, 1)
+    ptr = np.arange(len(vals) + 1, dtype=np.int32)
+    got = oracle.score_round(ens, X, ptr)
+    np.testing.assert_array_equal(got["prog"], np.array(want))
+
+
+def test_all_missing_row_follows_default_bits():
+    """A row of NaN reaches, in every complete tree, the leaf spelled by the default bits along
+    the default path: leaf number = the bits read as a binary number (1 = right)."""
+    cfg = mini_config(depth=5, n_trees=6, n_features=8)
+    ens = gen_ensemble(cfg)
+    X = np.full((8, 1), np.nan, dtype=np.float32)
+    got = oracle.score_round(ens, X, np.array([0, 1], np.int32))
+    D, M = cfg.depth, 2 ** (cfg.depth + 1) - 1
+    total = 0.0
+    for t in range(cfg.n_trees):
+        n, bits = 0, 0
+        for _ in range(D):
+            go_right = 0 if ens["default_left"][t * M + n] else 1
+            bits = 2 * bits + go_right
+            n = 2 * n + 1 + go_right
+        total += float(ens["leaf_value"][t * M + (2 ** D - 1) + bits])
+    assert got["prog"][0] == pytest.approx(total, abs=1e-12)
+
+
+def test_leafless_root_and_constant_leaves_closed_form():
+    """Constant leaves c = 2**-4: every statement scores T*c, every program n_stmt*T*c, exactly."""
+    cfg = mini_config(depth=4, n_trees=7, n_prog=40, s_max=9)
+    ens = gen_ensemble(cfg)
+    ens["leaf_value"] = np.where(ens["feature"] < 0, np.float32(2.0 ** -4), np.float32(0)).astype(np.float32)
+    b = gen_batch(cfg)
+    got = oracle.score_round(ens, b["features"], b["prog_ptr"])
+    n_stmt = np.diff(b["prog_ptr"]).astype(np.float64)
+    np.testing.assert_array_equal(got["prog"], n_stmt * cfg.n_trees * 2.0 ** -4)
+    np.testing.assert_array_equal(got["stmt"], np.full(b["n_rows"], cfg.n_trees * 2.0 ** -4))
+
+
+def test_program_sum_invariants_exact_variant():
+    """Dyadic leaves: every partial sum is exact in fp32; prog = sum of stmt exactly; a
+    one-statement program equals its statement; permuting statements changes nothing; fp32 sums
+    in forward and reverse order agree bit for bit with the fp64 oracle."""
+    cfg = get_config("tiny", exact=True).with_(n_prog=96)
+    ens = gen_ensemble(cfg)
+    b = gen_batch(cfg)
+    got = oracle.score_round(ens, b["features"], b["prog_ptr"])
+    ptr = b["prog_ptr"]
+    for p in range(cfg.n_prog):
+        rows = got["stmt"][ptr[p]:ptr[p + 1]]
+        assert got["prog"][p] == rows.sum()
+        fwd = np.float32(0)
+        for v in rows.astype(np.float32):
+            fwd = np.float32(fwd + v)
+        rev = np.float32(0)
+        for v in rows.astype(np.float32)[::-1]:
+            rev = np.float32(rev + v)
+        assert fwd == rev == np.float32(got["prog"][p])
+        if ptr[p + 1] - ptr[p] == 1:
+            assert got["prog"][p] == got["stmt"][ptr[p]]
+    # permute statements inside each program
+    rng = np.random.default_rng(5)
+    perm = np.concatenate([ptr[p] + rng.permutation(ptr[p + 1] - ptr[p]) for p in range(cfg.n_prog)])
+    got2 = oracle.score_round(ens, b["features"][:, perm], ptr)
+    np.testing.assert_array_equal(got2["prog"], got["prog"])
+
+
+def test_scale_bounds_score():
+    cfg = mini_config(depth=4, n_trees=5, p_nan=0.1)
+    ens, b = gen_ensemble(cfg), gen_batch(cfg)
+    got = oracle.score_round(ens, b["features"], b["prog_ptr"])
+    assert (np.abs(got["prog"]) <= got["scale"] + 1e-12).all()
+    assert (got["scale"] > 0).all()
+
+
+def test_base_score_and_empty_programs():
+    cfg = mini_config(depth=2, n_trees=3)
+    ens, b = gen_ensemble(cfg), gen_batch(cfg)
+    ens["base_score"] = 0.5
+    ptr = np.array([0, 0, 2, 2, 3], np.int32)      # programs 0 and 2 have no statements
+    got = oracle.score_round(ens, b["features"], ptr, n_rows=3)
+    assert got["prog"][0] == 0.5 and got["prog"][2] == 0.5
+    want, _ = brute.brute_stmt_scores(ens, b["features"], 3)
+    assert got["prog"][1] == pytest.approx(0.5 + want[0] + want[1], abs=1e-12)
+
+
+def test_malformed_inputs_rejected():
+    cfg = mini_config()
+    ens, b = gen_ensemble(cfg), gen_batch(cfg)
+    bad_ptr = b["prog_ptr"].copy()
+    bad_ptr[3] = bad_ptr[4] + 1
+    with pytest.raises(ValueError):
+        oracle.score_round(ens, b["features"], bad_ptr, n_rows=b["n_rows"])
+    cyc = dict(ens)
+    cyc["left"] = ens["left"].copy()
+    cyc["left"][0] = 0                                  # a cycle
+    cyc["default_left"] = np.ones_like(ens["default_left"])
+    X = np.full_like(b["features"], np.nan)
+    with pytest.raises(ValueError):
+        oracle.score_round(cyc, X, b["prog_ptr"])
+
+
+# ----------------------------------------------------------------------------------------------
+# actor / critic
+# ----------------------------------------------------------------------------------------------
+def test_bf16_rounding_rule():
+    """Ties go to even; the oracle's rounding agrees with an independent bit-level rounding and,
+    on fp32 inputs, with the input generator's fp32 -> bf16 rounding."""
+    assert oracle.round_bf16(1 + 2 ** -8) == 1.0                       # tie, even is 1.0
+    assert oracle.round_bf16(1 + 3 * 2 ** -8) == 1 + 2 ** -6           # tie, rounds up to even
+    assert oracle.round_bf16(1 + 2 ** -8 + 2 ** -30) == 1 + 2 ** -7    # just above the tie
+    assert oracle.round_bf16(-(1 + 2 ** -8)) == -1.0
+    assert oracle.round_bf16(2.0 ** -130) == 2.0 ** -130                 # bf16 subnormal, exact
+    rng = np.random.default_rng(11)
+    v = rng.standard_normal(4000) * np.exp(rng.uniform(-20, 20, 4000))
+    ties = np.array([1 + 2 ** -8, 3 + 2 ** -6, 0.75 + 2 ** -10, 100.0 + 0.25])
+    v = np.concatenate([v, ties, -ties])
+    ours = np.array([oracle.round_bf16(x) for x in v])
+    np.testing.assert_array_equal(ours, brute.bf16_round_bits(v))
+    f32 = v.astype(np.float32)
+    gen = f32_from_bf16_bits(bf16_bits_from_f32(f32)).astype(np.float64)
+    np.testing.assert_array_equal(np.array([oracle.round_bf16(float(x)) for x in f32]), gen)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_matches_numpy_matmul(dtype):
+    cfg = mini_config(pol_dtype=dtype, pol_s=24, pol_h1=40, pol_h2=36, pol_a=9, n_prog=70)
+    pol, st = gen_policy(cfg), gen_states(cfg)
+    got = oracle.policy_step(pol, st)
+    ref = brute.numpy_policy(pol, st)
+    np.testing.assert_allclose(got["logits"], ref["logits"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(got["value"], ref["value"], rtol=0, atol=1e-12)
+    gap = np.sort(ref["logits"], axis=1)
+    clear = (gap[:, -1] - gap[:, -2]) > 1e-9
+    np.testing.assert_array_equal(got["action"][clear], ref["action"][clear])
+    assert (np.abs(got["logits"]) <= got["logit_scale"] + 1e-12).all()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_policy_exact_integer_variant(dtype):
+    """Integer states/weights/biases: every activation is an integer of magnitude <= 85, exact in
+    bf16 and fp32; compare with pure-Python integer arithmetic; ties resolve to the lowest index."""
+    cfg = mini_config(pol_dtype=dtype, pol_s=16, pol_h1=32, pol_h2=32, pol_a=10, n_prog=50, exact=True)
+    pol, st = gen_policy(cfg), gen_states(cfg)
+    got = oracle.policy_step(pol, st)
+    W1, W2, Wa, Wv = (brute.decode(pol[k], dtype).astype(int).tolist() for k in ("w1", "w2", "wa", "wv"))
+    b1, b2, ba, bv = (np.asarray(pol[k]).astype(int).tolist() for k in ("b1", "b2", "ba", "bv"))
+    S = brute.decode(st, dtype).astype(int).tolist()
+    n_ties = 0
+    for i, s in enumerate(S):
+        h1 = [max(0, sum(w * x for w, x in zip(row, s)) + b) for row, b in zip(W1, b1)]
+        h2 = [max(0, sum(w * x for w, x in zip(row, h1)) + b) for row, b in zip(W2, b2)]
+        z = [sum(w * x for w, x in zip(row, h2)) + b for row, b in zip(Wa, ba)]
+        v = sum(w * x for w, x in zip(Wv[0], h2)) + bv[0]
+        assert max(map(abs, h1 + h2 + z)) <= 85
+        assert got["logits"][i].tolist() == z
+        assert got["value"][i] == v
+        assert got["action"][i] == z.index(max(z))
+        n_ties += z.count(max(z)) > 1
+    assert n_ties > 0, "the exact variant should exercise the lowest-index tie rule"
+
+
+def test_policy_positive_weights_collapse_to_one_linear_map():
+    """With non-negative states, weights and biases the ReLUs are identities, so the logits equal
+    (Wa W2 W1) s + Wa W2 b1 + Wa b2 + ba, with the matrices multiplied first."""
+    cfg = mini_config(pol_s=12, pol_h1=20, pol_h2=18, pol_a=7, n_prog=30)
+    pol = gen_policy(cfg)
+    for k in ("w1", "w2", "wa", "wv", "b1", "b2", "ba", "bv"):
+        pol[k] = np.abs(pol[k]).astype(np.float32)
+    st = np.abs(gen_states(cfg))
+    got = oracle.policy_step(pol, st)
+    W1, W2, Wa, Wv = (pol[k].astype(np.float64) for k in ("w1", "w2", "wa", "wv"))
+    b1, b2, ba, bv = (pol[k].astype(np.float64) for k in ("b1", "b2", "ba", "bv"))
+    M = Wa @ W2 @ W1
+    c = Wa @ W2 @ b1 + Wa @ b2 + ba
+    want = st.astype(np.float64) @ M.T + c
+    np.testing.assert_allclose(got["logits"], want, rtol=1e-12, atol=1e-12)
+    mv = Wv @ W2 @ W1
+    cv = Wv @ W2 @ b1 + Wv @ b2 + bv
+    np.testing.assert_allclose(got["value"], (st.astype(np.float64) @ mv.T + cv)[:, 0], rtol=1e-12)
+
+
+def test_softmax_invariants():
+    cfg = mini_config(pol_a=17, n_prog=64)
+    got = oracle.policy_step(gen_policy(cfg), gen_states(cfg))
+    np.testing.assert_allclose(got["probs"].sum(axis=1), 1.0, atol=1e-12)
+    assert (got["probs"] > 0).all()
+    best = got["probs"][np.arange(64), got["action"]]
+    assert (best >= got["probs"].max(axis=1) - 1e-15).all()
+    # softmax is invariant to adding a constant to every logit: compare ratios
+    z = got["logits"]
+    r = got["probs"][:, 1:] / got["probs"][:, :1]
+    np.testing.assert_allclose(r, np.exp(z[:, 1:] - z[:, :1]), rtol=1e-10)
+
+
+# ----------------------------------------------------------------------------------------------
+# top-K and the running heap
+# ----------------------------------------------------------------------------------------------
+def test_topk_matches_lexsort():
+    rng = np.random.default_rng(1)
+    s = rng.standard_normal(3000).astype(np.float32)
+    s[rng.integers(0, 3000, 400)] = np.float32(0.5)           # many exact ties
+    s[::97] = -0.0
+    s[::89] = 0.0
+    for k in (1, 7, 128, 3000):
+        got = oracle.topk(s, k, index_base=1000)
+        want = brute.lexsort_topk(s, k, index_base=1000)
+        np.testing.assert_array_equal(got[1], want[1])
+        np.testing.assert_array_equal(got[0], want[0])
+
+
+def test_topk_special_cases():
+    assert oracle.topk(np.zeros(10, np.float32), 4)[1].tolist() == [0, 1, 2, 3]
+    s = np.array([-0.0, 0.0, -0.0, 0.0], np.float32)
+    assert oracle.topk(s, 4)[1].tolist() == [0, 1, 2, 3]
+    s = np.array([1.0, np.nan, 3.0, -np.inf, 3.0], np.float32)
+    assert oracle.topk(s, 5)[1].tolist() == [2, 4, 0, 3, 1]
+    rng = np.random.default_rng(2)
+    s = rng.integers(0, 5, 200).astype(np.float32)
+    assert oracle.topk(s, 1)[1][0] == int(np.argmax(s))        # k = 1: lowest-index argmax
+    with pytest.raises(ValueError):
+        oracle.topk(s, 201)
+
+
+def test_merge_equals_topk_of_union_in_any_order():
+    rng = np.random.default_rng(4)
+    k, nb, n = 50, 6, 300
+    batches = [rng.integers(-20, 20, n).astype(np.float32) / 4 for _ in range(nb)]
+    allv = np.concatenate(batches)
+    want = oracle.topk(allv, k)
+    np.testing.assert_array_equal(want[1], brute.lexsort_topk(allv, k)[1])
+    for order in (range(nb), reversed(range(nb)), rng.permutation(nb)):
+        rs, ri = oracle.reset(k)
+        for bidx in order:
+            rs, ri = oracle.merge(rs, ri, batches[bidx], bidx * n)
+        np.testing.assert_array_equal(ri, want[1])
+        np.testing.assert_array_equal(rs, want[0])
+    # save after 3 batches, resume from the copy: identical
+    rs, ri = oracle.reset(k)
+    for bidx in range(3):
+        rs, ri = oracle.merge(rs, ri, batches[bidx], bidx * n)
+    saved = (rs.copy(), ri.copy())
+    for bidx in range(3, nb):
+        saved = oracle.merge(saved[0], saved[1], batches[bidx], bidx * n)
+    np.testing.assert_array_equal(saved[1], want[1])
+
+
+def test_merge_fewer_candidates_than_k_keeps_sentinels():
+    rs, ri = oracle.reset(8)
+    rs, ri = oracle.merge(rs, ri, np.array([3.0, -np.inf, 1.0], np.float32), 10)
+    assert ri[:3].tolist() == [10, 12, 11]
+    assert (ri[3:] == oracle.RESET_INDEX).all() and np.isneginf(rs[3:]).all()
