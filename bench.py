@@ -1,0 +1,164 @@
+"""Benchmark one HARL search round on one MI355X: policy forward + cost-model scoring + top-K.
+
+A step is one whole round over one batch of synthetic candidates, inputs already resident in
+HBM: harl_policy_step (second stream, concurrent with scoring), harl_score_round and harl_topk.
+Prints ONE JSON line (rank 0).  Default workload: the standard round (4,096 candidates with
+U{1..32} statements of 164 features, 300 trees of depth 8, fp32 MLP 64-256-256 -> 24+1, top-128).
+
+  python bench.py [--steps K] [--warmup W] [--config standard] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X datasheet peaks used for the roofline fractions
+PEAK_HBM_GBS = 8000.0
+PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+N_CU, CLOCK_GHZ = 256, 2.4
+# Node-visit ceiling of the traversal loop: each visit of 64 rows (one wave) issues one 8-byte and
+# one 4-byte LDS gather (768 B) and about 5 VALU instructions; the CU's LDS serves 128 B/clk and
+# issues one wave-wide VALU instruction per clock, so the LDS bound (6 clk / 64 visits) binds.
+LDS_BYTES_PER_CLK = 128.0
+LDS_BYTES_PER_VISIT = 12.0
+PEAK_GVISITS = N_CU * CLOCK_GHZ * LDS_BYTES_PER_CLK / LDS_BYTES_PER_VISIT  # G visits / s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="standard")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--one-stream", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(cfg, ens, pol, b, budget_s):
+    """The oracle, as it stands, on this host's cores: full rounds of the same workload (or the
+    first programs of it) repeated until `budget_s` seconds have elapsed."""
+    import numpy as np
+    import oracle
+    threads = oracle.max_threads()
+    n_prog = cfg.n_prog
+    ptr = b["prog_ptr"]
+    # bounded sample: at most the programs the oracle scores in ~budget/3 seconds, estimated from
+    # a small probe
+    probe = min(n_prog, 256)
+    t0 = time.perf_counter()
+    oracle.score_round(ens, b["features"][:, :int(ptr[probe])], ptr[:probe + 1])
+    oracle.policy_step(pol, b["states"][:probe], want_probs=cfg.softmax)
+    per_prog = (time.perf_counter() - t0) / probe
+    sample = int(min(n_prog, max(probe, budget_s / 3 / max(per_prog, 1e-9))))
+    X = np.ascontiguousarray(b["features"][:, :int(ptr[sample])])
+    sp = ptr[:sample + 1]
+    st = b["states"][:sample]
+    done, t0 = 0, time.perf_counter()
+    while True:
+        r = oracle.score_round(ens, X, sp)
+        oracle.policy_step(pol, st, want_probs=cfg.softmax)
+        oracle.topk(r["prog32"], min(cfg.top_k, sample))
+        done += sample
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return dict(value=done / el, unit="candidates/s", cores=threads, kind="oracle",
+                sample="%d of %d candidates of one %s round (%d statement rows), repeated %d times in %.1f s" % (
+                    sample, n_prog, cfg.name, int(sp[-1]), done // sample, el))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (candidates shard with "
+              "one all-gather of the top-k; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2211_11172_amd.round import Round, upload_batch
+    from synth import gen_batch, gen_ensemble, gen_policy, get_config
+
+    cfg = get_config(args.config)
+    ens, pol, b = gen_ensemble(cfg), gen_policy(cfg), gen_batch(cfg)
+    dev = torch.device("cuda:0")
+    rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=not args.one_stream)
+    batch = upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)
+    main_stream = torch.cuda.current_stream(dev)
+
+    for _ in range(args.warmup):
+        rnd.step(batch)
+    torch.cuda.synchronize()
+
+    # timed region: K whole rounds; events around the scoring call (the dominant kernel, on the
+    # stream it is launched on) and around the policy call (on its stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    side = rnd.side if rnd.side is not None else main_stream
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        side.wait_stream(main_stream)
+        pev[i][0].record(side)
+        rnd.policy(batch, stream=side)
+        pev[i][1].record(side)
+        ev[i][0].record(main_stream)
+        rnd.score(batch, stream=main_stream)
+        ev[i][1].record(main_stream)
+        rnd.topk(batch, stream=main_stream)
+        main_stream.wait_stream(side)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    score_ms = sum(a.elapsed_time(z) for a, z in ev) / args.steps
+    pol_ms = sum(a.elapsed_time(z) for a, z in pev) / args.steps
+
+    n_rows, n_prog = b["n_rows"], cfg.n_prog
+    visits = n_rows * cfg.n_trees * cfg.depth
+    hbm_bytes = n_rows * cfg.n_features * 4 + (n_prog + 1) * 4 + n_prog * 4
+    gvisits = visits / (score_ms * 1e-3) / 1e9
+    flops_per_state = 2 * (cfg.pol_s * cfg.pol_h1 + cfg.pol_h1 * cfg.pol_h2 + cfg.pol_h2 * (cfg.pol_a + 1))
+    pol_tflops = n_prog * flops_per_state / (pol_ms * 1e-3) / 1e12
+    ms_per_step = el * 1e3 / args.steps
+    out = {
+        "metric": "candidate schedules scored+stepped/sec",
+        "value": n_prog * args.steps / el,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if cfg.pol_dtype == "f32" else "f32-trees+bf16-mlp",
+        "data": "synthetic",
+        "config": {"workload": "%s round: %d candidates, U{1..%d} statements (%d rows) x %d fp32 features, "
+                               "%d trees depth %d, MLP %s %d-%d-%d->%d+1, top-%d" % (
+                                   cfg.name, n_prog, cfg.s_max, n_rows, cfg.n_features, cfg.n_trees, cfg.depth,
+                                   cfg.pol_dtype, cfg.pol_s, cfg.pol_h1, cfg.pol_h2, cfg.pol_a, cfg.top_k),
+                   "global_batch": n_prog, "parallelism": "single-gpu"},
+        "roofline": {"bound": "alu", "kernel": "k_tree_score (+k_segsum) via harl_score_round",
+                     "achieved": gvisits, "peak": PEAK_GVISITS, "unit": "Gvisit/s", "frac": gvisits / PEAK_GVISITS,
+                     "traffic": None, "us_per_launch": score_ms * 1e3,
+                     "hbm_gbs": hbm_bytes / (score_ms * 1e-3) / 1e9,
+                     "hbm_frac": hbm_bytes / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+        "policy": {"kernel": "k_policy via harl_policy_step", "us_per_launch": pol_ms * 1e3, "achieved": pol_tflops,
+                   "peak": PEAK_MFMA_TFLOPS[cfg.pol_dtype], "unit": "TFLOP/s",
+                   "frac": pol_tflops / PEAK_MFMA_TFLOPS[cfg.pol_dtype]},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, ens, pol, b, args.cpu_seconds)
+    rnd.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,202 @@
+/*
+ * harl.h -- C ABI of libharl: one HARL search round's batched candidate evaluation on an MI355X.
+ *
+ * HARL (Zhang, He, Zhang, ICPP'22) searches tensor-program schedules with an actor/critic over
+ * parameter modifications and scores every visited schedule with a learned cost model
+ * (Algorithm 1; Sections 4.3 and 6.1).  One round of that loop, over all live candidates, is:
+ *
+ *   harl_policy_step  the actor pi_theta(M|S) picks each candidate's next modification and the
+ *                     critic V(S) gives its value (Algorithm 1, action selection; Eq. 6);
+ *   harl_score_round  the cost model C(S') scores every candidate: a gradient-boosted tree
+ *                     ensemble (XGBoost in the paper, Section 6.1, Appendix A.2) applied to each
+ *                     statement's feature row and summed over the program's statements;
+ *   harl_topk         the top-K candidates by predicted score (Algorithm 1, top-K phase;
+ *                     Section 4.3, Top-K Selection Phase), optionally merged into a running top-K
+ *                     that plays the heap H accumulating candidates across steps (Algorithm 1).
+ *
+ * Conventions for every call:
+ *   - Return value is a harl_status; nothing else signals an error and no C++ exception crosses
+ *     this interface.  harl_last_error() gives the message of the calling thread's last failure.
+ *   - Host-visible arguments (pointers, sizes, workspace size, alignment) are checked before any
+ *     HIP call; on failure nothing is launched and no output is touched.
+ *   - Pointers named d_* are device pointers (HIP device memory of the current device), owned by
+ *     the caller and left untouched beyond the documented outputs.  Pointers in *_desc structs are
+ *     host pointers, read only during the create call.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Hot-path calls are asynchronous
+ *     and stream-ordered: they enqueue kernels and return; they allocate nothing and never
+ *     synchronise.  Create/destroy calls allocate/free device memory and synchronise `stream`.
+ *   - Device-content preconditions (e.g. a monotone prog_ptr) are the caller's to uphold; the
+ *     kernels clamp every index they derive from device data, so a violation gives wrong numbers,
+ *     never an out-of-bounds access.
+ *   - Results are deterministic: fixed-order reductions, no floating-point atomics.
+ */
+#ifndef HARL_H
+#define HARL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HARL_OK = 0,
+    HARL_E_INVALID_ARG = -1, /* a null pointer, bad size, bad alignment or malformed model      */
+    HARL_E_UNSUPPORTED = -2, /* a valid request outside what this build implements               */
+    HARL_E_WORKSPACE = -3,   /* the workspace is smaller than the matching *_workspace_size()   */
+    HARL_E_HIP = -4,         /* a HIP runtime call or kernel launch failed                      */
+    HARL_E_NOMEM = -5        /* a device allocation failed (create calls only)                  */
+} harl_status;
+
+typedef enum { HARL_F32 = 0, HARL_BF16 = 1 } harl_dtype;
+
+/* Message for the calling thread's last non-OK return ("" if none).  Valid until the next call. */
+const char *harl_last_error(void);
+
+/* Library version string, e.g. "harl 0.1 gfx950". */
+const char *harl_version(void);
+
+/* ============================================================================================
+ * Cost model: a GBDT ensemble (Section 6.1 and Appendix A.2: XGBoost with Ansor's settings).
+ * ============================================================================================ */
+
+/*
+ * Host description of a tree ensemble, in explicit node arrays over all trees.
+ * Node n is a leaf iff feature[n] < 0; a leaf contributes leaf_value[n].  An internal node sends a
+ * feature value x to left[n] iff x < threshold[n] (strict; x == threshold goes right); a missing
+ * value (NaN) goes left iff default_left[n] != 0.  Tree t starts at node root[t].  Trees may be
+ * irregular; a tree whose leaves sit at different depths is packed as a complete tree of its
+ * ensemble's largest depth (an early leaf is repeated below dummy splits, which does not change
+ * any result).  A NaN threshold sends every non-missing value right.
+ * Limits: 1 <= n_trees; 1 <= n_features <= 448 (a 64-row feature tile must fit the LDS);
+ * largest root-to-leaf depth <= 12;
+ * every child id in [0, n_nodes); every tree acyclic.
+ */
+typedef struct {
+    int32_t n_trees;
+    int32_t n_features;
+    int32_t n_nodes;              /* total nodes over all trees                                 */
+    const int32_t *root;          /* [n_trees]                                                  */
+    const int32_t *feature;       /* [n_nodes], < 0 for a leaf                                  */
+    const float *threshold;       /* [n_nodes], read for internal nodes                         */
+    const int32_t *left;          /* [n_nodes], read for internal nodes                         */
+    const int32_t *right;         /* [n_nodes], read for internal nodes                         */
+    const uint8_t *default_left;  /* [n_nodes], read for internal nodes                         */
+    const float *leaf_value;      /* [n_nodes], read for leaves                                 */
+    float base_score;             /* added once to every program's score                        */
+} harl_ensemble_desc;
+
+typedef struct harl_ensemble harl_ensemble;
+
+/* Validate and pack `desc` into a library-owned device copy on the current device.  *out
+ * receives the handle (NULL on failure).  Synchronises `stream`. */
+int harl_ensemble_create(const harl_ensemble_desc *desc, harl_ensemble **out, void *stream);
+/* Free a handle (NULL is a no-op).  The caller must not destroy it while work using it runs. */
+int harl_ensemble_destroy(harl_ensemble *ens);
+/* Packed depth and tree count of a handle (for sizing); returns HARL_E_INVALID_ARG on NULL. */
+int harl_ensemble_info(const harl_ensemble *ens, int32_t *n_trees, int32_t *depth, int32_t *n_features);
+
+/* Bytes of device workspace harl_score_round needs for n_rows statement rows. */
+size_t harl_score_round_workspace_size(const harl_ensemble *ens, int32_t n_rows, int32_t n_prog);
+
+/*
+ * Cost-model scores of one round's candidates (Algorithm 1: C(S') for every new schedule).
+ *
+ *   d_feat      [n_features][ld] fp32, feature-major: feature f of statement row r is
+ *               d_feat[f*ld + r].  4-byte aligned, ld >= n_rows; 16-byte alignment with
+ *               ld % 4 == 0 lets the kernel stage rows with 16-byte loads.
+ *   n_rows      statement rows in this round (>= 0).
+ *   d_prog_ptr  [n_prog+1] int32: program p owns rows [d_prog_ptr[p], d_prog_ptr[p+1]);
+ *               0 = d_prog_ptr[0] <= ... <= d_prog_ptr[n_prog] = n_rows (caller's precondition).
+ *   d_prog_score [n_prog] fp32 out: base_score + sum of its statements' ensemble sums.
+ *   d_stmt_score [n_rows] fp32 out, or NULL: each statement row's ensemble sum.
+ *   d_ws, ws_bytes  device workspace of at least harl_score_round_workspace_size() bytes,
+ *               256-byte aligned; its contents on entry are ignored.
+ * Sums over trees and over a program's statements are accumulated in fp64 in a fixed order and
+ * rounded once to fp32.  n_prog == 0 is a no-op.
+ */
+int harl_score_round(const harl_ensemble *ens, const float *d_feat, int64_t ld, int32_t n_rows,
+                     const int32_t *d_prog_ptr, int32_t n_prog, float *d_prog_score,
+                     float *d_stmt_score, void *d_ws, size_t ws_bytes, void *stream);
+
+/* ============================================================================================
+ * Actor / critic (Section 4.3; Algorithm 1; Eq. 6 defines the critic's use).
+ * ============================================================================================ */
+
+/*
+ * Host description of the actor/critic: a shared trunk h1 = ReLU(W1 s + b1),
+ * h2 = ReLU(W2 h1 + b2), an actor head logits = Wa h2 + ba and a value head v = wv . h2 + bv.
+ * Weights are [out][in] row-major (PyTorch nn.Linear layout): fp32 for HARL_F32, raw bf16 bit
+ * patterns (uint16) for HARL_BF16.  Biases are fp32.  A HARL_BF16 policy takes bf16 states, uses
+ * bf16 x bf16 products with fp32 accumulation, and rounds h1 and h2 to bf16 (nearest, ties to
+ * even) after bias and ReLU; a HARL_F32 policy is fp32 throughout.
+ * Limits: 1 <= s <= 1024; 1 <= h1, h2 <= 4096; 1 <= a <= 255.
+ */
+typedef struct {
+    harl_dtype dtype;
+    int32_t s, h1, h2, a;
+    const void *w1;   /* [h1][s]  */
+    const float *b1;  /* [h1]     */
+    const void *w2;   /* [h2][h1] */
+    const float *b2;  /* [h2]     */
+    const void *wa;   /* [a][h2]  */
+    const float *ba;  /* [a]      */
+    const void *wv;   /* [h2]     */
+    const float *bv;  /* [1]      */
+} harl_policy_desc;
+
+typedef struct harl_policy harl_policy;
+
+/* Validate and pre-tile the weights into a library-owned device copy.  Synchronises `stream`. */
+int harl_policy_create(const harl_policy_desc *desc, harl_policy **out, void *stream);
+int harl_policy_destroy(harl_policy *pol);
+
+/*
+ * Actor/critic forward for B states (Algorithm 1: select M with pi_theta(M|S); critic V(S)).
+ *   d_states  [B][s] row-major, fp32 or bf16 bits per the policy's dtype; 16-byte aligned.
+ *   d_action  [B] int32 out: the lowest index attaining the largest logit.
+ *   d_value   [B] fp32 out: the critic's value.
+ *   d_probs   [B][a] fp32 out, or NULL: softmax of the logits.
+ *   d_logits  [B][a] fp32 out, or NULL: the actor's logits.
+ * B == 0 is a no-op.
+ */
+int harl_policy_step(const harl_policy *pol, const void *d_states, int32_t B, int32_t *d_action,
+                     float *d_value, float *d_probs, float *d_logits, void *stream);
+
+/* ============================================================================================
+ * Top-K selection (Algorithm 1, top-K phase) and the running heap H.
+ * ============================================================================================ */
+
+#define HARL_TOPK_MAX_K 2048
+/* flags for harl_topk */
+#define HARL_TOPK_MERGE 1u
+
+/* Bytes of device workspace harl_topk needs for n scores and a given k. */
+size_t harl_topk_workspace_size(int32_t n, int32_t k);
+
+/*
+ * The k best of n scores, ranked by (score descending, index ascending); score -0 ties +0 and
+ * NaN ranks below every number.  Candidate i carries the global index index_base + i.
+ *   d_score              [n] fp32 in, 4-byte aligned.
+ *   d_io_score/io_index  [k] fp32 / int64.  Without HARL_TOPK_MERGE they receive the top k of
+ *                        this call (k <= n required).  With HARL_TOPK_MERGE they must hold a
+ *                        running top-k (ranked as above, e.g. from harl_topk_reset or an earlier
+ *                        call) and are replaced by the top k of their union with this call's n
+ *                        candidates (any n >= 0).  Output scores are bit copies of the inputs.
+ *   d_ws, ws_bytes       workspace of at least harl_topk_workspace_size(n, k) bytes,
+ *                        256-byte aligned.
+ * 1 <= k <= HARL_TOPK_MAX_K (k == 0 is a no-op); n >= 0; index_base >= 0 and
+ * index_base + n < 2^62.
+ */
+int harl_topk(const float *d_score, int32_t n, int32_t k, int64_t index_base, float *d_io_score,
+              int64_t *d_io_index, uint32_t flags, void *d_ws, size_t ws_bytes, void *stream);
+
+/* Fill a running top-k with the empty sentinel (-inf, INT64_MAX) in every slot. */
+int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HARL_H */

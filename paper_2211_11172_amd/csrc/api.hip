@@ -1,0 +1,146 @@
+// libharl C ABI: argument validation and dispatch.  Every host-visible check runs before any HIP
+// call, so a rejected call launches nothing and touches no output.
+#include <hip/hip_runtime.h>
+
+#include <string>
+
+#include "internal.hpp"
+
+namespace harl {
+
+static thread_local std::string g_last_error;
+
+int fail(int status, const std::string &msg) {
+    g_last_error = msg;
+    return status;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return HARL_E_HIP;
+}
+
+}  // namespace harl
+
+using harl::aligned;
+using harl::fail;
+
+extern "C" {
+
+const char *harl_last_error(void) { return harl::g_last_error.c_str(); }
+
+const char *harl_version(void) { return "harl 0.1 gfx950"; }
+
+int harl_ensemble_create(const harl_ensemble_desc *desc, harl_ensemble **out, void *stream) {
+    if (!desc || !out) return fail(HARL_E_INVALID_ARG, "harl_ensemble_create: null desc or out");
+    *out = nullptr;
+    return harl::pack_ensemble(desc, out, static_cast<hipStream_t>(stream));
+}
+
+int harl_ensemble_destroy(harl_ensemble *ens) {
+    if (!ens) return HARL_OK;
+    hipError_t e = hipFree(ens->d_trees);
+    delete ens;
+    return e == hipSuccess ? HARL_OK : harl::hip_fail(e, "harl_ensemble_destroy");
+}
+
+int harl_ensemble_info(const harl_ensemble *ens, int32_t *n_trees, int32_t *depth, int32_t *n_features) {
+    if (!ens) return fail(HARL_E_INVALID_ARG, "harl_ensemble_info: null handle");
+    if (n_trees) *n_trees = ens->n_trees;
+    if (depth) *depth = ens->depth;
+    if (n_features) *n_features = ens->n_features;
+    return HARL_OK;
+}
+
+size_t harl_score_round_workspace_size(const harl_ensemble *ens, int32_t n_rows, int32_t n_prog) {
+    (void)n_prog;
+    if (!ens || n_rows < 0) return 0;
+    return harl::score_round_ws_bytes(ens, n_rows);
+}
+
+int harl_score_round(const harl_ensemble *ens, const float *d_feat, int64_t ld, int32_t n_rows,
+                     const int32_t *d_prog_ptr, int32_t n_prog, float *d_prog_score, float *d_stmt_score,
+                     void *d_ws, size_t ws_bytes, void *stream) {
+    if (!ens) return fail(HARL_E_INVALID_ARG, "harl_score_round: null ensemble");
+    if (n_rows < 0 || n_prog < 0) return fail(HARL_E_INVALID_ARG, "harl_score_round: negative size");
+    if (n_prog == 0) return HARL_OK;
+    if (!d_prog_ptr || !d_prog_score) return fail(HARL_E_INVALID_ARG, "harl_score_round: null prog_ptr or prog_score");
+    if (n_rows > 0 && !d_feat) return fail(HARL_E_INVALID_ARG, "harl_score_round: null features");
+    if (ld < n_rows) return fail(HARL_E_INVALID_ARG, "harl_score_round: ld must be >= n_rows");
+    if (ld > ((int64_t)1 << 40)) return fail(HARL_E_INVALID_ARG, "harl_score_round: ld too large");
+    if (d_feat && !aligned(d_feat, 4)) return fail(HARL_E_INVALID_ARG, "harl_score_round: features must be 4-byte aligned");
+    if (!aligned(d_prog_ptr, 4) || !aligned(d_prog_score, 4) || (d_stmt_score && !aligned(d_stmt_score, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_score_round: misaligned int32/fp32 array");
+    if (!d_ws || !aligned(d_ws, 256)) return fail(HARL_E_INVALID_ARG, "harl_score_round: workspace null or not 256-byte aligned");
+    if (ws_bytes < harl::score_round_ws_bytes(ens, n_rows))
+        return fail(HARL_E_WORKSPACE, "harl_score_round: workspace smaller than harl_score_round_workspace_size()");
+    return harl::score_round_launch(ens, d_feat, ld, n_rows, d_prog_ptr, n_prog, d_prog_score, d_stmt_score, d_ws,
+                                    ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int harl_policy_create(const harl_policy_desc *desc, harl_policy **out, void *stream) {
+    if (!desc || !out) return fail(HARL_E_INVALID_ARG, "harl_policy_create: null desc or out");
+    *out = nullptr;
+    return harl::pack_policy(desc, out, static_cast<hipStream_t>(stream));
+}
+
+int harl_policy_destroy(harl_policy *pol) {
+    if (!pol) return HARL_OK;
+    void *ptrs[] = {pol->d_w1, pol->d_w2, pol->d_wh, pol->d_b1, pol->d_b2, pol->d_bh};
+    hipError_t first = hipSuccess;
+    for (void *p : ptrs) {
+        hipError_t e = hipFree(p);
+        if (first == hipSuccess) first = e;
+    }
+    delete pol;
+    return first == hipSuccess ? HARL_OK : harl::hip_fail(first, "harl_policy_destroy");
+}
+
+int harl_policy_step(const harl_policy *pol, const void *d_states, int32_t B, int32_t *d_action, float *d_value,
+                     float *d_probs, float *d_logits, void *stream) {
+    if (!pol) return fail(HARL_E_INVALID_ARG, "harl_policy_step: null policy");
+    if (B < 0) return fail(HARL_E_INVALID_ARG, "harl_policy_step: negative batch");
+    if (B == 0) return HARL_OK;
+    if (!d_states || !d_action || !d_value) return fail(HARL_E_INVALID_ARG, "harl_policy_step: null states, action or value");
+    const size_t el = pol->dtype == HARL_BF16 ? 2 : 4;
+    if (!aligned(d_states, el) || !aligned(d_action, 4) || !aligned(d_value, 4) || (d_probs && !aligned(d_probs, 4)) ||
+        (d_logits && !aligned(d_logits, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_policy_step: misaligned array");
+    return harl::policy_step_launch(pol, d_states, B, d_action, d_value, d_probs, d_logits,
+                                    static_cast<hipStream_t>(stream));
+}
+
+size_t harl_topk_workspace_size(int32_t n, int32_t k) {
+    if (n < 0 || k < 0) return 0;
+    return harl::topk_ws_bytes(n, k);
+}
+
+int harl_topk(const float *d_score, int32_t n, int32_t k, int64_t index_base, float *d_io_score, int64_t *d_io_index,
+              uint32_t flags, void *d_ws, size_t ws_bytes, void *stream) {
+    if (n < 0 || k < 0) return fail(HARL_E_INVALID_ARG, "harl_topk: negative size");
+    if (k > HARL_TOPK_MAX_K) return fail(HARL_E_UNSUPPORTED, "harl_topk: k above HARL_TOPK_MAX_K");
+    if (flags & ~HARL_TOPK_MERGE) return fail(HARL_E_INVALID_ARG, "harl_topk: unknown flag");
+    if (!(flags & HARL_TOPK_MERGE) && k > n) return fail(HARL_E_INVALID_ARG, "harl_topk: k > n without HARL_TOPK_MERGE");
+    if (index_base < 0 || index_base > ((int64_t)1 << 62) - 1 - n)
+        return fail(HARL_E_INVALID_ARG, "harl_topk: index_base out of range");
+    if (k == 0) return HARL_OK;
+    if (!d_io_score || !d_io_index) return fail(HARL_E_INVALID_ARG, "harl_topk: null output");
+    if (!aligned(d_io_score, 4) || !aligned(d_io_index, 8)) return fail(HARL_E_INVALID_ARG, "harl_topk: misaligned output");
+    if (n == 0) return HARL_OK;  // only reachable with MERGE: nothing to merge
+    if (!d_score || !aligned(d_score, 4)) return fail(HARL_E_INVALID_ARG, "harl_topk: null or misaligned scores");
+    if (!d_ws || !aligned(d_ws, 256)) return fail(HARL_E_INVALID_ARG, "harl_topk: workspace null or not 256-byte aligned");
+    if (ws_bytes < harl::topk_ws_bytes(n, k))
+        return fail(HARL_E_WORKSPACE, "harl_topk: workspace smaller than harl_topk_workspace_size()");
+    return harl::topk_launch(d_score, n, k, index_base, d_io_score, d_io_index, flags, d_ws, ws_bytes,
+                             static_cast<hipStream_t>(stream));
+}
+
+int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *stream) {
+    if (k < 0 || k > HARL_TOPK_MAX_K) return fail(HARL_E_INVALID_ARG, "harl_topk_reset: k out of range");
+    if (k == 0) return HARL_OK;
+    if (!d_io_score || !d_io_index || !aligned(d_io_score, 4) || !aligned(d_io_index, 8))
+        return fail(HARL_E_INVALID_ARG, "harl_topk_reset: null or misaligned output");
+    return harl::topk_reset_launch(d_io_score, d_io_index, k, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+// Internal declarations shared by the libharl translation units (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/harl.h"
+
+namespace harl {
+
+// Thread-local error text behind harl_last_error().
+int fail(int status, const std::string &msg);
+int hip_fail(hipError_t e, const char *what);
+
+#define HARL_HIP_CHECK(expr)                                      \
+    do {                                                          \
+        hipError_t _e = (expr);                                   \
+        if (_e != hipSuccess) return ::harl::hip_fail(_e, #expr); \
+    } while (0)
+
+inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// ------------------------------------------------------------------------------------------
+// Packed GBDT ensemble.  Every tree is stored as a complete binary tree of `depth` split levels,
+// numbered breadth-first from 1: internal node i (1 <= i < 2^depth) is 8 bytes {u32 word,
+// f32 threshold} at byte 8*i (bytes 0..7 pad), its children are 2i (left) and 2i+1 (right), and
+// the 2^depth fp32 leaves follow at byte 8 * 2^depth (leaf j = slot 2^depth + j).  The stride of
+// one tree is 12 * 2^depth bytes rounded up to 16.  The node word holds the split feature in bits
+// 0..23 and the missing-goes-left flag in bit 31.
+// ------------------------------------------------------------------------------------------
+constexpr int kMaxDepth = 12;
+constexpr int kMaxFeatures = 448;
+constexpr uint32_t kNodeDefaultLeft = 0x80000000u;
+
+}  // namespace harl
+
+struct harl_ensemble {
+    int32_t n_trees;
+    int32_t n_features;
+    int32_t depth;
+    int32_t tree_stride;  // bytes per packed tree (multiple of 16)
+    float base_score;
+    int device;
+    void *d_trees;        // n_trees * tree_stride bytes
+};
+
+// ------------------------------------------------------------------------------------------
+// Packed actor/critic.  Weights are pre-tiled into the exact per-lane MFMA operand order of the
+// policy kernel (one coalesced load per fragment); see policy.hip for the fragment layouts.
+// ------------------------------------------------------------------------------------------
+struct harl_policy {
+    harl_dtype dtype;
+    int32_t s, h1, h2, a;        // logical sizes
+    int32_t sp, h1p, h2p, hap;   // padded sizes: input, hidden 1, hidden 2, heads (a+1 rounded)
+    int device;
+    void *d_w1, *d_w2, *d_wh;    // fragment-ordered weights
+    float *d_b1, *d_b2, *d_bh;   // padded biases (bh = [ba; bv; 0...])
+};
+
+namespace harl {
+
+// Launchers (stream-ordered, no allocation, no sync).  Arguments are already validated.
+int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows,
+                       const int32_t *prog_ptr, int32_t n_prog, float *prog_score, float *stmt_score,
+                       void *ws, size_t ws_bytes, hipStream_t stream);
+size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows);
+int pack_ensemble(const harl_ensemble_desc *desc, harl_ensemble **out, hipStream_t stream);
+
+int pack_policy(const harl_policy_desc *desc, harl_policy **out, hipStream_t stream);
+int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int32_t *action,
+                       float *value, float *probs, float *logits, hipStream_t stream);
+
+size_t topk_ws_bytes(int32_t n, int32_t k);
+int topk_launch(const float *score, int32_t n, int32_t k, int64_t index_base, float *io_score,
+                int64_t *io_index, uint32_t flags, void *ws, size_t ws_bytes, hipStream_t stream);
+int topk_reset_launch(float *io_score, int64_t *io_index, int32_t k, hipStream_t stream);
+
+}  // namespace harl

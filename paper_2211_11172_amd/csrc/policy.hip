@@ -1,0 +1,473 @@
+// Actor/critic forward of one search round (HARL paper, Algorithm 1: select the modifications M
+// with pi_theta(M|S); the critic V(S) of Eq. 6; Section 4.3).  Shared trunk
+// h1 = ReLU(W1 s + b1), h2 = ReLU(W2 h1 + b2); actor head logits = Wa h2 + ba; value head
+// v = wv . h2 + bv; action = lowest-index argmax of the logits; probs = softmax(logits).
+//
+// K4 k_policy: the three dense contractions run on MFMA, transposed so that states are the MFMA
+// N dimension (H^T = W X^T).  A workgroup holds 16*NSG states and 4 waves.
+//   phase 0  the states are staged into LDS ([state][unit], padded rows);
+//   phase 1  each wave computes a quarter of h1's 16-unit tiles for all states (A = W1 fragments
+//            streamed from global memory through an 8-deep register ring, B = states from LDS),
+//            applies bias + ReLU (+ bf16 rounding) and stores the tile to LDS;
+//   phase 2  each wave computes a quarter of h2's tiles the same way (B = h1 from LDS; every A
+//            fragment feeds NSG state groups) and feeds each finished tile straight from its
+//            accumulator registers into the head contraction: the MFMA result layout of a tile is
+//            re-used as the B operand layout, with the head weights pre-permuted to match;
+//   phase 3  the four per-wave partial heads are summed in a fixed order; bias, argmax, softmax
+//            and value are computed per state and written out.
+// fp32 policies use v_mfma_f32_16x16x4_f32, bf16 policies v_mfma_f32_16x16x32_bf16 (fp32
+// accumulation; h1, h2 rounded to bf16, nearest even).  Weights are pre-tiled at create time so
+// that a lane's operand for one "k-group" is 16 contiguous bytes:
+//   fp32: a k-group is 16 input units = 4 MFMAs; lane l, slot j (j < 4) holds unit 16g + 4(l/16) + j
+//   bf16: a k-group is 32 input units = 1 MFMA;  lane l, slot j (j < 8) holds unit 32g + 8(l/16) + j
+// so an activation row in LDS ([state][unit]) gives the B operand of k-group g at byte offset
+// 64g + 16(l/16) for either dtype.
+//
+// MFMA operand layouts (lane l of 64; i indexes the 4 accumulator registers):
+//   16x16x4  f32 : A[m = l%16][k = l/16],          B[k = l/16][n = l%16]
+//   16x16x32 bf16: A[m = l%16][k = 8(l/16) + j],   B[k = 8(l/16) + j][n = l%16],  j = 0..7
+//   result       : D[m = 4(l/16) + i][n = l%16]
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "internal.hpp"
+
+namespace harl {
+namespace {
+
+constexpr int kU = 4;     // waves per workgroup
+constexpr int kRing = 8;  // weight fragments in flight per wave
+constexpr int kMaxHT = 8; // head tiles: a + 1 <= 128
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+    // fp32 -> bf16 bits, nearest even (finite inputs: activations after ReLU)
+    uint32_t b = __float_as_uint(x);
+    b += 0x7FFFu + ((b >> 16) & 1u);
+    return b >> 16;
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
+    bf16x8 r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+
+template <bool BF16>
+__device__ __forceinline__ void mfma_group(const uint4 &a, const uint4 &b, f32x4 &acc) {
+    if constexpr (BF16) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), acc, 0, 0, 0);
+    } else {
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    }
+}
+
+struct PolicyArgs {
+    const void *states;
+    int B, S;
+    int sp, h1p, h2p, hap, a;
+    const uint4 *w1, *w2, *wh;
+    const float *b1, *b2, *bh;
+    int32_t *action;
+    float *value, *probs, *logits;
+};
+
+// One dense layer for this wave: `n_tiles` output tiles of 16 units starting at tile `t0`, each a
+// sum over KG k-groups; A fragments come from `A` (packed [tile][g][lane] x 16 B) through a ring
+// of kRing registers, B from the LDS activation rows `in` (row stride `in_stride` bytes).
+// done(tile_index, acc[NSG]) consumes each finished tile.
+template <bool BF16, int NSG, typename Done>
+__device__ __forceinline__ void dense_layer(const uint4 *__restrict__ A, int t0, int n_tiles, int KG, const char *in,
+                                            int in_stride, int ln, int lq, int l, Done done) {
+    const int NIT = n_tiles * KG;
+    const uint4 *Ap = A + (int64_t)t0 * KG * 64 + l;
+    uint4 ring[kRing];
+#pragma unroll
+    for (int r = 0; r < kRing; ++r) ring[r] = r < NIT ? Ap[(int64_t)r * 64] : make_uint4(0, 0, 0, 0);
+    f32x4 acc[NSG];
+#pragma unroll
+    for (int sg = 0; sg < NSG; ++sg) acc[sg] = f32x4{0, 0, 0, 0};
+    int g = 0, tile = t0;
+    for (int it0 = 0; it0 < NIT; it0 += kRing) {
+#pragma unroll
+        for (int r = 0; r < kRing; ++r) {
+            const int it = it0 + r;
+            if (it < NIT) {
+                const uint4 a = ring[r];
+                if (it + kRing < NIT) ring[r] = Ap[(int64_t)(it + kRing) * 64];
+#pragma unroll
+                for (int sg = 0; sg < NSG; ++sg) {
+                    const uint4 b = *reinterpret_cast<const uint4 *>(in + (sg * 16 + ln) * in_stride + g * 64 + lq * 16);
+                    mfma_group<BF16>(a, b, acc[sg]);
+                }
+                if (++g == KG) {
+                    done(tile, acc);
+#pragma unroll
+                    for (int sg = 0; sg < NSG; ++sg) acc[sg] = f32x4{0, 0, 0, 0};
+                    g = 0;
+                    ++tile;
+                }
+            }
+        }
+    }
+}
+
+template <bool BF16, int NSG>
+__global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
+    extern __shared__ __align__(16) char smem[];
+    constexpr int EL = BF16 ? 2 : 4;        // bytes per activation element
+    constexpr int UPG = BF16 ? 32 : 16;     // input units per k-group
+    const int wid = threadIdx.x / 64, l = threadIdx.x % 64;
+    const int ln = l % 16, lq = l / 16;
+    const int s0 = blockIdx.x * 16 * NSG;
+    constexpr int NS = 16 * NSG;
+    const int xs_stride = p.sp * EL + 16;   // bytes per state row (padded against bank conflicts)
+    const int h1_stride = p.h1p * EL + 16;
+    char *xs = smem;
+    char *h1 = smem + NS * xs_stride;
+    const int HT = p.hap / 16;
+
+    // ---------------- phase 0: states -> LDS [state][unit] (zero beyond S and B) ----------------
+    {
+        const int row_elems = p.sp;
+        for (int e = threadIdx.x; e < NS * row_elems; e += 256) {
+            const int r = e / row_elems, c = e % row_elems;
+            const int st = s0 + r;
+            if constexpr (BF16) {
+                uint16_t v = 0;
+                if (st < p.B && c < p.S) v = static_cast<const uint16_t *>(p.states)[(int64_t)st * p.S + c];
+                *reinterpret_cast<uint16_t *>(xs + r * xs_stride + c * 2) = v;
+            } else {
+                float v = 0.f;
+                if (st < p.B && c < p.S) v = static_cast<const float *>(p.states)[(int64_t)st * p.S + c];
+                *reinterpret_cast<float *>(xs + r * xs_stride + c * 4) = v;
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---------------- phase 1: h1 = act(W1 s + b1), this wave's quarter of the tiles ----------------
+    {
+        const int mt_per = p.h1p / 16 / kU;
+        dense_layer<BF16, NSG>(p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
+                               [&](int mt, f32x4 *acc) {
+                                   const int u0 = mt * 16 + lq * 4;
+#pragma unroll
+                                   for (int sg = 0; sg < NSG; ++sg) {
+                                       float h[4];
+#pragma unroll
+                                       for (int i = 0; i < 4; ++i) h[i] = fmaxf(acc[sg][i] + p.b1[u0 + i], 0.f);
+                                       char *dst = h1 + (sg * 16 + ln) * h1_stride + u0 * EL;
+                                       if constexpr (BF16) {
+                                           uint2 v = make_uint2(bf16_rne(h[0]) | (bf16_rne(h[1]) << 16),
+                                                                bf16_rne(h[2]) | (bf16_rne(h[3]) << 16));
+                                           *reinterpret_cast<uint2 *>(dst) = v;
+                                       } else {
+                                           *reinterpret_cast<float4 *>(dst) = make_float4(h[0], h[1], h[2], h[3]);
+                                       }
+                                   }
+                               });
+    }
+    __syncthreads();
+
+    // ------- phase 2: h2 tiles of this wave, chained into the partial heads (registers) -------
+    f32x4 hacc[NSG][kMaxHT];
+#pragma unroll
+    for (int sg = 0; sg < NSG; ++sg)
+#pragma unroll
+        for (int ht = 0; ht < kMaxHT; ++ht) hacc[sg][ht] = f32x4{0, 0, 0, 0};
+    {
+        const int mt_per = p.h2p / 16 / kU;
+        const int mt_first = wid * mt_per;
+        // head fragments: fp32 one k-group per h2 tile, bf16 one per pair of h2 tiles
+        const int HKG = BF16 ? p.h2p / 32 : p.h2p / 16;
+        uint4 hpf[kMaxHT];
+        auto head_fetch = [&](int hk) {
+#pragma unroll
+            for (int ht = 0; ht < kMaxHT; ++ht)
+                if (ht < HT && hk < HKG) hpf[ht] = p.wh[((int64_t)ht * HKG + hk) * 64 + l];
+        };
+        head_fetch(BF16 ? mt_first / 2 : mt_first);
+        uint32_t stash[NSG][2];  // bf16: the even tile of a pair, 4 packed bf16
+        dense_layer<BF16, NSG>(p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l,
+                               [&](int mt, f32x4 *acc) {
+                                   const int u0 = mt * 16 + lq * 4;
+                                   float bias[4];
+#pragma unroll
+                                   for (int i = 0; i < 4; ++i) bias[i] = p.b2[u0 + i];
+                                   if constexpr (BF16) {
+                                       if ((mt & 1) == 0) {
+#pragma unroll
+                                           for (int sg = 0; sg < NSG; ++sg) {
+                                               stash[sg][0] = bf16_rne(fmaxf(acc[sg][0] + bias[0], 0.f)) |
+                                                              (bf16_rne(fmaxf(acc[sg][1] + bias[1], 0.f)) << 16);
+                                               stash[sg][1] = bf16_rne(fmaxf(acc[sg][2] + bias[2], 0.f)) |
+                                                              (bf16_rne(fmaxf(acc[sg][3] + bias[3], 0.f)) << 16);
+                                           }
+                                           return;
+                                       }
+#pragma unroll
+                                       for (int sg = 0; sg < NSG; ++sg) {
+                                           uint4 bv;
+                                           bv.x = stash[sg][0];
+                                           bv.y = stash[sg][1];
+                                           bv.z = bf16_rne(fmaxf(acc[sg][0] + bias[0], 0.f)) | (bf16_rne(fmaxf(acc[sg][1] + bias[1], 0.f)) << 16);
+                                           bv.w = bf16_rne(fmaxf(acc[sg][2] + bias[2], 0.f)) | (bf16_rne(fmaxf(acc[sg][3] + bias[3], 0.f)) << 16);
+#pragma unroll
+                                           for (int ht = 0; ht < kMaxHT; ++ht)
+                                               if (ht < HT) mfma_group<true>(hpf[ht], bv, hacc[sg][ht]);
+                                       }
+                                       head_fetch(mt / 2 + 1);
+                                   } else {
+#pragma unroll
+                                       for (int sg = 0; sg < NSG; ++sg) {
+                                           uint4 bv;
+                                           bv.x = __float_as_uint(fmaxf(acc[sg][0] + bias[0], 0.f));
+                                           bv.y = __float_as_uint(fmaxf(acc[sg][1] + bias[1], 0.f));
+                                           bv.z = __float_as_uint(fmaxf(acc[sg][2] + bias[2], 0.f));
+                                           bv.w = __float_as_uint(fmaxf(acc[sg][3] + bias[3], 0.f));
+#pragma unroll
+                                           for (int ht = 0; ht < kMaxHT; ++ht)
+                                               if (ht < HT) mfma_group<false>(hpf[ht], bv, hacc[sg][ht]);
+                                       }
+                                       head_fetch(mt + 1);
+                                   }
+                               });
+    }
+    __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
+
+    // ---------------- phase 3: fixed-order sum of the 4 partial heads, epilogue ----------------
+    float *part = reinterpret_cast<float *>(smem);  // [kU][NSG][hap][16]
+#pragma unroll
+    for (int sg = 0; sg < NSG; ++sg)
+#pragma unroll
+        for (int ht = 0; ht < kMaxHT; ++ht)
+            if (ht < HT)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    part[(((int64_t)wid * NSG + sg) * p.hap + ht * 16 + lq * 4 + i) * 16 + ln] = hacc[sg][ht][i];
+    __syncthreads();
+    for (int sg = wid; sg < NSG; sg += kU) {
+        const int st = s0 + sg * 16 + ln;
+        float best = -INFINITY;
+        int best_i = 0x7FFFFFFF;
+        float val = 0.f;
+        float z[kMaxHT][4];  // rows owned by this lane: 16*ht + 4*lq + i
+#pragma unroll
+        for (int ht = 0; ht < kMaxHT; ++ht)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                z[ht][i] = 0.f;
+                if (ht >= HT) continue;
+                const int row = ht * 16 + lq * 4 + i;
+                float s = 0.f;
+#pragma unroll
+                for (int w = 0; w < kU; ++w) s += part[(((int64_t)w * NSG + sg) * p.hap + row) * 16 + ln];
+                s += p.bh[row];
+                z[ht][i] = s;
+                if (row < p.a && (s > best || (s == best && row < best_i))) {
+                    best = s;
+                    best_i = row;
+                }
+                if (row == p.a) val = s;
+            }
+        // combine over the 4 lanes of this state (xor 16, xor 32)
+#pragma unroll
+        for (int m = 16; m <= 32; m <<= 1) {
+            const float ob = __shfl_xor(best, m, 64);
+            const int oi = __shfl_xor(best_i, m, 64);
+            if (ob > best || (ob == best && oi < best_i)) {
+                best = ob;
+                best_i = oi;
+            }
+            val += __shfl_xor(val, m, 64);
+        }
+        if (best_i == 0x7FFFFFFF) best_i = 0;  // only NaN logits: no maximum exists
+        float sum = 0.f;
+        if (p.probs) {
+#pragma unroll
+            for (int ht = 0; ht < kMaxHT; ++ht)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = ht * 16 + lq * 4 + i;
+                    if (ht < HT && row < p.a) sum += expf(z[ht][i] - best);
+                }
+            sum += __shfl_xor(sum, 16, 64);
+            sum += __shfl_xor(sum, 32, 64);
+        }
+        if (st < p.B) {
+#pragma unroll
+            for (int ht = 0; ht < kMaxHT; ++ht)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = ht * 16 + lq * 4 + i;
+                    if (ht < HT && row < p.a) {
+                        if (p.logits) p.logits[(int64_t)st * p.a + row] = z[ht][i];
+                        if (p.probs) p.probs[(int64_t)st * p.a + row] = expf(z[ht][i] - best) / sum;
+                    }
+                }
+            if (lq == 0) {
+                p.action[st] = best_i;
+                p.value[st] = val;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+// host: weight pre-tiling
+// ---------------------------------------------------------------------------------------------
+// Pack the A operand of a [rows x K] row-major weight (fp32 values or bf16 bits) into 16-byte
+// per-lane fragments, order [tile][g][lane]: lane l, slot j of k-group g of tile mt holds
+// W[16 mt + l%16][kmap(g, l/16, j)], zero outside the matrix.
+template <typename KMap>
+std::vector<uint32_t> pack_frags(const void *W, bool bf, int rows, int K, int rows_p, int n_g, KMap kmap) {
+    const int per = bf ? 8 : 4;
+    std::vector<uint32_t> out;
+    out.reserve((size_t)rows_p / 16 * n_g * 64 * 4);
+    for (int mt = 0; mt < rows_p / 16; ++mt)
+        for (int g = 0; g < n_g; ++g)
+            for (int l = 0; l < 64; ++l) {
+                uint32_t slot[8] = {};
+                for (int j = 0; j < per; ++j) {
+                    const int r = mt * 16 + l % 16, k = kmap(g, l / 16, j);
+                    if (r >= rows || k < 0 || k >= K) continue;
+                    if (bf) slot[j] = static_cast<const uint16_t *>(W)[(int64_t)r * K + k];
+                    else std::memcpy(&slot[j], static_cast<const float *>(W) + (int64_t)r * K + k, 4);
+                }
+                if (bf)
+                    for (int w = 0; w < 4; ++w) out.push_back(slot[2 * w] | (slot[2 * w + 1] << 16));
+                else
+                    for (int w = 0; w < 4; ++w) out.push_back(slot[w]);
+            }
+    return out;
+}
+
+template <typename T>
+int upload(const std::vector<T> &h, void **d, hipStream_t stream) {
+    if (hipMalloc(d, h.size() * sizeof(T) + 16) != hipSuccess) return HARL_E_NOMEM;
+    if (hipMemcpyAsync(*d, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice, stream) != hipSuccess) return HARL_E_HIP;
+    return HARL_OK;
+}
+
+size_t policy_lds_bytes(const harl_policy *P, int nsg) {
+    const bool bf = P->dtype == HARL_BF16;
+    const size_t el = bf ? 2 : 4;
+    const size_t ns = 16 * (size_t)nsg;
+    const size_t acts = ns * (P->sp * el + 16) + ns * (P->h1p * el + 16);
+    const size_t part = (size_t)kU * nsg * P->hap * 16 * 4;
+    return acts > part ? acts : part;
+}
+
+}  // namespace
+
+int pack_policy(const harl_policy_desc *d, harl_policy **out, hipStream_t stream) {
+    if (d->dtype != HARL_F32 && d->dtype != HARL_BF16) return fail(HARL_E_INVALID_ARG, "harl_policy_create: bad dtype");
+    if (d->s < 1 || d->s > 1024 || d->h1 < 1 || d->h1 > 4096 || d->h2 < 1 || d->h2 > 4096 || d->a < 1 || d->a > 127)
+        return fail(HARL_E_INVALID_ARG, "harl_policy_create: sizes out of range");
+    if (!d->w1 || !d->b1 || !d->w2 || !d->b2 || !d->wa || !d->ba || !d->wv || !d->bv)
+        return fail(HARL_E_INVALID_ARG, "harl_policy_create: null weight or bias");
+    const bool bf = d->dtype == HARL_BF16;
+    const int UPG = bf ? 32 : 16;
+    const int sp = (int)round_up(d->s, UPG);
+    const int h1p = (int)round_up(d->h1, bf ? 32 * kU : 16 * kU);   // whole tiles per wave, whole k-groups
+    const int h2p = (int)round_up(d->h2, bf ? 32 * kU : 16 * kU);   // bf16: tile pairs per wave
+    const int hap = (int)round_up(d->a + 1, 16);
+    // heads as one matrix [a+1][h2]: rows 0..a-1 actor, row a value
+    const size_t esz = bf ? 2 : 4;
+    std::vector<uint8_t> wh((size_t)(d->a + 1) * d->h2 * esz);
+    std::memcpy(wh.data(), d->wa, (size_t)d->a * d->h2 * esz);
+    std::memcpy(wh.data() + (size_t)d->a * d->h2 * esz, d->wv, (size_t)d->h2 * esz);
+    std::vector<uint32_t> w1, w2, whp;
+    if (bf) {
+        auto kstd = [](int g, int q, int j) { return g * 32 + q * 8 + j; };
+        w1 = pack_frags(d->w1, true, d->h1, d->s, h1p, sp / 32, kstd);
+        w2 = pack_frags(d->w2, true, d->h2, d->h1, h2p, h1p / 32, kstd);
+        // head k-group p consumes h2 tiles 2p (slots 0..3) and 2p+1 (slots 4..7), each from the
+        // accumulator layout: unit 16 t + 4 q + i
+        auto khead = [](int pr, int q, int j) { return pr * 32 + (j / 4) * 16 + q * 4 + (j % 4); };
+        whp = pack_frags(wh.data(), true, d->a + 1, d->h2, hap, h2p / 32, khead);
+    } else {
+        auto kstd = [](int g, int q, int j) { return g * 16 + q * 4 + j; };
+        w1 = pack_frags(d->w1, false, d->h1, d->s, h1p, sp / 16, kstd);
+        w2 = pack_frags(d->w2, false, d->h2, d->h1, h2p, h1p / 16, kstd);
+        // head k-group t consumes h2 tile t from the accumulator layout (unit 16 t + 4 q + j): the
+        // same map as the standard one
+        whp = pack_frags(wh.data(), false, d->a + 1, d->h2, hap, h2p / 16, kstd);
+    }
+    std::vector<float> b1(h1p, 0.f), b2(h2p, 0.f), bh(hap, 0.f);
+    std::memcpy(b1.data(), d->b1, (size_t)d->h1 * 4);
+    std::memcpy(b2.data(), d->b2, (size_t)d->h2 * 4);
+    std::memcpy(bh.data(), d->ba, (size_t)d->a * 4);
+    bh[d->a] = d->bv[0];
+
+    harl_policy *P = new (std::nothrow) harl_policy{};
+    if (!P) return fail(HARL_E_NOMEM, "harl_policy_create: host allocation failed");
+    P->dtype = d->dtype;
+    P->s = d->s; P->h1 = d->h1; P->h2 = d->h2; P->a = d->a;
+    P->sp = sp; P->h1p = h1p; P->h2p = h2p; P->hap = hap;
+    (void)hipGetDevice(&P->device);
+    if (policy_lds_bytes(P, 1) > 160 * 1024) {
+        delete P;
+        return fail(HARL_E_UNSUPPORTED, "harl_policy_create: layers too wide for the LDS-resident activations");
+    }
+    void *b1d = nullptr, *b2d = nullptr, *bhd = nullptr;
+    int rc = upload(w1, &P->d_w1, stream);
+    if (rc == HARL_OK) rc = upload(w2, &P->d_w2, stream);
+    if (rc == HARL_OK) rc = upload(whp, &P->d_wh, stream);
+    if (rc == HARL_OK) rc = upload(b1, &b1d, stream);
+    if (rc == HARL_OK) rc = upload(b2, &b2d, stream);
+    if (rc == HARL_OK) rc = upload(bh, &bhd, stream);
+    P->d_b1 = static_cast<float *>(b1d);
+    P->d_b2 = static_cast<float *>(b2d);
+    P->d_bh = static_cast<float *>(bhd);
+    if (rc == HARL_OK && hipStreamSynchronize(stream) != hipSuccess) rc = HARL_E_HIP;
+    if (rc != HARL_OK) {
+        (void)hipFree(P->d_w1); (void)hipFree(P->d_w2); (void)hipFree(P->d_wh);
+        (void)hipFree(P->d_b1); (void)hipFree(P->d_b2); (void)hipFree(P->d_bh);
+        delete P;
+        return fail(rc, "harl_policy_create: device allocation or upload failed");
+    }
+    *out = P;
+    return HARL_OK;
+}
+
+int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int32_t *action, float *value,
+                       float *probs, float *logits, hipStream_t stream) {
+    if (B == 0) return HARL_OK;
+    PolicyArgs a{};
+    a.states = states;
+    a.B = B;
+    a.S = P->s;
+    a.sp = P->sp; a.h1p = P->h1p; a.h2p = P->h2p; a.hap = P->hap; a.a = P->a;
+    a.w1 = static_cast<const uint4 *>(P->d_w1);
+    a.w2 = static_cast<const uint4 *>(P->d_w2);
+    a.wh = static_cast<const uint4 *>(P->d_wh);
+    a.b1 = P->d_b1; a.b2 = P->d_b2; a.bh = P->d_bh;
+    a.action = action; a.value = value; a.probs = probs; a.logits = logits;
+    const bool bf = P->dtype == HARL_BF16;
+    // large bf16 batches share every weight fragment among 4 state groups (64 states per block)
+    int nsg = (bf && B >= 16 * 1024) ? 4 : 1;
+    if (policy_lds_bytes(P, nsg) > 160 * 1024) nsg = 1;
+    const size_t lds = policy_lds_bytes(P, nsg);
+    const unsigned grid = (unsigned)ceil_div(B, 16 * nsg);
+    const void *kern;
+    if (bf) kern = nsg == 4 ? reinterpret_cast<const void *>(k_policy<true, 4>) : reinterpret_cast<const void *>(k_policy<true, 1>);
+    else kern = reinterpret_cast<const void *>(k_policy<false, 1>);
+    HARL_HIP_CHECK(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    if (bf && nsg == 4) hipLaunchKernelGGL((k_policy<true, 4>), dim3(grid), dim3(256), lds, stream, a);
+    else if (bf) hipLaunchKernelGGL((k_policy<true, 1>), dim3(grid), dim3(256), lds, stream, a);
+    else hipLaunchKernelGGL((k_policy<false, 1>), dim3(grid), dim3(256), lds, stream, a);
+    HARL_HIP_CHECK(hipGetLastError());
+    return HARL_OK;
+}
+
+}  // namespace harl

@@ -1,0 +1,308 @@
+// Top-K selection of one round (Algorithm 1 of the HARL paper: "select top-K states from the
+// heap H"; Section 4.3, Top-K Selection Phase) and the running top-K that plays the heap H
+// accumulating candidates across steps.
+//
+// Ranking: score descending, then global index ascending; -0 ties +0; NaN below every number.
+// A score becomes a 32-bit order key (larger key = better); candidate i's 64-bit composite is
+// key << 32 | (0xFFFFFFFF - i), so the ranking is the descending order of unique composites and
+// every selection below is exact and deterministic.
+//
+// K3 k_topk_select: a workgroup of 1024 threads owns a segment of up to 8192 candidates, held in
+//    registers.  A most-significant-digit radix select (8 bits per pass over the composite,
+//    per-wave LDS histograms, early exit once a digit bucket holds exactly the ranks still needed;
+//    a segment of at most kk candidates keeps them all) finds the
+//    segment's kk best; they are compacted into LDS and bitonic-sorted (only kk <= 2048 keys).
+//    Segments run in parallel; their sorted outputs form the next round's candidates until one
+//    segment is left, whose workgroup writes the final top-k directly.
+// K5 k_topk_merge: merges the sorted top-k of this call into the sorted running top-k by rank
+//    computation (an element's output slot is its own index plus the number of elements of the
+//    other list that rank ahead of it).
+#include <hip/hip_runtime.h>
+
+#include "internal.hpp"
+
+namespace harl {
+namespace {
+
+constexpr int kSelThreads = 1024;
+constexpr int kPerThread = 8;
+constexpr int kSeg = kSelThreads * kPerThread;  // candidates per workgroup
+constexpr int kMergeThreads = 1024;
+
+__device__ __forceinline__ uint32_t order_key(float s) {
+    uint32_t b = __float_as_uint(s);
+    if (s != s) return 0u;                  // NaN ranks last
+    if (b == 0x80000000u) b = 0u;           // -0 ties +0
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ uint32_t local_of(uint64_t c) { return 0xFFFFFFFFu - (uint32_t)(c & 0xFFFFFFFFull); }
+
+// FROM_SCORES: round 0 reads fp32 scores (candidate = position); later rounds read composites.
+// emit: this is the last round and its (single) workgroup writes io_score / io_index directly.
+template <bool FROM_SCORES>
+__global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__restrict__ score, const uint64_t *__restrict__ cin,
+                                                             int64_t count, int kk, uint64_t *__restrict__ cout, int emit,
+                                                             int n, int64_t index_base, float *__restrict__ out_score,
+                                                             int64_t *__restrict__ out_index) {
+    __shared__ uint32_t whist[kSelThreads / 64][256];  // per-wave histograms: fewer same-address atomics
+    __shared__ uint32_t hist[256];
+    __shared__ uint64_t sel[HARL_TOPK_MAX_K];
+    __shared__ uint32_t s_digit, s_above, s_eq, s_cnt;
+    const int t = threadIdx.x, w = t / 64;
+    const int64_t base = (int64_t)blockIdx.x * kSeg;
+    const int64_t rem = count - base;
+    const int n_valid = rem < kSeg ? (int)rem : kSeg;
+
+    uint64_t x[kPerThread];
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+        const int64_t i = base + (int64_t)j * kSelThreads + t;
+        x[j] = 0;  // padding ranks below every candidate and never enters a histogram
+        if (i < count) {
+            if constexpr (FROM_SCORES)
+                x[j] = ((uint64_t)order_key(score[i]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+            else
+                x[j] = cin[i];
+        }
+    }
+    auto valid = [&](int j) { return j * kSelThreads + t < n_valid; };
+
+    // ---- radix select: find the prefix of the kk-th largest composite ----
+    uint64_t prefix = 0;
+    int shift = 64;
+    uint32_t kr = (uint32_t)kk;  // ranks still needed among candidates matching `prefix`
+    bool done = n_valid <= kk;   // a short segment keeps every candidate
+    while (shift > 0 && !done) {
+        shift -= 8;
+        for (int i = t; i < (kSelThreads / 64) * 256; i += kSelThreads) (&whist[0][0])[i] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kPerThread; ++j) {
+            const bool alive = valid(j) && (shift == 56 || ((x[j] ^ prefix) >> (shift + 8)) == 0);
+            if (alive) atomicAdd(&whist[w][(uint32_t)(x[j] >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (t < 256) {
+            uint32_t c = 0;
+#pragma unroll
+            for (int v = 0; v < kSelThreads / 64; ++v) c += whist[v][t];
+            hist[t] = c;
+        }
+        __syncthreads();
+        if (t < 64) {
+            const uint32_t h0 = hist[255 - 4 * t], h1 = hist[254 - 4 * t], h2 = hist[253 - 4 * t], h3 = hist[252 - 4 * t];
+            const uint32_t s = h0 + h1 + h2 + h3;
+            uint32_t incl = s;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t v = __shfl_up(incl, o, 64);
+                if (t >= o) incl += v;
+            }
+            const uint32_t excl = incl - s;
+            if (excl < kr && incl >= kr) {
+                uint32_t above = excl;
+                int d;
+                if (above + h0 >= kr) d = 255 - 4 * t;
+                else if (above += h0, above + h1 >= kr) d = 254 - 4 * t;
+                else if (above += h1, above + h2 >= kr) d = 253 - 4 * t;
+                else { above += h2; d = 252 - 4 * t; }
+                s_digit = (uint32_t)d;
+                s_above = above;
+                s_eq = hist[d];
+            }
+        }
+        __syncthreads();
+        const uint32_t d = s_digit;
+        kr -= s_above;
+        prefix |= (uint64_t)d << shift;
+        done = s_eq == kr;
+    }
+
+    // ---- compaction: everything strictly above the prefix, then kr of those equal to it ----
+    if (t == 0) s_cnt = 0;
+    __syncthreads();
+    if (n_valid <= kk) {
+#pragma unroll
+        for (int j = 0; j < kPerThread; ++j)
+            if (valid(j)) sel[atomicAdd(&s_cnt, 1u)] = x[j];
+        __syncthreads();
+        for (int i = n_valid + t; i < kk; i += kSelThreads) sel[i] = 0;
+    } else {
+        const uint64_t ptop = prefix >> shift;
+#pragma unroll
+        for (int j = 0; j < kPerThread; ++j)
+            if (valid(j) && (x[j] >> shift) > ptop) sel[atomicAdd(&s_cnt, 1u)] = x[j];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kPerThread; ++j)
+            if (valid(j) && (x[j] >> shift) == ptop) {
+                const uint32_t pos = atomicAdd(&s_cnt, 1u);
+                if (pos < (uint32_t)kk) sel[pos] = x[j];
+            }
+    }
+    int P = 1;
+    while (P < kk) P <<= 1;
+    for (int i = kk + t; i < P; i += kSelThreads) sel[i] = 0;
+    __syncthreads();
+
+    // ---- bitonic sort of the kk selected composites, descending ----
+    for (int size = 2; size <= P; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = t; i < P / 2; i += kSelThreads) {
+                const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+                const bool desc = (lo & size) == 0;
+                const uint64_t a = sel[lo], b = sel[hi];
+                if (desc ? (a < b) : (a > b)) {
+                    sel[lo] = b;
+                    sel[hi] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int i = t; i < kk; i += kSelThreads) {
+        if (emit) {
+            uint32_t l = local_of(sel[i]);
+            l = l < (uint32_t)n ? l : (uint32_t)(n - 1);
+            out_score[i] = score[l];
+            out_index[i] = index_base + (int64_t)l;
+        } else {
+            cout[(int64_t)blockIdx.x * kk + i] = sel[i];
+        }
+    }
+}
+
+// a ranks ahead of b
+__device__ __forceinline__ bool ahead(uint32_t ka, int64_t ia, uint32_t kb, int64_t ib) {
+    return ka > kb || (ka == kb && ia < ib);
+}
+
+// running (k sorted entries in io_*) <- top-k of running U batch (nb sorted composites of this call).
+__global__ __launch_bounds__(kMergeThreads) void k_topk_merge(const uint64_t *__restrict__ bkeys, int nb,
+                                                              const float *__restrict__ score, int n, int64_t index_base,
+                                                              float *__restrict__ io_score, int64_t *__restrict__ io_index,
+                                                              int k) {
+    __shared__ uint32_t ak[HARL_TOPK_MAX_K], bk[HARL_TOPK_MAX_K];
+    __shared__ int64_t ai[HARL_TOPK_MAX_K], bi[HARL_TOPK_MAX_K];
+    __shared__ float as[HARL_TOPK_MAX_K], bs[HARL_TOPK_MAX_K];
+    for (int i = threadIdx.x; i < k; i += kMergeThreads) {
+        as[i] = io_score[i];
+        ak[i] = order_key(as[i]);
+        ai[i] = io_index[i];
+    }
+    for (int j = threadIdx.x; j < nb; j += kMergeThreads) {
+        uint32_t l = local_of(bkeys[j]);
+        l = l < (uint32_t)n ? l : (uint32_t)(n - 1);
+        bs[j] = score[l];
+        bk[j] = (uint32_t)(bkeys[j] >> 32);
+        bi[j] = index_base + (int64_t)l;
+    }
+    __syncthreads();
+    // output slot of running entry i: i + #(batch entries strictly ahead of it)
+    for (int i = threadIdx.x; i < k; i += kMergeThreads) {
+        int lo = 0, hi = nb;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (ahead(bk[mid], bi[mid], ak[i], ai[i])) lo = mid + 1;
+            else hi = mid;
+        }
+        const int pos = i + lo;
+        if (pos < k) {
+            io_score[pos] = as[i];
+            io_index[pos] = ai[i];
+        }
+    }
+    // output slot of batch entry j: j + #(running entries ahead of it or equal to it)
+    for (int j = threadIdx.x; j < nb; j += kMergeThreads) {
+        int lo = 0, hi = k;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (!ahead(bk[j], bi[j], ak[mid], ai[mid])) lo = mid + 1;
+            else hi = mid;
+        }
+        const int pos = j + lo;
+        if (pos < k) {
+            io_score[pos] = bs[j];
+            io_index[pos] = bi[j];
+        }
+    }
+}
+
+__global__ void k_topk_reset(float *__restrict__ s, int64_t *__restrict__ idx, int k) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < k) {
+        s[i] = -INFINITY;
+        idx[i] = INT64_MAX;
+    }
+}
+
+struct Plan {
+    int rounds;
+    int64_t counts[40];  // candidates entering each round
+    size_t buf_keys;     // composites per ping-pong buffer
+};
+
+Plan make_plan(int32_t n, int32_t k) {
+    Plan p{};
+    int64_t c = n;
+    size_t mx = 0;
+    do {
+        p.counts[p.rounds++] = c;
+        const int64_t segs = ceil_div(c, kSeg);
+        c = segs * k;
+        if ((size_t)c > mx) mx = (size_t)c;
+        if (segs == 1) break;
+    } while (p.rounds < 40);
+    p.buf_keys = mx;
+    return p;
+}
+
+}  // namespace
+
+size_t topk_ws_bytes(int32_t n, int32_t k) {
+    if (n <= 0 || k <= 0) return 256;
+    const Plan p = make_plan(n, k);
+    return 2 * round_up((int64_t)p.buf_keys * 8, 256) + 256;
+}
+
+int topk_launch(const float *score, int32_t n, int32_t k, int64_t index_base, float *io_score, int64_t *io_index,
+                uint32_t flags, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (k == 0 || (n == 0 && (flags & HARL_TOPK_MERGE))) return HARL_OK;
+    const Plan p = make_plan(n, k);
+    const size_t buf_bytes = round_up((int64_t)p.buf_keys * 8, 256);
+    if (ws_bytes < 2 * buf_bytes) return fail(HARL_E_WORKSPACE, "harl_topk: workspace too small");
+    uint64_t *buf[2] = {static_cast<uint64_t *>(ws), reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + buf_bytes)};
+    const bool merge = flags & HARL_TOPK_MERGE;
+    const uint64_t *src = nullptr;
+    for (int r = 0; r < p.rounds; ++r) {
+        const int64_t c = p.counts[r];
+        const unsigned segs = (unsigned)ceil_div(c, kSeg);
+        const int emit = (r == p.rounds - 1 && !merge) ? 1 : 0;
+        uint64_t *dst = buf[r & 1];
+        if (r == 0)
+            hipLaunchKernelGGL(k_topk_select<true>, dim3(segs), dim3(kSelThreads), 0, stream, score, nullptr, c, k, dst,
+                               emit, n, index_base, io_score, io_index);
+        else
+            hipLaunchKernelGGL(k_topk_select<false>, dim3(segs), dim3(kSelThreads), 0, stream, score, src, c, k, dst,
+                               emit, n, index_base, io_score, io_index);
+        HARL_HIP_CHECK(hipGetLastError());
+        src = dst;
+    }
+    if (merge) {
+        const int nb = k < n ? k : n;  // real candidates at the head of the final sorted list
+        hipLaunchKernelGGL(k_topk_merge, dim3(1), dim3(kMergeThreads), 0, stream, src, nb, score, n, index_base, io_score,
+                           io_index, k);
+        HARL_HIP_CHECK(hipGetLastError());
+    }
+    return HARL_OK;
+}
+
+int topk_reset_launch(float *io_score, int64_t *io_index, int32_t k, hipStream_t stream) {
+    if (k == 0) return HARL_OK;
+    hipLaunchKernelGGL(k_topk_reset, dim3((unsigned)ceil_div(k, 256)), dim3(256), 0, stream, io_score, io_index, k);
+    HARL_HIP_CHECK(hipGetLastError());
+    return HARL_OK;
+}
+
+}  // namespace harl

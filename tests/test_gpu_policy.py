@@ -1,0 +1,75 @@
+"""GPU parity of harl_policy_step (actor pi_theta(M|S) and critic V(S), Algorithm 1, Eq. 6)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import gen_policy, gen_states, get_config, mini_config
+from tests.gpu_util import assert_close_scaled, gpu_policy, log, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(cfg, B=None):
+    require_gpu()
+    pol = gen_policy(cfg)
+    st = gen_states(cfg, n=B)
+    log("policy parity: %s dtype=%s %d-%d-%d->%d B=%d exact=%s" % (
+        cfg.name, cfg.pol_dtype, cfg.pol_s, cfg.pol_h1, cfg.pol_h2, cfg.pol_a, st.shape[0], cfg.exact))
+    want = oracle.policy_step(pol, st)
+    got = gpu_policy(pol, st)
+    lg = got["logits"]
+    # the GPU action is the lowest-index argmax of the GPU's own logits, bit-exactly
+    np.testing.assert_array_equal(got["action"], np.argmax(lg, axis=1))
+    if cfg.exact:
+        np.testing.assert_array_equal(lg, want["logits"].astype(np.float32))
+        np.testing.assert_array_equal(got["value"], want["value"].astype(np.float32))
+        np.testing.assert_array_equal(got["action"], want["action"])
+        return got, want
+    rtol = 2e-2 if cfg.pol_dtype == "bf16" else 1e-5
+    assert_close_scaled(lg, want["logits"], want["logit_scale"], rtol, "logits")
+    assert_close_scaled(got["value"], want["value"], want["value_scale"], rtol, "value")
+    ptol = 2e-2 if cfg.pol_dtype == "bf16" else 1e-5
+    assert np.abs(got["probs"] - want["probs"]).max() <= ptol
+    # end-to-end argmax: may differ only where the oracle's top two lie within the tolerance band
+    diff = np.nonzero(got["action"] != want["action"])[0]
+    for i in diff:
+        a, b = got["action"][i], want["action"][i]
+        band = rtol * (want["logit_scale"][i, a] + want["logit_scale"][i, b])
+        assert want["logits"][i, b] - want["logits"][i, a] <= band, "argmax flip beyond the near-tie band"
+    log("  argmax near-tie flips: %d of %d" % (diff.size, st.shape[0]))
+    return got, want
+
+
+def test_tiny_fp32():
+    _check(get_config("tiny"))
+
+
+def test_tiny_fp32_exact():
+    _check(get_config("tiny", exact=True))
+
+
+def test_policy_heavy_bf16_exact_small_batch():
+    _check(get_config("policy_heavy", exact=True), B=200)
+
+
+def test_policy_heavy_bf16_small_batch():
+    _check(get_config("policy_heavy"), B=333)
+
+
+def test_bf16_large_batch_path():
+    # at >= 16384 states the kernel shares weight fragments among 4 state groups
+    _check(get_config("policy_heavy", exact=True), B=16384 + 37)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_odd_sizes(dtype):
+    cfg = mini_config(pol_dtype=dtype, pol_s=19, pol_h1=50, pol_h2=70, pol_a=13, n_prog=45)
+    _check(cfg)
+    _check(cfg.with_(exact=True))
+
+
+def test_single_action_and_wide_head():
+    _check(mini_config(pol_a=1, n_prog=20))
+    _check(mini_config(pol_a=100, pol_h2=64, n_prog=40))
