@@ -1,7 +1,8 @@
 """Benchmark one HARL search round on one MI355X: policy forward + cost-model scoring + top-K.
 
 A step is one whole round over one batch of synthetic candidates, inputs already resident in
-HBM: harl_policy_step (second stream, concurrent with scoring), harl_score_round and harl_topk.
+HBM: harl_policy_step, harl_score_round and harl_topk, in that order on one stream (the scoring
+kernel keeps every CU busy, so a concurrent policy stream only contends for them).
 Prints ONE JSON line (rank 0).  Default workload: the standard round (4,096 candidates with
 U{1..32} statements of 164 features, 300 trees of depth 8, fp32 MLP 64-256-256 -> 24+1, top-128).
 
@@ -38,7 +39,10 @@ def parse():
     ap.add_argument("--config", default="standard")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--one-stream", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="launch every call from the host instead of "
+                    "replaying a captured graph of the round")
+    ap.add_argument("--two-streams", action="store_true",
+                    help="run the policy on a second stream concurrently with scoring")
     return ap.parse_args()
 
 
@@ -90,35 +94,61 @@ def main():
     cfg = get_config(args.config)
     ens, pol, b = gen_ensemble(cfg), gen_policy(cfg), gen_batch(cfg)
     dev = torch.device("cuda:0")
-    rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=not args.one_stream)
+    rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=args.two_streams)
     batch = upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)
     main_stream = torch.cuda.current_stream(dev)
 
-    for _ in range(args.warmup):
-        rnd.step(batch)
+    # warm up eagerly (first calls also set kernel attributes), on a side stream as graph capture
+    # requires, then capture one round as a HIP graph: replaying it issues the round's kernels
+    # back to back without a host round trip per launch
+    cap = torch.cuda.Stream(device=dev)
+    cap.wait_stream(main_stream)
+    with torch.cuda.stream(cap):
+        for _ in range(max(args.warmup, 1)):
+            rnd.step(batch)
+    main_stream.wait_stream(cap)
     torch.cuda.synchronize()
+    eager_scores = rnd.prog_score.clone()
+    eager_top = rnd.top_index.clone()
+    graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            rnd.step(batch)
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
 
-    # timed region: K whole rounds; events around the scoring call (the dominant kernel, on the
-    # stream it is launched on) and around the policy call (on its stream)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    side = rnd.side if rnd.side is not None else main_stream
+    # timed region: K whole rounds
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        side.wait_stream(main_stream)
-        pev[i][0].record(side)
-        rnd.policy(batch, stream=side)
-        pev[i][1].record(side)
-        ev[i][0].record(main_stream)
-        rnd.score(batch, stream=main_stream)
-        ev[i][1].record(main_stream)
-        rnd.topk(batch, stream=main_stream)
-        main_stream.wait_stream(side)
+    for _ in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            rnd.step(batch)
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
-    score_ms = sum(a.elapsed_time(z) for a, z in ev) / args.steps
-    pol_ms = sum(a.elapsed_time(z) for a, z in pev) / args.steps
+    same = bool(torch.equal(rnd.prog_score, eager_scores) and torch.equal(rnd.top_index, eager_top))
+
+    # per-launch time of the dominant kernel (harl_score_round), the policy and top-K: K calls of
+    # one of them captured as a graph, replayed between two HIP events on the stream it runs on
+    def timed(fn):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(args.steps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main_stream)
+        g.replay()
+        e1.record(main_stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+    score_ms = timed(lambda: rnd.score(batch))
+    pol_ms = timed(lambda: rnd.policy(batch))
+    topk_ms = timed(lambda: rnd.topk(batch))
 
     n_rows, n_prog = b["n_rows"], cfg.n_prog
     visits = n_rows * cfg.n_trees * cfg.depth
@@ -150,6 +180,8 @@ def main():
                      "traffic": None, "us_per_launch": score_ms * 1e3,
                      "hbm_gbs": hbm_bytes / (score_ms * 1e-3) / 1e9,
                      "hbm_frac": hbm_bytes / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+        "graph_replay": graph is not None, "graph_matches_eager": same,
+        "topk_us_per_launch": topk_ms * 1e3,
         "policy": {"kernel": "k_policy via harl_policy_step", "us_per_launch": pol_ms * 1e3, "achieved": pol_tflops,
                    "peak": PEAK_MFMA_TFLOPS[cfg.pol_dtype], "unit": "TFLOP/s",
                    "frac": pol_tflops / PEAK_MFMA_TFLOPS[cfg.pol_dtype]},

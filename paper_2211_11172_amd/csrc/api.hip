@@ -2,6 +2,8 @@
 // call, so a rejected call launches nothing and touches no output.
 #include <hip/hip_runtime.h>
 
+#include <map>
+#include <mutex>
 #include <string>
 
 #include "internal.hpp"
@@ -18,6 +20,19 @@ int fail(int status, const std::string &msg) {
 int hip_fail(hipError_t e, const char *what) {
     g_last_error = std::string(what) + ": " + hipGetErrorString(e);
     return HARL_E_HIP;
+}
+
+int ensure_dynamic_lds(const void *kernel, size_t bytes) {
+    static std::mutex mu;
+    static std::map<std::pair<const void *, int>, size_t> done;
+    int dev = 0;
+    HARL_HIP_CHECK(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lock(mu);
+    size_t &have = done[{kernel, dev}];
+    if (have >= bytes) return HARL_OK;
+    HARL_HIP_CHECK(hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes));
+    have = bytes;
+    return HARL_OK;
 }
 
 }  // namespace harl

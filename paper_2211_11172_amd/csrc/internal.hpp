@@ -21,6 +21,10 @@ int hip_fail(hipError_t e, const char *what);
         if (_e != hipSuccess) return ::harl::hip_fail(_e, #expr); \
     } while (0)
 
+// Raise a kernel's dynamic-LDS limit to at least `bytes` on the current device; the attribute is
+// set once per (kernel, device) and remembered, so hot-path launches make no extra runtime call.
+int ensure_dynamic_lds(const void *kernel, size_t bytes);
+
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }

@@ -6,9 +6,10 @@
 // K4 k_policy: the three dense contractions run on MFMA, transposed so that states are the MFMA
 // N dimension (H^T = W X^T).  A workgroup holds 16*NSG states and 4 waves.
 //   phase 0  the states are staged into LDS ([state][unit], padded rows);
-//   phase 1  each wave computes a quarter of h1's 16-unit tiles for all states (A = W1 fragments
-//            streamed from global memory through an 8-deep register ring, B = states from LDS),
-//            applies bias + ReLU (+ bf16 rounding) and stores the tile to LDS;
+//   phase 1  each wave computes a quarter of h1's 16-unit tiles for all states, two tiles at a
+//            time (A = W1 fragments streamed from global memory through a register ring, B =
+//            states from LDS, read one k-group ahead), applies bias + ReLU (+ bf16 rounding) and
+//            stores the tiles to LDS;
 //   phase 2  each wave computes a quarter of h2's tiles the same way (B = h1 from LDS; every A
 //            fragment feeds NSG state groups) and feeds each finished tile straight from its
 //            accumulator registers into the head contraction: the MFMA result layout of a tile is
@@ -39,8 +40,8 @@ namespace harl {
 namespace {
 
 constexpr int kU = 4;     // waves per workgroup
-constexpr int kRing = 8;  // weight fragments in flight per wave
-constexpr int kMaxHT = 8; // head tiles: a + 1 <= 128
+constexpr int kRing = 4;  // weight fragment pairs in flight per wave
+constexpr int kMaxHT = 8; // head tiles: a + 1 <= 128 (kernels are instantiated for at most 2 or 8)
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -81,46 +82,77 @@ struct PolicyArgs {
 };
 
 // One dense layer for this wave: `n_tiles` output tiles of 16 units starting at tile `t0`, each a
-// sum over KG k-groups; A fragments come from `A` (packed [tile][g][lane] x 16 B) through a ring
-// of kRing registers, B from the LDS activation rows `in` (row stride `in_stride` bytes).
-// done(tile_index, acc[NSG]) consumes each finished tile.
+// sum over KG k-groups, computed two tiles at a time (two independent accumulator chains sharing
+// every B fragment).  A fragments come from `A` (packed [tile][g][lane] x 16 B) through a ring of
+// kRing register pairs; the B fragments of the next k-group are read from the LDS activation rows
+// `in` (row stride `in_stride` bytes) while the current k-group's MFMAs run.
+// done(first_tile, acc[2][NSG]) consumes each finished pair of tiles.
 template <bool BF16, int NSG, typename Done>
 __device__ __forceinline__ void dense_layer(const uint4 *__restrict__ A, int t0, int n_tiles, int KG, const char *in,
                                             int in_stride, int ln, int lq, int l, Done done) {
-    const int NIT = n_tiles * KG;
-    const uint4 *Ap = A + (int64_t)t0 * KG * 64 + l;
-    uint4 ring[kRing];
+    const int NIT = (n_tiles / 2) * KG;
+    const int64_t tstride = (int64_t)KG * 64;  // uint4 between the same k-group of consecutive tiles
+    auto a_ptr = [&](int it) { return A + (int64_t)(t0 + 2 * (it / KG)) * tstride + (int64_t)(it % KG) * 64 + l; };
+    uint4 ring[kRing][2];
 #pragma unroll
-    for (int r = 0; r < kRing; ++r) ring[r] = r < NIT ? Ap[(int64_t)r * 64] : make_uint4(0, 0, 0, 0);
-    f32x4 acc[NSG];
+    for (int r = 0; r < kRing; ++r) {
+        if (r < NIT) {
+            const uint4 *ap = a_ptr(r);
+            ring[r][0] = ap[0];
+            ring[r][1] = ap[tstride];
+        } else {
+            ring[r][0] = ring[r][1] = make_uint4(0, 0, 0, 0);
+        }
+    }
+    auto b_load = [&](int g, uint4 (&b)[NSG]) {
 #pragma unroll
-    for (int sg = 0; sg < NSG; ++sg) acc[sg] = f32x4{0, 0, 0, 0};
+        for (int sg = 0; sg < NSG; ++sg)
+            b[sg] = *reinterpret_cast<const uint4 *>(in + (sg * 16 + ln) * in_stride + g * 64 + lq * 16);
+    };
+    f32x4 acc[2][NSG];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int sg = 0; sg < NSG; ++sg) acc[h][sg] = f32x4{0, 0, 0, 0};
+    uint4 bcur[NSG];
+    b_load(0, bcur);
     int g = 0, tile = t0;
     for (int it0 = 0; it0 < NIT; it0 += kRing) {
 #pragma unroll
         for (int r = 0; r < kRing; ++r) {
             const int it = it0 + r;
             if (it < NIT) {
-                const uint4 a = ring[r];
-                if (it + kRing < NIT) ring[r] = Ap[(int64_t)(it + kRing) * 64];
+                const uint4 a0 = ring[r][0], a1 = ring[r][1];
+                if (it + kRing < NIT) {
+                    const uint4 *ap = a_ptr(it + kRing);
+                    ring[r][0] = ap[0];
+                    ring[r][1] = ap[tstride];
+                }
+                uint4 bnext[NSG];
+                const int gn = g + 1 == KG ? 0 : g + 1;
+                if (it + 1 < NIT) b_load(gn, bnext);
 #pragma unroll
                 for (int sg = 0; sg < NSG; ++sg) {
-                    const uint4 b = *reinterpret_cast<const uint4 *>(in + (sg * 16 + ln) * in_stride + g * 64 + lq * 16);
-                    mfma_group<BF16>(a, b, acc[sg]);
+                    mfma_group<BF16>(a0, bcur[sg], acc[0][sg]);
+                    mfma_group<BF16>(a1, bcur[sg], acc[1][sg]);
                 }
+#pragma unroll
+                for (int sg = 0; sg < NSG; ++sg) bcur[sg] = bnext[sg];
                 if (++g == KG) {
                     done(tile, acc);
 #pragma unroll
-                    for (int sg = 0; sg < NSG; ++sg) acc[sg] = f32x4{0, 0, 0, 0};
+                    for (int h = 0; h < 2; ++h)
+#pragma unroll
+                        for (int sg = 0; sg < NSG; ++sg) acc[h][sg] = f32x4{0, 0, 0, 0};
                     g = 0;
-                    ++tile;
+                    tile += 2;
                 }
             }
         }
     }
 }
 
-template <bool BF16, int NSG>
+template <bool BF16, int NSG, int HTM>
 __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
     extern __shared__ __align__(16) char smem[];
     constexpr int EL = BF16 ? 2 : 4;        // bytes per activation element
@@ -158,88 +190,87 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
     {
         const int mt_per = p.h1p / 16 / kU;
         dense_layer<BF16, NSG>(p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
-                               [&](int mt, f32x4 *acc) {
-                                   const int u0 = mt * 16 + lq * 4;
+                               [&](int mt0, f32x4 (&acc)[2][NSG]) {
 #pragma unroll
-                                   for (int sg = 0; sg < NSG; ++sg) {
-                                       float h[4];
+                                   for (int h = 0; h < 2; ++h) {
+                                       const int u0 = (mt0 + h) * 16 + lq * 4;
 #pragma unroll
-                                       for (int i = 0; i < 4; ++i) h[i] = fmaxf(acc[sg][i] + p.b1[u0 + i], 0.f);
-                                       char *dst = h1 + (sg * 16 + ln) * h1_stride + u0 * EL;
-                                       if constexpr (BF16) {
-                                           uint2 v = make_uint2(bf16_rne(h[0]) | (bf16_rne(h[1]) << 16),
-                                                                bf16_rne(h[2]) | (bf16_rne(h[3]) << 16));
-                                           *reinterpret_cast<uint2 *>(dst) = v;
-                                       } else {
-                                           *reinterpret_cast<float4 *>(dst) = make_float4(h[0], h[1], h[2], h[3]);
+                                       for (int sg = 0; sg < NSG; ++sg) {
+                                           float v[4];
+#pragma unroll
+                                           for (int i = 0; i < 4; ++i) v[i] = fmaxf(acc[h][sg][i] + p.b1[u0 + i], 0.f);
+                                           char *dst = h1 + (sg * 16 + ln) * h1_stride + u0 * EL;
+                                           if constexpr (BF16) {
+                                               *reinterpret_cast<uint2 *>(dst) = make_uint2(bf16_rne(v[0]) | (bf16_rne(v[1]) << 16),
+                                                                                           bf16_rne(v[2]) | (bf16_rne(v[3]) << 16));
+                                           } else {
+                                               *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+                                           }
                                        }
                                    }
                                });
     }
     __syncthreads();
 
-    // ------- phase 2: h2 tiles of this wave, chained into the partial heads (registers) -------
-    f32x4 hacc[NSG][kMaxHT];
+    // ------- phase 2: h2 tile pairs of this wave, chained into the partial heads (registers) -------
+    f32x4 hacc[NSG][HTM];
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
-        for (int ht = 0; ht < kMaxHT; ++ht) hacc[sg][ht] = f32x4{0, 0, 0, 0};
+        for (int ht = 0; ht < HTM; ++ht) hacc[sg][ht] = f32x4{0, 0, 0, 0};
     {
         const int mt_per = p.h2p / 16 / kU;
         const int mt_first = wid * mt_per;
-        // head fragments: fp32 one k-group per h2 tile, bf16 one per pair of h2 tiles
+        // head fragments: fp32 one k-group per h2 tile (2 per pair), bf16 one per pair of tiles
         const int HKG = BF16 ? p.h2p / 32 : p.h2p / 16;
-        uint4 hpf[kMaxHT];
-        auto head_fetch = [&](int hk) {
+        constexpr int HPP = BF16 ? 1 : 2;  // head k-groups per tile pair
+        uint4 hpf[HPP][HTM];
+        auto head_fetch = [&](int pair) {
 #pragma unroll
-            for (int ht = 0; ht < kMaxHT; ++ht)
-                if (ht < HT && hk < HKG) hpf[ht] = p.wh[((int64_t)ht * HKG + hk) * 64 + l];
+            for (int q = 0; q < HPP; ++q)
+#pragma unroll
+                for (int ht = 0; ht < HTM; ++ht) {
+                    const int hk = pair * HPP + q;
+                    if (ht < HT && hk < HKG) hpf[q][ht] = p.wh[((int64_t)ht * HKG + hk) * 64 + l];
+                }
         };
-        head_fetch(BF16 ? mt_first / 2 : mt_first);
-        uint32_t stash[NSG][2];  // bf16: the even tile of a pair, 4 packed bf16
+        head_fetch(mt_first / 2);
         dense_layer<BF16, NSG>(p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l,
-                               [&](int mt, f32x4 *acc) {
-                                   const int u0 = mt * 16 + lq * 4;
-                                   float bias[4];
+                               [&](int mt0, f32x4 (&acc)[2][NSG]) {
+                                   float bias[2][4];
 #pragma unroll
-                                   for (int i = 0; i < 4; ++i) bias[i] = p.b2[u0 + i];
-                                   if constexpr (BF16) {
-                                       if ((mt & 1) == 0) {
+                                   for (int h = 0; h < 2; ++h)
 #pragma unroll
-                                           for (int sg = 0; sg < NSG; ++sg) {
-                                               stash[sg][0] = bf16_rne(fmaxf(acc[sg][0] + bias[0], 0.f)) |
-                                                              (bf16_rne(fmaxf(acc[sg][1] + bias[1], 0.f)) << 16);
-                                               stash[sg][1] = bf16_rne(fmaxf(acc[sg][2] + bias[2], 0.f)) |
-                                                              (bf16_rne(fmaxf(acc[sg][3] + bias[3], 0.f)) << 16);
+                                       for (int i = 0; i < 4; ++i) bias[h][i] = p.b2[(mt0 + h) * 16 + lq * 4 + i];
+#pragma unroll
+                                   for (int sg = 0; sg < NSG; ++sg) {
+                                       float v[2][4];
+#pragma unroll
+                                       for (int h = 0; h < 2; ++h)
+#pragma unroll
+                                           for (int i = 0; i < 4; ++i) v[h][i] = fmaxf(acc[h][sg][i] + bias[h][i], 0.f);
+                                       if constexpr (BF16) {
+                                           // slots 0..3: tile mt0, slots 4..7: tile mt0 + 1 (accumulator layout)
+                                           uint4 bv;
+                                           bv.x = bf16_rne(v[0][0]) | (bf16_rne(v[0][1]) << 16);
+                                           bv.y = bf16_rne(v[0][2]) | (bf16_rne(v[0][3]) << 16);
+                                           bv.z = bf16_rne(v[1][0]) | (bf16_rne(v[1][1]) << 16);
+                                           bv.w = bf16_rne(v[1][2]) | (bf16_rne(v[1][3]) << 16);
+#pragma unroll
+                                           for (int ht = 0; ht < HTM; ++ht)
+                                               if (ht < HT) mfma_group<true>(hpf[0][ht], bv, hacc[sg][ht]);
+                                       } else {
+#pragma unroll
+                                           for (int h = 0; h < 2; ++h) {
+                                               const uint4 bv = make_uint4(__float_as_uint(v[h][0]), __float_as_uint(v[h][1]),
+                                                                           __float_as_uint(v[h][2]), __float_as_uint(v[h][3]));
+#pragma unroll
+                                               for (int ht = 0; ht < HTM; ++ht)
+                                                   if (ht < HT) mfma_group<false>(hpf[h][ht], bv, hacc[sg][ht]);
                                            }
-                                           return;
                                        }
-#pragma unroll
-                                       for (int sg = 0; sg < NSG; ++sg) {
-                                           uint4 bv;
-                                           bv.x = stash[sg][0];
-                                           bv.y = stash[sg][1];
-                                           bv.z = bf16_rne(fmaxf(acc[sg][0] + bias[0], 0.f)) | (bf16_rne(fmaxf(acc[sg][1] + bias[1], 0.f)) << 16);
-                                           bv.w = bf16_rne(fmaxf(acc[sg][2] + bias[2], 0.f)) | (bf16_rne(fmaxf(acc[sg][3] + bias[3], 0.f)) << 16);
-#pragma unroll
-                                           for (int ht = 0; ht < kMaxHT; ++ht)
-                                               if (ht < HT) mfma_group<true>(hpf[ht], bv, hacc[sg][ht]);
-                                       }
-                                       head_fetch(mt / 2 + 1);
-                                   } else {
-#pragma unroll
-                                       for (int sg = 0; sg < NSG; ++sg) {
-                                           uint4 bv;
-                                           bv.x = __float_as_uint(fmaxf(acc[sg][0] + bias[0], 0.f));
-                                           bv.y = __float_as_uint(fmaxf(acc[sg][1] + bias[1], 0.f));
-                                           bv.z = __float_as_uint(fmaxf(acc[sg][2] + bias[2], 0.f));
-                                           bv.w = __float_as_uint(fmaxf(acc[sg][3] + bias[3], 0.f));
-#pragma unroll
-                                           for (int ht = 0; ht < kMaxHT; ++ht)
-                                               if (ht < HT) mfma_group<false>(hpf[ht], bv, hacc[sg][ht]);
-                                       }
-                                       head_fetch(mt + 1);
                                    }
+                                   head_fetch(mt0 / 2 + 1);
                                });
     }
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
@@ -249,7 +280,7 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
-        for (int ht = 0; ht < kMaxHT; ++ht)
+        for (int ht = 0; ht < HTM; ++ht)
             if (ht < HT)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
@@ -260,9 +291,9 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
         float best = -INFINITY;
         int best_i = 0x7FFFFFFF;
         float val = 0.f;
-        float z[kMaxHT][4];  // rows owned by this lane: 16*ht + 4*lq + i
+        float z[HTM][4];  // rows owned by this lane: 16*ht + 4*lq + i
 #pragma unroll
-        for (int ht = 0; ht < kMaxHT; ++ht)
+        for (int ht = 0; ht < HTM; ++ht)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 z[ht][i] = 0.f;
@@ -294,7 +325,7 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
         float sum = 0.f;
         if (p.probs) {
 #pragma unroll
-            for (int ht = 0; ht < kMaxHT; ++ht)
+            for (int ht = 0; ht < HTM; ++ht)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int row = ht * 16 + lq * 4 + i;
@@ -305,7 +336,7 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
         }
         if (st < p.B) {
 #pragma unroll
-            for (int ht = 0; ht < kMaxHT; ++ht)
+            for (int ht = 0; ht < HTM; ++ht)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int row = ht * 16 + lq * 4 + i;
@@ -378,8 +409,8 @@ int pack_policy(const harl_policy_desc *d, harl_policy **out, hipStream_t stream
     const bool bf = d->dtype == HARL_BF16;
     const int UPG = bf ? 32 : 16;
     const int sp = (int)round_up(d->s, UPG);
-    const int h1p = (int)round_up(d->h1, bf ? 32 * kU : 16 * kU);   // whole tiles per wave, whole k-groups
-    const int h2p = (int)round_up(d->h2, bf ? 32 * kU : 16 * kU);   // bf16: tile pairs per wave
+    const int h1p = (int)round_up(d->h1, 32 * kU);   // whole tile pairs per wave, whole k-groups
+    const int h2p = (int)round_up(d->h2, 32 * kU);
     const int hap = (int)round_up(d->a + 1, 16);
     // heads as one matrix [a+1][h2]: rows 0..a-1 actor, row a value
     const size_t esz = bf ? 2 : 4;
@@ -459,13 +490,17 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     if (policy_lds_bytes(P, nsg) > 160 * 1024) nsg = 1;
     const size_t lds = policy_lds_bytes(P, nsg);
     const unsigned grid = (unsigned)ceil_div(B, 16 * nsg);
-    const void *kern;
-    if (bf) kern = nsg == 4 ? reinterpret_cast<const void *>(k_policy<true, 4>) : reinterpret_cast<const void *>(k_policy<true, 1>);
-    else kern = reinterpret_cast<const void *>(k_policy<false, 1>);
-    HARL_HIP_CHECK(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-    if (bf && nsg == 4) hipLaunchKernelGGL((k_policy<true, 4>), dim3(grid), dim3(256), lds, stream, a);
-    else if (bf) hipLaunchKernelGGL((k_policy<true, 1>), dim3(grid), dim3(256), lds, stream, a);
-    else hipLaunchKernelGGL((k_policy<false, 1>), dim3(grid), dim3(256), lds, stream, a);
+    const int htm = P->hap / 16 <= 2 ? 2 : 8;
+    const void *kern = nullptr;
+#define HARL_POL(BF, NSG, HTM) \
+    if (bf == BF && nsg == NSG && htm == HTM) kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM>);
+    HARL_POL(false, 1, 2) HARL_POL(false, 1, 8) HARL_POL(true, 1, 2) HARL_POL(true, 1, 8) HARL_POL(true, 4, 2)
+    HARL_POL(true, 4, 8)
+#undef HARL_POL
+    if (!kern) return fail(HARL_E_UNSUPPORTED, "harl_policy_step: no kernel for this policy shape");
+    if (const int rc = ensure_dynamic_lds(kern, lds)) return rc;
+    void *args[] = {&a};
+    HARL_HIP_CHECK(hipLaunchKernel(kern, dim3(grid), dim3(256), args, lds, stream));
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
 }

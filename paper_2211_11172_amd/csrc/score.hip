@@ -3,16 +3,22 @@
 // program of statements; each statement row has F fp32 features; the program score is the base
 // score plus the sum over its statements of the ensemble's leaf sum.
 //
-// K1 k_tree_score: one workgroup owns a tile of 64*RW statement rows and one group of trees.
-//   The row tile's features are staged once into LDS, feature-major ([F][64*RW] fp32: a lane's
-//   feature gather hits bank = lane for every feature, so it is conflict-free whatever feature a
-//   node asks for).  The group's trees stream through LDS in chunks of TW*ILP packed complete
-//   trees (the next chunk is fetched into registers while the current one is walked).  Wave
-//   (rw, tw) walks ILP trees of each chunk at once for its 64 rows (lane = row); each level issues
-//   the current node's feature read together with the read of both its children (16 bytes) and
-//   picks the child in registers, so a level costs one LDS round trip.  Row sums are accumulated
-//   in fp64 and combined over the TW waves in a fixed order.
-// K2 k_segsum: one thread per program sums its rows' per-group partials in a fixed order (fp64).
+// K1 tree traversal.  A workgroup owns a tile of statement rows and one group of trees.  The
+//   tile's features are staged once into LDS, feature-major ([F][rows] fp32, so a lane's gather
+//   of any feature of its own row hits bank = lane: conflict-free whatever feature a node asks
+//   for).  Lane = row.  Each level of a walk issues the current node's feature read together with
+//   the read of both its children (16 bytes) and picks the child in registers, so a level costs
+//   one LDS round trip; the leaf pair comes with the last level.  Row sums are accumulated in fp64
+//   and combined over the waves in a fixed order.  Two variants:
+//   k_tree_score_wp (depth <= 8): every wave streams its own trees (tree t + k*TW) through a
+//     private two-slot LDS ring -- the next tree is fetched into registers while the current one
+//     is walked -- so waves never wait on each other between the feature staging and the final
+//     reduction.  Each lane walks RPL rows per tree (ILP across rows; the staged tree serves
+//     64*RPL rows).
+//   k_tree_score_ch (deeper trees, whose 2^depth-node trees are too big for per-wave rings): the
+//     workgroup stages chunks of TW*ILP trees shared by all waves, the next chunk fetched into
+//     registers during the walk of the current one.
+// K2 k_segsum: one wave per program sums its rows' partial slots in a fixed order (fp64).
 //
 // Grid mapping is XCD-aware: workgroup b takes tree group b % G and row tile b / G; workgroups
 // are dealt to the 8 XCDs round-robin, so with G in {2,4,8} every XCD's L2 only ever holds its
@@ -33,12 +39,12 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kLdsBytes = 160 * 1024;
 
+constexpr int tree_stride_bytes(int D) { return ((1 << D) * 12 + 15) / 16 * 16; }
+
 // Packed tree (1-based breadth-first): byte 8*i holds internal node i (i = 1 .. 2^D - 1; bytes 0..7
 // are padding), so the two children of node i sit together, 16-byte aligned, at byte 16*i; the
-// 2^D leaves follow at byte 8 * 2^D, and the two leaves below a last-level node i at
-// 8 * 2^D + 8*i - 4 * 2^D.  One level of the walk therefore issues the feature read of the current
-// node and the read of both its children at once, and selects the child in registers: one LDS
-// round trip per level, the leaf pair coming with the last level.
+// 2^D leaves follow at byte 8 * 2^D, the two leaves below a last-level node i at
+// 8 * 2^D + 8*i - 4 * 2^D.
 template <bool NAN_AWARE>
 __device__ __forceinline__ uint32_t go_right(float x, float thr, uint32_t word) {
     uint32_t right = x >= thr ? 1u : 0u;
@@ -46,57 +52,237 @@ __device__ __forceinline__ uint32_t go_right(float x, float thr, uint32_t word) 
     return right;
 }
 
-template <int D, int RW, int TW, int ILP, bool NAN_AWARE>
-__device__ __forceinline__ void walk_chunk(const char *smem, uint32_t chunk_off, uint32_t stride,
-                                           int tw, uint32_t lane_off, double &acc) {
-    constexpr uint32_t RT4 = 64u * RW * 4u;
+// Walk NT_ trees at LDS byte offsets tb[] for R rows of this lane (feature tile row stride RT4
+// bytes per feature; lane_off[r] = byte offset of the lane's r-th row).  Every (tree, row) pair is
+// an independent chain; all chains of a level are issued together.
+template <int D, int NT_, int R, uint32_t RT4, bool NAN_AWARE>
+__device__ __forceinline__ void walk_trees(const char *smem, const uint32_t (&tb)[NT_], const uint32_t (&lane_off)[R],
+                                           double (&acc)[R]) {
     constexpr uint32_t kLeafBase = 8u << D;
-    uint32_t base[ILP], idx[ILP], word[ILP];
-    float thr[ILP];
+    uint32_t idx[NT_][R], word[NT_][R];
+    float thr[NT_][R];
 #pragma unroll
-    for (int i = 0; i < ILP; ++i) {
-        base[i] = chunk_off + (uint32_t)(tw * ILP + i) * stride;
-        const uint2 root = *reinterpret_cast<const uint2 *>(smem + base[i] + 8u);
-        word[i] = root.x;
-        thr[i] = __uint_as_float(root.y);
-        idx[i] = 1;
+    for (int i = 0; i < NT_; ++i) {
+        const uint2 root = *reinterpret_cast<const uint2 *>(smem + tb[i] + 8u);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            word[i][r] = root.x;
+            thr[i][r] = __uint_as_float(root.y);
+            idx[i][r] = 1;
+        }
     }
 #pragma unroll
     for (int lvl = 0; lvl + 1 < D; ++lvl) {
-        float x[ILP];
-        uint4 kids[ILP];
+        float x[NT_][R];
+        uint4 kids[NT_][R];
 #pragma unroll
-        for (int i = 0; i < ILP; ++i) {
-            x[i] = *reinterpret_cast<const float *>(smem + __umul24(word[i], RT4) + lane_off);
-            kids[i] = *reinterpret_cast<const uint4 *>(smem + base[i] + idx[i] * 16u);
+        for (int i = 0; i < NT_; ++i)
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                x[i][r] = *reinterpret_cast<const float *>(smem + __umul24(word[i][r], RT4) + lane_off[r]);
+                kids[i][r] = *reinterpret_cast<const uint4 *>(smem + tb[i] + idx[i][r] * 16u);
+            }
+#pragma unroll
+        for (int i = 0; i < NT_; ++i)
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const uint32_t g = go_right<NAN_AWARE>(x[i][r], thr[i][r], word[i][r]);
+                idx[i][r] = 2u * idx[i][r] + g;
+                word[i][r] = g ? kids[i][r].z : kids[i][r].x;
+                thr[i][r] = __uint_as_float(g ? kids[i][r].w : kids[i][r].y);
+            }
+    }
+    float x[NT_][R];
+    float2 lv[NT_][R];
+#pragma unroll
+    for (int i = 0; i < NT_; ++i)
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            x[i][r] = *reinterpret_cast<const float *>(smem + __umul24(word[i][r], RT4) + lane_off[r]);
+            lv[i][r] = *reinterpret_cast<const float2 *>(smem + tb[i] + kLeafBase + idx[i][r] * 8u - (4u << D));
         }
 #pragma unroll
-        for (int i = 0; i < ILP; ++i) {
-            const uint32_t r = go_right<NAN_AWARE>(x[i], thr[i], word[i]);
-            idx[i] = 2u * idx[i] + r;
-            word[i] = r ? kids[i].z : kids[i].x;
-            thr[i] = __uint_as_float(r ? kids[i].w : kids[i].y);
-        }
-    }
-    float x[ILP];
-    float2 lv[ILP];
+    for (int i = 0; i < NT_; ++i)
 #pragma unroll
-    for (int i = 0; i < ILP; ++i) {
-        x[i] = *reinterpret_cast<const float *>(smem + __umul24(word[i], RT4) + lane_off);
-        lv[i] = *reinterpret_cast<const float2 *>(smem + base[i] + kLeafBase + idx[i] * 8u - (4u << D));
-    }
-#pragma unroll
-    for (int i = 0; i < ILP; ++i) acc += (double)(go_right<NAN_AWARE>(x[i], thr[i], word[i]) ? lv[i].y : lv[i].x);
+        for (int r = 0; r < R; ++r)
+            acc[r] += (double)(go_right<NAN_AWARE>(x[i][r], thr[i][r], word[i][r]) ? lv[i][r].y : lv[i][r].x);
 }
 
-constexpr int tree_stride_bytes(int D) { return ((1 << D) * 12 + 15) / 16 * 16; }
+// Stage rows [row0, row0 + RT) of every feature into LDS ([F][RT] fp32, zero past n_rows), with
+// 8 loads in flight per thread; returns (block-wide) whether any staged value is NaN.
+template <int RT, int NT>
+__device__ __forceinline__ int stage_features(char *smem, const float *__restrict__ X, int64_t ld, int n_rows, int F,
+                                              int vec_ok, int row0) {
+    constexpr int V = RT / 4;  // float4 per feature row of the tile
+    constexpr int B = 8;
+    int has_nan = 0;
+    const int total = F * V;
+    float4 *dst = reinterpret_cast<float4 *>(smem);
+    for (int i0 = threadIdx.x; i0 < total; i0 += B * NT) {
+        float4 v[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const int i = i0 + j * NT;
+            v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (i < total) {
+                const int f = i / V, r = row0 + 4 * (i % V);
+                const float *src = X + (int64_t)f * ld + r;
+                if (vec_ok && r + 3 < n_rows) {
+                    v[j] = *reinterpret_cast<const float4 *>(src);
+                } else {
+                    if (r + 0 < n_rows) v[j].x = src[0];
+                    if (r + 1 < n_rows) v[j].y = src[1];
+                    if (r + 2 < n_rows) v[j].z = src[2];
+                    if (r + 3 < n_rows) v[j].w = src[3];
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            const int i = i0 + j * NT;
+            if (i < total) {
+                has_nan |= (v[j].x != v[j].x) | (v[j].y != v[j].y) | (v[j].z != v[j].z) | (v[j].w != v[j].w);
+                dst[i] = v[j];
+            }
+        }
+    }
+    return __syncthreads_or(has_nan);
+}
 
-template <int D, int RW, int TW, int ILP>
-__global__ __launch_bounds__(64 * RW * TW) void k_tree_score(
+// Fixed-order combination of the per-wave row sums (acc[r] of wave w for tile row r*64 + lane),
+// written as this group's fp32 partials.  `red` must not overlap live data; ends the kernel.
+template <int RPL, int NW>
+__device__ __forceinline__ void reduce_rows(double *red, const double (&acc)[RPL], int wid, int lane, int row0, int n_rows,
+                                            float *__restrict__ partial_g) {
+    constexpr int RT = 64 * RPL;
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) red[wid * RT + r * 64 + lane] = acc[r];
+    __syncthreads();
+    for (int t = threadIdx.x; t < RT; t += NW * kWave) {
+        double s = 0.0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) s += red[w * RT + t];
+        if (row0 + t < n_rows) partial_g[row0 + t] = (float)s;
+    }
+}
+
+// Per-wave tree staging: lane l moves uint4 j*64 + l of a packed tree (S16 uint4 in all).
+template <int S16, int PF>
+__device__ __forceinline__ void wave_fetch(uint4 (&pf)[PF], const uint4 *__restrict__ src, int lane) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j)
+        if (S16 % kWave == 0 || j * kWave + lane < S16) pf[j] = src[j * kWave + lane];
+}
+
+template <int S16, int PF>
+__device__ __forceinline__ void wave_commit(const uint4 (&pf)[PF], uint4 *dst, int lane) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j)
+        if (S16 % kWave == 0 || j * kWave + lane < S16) dst[j * kWave + lane] = pf[j];
+}
+
+// ---- K1, depth <= 8: persistent workgroups with per-wave private tree rings ----
+// The work is the space of (row tile, tree) pairs, tile-major: v = tile * T + tree.  Workgroup b
+// owns the contiguous slice [b*L, (b+1)*L), so every workgroup walks the same number of trees and
+// the machine is busy to the end; a tile whose trees are split between workgroups gets one partial
+// slot per piece (piece = b - first workgroup of the tile), summed later in piece order.
+template <int D, int RPL, int TW>
+__global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
+    const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
+    int T, int64_t V, int64_t L, float *__restrict__ partial, int64_t ldp) {
+    constexpr int RT = 64 * RPL;
+    constexpr int S16 = tree_stride_bytes(D) / 16;  // uint4 per packed tree
+    constexpr int PF = (S16 + kWave - 1) / kWave;   // uint4 per lane per tree
+    extern __shared__ __align__(16) char smem[];
+
+    const int64_t v_begin = (int64_t)blockIdx.x * L;
+    const int64_t v_end = v_begin + L < V ? v_begin + L : V;
+    if (v_begin >= v_end) return;  // whole workgroup: no barrier is skipped by part of it
+    const int wid = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const uint32_t ring_off = (uint32_t)F * RT * 4u;
+    char *const ring = smem + ring_off + (uint32_t)wid * 2u * (S16 * 16);
+
+    uint4 pf[PF];
+#pragma unroll
+    for (int j = 0; j < PF; ++j) pf[j] = make_uint4(0, 0, 0, 0);
+    uint32_t lane_off[RPL];
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) lane_off[r] = (uint32_t)(r * 64 + lane) * 4u;
+
+    int64_t v = v_begin;
+    int tile = (int)(v / T);
+    int t0 = (int)(v % T);
+    int t1 = (int)(T - t0 < v_end - v ? T : t0 + (v_end - v));
+    int t = t0 + wid;
+    if (t < t1) wave_fetch<S16>(pf, trees + (int64_t)t * S16, lane);   // overlaps the feature staging
+    while (true) {
+        const int row0 = tile * RT;
+        const int has_nan = stage_features<RT, 64 * TW>(smem, X, ld, n_rows, F, vec_ok, row0);
+        if (t < t1) wave_commit<S16>(pf, reinterpret_cast<uint4 *>(ring), lane);
+        if (t + TW < t1) wave_fetch<S16>(pf, trees + (int64_t)(t + TW) * S16, lane);
+        double acc[RPL];
+#pragma unroll
+        for (int r = 0; r < RPL; ++r) acc[r] = 0.0;
+        int s = 0;
+        for (; t < t1; t += TW) {
+            const uint32_t tb[1] = {ring_off + (uint32_t)wid * 2u * (S16 * 16) + (uint32_t)s * (S16 * 16)};
+            if (has_nan)
+                walk_trees<D, 1, RPL, (uint32_t)RT * 4u, true>(smem, tb, lane_off, acc);
+            else
+                walk_trees<D, 1, RPL, (uint32_t)RT * 4u, false>(smem, tb, lane_off, acc);
+            if (t + TW < t1) {                 // LDS ops of a wave run in order: the walk's reads of
+                                               // slot s complete before the next commit overwrites it
+                wave_commit<S16>(pf, reinterpret_cast<uint4 *>(ring + (uint32_t)(s ^ 1) * (S16 * 16)), lane);
+                if (t + 2 * TW < t1) wave_fetch<S16>(pf, trees + (int64_t)(t + 2 * TW) * S16, lane);
+            }
+            s ^= 1;
+        }
+        // the next piece (if any) starts at tree 0 of the next tile: prefetch its first tree now
+        v += t1 - t0;
+        const bool next = v < v_end;
+        const int nt1 = next ? (int)(T < v_end - v ? T : v_end - v) : 0;
+        if (next && wid < nt1) wave_fetch<S16>(pf, trees + (int64_t)wid * S16, lane);
+        __syncthreads();  // every wave is done with its ring: reuse the ring region for the reduction
+        const int piece = (int)(blockIdx.x - ((int64_t)tile * T) / L);
+        reduce_rows<RPL, TW>(reinterpret_cast<double *>(smem + ring_off), acc, wid, lane, row0, n_rows,
+                             partial + (int64_t)piece * ldp);
+        if (!next) break;
+        ++tile;
+        t0 = 0;
+        t1 = nt1;
+        t = wid;
+    }
+}
+
+// Workgroup chunk staging: thread t moves uint4 t + j*NT of C consecutive packed trees starting
+// at tree t0; slots past t_end are zero (a zero tree reaches a 0.0 leaf).
+template <int C, int S16, int NT, int NPF>
+__device__ __forceinline__ void block_fetch(uint4 (&pf)[NPF], const uint4 *__restrict__ trees, int t0, int t_end) {
+    const int valid16 = min(C, t_end - t0) * S16;
+    const uint4 *src = trees + (int64_t)t0 * S16;
+#pragma unroll
+    for (int j = 0; j < NPF; ++j) {
+        const int i = threadIdx.x + j * NT;
+        pf[j] = i < valid16 ? src[i] : make_uint4(0, 0, 0, 0);
+    }
+}
+
+template <int C, int S16, int NT, int NPF>
+__device__ __forceinline__ void block_commit(const uint4 (&pf)[NPF], uint4 *dst) {
+#pragma unroll
+    for (int j = 0; j < NPF; ++j) {
+        const int i = threadIdx.x + j * NT;
+        if (i < C * S16) dst[i] = pf[j];
+    }
+}
+
+// ---- K1, deeper trees: chunks of TW*ILP trees shared by the workgroup ----
+template <int D, int TW, int ILP>
+__global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
     const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
     int n_trees, int trees_per_group, int n_groups, float *__restrict__ partial, int64_t ldp) {
-    constexpr int RT = 64 * RW;
-    constexpr int NT = 64 * RW * TW;
+    constexpr int RT = 64;
+    constexpr int NT = 64 * TW;
     constexpr int C = TW * ILP;                       // trees per chunk
     constexpr int S16 = tree_stride_bytes(D) / 16;    // uint4 per packed tree
     constexpr int CH16 = C * S16;                     // uint4 per chunk
@@ -104,265 +290,262 @@ __global__ __launch_bounds__(64 * RW * TW) void k_tree_score(
     extern __shared__ __align__(16) char smem[];
 
     const int g = blockIdx.x % n_groups;
-    const int tile = blockIdx.x / n_groups;
-    const int row0 = tile * RT;
+    const int row0 = (blockIdx.x / n_groups) * RT;
     const int t_begin = g * trees_per_group;
     const int t_end = min(n_trees, t_begin + trees_per_group);
     const uint32_t chunk_off = (uint32_t)F * RT * 4u;
 
-    // The next chunk of trees is fetched into registers while the current one is walked.
     uint4 pf[NPF];
-    auto fetch = [&](int t0) {
-        const int valid16 = min(C, t_end - t0) * S16;
-        const uint4 *src = trees + (int64_t)t0 * S16;
-#pragma unroll
-        for (int j = 0; j < NPF; ++j) {
-            const int i = threadIdx.x + j * NT;
-            pf[j] = i < valid16 ? src[i] : make_uint4(0, 0, 0, 0);   // slots past the group: leaf 0.0
-        }
-    };
-    auto commit = [&]() {
-        uint4 *dst = reinterpret_cast<uint4 *>(smem + chunk_off);
-#pragma unroll
-        for (int j = 0; j < NPF; ++j) {
-            const int i = threadIdx.x + j * NT;
-            if (i < CH16) dst[i] = pf[j];
-        }
-    };
-    if (t_begin < t_end) fetch(t_begin);
-
-    // ---- stage the row tile's features (feature-major), 8 loads in flight per thread ----
-    int has_nan = 0;
-    {
-        constexpr int V = RT / 4;  // float4 per feature row of the tile
-        constexpr int B = 8;
-        const int total = F * V;
-        float4 *dst = reinterpret_cast<float4 *>(smem);
-        for (int i0 = threadIdx.x; i0 < total; i0 += B * NT) {
-            float4 v[B];
-#pragma unroll
-            for (int j = 0; j < B; ++j) {
-                const int i = i0 + j * NT;
-                v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (i < total) {
-                    const int f = i / V, r = row0 + 4 * (i % V);
-                    const float *src = X + (int64_t)f * ld + r;
-                    if (vec_ok && r + 3 < n_rows) {
-                        v[j] = *reinterpret_cast<const float4 *>(src);
-                    } else {
-                        if (r + 0 < n_rows) v[j].x = src[0];
-                        if (r + 1 < n_rows) v[j].y = src[1];
-                        if (r + 2 < n_rows) v[j].z = src[2];
-                        if (r + 3 < n_rows) v[j].w = src[3];
-                    }
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < B; ++j) {
-                const int i = i0 + j * NT;
-                if (i < total) {
-                    has_nan |= (v[j].x != v[j].x) | (v[j].y != v[j].y) | (v[j].z != v[j].z) | (v[j].w != v[j].w);
-                    dst[i] = v[j];
-                }
-            }
-        }
-    }
-    if (t_begin < t_end) commit();
-    has_nan = __syncthreads_or(has_nan);
+    if (t_begin < t_end) block_fetch<C, S16, NT>(pf, trees, t_begin, t_end);
+    const int has_nan = stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, row0);
+    if (t_begin < t_end) block_commit<C, S16, NT>(pf, reinterpret_cast<uint4 *>(smem + chunk_off));
+    __syncthreads();
 
     const int wid = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int rw = wid / TW, tw = wid % TW;
-    const uint32_t lane_off = (uint32_t)(rw * 64 + lane) * 4u;
-    double acc = 0.0;
-
+    const uint32_t lane_off[1] = {(uint32_t)lane * 4u};
+    double acc[1] = {0.0};
     for (int t0 = t_begin; t0 < t_end; t0 += C) {
         const bool more = t0 + C < t_end;
-        if (more) fetch(t0 + C);
+        if (more) block_fetch<C, S16, NT>(pf, trees, t0 + C, t_end);
+        uint32_t tb[ILP];
+#pragma unroll
+        for (int i = 0; i < ILP; ++i) tb[i] = chunk_off + (uint32_t)(wid * ILP + i) * (S16 * 16);
         if (has_nan)
-            walk_chunk<D, RW, TW, ILP, true>(smem, chunk_off, (uint32_t)(S16 * 16), tw, lane_off, acc);
+            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, true>(smem, tb, lane_off, acc);
         else
-            walk_chunk<D, RW, TW, ILP, false>(smem, chunk_off, (uint32_t)(S16 * 16), tw, lane_off, acc);
+            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, false>(smem, tb, lane_off, acc);
         __syncthreads();
         if (more) {
-            commit();
+            block_commit<C, S16, NT>(pf, reinterpret_cast<uint4 *>(smem + chunk_off));
             __syncthreads();
         }
     }
-
-    // ---- combine the TW partial sums of each row in a fixed order ----
-    double *red = reinterpret_cast<double *>(smem + chunk_off);
-    red[tw * RT + rw * 64 + lane] = acc;
-    __syncthreads();
-    if (tw == 0) {
-        double s = 0.0;
-#pragma unroll
-        for (int w = 0; w < TW; ++w) s += red[w * RT + rw * 64 + lane];
-        const int r = row0 + rw * 64 + lane;
-        if (r < n_rows) partial[(int64_t)g * ldp + r] = (float)s;
-    }
+    reduce_rows<1, TW>(reinterpret_cast<double *>(smem + chunk_off), acc, wid, lane, row0, n_rows,
+                       partial + (int64_t)g * ldp);
 }
 
-__global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int n_groups,
-                                                const int32_t *__restrict__ prog_ptr, int n_prog, int n_rows,
-                                                float base_score, float *__restrict__ prog_score,
+// Number of partial slots of row tile `tile`: `groups` in the grouped layout (L == 0), else the
+// number of workgroup slices of length L that the tile's T trees are cut into.
+__device__ __forceinline__ int tile_pieces(int64_t tile, int T, int64_t L, int groups) {
+    if (L == 0) return groups;
+    const int64_t a = tile * T, b = (tile + 1) * T - 1;
+    if (b < ((int64_t)1 << 31) && L < ((int64_t)1 << 31))
+        return (int)((uint32_t)b / (uint32_t)L - (uint32_t)a / (uint32_t)L + 1u);
+    return (int)(b / L - a / L + 1);
+}
+
+// K2: one wave per program (lane = statement row, looping for programs of more than 64 rows):
+// each row sums its partial slots in slot order (fp64), the wave then sums its rows with a
+// fixed xor-butterfly, so the result does not depend on scheduling.
+__global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int rt_shift, int T,
+                                                int64_t L, int groups, const int32_t *__restrict__ prog_ptr, int n_prog,
+                                                int n_rows, float base_score, float *__restrict__ prog_score,
                                                 float *__restrict__ stmt_score) {
-    const int p = blockIdx.x * blockDim.x + threadIdx.x;
-    if (p >= n_prog) return;
+    const int p = blockIdx.x * 4 + threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    if (p >= n_prog) return;  // whole wave
     const int b = min(max(prog_ptr[p], 0), n_rows);
     const int e = min(max(prog_ptr[p + 1], b), n_rows);
-    double acc = (double)base_score;
-    constexpr int B = 8;  // rows loaded per batch, all loads issued before the first add
-    for (int r0 = b; r0 < e; r0 += B) {
-        double s[B];
-#pragma unroll
-        for (int j = 0; j < B; ++j) s[j] = 0.0;
-        for (int gi = 0; gi < n_groups; ++gi) {
-            float v[B];
-#pragma unroll
-            for (int j = 0; j < B; ++j) v[j] = r0 + j < e ? partial[(int64_t)gi * ldp + r0 + j] : 0.f;
-#pragma unroll
-            for (int j = 0; j < B; ++j) s[j] += (double)v[j];
-        }
-#pragma unroll
-        for (int j = 0; j < B; ++j) {
-            if (r0 + j < e) {
-                if (stmt_score) stmt_score[r0 + j] = (float)s[j];
-                acc += s[j];
-            }
-        }
+    double acc = 0.0;
+    for (int r = b + lane; r < e; r += kWave) {
+        const int np = tile_pieces(r >> rt_shift, T, L, groups);
+        double s = (double)partial[r];
+        for (int gi = 1; gi < np; ++gi) s += (double)partial[(int64_t)gi * ldp + r];
+        if (stmt_score) stmt_score[r] = (float)s;
+        acc += s;
     }
-    prog_score[p] = (float)acc;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
+    if (lane == 0) prog_score[p] = (float)((double)base_score + acc);
 }
 
 // ---------------------------------------------------------------------------------------------
 // launch configuration
 // ---------------------------------------------------------------------------------------------
+using ChKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int, int, float *, int64_t);
+using WpKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int64_t, int64_t, float *, int64_t);
+
 struct ScoreCfg {
-    int rw, tw, ilp;
+    bool wp;            // persistent per-wave rings (else grid of shared chunks)
+    int a, b;           // wp: RPL, TW;  ch: TW, ILP
+    const void *kern;
+    int rows_per_tile, threads;
+    size_t lds;
 };
 
-using ScoreKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int, int, float *, int64_t);
-
 template <int D>
-ScoreKernel pick_for_depth(ScoreCfg c) {
-#define HARL_CFG(RW, TW, ILP) \
-    if (c.rw == RW && c.tw == TW && c.ilp == ILP) return k_tree_score<D, RW, TW, ILP>;
-    HARL_CFG(1, 4, 1)
-    HARL_CFG(1, 4, 2)
-    HARL_CFG(1, 2, 1)
-    HARL_CFG(1, 2, 2)
-    if constexpr (D == 6 || D == 8 || D == 10) {
-        HARL_CFG(1, 4, 3)
-        HARL_CFG(1, 4, 4)
-        HARL_CFG(1, 8, 1)
-        HARL_CFG(1, 8, 2)
-        HARL_CFG(2, 4, 1)
-        HARL_CFG(2, 4, 2)
-        HARL_CFG(2, 2, 2)
-        HARL_CFG(2, 2, 4)
-        HARL_CFG(1, 16, 1)
-        HARL_CFG(1, 16, 2)
-        HARL_CFG(2, 8, 1)
+const void *pick_wp(int rpl, int tw) {
+    if constexpr (D <= 8) {
+#define HARL_WP(R, T) \
+    if (rpl == R && tw == T) return reinterpret_cast<const void *>(k_tree_score_wp<D, R, T>);
+        HARL_WP(1, 4) HARL_WP(1, 8) HARL_WP(1, 16) HARL_WP(2, 4) HARL_WP(2, 8) HARL_WP(2, 12)
+#undef HARL_WP
     }
-#undef HARL_CFG
     return nullptr;
 }
 
-ScoreKernel pick_kernel(int depth, ScoreCfg c) {
-    switch (depth) {
-        case 1: return pick_for_depth<1>(c);
-        case 2: return pick_for_depth<2>(c);
-        case 3: return pick_for_depth<3>(c);
-        case 4: return pick_for_depth<4>(c);
-        case 5: return pick_for_depth<5>(c);
-        case 6: return pick_for_depth<6>(c);
-        case 7: return pick_for_depth<7>(c);
-        case 8: return pick_for_depth<8>(c);
-        case 9: return pick_for_depth<9>(c);
-        case 10: return pick_for_depth<10>(c);
-        case 11: return pick_for_depth<11>(c);
-        case 12: return pick_for_depth<12>(c);
-        default: return nullptr;
+template <int D>
+const void *pick_ch(int tw, int ilp) {
+#define HARL_CH(T, I) \
+    if (tw == T && ilp == I) return reinterpret_cast<const void *>(k_tree_score_ch<D, T, I>);
+    HARL_CH(2, 1) HARL_CH(4, 1) HARL_CH(8, 1) HARL_CH(4, 2)
+#undef HARL_CH
+    return nullptr;
+}
+
+template <int... Ds>
+const void *pick_depth(int depth, bool wp, int a, int b, std::integer_sequence<int, Ds...>) {
+    const void *k = nullptr;
+    ((depth == Ds + 1 ? (void)(k = wp ? pick_wp<Ds + 1>(a, b) : pick_ch<Ds + 1>(a, b)) : (void)0), ...);
+    return k;
+}
+
+ScoreCfg make_cfg(const harl_ensemble *E, bool wp, int a, int b) {
+    ScoreCfg c{wp, a, b, pick_depth(E->depth, wp, a, b, std::make_integer_sequence<int, kMaxDepth>{}), 0, 0, 0};
+    const size_t stride = (size_t)E->tree_stride;
+    if (wp) {
+        c.rows_per_tile = 64 * a;
+        c.threads = 64 * b;
+        const size_t ring = (size_t)b * 2 * stride, red = (size_t)b * c.rows_per_tile * 8;
+        c.lds = (size_t)E->n_features * c.rows_per_tile * 4 + (ring > red ? ring : red);
+    } else {
+        c.rows_per_tile = 64;
+        c.threads = 64 * a;
+        const size_t chunk = (size_t)a * b * stride, red = (size_t)a * 64 * 8;
+        c.lds = (size_t)E->n_features * 64 * 4 + (chunk > red ? chunk : red);
     }
+    return c;
 }
 
-size_t lds_need(const harl_ensemble *E, ScoreCfg c) {
-    const size_t rt = 64 * c.rw;
-    const size_t feat = (size_t)E->n_features * rt * 4;
-    const size_t chunk = (size_t)c.tw * c.ilp * E->tree_stride;
-    const size_t red = (size_t)c.tw * rt * 8;
-    return feat + (chunk > red ? chunk : red);
-}
-
-// Default shape per depth; HARL_SCORE_CFG="rw,tw,ilp" overrides it (tuning sweeps).  The first
-// candidate whose feature tile and tree chunk fit in LDS is used.
+// Preferred shapes, best first; the first whose LDS fits is used.  HARL_SCORE_CFG="wp,RPL,TW" or
+// "ch,TW,ILP" puts a shape first (tuning sweeps).
 ScoreCfg choose_cfg(const harl_ensemble *E) {
-    ScoreCfg pref{1, 4, 2};
-    if (E->depth <= 6) pref = ScoreCfg{1, 4, 4};
-    else if (E->depth <= 8) pref = ScoreCfg{1, 4, 3};
-    else if (E->depth <= 10) pref = ScoreCfg{1, 4, 1};
-    else pref = ScoreCfg{1, 2, 1};
+    std::vector<ScoreCfg> cands;
     if (const char *env = std::getenv("HARL_SCORE_CFG")) {
-        ScoreCfg o{};
-        if (std::sscanf(env, "%d,%d,%d", &o.rw, &o.tw, &o.ilp) == 3 && pick_kernel(E->depth, o)) pref = o;
+        char kind[3] = {0, 0, 0};
+        int a = 0, b = 0;
+        if (std::sscanf(env, "%2[a-z],%d,%d", kind, &a, &b) == 3) cands.push_back(make_cfg(E, kind[0] == 'w', a, b));
     }
-    const ScoreCfg cands[] = {pref, {1, 4, 2}, {1, 4, 1}, {1, 2, 2}, {1, 2, 1}};
+    const int wp_pref[][2] = {{2, 12}, {1, 16}, {2, 8}, {2, 4}, {1, 8}, {1, 4}};
+    for (auto &p : wp_pref) cands.push_back(make_cfg(E, true, p[0], p[1]));
+    const int ch_pref[][2] = {{8, 1}, {4, 2}, {4, 1}, {2, 1}};
+    for (auto &p : ch_pref) cands.push_back(make_cfg(E, false, p[0], p[1]));
     for (const ScoreCfg &c : cands)
-        if (pick_kernel(E->depth, c) && lds_need(E, c) <= (size_t)kLdsBytes) return c;
-    return pref;  // does not fit: the launch reports HARL_E_UNSUPPORTED
+        if (c.kern && c.lds <= (size_t)kLdsBytes) return c;
+    return cands.back();  // nothing fits: the launch reports HARL_E_UNSUPPORTED
 }
 
-// Number of tree groups: the ensemble share per group should stay L2-resident (about 2 MB per
-// XCD) and the grid should hold enough workgroups to fill 256 CUs.  HARL_SCORE_GROUPS overrides.
-int choose_groups(const harl_ensemble *E, int32_t n_rows, ScoreCfg c) {
-    const int64_t tiles = ceil_div(n_rows > 0 ? n_rows : 1, 64 * c.rw);
+int device_cus(int device) {
+    static int cached[64] = {0};
+    if (device < 0 || device >= 64) return 256;
+    if (!cached[device]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || n <= 0) n = 256;
+        cached[device] = n;
+    }
+    return cached[device];
+}
+
+// Work split of the persistent kernel: nb workgroups, each a slice of L (tile, tree) pairs; at
+// least 2 trees per wave per slice so the feature staging stays amortised.
+struct WpSplit {
+    int64_t V, L;
+    int nb, max_pieces;
+};
+
+WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
+    WpSplit w{};
+    const int64_t tiles = ceil_div(n_rows > 0 ? n_rows : 1, c.rows_per_tile);
+    w.V = tiles * E->n_trees;
+    const int per_cu = (int)(kLdsBytes / c.lds) > 0 ? (int)(kLdsBytes / c.lds) : 1;
+    int64_t nb = (int64_t)device_cus(E->device) * per_cu;
+    const int64_t min_l = 2LL * c.b;
+    if (ceil_div(w.V, nb) < min_l) nb = ceil_div(w.V, min_l);
+    w.L = ceil_div(w.V, nb);
+    w.nb = (int)ceil_div(w.V, w.L);
+    w.max_pieces = (int)(ceil_div(E->n_trees, w.L) + 1);
+    return w;
+}
+
+// Number of tree groups G of the grid kernel.  Each group's share of the ensemble should stay
+// L2-resident (about 2 MB per XCD), and the work items (row tile x group) should fill whole waves
+// of the machine: G minimises (rounds of co-resident workgroups) x (walk time + staging time per
+// item).  HARL_SCORE_GROUPS overrides.
+int choose_groups(const harl_ensemble *E, int32_t n_rows, const ScoreCfg &c) {
+    const int64_t tiles = ceil_div(n_rows > 0 ? n_rows : 1, c.rows_per_tile);
     const int64_t bytes = (int64_t)E->n_trees * E->tree_stride;
-    int g = 1;
-    while (g < 8 && g < E->n_trees && (bytes / g > (2 << 20) || tiles * g < 1024)) g *= 2;
+    const int per_cu = c.lds > 0 ? (int)(kLdsBytes / c.lds) : 1;
+    const int64_t slots = (int64_t)device_cus(E->device) * (per_cu > 0 ? per_cu : 1);
+    const double walk = (double)E->n_trees * c.rows_per_tile * E->depth / 8.0;
+    const double stage = (double)E->n_features * c.rows_per_tile * 4 / 32.0 + 2000.0;
+    int best = 1;
+    double best_cost = 1e300;
+    for (int g = 1; g <= 8 && g <= E->n_trees; g *= 2) {
+        if (g < 8 && bytes / g > (3 << 20)) continue;
+        const double cost = (double)ceil_div(tiles * g, slots) * (walk / g + stage);
+        if (cost < best_cost * 0.97) {
+            best_cost = cost;
+            best = g;
+        }
+    }
     if (const char *env = std::getenv("HARL_SCORE_GROUPS")) {
         const int o = std::atoi(env);
-        if (o >= 1 && o <= E->n_trees && o <= 64) g = o;
+        if (o >= 1 && o <= E->n_trees && o <= 64) best = o;
     }
-    return g;
+    return best;
+}
+
+int partial_slots(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
+    return c.wp ? wp_split(E, c, n_rows).max_pieces : choose_groups(E, n_rows, c);
 }
 
 }  // namespace
 
 size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows) {
     const ScoreCfg c = choose_cfg(E);
-    const int g = choose_groups(E, n_rows, c);
-    return (size_t)g * (size_t)round_up(n_rows > 0 ? n_rows : 1, 64) * sizeof(float) + 256;
+    return (size_t)partial_slots(E, c, n_rows) * (size_t)round_up(n_rows > 0 ? n_rows : 1, 64) * sizeof(float) + 256;
 }
 
 int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows,
                        const int32_t *prog_ptr, int32_t n_prog, float *prog_score, float *stmt_score,
                        void *ws, size_t ws_bytes, hipStream_t stream) {
     const ScoreCfg c = choose_cfg(E);
-    const int G = choose_groups(E, n_rows, c);
     const int64_t ldp = round_up(n_rows > 0 ? n_rows : 1, 64);
-    if (ws_bytes < (size_t)G * ldp * sizeof(float))
+    if (ws_bytes < (size_t)partial_slots(E, c, n_rows) * ldp * sizeof(float))
         return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
     float *partial = static_cast<float *>(ws);
-    if (n_rows > 0) {
-        ScoreKernel kern = pick_kernel(E->depth, c);
-        const size_t lds = lds_need(E, c);
-        if (!kern || lds > (size_t)kLdsBytes)
-            return fail(HARL_E_UNSUPPORTED, "harl_score_round: no kernel shape fits this ensemble in LDS");
-        const int tiles = (int)ceil_div(n_rows, 64 * c.rw);
+    const unsigned seg_grid = (unsigned)ceil_div(n_prog, 4);  // one wave per program
+    const int rt_shift = c.rows_per_tile == 128 ? 7 : 6;
+    if (n_rows == 0) {
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, 6, 1, (int64_t)0, 0, prog_ptr,
+                           n_prog, 0, E->base_score, prog_score, stmt_score);
+        HARL_HIP_CHECK(hipGetLastError());
+        return HARL_OK;
+    }
+    if (!c.kern || c.lds > (size_t)kLdsBytes)
+        return fail(HARL_E_UNSUPPORTED, "harl_score_round: no kernel shape fits this ensemble in LDS");
+    if (const int rc = ensure_dynamic_lds(c.kern, c.lds)) return rc;
+    const int vec_ok = (ld % 4 == 0) && aligned(X, 16);
+    const uint4 *trees = static_cast<const uint4 *>(E->d_trees);
+    if (c.wp) {
+        const WpSplit w = wp_split(E, c, n_rows);
+        hipLaunchKernelGGL(reinterpret_cast<WpKernel>(const_cast<void *>(c.kern)), dim3((unsigned)w.nb), dim3(c.threads),
+                           c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.V, w.L, partial,
+                           ldp);
+        HARL_HIP_CHECK(hipGetLastError());
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, rt_shift, E->n_trees, w.L, 0,
+                           prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
+    } else {
+        const int G = choose_groups(E, n_rows, c);
+        const int tiles = (int)ceil_div(n_rows, c.rows_per_tile);
         const int tpg = (int)ceil_div(E->n_trees, G);
         const int groups = (int)ceil_div(E->n_trees, tpg);
-        HARL_HIP_CHECK(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-        const int vec_ok = (ld % 4 == 0) && aligned(X, 16);
-        hipLaunchKernelGGL(kern, dim3((unsigned)tiles * groups), dim3(64 * c.rw * c.tw), lds, stream, X, ld,
-                           n_rows, E->n_features, vec_ok, static_cast<const uint4 *>(E->d_trees), E->n_trees, tpg,
-                           groups, partial, ldp);
+        hipLaunchKernelGGL(reinterpret_cast<ChKernel>(const_cast<void *>(c.kern)), dim3((unsigned)tiles * groups),
+                           dim3(c.threads), c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees,
+                           tpg, groups, partial, ldp);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3((unsigned)ceil_div(n_prog, 256)), dim3(256), 0, stream, partial, ldp,
-                           groups, prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
-    } else {
-        hipLaunchKernelGGL(k_segsum, dim3((unsigned)ceil_div(n_prog, 256)), dim3(256), 0, stream, partial, ldp, 0,
-                           prog_ptr, n_prog, 0, E->base_score, prog_score, stmt_score);
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, rt_shift, E->n_trees,
+                           (int64_t)0, groups, prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
     }
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;

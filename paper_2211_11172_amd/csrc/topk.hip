@@ -7,11 +7,12 @@
 // key << 32 | (0xFFFFFFFF - i), so the ranking is the descending order of unique composites and
 // every selection below is exact and deterministic.
 //
-// K3 k_topk_select: a workgroup of 1024 threads owns a segment of up to 8192 candidates, held in
+// K3 k_topk_select: a workgroup of 512 threads owns a segment of up to 8192 candidates, held in
 //    registers.  A most-significant-digit radix select (8 bits per pass over the composite,
 //    per-wave LDS histograms, early exit once a digit bucket holds exactly the ranks still needed;
-//    a segment of at most kk candidates keeps them all) finds the
-//    segment's kk best; they are compacted into LDS and bitonic-sorted (only kk <= 2048 keys).
+//    a segment of at most kk candidates keeps them all) finds the segment's kk best; they are
+//    compacted into LDS and sorted (kk <= 512: each key's slot is its rank, counted against all
+//    others in one pass; larger kk: bitonic).
 //    Segments run in parallel; their sorted outputs form the next round's candidates until one
 //    segment is left, whose workgroup writes the final top-k directly.
 // K5 k_topk_merge: merges the sorted top-k of this call into the sorted running top-k by rank
@@ -24,8 +25,9 @@
 namespace harl {
 namespace {
 
-constexpr int kSelThreads = 1024;
-constexpr int kPerThread = 8;
+constexpr int kSelThreads = 512;
+constexpr int kPerThread = 16;
+constexpr int kRankSortMax = 512;  // up to this many selected keys are ranked directly, else bitonic
 constexpr int kSeg = kSelThreads * kPerThread;  // candidates per workgroup
 constexpr int kMergeThreads = 1024;
 
@@ -48,6 +50,7 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
     __shared__ uint32_t whist[kSelThreads / 64][256];  // per-wave histograms: fewer same-address atomics
     __shared__ uint32_t hist[256];
     __shared__ uint64_t sel[HARL_TOPK_MAX_K];
+    __shared__ uint64_t ranked[kRankSortMax];
     __shared__ uint32_t s_digit, s_above, s_eq, s_cnt;
     const int t = threadIdx.x, w = t / 64;
     const int64_t base = (int64_t)blockIdx.x * kSeg;
@@ -141,34 +144,52 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
                 if (pos < (uint32_t)kk) sel[pos] = x[j];
             }
     }
-    int P = 1;
-    while (P < kk) P <<= 1;
-    for (int i = kk + t; i < P; i += kSelThreads) sel[i] = 0;
-    __syncthreads();
-
-    // ---- bitonic sort of the kk selected composites, descending ----
-    for (int size = 2; size <= P; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = t; i < P / 2; i += kSelThreads) {
-                const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
-                const bool desc = (lo & size) == 0;
-                const uint64_t a = sel[lo], b = sel[hi];
-                if (desc ? (a < b) : (a > b)) {
-                    sel[lo] = b;
-                    sel[hi] = a;
-                }
+    const uint64_t *out_keys = sel;
+    if (kk <= kRankSortMax) {
+        // rank sort: an entry's output slot is the number of entries ranking ahead of it (a larger
+        // composite, or an equal one -- identical padding only -- at a lower position)
+        __syncthreads();
+        for (int i = t; i < kk; i += kSelThreads) {
+            const uint64_t v = sel[i];
+            int rank = 0;
+            for (int j = 0; j < kk; ++j) {
+                const uint64_t u = sel[j];
+                rank += (u > v) | ((u == v) & (j < i));
             }
-            __syncthreads();
+            ranked[rank] = v;
+        }
+        __syncthreads();
+        out_keys = ranked;
+    } else {
+        int P = 1;
+        while (P < kk) P <<= 1;
+        for (int i = kk + t; i < P; i += kSelThreads) sel[i] = 0;
+        __syncthreads();
+        // bitonic sort of the kk selected composites, descending
+        for (int size = 2; size <= P; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int i = t; i < P / 2; i += kSelThreads) {
+                    const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+                    const bool desc = (lo & size) == 0;
+                    const uint64_t a = sel[lo], b = sel[hi];
+                    if (desc ? (a < b) : (a > b)) {
+                        sel[lo] = b;
+                        sel[hi] = a;
+                    }
+                }
+                __syncthreads();
+            }
         }
     }
     for (int i = t; i < kk; i += kSelThreads) {
+        const uint64_t key = out_keys[i];
         if (emit) {
-            uint32_t l = local_of(sel[i]);
+            uint32_t l = local_of(key);
             l = l < (uint32_t)n ? l : (uint32_t)(n - 1);
             out_score[i] = score[l];
             out_index[i] = index_base + (int64_t)l;
         } else {
-            cout[(int64_t)blockIdx.x * kk + i] = sel[i];
+            cout[(int64_t)blockIdx.x * kk + i] = key;
         }
     }
 }

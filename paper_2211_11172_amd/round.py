@@ -3,8 +3,9 @@
 ``Round`` owns the model handles and every per-round device buffer (allocated once, with torch, at
 construction); ``Round.step`` enqueues the three hot-path calls of a round: the actor/critic
 forward, cost-model scoring and top-K (optionally merged into the running top-K).  The policy runs
-on a second stream, concurrently with scoring: the two read disjoint inputs (the states and the
-candidates' statement features) and only top-K depends on scoring.
+on a second stream when asked (`two_streams`): the two read disjoint inputs (the states and the
+candidates' statement features) and only top-K depends on scoring; by default all three run on
+one stream, because the scoring kernel keeps every CU busy on its own.
 """
 from __future__ import annotations
 
@@ -41,8 +42,10 @@ def upload_batch(features: np.ndarray, prog_ptr: np.ndarray, states: np.ndarray,
 
 class Round:
     def __init__(self, ens: dict, pol: dict, max_rows: int, max_prog: int, k: int, device="cuda",
-                 want_stmt=False, want_logits=False, want_probs=False, two_streams=True):
+                 want_stmt=False, want_logits=False, want_probs=False, two_streams=False):
         self.device = torch.device(device)
+        if self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
         torch.cuda.set_device(self.device)
         self.ens = harl.harl_ensemble_create(ens, stream=0)
         self.pol = harl.harl_policy_create(pol, stream=0)
