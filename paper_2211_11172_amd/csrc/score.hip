@@ -150,10 +150,11 @@ __device__ __forceinline__ int stage_features(char *smem, const float *__restric
 }
 
 // Fixed-order combination of the per-wave row sums (acc[r] of wave w for tile row r*64 + lane),
-// written as this group's fp32 partials.  `red` must not overlap live data; ends the kernel.
+// written as fp32 partials out[t] for tile rows t with row0 + t < n_rows.  `red` must not overlap
+// live data.
 template <int RPL, int NW>
 __device__ __forceinline__ void reduce_rows(double *red, const double (&acc)[RPL], int wid, int lane, int row0, int n_rows,
-                                            float *__restrict__ partial_g) {
+                                            float *__restrict__ out) {
     constexpr int RT = 64 * RPL;
 #pragma unroll
     for (int r = 0; r < RPL; ++r) red[wid * RT + r * 64 + lane] = acc[r];
@@ -162,7 +163,7 @@ __device__ __forceinline__ void reduce_rows(double *red, const double (&acc)[RPL
         double s = 0.0;
 #pragma unroll
         for (int w = 0; w < NW; ++w) s += red[w * RT + t];
-        if (row0 + t < n_rows) partial_g[row0 + t] = (float)s;
+        if (row0 + t < n_rows) out[t] = (float)s;
     }
 }
 
@@ -184,12 +185,14 @@ __device__ __forceinline__ void wave_commit(const uint4 (&pf)[PF], uint4 *dst, i
 // ---- K1, depth <= 8: persistent workgroups with per-wave private tree rings ----
 // The work is the space of (row tile, tree) pairs, tile-major: v = tile * T + tree.  Workgroup b
 // owns the contiguous slice [b*L, (b+1)*L), so every workgroup walks the same number of trees and
-// the machine is busy to the end; a tile whose trees are split between workgroups gets one partial
-// slot per piece (piece = b - first workgroup of the tile), summed later in piece order.
+// the machine is busy to the end.  The partial sums of the piece of tile i walked by workgroup b are
+// stored at block (i + b) of RT floats: a workgroup covers a contiguous run of tiles, so i + b
+// grows strictly along the (workgroup, tile) pieces and (tiles + workgroups) blocks hold them all;
+// a tile's pieces are summed later in workgroup order.
 template <int D, int RPL, int TW>
 __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
-    int T, int64_t V, int64_t L, float *__restrict__ partial, int64_t ldp) {
+    int T, int64_t V, int64_t L, float *__restrict__ partial) {
     constexpr int RT = 64 * RPL;
     constexpr int S16 = tree_stride_bytes(D) / 16;  // uint4 per packed tree
     constexpr int PF = (S16 + kWave - 1) / kWave;   // uint4 per lane per tree
@@ -243,9 +246,8 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
         const int nt1 = next ? (int)(T < v_end - v ? T : v_end - v) : 0;
         if (next && wid < nt1) wave_fetch<S16>(pf, trees + (int64_t)wid * S16, lane);
         __syncthreads();  // every wave is done with its ring: reuse the ring region for the reduction
-        const int piece = (int)(blockIdx.x - ((int64_t)tile * T) / L);
         reduce_rows<RPL, TW>(reinterpret_cast<double *>(smem + ring_off), acc, wid, lane, row0, n_rows,
-                             partial + (int64_t)piece * ldp);
+                             partial + ((int64_t)tile + blockIdx.x) * RT);
         if (!next) break;
         ++tile;
         t0 = 0;
@@ -321,22 +323,14 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
         }
     }
     reduce_rows<1, TW>(reinterpret_cast<double *>(smem + chunk_off), acc, wid, lane, row0, n_rows,
-                       partial + (int64_t)g * ldp);
+                       partial + (int64_t)g * ldp + row0);
 }
 
-// Number of partial slots of row tile `tile`: `groups` in the grouped layout (L == 0), else the
-// number of workgroup slices of length L that the tile's T trees are cut into.
-__device__ __forceinline__ int tile_pieces(int64_t tile, int T, int64_t L, int groups) {
-    if (L == 0) return groups;
-    const int64_t a = tile * T, b = (tile + 1) * T - 1;
-    if (b < ((int64_t)1 << 31) && L < ((int64_t)1 << 31))
-        return (int)((uint32_t)b / (uint32_t)L - (uint32_t)a / (uint32_t)L + 1u);
-    return (int)(b / L - a / L + 1);
-}
-
-// K2: one wave per program (lane = statement row, looping for programs of more than 64 rows):
-// each row sums its partial slots in slot order (fp64), the wave then sums its rows with a
-// fixed xor-butterfly, so the result does not depend on scheduling.
+// K2: one wave per program (lane = statement row, looping for programs of more than 64 rows).
+// Each row sums its partials in a fixed order (fp64) -- grouped layout (L == 0): `groups` slots
+// partial[g * ldp + r]; sliced layout: the workgroups b = first..last whose slices cut the row's
+// tile i (RT rows, T trees), at partial[(i + b) * RT + r % RT] -- and the wave then sums its rows
+// with a fixed xor-butterfly, so the result does not depend on scheduling.
 __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int rt_shift, int T,
                                                 int64_t L, int groups, const int32_t *__restrict__ prog_ptr, int n_prog,
                                                 int n_rows, float base_score, float *__restrict__ prog_score,
@@ -348,9 +342,15 @@ __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partia
     const int e = min(max(prog_ptr[p + 1], b), n_rows);
     double acc = 0.0;
     for (int r = b + lane; r < e; r += kWave) {
-        const int np = tile_pieces(r >> rt_shift, T, L, groups);
-        double s = (double)partial[r];
-        for (int gi = 1; gi < np; ++gi) s += (double)partial[(int64_t)gi * ldp + r];
+        double s = 0.0;
+        if (L == 0) {
+            for (int gi = 0; gi < groups; ++gi) s += (double)partial[(int64_t)gi * ldp + r];
+        } else {
+            const int64_t tile = r >> rt_shift;
+            const int64_t first = tile * T / L, last = ((tile + 1) * T - 1) / L;
+            const float *src = partial + (tile << rt_shift) + (r & ((1 << rt_shift) - 1));
+            for (int64_t wb = first; wb <= last; ++wb) s += (double)src[wb << rt_shift];
+        }
         if (stmt_score) stmt_score[r] = (float)s;
         acc += s;
     }
@@ -363,7 +363,7 @@ __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partia
 // launch configuration
 // ---------------------------------------------------------------------------------------------
 using ChKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int, int, float *, int64_t);
-using WpKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int64_t, int64_t, float *, int64_t);
+using WpKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int64_t, int64_t, float *);
 
 struct ScoreCfg {
     bool wp;            // persistent per-wave rings (else grid of shared chunks)
@@ -449,13 +449,14 @@ int device_cus(int device) {
 // Work split of the persistent kernel: nb workgroups, each a slice of L (tile, tree) pairs; at
 // least 2 trees per wave per slice so the feature staging stays amortised.
 struct WpSplit {
-    int64_t V, L;
-    int nb, max_pieces;
+    int64_t V, L, tiles;
+    int nb;
 };
 
 WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
     WpSplit w{};
     const int64_t tiles = ceil_div(n_rows > 0 ? n_rows : 1, c.rows_per_tile);
+    w.tiles = tiles;
     w.V = tiles * E->n_trees;
     const int per_cu = (int)(kLdsBytes / c.lds) > 0 ? (int)(kLdsBytes / c.lds) : 1;
     int64_t nb = (int64_t)device_cus(E->device) * per_cu;
@@ -463,7 +464,6 @@ WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
     if (ceil_div(w.V, nb) < min_l) nb = ceil_div(w.V, min_l);
     w.L = ceil_div(w.V, nb);
     w.nb = (int)ceil_div(w.V, w.L);
-    w.max_pieces = (int)(ceil_div(E->n_trees, w.L) + 1);
     return w;
 }
 
@@ -495,15 +495,22 @@ int choose_groups(const harl_ensemble *E, int32_t n_rows, const ScoreCfg &c) {
     return best;
 }
 
-int partial_slots(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
-    return c.wp ? wp_split(E, c, n_rows).max_pieces : choose_groups(E, n_rows, c);
+// Floats of partial sums: sliced layout (tiles + workgroups) blocks of RT rows; grouped layout
+// G rows-long slots.
+size_t partial_floats(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
+    const int64_t ldp = round_up(n_rows > 0 ? n_rows : 1, 64);
+    if (c.wp) {
+        const WpSplit w = wp_split(E, c, n_rows);
+        return (size_t)(w.tiles + w.nb) * c.rows_per_tile;
+    }
+    return (size_t)choose_groups(E, n_rows, c) * ldp;
 }
 
 }  // namespace
 
 size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows) {
     const ScoreCfg c = choose_cfg(E);
-    return (size_t)partial_slots(E, c, n_rows) * (size_t)round_up(n_rows > 0 ? n_rows : 1, 64) * sizeof(float) + 256;
+    return partial_floats(E, c, n_rows) * sizeof(float) + 256;
 }
 
 int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows,
@@ -511,7 +518,7 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
                        void *ws, size_t ws_bytes, hipStream_t stream) {
     const ScoreCfg c = choose_cfg(E);
     const int64_t ldp = round_up(n_rows > 0 ? n_rows : 1, 64);
-    if (ws_bytes < (size_t)partial_slots(E, c, n_rows) * ldp * sizeof(float))
+    if (ws_bytes < partial_floats(E, c, n_rows) * sizeof(float))
         return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
     float *partial = static_cast<float *>(ws);
     const unsigned seg_grid = (unsigned)ceil_div(n_prog, 4);  // one wave per program
@@ -530,8 +537,7 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
     if (c.wp) {
         const WpSplit w = wp_split(E, c, n_rows);
         hipLaunchKernelGGL(reinterpret_cast<WpKernel>(const_cast<void *>(c.kern)), dim3((unsigned)w.nb), dim3(c.threads),
-                           c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.V, w.L, partial,
-                           ldp);
+                           c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.V, w.L, partial);
         HARL_HIP_CHECK(hipGetLastError());
         hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, rt_shift, E->n_trees, w.L, 0,
                            prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
