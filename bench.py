@@ -23,10 +23,10 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 N_CU, CLOCK_GHZ = 256, 2.4
-# Node-visit ceiling of the traversal loop: each visit of 64 rows (one wave) issues one 8-byte and
-# one 4-byte LDS gather (768 B) and about 5 VALU instructions; the CU's LDS serves 128 B/clk and
-# issues one wave-wide VALU instruction per clock, so the LDS bound (6 clk / 64 visits) binds.
-LDS_BYTES_PER_CLK = 128.0
+# Node-visit ceiling of tree traversal: a visit must read at least 12 bytes from LDS (an 8-byte
+# node and a 4-byte feature); the LDS read rate measured on MI355X with 16-byte reads is
+# 152 B/clk/CU (100 B/clk/CU with 4- and 8-byte reads).
+LDS_BYTES_PER_CLK = 152.0
 LDS_BYTES_PER_VISIT = 12.0
 PEAK_GVISITS = N_CU * CLOCK_GHZ * LDS_BYTES_PER_CLK / LDS_BYTES_PER_VISIT  # G visits / s
 
@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--config", default="standard")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--counter-probe", action="store_true",
+                    help="for hardware-counter runs: one 256 MiB device-to-device copy (calibration of the "
+                         "byte counters) followed by 3 eager harl_score_round calls; prints sizes and exits")
     ap.add_argument("--no-graph", action="store_true", help="launch every call from the host instead of "
                     "replaying a captured graph of the round")
     ap.add_argument("--two-streams", action="store_true",
@@ -97,6 +100,20 @@ def main():
     rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=args.two_streams)
     batch = upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)
     main_stream = torch.cuda.current_stream(dev)
+
+    if args.counter_probe:
+        n_copy = 256 << 20
+        src = torch.ones(n_copy // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            rnd.score(batch)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n_copy, "score_calls": 3, "feature_bytes": b["n_rows"] * cfg.n_features * 4,
+                          "n_rows": b["n_rows"], "n_prog": cfg.n_prog}), flush=True)
+        rnd.close()
+        return
 
     # warm up eagerly (first calls also set kernel attributes), on a side stream as graph capture
     # requires, then capture one round as a HIP graph: replaying it issues the round's kernels
