@@ -30,16 +30,14 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
 // ------------------------------------------------------------------------------------------
-// Packed GBDT ensemble.  Every tree is stored as a complete binary tree of `depth` split levels,
-// numbered breadth-first from 1: internal node i (1 <= i < 2^depth) is 8 bytes {u32 word,
-// f32 threshold} at byte 8*i (bytes 0..7 pad), its children are 2i (left) and 2i+1 (right), and
-// the 2^depth fp32 leaves follow at byte 8 * 2^depth (leaf j = slot 2^depth + j).  The stride of
-// one tree is 12 * 2^depth bytes rounded up to 16.  The node word holds the split feature in bits
-// 0..23 and the missing-goes-left flag in bit 31.
+// Packed GBDT ensemble.  Every tree is stored as a complete binary tree of `depth` split levels
+// (an early leaf repeats below dummy splits), in the record layout described in score.hip: 8-byte
+// records {threshold, children's feature codes} for the upper levels and 16-byte records
+// {threshold, left leaf, right leaf, 0} for the last split level.  A feature code is the split
+// feature (< 2^15) with bit 15 set when missing values go left.
 // ------------------------------------------------------------------------------------------
 constexpr int kMaxDepth = 12;
 constexpr int kMaxFeatures = 448;
-constexpr uint32_t kNodeDefaultLeft = 0x80000000u;
 
 }  // namespace harl
 

@@ -7,15 +7,15 @@
 //   tile's features are staged once into LDS, feature-major ([F][rows] fp32, so a lane's gather
 //   of any feature of its own row hits bank = lane: conflict-free whatever feature a node asks
 //   for).  Lane = row.  Each level of a walk issues the current node's feature read together with
-//   the read of both its children (16 bytes) and picks the child in registers, so a level costs
-//   one LDS round trip; the leaf pair comes with the last level.  Row sums are accumulated in fp64
-//   and combined over the waves in a fixed order.  Two variants:
-//   k_tree_score_wp (depth <= 8): every wave streams its own trees (tree t + k*TW) through a
-//     private two-slot LDS ring -- the next tree is fetched into registers while the current one
-//     is walked -- so waves never wait on each other between the feature staging and the final
-//     reduction.  Each lane walks RPL rows per tree (ILP across rows; the staged tree serves
-//     64*RPL rows).
-//   k_tree_score_ch (deeper trees, whose 2^depth-node trees are too big for per-wave rings): the
+//   the read of the node's record (threshold and both children's feature codes), so a level costs
+//   one LDS round trip; the last level's record carries both leaves.  Row sums are accumulated in
+//   fp64 and combined over the waves in a fixed order.  Two variants:
+//   k_tree_score_wp (depth <= 10): every wave streams its own trees (tree t + k*TW) through
+//     private LDS slots, NTW trees walked at once, the next ones fetched into registers while the
+//     current ones are walked -- so waves never wait on each other between the feature staging
+//     and the final reduction.  Each lane walks RPL rows per tree (ILP across rows and trees; the
+//     staged tree serves 64*RPL rows).
+//   k_tree_score_ch (deeper trees, whose 2^depth-node trees are too big for per-wave slots): the
 //     workgroup stages chunks of TW*ILP trees shared by all waves, the next chunk fetched into
 //     registers during the walk of the current one.
 // K2 k_segsum: one wave per program sums its rows' partial slots in a fixed order (fp64).
@@ -38,81 +38,153 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kLdsBytes = 160 * 1024;
+constexpr int kMaxWpDepth = 10;  // deeper trees (up to 48 KB each) use the shared-chunk kernel
 
-constexpr int tree_stride_bytes(int D) { return ((1 << D) * 12 + 15) / 16 * 16; }
+// Packed tree of D split levels (M = 2^D leaves), nodes numbered breadth-first from 1:
+//   bytes 0..7      record 0: {0, code(1)} -- the root's feature code
+//   byte 8*i        record i, 1 <= i < M/2 (levels 0 .. D-2): {threshold(i), code(2i) | code(2i+1) << 16}
+//   byte LL+16*j    last-level node i = M/2 + j: {threshold(i), leaf(2i - M), leaf(2i + 1 - M), 0}
+// with LL = max(4M, 16) and code(n) = feature(n) | 0x8000 when missing values go left at n.  A
+// level of a walk reads the feature value of the current node and the current node's record
+// (threshold + both children's codes, 8 bytes) -- both addresses are known when the level starts,
+// so a level is one LDS round trip of 12 bytes -- and the last level reads its threshold and both
+// leaves in one 16-byte record.  The first 16 bytes {0, code(1), threshold(1), codes(2, 3)} are
+// the same for every row, so the walk takes them as wave-uniform values.
+constexpr uint32_t tree_ll_bytes(int D) { return (4u << D) > 16u ? (4u << D) : 16u; }
+constexpr int tree_stride_bytes(int D) { return (int)((tree_ll_bytes(D) + (8u << D) + 15u) / 16u * 16u); }
+constexpr uint32_t kCodeDefaultLeft = 0x8000u;
+constexpr uint32_t kCodeFeature = 0x7FFFu;
 
-// Packed tree (1-based breadth-first): byte 8*i holds internal node i (i = 1 .. 2^D - 1; bytes 0..7
-// are padding), so the two children of node i sit together, 16-byte aligned, at byte 16*i; the
-// 2^D leaves follow at byte 8 * 2^D, the two leaves below a last-level node i at
-// 8 * 2^D + 8*i - 4 * 2^D.
+// x < threshold goes left; a missing value (NaN) goes the node's default way.
 template <bool NAN_AWARE>
-__device__ __forceinline__ uint32_t go_right(float x, float thr, uint32_t word) {
-    uint32_t right = x >= thr ? 1u : 0u;
-    if (NAN_AWARE) right |= (x != x && !(word & kNodeDefaultLeft)) ? 1u : 0u;
-    return right;
+__device__ __forceinline__ uint32_t go_right(float x, float thr, uint32_t code) {
+    if (!NAN_AWARE) return x >= thr ? 1u : 0u;
+    const bool left = x < thr || (x != x && code > kCodeFeature);
+    return left ? 0u : 1u;
 }
 
-// Walk NT_ trees at LDS byte offsets tb[] for R rows of this lane (feature tile row stride RT4
-// bytes per feature; lane_off[r] = byte offset of the lane's r-th row).  Every (tree, row) pair is
-// an independent chain; all chains of a level are issued together.
+// Wave-uniform head of a packed tree (its first 16 bytes).
+struct TreeHead {
+    uint32_t code, thr, pair;
+};
+
+// An opaque VGPR copy of a wave-uniform value, so that one v_cndmask can pick between two of
+// them (a VALU instruction reads at most one scalar operand).
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
+// LDS accesses by absolute LDS byte address (the walk carries addresses as plain integers).
+typedef __attribute__((address_space(3))) char lds_char;
+__device__ __forceinline__ uint32_t lds_addr(const char *p) { return (uint32_t)(uintptr_t)(const lds_char *)p; }
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <class T>
+__device__ __forceinline__ T lds_ld(uint32_t a);
+template <>
+__device__ __forceinline__ float lds_ld<float>(uint32_t a) {
+    return *(const __attribute__((address_space(3))) float *)(uintptr_t)a;
+}
+template <>
+__device__ __forceinline__ uint2 lds_ld<uint2>(uint32_t a) {
+    const u32x2 v = *(const __attribute__((address_space(3))) u32x2 *)(uintptr_t)a;
+    return make_uint2(v.x, v.y);
+}
+template <>
+__device__ __forceinline__ uint4 lds_ld<uint4>(uint32_t a) {
+    const u32x4 v = *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)a;
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Feature value of this lane's row for the feature of a 15-bit code.
+template <uint32_t RT4>
+__device__ __forceinline__ float feature_at(uint32_t feature, uint32_t lane_off) {
+    return lds_ld<float>(feature * RT4 + lane_off);
+}
+
+// Walk NT_ trees at LDS addresses tb[] (heads hd[]) for R rows of this lane (feature tile row
+// stride RT4 bytes per feature; lane_off[r] = LDS address of the lane's r-th row of feature 0).  Every
+// (tree, row) pair is an independent chain c = tree * R + row.  A chain's step at one level picks
+// the child, then at once issues the child's two LDS reads (feature value, record); the chains
+// take their steps in turn, so while one chain decides, the reads of all the others are in flight
+// (LDS reads of a wave return in order, and the scheduling barriers keep that order).  The
+// record address is carried directly: child record = 2 * current - tb + 8 * go_right.  Codes
+// keep the missing-goes-left flag only in the NaN-aware walk.
 template <int D, int NT_, int R, uint32_t RT4, bool NAN_AWARE>
-__device__ __forceinline__ void walk_trees(const char *smem, const uint32_t (&tb)[NT_], const uint32_t (&lane_off)[R],
-                                           double (&acc)[R]) {
-    constexpr uint32_t kLeafBase = 8u << D;
-    uint32_t idx[NT_][R], word[NT_][R];
-    float thr[NT_][R];
+__device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const TreeHead (&hd)[NT_],
+                                           const uint32_t (&lane_off)[R], double (&acc)[R]) {
+    constexpr int NC = NT_ * R;
+    constexpr uint32_t W = NAN_AWARE ? 16u : 15u;
+    constexpr uint32_t kLast = tree_ll_bytes(D) - (8u << D);  // last-level record = 2 * rec(i) - tb + kLast
+    uint32_t c_left[NT_], c_right[NT_], c_root_l[NT_], c_root_r[NT_];
 #pragma unroll
     for (int i = 0; i < NT_; ++i) {
-        const uint2 root = *reinterpret_cast<const uint2 *>(smem + tb[i] + 8u);
+        c_left[i] = in_vgpr(0u - tb[i]);
+        c_right[i] = in_vgpr(8u - tb[i]);
+        c_root_l[i] = in_vgpr(tb[i] + 16u);
+        c_root_r[i] = in_vgpr(tb[i] + 24u);
+    }
+    float x[NC];
+    uint32_t a[NC], code[NC];
+    uint2 rec[NC];
+    uint4 lv[NC];
+    // level 0: the root is the same node for every row of a tree
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            word[i][r] = root.x;
-            thr[i][r] = __uint_as_float(root.y);
-            idx[i][r] = 1;
+    for (int c = 0; c < NC; ++c) x[c] = feature_at<RT4>(hd[c / R].code & kCodeFeature, lane_off[c % R]);
+    if constexpr (D == 1) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) lv[c] = lds_ld<uint4>(tb[c / R] + 16u);
+    } else {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int i = c / R;
+            const uint32_t g = go_right<NAN_AWARE>(x[c], __uint_as_float(hd[i].thr), hd[i].code);
+            a[c] = g ? c_root_r[i] : c_root_l[i];
+            const uint32_t sh = g ? 16u : 0u;
+            code[c] = __builtin_amdgcn_ubfe(hd[i].pair, sh, W);
+            x[c] = feature_at<RT4>(NAN_AWARE ? __builtin_amdgcn_ubfe(hd[i].pair, sh, 15u) : code[c], lane_off[c % R]);
+            if constexpr (D > 2)
+                rec[c] = lds_ld<uint2>(a[c]);
+            else
+                lv[c] = lds_ld<uint4>(2u * a[c] - tb[i] + kLast);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // levels 1 .. D-2
+#pragma unroll
+        for (int lvl = 1; lvl + 1 < D; ++lvl) {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const int i = c / R;
+                const uint32_t g = go_right<NAN_AWARE>(x[c], __uint_as_float(rec[c].x), code[c]);
+                a[c] = 2u * a[c] + (g ? c_right[i] : c_left[i]);
+                const uint32_t sh = g ? 16u : 0u;
+                code[c] = __builtin_amdgcn_ubfe(rec[c].y, sh, W);
+                x[c] = feature_at<RT4>(NAN_AWARE ? __builtin_amdgcn_ubfe(rec[c].y, sh, 15u) : code[c], lane_off[c % R]);
+                if (lvl + 2 < D)
+                    rec[c] = lds_ld<uint2>(a[c]);
+                else
+                    lv[c] = lds_ld<uint4>(2u * a[c] - tb[i] + kLast);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     }
+    // last level: threshold and both leaves
 #pragma unroll
-    for (int lvl = 0; lvl + 1 < D; ++lvl) {
-        float x[NT_][R];
-        uint4 kids[NT_][R];
-#pragma unroll
-        for (int i = 0; i < NT_; ++i)
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                x[i][r] = *reinterpret_cast<const float *>(smem + __umul24(word[i][r], RT4) + lane_off[r]);
-                kids[i][r] = *reinterpret_cast<const uint4 *>(smem + tb[i] + idx[i][r] * 16u);
-            }
-#pragma unroll
-        for (int i = 0; i < NT_; ++i)
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const uint32_t g = go_right<NAN_AWARE>(x[i][r], thr[i][r], word[i][r]);
-                idx[i][r] = 2u * idx[i][r] + g;
-                word[i][r] = g ? kids[i][r].z : kids[i][r].x;
-                thr[i][r] = __uint_as_float(g ? kids[i][r].w : kids[i][r].y);
-            }
+    for (int c = 0; c < NC; ++c) {
+        const uint32_t cd = D == 1 ? hd[c / R].code : code[c];
+        const uint32_t g = go_right<NAN_AWARE>(x[c], __uint_as_float(lv[c].x), cd);
+        acc[c % R] += (double)__uint_as_float(g ? lv[c].z : lv[c].y);
     }
-    float x[NT_][R];
-    float2 lv[NT_][R];
-#pragma unroll
-    for (int i = 0; i < NT_; ++i)
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            x[i][r] = *reinterpret_cast<const float *>(smem + __umul24(word[i][r], RT4) + lane_off[r]);
-            lv[i][r] = *reinterpret_cast<const float2 *>(smem + tb[i] + kLeafBase + idx[i][r] * 8u - (4u << D));
-        }
-#pragma unroll
-    for (int i = 0; i < NT_; ++i)
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-            acc[r] += (double)(go_right<NAN_AWARE>(x[i][r], thr[i][r], word[i][r]) ? lv[i][r].y : lv[i][r].x);
 }
 
 // Stage rows [row0, row0 + RT) of every feature into LDS ([F][RT] fp32, zero past n_rows), with
-// 8 loads in flight per thread; returns (block-wide) whether any staged value is NaN.
+// 8 loads in flight per thread; returns (block-wide) whether any staged value is NaN.  `flag` is
+// an LDS word that is 0 on entry (ordered before this call by a barrier); threads that see a NaN
+// set it, and the barrier at the end publishes it.
 template <int RT, int NT>
 __device__ __forceinline__ int stage_features(char *smem, const float *__restrict__ X, int64_t ld, int n_rows, int F,
-                                              int vec_ok, int row0) {
+                                              int vec_ok, int row0, volatile int *flag) {
     constexpr int V = RT / 4;  // float4 per feature row of the tile
     constexpr int B = 8;
     int has_nan = 0;
@@ -146,7 +218,9 @@ __device__ __forceinline__ int stage_features(char *smem, const float *__restric
             }
         }
     }
-    return __syncthreads_or(has_nan);
+    if (has_nan) *flag = 1;
+    __syncthreads();
+    return *flag;
 }
 
 // Fixed-order combination of the per-wave row sums (acc[r] of wave w for tile row r*64 + lane),
@@ -182,70 +256,119 @@ __device__ __forceinline__ void wave_commit(const uint4 (&pf)[PF], uint4 *dst, i
         if (S16 % kWave == 0 || j * kWave + lane < S16) dst[j * kWave + lane] = pf[j];
 }
 
-// ---- K1, depth <= 8: persistent workgroups with per-wave private tree rings ----
+// Trees t + j*TW (j < NTW, t + j*TW < t_end) of a wave: fetch into registers, commit to the wave's
+// LDS slots (slot j) and take their wave-uniform heads (lane 0 holds each tree's first uint4).
+template <int S16, int PF, int NTW, int TW>
+__device__ __forceinline__ void group_fetch(uint4 (&pf)[NTW][PF], const uint4 *__restrict__ trees, int t, int t_end,
+                                            int lane) {
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+        if (t + j * TW < t_end) wave_fetch<S16>(pf[j], trees + (int64_t)(t + j * TW) * S16, lane);
+}
+
+template <int S16, int PF, int NTW, int TW>
+__device__ __forceinline__ void group_commit(const uint4 (&pf)[NTW][PF], char *slots, TreeHead (&hd)[NTW], int t,
+                                             int t_end, int lane) {
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+        if (t + j * TW < t_end) {
+            wave_commit<S16>(pf[j], reinterpret_cast<uint4 *>(slots + (uint32_t)j * (S16 * 16)), lane);
+            hd[j].code = __builtin_amdgcn_readfirstlane(pf[j][0].y);
+            hd[j].thr = __builtin_amdgcn_readfirstlane(pf[j][0].z);
+            hd[j].pair = __builtin_amdgcn_readfirstlane(pf[j][0].w);
+        }
+}
+
+// ---- K1, depth <= 10: persistent workgroups with per-wave private tree slots ----
 // The work is the space of (row tile, tree) pairs, tile-major: v = tile * T + tree.  Workgroup b
 // owns the contiguous slice [b*L, (b+1)*L), so every workgroup walks the same number of trees and
-// the machine is busy to the end.  The partial sums of the piece of tile i walked by workgroup b are
-// stored at block (i + b) of RT floats: a workgroup covers a contiguous run of tiles, so i + b
-// grows strictly along the (workgroup, tile) pieces and (tiles + workgroups) blocks hold them all;
-// a tile's pieces are summed later in workgroup order.
-template <int D, int RPL, int TW>
+// the machine is busy to the end.  Wave w walks trees w, w + TW, ... of each piece, NTW at a time
+// from its NTW LDS slots; the next NTW trees are fetched into registers meanwhile and committed
+// over the slots after the walk (LDS operations of one wave execute in order, so the walk's reads
+// are served before the commit's writes).  The partial sums of the piece of tile i walked by
+// workgroup b are stored at block (i + b) of RT floats: a workgroup covers a contiguous run of
+// tiles, so i + b grows strictly along the (workgroup, tile) pieces and (tiles + workgroups)
+// blocks hold them all; a tile's pieces are summed later in workgroup order.
+template <int D, int RPL, int TW, int NTW>
 __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
     int T, int64_t V, int64_t L, float *__restrict__ partial) {
     constexpr int RT = 64 * RPL;
     constexpr int S16 = tree_stride_bytes(D) / 16;  // uint4 per packed tree
     constexpr int PF = (S16 + kWave - 1) / kWave;   // uint4 per lane per tree
+    constexpr int STEP = NTW * TW;                  // trees between a wave's consecutive groups
     extern __shared__ __align__(16) char smem[];
-
     const int64_t v_begin = (int64_t)blockIdx.x * L;
     const int64_t v_end = v_begin + L < V ? v_begin + L : V;
     if (v_begin >= v_end) return;  // whole workgroup: no barrier is skipped by part of it
-    const int wid = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const uint32_t ring_off = (uint32_t)F * RT * 4u;
-    char *const ring = smem + ring_off + (uint32_t)wid * 2u * (S16 * 16);
+    const uint32_t slot0 = ring_off + (uint32_t)wid * NTW * (S16 * 16);
+    char *const slots = smem + slot0;
+    // two NaN flags past the slot / reduction region, alternating between pieces: the flag of the
+    // next piece is cleared by thread 0 once the current one has been read by every thread
+    constexpr uint32_t kSlots = (uint32_t)TW * NTW * S16 * 16, kRed = (uint32_t)TW * RT * 8;
+    volatile int *const flags = reinterpret_cast<volatile int *>(smem + ring_off + (kSlots > kRed ? kSlots : kRed));
+    if (threadIdx.x == 0) flags[0] = flags[1] = 0;
+    __syncthreads();
+    int piece = 0;
 
-    uint4 pf[PF];
+    uint4 pf[NTW][PF];
 #pragma unroll
-    for (int j = 0; j < PF; ++j) pf[j] = make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+        for (int k = 0; k < PF; ++k) pf[j][k] = make_uint4(0, 0, 0, 0);
+    TreeHead hd[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) hd[j] = TreeHead{0, 0, 0};
+    const uint32_t base = lds_addr(smem);
     uint32_t lane_off[RPL];
 #pragma unroll
-    for (int r = 0; r < RPL; ++r) lane_off[r] = (uint32_t)(r * 64 + lane) * 4u;
+    for (int r = 0; r < RPL; ++r) lane_off[r] = base + (uint32_t)(r * 64 + lane) * 4u;
 
     int64_t v = v_begin;
     int tile = (int)(v / T);
     int t0 = (int)(v % T);
     int t1 = (int)(T - t0 < v_end - v ? T : t0 + (v_end - v));
     int t = t0 + wid;
-    if (t < t1) wave_fetch<S16>(pf, trees + (int64_t)t * S16, lane);   // overlaps the feature staging
+    group_fetch<S16, PF, NTW, TW>(pf, trees, t, t1, lane);   // overlaps the feature staging
     while (true) {
         const int row0 = tile * RT;
-        const int has_nan = stage_features<RT, 64 * TW>(smem, X, ld, n_rows, F, vec_ok, row0);
-        if (t < t1) wave_commit<S16>(pf, reinterpret_cast<uint4 *>(ring), lane);
-        if (t + TW < t1) wave_fetch<S16>(pf, trees + (int64_t)(t + TW) * S16, lane);
+        const int has_nan = stage_features<RT, 64 * TW>(smem, X, ld, n_rows, F, vec_ok, row0, flags + (piece & 1));
+        if (threadIdx.x == 0) flags[(piece + 1) & 1] = 0;
+        ++piece;
+        group_commit<S16, PF, NTW, TW>(pf, slots, hd, t, t1, lane);
+        group_fetch<S16, PF, NTW, TW>(pf, trees, t + STEP, t1, lane);
         double acc[RPL];
 #pragma unroll
         for (int r = 0; r < RPL; ++r) acc[r] = 0.0;
-        int s = 0;
-        for (; t < t1; t += TW) {
-            const uint32_t tb[1] = {ring_off + (uint32_t)wid * 2u * (S16 * 16) + (uint32_t)s * (S16 * 16)};
-            if (has_nan)
-                walk_trees<D, 1, RPL, (uint32_t)RT * 4u, true>(smem, tb, lane_off, acc);
-            else
-                walk_trees<D, 1, RPL, (uint32_t)RT * 4u, false>(smem, tb, lane_off, acc);
-            if (t + TW < t1) {                 // LDS ops of a wave run in order: the walk's reads of
-                                               // slot s complete before the next commit overwrites it
-                wave_commit<S16>(pf, reinterpret_cast<uint4 *>(ring + (uint32_t)(s ^ 1) * (S16 * 16)), lane);
-                if (t + 2 * TW < t1) wave_fetch<S16>(pf, trees + (int64_t)(t + 2 * TW) * S16, lane);
+        for (; t < t1; t += STEP) {
+            if (NTW == 2 && t + TW < t1) {
+                const uint32_t tb[2] = {base + slot0, base + slot0 + S16 * 16};
+                const TreeHead h2[2] = {hd[0], hd[NTW - 1]};
+                if (has_nan)
+                    walk_trees<D, 2, RPL, (uint32_t)RT * 4u, true>(tb, h2, lane_off, acc);
+                else
+                    walk_trees<D, 2, RPL, (uint32_t)RT * 4u, false>(tb, h2, lane_off, acc);
+            } else {
+                const uint32_t tb[1] = {base + slot0};
+                const TreeHead h1[1] = {hd[0]};
+                if (has_nan)
+                    walk_trees<D, 1, RPL, (uint32_t)RT * 4u, true>(tb, h1, lane_off, acc);
+                else
+                    walk_trees<D, 1, RPL, (uint32_t)RT * 4u, false>(tb, h1, lane_off, acc);
             }
-            s ^= 1;
+            if (t + STEP < t1) {
+                group_commit<S16, PF, NTW, TW>(pf, slots, hd, t + STEP, t1, lane);
+                group_fetch<S16, PF, NTW, TW>(pf, trees, t + 2 * STEP, t1, lane);
+            }
         }
-        // the next piece (if any) starts at tree 0 of the next tile: prefetch its first tree now
+        // the next piece (if any) starts at tree 0 of the next tile: prefetch its first trees now
         v += t1 - t0;
         const bool next = v < v_end;
         const int nt1 = next ? (int)(T < v_end - v ? T : v_end - v) : 0;
-        if (next && wid < nt1) wave_fetch<S16>(pf, trees + (int64_t)wid * S16, lane);
-        __syncthreads();  // every wave is done with its ring: reuse the ring region for the reduction
+        if (next) group_fetch<S16, PF, NTW, TW>(pf, trees, wid, nt1, lane);
+        __syncthreads();  // every wave is done with its slots: reuse the region for the reduction
         reduce_rows<RPL, TW>(reinterpret_cast<double *>(smem + ring_off), acc, wid, lane, row0, n_rows,
                              partial + ((int64_t)tile + blockIdx.x) * RT);
         if (!next) break;
@@ -299,23 +422,34 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
 
     uint4 pf[NPF];
     if (t_begin < t_end) block_fetch<C, S16, NT>(pf, trees, t_begin, t_end);
-    const int has_nan = stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, row0);
+    constexpr uint32_t kChunk = (uint32_t)CH16 * 16, kRed = (uint32_t)TW * RT * 8;
+    volatile int *const flag = reinterpret_cast<volatile int *>(smem + chunk_off + (kChunk > kRed ? kChunk : kRed));
+    if (threadIdx.x == 0) *flag = 0;
+    __syncthreads();
+    const int has_nan = stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, row0, flag);
     if (t_begin < t_end) block_commit<C, S16, NT>(pf, reinterpret_cast<uint4 *>(smem + chunk_off));
     __syncthreads();
 
-    const int wid = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const uint32_t lane_off[1] = {(uint32_t)lane * 4u};
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const uint32_t base = lds_addr(smem);
+    const uint32_t lane_off[1] = {base + (uint32_t)lane * 4u};
     double acc[1] = {0.0};
     for (int t0 = t_begin; t0 < t_end; t0 += C) {
         const bool more = t0 + C < t_end;
         if (more) block_fetch<C, S16, NT>(pf, trees, t0 + C, t_end);
         uint32_t tb[ILP];
+        TreeHead hd[ILP];
 #pragma unroll
-        for (int i = 0; i < ILP; ++i) tb[i] = chunk_off + (uint32_t)(wid * ILP + i) * (S16 * 16);
+        for (int i = 0; i < ILP; ++i) {
+            tb[i] = base + chunk_off + (uint32_t)(wid * ILP + i) * (S16 * 16);
+            const uint4 h = lds_ld<uint4>(tb[i]);
+            hd[i] = TreeHead{(uint32_t)__builtin_amdgcn_readfirstlane(h.y), (uint32_t)__builtin_amdgcn_readfirstlane(h.z),
+                             (uint32_t)__builtin_amdgcn_readfirstlane(h.w)};
+        }
         if (has_nan)
-            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, true>(smem, tb, lane_off, acc);
+            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, true>(tb, hd, lane_off, acc);
         else
-            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, false>(smem, tb, lane_off, acc);
+            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, false>(tb, hd, lane_off, acc);
         __syncthreads();
         if (more) {
             block_commit<C, S16, NT>(pf, reinterpret_cast<uint4 *>(smem + chunk_off));
@@ -366,21 +500,27 @@ using ChKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, 
 using WpKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int64_t, int64_t, float *);
 
 struct ScoreCfg {
-    bool wp;            // persistent per-wave rings (else grid of shared chunks)
-    int a, b;           // wp: RPL, TW;  ch: TW, ILP
+    bool wp;            // persistent per-wave tree slots (else grid of shared chunks)
+    int a, b, c;        // wp: RPL, TW, NTW;  ch: TW, ILP, -
     const void *kern;
     int rows_per_tile, threads;
     size_t lds;
 };
 
+// A per-wave-slot shape is instantiated for depth D only if its tree slots alone fit in LDS.
+template <int D, int RPL, int TW, int NTW>
+constexpr bool wp_fits() {
+    return D <= kMaxWpDepth && (size_t)TW * NTW * tree_stride_bytes(D) + 64 * RPL * 4 <= (size_t)kLdsBytes;
+}
+
 template <int D>
-const void *pick_wp(int rpl, int tw) {
-    if constexpr (D <= 8) {
-#define HARL_WP(R, T) \
-    if (rpl == R && tw == T) return reinterpret_cast<const void *>(k_tree_score_wp<D, R, T>);
-        HARL_WP(1, 4) HARL_WP(1, 8) HARL_WP(1, 16) HARL_WP(2, 4) HARL_WP(2, 8) HARL_WP(2, 12)
+const void *pick_wp(int rpl, int tw, int ntw) {
+#define HARL_WP(R, T, N)                                                                          \
+    if constexpr (wp_fits<D, R, T, N>())                                                          \
+        if (rpl == R && tw == T && ntw == N) return reinterpret_cast<const void *>(k_tree_score_wp<D, R, T, N>);
+    HARL_WP(2, 16, 1) HARL_WP(2, 12, 2) HARL_WP(2, 12, 1) HARL_WP(2, 8, 1) HARL_WP(2, 6, 1) HARL_WP(2, 4, 1)
+    HARL_WP(1, 16, 2) HARL_WP(1, 8, 1) HARL_WP(1, 4, 1)
 #undef HARL_WP
-    }
     return nullptr;
 }
 
@@ -394,42 +534,43 @@ const void *pick_ch(int tw, int ilp) {
 }
 
 template <int... Ds>
-const void *pick_depth(int depth, bool wp, int a, int b, std::integer_sequence<int, Ds...>) {
+const void *pick_depth(int depth, bool wp, int a, int b, int c, std::integer_sequence<int, Ds...>) {
     const void *k = nullptr;
-    ((depth == Ds + 1 ? (void)(k = wp ? pick_wp<Ds + 1>(a, b) : pick_ch<Ds + 1>(a, b)) : (void)0), ...);
+    ((depth == Ds + 1 ? (void)(k = wp ? pick_wp<Ds + 1>(a, b, c) : pick_ch<Ds + 1>(a, b)) : (void)0), ...);
     return k;
 }
 
-ScoreCfg make_cfg(const harl_ensemble *E, bool wp, int a, int b) {
-    ScoreCfg c{wp, a, b, pick_depth(E->depth, wp, a, b, std::make_integer_sequence<int, kMaxDepth>{}), 0, 0, 0};
+ScoreCfg make_cfg(const harl_ensemble *E, bool wp, int a, int b, int n) {
+    ScoreCfg c{wp, a, b, n, pick_depth(E->depth, wp, a, b, n, std::make_integer_sequence<int, kMaxDepth>{}), 0, 0, 0};
     const size_t stride = (size_t)E->tree_stride;
     if (wp) {
         c.rows_per_tile = 64 * a;
         c.threads = 64 * b;
-        const size_t ring = (size_t)b * 2 * stride, red = (size_t)b * c.rows_per_tile * 8;
-        c.lds = (size_t)E->n_features * c.rows_per_tile * 4 + (ring > red ? ring : red);
+        const size_t ring = (size_t)b * n * stride, red = (size_t)b * c.rows_per_tile * 8;
+        c.lds = (size_t)E->n_features * c.rows_per_tile * 4 + (ring > red ? ring : red) + 16;  // + NaN flags
     } else {
         c.rows_per_tile = 64;
         c.threads = 64 * a;
         const size_t chunk = (size_t)a * b * stride, red = (size_t)a * 64 * 8;
-        c.lds = (size_t)E->n_features * 64 * 4 + (chunk > red ? chunk : red);
+        c.lds = (size_t)E->n_features * 64 * 4 + (chunk > red ? chunk : red) + 16;  // + NaN flag
     }
     return c;
 }
 
-// Preferred shapes, best first; the first whose LDS fits is used.  HARL_SCORE_CFG="wp,RPL,TW" or
-// "ch,TW,ILP" puts a shape first (tuning sweeps).
+// Preferred shapes, best first; the first whose LDS fits is used.  HARL_SCORE_CFG="wp,RPL,TW,NTW"
+// or "ch,TW,ILP" puts a shape first (tuning sweeps).
 ScoreCfg choose_cfg(const harl_ensemble *E) {
     std::vector<ScoreCfg> cands;
     if (const char *env = std::getenv("HARL_SCORE_CFG")) {
         char kind[3] = {0, 0, 0};
-        int a = 0, b = 0;
-        if (std::sscanf(env, "%2[a-z],%d,%d", kind, &a, &b) == 3) cands.push_back(make_cfg(E, kind[0] == 'w', a, b));
+        int a = 0, b = 0, n = 1;
+        if (std::sscanf(env, "%2[a-z],%d,%d,%d", kind, &a, &b, &n) >= 3) cands.push_back(make_cfg(E, kind[0] == 'w', a, b, n));
     }
-    const int wp_pref[][2] = {{2, 12}, {1, 16}, {2, 8}, {2, 4}, {1, 8}, {1, 4}};
-    for (auto &p : wp_pref) cands.push_back(make_cfg(E, true, p[0], p[1]));
+    const int wp_pref[][3] = {{2, 16, 1}, {2, 12, 2}, {2, 12, 1}, {2, 8, 1}, {2, 6, 1}, {2, 4, 1},
+                              {1, 16, 2}, {1, 8, 1}, {1, 4, 1}};
+    for (auto &p : wp_pref) cands.push_back(make_cfg(E, true, p[0], p[1], p[2]));
     const int ch_pref[][2] = {{8, 1}, {4, 2}, {4, 1}, {2, 1}};
-    for (auto &p : ch_pref) cands.push_back(make_cfg(E, false, p[0], p[1]));
+    for (auto &p : ch_pref) cands.push_back(make_cfg(E, false, p[0], p[1], 1));
     for (const ScoreCfg &c : cands)
         if (c.kern && c.lds <= (size_t)kLdsBytes) return c;
     return cands.back();  // nothing fits: the launch reports HARL_E_UNSUPPORTED
@@ -460,7 +601,7 @@ WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
     w.V = tiles * E->n_trees;
     const int per_cu = (int)(kLdsBytes / c.lds) > 0 ? (int)(kLdsBytes / c.lds) : 1;
     int64_t nb = (int64_t)device_cus(E->device) * per_cu;
-    const int64_t min_l = 2LL * c.b;
+    const int64_t min_l = 2LL * c.b * c.c;
     if (ceil_div(w.V, nb) < min_l) nb = ceil_div(w.V, min_l);
     w.L = ceil_div(w.V, nb);
     w.nb = (int)ceil_div(w.V, w.L);
@@ -595,21 +736,22 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
         }
     }
     const int D = depth;
-    const int n_leaf = 1 << D;
+    const int M = 1 << D;
+    const uint32_t LL = tree_ll_bytes(D);
     const int stride = tree_stride_bytes(D);
     std::vector<uint8_t> host((size_t)T * stride, 0);
-    std::vector<int32_t> map(2 * (size_t)n_leaf);  // complete-tree slot (1-based) -> original node
+    std::vector<int32_t> map(2 * (size_t)M);      // complete-tree slot (1-based) -> original node
+    std::vector<uint32_t> code(M), thr_bits(M);   // per internal slot 1 .. M-1
+    auto put = [](uint8_t *dst, uint32_t w) { std::memcpy(dst, &w, 4); };
     for (int t = 0; t < T; ++t) {
         uint8_t *tb = host.data() + (size_t)t * stride;
-        uint32_t *words = reinterpret_cast<uint32_t *>(tb);
-        float *leaves = reinterpret_cast<float *>(tb + (size_t)n_leaf * 8);
         map[1] = d->root[t];
-        for (int s = 1; s < n_leaf; ++s) {
+        for (int s = 1; s < M; ++s) {
             const int32_t n = map[s];
-            uint32_t word = 0;
             float thr = 0.f;
+            code[s] = 0;
             if (d->feature[n] >= 0) {
-                word = (uint32_t)d->feature[n] | (d->default_left[n] ? kNodeDefaultLeft : 0u);
+                code[s] = (uint32_t)d->feature[n] | (d->default_left[n] ? kCodeDefaultLeft : 0u);
                 thr = d->threshold[n];
                 if (std::isnan(thr)) thr = -INFINITY;   // no value is < NaN: everything present goes right
                 map[2 * s] = d->left[n];
@@ -618,10 +760,20 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
                 map[2 * s] = n;
                 map[2 * s + 1] = n;
             }
-            words[2 * s] = word;
-            std::memcpy(&words[2 * s + 1], &thr, 4);
+            std::memcpy(&thr_bits[s], &thr, 4);
         }
-        for (int j = 0; j < n_leaf; ++j) leaves[j] = d->leaf_value[map[n_leaf + j]];
+        put(tb + 4, code[1]);
+        for (int s = 1; s < M / 2; ++s) {
+            put(tb + 8 * s, thr_bits[s]);
+            put(tb + 8 * s + 4, code[2 * s] | code[2 * s + 1] << 16);
+        }
+        for (int s = M / 2; s < M; ++s) {
+            uint8_t *rec = tb + LL + 16 * (s - M / 2);
+            const float l0 = d->leaf_value[map[2 * s]], l1 = d->leaf_value[map[2 * s + 1]];
+            put(rec, thr_bits[s]);
+            std::memcpy(rec + 4, &l0, 4);
+            std::memcpy(rec + 8, &l1, 4);
+        }
     }
     harl_ensemble *E = new (std::nothrow) harl_ensemble{};
     if (!E) return fail(HARL_E_NOMEM, "harl_ensemble_create: host allocation failed");
