@@ -4,17 +4,18 @@
 // v = wv . h2 + bv; action = lowest-index argmax of the logits; probs = softmax(logits).
 //
 // K4 k_policy: the three dense contractions run on MFMA, transposed so that states are the MFMA
-// N dimension (H^T = W X^T).  A workgroup holds 16*NSG states and 4 waves.
+// N dimension (H^T = W X^T).  A workgroup holds 16*NSG states and U waves; a wave computes its
+// share of each layer's 16-unit tiles in groups of TP tiles.
 //   phase 0  the states are staged into LDS ([state][unit], padded rows);
-//   phase 1  each wave computes a quarter of h1's 16-unit tiles for all states, two tiles at a
-//            time (A = W1 fragments streamed from global memory through a register ring, B =
+//   phase 1  each wave computes its 1/U of h1's tiles for all states, TP tiles at a time (A =
+//            W1 fragments streamed from global memory through a kRing-deep register ring, B =
 //            states from LDS, read one k-group ahead), applies bias + ReLU (+ bf16 rounding) and
 //            stores the tiles to LDS;
-//   phase 2  each wave computes a quarter of h2's tiles the same way (B = h1 from LDS; every A
+//   phase 2  each wave computes its 1/U of h2's tiles the same way (B = h1 from LDS; every A
 //            fragment feeds NSG state groups) and feeds each finished tile straight from its
 //            accumulator registers into the head contraction: the MFMA result layout of a tile is
 //            re-used as the B operand layout, with the head weights pre-permuted to match;
-//   phase 3  the four per-wave partial heads are summed in a fixed order; bias, argmax, softmax
+//   phase 3  the U per-wave partial heads are summed in a fixed order; bias, argmax, softmax
 //            and value are computed per state and written out.
 // fp32 policies use v_mfma_f32_16x16x4_f32, bf16 policies v_mfma_f32_16x16x32_bf16 (fp32
 // accumulation; h1, h2 rounded to bf16, nearest even).  Weights are pre-tiled at create time so
@@ -39,9 +40,9 @@
 namespace harl {
 namespace {
 
-constexpr int kU = 4;     // waves per workgroup
-constexpr int kRing = 4;  // weight fragment pairs in flight per wave
-constexpr int kMaxHT = 8; // head tiles: a + 1 <= 128 (kernels are instantiated for at most 2 or 8)
+constexpr int kMaxU = 8;      // waves per workgroup (at most)
+constexpr int kRing = 4;      // k-groups of weight fragments in flight per wave
+constexpr int kHiddenPad = 256;  // hidden widths padded to whole tile groups of every kernel shape
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -82,26 +83,33 @@ struct PolicyArgs {
 };
 
 // One dense layer for this wave: `n_tiles` output tiles of 16 units starting at tile `t0`, each a
-// sum over KG k-groups, computed two tiles at a time (two independent accumulator chains sharing
-// every B fragment).  A fragments come from `A` (packed [tile][g][lane] x 16 B) through a ring of
-// kRing register pairs; the B fragments of the next k-group are read from the LDS activation rows
-// `in` (row stride `in_stride` bytes) while the current k-group's MFMAs run.
-// done(first_tile, acc[2][NSG]) consumes each finished pair of tiles.
-template <bool BF16, int NSG, typename Done>
+// sum over KG k-groups (KG a multiple of RING), computed TP tiles at a time (TP independent
+// accumulator chains sharing every B fragment).  The wave's iterations (tile group, k-group) run
+// in order; the A fragments of iteration it + RING are loaded from `A` (packed [tile][g][lane] x
+// 16 B) into ring slot it % RING as soon as iteration it has issued its MFMAs, and the B
+// fragments of the next k-group are read from the LDS activation rows `in` (row stride
+// `in_stride` bytes) into the other half of a double buffer.  done(first_tile, acc[TP][NSG])
+// consumes each finished group.
+template <bool BF16, int NSG, int TP, int RING, typename Done>
 __device__ __forceinline__ void dense_layer(const uint4 *__restrict__ A, int t0, int n_tiles, int KG, const char *in,
                                             int in_stride, int ln, int lq, int l, Done done) {
-    const int NIT = (n_tiles / 2) * KG;
+    static_assert(RING % 2 == 0, "the B double buffer alternates with the ring slot");
+    const int n_groups = n_tiles / TP;
+    const int NIT = n_groups * KG;
     const int64_t tstride = (int64_t)KG * 64;  // uint4 between the same k-group of consecutive tiles
-    auto a_ptr = [&](int it) { return A + (int64_t)(t0 + 2 * (it / KG)) * tstride + (int64_t)(it % KG) * 64 + l; };
-    uint4 ring[kRing][2];
+    auto a_src = [&](int it) {
+        return A + (int64_t)(t0 + TP * (it / KG)) * tstride + (int64_t)(it % KG) * 64 + l;
+    };
+    uint4 ring[RING][TP];
 #pragma unroll
-    for (int r = 0; r < kRing; ++r) {
+    for (int r = 0; r < RING; ++r) {
         if (r < NIT) {
-            const uint4 *ap = a_ptr(r);
-            ring[r][0] = ap[0];
-            ring[r][1] = ap[tstride];
+            const uint4 *src = a_src(r);
+#pragma unroll
+            for (int j = 0; j < TP; ++j) ring[r][j] = src[j * tstride];
         } else {
-            ring[r][0] = ring[r][1] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int j = 0; j < TP; ++j) ring[r][j] = make_uint4(0, 0, 0, 0);
         }
     }
     auto b_load = [&](int g, uint4 (&b)[NSG]) {
@@ -109,54 +117,42 @@ __device__ __forceinline__ void dense_layer(const uint4 *__restrict__ A, int t0,
         for (int sg = 0; sg < NSG; ++sg)
             b[sg] = *reinterpret_cast<const uint4 *>(in + (sg * 16 + ln) * in_stride + g * 64 + lq * 16);
     };
-    f32x4 acc[2][NSG];
+    uint4 b[2][NSG];
+    b_load(0, b[0]);
+    for (int grp = 0; grp < n_groups; ++grp) {
+        f32x4 acc[TP][NSG];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < TP; ++h)
 #pragma unroll
-        for (int sg = 0; sg < NSG; ++sg) acc[h][sg] = f32x4{0, 0, 0, 0};
-    uint4 bcur[NSG];
-    b_load(0, bcur);
-    int g = 0, tile = t0;
-    for (int it0 = 0; it0 < NIT; it0 += kRing) {
+            for (int sg = 0; sg < NSG; ++sg) acc[h][sg] = f32x4{0, 0, 0, 0};
+        for (int g0 = 0; g0 < KG; g0 += RING) {
 #pragma unroll
-        for (int r = 0; r < kRing; ++r) {
-            const int it = it0 + r;
-            if (it < NIT) {
-                const uint4 a0 = ring[r][0], a1 = ring[r][1];
-                if (it + kRing < NIT) {
-                    const uint4 *ap = a_ptr(it + kRing);
-                    ring[r][0] = ap[0];
-                    ring[r][1] = ap[tstride];
-                }
-                uint4 bnext[NSG];
-                const int gn = g + 1 == KG ? 0 : g + 1;
-                if (it + 1 < NIT) b_load(gn, bnext);
+            for (int r = 0; r < RING; ++r) {
+                const int g = g0 + r;
+                const int it = grp * KG + g;
+                if (it + 1 < NIT) b_load(g + 1 == KG ? 0 : g + 1, b[(r + 1) & 1]);
 #pragma unroll
-                for (int sg = 0; sg < NSG; ++sg) {
-                    mfma_group<BF16>(a0, bcur[sg], acc[0][sg]);
-                    mfma_group<BF16>(a1, bcur[sg], acc[1][sg]);
-                }
+                for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
-                for (int sg = 0; sg < NSG; ++sg) bcur[sg] = bnext[sg];
-                if (++g == KG) {
-                    done(tile, acc);
+                    for (int j = 0; j < TP; ++j) mfma_group<BF16>(ring[r][j], b[r & 1][sg], acc[j][sg]);
+                if (it + RING < NIT) {
+                    const uint4 *src = a_src(it + RING);
 #pragma unroll
-                    for (int h = 0; h < 2; ++h)
-#pragma unroll
-                        for (int sg = 0; sg < NSG; ++sg) acc[h][sg] = f32x4{0, 0, 0, 0};
-                    g = 0;
-                    tile += 2;
+                    for (int j = 0; j < TP; ++j) ring[r][j] = src[j * tstride];
                 }
             }
         }
+        done(t0 + grp * TP, acc);
     }
 }
 
-template <bool BF16, int NSG, int HTM>
-__global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
+// U waves per workgroup, 16*NSG states; HTM >= head tiles; layers in groups of TP tiles per wave.
+template <bool BF16, int NSG, int HTM, int U, int TP, int RING>
+__global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     extern __shared__ __align__(16) char smem[];
     constexpr int EL = BF16 ? 2 : 4;        // bytes per activation element
     constexpr int UPG = BF16 ? 32 : 16;     // input units per k-group
+    constexpr int NTH = 64 * U;
     const int wid = threadIdx.x / 64, l = threadIdx.x % 64;
     const int ln = l % 16, lq = l / 16;
     const int s0 = blockIdx.x * 16 * NSG;
@@ -170,7 +166,7 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
     // ---------------- phase 0: states -> LDS [state][unit] (zero beyond S and B) ----------------
     {
         const int row_elems = p.sp;
-        for (int e = threadIdx.x; e < NS * row_elems; e += 256) {
+        for (int e = threadIdx.x; e < NS * row_elems; e += NTH) {
             const int r = e / row_elems, c = e % row_elems;
             const int st = s0 + r;
             if constexpr (BF16) {
@@ -186,97 +182,102 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
     }
     __syncthreads();
 
-    // ---------------- phase 1: h1 = act(W1 s + b1), this wave's quarter of the tiles ----------------
+    // ---------------- phase 1: h1 = act(W1 s + b1), this wave's share of the tiles ----------------
     {
-        const int mt_per = p.h1p / 16 / kU;
-        dense_layer<BF16, NSG>(p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
-                               [&](int mt0, f32x4 (&acc)[2][NSG]) {
+        const int mt_per = p.h1p / 16 / U;
+        dense_layer<BF16, NSG, TP, RING>(p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
+                                         [&](int mt0, f32x4 (&acc)[TP][NSG]) {
 #pragma unroll
-                                   for (int h = 0; h < 2; ++h) {
-                                       const int u0 = (mt0 + h) * 16 + lq * 4;
+                                             for (int h = 0; h < TP; ++h) {
+                                                 const int u0 = (mt0 + h) * 16 + lq * 4;
 #pragma unroll
-                                       for (int sg = 0; sg < NSG; ++sg) {
-                                           float v[4];
+                                                 for (int sg = 0; sg < NSG; ++sg) {
+                                                     float v[4];
 #pragma unroll
-                                           for (int i = 0; i < 4; ++i) v[i] = fmaxf(acc[h][sg][i] + p.b1[u0 + i], 0.f);
-                                           char *dst = h1 + (sg * 16 + ln) * h1_stride + u0 * EL;
-                                           if constexpr (BF16) {
-                                               *reinterpret_cast<uint2 *>(dst) = make_uint2(bf16_rne(v[0]) | (bf16_rne(v[1]) << 16),
-                                                                                           bf16_rne(v[2]) | (bf16_rne(v[3]) << 16));
-                                           } else {
-                                               *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-                                           }
-                                       }
-                                   }
-                               });
+                                                     for (int i = 0; i < 4; ++i) v[i] = fmaxf(acc[h][sg][i] + p.b1[u0 + i], 0.f);
+                                                     char *dst = h1 + (sg * 16 + ln) * h1_stride + u0 * EL;
+                                                     if constexpr (BF16) {
+                                                         *reinterpret_cast<uint2 *>(dst) =
+                                                             make_uint2(bf16_rne(v[0]) | (bf16_rne(v[1]) << 16),
+                                                                        bf16_rne(v[2]) | (bf16_rne(v[3]) << 16));
+                                                     } else {
+                                                         *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+                                                     }
+                                                 }
+                                             }
+                                         });
     }
     __syncthreads();
 
-    // ------- phase 2: h2 tile pairs of this wave, chained into the partial heads (registers) -------
+    // ------- phase 2: h2 tile groups of this wave, chained into the partial heads (registers) -------
     f32x4 hacc[NSG][HTM];
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
         for (int ht = 0; ht < HTM; ++ht) hacc[sg][ht] = f32x4{0, 0, 0, 0};
     {
-        const int mt_per = p.h2p / 16 / kU;
+        const int mt_per = p.h2p / 16 / U;
         const int mt_first = wid * mt_per;
-        // head fragments: fp32 one k-group per h2 tile (2 per pair), bf16 one per pair of tiles
+        // head fragments: fp32 one k-group per h2 tile, bf16 one per pair of tiles
         const int HKG = BF16 ? p.h2p / 32 : p.h2p / 16;
-        constexpr int HPP = BF16 ? 1 : 2;  // head k-groups per tile pair
-        uint4 hpf[HPP][HTM];
-        auto head_fetch = [&](int pair) {
+        constexpr int HPG = BF16 ? TP / 2 : TP;  // head k-groups per group of TP tiles
+        uint4 hpf[HPG][HTM];
+        auto head_fetch = [&](int tile) {
+            const int hk0 = BF16 ? tile / 2 : tile;
 #pragma unroll
-            for (int q = 0; q < HPP; ++q)
+            for (int q = 0; q < HPG; ++q)
 #pragma unroll
                 for (int ht = 0; ht < HTM; ++ht) {
-                    const int hk = pair * HPP + q;
+                    const int hk = hk0 + q;
                     if (ht < HT && hk < HKG) hpf[q][ht] = p.wh[((int64_t)ht * HKG + hk) * 64 + l];
                 }
         };
-        head_fetch(mt_first / 2);
-        dense_layer<BF16, NSG>(p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l,
-                               [&](int mt0, f32x4 (&acc)[2][NSG]) {
-                                   float bias[2][4];
+        head_fetch(mt_first);
+        dense_layer<BF16, NSG, TP, RING>(
+            p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l, [&](int mt0, f32x4 (&acc)[TP][NSG]) {
+                float bias[TP][4];
 #pragma unroll
-                                   for (int h = 0; h < 2; ++h)
+                for (int h = 0; h < TP; ++h)
 #pragma unroll
-                                       for (int i = 0; i < 4; ++i) bias[h][i] = p.b2[(mt0 + h) * 16 + lq * 4 + i];
+                    for (int i = 0; i < 4; ++i) bias[h][i] = p.b2[(mt0 + h) * 16 + lq * 4 + i];
 #pragma unroll
-                                   for (int sg = 0; sg < NSG; ++sg) {
-                                       float v[2][4];
+                for (int sg = 0; sg < NSG; ++sg) {
+                    float v[TP][4];
 #pragma unroll
-                                       for (int h = 0; h < 2; ++h)
+                    for (int h = 0; h < TP; ++h)
 #pragma unroll
-                                           for (int i = 0; i < 4; ++i) v[h][i] = fmaxf(acc[h][sg][i] + bias[h][i], 0.f);
-                                       if constexpr (BF16) {
-                                           // slots 0..3: tile mt0, slots 4..7: tile mt0 + 1 (accumulator layout)
-                                           uint4 bv;
-                                           bv.x = bf16_rne(v[0][0]) | (bf16_rne(v[0][1]) << 16);
-                                           bv.y = bf16_rne(v[0][2]) | (bf16_rne(v[0][3]) << 16);
-                                           bv.z = bf16_rne(v[1][0]) | (bf16_rne(v[1][1]) << 16);
-                                           bv.w = bf16_rne(v[1][2]) | (bf16_rne(v[1][3]) << 16);
+                        for (int i = 0; i < 4; ++i) v[h][i] = fmaxf(acc[h][sg][i] + bias[h][i], 0.f);
+                    if constexpr (BF16) {
+                        // head k-group of tiles (2q, 2q+1): slots 0..3 tile 2q, 4..7 tile 2q+1 (accumulator layout)
 #pragma unroll
-                                           for (int ht = 0; ht < HTM; ++ht)
-                                               if (ht < HT) mfma_group<true>(hpf[0][ht], bv, hacc[sg][ht]);
-                                       } else {
+                        for (int q = 0; q < HPG; ++q) {
+                            uint4 bv;
+                            bv.x = bf16_rne(v[2 * q][0]) | (bf16_rne(v[2 * q][1]) << 16);
+                            bv.y = bf16_rne(v[2 * q][2]) | (bf16_rne(v[2 * q][3]) << 16);
+                            bv.z = bf16_rne(v[2 * q + 1][0]) | (bf16_rne(v[2 * q + 1][1]) << 16);
+                            bv.w = bf16_rne(v[2 * q + 1][2]) | (bf16_rne(v[2 * q + 1][3]) << 16);
 #pragma unroll
-                                           for (int h = 0; h < 2; ++h) {
-                                               const uint4 bv = make_uint4(__float_as_uint(v[h][0]), __float_as_uint(v[h][1]),
-                                                                           __float_as_uint(v[h][2]), __float_as_uint(v[h][3]));
+                            for (int ht = 0; ht < HTM; ++ht)
+                                if (ht < HT) mfma_group<true>(hpf[q][ht], bv, hacc[sg][ht]);
+                        }
+                    } else {
 #pragma unroll
-                                               for (int ht = 0; ht < HTM; ++ht)
-                                                   if (ht < HT) mfma_group<false>(hpf[h][ht], bv, hacc[sg][ht]);
-                                           }
-                                       }
-                                   }
-                                   head_fetch(mt0 / 2 + 1);
-                               });
+                        for (int h = 0; h < TP; ++h) {
+                            const uint4 bv = make_uint4(__float_as_uint(v[h][0]), __float_as_uint(v[h][1]),
+                                                        __float_as_uint(v[h][2]), __float_as_uint(v[h][3]));
+#pragma unroll
+                            for (int ht = 0; ht < HTM; ++ht)
+                                if (ht < HT) mfma_group<false>(hpf[h][ht], bv, hacc[sg][ht]);
+                        }
+                    }
+                }
+                head_fetch(mt0 + TP);
+            });
     }
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
 
-    // ---------------- phase 3: fixed-order sum of the 4 partial heads, epilogue ----------------
-    float *part = reinterpret_cast<float *>(smem);  // [kU][NSG][hap][16]
+    // ---------------- phase 3: fixed-order sum of the U partial heads, epilogue ----------------
+    float *part = reinterpret_cast<float *>(smem);  // [U][NSG][hap][16]
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
                 for (int i = 0; i < 4; ++i)
                     part[(((int64_t)wid * NSG + sg) * p.hap + ht * 16 + lq * 4 + i) * 16 + ln] = hacc[sg][ht][i];
     __syncthreads();
-    for (int sg = wid; sg < NSG; sg += kU) {
+    for (int sg = wid; sg < NSG; sg += U) {
         const int st = s0 + sg * 16 + ln;
         float best = -INFINITY;
         int best_i = 0x7FFFFFFF;
@@ -301,7 +302,7 @@ __global__ __launch_bounds__(256) void k_policy(PolicyArgs p) {
                 const int row = ht * 16 + lq * 4 + i;
                 float s = 0.f;
 #pragma unroll
-                for (int w = 0; w < kU; ++w) s += part[(((int64_t)w * NSG + sg) * p.hap + row) * 16 + ln];
+                for (int w = 0; w < U; ++w) s += part[(((int64_t)w * NSG + sg) * p.hap + row) * 16 + ln];
                 s += p.bh[row];
                 z[ht][i] = s;
                 if (row < p.a && (s > best || (s == best && row < best_i))) {
@@ -389,12 +390,12 @@ int upload(const std::vector<T> &h, void **d, hipStream_t stream) {
     return HARL_OK;
 }
 
-size_t policy_lds_bytes(const harl_policy *P, int nsg) {
+size_t policy_lds_bytes(const harl_policy *P, int nsg, int u) {
     const bool bf = P->dtype == HARL_BF16;
     const size_t el = bf ? 2 : 4;
     const size_t ns = 16 * (size_t)nsg;
     const size_t acts = ns * (P->sp * el + 16) + ns * (P->h1p * el + 16);
-    const size_t part = (size_t)kU * nsg * P->hap * 16 * 4;
+    const size_t part = (size_t)u * nsg * P->hap * 16 * 4;
     return acts > part ? acts : part;
 }
 
@@ -408,9 +409,9 @@ int pack_policy(const harl_policy_desc *d, harl_policy **out, hipStream_t stream
         return fail(HARL_E_INVALID_ARG, "harl_policy_create: null weight or bias");
     const bool bf = d->dtype == HARL_BF16;
     const int UPG = bf ? 32 : 16;
-    const int sp = (int)round_up(d->s, UPG);
-    const int h1p = (int)round_up(d->h1, 32 * kU);   // whole tile pairs per wave, whole k-groups
-    const int h2p = (int)round_up(d->h2, 32 * kU);
+    const int sp = (int)round_up(d->s, UPG * kRing);   // whole rings of k-groups
+    const int h1p = (int)round_up(d->h1, kHiddenPad);   // whole tile groups per wave, whole k-groups
+    const int h2p = (int)round_up(d->h2, kHiddenPad);
     const int hap = (int)round_up(d->a + 1, 16);
     // heads as one matrix [a+1][h2]: rows 0..a-1 actor, row a value
     const size_t esz = bf ? 2 : 4;
@@ -446,7 +447,7 @@ int pack_policy(const harl_policy_desc *d, harl_policy **out, hipStream_t stream
     P->s = d->s; P->h1 = d->h1; P->h2 = d->h2; P->a = d->a;
     P->sp = sp; P->h1p = h1p; P->h2p = h2p; P->hap = hap;
     (void)hipGetDevice(&P->device);
-    if (policy_lds_bytes(P, 1) > 160 * 1024) {
+    if (policy_lds_bytes(P, 1, kMaxU) > 160 * 1024) {
         delete P;
         return fail(HARL_E_UNSUPPORTED, "harl_policy_create: layers too wide for the LDS-resident activations");
     }
@@ -485,22 +486,28 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     a.b1 = P->d_b1; a.b2 = P->d_b2; a.bh = P->d_bh;
     a.action = action; a.value = value; a.probs = probs; a.logits = logits;
     const bool bf = P->dtype == HARL_BF16;
-    // large bf16 batches share every weight fragment among 4 state groups (64 states per block)
+    // Large bf16 batches: 64 states per workgroup share every weight fragment (4 state groups), 4
+    // waves of 4-tile groups with deep weight prefetch.  Otherwise 16 states per workgroup and 8
+    // waves, so that a small batch still spreads over every CU.
     int nsg = (bf && B >= 16 * 1024) ? 4 : 1;
-    if (policy_lds_bytes(P, nsg) > 160 * 1024) nsg = 1;
-    const size_t lds = policy_lds_bytes(P, nsg);
+    if (policy_lds_bytes(P, nsg, 4) > 160 * 1024) nsg = 1;
+    const int u = nsg == 4 ? 4 : 8;
+    const size_t lds = policy_lds_bytes(P, nsg, u);
     const unsigned grid = (unsigned)ceil_div(B, 16 * nsg);
-    const int htm = P->hap / 16 <= 2 ? 2 : 8;
+    const int ht = P->hap / 16;
+    const int htm = ht <= 2 ? 2 : ht <= 5 ? 5 : 8;
     const void *kern = nullptr;
-#define HARL_POL(BF, NSG, HTM) \
-    if (bf == BF && nsg == NSG && htm == HTM) kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM>);
-    HARL_POL(false, 1, 2) HARL_POL(false, 1, 8) HARL_POL(true, 1, 2) HARL_POL(true, 1, 8) HARL_POL(true, 4, 2)
-    HARL_POL(true, 4, 8)
+#define HARL_POL(BF, NSG, HTM, U, TP)                  \
+    if (bf == BF && nsg == NSG && htm == HTM && u == U) \
+        kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM, U, TP, kRing>);
+    HARL_POL(false, 1, 2, 8, 2) HARL_POL(false, 1, 5, 8, 2) HARL_POL(false, 1, 8, 8, 2)
+    HARL_POL(true, 1, 2, 8, 2) HARL_POL(true, 1, 5, 8, 2) HARL_POL(true, 1, 8, 8, 2)
+    HARL_POL(true, 4, 2, 4, 4) HARL_POL(true, 4, 5, 4, 4) HARL_POL(true, 4, 8, 4, 4)
 #undef HARL_POL
     if (!kern) return fail(HARL_E_UNSUPPORTED, "harl_policy_step: no kernel for this policy shape");
     if (const int rc = ensure_dynamic_lds(kern, lds)) return rc;
     void *args[] = {&a};
-    HARL_HIP_CHECK(hipLaunchKernel(kern, dim3(grid), dim3(256), args, lds, stream));
+    HARL_HIP_CHECK(hipLaunchKernel(kern, dim3(grid), dim3(64 * u), args, lds, stream));
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
 }

@@ -39,6 +39,7 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kLdsBytes = 160 * 1024;
 constexpr int kMaxWpDepth = 10;  // deeper trees (up to 48 KB each) use the shared-chunk kernel
+constexpr int kRegTileFeatures = 192;  // features per row of a register-prefetched tile
 
 // Packed tree of D split levels (M = 2^D leaves), nodes numbered breadth-first from 1:
 //   bytes 0..7      record 0: {0, code(1)} -- the root's feature code
@@ -49,7 +50,8 @@ constexpr int kMaxWpDepth = 10;  // deeper trees (up to 48 KB each) use the shar
 // (threshold + both children's codes, 8 bytes) -- both addresses are known when the level starts,
 // so a level is one LDS round trip of 12 bytes -- and the last level reads its threshold and both
 // leaves in one 16-byte record.  The first 16 bytes {0, code(1), threshold(1), codes(2, 3)} are
-// the same for every row, so the walk takes them as wave-uniform values.
+// the same for every row, so the walk takes them as wave-uniform values, and it picks the record
+// of node 2 or 3 (the next 16 bytes) in registers: the first LDS record read is at level 2.
 constexpr uint32_t tree_ll_bytes(int D) { return (4u << D) > 16u ? (4u << D) : 16u; }
 constexpr int tree_stride_bytes(int D) { return (int)((tree_ll_bytes(D) + (8u << D) + 15u) / 16u * 16u); }
 constexpr uint32_t kCodeDefaultLeft = 0x8000u;
@@ -63,9 +65,11 @@ __device__ __forceinline__ uint32_t go_right(float x, float thr, uint32_t code) 
     return left ? 0u : 1u;
 }
 
-// Wave-uniform head of a packed tree (its first 16 bytes).
+// Wave-uniform head of a packed tree: its first 32 bytes (root code, root record, and for depth
+// >= 3 the records of nodes 2 and 3, which the walk then selects in registers instead of reading).
 struct TreeHead {
     uint32_t code, thr, pair;
+    uint32_t thr2, pair2, thr3, pair3;
 };
 
 // An opaque VGPR copy of a wave-uniform value, so that one v_cndmask can pick between two of
@@ -117,13 +121,19 @@ __device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const Tree
     constexpr int NC = NT_ * R;
     constexpr uint32_t W = NAN_AWARE ? 16u : 15u;
     constexpr uint32_t kLast = tree_ll_bytes(D) - (8u << D);  // last-level record = 2 * rec(i) - tb + kLast
-    uint32_t c_left[NT_], c_right[NT_], c_root_l[NT_], c_root_r[NT_];
+    uint32_t c_left[NT_], c_right[NT_], c_root_l[NT_], c_root_r[NT_], l1_thr[NT_][2], l1_pair[NT_][2];
 #pragma unroll
     for (int i = 0; i < NT_; ++i) {
         c_left[i] = in_vgpr(0u - tb[i]);
         c_right[i] = in_vgpr(8u - tb[i]);
         c_root_l[i] = in_vgpr(tb[i] + 16u);
         c_root_r[i] = in_vgpr(tb[i] + 24u);
+        if constexpr (D > 2) {
+            l1_thr[i][0] = in_vgpr(hd[i].thr2);
+            l1_pair[i][0] = in_vgpr(hd[i].pair2);
+            l1_thr[i][1] = in_vgpr(hd[i].thr3);
+            l1_pair[i][1] = in_vgpr(hd[i].pair3);
+        }
     }
     float x[NC];
     uint32_t a[NC], code[NC];
@@ -145,7 +155,7 @@ __device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const Tree
             code[c] = __builtin_amdgcn_ubfe(hd[i].pair, sh, W);
             x[c] = feature_at<RT4>(NAN_AWARE ? __builtin_amdgcn_ubfe(hd[i].pair, sh, 15u) : code[c], lane_off[c % R]);
             if constexpr (D > 2)
-                rec[c] = lds_ld<uint2>(a[c]);
+                rec[c] = make_uint2(g ? l1_thr[i][1] : l1_thr[i][0], g ? l1_pair[i][1] : l1_pair[i][0]);
             else
                 lv[c] = lds_ld<uint4>(2u * a[c] - tb[i] + kLast);
             __builtin_amdgcn_sched_barrier(0);
@@ -178,15 +188,38 @@ __device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const Tree
     }
 }
 
-// Stage rows [row0, row0 + RT) of every feature into LDS ([F][RT] fp32, zero past n_rows), with
-// 8 loads in flight per thread; returns (block-wide) whether any staged value is NaN.  `flag` is
-// an LDS word that is 0 on entry (ordered before this call by a barrier); threads that see a NaN
-// set it, and the barrier at the end publishes it.
+// Item i of a row tile ([F][RT] fp32 in LDS, RT/4 float4 per feature): rows row0 + 4*(i % V) ..
+// + 3 of feature i / V, zero past n_rows.
+template <int V>
+__device__ __forceinline__ float4 tile_item(const float *__restrict__ X, int64_t ld, int n_rows, int vec_ok, int row0,
+                                            int i) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int f = i / V, r = row0 + 4 * (i % V);
+    const float *src = X + (int64_t)f * ld + r;
+    if (vec_ok && r + 3 < n_rows) {
+        v = *reinterpret_cast<const float4 *>(src);
+    } else {
+        if (r + 0 < n_rows) v.x = src[0];
+        if (r + 1 < n_rows) v.y = src[1];
+        if (r + 2 < n_rows) v.z = src[2];
+        if (r + 3 < n_rows) v.w = src[3];
+    }
+    return v;
+}
+
+__device__ __forceinline__ int any_nan(float4 v) {
+    return (v.x != v.x) | (v.y != v.y) | (v.z != v.z) | (v.w != v.w);
+}
+
+// Stage rows [row0, row0 + RT) of every feature into LDS, with 4 loads in flight per thread;
+// returns (block-wide) whether any staged value is NaN.  `flag` is an LDS word that is 0 on entry
+// (ordered before this call by a barrier); threads that see a NaN set it, and the barrier at the
+// end publishes it.
 template <int RT, int NT>
 __device__ __forceinline__ int stage_features(char *smem, const float *__restrict__ X, int64_t ld, int n_rows, int F,
                                               int vec_ok, int row0, volatile int *flag) {
     constexpr int V = RT / 4;  // float4 per feature row of the tile
-    constexpr int B = 8;
+    constexpr int B = 4;
     int has_nan = 0;
     const int total = F * V;
     float4 *dst = reinterpret_cast<float4 *>(smem);
@@ -195,25 +228,13 @@ __device__ __forceinline__ int stage_features(char *smem, const float *__restric
 #pragma unroll
         for (int j = 0; j < B; ++j) {
             const int i = i0 + j * NT;
-            v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (i < total) {
-                const int f = i / V, r = row0 + 4 * (i % V);
-                const float *src = X + (int64_t)f * ld + r;
-                if (vec_ok && r + 3 < n_rows) {
-                    v[j] = *reinterpret_cast<const float4 *>(src);
-                } else {
-                    if (r + 0 < n_rows) v[j].x = src[0];
-                    if (r + 1 < n_rows) v[j].y = src[1];
-                    if (r + 2 < n_rows) v[j].z = src[2];
-                    if (r + 3 < n_rows) v[j].w = src[3];
-                }
-            }
+            v[j] = i < total ? tile_item<V>(X, ld, n_rows, vec_ok, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
         for (int j = 0; j < B; ++j) {
             const int i = i0 + j * NT;
             if (i < total) {
-                has_nan |= (v[j].x != v[j].x) | (v[j].y != v[j].y) | (v[j].z != v[j].z) | (v[j].w != v[j].w);
+                has_nan |= any_nan(v[j]);
                 dst[i] = v[j];
             }
         }
@@ -223,22 +244,63 @@ __device__ __forceinline__ int stage_features(char *smem, const float *__restric
     return *flag;
 }
 
-// Fixed-order combination of the per-wave row sums (acc[r] of wave w for tile row r*64 + lane),
-// written as fp32 partials out[t] for tile rows t with row0 + t < n_rows.  `red` must not overlap
-// live data.
-template <int RPL, int NW>
-__device__ __forceinline__ void reduce_rows(double *red, const double (&acc)[RPL], int wid, int lane, int row0, int n_rows,
-                                            float *__restrict__ out) {
-    constexpr int RT = 64 * RPL;
+// Register prefetch of a whole row tile (used when F * RT/4 <= NPF * NT): thread t holds items
+// t + j*NT.  The commit writes them to LDS and sets `flag` if any is NaN; the caller's next barrier
+// publishes both.
+template <int RT, int NT, int NPF>
+__device__ __forceinline__ void tile_fetch(float4 (&xf)[NPF], const float *__restrict__ X, int64_t ld, int n_rows,
+                                           int F, int vec_ok, int row0) {
+    constexpr int V = RT / 4;
+    const int total = F * V;
 #pragma unroll
-    for (int r = 0; r < RPL; ++r) red[wid * RT + r * 64 + lane] = acc[r];
-    __syncthreads();
+    for (int j = 0; j < NPF; ++j) {
+        const int i = threadIdx.x + j * NT;
+        xf[j] = i < total ? tile_item<V>(X, ld, n_rows, vec_ok, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+}
+
+template <int RT, int NT, int NPF>
+__device__ __forceinline__ void tile_commit(const float4 (&xf)[NPF], char *smem, int F, volatile int *flag) {
+    const int total = F * (RT / 4);
+    float4 *dst = reinterpret_cast<float4 *>(smem);
+    int has_nan = 0;
+#pragma unroll
+    for (int j = 0; j < NPF; ++j) {
+        const int i = threadIdx.x + j * NT;
+        if (i < total) {
+            has_nan |= any_nan(xf[j]);
+            dst[i] = xf[j];
+        }
+    }
+    if (has_nan) *flag = 1;
+}
+
+// Fixed-order combination of the per-wave row sums (acc[r] of wave w for tile row r*64 + lane):
+// reduce_put stores them to `red`; after a barrier, reduce_sum writes the fp32 partials out[t] for
+// tile rows t with row0 + t < n_rows.  `red` must not overlap live data.
+template <int RPL>
+__device__ __forceinline__ void reduce_put(double *red, const double (&acc)[RPL], int wid, int lane) {
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) red[wid * 64 * RPL + r * 64 + lane] = acc[r];
+}
+
+template <int RPL, int NW>
+__device__ __forceinline__ void reduce_sum(const double *red, int row0, int n_rows, float *__restrict__ out) {
+    constexpr int RT = 64 * RPL;
     for (int t = threadIdx.x; t < RT; t += NW * kWave) {
         double s = 0.0;
 #pragma unroll
         for (int w = 0; w < NW; ++w) s += red[w * RT + t];
         if (row0 + t < n_rows) out[t] = (float)s;
     }
+}
+
+template <int RPL, int NW>
+__device__ __forceinline__ void reduce_rows(double *red, const double (&acc)[RPL], int wid, int lane, int row0, int n_rows,
+                                            float *__restrict__ out) {
+    reduce_put<RPL>(red, acc, wid, lane);
+    __syncthreads();
+    reduce_sum<RPL, NW>(red, row0, n_rows, out);
 }
 
 // Per-wave tree staging: lane l moves uint4 j*64 + l of a packed tree (S16 uint4 in all).
@@ -257,7 +319,7 @@ __device__ __forceinline__ void wave_commit(const uint4 (&pf)[PF], uint4 *dst, i
 }
 
 // Trees t + j*TW (j < NTW, t + j*TW < t_end) of a wave: fetch into registers, commit to the wave's
-// LDS slots (slot j) and take their wave-uniform heads (lane 0 holds each tree's first uint4).
+// LDS slots (slot j) and take their wave-uniform heads (lane l holds uint4 l of each tree).
 template <int S16, int PF, int NTW, int TW>
 __device__ __forceinline__ void group_fetch(uint4 (&pf)[NTW][PF], const uint4 *__restrict__ trees, int t, int t_end,
                                             int lane) {
@@ -273,9 +335,13 @@ __device__ __forceinline__ void group_commit(const uint4 (&pf)[NTW][PF], char *s
     for (int j = 0; j < NTW; ++j)
         if (t + j * TW < t_end) {
             wave_commit<S16>(pf[j], reinterpret_cast<uint4 *>(slots + (uint32_t)j * (S16 * 16)), lane);
-            hd[j].code = __builtin_amdgcn_readfirstlane(pf[j][0].y);
-            hd[j].thr = __builtin_amdgcn_readfirstlane(pf[j][0].z);
-            hd[j].pair = __builtin_amdgcn_readfirstlane(pf[j][0].w);
+            hd[j].code = __builtin_amdgcn_readlane(pf[j][0].y, 0);
+            hd[j].thr = __builtin_amdgcn_readlane(pf[j][0].z, 0);
+            hd[j].pair = __builtin_amdgcn_readlane(pf[j][0].w, 0);
+            hd[j].thr2 = __builtin_amdgcn_readlane(pf[j][0].x, 1);
+            hd[j].pair2 = __builtin_amdgcn_readlane(pf[j][0].y, 1);
+            hd[j].thr3 = __builtin_amdgcn_readlane(pf[j][0].z, 1);
+            hd[j].pair3 = __builtin_amdgcn_readlane(pf[j][0].w, 1);
         }
 }
 
@@ -305,13 +371,14 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     const uint32_t ring_off = (uint32_t)F * RT * 4u;
     const uint32_t slot0 = ring_off + (uint32_t)wid * NTW * (S16 * 16);
     char *const slots = smem + slot0;
-    // two NaN flags past the slot / reduction region, alternating between pieces: the flag of the
-    // next piece is cleared by thread 0 once the current one has been read by every thread
+    // four words past the slot / reduction region: two NaN flags and two tree-progress counters,
+    // alternating between pieces; thread 0 clears the next piece's pair once every thread is done
+    // with its previous use
     constexpr uint32_t kSlots = (uint32_t)TW * NTW * S16 * 16, kRed = (uint32_t)TW * RT * 8;
     volatile int *const flags = reinterpret_cast<volatile int *>(smem + ring_off + (kSlots > kRed ? kSlots : kRed));
-    if (threadIdx.x == 0) flags[0] = flags[1] = 0;
+    unsigned int *const progress = const_cast<unsigned int *>(reinterpret_cast<volatile unsigned int *>(flags)) + 2;
+    if (threadIdx.x == 0) flags[0] = flags[1] = flags[2] = flags[3] = 0;
     __syncthreads();
-    int piece = 0;
 
     uint4 pf[NTW][PF];
 #pragma unroll
@@ -320,11 +387,24 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
         for (int k = 0; k < PF; ++k) pf[j][k] = make_uint4(0, 0, 0, 0);
     TreeHead hd[NTW];
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) hd[j] = TreeHead{0, 0, 0};
+    for (int j = 0; j < NTW; ++j) hd[j] = TreeHead{0, 0, 0, 0, 0, 0, 0};
     const uint32_t base = lds_addr(smem);
     uint32_t lane_off[RPL];
 #pragma unroll
     for (int r = 0; r < RPL; ++r) lane_off[r] = base + (uint32_t)(r * 64 + lane) * 4u;
+
+    // the next tile's features are loaded into registers during the walk of the current one when
+    // they fit (F <= kRegTileFeatures, and the tree and tile prefetch registers within what the
+    // shape's occupancy leaves beside the walk), else staged between the pieces
+    constexpr int NT = 64 * TW;
+    constexpr int kNpx = (kRegTileFeatures * (RT / 4) + NT - 1) / NT;
+    constexpr int kWavesPerSimd = (TW + 3) / 4;
+    constexpr int kVgprBudget = (512 / kWavesPerSimd < 256 ? 512 / kWavesPerSimd : 256) - 80 - 2 * PF * NTW;  // walk
+    constexpr bool kRegTile = RPL <= 2 && 4 * (PF * NTW + kNpx) <= kVgprBudget;
+    constexpr int NPX = kRegTile ? kNpx : 1;
+    const bool x_regs = kRegTile && F * (RT / 4) <= NPX * NT;
+    float4 xf[NPX];
+    double *const red = reinterpret_cast<double *>(smem + ring_off);
 
     int64_t v = v_begin;
     int tile = (int)(v / T);
@@ -332,13 +412,18 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     int t1 = (int)(T - t0 < v_end - v ? T : t0 + (v_end - v));
     int t = t0 + wid;
     group_fetch<S16, PF, NTW, TW>(pf, trees, t, t1, lane);   // overlaps the feature staging
-    while (true) {
+    int has_nan = __builtin_amdgcn_readfirstlane(stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, tile * RT, flags));
+    for (int piece = 0;; ++piece) {
         const int row0 = tile * RT;
-        const int has_nan = stage_features<RT, 64 * TW>(smem, X, ld, n_rows, F, vec_ok, row0, flags + (piece & 1));
-        if (threadIdx.x == 0) flags[(piece + 1) & 1] = 0;
-        ++piece;
+        if (threadIdx.x == 0) {
+            flags[(piece + 1) & 1] = 0;      // NaN flag of the next tile (set at its staging, after B1)
+            flags[2 + ((piece + 1) & 1)] = 0;  // progress count of the next piece
+        }
+        uint32_t my_done = 0;
         group_commit<S16, PF, NTW, TW>(pf, slots, hd, t, t1, lane);
         group_fetch<S16, PF, NTW, TW>(pf, trees, t + STEP, t1, lane);
+        const bool next = v + (t1 - t0) < v_end;  // the next piece is tile + 1 from tree 0
+        if (next && x_regs) tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, row0 + RT);
         double acc[RPL];
 #pragma unroll
         for (int r = 0; r < RPL; ++r) acc[r] = 0.0;
@@ -362,16 +447,36 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
                 group_commit<S16, PF, NTW, TW>(pf, slots, hd, t + STEP, t1, lane);
                 group_fetch<S16, PF, NTW, TW>(pf, trees, t + 2 * STEP, t1, lane);
             }
+            // Fair progress: the SIMD arbiter favours older waves, and a piece ends at a barrier,
+            // so a wave that has walked fewer trees than its workgroup's average takes the top
+            // issue priority until it catches up.
+            const uint32_t walked = (NTW == 2 && t + TW < t1) ? 2u : 1u;
+            my_done += walked;
+            uint32_t total = 0;
+            if (lane == 0) total = atomicAdd(progress + (piece & 1), walked) + walked;
+            total = __builtin_amdgcn_readfirstlane(total);
+            if (my_done * TW < total)
+                __builtin_amdgcn_s_setprio(3);
+            else
+                __builtin_amdgcn_s_setprio(0);
         }
-        // the next piece (if any) starts at tree 0 of the next tile: prefetch its first trees now
+        __builtin_amdgcn_s_setprio(0);
         v += t1 - t0;
-        const bool next = v < v_end;
         const int nt1 = next ? (int)(T < v_end - v ? T : v_end - v) : 0;
-        if (next) group_fetch<S16, PF, NTW, TW>(pf, trees, wid, nt1, lane);
-        __syncthreads();  // every wave is done with its slots: reuse the region for the reduction
-        reduce_rows<RPL, TW>(reinterpret_cast<double *>(smem + ring_off), acc, wid, lane, row0, n_rows,
-                             partial + ((int64_t)tile + blockIdx.x) * RT);
+        if (next) group_fetch<S16, PF, NTW, TW>(pf, trees, wid, nt1, lane);  // first trees of the next piece
+        __syncthreads();  // B1: every wave is done with the tile and its slots
+        reduce_put<RPL>(red, acc, wid, lane);
+        if (next && x_regs) tile_commit<RT, NT, NPX>(xf, smem, F, flags + ((piece + 1) & 1));
+        __syncthreads();  // B2: row sums and the next tile are in LDS
+        reduce_sum<RPL, TW>(red, row0, n_rows, partial + ((int64_t)tile + blockIdx.x) * RT);
         if (!next) break;
+        if (x_regs) {
+            __syncthreads();  // B3: the sums are read before the next trees overwrite the slots
+            has_nan = __builtin_amdgcn_readfirstlane(flags[(piece + 1) & 1]);
+        } else {
+            has_nan = __builtin_amdgcn_readfirstlane(
+                stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, row0 + RT, flags + ((piece + 1) & 1)));
+        }
         ++tile;
         t0 = 0;
         t1 = nt1;
@@ -442,9 +547,11 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
 #pragma unroll
         for (int i = 0; i < ILP; ++i) {
             tb[i] = base + chunk_off + (uint32_t)(wid * ILP + i) * (S16 * 16);
-            const uint4 h = lds_ld<uint4>(tb[i]);
-            hd[i] = TreeHead{(uint32_t)__builtin_amdgcn_readfirstlane(h.y), (uint32_t)__builtin_amdgcn_readfirstlane(h.z),
-                             (uint32_t)__builtin_amdgcn_readfirstlane(h.w)};
+            const uint4 h = lds_ld<uint4>(tb[i]), h1 = lds_ld<uint4>(tb[i] + 16u);
+            hd[i] = TreeHead{(uint32_t)__builtin_amdgcn_readfirstlane(h.y),  (uint32_t)__builtin_amdgcn_readfirstlane(h.z),
+                             (uint32_t)__builtin_amdgcn_readfirstlane(h.w),  (uint32_t)__builtin_amdgcn_readfirstlane(h1.x),
+                             (uint32_t)__builtin_amdgcn_readfirstlane(h1.y), (uint32_t)__builtin_amdgcn_readfirstlane(h1.z),
+                             (uint32_t)__builtin_amdgcn_readfirstlane(h1.w)};
         }
         if (has_nan)
             walk_trees<D, ILP, 1, (uint32_t)RT * 4u, true>(tb, hd, lane_off, acc);
@@ -465,7 +572,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
 // partial[g * ldp + r]; sliced layout: the workgroups b = first..last whose slices cut the row's
 // tile i (RT rows, T trees), at partial[(i + b) * RT + r % RT] -- and the wave then sums its rows
 // with a fixed xor-butterfly, so the result does not depend on scheduling.
-__global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int rt_shift, int T,
+__global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int RT, int T,
                                                 int64_t L, int groups, const int32_t *__restrict__ prog_ptr, int n_prog,
                                                 int n_rows, float base_score, float *__restrict__ prog_score,
                                                 float *__restrict__ stmt_score) {
@@ -480,10 +587,10 @@ __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partia
         if (L == 0) {
             for (int gi = 0; gi < groups; ++gi) s += (double)partial[(int64_t)gi * ldp + r];
         } else {
-            const int64_t tile = r >> rt_shift;
+            const int64_t tile = (uint32_t)r / (uint32_t)RT;
             const int64_t first = tile * T / L, last = ((tile + 1) * T - 1) / L;
-            const float *src = partial + (tile << rt_shift) + (r & ((1 << rt_shift) - 1));
-            for (int64_t wb = first; wb <= last; ++wb) s += (double)src[wb << rt_shift];
+            const float *src = partial + (int64_t)r;  // block (tile + wb), row r - tile * RT
+            for (int64_t wb = first; wb <= last; ++wb) s += (double)src[wb * RT];
         }
         if (stmt_score) stmt_score[r] = (float)s;
         acc += s;
@@ -518,6 +625,7 @@ const void *pick_wp(int rpl, int tw, int ntw) {
 #define HARL_WP(R, T, N)                                                                          \
     if constexpr (wp_fits<D, R, T, N>())                                                          \
         if (rpl == R && tw == T && ntw == N) return reinterpret_cast<const void *>(k_tree_score_wp<D, R, T, N>);
+    HARL_WP(3, 11, 1) HARL_WP(3, 8, 1) HARL_WP(3, 5, 2)
     HARL_WP(2, 16, 1) HARL_WP(2, 12, 2) HARL_WP(2, 12, 1) HARL_WP(2, 8, 1) HARL_WP(2, 6, 1) HARL_WP(2, 4, 1)
     HARL_WP(1, 16, 2) HARL_WP(1, 8, 1) HARL_WP(1, 4, 1)
 #undef HARL_WP
@@ -526,8 +634,9 @@ const void *pick_wp(int rpl, int tw, int ntw) {
 
 template <int D>
 const void *pick_ch(int tw, int ilp) {
-#define HARL_CH(T, I) \
-    if (tw == T && ilp == I) return reinterpret_cast<const void *>(k_tree_score_ch<D, T, I>);
+#define HARL_CH(T, I)                                                                           \
+    if constexpr ((size_t)T * I * tree_stride_bytes(D) + 64 * 4 <= (size_t)kLdsBytes)          \
+        if (tw == T && ilp == I) return reinterpret_cast<const void *>(k_tree_score_ch<D, T, I>);
     HARL_CH(2, 1) HARL_CH(4, 1) HARL_CH(8, 1) HARL_CH(4, 2)
 #undef HARL_CH
     return nullptr;
@@ -547,7 +656,7 @@ ScoreCfg make_cfg(const harl_ensemble *E, bool wp, int a, int b, int n) {
         c.rows_per_tile = 64 * a;
         c.threads = 64 * b;
         const size_t ring = (size_t)b * n * stride, red = (size_t)b * c.rows_per_tile * 8;
-        c.lds = (size_t)E->n_features * c.rows_per_tile * 4 + (ring > red ? ring : red) + 16;  // + NaN flags
+        c.lds = (size_t)E->n_features * c.rows_per_tile * 4 + (ring > red ? ring : red) + 16;  // + NaN flags, progress counters
     } else {
         c.rows_per_tile = 64;
         c.threads = 64 * a;
@@ -663,9 +772,8 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
         return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
     float *partial = static_cast<float *>(ws);
     const unsigned seg_grid = (unsigned)ceil_div(n_prog, 4);  // one wave per program
-    const int rt_shift = c.rows_per_tile == 128 ? 7 : 6;
     if (n_rows == 0) {
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, 6, 1, (int64_t)0, 0, prog_ptr,
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, 64, 1, (int64_t)0, 0, prog_ptr,
                            n_prog, 0, E->base_score, prog_score, stmt_score);
         HARL_HIP_CHECK(hipGetLastError());
         return HARL_OK;
@@ -680,7 +788,7 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
         hipLaunchKernelGGL(reinterpret_cast<WpKernel>(const_cast<void *>(c.kern)), dim3((unsigned)w.nb), dim3(c.threads),
                            c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.V, w.L, partial);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, rt_shift, E->n_trees, w.L, 0,
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees, w.L, 0,
                            prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
     } else {
         const int G = choose_groups(E, n_rows, c);
@@ -691,7 +799,7 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
                            dim3(c.threads), c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees,
                            tpg, groups, partial, ldp);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, rt_shift, E->n_trees,
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees,
                            (int64_t)0, groups, prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
     }
     HARL_HIP_CHECK(hipGetLastError());
