@@ -41,7 +41,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--counter-probe", action="store_true",
                     help="for hardware-counter runs: one 256 MiB device-to-device copy (calibration of the "
-                         "byte counters) followed by 3 eager harl_score_round calls; prints sizes and exits")
+                         "byte counters) followed by 3 eager calls each of harl_score_round, harl_policy_step "
+                         "and harl_topk; prints sizes and exits")
     ap.add_argument("--no-graph", action="store_true", help="launch every call from the host instead of "
                     "replaying a captured graph of the round")
     ap.add_argument("--two-streams", action="store_true",
@@ -110,7 +111,13 @@ def main():
         for _ in range(3):
             rnd.score(batch)
         torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes": n_copy, "score_calls": 3, "feature_bytes": b["n_rows"] * cfg.n_features * 4,
+        for _ in range(3):
+            rnd.policy(batch)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            rnd.topk(batch)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n_copy, "calls_each": 3, "feature_bytes": b["n_rows"] * cfg.n_features * 4,
                           "n_rows": b["n_rows"], "n_prog": cfg.n_prog}), flush=True)
         rnd.close()
         return

@@ -50,33 +50,46 @@ constexpr int kRegTileFeatures = 192;  // features per row of a register-prefetc
 // (threshold + both children's codes, 8 bytes) -- both addresses are known when the level starts,
 // so a level is one LDS round trip of 12 bytes -- and the last level reads its threshold and both
 // leaves in one 16-byte record.  The first 16 bytes {0, code(1), threshold(1), codes(2, 3)} are
-// the same for every row, so the walk takes them as wave-uniform values, and it picks the record
-// of node 2 or 3 (the next 16 bytes) in registers: the first LDS record read is at level 2.
+// the same for every row and are taken as wave-uniform values.
 constexpr uint32_t tree_ll_bytes(int D) { return (4u << D) > 16u ? (4u << D) : 16u; }
 constexpr int tree_stride_bytes(int D) { return (int)((tree_ll_bytes(D) + (8u << D) + 15u) / 16u * 16u); }
 constexpr uint32_t kCodeDefaultLeft = 0x8000u;
 constexpr uint32_t kCodeFeature = 0x7FFFu;
+// Up to this many features a code's feature fits its low byte, so a child's feature is selected
+// with one byte-select instruction; wider ensembles select the 16-bit code and mask the flag.
+constexpr int kNarrowFeatures = 256;
 
-// x < threshold goes left; a missing value (NaN) goes the node's default way.
-template <bool NAN_AWARE>
-__device__ __forceinline__ uint32_t go_right(float x, float thr, uint32_t code) {
-    if (!NAN_AWARE) return x >= thr ? 1u : 0u;
-    const bool left = x < thr || (x != x && code > kCodeFeature);
-    return left ? 0u : 1u;
-}
-
-// Wave-uniform head of a packed tree: its first 32 bytes (root code, root record, and for depth
-// >= 3 the records of nodes 2 and 3, which the walk then selects in registers instead of reading).
+// Wave-uniform head of a packed tree (its bytes 4..15): root code, root threshold, codes of 2 and 3.
 struct TreeHead {
     uint32_t code, thr, pair;
-    uint32_t thr2, pair2, thr3, pair3;
 };
 
-// An opaque VGPR copy of a wave-uniform value, so that one v_cndmask can pick between two of
-// them (a VALU instruction reads at most one scalar operand).
+// Per-slot address constants of the walk (VGPR copies of wave-uniform values, so that one
+// v_cndmask can pick between two of them).  With a = the LDS address of the current record:
+//   inner level:           next record  = 2a + (go right ? r : l),            l = -tb,  r = 8 - tb
+//   into the last level:   next record  = 4a + (go right ? r_last : l_last),   l_last = LL - 8M - 3tb
+//   from the root:         next record  = go right ? r0 : l0 (absolute)
+struct WalkConst {
+    uint32_t l, r, l_last, r_last, l0, r0;
+};
+
+// An opaque VGPR copy of a wave-uniform value.
 __device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
     asm("" : "+v"(v));
     return v;
+}
+
+template <int D>
+__device__ __forceinline__ WalkConst walk_const(uint32_t tb) {
+    constexpr uint32_t M = 1u << D, LL = tree_ll_bytes(D);
+    WalkConst w;
+    w.l = in_vgpr(0u - tb);
+    w.r = in_vgpr(8u - tb);
+    w.l_last = in_vgpr(LL - 8u * M - 3u * tb);
+    w.r_last = in_vgpr(LL - 8u * M - 3u * tb + 16u);
+    w.l0 = in_vgpr(D > 2 ? tb + 16u : tb + LL);
+    w.r0 = in_vgpr(D > 2 ? tb + 24u : tb + LL + 16u);
+    return w;
 }
 
 // LDS accesses by absolute LDS byte address (the walk carries addresses as plain integers).
@@ -101,63 +114,125 @@ __device__ __forceinline__ uint4 lds_ld<uint4>(uint32_t a) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// Feature value of this lane's row for the feature of a 15-bit code.
-template <uint32_t RT4>
-__device__ __forceinline__ float feature_at(uint32_t feature, uint32_t lane_off) {
-    return lds_ld<float>(feature * RT4 + lane_off);
-}
-
-// Walk NT_ trees at LDS addresses tb[] (heads hd[]) for R rows of this lane (feature tile row
-// stride RT4 bytes per feature; lane_off[r] = LDS address of the lane's r-th row of feature 0).  Every
-// (tree, row) pair is an independent chain c = tree * R + row.  A chain's step at one level picks
-// the child, then at once issues the child's two LDS reads (feature value, record); the chains
-// take their steps in turn, so while one chain decides, the reads of all the others are in flight
-// (LDS reads of a wave return in order, and the scheduling barriers keep that order).  The
-// record address is carried directly: child record = 2 * current - tb + 8 * go_right.  Codes
-// keep the missing-goes-left flag only in the NaN-aware walk.
-template <int D, int NT_, int R, uint32_t RT4, bool NAN_AWARE>
-__device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const TreeHead (&hd)[NT_],
-                                           const uint32_t (&lane_off)[R], double (&acc)[R]) {
-    constexpr int NC = NT_ * R;
-    constexpr uint32_t W = NAN_AWARE ? 16u : 15u;
-    constexpr uint32_t kLast = tree_ll_bytes(D) - (8u << D);  // last-level record = 2 * rec(i) - tb + kLast
-    uint32_t c_left[NT_], c_right[NT_], c_root_l[NT_], c_root_r[NT_], l1_thr[NT_][2], l1_pair[NT_][2];
-#pragma unroll
-    for (int i = 0; i < NT_; ++i) {
-        c_left[i] = in_vgpr(0u - tb[i]);
-        c_right[i] = in_vgpr(8u - tb[i]);
-        c_root_l[i] = in_vgpr(tb[i] + 16u);
-        c_root_r[i] = in_vgpr(tb[i] + 24u);
-        if constexpr (D > 2) {
-            l1_thr[i][0] = in_vgpr(hd[i].thr2);
-            l1_pair[i][0] = in_vgpr(hd[i].pair2);
-            l1_thr[i][1] = in_vgpr(hd[i].thr3);
-            l1_pair[i][1] = in_vgpr(hd[i].pair3);
+// One decision of a walk.  Given this lane's feature value x at the current node, the node's
+// threshold and the packed codes `pair` of its children: the child's feature index `feat`, the
+// child's 16-bit code moved to the upper half of `fw` (its missing-goes-left flag is then the sign
+// bit; NaN-aware walk only) and `sel` = go right ? r : l.  A node sends x left iff x < threshold,
+// or x is missing (NaN) and the node's own flag (the sign of `fw_cur`) is set.  The children's
+// codes are picked with SDWA byte/word selects: one instruction instead of a shift, a mask and a
+// select (the compare writes VCC, which the selects read; two wait states separate a VALU write
+// of VCC from a VALU read of it as a mask).
+template <bool NAN_AWARE, bool NARROW>
+__device__ __forceinline__ void decide(float x, uint32_t thr, uint32_t pair, int32_t fw_cur, uint32_t l, uint32_t r,
+                                       uint32_t &feat, int32_t &fw, uint32_t &sel) {
+    if constexpr (!NAN_AWARE) {
+        if constexpr (NARROW) {
+            asm("v_cmp_ge_f32 vcc, %2, %3\n\t"
+                "s_nop 1\n\t"
+                "v_cndmask_b32_sdwa %0, %4, %4, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 src1_sel:BYTE_2\n\t"
+                "v_cndmask_b32 %1, %5, %6, vcc"
+                : "=&v"(feat), "=&v"(sel)
+                : "v"(x), "v"(thr), "v"(pair), "v"(l), "v"(r)
+                : "vcc");
+        } else {
+            asm("v_cmp_ge_f32 vcc, %2, %3\n\t"
+                "s_nop 1\n\t"
+                "v_cndmask_b32_sdwa %0, %4, %4, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t"
+                "v_cndmask_b32 %1, %5, %6, vcc"
+                : "=&v"(feat), "=&v"(sel)
+                : "v"(x), "v"(thr), "v"(pair), "v"(l), "v"(r)
+                : "vcc");
+            feat &= kCodeFeature;
+        }
+        fw = 0;
+        (void)fw_cur;
+    } else {
+        uint64_t t0, t1;
+        // vcc = go left = x < thr || (isnan(x) && flag)
+        if constexpr (NARROW) {
+            asm("v_cmp_u_f32 %[t0], %[x], %[x]\n\t"
+                "v_cmp_gt_i32 %[t1], 0, %[fc]\n\t"
+                "s_and_b64 %[t0], %[t0], %[t1]\n\t"
+                "v_cmp_lt_f32 vcc, %[x], %[th]\n\t"
+                "s_or_b64 vcc, vcc, %[t0]\n\t"
+                "v_cndmask_b32_sdwa %[ft], %[p], %[p], vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:BYTE_0\n\t"
+                "v_cndmask_b32_sdwa %[fw], %[p], %[p], vcc dst_sel:WORD_1 dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:WORD_0\n\t"
+                "v_cndmask_b32 %[sl], %[r], %[l], vcc"
+                : [ft] "=&v"(feat), [fw] "=&v"(fw), [sl] "=&v"(sel), [t0] "=&s"(t0), [t1] "=&s"(t1)
+                : [x] "v"(x), [th] "v"(thr), [p] "v"(pair), [fc] "v"(fw_cur), [l] "v"(l), [r] "v"(r)
+                : "vcc");
+        } else {
+            asm("v_cmp_u_f32 %[t0], %[x], %[x]\n\t"
+                "v_cmp_gt_i32 %[t1], 0, %[fc]\n\t"
+                "s_and_b64 %[t0], %[t0], %[t1]\n\t"
+                "v_cmp_lt_f32 vcc, %[x], %[th]\n\t"
+                "s_or_b64 vcc, vcc, %[t0]\n\t"
+                "v_cndmask_b32_sdwa %[ft], %[p], %[p], vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:WORD_0\n\t"
+                "v_cndmask_b32_sdwa %[fw], %[p], %[p], vcc dst_sel:WORD_1 dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:WORD_0\n\t"
+                "v_cndmask_b32 %[sl], %[r], %[l], vcc"
+                : [ft] "=&v"(feat), [fw] "=&v"(fw), [sl] "=&v"(sel), [t0] "=&s"(t0), [t1] "=&s"(t1)
+                : [x] "v"(x), [th] "v"(thr), [p] "v"(pair), [fc] "v"(fw_cur), [l] "v"(l), [r] "v"(r)
+                : "vcc");
+            feat &= kCodeFeature;
         }
     }
+}
+
+// Last level: the leaf reached from a last-level record {threshold, left leaf, right leaf, 0}.
+template <bool NAN_AWARE>
+__device__ __forceinline__ float leaf_of(float x, const uint4 &lv, int32_t fw_cur) {
+    bool left = x < __uint_as_float(lv.x);
+    if (NAN_AWARE) left = left || (x != x && fw_cur < 0);
+    return __uint_as_float(left ? lv.y : lv.z);
+}
+
+// Walk NT_ trees at LDS addresses tb[] (heads hd[], address constants wc[]) for R rows of this
+// lane (feature tile row stride RT4 bytes per feature; lane_off[r] = LDS address of the lane's
+// r-th row of feature 0).  Every (tree, row) pair is an independent chain c = tree * R + row.  A
+// chain's step at one level decides the child, then at once issues the child's two LDS reads
+// (feature value, record); the chains take their steps in turn, so while one chain decides, the
+// reads of all the others are in flight (LDS reads of a wave return in order, and the scheduling
+// barriers keep that order).  Per chain and inner level: a compare, two selects and two address
+// computations.
+template <int D, int NT_, int R, uint32_t RT4, bool NAN_AWARE, bool NARROW>
+__device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const TreeHead (&hd)[NT_],
+                                           const WalkConst (&wc)[NT_], const uint32_t (&lane_off)[R],
+                                           double (&acc)[R]) {
+    constexpr int NC = NT_ * R;
+    uint32_t thr0[NT_], pair0[NT_];
+    int32_t fw0[NT_];
+#pragma unroll
+    for (int i = 0; i < NT_; ++i) {
+        thr0[i] = in_vgpr(hd[i].thr);
+        pair0[i] = in_vgpr(hd[i].pair);
+        fw0[i] = NAN_AWARE ? (int32_t)in_vgpr(hd[i].code << 16) : 0;
+    }
     float x[NC];
-    uint32_t a[NC], code[NC];
+    uint32_t a[NC];
+    int32_t fw[NC];
     uint2 rec[NC];
     uint4 lv[NC];
     // level 0: the root is the same node for every row of a tree
 #pragma unroll
-    for (int c = 0; c < NC; ++c) x[c] = feature_at<RT4>(hd[c / R].code & kCodeFeature, lane_off[c % R]);
+    for (int c = 0; c < NC; ++c) x[c] = lds_ld<float>((hd[c / R].code & kCodeFeature) * RT4 + lane_off[c % R]);
     if constexpr (D == 1) {
 #pragma unroll
-        for (int c = 0; c < NC; ++c) lv[c] = lds_ld<uint4>(tb[c / R] + 16u);
+        for (int c = 0; c < NC; ++c) {
+            lv[c] = lds_ld<uint4>(tb[c / R] + 16u);
+            fw[c] = fw0[c / R];
+        }
     } else {
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             const int i = c / R;
-            const uint32_t g = go_right<NAN_AWARE>(x[c], __uint_as_float(hd[i].thr), hd[i].code);
-            a[c] = g ? c_root_r[i] : c_root_l[i];
-            const uint32_t sh = g ? 16u : 0u;
-            code[c] = __builtin_amdgcn_ubfe(hd[i].pair, sh, W);
-            x[c] = feature_at<RT4>(NAN_AWARE ? __builtin_amdgcn_ubfe(hd[i].pair, sh, 15u) : code[c], lane_off[c % R]);
+            uint32_t f, sel;
+            decide<NAN_AWARE, NARROW>(x[c], thr0[i], pair0[i], fw0[i], wc[i].l0, wc[i].r0, f, fw[c], sel);
+            x[c] = lds_ld<float>(f * RT4 + lane_off[c % R]);
+            a[c] = sel;
             if constexpr (D > 2)
-                rec[c] = make_uint2(g ? l1_thr[i][1] : l1_thr[i][0], g ? l1_pair[i][1] : l1_pair[i][0]);
+                rec[c] = lds_ld<uint2>(sel);
             else
-                lv[c] = lds_ld<uint4>(2u * a[c] - tb[i] + kLast);
+                lv[c] = lds_ld<uint4>(sel);
             __builtin_amdgcn_sched_barrier(0);
         }
         // levels 1 .. D-2
@@ -166,28 +241,26 @@ __device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const Tree
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
                 const int i = c / R;
-                const uint32_t g = go_right<NAN_AWARE>(x[c], __uint_as_float(rec[c].x), code[c]);
-                a[c] = 2u * a[c] + (g ? c_right[i] : c_left[i]);
-                const uint32_t sh = g ? 16u : 0u;
-                code[c] = __builtin_amdgcn_ubfe(rec[c].y, sh, W);
-                x[c] = feature_at<RT4>(NAN_AWARE ? __builtin_amdgcn_ubfe(rec[c].y, sh, 15u) : code[c], lane_off[c % R]);
-                if (lvl + 2 < D)
+                const bool to_last = lvl + 2 == D;
+                uint32_t f, sel;
+                decide<NAN_AWARE, NARROW>(x[c], rec[c].x, rec[c].y, fw[c], to_last ? wc[i].l_last : wc[i].l,
+                                          to_last ? wc[i].r_last : wc[i].r, f, fw[c], sel);
+                x[c] = lds_ld<float>(f * RT4 + lane_off[c % R]);
+                if (!to_last) {
+                    a[c] = 2u * a[c] + sel;
                     rec[c] = lds_ld<uint2>(a[c]);
-                else
-                    lv[c] = lds_ld<uint4>(2u * a[c] - tb[i] + kLast);
+                } else {
+                    a[c] = 4u * a[c] + sel;
+                    lv[c] = lds_ld<uint4>(a[c]);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
     }
     // last level: threshold and both leaves
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        const uint32_t cd = D == 1 ? hd[c / R].code : code[c];
-        const uint32_t g = go_right<NAN_AWARE>(x[c], __uint_as_float(lv[c].x), cd);
-        acc[c % R] += (double)__uint_as_float(g ? lv[c].z : lv[c].y);
-    }
+    for (int c = 0; c < NC; ++c) acc[c % R] += (double)leaf_of<NAN_AWARE>(x[c], lv[c], fw[c]);
 }
-
 // Item i of a row tile ([F][RT] fp32 in LDS, RT/4 float4 per feature): rows row0 + 4*(i % V) ..
 // + 3 of feature i / V, zero past n_rows.
 template <int V>
@@ -338,24 +411,29 @@ __device__ __forceinline__ void group_commit(const uint4 (&pf)[NTW][PF], char *s
             hd[j].code = __builtin_amdgcn_readlane(pf[j][0].y, 0);
             hd[j].thr = __builtin_amdgcn_readlane(pf[j][0].z, 0);
             hd[j].pair = __builtin_amdgcn_readlane(pf[j][0].w, 0);
-            hd[j].thr2 = __builtin_amdgcn_readlane(pf[j][0].x, 1);
-            hd[j].pair2 = __builtin_amdgcn_readlane(pf[j][0].y, 1);
-            hd[j].thr3 = __builtin_amdgcn_readlane(pf[j][0].z, 1);
-            hd[j].pair3 = __builtin_amdgcn_readlane(pf[j][0].w, 1);
         }
 }
 
 // ---- K1, depth <= 10: persistent workgroups with per-wave private tree slots ----
-// The work is the space of (row tile, tree) pairs, tile-major: v = tile * T + tree.  Workgroup b
-// owns the contiguous slice [b*L, (b+1)*L), so every workgroup walks the same number of trees and
-// the machine is busy to the end.  Wave w walks trees w, w + TW, ... of each piece, NTW at a time
-// from its NTW LDS slots; the next NTW trees are fetched into registers meanwhile and committed
-// over the slots after the walk (LDS operations of one wave execute in order, so the walk's reads
-// are served before the commit's writes).  The partial sums of the piece of tile i walked by
-// workgroup b are stored at block (i + b) of RT floats: a workgroup covers a contiguous run of
-// tiles, so i + b grows strictly along the (workgroup, tile) pieces and (tiles + workgroups)
-// blocks hold them all; a tile's pieces are summed later in workgroup order.
-template <int D, int RPL, int TW, int NTW>
+// The work is the space of (row tile, tree) pairs, tile-major: v = tile * T + tree.  Slice s owns
+// the contiguous range [s*L, (s+1)*L), so every workgroup walks the same number of trees and the
+// machine is busy to the end.  A slice covers whole tiles plus, at each end, possibly part of a
+// tile that the neighbouring slice also covers; both must stage that tile's features.  So that
+// the second staging hits L2: consecutive slices run on the same XCD (workgroups are dealt to the
+// 8 XCDs round-robin, so workgroup b takes slice (b % 8) * (grid / 8) + b / 8), and even slices
+// walk their tiles last to first while odd slices walk first to last -- a shared tile is then the
+// first tile of both slices or the last tile of both.  Wave w walks trees w, w + TW, ... of each
+// piece, NTW at a time from its NTW LDS slots; the next NTW trees are fetched into registers
+// meanwhile and committed over the slots after the walk (LDS operations of one wave execute in
+// order, so the walk's reads are served before the commit's writes).  The partial sums of the
+// piece of tile i walked by slice s are stored at block (i + s) of RT floats: a slice covers a
+// contiguous run of tiles, so i + s grows strictly along the (slice, tile) pieces and (tiles +
+// slices) blocks hold them all; a tile's pieces are summed later in slice order.
+__device__ __forceinline__ int slice_of_block(int b, int nb) {
+    return (nb % 8 == 0) ? (b % 8) * (nb / 8) + b / 8 : b;
+}
+
+template <int D, int RPL, int TW, int NTW, bool NARROW>
 __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
     int T, int64_t V, int64_t L, float *__restrict__ partial) {
@@ -364,9 +442,17 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     constexpr int PF = (S16 + kWave - 1) / kWave;   // uint4 per lane per tree
     constexpr int STEP = NTW * TW;                  // trees between a wave's consecutive groups
     extern __shared__ __align__(16) char smem[];
-    const int64_t v_begin = (int64_t)blockIdx.x * L;
+    const int s = slice_of_block(blockIdx.x, gridDim.x);
+    const int64_t v_begin = (int64_t)s * L;
     const int64_t v_end = v_begin + L < V ? v_begin + L : V;
     if (v_begin >= v_end) return;  // whole workgroup: no barrier is skipped by part of it
+    const int tile_first = (int)(v_begin / T), tile_last = (int)((v_end - 1) / T);
+    const int dir = (s & 1) ? 1 : -1;
+    const int n_pieces = tile_last - tile_first + 1;
+    // trees [lo, hi) of tile i that belong to this slice
+    auto piece_lo = [&](int i) { return (int)(v_begin - (int64_t)i * T > 0 ? v_begin - (int64_t)i * T : 0); };
+    auto piece_hi = [&](int i) { return (int)(v_end - (int64_t)i * T < T ? v_end - (int64_t)i * T : T); };
+
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const uint32_t ring_off = (uint32_t)F * RT * 4u;
     const uint32_t slot0 = ring_off + (uint32_t)wid * NTW * (S16 * 16);
@@ -387,11 +473,16 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
         for (int k = 0; k < PF; ++k) pf[j][k] = make_uint4(0, 0, 0, 0);
     TreeHead hd[NTW];
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) hd[j] = TreeHead{0, 0, 0, 0, 0, 0, 0};
+    for (int j = 0; j < NTW; ++j) hd[j] = TreeHead{0, 0, 0};
     const uint32_t base = lds_addr(smem);
     uint32_t lane_off[RPL];
 #pragma unroll
     for (int r = 0; r < RPL; ++r) lane_off[r] = base + (uint32_t)(r * 64 + lane) * 4u;
+    // slot addresses and walk constants (both entries the same slot when NTW == 1)
+    const uint32_t tb[2] = {base + slot0, base + slot0 + (NTW > 1 ? S16 * 16 : 0)};
+    WalkConst wc[2];
+    wc[0] = walk_const<D>(tb[0]);
+    wc[1] = NTW > 1 ? walk_const<D>(tb[1]) : wc[0];
 
     // the next tile's features are loaded into registers during the walk of the current one when
     // they fit (F <= kRegTileFeatures, and the tree and tile prefetch registers within what the
@@ -406,10 +497,8 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     float4 xf[NPX];
     double *const red = reinterpret_cast<double *>(smem + ring_off);
 
-    int64_t v = v_begin;
-    int tile = (int)(v / T);
-    int t0 = (int)(v % T);
-    int t1 = (int)(T - t0 < v_end - v ? T : t0 + (v_end - v));
+    int tile = dir > 0 ? tile_first : tile_last;
+    int t0 = piece_lo(tile), t1 = piece_hi(tile);
     int t = t0 + wid;
     group_fetch<S16, PF, NTW, TW>(pf, trees, t, t1, lane);   // overlaps the feature staging
     int has_nan = __builtin_amdgcn_readfirstlane(stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, tile * RT, flags));
@@ -422,26 +511,27 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
         uint32_t my_done = 0;
         group_commit<S16, PF, NTW, TW>(pf, slots, hd, t, t1, lane);
         group_fetch<S16, PF, NTW, TW>(pf, trees, t + STEP, t1, lane);
-        const bool next = v + (t1 - t0) < v_end;  // the next piece is tile + 1 from tree 0
-        if (next && x_regs) tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, row0 + RT);
+        const bool next = piece + 1 < n_pieces;
+        const int ntile = tile + dir;
+        if (next && x_regs) tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, ntile * RT);
         double acc[RPL];
 #pragma unroll
         for (int r = 0; r < RPL; ++r) acc[r] = 0.0;
         for (; t < t1; t += STEP) {
             if (NTW == 2 && t + TW < t1) {
-                const uint32_t tb[2] = {base + slot0, base + slot0 + S16 * 16};
                 const TreeHead h2[2] = {hd[0], hd[NTW - 1]};
                 if (has_nan)
-                    walk_trees<D, 2, RPL, (uint32_t)RT * 4u, true>(tb, h2, lane_off, acc);
+                    walk_trees<D, 2, RPL, (uint32_t)RT * 4u, true, NARROW>(tb, h2, wc, lane_off, acc);
                 else
-                    walk_trees<D, 2, RPL, (uint32_t)RT * 4u, false>(tb, h2, lane_off, acc);
+                    walk_trees<D, 2, RPL, (uint32_t)RT * 4u, false, NARROW>(tb, h2, wc, lane_off, acc);
             } else {
-                const uint32_t tb[1] = {base + slot0};
+                const uint32_t tb1[1] = {tb[0]};
                 const TreeHead h1[1] = {hd[0]};
+                const WalkConst w1[1] = {wc[0]};
                 if (has_nan)
-                    walk_trees<D, 1, RPL, (uint32_t)RT * 4u, true>(tb, h1, lane_off, acc);
+                    walk_trees<D, 1, RPL, (uint32_t)RT * 4u, true, NARROW>(tb1, h1, w1, lane_off, acc);
                 else
-                    walk_trees<D, 1, RPL, (uint32_t)RT * 4u, false>(tb, h1, lane_off, acc);
+                    walk_trees<D, 1, RPL, (uint32_t)RT * 4u, false, NARROW>(tb1, h1, w1, lane_off, acc);
             }
             if (t + STEP < t1) {
                 group_commit<S16, PF, NTW, TW>(pf, slots, hd, t + STEP, t1, lane);
@@ -461,26 +551,25 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
                 __builtin_amdgcn_s_setprio(0);
         }
         __builtin_amdgcn_s_setprio(0);
-        v += t1 - t0;
-        const int nt1 = next ? (int)(T < v_end - v ? T : v_end - v) : 0;
-        if (next) group_fetch<S16, PF, NTW, TW>(pf, trees, wid, nt1, lane);  // first trees of the next piece
+        const int nt0 = next ? piece_lo(ntile) : 0, nt1 = next ? piece_hi(ntile) : 0;
+        if (next) group_fetch<S16, PF, NTW, TW>(pf, trees, nt0 + wid, nt1, lane);  // first trees of the next piece
         __syncthreads();  // B1: every wave is done with the tile and its slots
         reduce_put<RPL>(red, acc, wid, lane);
         if (next && x_regs) tile_commit<RT, NT, NPX>(xf, smem, F, flags + ((piece + 1) & 1));
         __syncthreads();  // B2: row sums and the next tile are in LDS
-        reduce_sum<RPL, TW>(red, row0, n_rows, partial + ((int64_t)tile + blockIdx.x) * RT);
+        reduce_sum<RPL, TW>(red, row0, n_rows, partial + ((int64_t)tile + s) * RT);
         if (!next) break;
         if (x_regs) {
             __syncthreads();  // B3: the sums are read before the next trees overwrite the slots
             has_nan = __builtin_amdgcn_readfirstlane(flags[(piece + 1) & 1]);
         } else {
             has_nan = __builtin_amdgcn_readfirstlane(
-                stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, row0 + RT, flags + ((piece + 1) & 1)));
+                stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, ntile * RT, flags + ((piece + 1) & 1)));
         }
-        ++tile;
-        t0 = 0;
+        tile = ntile;
+        t0 = nt0;
         t1 = nt1;
-        t = wid;
+        t = t0 + wid;
     }
 }
 
@@ -507,7 +596,7 @@ __device__ __forceinline__ void block_commit(const uint4 (&pf)[NPF], uint4 *dst)
 }
 
 // ---- K1, deeper trees: chunks of TW*ILP trees shared by the workgroup ----
-template <int D, int TW, int ILP>
+template <int D, int TW, int ILP, bool NARROW>
 __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
     const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
     int n_trees, int trees_per_group, int n_groups, float *__restrict__ partial, int64_t ldp) {
@@ -544,19 +633,19 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
         if (more) block_fetch<C, S16, NT>(pf, trees, t0 + C, t_end);
         uint32_t tb[ILP];
         TreeHead hd[ILP];
+        WalkConst wc[ILP];
 #pragma unroll
         for (int i = 0; i < ILP; ++i) {
             tb[i] = base + chunk_off + (uint32_t)(wid * ILP + i) * (S16 * 16);
-            const uint4 h = lds_ld<uint4>(tb[i]), h1 = lds_ld<uint4>(tb[i] + 16u);
-            hd[i] = TreeHead{(uint32_t)__builtin_amdgcn_readfirstlane(h.y),  (uint32_t)__builtin_amdgcn_readfirstlane(h.z),
-                             (uint32_t)__builtin_amdgcn_readfirstlane(h.w),  (uint32_t)__builtin_amdgcn_readfirstlane(h1.x),
-                             (uint32_t)__builtin_amdgcn_readfirstlane(h1.y), (uint32_t)__builtin_amdgcn_readfirstlane(h1.z),
-                             (uint32_t)__builtin_amdgcn_readfirstlane(h1.w)};
+            const uint4 h = lds_ld<uint4>(tb[i]);
+            hd[i] = TreeHead{(uint32_t)__builtin_amdgcn_readfirstlane(h.y), (uint32_t)__builtin_amdgcn_readfirstlane(h.z),
+                             (uint32_t)__builtin_amdgcn_readfirstlane(h.w)};
+            wc[i] = walk_const<D>(tb[i]);
         }
         if (has_nan)
-            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, true>(tb, hd, lane_off, acc);
+            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, true, NARROW>(tb, hd, wc, lane_off, acc);
         else
-            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, false>(tb, hd, lane_off, acc);
+            walk_trees<D, ILP, 1, (uint32_t)RT * 4u, false, NARROW>(tb, hd, wc, lane_off, acc);
         __syncthreads();
         if (more) {
             block_commit<C, S16, NT>(pf, reinterpret_cast<uint4 *>(smem + chunk_off));
@@ -620,37 +709,41 @@ constexpr bool wp_fits() {
     return D <= kMaxWpDepth && (size_t)TW * NTW * tree_stride_bytes(D) + 64 * RPL * 4 <= (size_t)kLdsBytes;
 }
 
-template <int D>
+template <int D, bool NARROW>
 const void *pick_wp(int rpl, int tw, int ntw) {
 #define HARL_WP(R, T, N)                                                                          \
     if constexpr (wp_fits<D, R, T, N>())                                                          \
-        if (rpl == R && tw == T && ntw == N) return reinterpret_cast<const void *>(k_tree_score_wp<D, R, T, N>);
-    HARL_WP(3, 11, 1) HARL_WP(3, 8, 1) HARL_WP(3, 5, 2)
+        if (rpl == R && tw == T && ntw == N)                                                      \
+            return reinterpret_cast<const void *>(k_tree_score_wp<D, R, T, N, NARROW>);
     HARL_WP(2, 16, 1) HARL_WP(2, 12, 2) HARL_WP(2, 12, 1) HARL_WP(2, 8, 1) HARL_WP(2, 6, 1) HARL_WP(2, 4, 1)
     HARL_WP(1, 16, 2) HARL_WP(1, 8, 1) HARL_WP(1, 4, 1)
 #undef HARL_WP
     return nullptr;
 }
 
-template <int D>
+template <int D, bool NARROW>
 const void *pick_ch(int tw, int ilp) {
 #define HARL_CH(T, I)                                                                           \
     if constexpr ((size_t)T * I * tree_stride_bytes(D) + 64 * 4 <= (size_t)kLdsBytes)          \
-        if (tw == T && ilp == I) return reinterpret_cast<const void *>(k_tree_score_ch<D, T, I>);
+        if (tw == T && ilp == I) return reinterpret_cast<const void *>(k_tree_score_ch<D, T, I, NARROW>);
     HARL_CH(2, 1) HARL_CH(4, 1) HARL_CH(8, 1) HARL_CH(4, 2)
 #undef HARL_CH
     return nullptr;
 }
 
-template <int... Ds>
+template <bool NARROW, int... Ds>
 const void *pick_depth(int depth, bool wp, int a, int b, int c, std::integer_sequence<int, Ds...>) {
     const void *k = nullptr;
-    ((depth == Ds + 1 ? (void)(k = wp ? pick_wp<Ds + 1>(a, b, c) : pick_ch<Ds + 1>(a, b)) : (void)0), ...);
+    ((depth == Ds + 1 ? (void)(k = wp ? pick_wp<Ds + 1, NARROW>(a, b, c) : pick_ch<Ds + 1, NARROW>(a, b)) : (void)0), ...);
     return k;
 }
 
 ScoreCfg make_cfg(const harl_ensemble *E, bool wp, int a, int b, int n) {
-    ScoreCfg c{wp, a, b, n, pick_depth(E->depth, wp, a, b, n, std::make_integer_sequence<int, kMaxDepth>{}), 0, 0, 0};
+    const bool narrow = E->n_features <= kNarrowFeatures;
+    ScoreCfg c{wp, a, b, n,
+               narrow ? pick_depth<true>(E->depth, wp, a, b, n, std::make_integer_sequence<int, kMaxDepth>{})
+                      : pick_depth<false>(E->depth, wp, a, b, n, std::make_integer_sequence<int, kMaxDepth>{}),
+               0, 0, 0};
     const size_t stride = (size_t)E->tree_stride;
     if (wp) {
         c.rows_per_tile = 64 * a;
@@ -697,7 +790,8 @@ int device_cus(int device) {
 }
 
 // Work split of the persistent kernel: nb workgroups, each a slice of L (tile, tree) pairs; at
-// least 2 trees per wave per slice so the feature staging stays amortised.
+// least 2 trees per wave per slice so the feature staging stays amortised.  The grid is a whole
+// number of XCD rounds (a multiple of 8); slices past the work are empty.
 struct WpSplit {
     int64_t V, L, tiles;
     int nb;
@@ -713,7 +807,7 @@ WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
     const int64_t min_l = 2LL * c.b * c.c;
     if (ceil_div(w.V, nb) < min_l) nb = ceil_div(w.V, min_l);
     w.L = ceil_div(w.V, nb);
-    w.nb = (int)ceil_div(w.V, w.L);
+    w.nb = (int)round_up(ceil_div(w.V, w.L), 8);
     return w;
 }
 
