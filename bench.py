@@ -98,7 +98,9 @@ def main():
     cfg = get_config(args.config)
     ens, pol, b = gen_ensemble(cfg), gen_policy(cfg), gen_batch(cfg)
     dev = torch.device("cuda:0")
-    rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=args.two_streams)
+    # a workload with a softmax output (policy-heavy, streamed) produces the probabilities every step
+    rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=args.two_streams,
+                want_probs=cfg.softmax)
     batch = upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)
     main_stream = torch.cuda.current_stream(dev)
 

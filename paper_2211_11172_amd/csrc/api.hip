@@ -101,7 +101,7 @@ int harl_policy_create(const harl_policy_desc *desc, harl_policy **out, void *st
 
 int harl_policy_destroy(harl_policy *pol) {
     if (!pol) return HARL_OK;
-    void *ptrs[] = {pol->d_w1, pol->d_w2, pol->d_wh, pol->d_b1, pol->d_b2, pol->d_bh};
+    void *ptrs[] = {pol->d_w1, pol->d_w2, pol->d_wh, pol->d_b1, pol->d_b2, pol->d_bh, pol->x32_stream, pol->x32_bias};
     hipError_t first = hipSuccess;
     for (void *p : ptrs) {
         hipError_t e = hipFree(p);

@@ -62,6 +62,10 @@ struct harl_policy {
     int device;
     void *d_w1, *d_w2, *d_wh;    // fragment-ordered weights
     float *d_b1, *d_b2, *d_bh;   // padded biases (bh = [ba; bv; 0...])
+    // large-batch bf16 kernel (policy_x32.hip): chunked weight stream and accumulator-order biases;
+    // x32_stream is null when the shape is outside that kernel's limits
+    void *x32_stream, *x32_bias;
+    int32_t x32_ks2, x32_ht, x32_nt1, x32_nt2, x32_chunk;
 };
 
 namespace harl {
@@ -74,6 +78,10 @@ size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows);
 int pack_ensemble(const harl_ensemble_desc *desc, harl_ensemble **out, hipStream_t stream);
 
 int pack_policy(const harl_policy_desc *desc, harl_policy **out, hipStream_t stream);
+bool policy_x32_eligible(const harl_policy_desc *desc);
+int pack_policy_x32(const harl_policy_desc *desc, harl_policy *P, hipStream_t stream);
+int policy_x32_launch(const harl_policy *P, const void *states, int32_t B, int32_t *action, float *value,
+                      float *probs, float *logits, hipStream_t stream);
 int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int32_t *action,
                        float *value, float *probs, float *logits, hipStream_t stream);
 

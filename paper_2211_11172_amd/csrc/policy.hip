@@ -43,6 +43,7 @@ namespace {
 constexpr int kMaxU = 8;      // waves per workgroup (at most)
 constexpr int kRing = 4;      // k-groups of weight fragments in flight per wave
 constexpr int kHiddenPad = 256;  // hidden widths padded to whole tile groups of every kernel shape
+constexpr int kX32MinBatch = 16384;  // bf16 batches from this size use k_policy_x32 (policy_x32.hip)
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -462,9 +463,11 @@ int pack_policy(const harl_policy_desc *d, harl_policy **out, hipStream_t stream
     P->d_b2 = static_cast<float *>(b2d);
     P->d_bh = static_cast<float *>(bhd);
     if (rc == HARL_OK && hipStreamSynchronize(stream) != hipSuccess) rc = HARL_E_HIP;
+    if (rc == HARL_OK && policy_x32_eligible(d)) rc = pack_policy_x32(d, P, stream);
     if (rc != HARL_OK) {
         (void)hipFree(P->d_w1); (void)hipFree(P->d_w2); (void)hipFree(P->d_wh);
         (void)hipFree(P->d_b1); (void)hipFree(P->d_b2); (void)hipFree(P->d_bh);
+        (void)hipFree(P->x32_stream); (void)hipFree(P->x32_bias);
         delete P;
         return fail(rc, "harl_policy_create: device allocation or upload failed");
     }
@@ -486,6 +489,8 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     a.b1 = P->d_b1; a.b2 = P->d_b2; a.bh = P->d_bh;
     a.action = action; a.value = value; a.probs = probs; a.logits = logits;
     const bool bf = P->dtype == HARL_BF16;
+    // Large bf16 batches of the shapes it covers go to the 128-states-per-workgroup kernel
+    if (P->x32_stream && B >= kX32MinBatch) return policy_x32_launch(P, states, B, action, value, probs, logits, stream);
     // Large bf16 batches: 64 states per workgroup share every weight fragment (4 state groups), 4
     // waves of 4-tile groups with deep weight prefetch.  Otherwise 16 states per workgroup and 8
     // waves, so that a small batch still spreads over every CU.

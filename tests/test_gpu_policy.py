@@ -73,3 +73,28 @@ def test_odd_sizes(dtype):
 def test_single_action_and_wide_head():
     _check(mini_config(pol_a=1, n_prog=20))
     _check(mini_config(pol_a=100, pol_h2=64, n_prog=40))
+
+
+# Batches of 16384 states and more of a bf16 policy take the 128-states-per-workgroup kernel
+# (h1 kept in registers, weights streamed through LDS): its shape limits and ragged edges.
+_LARGE = 16384
+
+
+@pytest.mark.parametrize("exact", [True, False])
+def test_large_batch_odd_shapes(exact):
+    # h1 <= 512 variant, h2 not a multiple of 32, 41 head rows, a ragged last workgroup
+    cfg = mini_config(pol_dtype="bf16", pol_s=64, pol_h1=300, pol_h2=100, pol_a=40, exact=exact)
+    _check(cfg, B=_LARGE + 77)
+
+
+@pytest.mark.parametrize("a", [95, 127])
+def test_large_batch_wide_heads(a):
+    # 95 actions + value fill the large-batch kernel's 3 head tiles of 32 rows; 127 are beyond its
+    # limit and take the general kernel.  h1 of 1000 units (1024-unit variant)
+    cfg = mini_config(pol_dtype="bf16", pol_s=128, pol_h1=1000, pol_h2=70, pol_a=a, exact=True)
+    _check(cfg, B=_LARGE + 3)
+
+
+def test_large_batch_policy_heavy_values():
+    # the policy-heavy network with its own (non-integer) weights and states
+    _check(get_config("policy_heavy"), B=_LARGE + 129)
