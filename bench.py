@@ -1,8 +1,8 @@
 """Benchmark one HARL search round on one MI355X: policy forward + cost-model scoring + top-K.
 
 A step is one whole round over one batch of synthetic candidates, inputs already resident in
-HBM: harl_policy_step, harl_score_round and harl_topk, in that order on one stream (the scoring
-kernel keeps every CU busy, so a concurrent policy stream only contends for them).
+HBM: harl_policy_step, harl_score_round and harl_topk in turn on one stream (--two-streams: the
+policy on a second stream after scoring, beside top-K).
 Prints ONE JSON line (rank 0).  Default workload: the standard round (4,096 candidates with
 U{1..32} statements of 164 features, 300 trees of depth 8, fp32 MLP 64-256-256 -> 24+1, top-128).
 
@@ -46,7 +46,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch every call from the host instead of "
                     "replaying a captured graph of the round")
     ap.add_argument("--two-streams", action="store_true",
-                    help="run the policy on a second stream concurrently with scoring")
+                    help="run the policy on a second stream after scoring, beside top-K (default: the "
+                         "three calls in turn on one stream, which measured faster on the standard round)")
     return ap.parse_args()
 
 

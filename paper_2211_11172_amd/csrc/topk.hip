@@ -7,12 +7,14 @@
 // key << 32 | (0xFFFFFFFF - i), so the ranking is the descending order of unique composites and
 // every selection below is exact and deterministic.
 //
-// K3 k_topk_select: a workgroup of 512 threads owns a segment of up to 8192 candidates, held in
+// K3 k_topk_select: a workgroup of 1024 threads owns a segment of up to 8192 candidates, held in
 //    registers.  A most-significant-digit radix select (8 bits per pass over the composite,
 //    per-wave LDS histograms, early exit once a digit bucket holds exactly the ranks still needed;
 //    a segment of at most kk candidates keeps them all) finds the segment's kk best; they are
-//    compacted into LDS and sorted (kk <= 512: each key's slot is its rank, counted against all
-//    others in one pass; larger kk: bitonic).
+//    compacted into LDS and sorted (kk <= 128: each key's slot is its rank, counted against all
+//    others by several threads per key; larger kk: bitonic).  Lanes of one LDS atomic that hit
+//    the same address are serialised, so histogram updates and compaction slots are aggregated per
+//    wave first.
 //    Segments run in parallel; their sorted outputs form the next round's candidates until one
 //    segment is left, whose workgroup writes the final top-k directly.
 // K5 k_topk_merge: merges the sorted top-k of this call into the sorted running top-k by rank
@@ -25,9 +27,9 @@
 namespace harl {
 namespace {
 
-constexpr int kSelThreads = 512;
-constexpr int kPerThread = 16;
-constexpr int kRankSortMax = 512;  // up to this many selected keys are ranked directly, else bitonic
+constexpr int kSelThreads = 1024;
+constexpr int kPerThread = 8;
+constexpr int kRankSortMax = 128;  // up to this many selected keys are ranked directly, else bitonic
 constexpr int kSeg = kSelThreads * kPerThread;  // candidates per workgroup
 constexpr int kMergeThreads = 1024;
 
@@ -51,6 +53,7 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
     __shared__ uint32_t hist[256];
     __shared__ uint64_t sel[HARL_TOPK_MAX_K];
     __shared__ uint64_t ranked[kRankSortMax];
+    __shared__ uint32_t rank_cnt[kRankSortMax];
     __shared__ uint32_t s_digit, s_above, s_eq, s_cnt;
     const int t = threadIdx.x, w = t / 64;
     const int64_t base = (int64_t)blockIdx.x * kSeg;
@@ -80,10 +83,22 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         shift -= 8;
         for (int i = t; i < (kSelThreads / 64) * 256; i += kSelThreads) (&whist[0][0])[i] = 0;
         __syncthreads();
+        // Scores concentrate in few digit values (the leading digits are sign and exponent), and
+        // lanes of one atomic instruction that hit the same bin are serialised.  So the lanes that
+        // share the first live lane's bin are counted with a single atomic, the rest (few, and
+        // spread) with their own.
 #pragma unroll
         for (int j = 0; j < kPerThread; ++j) {
             const bool alive = valid(j) && (shift == 56 || ((x[j] ^ prefix) >> (shift + 8)) == 0);
-            if (alive) atomicAdd(&whist[w][(uint32_t)(x[j] >> shift) & 255u], 1u);
+            const uint32_t bin = (uint32_t)(x[j] >> shift) & 255u;
+            const uint64_t live = __ballot(alive);
+            if (live) {
+                const int first = __builtin_ctzll(live);
+                const uint32_t b0 = __builtin_amdgcn_readlane(bin, first);
+                const uint64_t same = __ballot(alive && bin == b0);
+                if (t % 64 == first) atomicAdd(&whist[w][b0], (uint32_t)__popcll(same));
+                if (alive && bin != b0) atomicAdd(&whist[w][bin], 1u);
+            }
         }
         __syncthreads();
         if (t < 256) {
@@ -125,39 +140,65 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
     // ---- compaction: everything strictly above the prefix, then kr of those equal to it ----
     if (t == 0) s_cnt = 0;
     __syncthreads();
+    // one counter atomic per wave: a lane's slot is the wave's base plus the number of lower lanes
+    // that also append
+    auto append_slot = [&](bool take) -> uint32_t {
+        const uint64_t m = __ballot(take);
+        uint32_t slot = 0;
+        if (m) {
+            const int first = __builtin_ctzll(m);
+            uint32_t wbase = 0;
+            if (t % 64 == first) wbase = atomicAdd(&s_cnt, (uint32_t)__popcll(m));
+            wbase = __builtin_amdgcn_readlane(wbase, first);
+            slot = wbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        }
+        return slot;
+    };
     if (n_valid <= kk) {
 #pragma unroll
-        for (int j = 0; j < kPerThread; ++j)
-            if (valid(j)) sel[atomicAdd(&s_cnt, 1u)] = x[j];
+        for (int j = 0; j < kPerThread; ++j) {
+            const uint32_t pos = append_slot(valid(j));
+            if (valid(j)) sel[pos] = x[j];
+        }
         __syncthreads();
         for (int i = n_valid + t; i < kk; i += kSelThreads) sel[i] = 0;
     } else {
         const uint64_t ptop = prefix >> shift;
 #pragma unroll
-        for (int j = 0; j < kPerThread; ++j)
-            if (valid(j) && (x[j] >> shift) > ptop) sel[atomicAdd(&s_cnt, 1u)] = x[j];
+        for (int j = 0; j < kPerThread; ++j) {
+            const bool take = valid(j) && (x[j] >> shift) > ptop;
+            const uint32_t pos = append_slot(take);
+            if (take) sel[pos] = x[j];
+        }
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < kPerThread; ++j)
-            if (valid(j) && (x[j] >> shift) == ptop) {
-                const uint32_t pos = atomicAdd(&s_cnt, 1u);
-                if (pos < (uint32_t)kk) sel[pos] = x[j];
-            }
+        for (int j = 0; j < kPerThread; ++j) {
+            const bool take = valid(j) && (x[j] >> shift) == ptop;
+            const uint32_t pos = append_slot(take);
+            if (take && pos < (uint32_t)kk) sel[pos] = x[j];
+        }
     }
     const uint64_t *out_keys = sel;
     if (kk <= kRankSortMax) {
         // rank sort: an entry's output slot is the number of entries ranking ahead of it (a larger
-        // composite, or an equal one -- identical padding only -- at a lower position)
+        // composite, or an equal one -- identical padding only -- at a lower position); G threads
+        // count each entry's rank over disjoint parts of the list
+        const int G = kSelThreads / kk;
+        for (int i = t; i < kk; i += kSelThreads) rank_cnt[i] = 0;
         __syncthreads();
-        for (int i = t; i < kk; i += kSelThreads) {
+        if (t < G * kk) {
+            const int i = t / G, part = t % G;
             const uint64_t v = sel[i];
-            int rank = 0;
-            for (int j = 0; j < kk; ++j) {
+            const int j0 = part * kk / G, j1 = (part + 1) * kk / G;
+            uint32_t rank = 0;
+            for (int j = j0; j < j1; ++j) {
                 const uint64_t u = sel[j];
                 rank += (u > v) | ((u == v) & (j < i));
             }
-            ranked[rank] = v;
+            if (rank) atomicAdd(&rank_cnt[i], rank);
         }
+        __syncthreads();
+        for (int i = t; i < kk; i += kSelThreads) ranked[rank_cnt[i]] = sel[i];
         __syncthreads();
         out_keys = ranked;
     } else {

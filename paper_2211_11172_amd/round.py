@@ -2,10 +2,10 @@
 
 ``Round`` owns the model handles and every per-round device buffer (allocated once, with torch, at
 construction); ``Round.step`` enqueues the three hot-path calls of a round: the actor/critic
-forward, cost-model scoring and top-K (optionally merged into the running top-K).  The policy runs
-on a second stream when asked (`two_streams`): the two read disjoint inputs (the states and the
-candidates' statement features) and only top-K depends on scoring; by default all three run on
-one stream, because the scoring kernel keeps every CU busy on its own.
+forward, cost-model scoring and top-K (optionally merged into the running top-K).  The policy and
+scoring read disjoint inputs (the states and the candidates' statement features) and only top-K
+depends on scoring.  With `two_streams` the policy runs on a second stream after scoring, beside
+top-K; otherwise the three calls run in turn on one stream.
 """
 from __future__ import annotations
 
@@ -82,17 +82,23 @@ class Round:
                        harl.HARL_TOPK_MERGE if merge else 0, self.ws_topk, self.ws_topk_bytes, stream=stream)
 
     def step(self, b: Batch, merge=False, index_base=0):
-        """Enqueue one round on the current stream (policy on the side stream when enabled)."""
+        """Enqueue one round on the current stream.
+
+        With the side stream, scoring runs first on all CUs; the policy is then issued on the side
+        stream, where it runs beside top-K (a one-workgroup kernel on the main stream, which needs
+        the scores), and the main stream waits for both.  Without it, the three calls run in turn.
+        """
         main = torch.cuda.current_stream(self.device)
         if self.side is not None:
+            self.score(b, stream=main)
             self.side.wait_stream(main)
             self.policy(b, stream=self.side)
+            self.topk(b, merge=merge, index_base=index_base, stream=main)
+            main.wait_stream(self.side)
         else:
             self.policy(b, stream=main)
-        self.score(b, stream=main)
-        self.topk(b, merge=merge, index_base=index_base, stream=main)
-        if self.side is not None:
-            main.wait_stream(self.side)
+            self.score(b, stream=main)
+            self.topk(b, merge=merge, index_base=index_base, stream=main)
 
     def close(self):
         self.ens.close()
