@@ -429,20 +429,42 @@ __device__ __forceinline__ void group_commit(const uint4 (&pf)[NTW][PF], char *s
 // piece of tile i walked by slice s are stored at block (i + s) of RT floats: a slice covers a
 // contiguous run of tiles, so i + s grows strictly along the (slice, tile) pieces and (tiles +
 // slices) blocks hold them all; a tile's pieces are summed later in slice order.
-__device__ __forceinline__ int slice_of_block(int b, int nb) {
-    return (nb % 8 == 0) ? (b % 8) * (nb / 8) + b / 8 : b;
+// Tree groups: an ensemble too large for one XCD's L2 is split into G groups of consecutive trees
+// (G divides 8); the workgroups of XCD x all walk group x % G, so every XCD keeps only its group
+// L2-resident and a tile's features are staged once per group.  Within a group the work is sliced
+// as above.  Group g: trees [g Tg, g Tg + Tc) with Tg = ceil(T / G); its slices r = 0 .. nb/G - 1.
+__device__ __forceinline__ void block_slice(int b, int nb, int G, int &g, int &r) {
+    const int x = b % 8, j = b / 8;  // nb is a multiple of 8
+    g = x % G;
+    r = (x / G) * (nb / 8) + j;
+}
+
+// Trees of group g, its (tile, tree) pairs per slice, and the offset of its partial-sum blocks.
+__host__ __device__ __forceinline__ int group_trees(int T, int G, int g) {
+    const int tg = (T + G - 1) / G;
+    return T - g * tg < tg ? T - g * tg : tg;
+}
+__host__ __device__ __forceinline__ int64_t group_slice_len(int64_t tiles, int tc, int nbg) {
+    return (tiles * tc + nbg - 1) / nbg;
 }
 
 template <int D, int RPL, int TW, int NTW, bool NARROW>
 __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
-    const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees,
-    int T, int64_t V, int64_t L, float *__restrict__ partial) {
+    const float *__restrict__ X, int64_t ld, int n_rows, int F, int vec_ok, const uint4 *__restrict__ trees_all,
+    int T_all, int G, int tiles, float *__restrict__ partial_all) {
     constexpr int RT = 64 * RPL;
     constexpr int S16 = tree_stride_bytes(D) / 16;  // uint4 per packed tree
     constexpr int PF = (S16 + kWave - 1) / kWave;   // uint4 per lane per tree
     constexpr int STEP = NTW * TW;                  // trees between a wave's consecutive groups
     extern __shared__ __align__(16) char smem[];
-    const int s = slice_of_block(blockIdx.x, gridDim.x);
+    int g, s;
+    block_slice(blockIdx.x, gridDim.x, G, g, s);
+    const int nbg = gridDim.x / G;
+    const int T = group_trees(T_all, G, g);
+    if (T <= 0) return;  // whole workgroup
+    const uint4 *__restrict__ trees = trees_all + (int64_t)g * ((T_all + G - 1) / G) * S16;
+    float *__restrict__ partial = partial_all + (int64_t)g * (tiles + nbg) * RT;
+    const int64_t V = (int64_t)tiles * T, L = group_slice_len(tiles, T, nbg);
     const int64_t v_begin = (int64_t)s * L;
     const int64_t v_end = v_begin + L < V ? v_begin + L : V;
     if (v_begin >= v_end) return;  // whole workgroup: no barrier is skipped by part of it
@@ -657,13 +679,14 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
 }
 
 // K2: one wave per program (lane = statement row, looping for programs of more than 64 rows).
-// Each row sums its partials in a fixed order (fp64) -- grouped layout (L == 0): `groups` slots
-// partial[g * ldp + r]; sliced layout: the workgroups b = first..last whose slices cut the row's
-// tile i (RT rows, T trees), at partial[(i + b) * RT + r % RT] -- and the wave then sums its rows
-// with a fixed xor-butterfly, so the result does not depend on scheduling.
+// Each row sums its partials in a fixed order (fp64) -- grouped layout: `groups` slots
+// partial[g * ldp + r]; sliced layout: per tree group g, the slices b = first..last that cut the
+// row's tile i, at block (i + b) of the group's region -- and the wave then sums its rows with a
+// fixed xor-butterfly, so the result does not depend on scheduling.
 __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int RT, int T,
-                                                int64_t L, int groups, const int32_t *__restrict__ prog_ptr, int n_prog,
-                                                int n_rows, float base_score, float *__restrict__ prog_score,
+                                                int sliced, int groups, int tiles, int nbg,
+                                                const int32_t *__restrict__ prog_ptr, int n_prog, int n_rows,
+                                                float base_score, float *__restrict__ prog_score,
                                                 float *__restrict__ stmt_score) {
     const int p = blockIdx.x * 4 + threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
@@ -673,13 +696,19 @@ __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partia
     double acc = 0.0;
     for (int r = b + lane; r < e; r += kWave) {
         double s = 0.0;
-        if (L == 0) {
+        if (!sliced) {
             for (int gi = 0; gi < groups; ++gi) s += (double)partial[(int64_t)gi * ldp + r];
         } else {
             const int64_t tile = (uint32_t)r / (uint32_t)RT;
-            const int64_t first = tile * T / L, last = ((tile + 1) * T - 1) / L;
-            const float *src = partial + (int64_t)r;  // block (tile + wb), row r - tile * RT
-            for (int64_t wb = first; wb <= last; ++wb) s += (double)src[wb * RT];
+            for (int gi = 0; gi < groups; ++gi) {  // tree groups, then slices, in order
+                const int tc = group_trees(T, groups, gi);
+                if (tc <= 0) continue;
+                const int64_t L = group_slice_len(tiles, tc, nbg);
+                const int64_t first = tile * tc / L, last = ((tile + 1) * tc - 1) / L;
+                // block (tile + wb) of group gi, row r - tile * RT
+                const float *src = partial + (int64_t)gi * (tiles + nbg) * RT + (int64_t)r;
+                for (int64_t wb = first; wb <= last; ++wb) s += (double)src[wb * RT];
+            }
         }
         if (stmt_score) stmt_score[r] = (float)s;
         acc += s;
@@ -693,7 +722,7 @@ __global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partia
 // launch configuration
 // ---------------------------------------------------------------------------------------------
 using ChKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int, int, float *, int64_t);
-using WpKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int64_t, int64_t, float *);
+using WpKernel = void (*)(const float *, int64_t, int, int, int, const uint4 *, int, int, int, float *);
 
 struct ScoreCfg {
     bool wp;            // persistent per-wave tree slots (else grid of shared chunks)
@@ -793,21 +822,34 @@ int device_cus(int device) {
 // least 2 trees per wave per slice so the feature staging stays amortised.  The grid is a whole
 // number of XCD rounds (a multiple of 8); slices past the work are empty.
 struct WpSplit {
-    int64_t V, L, tiles;
-    int nb;
+    int64_t tiles;
+    int nb, G;  // workgroups (a multiple of 8) and tree groups
 };
+
+// Tree groups: the fewest (a power of 2 up to 8) whose share of the packed ensemble fits in about
+// 3 MB of an XCD's 4 MB L2.  HARL_SCORE_TREE_GROUPS overrides.
+int tree_groups(const harl_ensemble *E) {
+    int G = 1;
+    const int64_t bytes = (int64_t)E->n_trees * E->tree_stride;
+    while (G < 8 && 2 * G <= E->n_trees && bytes / G > (3 << 20)) G *= 2;
+    if (const char *env = std::getenv("HARL_SCORE_TREE_GROUPS")) {
+        const int o = std::atoi(env);
+        if ((o == 1 || o == 2 || o == 4 || o == 8) && o <= E->n_trees) G = o;
+    }
+    return G;
+}
 
 WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
     WpSplit w{};
-    const int64_t tiles = ceil_div(n_rows > 0 ? n_rows : 1, c.rows_per_tile);
-    w.tiles = tiles;
-    w.V = tiles * E->n_trees;
+    w.tiles = ceil_div(n_rows > 0 ? n_rows : 1, c.rows_per_tile);
+    w.G = tree_groups(E);
     const int per_cu = (int)(kLdsBytes / c.lds) > 0 ? (int)(kLdsBytes / c.lds) : 1;
     int64_t nb = (int64_t)device_cus(E->device) * per_cu;
+    // at least 2 trees per wave per slice, so the feature staging stays amortised
     const int64_t min_l = 2LL * c.b * c.c;
-    if (ceil_div(w.V, nb) < min_l) nb = ceil_div(w.V, min_l);
-    w.L = ceil_div(w.V, nb);
-    w.nb = (int)round_up(ceil_div(w.V, w.L), 8);
+    const int64_t vg = w.tiles * ceil_div(E->n_trees, w.G);  // pairs of the largest group
+    if (ceil_div(vg, nb / w.G > 0 ? nb / w.G : 1) < min_l) nb = ceil_div(vg, min_l) * w.G;
+    w.nb = (int)round_up(nb < 8 ? 8 : nb, 8);
     return w;
 }
 
@@ -845,7 +887,7 @@ size_t partial_floats(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows)
     const int64_t ldp = round_up(n_rows > 0 ? n_rows : 1, 64);
     if (c.wp) {
         const WpSplit w = wp_split(E, c, n_rows);
-        return (size_t)(w.tiles + w.nb) * c.rows_per_tile;
+        return (size_t)w.G * (w.tiles + w.nb / w.G) * c.rows_per_tile;
     }
     return (size_t)choose_groups(E, n_rows, c) * ldp;
 }
@@ -867,7 +909,7 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
     float *partial = static_cast<float *>(ws);
     const unsigned seg_grid = (unsigned)ceil_div(n_prog, 4);  // one wave per program
     if (n_rows == 0) {
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, 64, 1, (int64_t)0, 0, prog_ptr,
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, 64, 1, 0, 0, 1, 8, prog_ptr,
                            n_prog, 0, E->base_score, prog_score, stmt_score);
         HARL_HIP_CHECK(hipGetLastError());
         return HARL_OK;
@@ -880,10 +922,12 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
     if (c.wp) {
         const WpSplit w = wp_split(E, c, n_rows);
         hipLaunchKernelGGL(reinterpret_cast<WpKernel>(const_cast<void *>(c.kern)), dim3((unsigned)w.nb), dim3(c.threads),
-                           c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.V, w.L, partial);
+                           c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.G, (int)w.tiles,
+                           partial);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees, w.L, 0,
-                           prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees, 1,
+                           w.G, (int)w.tiles, w.nb / w.G, prog_ptr, n_prog, n_rows, E->base_score, prog_score,
+                           stmt_score);
     } else {
         const int G = choose_groups(E, n_rows, c);
         const int tiles = (int)ceil_div(n_rows, c.rows_per_tile);
@@ -893,8 +937,8 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
                            dim3(c.threads), c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees,
                            tpg, groups, partial, ldp);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees,
-                           (int64_t)0, groups, prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees, 0,
+                           groups, tiles, 8, prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
     }
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;

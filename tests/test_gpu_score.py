@@ -52,6 +52,16 @@ def test_depths_exact_many_tiles(depth):
     _check(cfg)
 
 
+@pytest.mark.parametrize("groups", [2, 4, 8])
+def test_tree_groups_exact(groups, monkeypatch):
+    # the ensemble split into tree groups walked by different XCDs (the split large ensembles get
+    # so that each group stays L2-resident), forced here on a small ensemble with a ragged tree
+    # count; exact leaves make every grouping bit-identical to the oracle
+    monkeypatch.setenv("HARL_SCORE_TREE_GROUPS", str(groups))
+    cfg = get_config("tiny", exact=True).with_(depth=8, n_trees=45, n_prog=900, p_nan=0.1, name="groups%d" % groups)
+    _check(cfg)
+
+
 def test_standard_config_exact():
     _check(get_config("standard", exact=True))
 
