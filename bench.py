@@ -99,11 +99,30 @@ def main():
     cfg = get_config(args.config)
     ens, pol, b = gen_ensemble(cfg), gen_policy(cfg), gen_batch(cfg)
     dev = torch.device("cuda:0")
+    # A streamed search holds all its batches in HBM (16 x 1.4 GB for the streamed workload); a
+    # step is the whole search: reset the running top-K, then one round per batch, each merged into
+    # it with the batch's global index base.  Batch 0 also serves the counter probe and the oracle.
+    n_batches = 1 if args.counter_probe else cfg.n_batches
+    batches = [upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)]
+    max_rows = b["n_rows"]
+    for i in range(1, n_batches):
+        bi = gen_batch(cfg, batch=i)
+        max_rows = max(max_rows, bi["n_rows"])
+        batches.append(upload_batch(bi["features"], bi["prog_ptr"], bi["states"], device=dev))
+        del bi
     # a workload with a softmax output (policy-heavy, streamed) produces the probabilities every step
-    rnd = Round(ens, pol, b["n_rows"], cfg.n_prog, cfg.top_k, device=dev, two_streams=args.two_streams,
+    rnd = Round(ens, pol, max_rows, cfg.n_prog, cfg.top_k, device=dev, two_streams=args.two_streams,
                 want_probs=cfg.softmax)
-    batch = upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)
+    batch = batches[0]
     main_stream = torch.cuda.current_stream(dev)
+
+    def step():
+        if n_batches == 1:
+            rnd.step(batch)
+            return
+        rnd.reset_running()
+        for i, db in enumerate(batches):
+            rnd.step(db, merge=True, index_base=i * cfg.n_prog)
 
     if args.counter_probe:
         n_copy = 256 << 20
@@ -132,7 +151,7 @@ def main():
     cap.wait_stream(main_stream)
     with torch.cuda.stream(cap):
         for _ in range(max(args.warmup, 1)):
-            rnd.step(batch)
+            step()
     main_stream.wait_stream(cap)
     torch.cuda.synchronize()
     eager_scores = rnd.prog_score.clone()
@@ -141,7 +160,7 @@ def main():
     if not args.no_graph:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            rnd.step(batch)
+            step()
         for _ in range(args.warmup):
             graph.replay()
         torch.cuda.synchronize()
@@ -153,7 +172,7 @@ def main():
         if graph is not None:
             graph.replay()
         else:
-            rnd.step(batch)
+            step()
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     same = bool(torch.equal(rnd.prog_score, eager_scores) and torch.equal(rnd.top_index, eager_top))
@@ -186,7 +205,7 @@ def main():
     ms_per_step = el * 1e3 / args.steps
     out = {
         "metric": "candidate schedules scored+stepped/sec",
-        "value": n_prog * args.steps / el,
+        "value": n_prog * n_batches * args.steps / el,
         "unit": "candidates/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -197,11 +216,17 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if cfg.pol_dtype == "f32" else "f32-trees+bf16-mlp",
         "data": "synthetic",
-        "config": {"workload": "%s round: %d candidates, U{1..%d} statements (%d rows) x %d fp32 features, "
-                               "%d trees depth %d, MLP %s %d-%d-%d->%d+1, top-%d" % (
-                                   cfg.name, n_prog, cfg.s_max, n_rows, cfg.n_features, cfg.n_trees, cfg.depth,
-                                   cfg.pol_dtype, cfg.pol_s, cfg.pol_h1, cfg.pol_h2, cfg.pol_a, cfg.top_k),
-                   "global_batch": n_prog, "parallelism": "single-gpu"},
+        "config": {"workload": "%s round: %s candidates, U{1..%d} statements (%d rows%s) x %d fp32 features%s, "
+                               "%d trees depth %d, MLP %s %d-%d-%d->%d+1%s, %s" % (
+                                   cfg.name, ("%d" % n_prog) if n_batches == 1 else
+                                   "%d x %d = %d" % (n_batches, n_prog, n_batches * n_prog), cfg.s_max, n_rows,
+                                   "" if n_batches == 1 else " in batch 0", cfg.n_features,
+                                   "" if cfg.p_nan == 0 else " (%d%% NaN)" % round(100 * cfg.p_nan),
+                                   cfg.n_trees, cfg.depth, cfg.pol_dtype, cfg.pol_s, cfg.pol_h1, cfg.pol_h2, cfg.pol_a,
+                                   " with softmax" if cfg.softmax else "",
+                                   ("top-%d" % cfg.top_k) if n_batches == 1 else
+                                   "running top-%d merged across batches" % cfg.top_k),
+                   "global_batch": n_prog * n_batches, "parallelism": "single-gpu"},
         "roofline": {"bound": "alu", "kernel": "k_tree_score (+k_segsum) via harl_score_round",
                      "achieved": gvisits, "peak": PEAK_GVISITS, "unit": "Gvisit/s", "frac": gvisits / PEAK_GVISITS,
                      "traffic": None, "us_per_launch": score_ms * 1e3,

@@ -32,6 +32,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <vector>
 
@@ -491,12 +493,22 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     const bool bf = P->dtype == HARL_BF16;
     // Large bf16 batches of the shapes it covers go to the 128-states-per-workgroup kernel
     if (P->x32_stream && B >= kX32MinBatch) return policy_x32_launch(P, states, B, action, value, probs, logits, stream);
-    // Large bf16 batches: 64 states per workgroup share every weight fragment (4 state groups), 4
-    // waves of 4-tile groups with deep weight prefetch.  Otherwise 16 states per workgroup and 8
-    // waves, so that a small batch still spreads over every CU.
-    int nsg = (bf && B >= 16 * 1024) ? 4 : 1;
-    if (policy_lds_bytes(P, nsg, 4) > 160 * 1024) nsg = 1;
-    const int u = nsg == 4 ? 4 : 8;
+    // Large batches share every weight fragment among several state groups (bf16: 4 groups of 16
+    // states, 4 waves; fp32: 2 groups, 8 waves -- measured best on 65,536 states); small batches
+    // use 16 states per workgroup so that they still spread over every CU.
+    int nsg = B >= 16 * 1024 ? (bf ? 4 : 2) : 1;
+    int u = nsg == 4 ? 4 : 8;
+    if (const char *env = std::getenv("HARL_POLICY_CFG")) {  // "nsg,u" (tuning sweeps)
+        int e_nsg = 0, e_u = 0;
+        if (std::sscanf(env, "%d,%d", &e_nsg, &e_u) == 2) {
+            nsg = e_nsg;
+            u = e_u;
+        }
+    }
+    if (policy_lds_bytes(P, nsg, u) > 160 * 1024) {
+        nsg = 1;
+        u = 8;
+    }
     const size_t lds = policy_lds_bytes(P, nsg, u);
     const unsigned grid = (unsigned)ceil_div(B, 16 * nsg);
     const int ht = P->hap / 16;
@@ -506,6 +518,7 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     if (bf == BF && nsg == NSG && htm == HTM && u == U) \
         kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM, U, TP, kRing>);
     HARL_POL(false, 1, 2, 8, 2) HARL_POL(false, 1, 5, 8, 2) HARL_POL(false, 1, 8, 8, 2)
+    HARL_POL(false, 2, 2, 8, 2) HARL_POL(false, 2, 5, 8, 2) HARL_POL(false, 2, 8, 8, 2)
     HARL_POL(true, 1, 2, 8, 2) HARL_POL(true, 1, 5, 8, 2) HARL_POL(true, 1, 8, 8, 2)
     HARL_POL(true, 4, 2, 4, 4) HARL_POL(true, 4, 5, 4, 4) HARL_POL(true, 4, 8, 4, 4)
 #undef HARL_POL

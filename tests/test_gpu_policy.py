@@ -95,6 +95,13 @@ def test_large_batch_wide_heads(a):
     _check(cfg, B=_LARGE + 3)
 
 
+@pytest.mark.parametrize("exact", [True, False])
+def test_large_fp32_batch(exact):
+    # fp32 batches of 16384 states and more share weight fragments between two state groups
+    cfg = mini_config(pol_s=64, pol_h1=256, pol_h2=200, pol_a=24, exact=exact)
+    _check(cfg, B=_LARGE + 45)
+
+
 def test_large_batch_policy_heavy_values():
     # the policy-heavy network with its own (non-integer) weights and states
     _check(get_config("policy_heavy"), B=_LARGE + 129)
