@@ -30,6 +30,23 @@ LDS_BYTES_PER_CLK = 152.0
 LDS_BYTES_PER_VISIT = 12.0
 PEAK_GVISITS = N_CU * CLOCK_GHZ * LDS_BYTES_PER_CLK / LDS_BYTES_PER_VISIT  # G visits / s
 
+# HBM bytes of one harl_score_round call (tree walk + segmented sum), measured with rocprofv3 --pmc
+# FETCH_SIZE and WRITE_SIZE over 3 eager calls and scaled by what the same counters read for a
+# 256 MiB device-to-device copy (x2.000 for FETCH_SIZE, x1.000 for WRITE_SIZE).  Keyed by workload
+# and by the SHA-256 of the scoring source the counters were taken with: any other source reports
+# null.
+SCORE_TRAFFIC_BYTES = {
+    ("standard", "aa68cf47d905a87ae6302d79c52aefb2f184f4bb31b3bac80c33f6b3762b9354"): 58.75e6,
+}
+
+
+def score_traffic(cfg_name):
+    import hashlib
+    src = os.path.join(ROOT, "paper_2211_11172_amd", "csrc", "score.hip")
+    with open(src, "rb") as f:
+        digest = hashlib.sha256(f.read()).hexdigest()
+    return SCORE_TRAFFIC_BYTES.get((cfg_name, digest))
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -229,7 +246,8 @@ def main():
                    "global_batch": n_prog * n_batches, "parallelism": "single-gpu"},
         "roofline": {"bound": "alu", "kernel": "k_tree_score (+k_segsum) via harl_score_round",
                      "achieved": gvisits, "peak": PEAK_GVISITS, "unit": "Gvisit/s", "frac": gvisits / PEAK_GVISITS,
-                     "traffic": None, "us_per_launch": score_ms * 1e3,
+                     "traffic": score_traffic(cfg.name), "traffic_unit": "bytes per launch",
+                     "us_per_launch": score_ms * 1e3,
                      "hbm_gbs": hbm_bytes / (score_ms * 1e-3) / 1e9,
                      "hbm_frac": hbm_bytes / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
         "graph_replay": graph is not None, "graph_matches_eager": same,

@@ -131,7 +131,7 @@ int harl_score_round(const harl_ensemble *ens, const float *d_feat, int64_t ld, 
  * patterns (uint16) for HARL_BF16.  Biases are fp32.  A HARL_BF16 policy takes bf16 states, uses
  * bf16 x bf16 products with fp32 accumulation, and rounds h1 and h2 to bf16 (nearest, ties to
  * even) after bias and ReLU; a HARL_F32 policy is fp32 throughout.
- * Limits: 1 <= s <= 1024; 1 <= h1, h2 <= 4096; 1 <= a <= 255.
+ * Limits: 1 <= s <= 1024; 1 <= h1, h2 <= 4096; 1 <= a <= 127.
  */
 typedef struct {
     harl_dtype dtype;
