@@ -62,6 +62,10 @@ def parse():
                          "and harl_topk; prints sizes and exits")
     ap.add_argument("--no-graph", action="store_true", help="launch every call from the host instead of "
                     "replaying a captured graph of the round")
+    ap.add_argument("--ingest", action="store_true",
+                    help="feature-ingest calibration: harl_score_round over the throughput round's 2.13 M "
+                         "statement rows (1.4 GB of features) with shallow ensembles (node visits per row "
+                         "<= 16), so that staging the features dominates; prints HBM GB/s and exits")
     ap.add_argument("--two-streams", action="store_true",
                     help="run the policy on a second stream after scoring, beside top-K (default: the "
                          "three calls in turn on one stream, which measured faster on the standard round)")
@@ -101,12 +105,60 @@ def cpu_baseline(cfg, ens, pol, b, budget_s):
                     sample, n_prog, cfg.name, int(sp[-1]), done // sample, el))
 
 
+def ingest_calibration(args):
+    """Time harl_score_round on the throughput round's features with ensembles whose walk is
+    negligible (T x D <= 16 node visits per row): the call is then bound by streaming 656 B of
+    features per statement row from HBM into LDS."""
+    import torch
+
+    from paper_2211_11172_amd.round import Round, upload_batch
+    from synth import gen_batch, gen_ensemble, gen_policy, get_config
+
+    base = get_config("throughput")
+    b = gen_batch(base)
+    dev = torch.device("cuda:0")
+    batch = upload_batch(b["features"], b["prog_ptr"], b["states"], device=dev)
+    main_stream = torch.cuda.current_stream(dev)
+    n_rows, n_prog = b["n_rows"], base.n_prog
+    alg_bytes = n_rows * base.n_features * 4 + (n_prog + 1) * 4 + n_prog * 4
+    pol = gen_policy(base)
+    rows = []
+    for n_trees, depth in ((16, 1), (4, 4), (2, 8)):
+        cfg = base.with_(n_trees=n_trees, depth=depth, name="ingest-%dx%d" % (n_trees, depth))
+        rnd = Round(gen_ensemble(cfg), pol, n_rows, n_prog, base.top_k, device=dev)
+        for _ in range(max(args.warmup, 1)):
+            rnd.score(batch)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(args.steps):
+                rnd.score(batch)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main_stream)
+        g.replay()
+        e1.record(main_stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / args.steps * 1e3
+        gbs = alg_bytes / (us * 1e-6) / 1e9
+        rows.append({"trees": n_trees, "depth": depth, "us_per_launch": us, "hbm_gbs": gbs,
+                     "hbm_frac": gbs / PEAK_HBM_GBS})
+        print("ingest %d trees x depth %d: %.1f us, %.0f GB/s" % (n_trees, depth, us, gbs), file=sys.stderr, flush=True)
+        rnd.close()
+    print(json.dumps({"metric": "feature ingest HBM bandwidth (harl_score_round, shallow ensembles)",
+                      "rows": n_rows, "algorithmic_bytes": alg_bytes, "peak_gbs": PEAK_HBM_GBS,
+                      "steps": args.steps, "results": rows}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (candidates shard with "
               "one all-gather of the top-k; see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+    if args.ingest:
+        ingest_calibration(args)
+        return
     import numpy as np
     import torch
 

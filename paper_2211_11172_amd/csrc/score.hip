@@ -262,22 +262,23 @@ __device__ __forceinline__ void walk_trees(const uint32_t (&tb)[NT_], const Tree
     for (int c = 0; c < NC; ++c) acc[c % R] += (double)leaf_of<NAN_AWARE>(x[c], lv[c], fw[c]);
 }
 // Item i of a row tile ([F][RT] fp32 in LDS, RT/4 float4 per feature): rows row0 + 4*(i % V) ..
-// + 3 of feature i / V, zero past n_rows.
+// + 3 of feature i / V.  tile_item_vec: one 16-byte load (the tile lies below n_rows and ld, the
+// base are 16-byte aligned); tile_item_any: four loads at row indices clamped to n_rows - 1
+// (n_rows >= 1), zero past n_rows -- branch-free, for the ragged last tile or an unaligned ld.
+// Which one is used is decided once per tile, so full tiles compile to plain vector loads.
 template <int V>
-__device__ __forceinline__ float4 tile_item(const float *__restrict__ X, int64_t ld, int n_rows, int vec_ok, int row0,
-                                            int i) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+__device__ __forceinline__ float4 tile_item_vec(const float *__restrict__ X, int64_t ld, int row0, int i) {
     const int f = i / V, r = row0 + 4 * (i % V);
-    const float *src = X + (int64_t)f * ld + r;
-    if (vec_ok && r + 3 < n_rows) {
-        v = *reinterpret_cast<const float4 *>(src);
-    } else {
-        if (r + 0 < n_rows) v.x = src[0];
-        if (r + 1 < n_rows) v.y = src[1];
-        if (r + 2 < n_rows) v.z = src[2];
-        if (r + 3 < n_rows) v.w = src[3];
-    }
-    return v;
+    return *reinterpret_cast<const float4 *>(X + (int64_t)f * ld + r);
+}
+
+template <int V>
+__device__ __forceinline__ float4 tile_item_any(const float *__restrict__ X, int64_t ld, int n_rows, int row0, int i) {
+    const int f = i / V, r = row0 + 4 * (i % V);
+    const float *src = X + (int64_t)f * ld;
+    const int last = n_rows - 1;
+    const float x = src[min(r, last)], y = src[min(r + 1, last)], z = src[min(r + 2, last)], w = src[min(r + 3, last)];
+    return make_float4(r < n_rows ? x : 0.f, r + 1 < n_rows ? y : 0.f, r + 2 < n_rows ? z : 0.f, r + 3 < n_rows ? w : 0.f);
 }
 
 __device__ __forceinline__ int any_nan(float4 v) {
@@ -295,13 +296,22 @@ __device__ __forceinline__ int stage_features(char *smem, const float *__restric
     constexpr int B = 4;
     int has_nan = 0;
     const int total = F * V;
+    const bool full = vec_ok && row0 + RT <= n_rows;
     float4 *dst = reinterpret_cast<float4 *>(smem);
     for (int i0 = threadIdx.x; i0 < total; i0 += B * NT) {
         float4 v[B];
+        if (full) {
 #pragma unroll
-        for (int j = 0; j < B; ++j) {
-            const int i = i0 + j * NT;
-            v[j] = i < total ? tile_item<V>(X, ld, n_rows, vec_ok, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int j = 0; j < B; ++j) {
+                const int i = i0 + j * NT;
+                v[j] = i < total ? tile_item_vec<V>(X, ld, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const int i = i0 + j * NT;
+                v[j] = i < total ? tile_item_any<V>(X, ld, n_rows, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
         }
 #pragma unroll
         for (int j = 0; j < B; ++j) {
@@ -325,10 +335,18 @@ __device__ __forceinline__ void tile_fetch(float4 (&xf)[NPF], const float *__res
                                            int F, int vec_ok, int row0) {
     constexpr int V = RT / 4;
     const int total = F * V;
+    if (vec_ok && row0 + RT <= n_rows) {
 #pragma unroll
-    for (int j = 0; j < NPF; ++j) {
-        const int i = threadIdx.x + j * NT;
-        xf[j] = i < total ? tile_item<V>(X, ld, n_rows, vec_ok, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < NPF; ++j) {
+            const int i = threadIdx.x + j * NT;
+            xf[j] = i < total ? tile_item_vec<V>(X, ld, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < NPF; ++j) {
+            const int i = threadIdx.x + j * NT;
+            xf[j] = i < total ? tile_item_any<V>(X, ld, n_rows, row0, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
 }
 
@@ -523,7 +541,19 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
     int t0 = piece_lo(tile), t1 = piece_hi(tile);
     int t = t0 + wid;
     group_fetch<S16, PF, NTW, TW>(pf, trees, t, t1, lane);   // overlaps the feature staging
-    int has_nan = __builtin_amdgcn_readfirstlane(stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, tile * RT, flags));
+    int has_nan;
+    if (x_regs) {  // the whole first tile in one batch of loads
+        tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, tile * RT);
+        tile_commit<RT, NT, NPX>(xf, smem, F, flags);
+        __syncthreads();
+        has_nan = __builtin_amdgcn_readfirstlane(flags[0]);
+        if (n_pieces > 1) tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, (tile + dir) * RT);
+    } else {
+        has_nan = __builtin_amdgcn_readfirstlane(stage_features<RT, NT>(smem, X, ld, n_rows, F, vec_ok, tile * RT, flags));
+    }
+    // With x_regs, xf holds the loads of the next tile from the commit of the current one on (its
+    // fetch is issued as soon as the registers are free), so the stream of feature tiles keeps a
+    // tile in flight through the barriers and row-sum reduction between pieces.
     for (int piece = 0;; ++piece) {
         const int row0 = tile * RT;
         if (threadIdx.x == 0) {
@@ -535,7 +565,6 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
         group_fetch<S16, PF, NTW, TW>(pf, trees, t + STEP, t1, lane);
         const bool next = piece + 1 < n_pieces;
         const int ntile = tile + dir;
-        if (next && x_regs) tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, ntile * RT);
         double acc[RPL];
 #pragma unroll
         for (int r = 0; r < RPL; ++r) acc[r] = 0.0;
@@ -577,7 +606,10 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_wp(
         if (next) group_fetch<S16, PF, NTW, TW>(pf, trees, nt0 + wid, nt1, lane);  // first trees of the next piece
         __syncthreads();  // B1: every wave is done with the tile and its slots
         reduce_put<RPL>(red, acc, wid, lane);
-        if (next && x_regs) tile_commit<RT, NT, NPX>(xf, smem, F, flags + ((piece + 1) & 1));
+        if (next && x_regs) {
+            tile_commit<RT, NT, NPX>(xf, smem, F, flags + ((piece + 1) & 1));
+            if (piece + 2 < n_pieces) tile_fetch<RT, NT, NPX>(xf, X, ld, n_rows, F, vec_ok, (ntile + dir) * RT);
+        }
         __syncthreads();  // B2: row sums and the next tile are in LDS
         reduce_sum<RPL, TW>(red, row0, n_rows, partial + ((int64_t)tile + s) * RT);
         if (!next) break;
@@ -678,45 +710,132 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_ch(
                        partial + (int64_t)g * ldp + row0);
 }
 
-// K2: one wave per program (lane = statement row, looping for programs of more than 64 rows).
-// Each row sums its partials in a fixed order (fp64) -- grouped layout: `groups` slots
-// partial[g * ldp + r]; sliced layout: per tree group g, the slices b = first..last that cut the
-// row's tile i, at block (i + b) of the group's region -- and the wave then sums its rows with a
-// fixed xor-butterfly, so the result does not depend on scheduling.
-__global__ __launch_bounds__(256) void k_segsum(const float *__restrict__ partial, int64_t ldp, int RT, int T,
-                                                int sliced, int groups, int tiles, int nbg,
-                                                const int32_t *__restrict__ prog_ptr, int n_prog, int n_rows,
-                                                float base_score, float *__restrict__ prog_score,
-                                                float *__restrict__ stmt_score) {
-    const int p = blockIdx.x * 4 + threadIdx.x / kWave;
-    const int lane = threadIdx.x % kWave;
-    if (p >= n_prog) return;  // whole wave
-    const int b = min(max(prog_ptr[p], 0), n_rows);
-    const int e = min(max(prog_ptr[p + 1], b), n_rows);
+// K2: per-program sums.  A workgroup owns `ppw` (<= 64) consecutive programs and walks the rows
+// they cover in chunks of kSegChunk rows.  Every thread forms the sums s_r of its rows of a chunk
+// into LDS, in a fixed order in fp64 -- grouped layout: the `groups` slots partial[g * ldp + r];
+// sliced layout: per tree group g, the slices b = first..last that cut the row's tile i, at block
+// (i + b) of the group's region, with (first, last) computed once per (tile, group) of the chunk.
+// Thread j then adds the rows of program j that lie in the chunk, in row order.  No sum depends on
+// scheduling.  A row's first two slices are loaded for all of a thread's rows at once; a tile cut
+// by more than two slices of one group (small rounds) takes the remaining ones in a loop.
+constexpr int kSegThreads = 256, kSegChunk = 2048, kSegRows = kSegChunk / kSegThreads;
+constexpr int kSegMaxProg = 64, kSegMaxGroups = 8, kSegMaxTiles = kSegChunk / 64 + 1;
+
+__global__ __launch_bounds__(kSegThreads) void k_segsum(const float *__restrict__ partial, int64_t ldp, int rt_shift,
+                                                        int T, int sliced, int groups, int tiles, int nbg,
+                                                        const int32_t *__restrict__ prog_ptr, int n_prog, int n_rows,
+                                                        int ppw, float base_score, float *__restrict__ prog_score,
+                                                        float *__restrict__ stmt_score) {
+    __shared__ double srow[kSegChunk];
+    __shared__ int2 span[kSegMaxGroups * kSegMaxTiles];
+    __shared__ int pb[kSegMaxProg], pe[kSegMaxProg], range[2];
+    const int t = threadIdx.x;
+    const int p0 = blockIdx.x * ppw;
+    const int np = min(ppw, n_prog - p0);
+    const int RT = 1 << rt_shift;
+    if (t < kWave) {  // wave 0: the programs' clamped bounds and the rows they cover
+        int b = n_rows, e = 0;
+        if (t < np) {
+            b = min(max(prog_ptr[p0 + t], 0), n_rows);
+            e = min(max(prog_ptr[p0 + t + 1], b), n_rows);
+            pb[t] = b;
+            pe[t] = e;
+        }
+        int lo = b, hi = e;
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) {
+            lo = min(lo, __shfl_xor(lo, m, kWave));
+            hi = max(hi, __shfl_xor(hi, m, kWave));
+        }
+        if (t == 0) {
+            range[0] = lo;
+            range[1] = hi;
+        }
+    }
+    __syncthreads();
+    const int lo = range[0], hi = range[1];
     double acc = 0.0;
-    for (int r = b + lane; r < e; r += kWave) {
-        double s = 0.0;
-        if (!sliced) {
-            for (int gi = 0; gi < groups; ++gi) s += (double)partial[(int64_t)gi * ldp + r];
-        } else {
-            const int64_t tile = (uint32_t)r / (uint32_t)RT;
-            for (int gi = 0; gi < groups; ++gi) {  // tree groups, then slices, in order
+    for (int c0 = lo; c0 < hi; c0 += kSegChunk) {
+        const int c1 = min(c0 + kSegChunk, hi);
+        const int tile0 = c0 >> rt_shift;
+        if (sliced) {
+            const int ntc = ((c1 - 1) >> rt_shift) - tile0 + 1;
+            for (int i = t; i < ntc * groups; i += kSegThreads) {
+                const int gi = i / ntc, ti = i - gi * ntc;
+                const int64_t tile = tile0 + ti;
                 const int tc = group_trees(T, groups, gi);
-                if (tc <= 0) continue;
-                const int64_t L = group_slice_len(tiles, tc, nbg);
-                const int64_t first = tile * tc / L, last = ((tile + 1) * tc - 1) / L;
-                // block (tile + wb) of group gi, row r - tile * RT
-                const float *src = partial + (int64_t)gi * (tiles + nbg) * RT + (int64_t)r;
-                for (int64_t wb = first; wb <= last; ++wb) s += (double)src[wb * RT];
+                int2 sp = make_int2(0, -1);
+                if (tc > 0) {
+                    const int64_t L = group_slice_len(tiles, tc, nbg);
+                    sp = make_int2((int)(tile * tc / L), (int)(((tile + 1) * tc - 1) / L));
+                }
+                span[gi * kSegMaxTiles + ti] = sp;
+            }
+            __syncthreads();
+        }
+        double s[kSegRows];
+#pragma unroll
+        for (int k = 0; k < kSegRows; ++k) s[k] = 0.0;
+        for (int gi = 0; gi < groups; ++gi) {
+            const float *__restrict__ src = sliced ? partial + (int64_t)gi * (tiles + nbg) * RT : partial + (int64_t)gi * ldp;
+            float v0[kSegRows], v1[kSegRows];
+            int2 sp[kSegRows];
+#pragma unroll
+            for (int k = 0; k < kSegRows; ++k) {
+                const int r = c0 + t + k * kSegThreads;
+                v0[k] = v1[k] = 0.f;
+                sp[k] = make_int2(0, 0);
+                if (r < c1) {
+                    if (sliced) {
+                        sp[k] = span[gi * kSegMaxTiles + ((r >> rt_shift) - tile0)];
+                        // slice b's piece of row r (tile i) is at block (i + b): src + r + b * RT
+                        const float *q = src + r + (int64_t)sp[k].x * RT;
+                        if (sp[k].y >= sp[k].x) v0[k] = q[0];
+                        if (sp[k].y > sp[k].x) v1[k] = q[RT];
+                    } else {
+                        v0[k] = src[r];
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kSegRows; ++k) {
+                s[k] += (double)v0[k];
+                s[k] += (double)v1[k];
+                const int r = c0 + t + k * kSegThreads;
+                if (sliced && r < c1 && sp[k].y > sp[k].x + 1) {
+                    const float *q = src + r + (int64_t)sp[k].x * RT;
+                    for (int j = 2; j <= sp[k].y - sp[k].x; ++j) s[k] += (double)q[(int64_t)j * RT];
+                }
             }
         }
-        if (stmt_score) stmt_score[r] = (float)s;
-        acc += s;
-    }
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-    if (lane == 0) prog_score[p] = (float)((double)base_score + acc);
+        for (int k = 0; k < kSegRows; ++k) {
+            const int r = c0 + t + k * kSegThreads;
+            if (r < c1) {
+                srow[r - c0] = s[k];
+                if (stmt_score) stmt_score[r] = (float)s[k];
+            }
+        }
+        __syncthreads();
+        if (t < np) {
+            const int b = max(pb[t], c0) - c0, e = min(pe[t], c1) - c0;
+            int r = b;
+            for (; r + 4 <= e; r += 4) {
+                const double a0 = srow[r], a1 = srow[r + 1], a2 = srow[r + 2], a3 = srow[r + 3];
+                acc += a0;
+                acc += a1;
+                acc += a2;
+                acc += a3;
+            }
+            for (; r < e; ++r) acc += srow[r];
+        }
+        __syncthreads();  // srow and span are rewritten by the next chunk
+    }
+    if (t < np) prog_score[p0 + t] = (float)((double)base_score + acc);
 }
+
+// Programs per workgroup of K2: enough workgroups to cover the machine at every batch size.
+int segsum_ppw(int32_t n_prog) { return n_prog >= 32768 ? 64 : 16; }
 
 // ---------------------------------------------------------------------------------------------
 // launch configuration
@@ -907,10 +1026,12 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
     if (ws_bytes < partial_floats(E, c, n_rows) * sizeof(float))
         return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
     float *partial = static_cast<float *>(ws);
-    const unsigned seg_grid = (unsigned)ceil_div(n_prog, 4);  // one wave per program
+    if (n_prog <= 0) return HARL_OK;
+    const int ppw = segsum_ppw(n_prog);
+    const unsigned seg_grid = (unsigned)ceil_div(n_prog, ppw);
     if (n_rows == 0) {
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, 64, 1, 0, 0, 1, 8, prog_ptr,
-                           n_prog, 0, E->base_score, prog_score, stmt_score);
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(kSegThreads), 0, stream, partial, ldp, 6, 1, 0, 0, 1, 8,
+                           prog_ptr, n_prog, 0, ppw, E->base_score, prog_score, stmt_score);
         HARL_HIP_CHECK(hipGetLastError());
         return HARL_OK;
     }
@@ -925,9 +1046,9 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
                            c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees, w.G, (int)w.tiles,
                            partial);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees, 1,
-                           w.G, (int)w.tiles, w.nb / w.G, prog_ptr, n_prog, n_rows, E->base_score, prog_score,
-                           stmt_score);
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(kSegThreads), 0, stream, partial, ldp,
+                           __builtin_ctz((unsigned)c.rows_per_tile), E->n_trees, 1, w.G, (int)w.tiles, w.nb / w.G,
+                           prog_ptr, n_prog, n_rows, ppw, E->base_score, prog_score, stmt_score);
     } else {
         const int G = choose_groups(E, n_rows, c);
         const int tiles = (int)ceil_div(n_rows, c.rows_per_tile);
@@ -937,8 +1058,9 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
                            dim3(c.threads), c.lds, stream, X, ld, n_rows, E->n_features, vec_ok, trees, E->n_trees,
                            tpg, groups, partial, ldp);
         HARL_HIP_CHECK(hipGetLastError());
-        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(256), 0, stream, partial, ldp, c.rows_per_tile, E->n_trees, 0,
-                           groups, tiles, 8, prog_ptr, n_prog, n_rows, E->base_score, prog_score, stmt_score);
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(kSegThreads), 0, stream, partial, ldp,
+                           __builtin_ctz((unsigned)c.rows_per_tile), E->n_trees, 0, groups, tiles, 8, prog_ptr, n_prog,
+                           n_rows, ppw, E->base_score, prog_score, stmt_score);
     }
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;

@@ -62,6 +62,16 @@ def test_tree_groups_exact(groups, monkeypatch):
     _check(cfg)
 
 
+@pytest.mark.parametrize("trees_depth", [(16, 1), (4, 4), (2, 8), (1, 5)])
+def test_shallow_ensembles_many_tiles(trees_depth):
+    """Few, shallow trees over many row tiles: every slice spans many tiles (the ingest-bound
+    shape); 164 features, 10 % missing values."""
+    n_trees, depth = trees_depth
+    cfg = get_config("tiny").with_(n_trees=n_trees, depth=depth, n_prog=2500, s_max=16, p_nan=0.1,
+                                   name="shallow-%dx%d" % trees_depth)
+    _check(cfg)
+
+
 def test_standard_config_exact():
     _check(get_config("standard", exact=True))
 
