@@ -85,29 +85,17 @@ struct PolicyArgs {
     float *value, *probs, *logits;
 };
 
-// One dense layer for this wave: `n_tiles` output tiles of 16 units starting at tile `t0`, each a
-// sum over KG k-groups (KG a multiple of RING), computed TP tiles at a time (TP independent
-// accumulator chains sharing every B fragment).  The wave's iterations (tile group, k-group) run
-// in order; the A fragments of iteration it + RING are loaded from `A` (packed [tile][g][lane] x
-// 16 B) into ring slot it % RING as soon as iteration it has issued its MFMAs, and the B
-// fragments of the next k-group are read from the LDS activation rows `in` (row stride
-// `in_stride` bytes) into the other half of a double buffer.  done(first_tile, acc[TP][NSG])
-// consumes each finished group.
-template <bool BF16, int NSG, int TP, int RING, typename Done>
-__device__ __forceinline__ void dense_layer(const uint4 *__restrict__ A, int t0, int n_tiles, int KG, const char *in,
-                                            int in_stride, int ln, int lq, int l, Done done) {
-    static_assert(RING % 2 == 0, "the B double buffer alternates with the ring slot");
-    const int n_groups = n_tiles / TP;
-    const int NIT = n_groups * KG;
-    const int64_t tstride = (int64_t)KG * 64;  // uint4 between the same k-group of consecutive tiles
-    auto a_src = [&](int it) {
-        return A + (int64_t)(t0 + TP * (it / KG)) * tstride + (int64_t)(it % KG) * 64 + l;
-    };
-    uint4 ring[RING][TP];
+// The A fragments of a layer's first RING iterations (see dense_layer), loaded before the layer
+// starts so that their latency overlaps the work before it.
+template <int TP, int RING>
+__device__ __forceinline__ void ring_fill(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int t0, int n_tiles,
+                                          int KG, int l) {
+    const int NIT = n_tiles / TP * KG;
+    const int64_t tstride = (int64_t)KG * 64;
 #pragma unroll
     for (int r = 0; r < RING; ++r) {
         if (r < NIT) {
-            const uint4 *src = a_src(r);
+            const uint4 *src = A + (int64_t)(t0 + TP * (r / KG)) * tstride + (int64_t)(r % KG) * 64 + l;
 #pragma unroll
             for (int j = 0; j < TP; ++j) ring[r][j] = src[j * tstride];
         } else {
@@ -115,6 +103,26 @@ __device__ __forceinline__ void dense_layer(const uint4 *__restrict__ A, int t0,
             for (int j = 0; j < TP; ++j) ring[r][j] = make_uint4(0, 0, 0, 0);
         }
     }
+}
+
+// One dense layer for this wave: `n_tiles` output tiles of 16 units starting at tile `t0`, each a
+// sum over KG k-groups (KG a multiple of RING), computed TP tiles at a time (TP independent
+// accumulator chains sharing every B fragment).  The wave's iterations (tile group, k-group) run
+// in order; `ring` holds the A fragments of the first RING iterations (ring_fill), and those of
+// iteration it + RING are loaded from `A` (packed [tile][g][lane] x 16 B) into ring slot it % RING
+// as soon as iteration it has issued its MFMAs; the B fragments of the next k-group are read from
+// the LDS activation rows `in` (row stride `in_stride` bytes) into the other half of a double
+// buffer.  done(first_tile, acc[TP][NSG]) consumes each finished group.
+template <bool BF16, int NSG, int TP, int RING, typename Done>
+__device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int t0, int n_tiles,
+                                            int KG, const char *in, int in_stride, int ln, int lq, int l, Done done) {
+    static_assert(RING % 2 == 0, "the B double buffer alternates with the ring slot");
+    const int n_groups = n_tiles / TP;
+    const int NIT = n_groups * KG;
+    const int64_t tstride = (int64_t)KG * 64;  // uint4 between the same k-group of consecutive tiles
+    auto a_src = [&](int it) {
+        return A + (int64_t)(t0 + TP * (it / KG)) * tstride + (int64_t)(it % KG) * 64 + l;
+    };
     auto b_load = [&](int g, uint4 (&b)[NSG]) {
 #pragma unroll
         for (int sg = 0; sg < NSG; ++sg)
@@ -165,6 +173,10 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     char *xs = smem;
     char *h1 = smem + NS * xs_stride;
     const int HT = p.hap / 16;
+    // the first W1 fragments are loaded while the states are staged
+    const int mt1 = p.h1p / 16 / U, mt2 = p.h2p / 16 / U;
+    uint4 ring[RING][TP];
+    ring_fill<TP, RING>(ring, p.w1, wid * mt1, mt1, p.sp / UPG, l);
 
     // ---------------- phase 0: states -> LDS [state][unit] (zero beyond S and B) ----------------
     {
@@ -187,8 +199,8 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
 
     // ---------------- phase 1: h1 = act(W1 s + b1), this wave's share of the tiles ----------------
     {
-        const int mt_per = p.h1p / 16 / U;
-        dense_layer<BF16, NSG, TP, RING>(p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
+        const int mt_per = mt1;
+        dense_layer<BF16, NSG, TP, RING>(ring, p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
                                          [&](int mt0, f32x4 (&acc)[TP][NSG]) {
 #pragma unroll
                                              for (int h = 0; h < TP; ++h) {
@@ -210,6 +222,8 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                                              }
                                          });
     }
+    // the first W2 fragments are loaded before the barrier that publishes h1
+    ring_fill<TP, RING>(ring, p.w2, wid * mt2, mt2, p.h1p / UPG, l);
     __syncthreads();
 
     // ------- phase 2: h2 tile groups of this wave, chained into the partial heads (registers) -------
@@ -219,7 +233,7 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
 #pragma unroll
         for (int ht = 0; ht < HTM; ++ht) hacc[sg][ht] = f32x4{0, 0, 0, 0};
     {
-        const int mt_per = p.h2p / 16 / U;
+        const int mt_per = mt2;
         const int mt_first = wid * mt_per;
         // head fragments: fp32 one k-group per h2 tile, bf16 one per pair of tiles
         const int HKG = BF16 ? p.h2p / 32 : p.h2p / 16;
@@ -237,7 +251,7 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
         };
         head_fetch(mt_first);
         dense_layer<BF16, NSG, TP, RING>(
-            p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l, [&](int mt0, f32x4 (&acc)[TP][NSG]) {
+            ring, p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l, [&](int mt0, f32x4 (&acc)[TP][NSG]) {
                 float bias[TP][4];
 #pragma unroll
                 for (int h = 0; h < TP; ++h)
@@ -280,7 +294,10 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
 
     // ---------------- phase 3: fixed-order sum of the U partial heads, epilogue ----------------
+    // Every thread sums some of the NSG*hap*16 head values over the U waves (in wave order, then
+    // the bias) into zs; the waves of the state groups then take argmax, softmax and the value.
     float *part = reinterpret_cast<float *>(smem);  // [U][NSG][hap][16]
+    float *zs = part + (int64_t)U * NSG * p.hap * 16;  // [NSG][hap][16]
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
@@ -289,6 +306,17 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     part[(((int64_t)wid * NSG + sg) * p.hap + ht * 16 + lq * 4 + i) * 16 + ln] = hacc[sg][ht][i];
+    __syncthreads();
+    {
+        const int nz = NSG * p.hap * 16;
+        for (int v = threadIdx.x; v < nz; v += NTH) {
+            const int row = (v / 16) % p.hap;
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < U; ++w) s += part[(int64_t)w * nz + v];
+            zs[v] = s + p.bh[row];
+        }
+    }
     __syncthreads();
     for (int sg = wid; sg < NSG; sg += U) {
         const int st = s0 + sg * 16 + ln;
@@ -303,10 +331,7 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                 z[ht][i] = 0.f;
                 if (ht >= HT) continue;
                 const int row = ht * 16 + lq * 4 + i;
-                float s = 0.f;
-#pragma unroll
-                for (int w = 0; w < U; ++w) s += part[(((int64_t)w * NSG + sg) * p.hap + row) * 16 + ln];
-                s += p.bh[row];
+                const float s = zs[((int64_t)sg * p.hap + row) * 16 + ln];
                 z[ht][i] = s;
                 if (row < p.a && (s > best || (s == best && row < best_i))) {
                     best = s;
@@ -398,7 +423,7 @@ size_t policy_lds_bytes(const harl_policy *P, int nsg, int u) {
     const size_t el = bf ? 2 : 4;
     const size_t ns = 16 * (size_t)nsg;
     const size_t acts = ns * (P->sp * el + 16) + ns * (P->h1p * el + 16);
-    const size_t part = (size_t)u * nsg * P->hap * 16 * 4;
+    const size_t part = (size_t)(u + 1) * nsg * P->hap * 16 * 4;  // partial heads and their sums
     return acts > part ? acts : part;
 }
 

@@ -42,6 +42,16 @@ __device__ __forceinline__ uint32_t order_key(float s) {
 
 __device__ __forceinline__ uint32_t local_of(uint64_t c) { return 0xFFFFFFFFu - (uint32_t)(c & 0xFFFFFFFFull); }
 
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t u = __shfl_up(v, o, 64);
+        if (lane >= o) v += u;
+    }
+    return v;
+}
+
 // FROM_SCORES: round 0 reads fp32 scores (candidate = position); later rounds read composites.
 // emit: this is the last round and its (single) workgroup writes io_score / io_index directly.
 template <bool FROM_SCORES>
@@ -49,13 +59,11 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
                                                              int64_t count, int kk, uint64_t *__restrict__ cout, int emit,
                                                              int n, int64_t index_base, float *__restrict__ out_score,
                                                              int64_t *__restrict__ out_index) {
-    __shared__ uint32_t whist[kSelThreads / 64][256];  // per-wave histograms: fewer same-address atomics
-    __shared__ uint32_t hist[256];
-    __shared__ uint64_t sel[HARL_TOPK_MAX_K];
+    __shared__ uint32_t hist[2][256];  // digit histograms of consecutive passes (one is cleared meanwhile)
+    __shared__ uint64_t sel[HARL_TOPK_MAX_K > kRankSortMax ? HARL_TOPK_MAX_K : kRankSortMax];
     __shared__ uint64_t ranked[kRankSortMax];
-    __shared__ uint32_t rank_cnt[kRankSortMax];
     __shared__ uint32_t s_digit, s_above, s_eq, s_cnt;
-    const int t = threadIdx.x, w = t / 64;
+    const int t = threadIdx.x, lane = t % 64;
     const int64_t base = (int64_t)blockIdx.x * kSeg;
     const int64_t rem = count - base;
     const int n_valid = rem < kSeg ? (int)rem : kSeg;
@@ -73,16 +81,17 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         }
     }
     auto valid = [&](int j) { return j * kSelThreads + t < n_valid; };
+    for (int i = t; i < 2 * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
+    if (t == 0) s_cnt = 0;
+    __syncthreads();
 
     // ---- radix select: find the prefix of the kk-th largest composite ----
     uint64_t prefix = 0;
-    int shift = 64;
+    int shift = 64, hb = 0;
     uint32_t kr = (uint32_t)kk;  // ranks still needed among candidates matching `prefix`
     bool done = n_valid <= kk;   // a short segment keeps every candidate
     while (shift > 0 && !done) {
         shift -= 8;
-        for (int i = t; i < (kSelThreads / 64) * 256; i += kSelThreads) (&whist[0][0])[i] = 0;
-        __syncthreads();
         // Scores concentrate in few digit values (the leading digits are sign and exponent), and
         // lanes of one atomic instruction that hit the same bin are serialised.  So the lanes that
         // share the first live lane's bin are counted with a single atomic, the rest (few, and
@@ -96,27 +105,18 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
                 const int first = __builtin_ctzll(live);
                 const uint32_t b0 = __builtin_amdgcn_readlane(bin, first);
                 const uint64_t same = __ballot(alive && bin == b0);
-                if (t % 64 == first) atomicAdd(&whist[w][b0], (uint32_t)__popcll(same));
-                if (alive && bin != b0) atomicAdd(&whist[w][bin], 1u);
+                if (lane == first) atomicAdd(&hist[hb][b0], (uint32_t)__popcll(same));
+                if (alive && bin != b0) atomicAdd(&hist[hb][bin], 1u);
             }
         }
-        __syncthreads();
-        if (t < 256) {
-            uint32_t c = 0;
-#pragma unroll
-            for (int v = 0; v < kSelThreads / 64; ++v) c += whist[v][t];
-            hist[t] = c;
-        }
+        // the other histogram was last read by the previous pass's scan, before its final barrier
+        if (t < 256) hist[hb ^ 1][t] = 0;
         __syncthreads();
         if (t < 64) {
-            const uint32_t h0 = hist[255 - 4 * t], h1 = hist[254 - 4 * t], h2 = hist[253 - 4 * t], h3 = hist[252 - 4 * t];
+            const uint32_t *h = hist[hb];
+            const uint32_t h0 = h[255 - 4 * t], h1 = h[254 - 4 * t], h2 = h[253 - 4 * t], h3 = h[252 - 4 * t];
             const uint32_t s = h0 + h1 + h2 + h3;
-            uint32_t incl = s;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const uint32_t v = __shfl_up(incl, o, 64);
-                if (t >= o) incl += v;
-            }
+            const uint32_t incl = wave_incl_scan(s, t);
             const uint32_t excl = incl - s;
             if (excl < kr && incl >= kr) {
                 uint32_t above = excl;
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
                 else { above += h2; d = 252 - 4 * t; }
                 s_digit = (uint32_t)d;
                 s_above = above;
-                s_eq = hist[d];
+                s_eq = h[d];
             }
         }
         __syncthreads();
@@ -135,70 +135,64 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         kr -= s_above;
         prefix |= (uint64_t)d << shift;
         done = s_eq == kr;
+        hb ^= 1;
     }
 
-    // ---- compaction: everything strictly above the prefix, then kr of those equal to it ----
-    if (t == 0) s_cnt = 0;
-    __syncthreads();
-    // one counter atomic per wave: a lane's slot is the wave's base plus the number of lower lanes
-    // that also append
-    auto append_slot = [&](bool take) -> uint32_t {
-        const uint64_t m = __ballot(take);
-        uint32_t slot = 0;
-        if (m) {
-            const int first = __builtin_ctzll(m);
-            uint32_t wbase = 0;
-            if (t % 64 == first) wbase = atomicAdd(&s_cnt, (uint32_t)__popcll(m));
-            wbase = __builtin_amdgcn_readlane(wbase, first);
-            slot = wbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-        }
-        return slot;
-    };
-    if (n_valid <= kk) {
+    // ---- compaction: the composites strictly above the prefix bucket take slots [0, kk - kr), the
+    // kr in it slots [kk - kr, kk) (a short segment: all of them, [0, n_valid)).  A lane's slots
+    // follow from a prefix sum over the wave of both counts (packed in one word, each < 2^16) and
+    // one counter atomic per wave.
+    {
+        const bool all = n_valid <= kk;
+        const uint64_t ptop = all ? 0 : prefix >> shift;
+        uint32_t cnt = 0;
 #pragma unroll
         for (int j = 0; j < kPerThread; ++j) {
-            const uint32_t pos = append_slot(valid(j));
-            if (valid(j)) sel[pos] = x[j];
+            if (!valid(j)) continue;
+            const uint64_t top = all ? 1 : x[j] >> shift;
+            cnt += top > ptop ? 1u : (top == ptop ? 0x10000u : 0u);
         }
-        __syncthreads();
-        for (int i = n_valid + t; i < kk; i += kSelThreads) sel[i] = 0;
-    } else {
-        const uint64_t ptop = prefix >> shift;
+        const uint32_t incl = wave_incl_scan(cnt, lane);
+        const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+        uint32_t wbase = 0;
+        if (lane == 63 && total) wbase = atomicAdd(&s_cnt, total);
+        wbase = __builtin_amdgcn_readlane(wbase, 63) + (incl - cnt);
+        uint32_t a_slot = wbase & 0xFFFFu, e_slot = (uint32_t)kk - kr + (wbase >> 16);
 #pragma unroll
         for (int j = 0; j < kPerThread; ++j) {
-            const bool take = valid(j) && (x[j] >> shift) > ptop;
-            const uint32_t pos = append_slot(take);
-            if (take) sel[pos] = x[j];
+            if (!valid(j)) continue;
+            const uint64_t top = all ? 1 : x[j] >> shift;
+            if (top > ptop) {
+                sel[a_slot++] = x[j];
+            } else if (top == ptop) {
+                if (e_slot < (uint32_t)kk) sel[e_slot] = x[j];
+                ++e_slot;
+            }
         }
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < kPerThread; ++j) {
-            const bool take = valid(j) && (x[j] >> shift) == ptop;
-            const uint32_t pos = append_slot(take);
-            if (take && pos < (uint32_t)kk) sel[pos] = x[j];
-        }
+        if (all)
+            for (int i = n_valid + t; i < kk; i += kSelThreads) sel[i] = 0;
     }
     const uint64_t *out_keys = sel;
     if (kk <= kRankSortMax) {
         // rank sort: an entry's output slot is the number of entries ranking ahead of it (a larger
-        // composite, or an equal one -- identical padding only -- at a lower position); G threads
-        // count each entry's rank over disjoint parts of the list
-        const int G = kSelThreads / kk;
-        for (int i = t; i < kk; i += kSelThreads) rank_cnt[i] = 0;
+        // composite, or an equal one -- identical padding only -- at a lower position).  The list
+        // is padded to kRankSortMax with zero composites (they rank behind every entry, and only
+        // entries below kk are placed); 8 consecutive lanes count one entry's rank over 1/8 of it.
+        constexpr int G = kSelThreads / kRankSortMax, PART = kRankSortMax / G;
+        for (int i = kk + t; i < kRankSortMax; i += kSelThreads) sel[i] = 0;
         __syncthreads();
-        if (t < G * kk) {
-            const int i = t / G, part = t % G;
-            const uint64_t v = sel[i];
-            const int j0 = part * kk / G, j1 = (part + 1) * kk / G;
-            uint32_t rank = 0;
-            for (int j = j0; j < j1; ++j) {
-                const uint64_t u = sel[j];
-                rank += (u > v) | ((u == v) & (j < i));
-            }
-            if (rank) atomicAdd(&rank_cnt[i], rank);
+        const int i = t / G, part = t % G;
+        const uint64_t v = sel[i];
+        uint32_t rank = 0;
+#pragma unroll
+        for (int q = 0; q < PART; ++q) {
+            const int j = part * PART + q;
+            const uint64_t u = sel[j];
+            rank += (u > v) | ((u == v) & (j < i));
         }
-        __syncthreads();
-        for (int i = t; i < kk; i += kSelThreads) ranked[rank_cnt[i]] = sel[i];
+#pragma unroll
+        for (int m = 1; m < G; m <<= 1) rank += __shfl_xor(rank, m, 64);
+        if (part == 0 && i < kk) ranked[rank] = v;
         __syncthreads();
         out_keys = ranked;
     } else {
