@@ -36,7 +36,10 @@ PEAK_GVISITS = N_CU * CLOCK_GHZ * LDS_BYTES_PER_CLK / LDS_BYTES_PER_VISIT  # G v
 # and by the SHA-256 of the scoring source the counters were taken with: any other source reports
 # null.
 SCORE_TRAFFIC_BYTES = {
-    ("standard", "aa68cf47d905a87ae6302d79c52aefb2f184f4bb31b3bac80c33f6b3762b9354"): 58.75e6,
+    ("standard", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 58.93e6,
+    ("ingest-16x1", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 1.4612e9,
+    ("ingest-4x4", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 1.4608e9,
+    ("ingest-2x8", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 1.4702e9,
 }
 
 
@@ -123,9 +126,20 @@ def ingest_calibration(args):
     alg_bytes = n_rows * base.n_features * 4 + (n_prog + 1) * 4 + n_prog * 4
     pol = gen_policy(base)
     rows = []
+    if args.counter_probe:  # byte-counter calibration copy, then 3 eager calls per ensemble
+        n_copy = 256 << 20
+        src = torch.ones(n_copy // 4, dtype=torch.float32, device=dev)
+        torch.empty_like(src).copy_(src)
+        torch.cuda.synchronize()
     for n_trees, depth in ((16, 1), (4, 4), (2, 8)):
         cfg = base.with_(n_trees=n_trees, depth=depth, name="ingest-%dx%d" % (n_trees, depth))
         rnd = Round(gen_ensemble(cfg), pol, n_rows, n_prog, base.top_k, device=dev)
+        if args.counter_probe:
+            for _ in range(3):
+                rnd.score(batch)
+            torch.cuda.synchronize()
+            rnd.close()
+            continue
         for _ in range(max(args.warmup, 1)):
             rnd.score(batch)
         g = torch.cuda.CUDAGraph()
@@ -142,9 +156,14 @@ def ingest_calibration(args):
         us = e0.elapsed_time(e1) / args.steps * 1e3
         gbs = alg_bytes / (us * 1e-6) / 1e9
         rows.append({"trees": n_trees, "depth": depth, "us_per_launch": us, "hbm_gbs": gbs,
-                     "hbm_frac": gbs / PEAK_HBM_GBS})
+                     "hbm_frac": gbs / PEAK_HBM_GBS, "traffic": score_traffic(cfg.name),
+                     "traffic_unit": "bytes per launch"})
         print("ingest %d trees x depth %d: %.1f us, %.0f GB/s" % (n_trees, depth, us, gbs), file=sys.stderr, flush=True)
         rnd.close()
+    if args.counter_probe:
+        print(json.dumps({"copy_bytes": 256 << 20, "calls_each": 3, "feature_bytes": n_rows * base.n_features * 4,
+                          "algorithmic_bytes": alg_bytes}), flush=True)
+        return
     print(json.dumps({"metric": "feature ingest HBM bandwidth (harl_score_round, shallow ensembles)",
                       "rows": n_rows, "algorithmic_bytes": alg_bytes, "peak_gbs": PEAK_HBM_GBS,
                       "steps": args.steps, "results": rows}), flush=True)

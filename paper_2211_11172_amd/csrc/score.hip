@@ -760,6 +760,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(const float *__restrict_
         const int tile0 = c0 >> rt_shift;
         if (sliced) {
             const int ntc = ((c1 - 1) >> rt_shift) - tile0 + 1;
+            const bool narrow = (int64_t)(tiles + 1) * T <= (int64_t)UINT32_MAX;  // 32-bit divisions suffice
             for (int i = t; i < ntc * groups; i += kSegThreads) {
                 const int gi = i / ntc, ti = i - gi * ntc;
                 const int64_t tile = tile0 + ti;
@@ -767,7 +768,11 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(const float *__restrict_
                 int2 sp = make_int2(0, -1);
                 if (tc > 0) {
                     const int64_t L = group_slice_len(tiles, tc, nbg);
-                    sp = make_int2((int)(tile * tc / L), (int)(((tile + 1) * tc - 1) / L));
+                    if (narrow)
+                        sp = make_int2((int)((uint32_t)(tile * tc) / (uint32_t)L),
+                                       (int)((uint32_t)((tile + 1) * tc - 1) / (uint32_t)L));
+                    else
+                        sp = make_int2((int)(tile * tc / L), (int)(((tile + 1) * tc - 1) / L));
                 }
                 span[gi * kSegMaxTiles + ti] = sp;
             }

@@ -80,6 +80,8 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
                 x[j] = cin[i];
         }
     }
+    // register slots j >= jn hold no candidate in any thread: the loops below skip them uniformly
+    const int jn = (n_valid + kSelThreads - 1) / kSelThreads;
     auto valid = [&](int j) { return j * kSelThreads + t < n_valid; };
     for (int i = t; i < 2 * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
     if (t == 0) s_cnt = 0;
@@ -98,6 +100,7 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         // spread) with their own.
 #pragma unroll
         for (int j = 0; j < kPerThread; ++j) {
+            if (j >= jn) break;
             const bool alive = valid(j) && (shift == 56 || ((x[j] ^ prefix) >> (shift + 8)) == 0);
             const uint32_t bin = (uint32_t)(x[j] >> shift) & 255u;
             const uint64_t live = __ballot(alive);
@@ -148,6 +151,7 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         uint32_t cnt = 0;
 #pragma unroll
         for (int j = 0; j < kPerThread; ++j) {
+            if (j >= jn) break;
             if (!valid(j)) continue;
             const uint64_t top = all ? 1 : x[j] >> shift;
             cnt += top > ptop ? 1u : (top == ptop ? 0x10000u : 0u);
@@ -160,6 +164,7 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         uint32_t a_slot = wbase & 0xFFFFu, e_slot = (uint32_t)kk - kr + (wbase >> 16);
 #pragma unroll
         for (int j = 0; j < kPerThread; ++j) {
+            if (j >= jn) break;
             if (!valid(j)) continue;
             const uint64_t top = all ? 1 : x[j] >> shift;
             if (top > ptop) {
