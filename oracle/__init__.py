@@ -3,7 +3,8 @@
 A ctypes wrapper over ``harl_oracle.c`` (plain C, fp64, optional OpenMP).  It computes, from the
 paper's definitions, what the HIP path must reproduce: per-program cost-model scores (GBDT over
 statement rows, summed per program), the actor/critic forward with its argmax action, and the
-top-K / running-heap selection.  Only ``tests/``, the package's ``smoke()`` check and
+top-K / running-heap selection, and for schedule tracks the reward, the advantage and the
+adaptive-stopping elimination.  Only ``tests/``, the package's ``smoke()`` check and
 ``bench.py``'s ``cpu_baseline`` leg may import this package; the product path never does.
 """
 from __future__ import annotations
@@ -45,11 +46,14 @@ def _bind(lib):
                                        P, i32, P, P, P, P, P, P, ctypes.c_int]
     lib.oracle_topk.argtypes = [P, i64, i32, i64, P, P]
     lib.oracle_merge.argtypes = [P, P, i32, P, i64, i64]
+    lib.oracle_track_advantage.argtypes = [P, P, P, P, i64, dbl, dbl, P, P, P]
+    lib.oracle_track_eliminate.argtypes = [P, i64, i64, P]
     lib.oracle_max_threads.argtypes = []
     lib.oracle_round_bf16.argtypes = [dbl]
     lib.oracle_round_bf16.restype = dbl
     for f in (lib.oracle_score_round, lib.oracle_policy_step, lib.oracle_topk,
-              lib.oracle_merge, lib.oracle_max_threads):
+              lib.oracle_merge, lib.oracle_max_threads, lib.oracle_track_advantage,
+              lib.oracle_track_eliminate):
         f.restype = ctypes.c_int
     return lib
 
@@ -181,3 +185,39 @@ def merge(run_score: np.ndarray, run_index: np.ndarray, score: np.ndarray, index
     if rc != 0:
         raise ValueError("oracle_merge failed (%d)" % rc)
     return rs, ri
+
+
+def track_advantage(c_prev, c_next, v_prev, v_next, gamma: float = 0.9, eps: float = 1e-6) -> dict:
+    """Reward (Algorithm 1, denominator max(|C(s)|, eps)) and advantage (Eq. 4) of one step of
+    every schedule track, fp64 over the fp32 inputs; ``scale`` = |r| + |gamma V(s')| + |V(s)|.
+    ``gamma`` and ``eps`` are taken at their fp32 values (the values the GPU path computes with)."""
+    lib = _load()
+    a = [_c(x, np.float32) for x in (c_prev, c_next, v_prev, v_next)]
+    n = a[0].size
+    assert all(x.size == n for x in a)
+    reward = np.zeros(n, dtype=np.float64)
+    adv = np.zeros(n, dtype=np.float64)
+    scale = np.zeros(n, dtype=np.float64)
+    rc = lib.oracle_track_advantage(*[_p(x) for x in a], n, float(np.float32(gamma)), float(np.float32(eps)),
+                                    _p(reward), _p(adv), _p(scale))
+    if rc != 0:
+        raise ValueError("oracle_track_advantage failed (%d)" % rc)
+    return dict(reward=reward, adv=adv, scale=scale)
+
+
+def track_eliminate(adv, n_keep: int) -> np.ndarray:
+    """Adaptive-stopping elimination (Section 5): the indices of the n_keep tracks ranked first by
+    (advantage desc, NaN last, -0 ties +0, lower index first), in ascending order."""
+    lib = _load()
+    a = _c(adv, np.float32)
+    out = np.zeros(max(n_keep, 0), dtype=np.int32)
+    rc = lib.oracle_track_eliminate(_p(a), a.size, n_keep, _p(out))
+    if rc != 0:
+        raise ValueError("oracle_track_eliminate failed (%d)" % rc)
+    return out
+
+
+def eliminate_count(n: int, rho: float = 0.5) -> int:
+    """Tracks that survive one elimination of proportion rho (Section 5): the eliminated number
+    floor(rho * n) is rounded down."""
+    return n - int(np.floor(rho * n))

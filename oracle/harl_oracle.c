@@ -14,7 +14,11 @@
  *                        trunk with a linear actor head and a linear value head;
  *   oracle_topk          "select top-K states from the heap H" (Algorithm 1, top-K phase;
  *                        Section 4.3, Top-K Selection Phase): the K best predicted scores;
- *   oracle_merge         the heap H accumulating candidates across steps (Algorithm 1).
+ *   oracle_merge         the heap H accumulating candidates across steps (Algorithm 1);
+ *   oracle_track_advantage  reward of a modification step (Algorithm 1) and the advantage of
+ *                        Eq. 4 for every schedule track;
+ *   oracle_track_eliminate  adaptive-stopping elimination of the tracks with the lowest
+ *                        advantages (Section 5).
  *
  * All arithmetic on scores and activations is fp64 over the given fp32 / bf16 input values.
  * Nothing here is blocked, fused or reordered beyond the definitions.  Only tests/, the package's
@@ -29,7 +33,11 @@
  *   - bf16 policies round the hidden activations h1, h2 to bf16 (nearest, ties to even) after
  *     bias and ReLU; fp32 policies keep them exact (fp64 here);
  *   - the action is the lowest index attaining the maximum logit; probabilities are the softmax
- *     of the logits.
+ *     of the logits;
+ *   - the reward's denominator C(s) is taken as max(|C(s)|, eps): the paper's scores are
+ *     positive, signed scores keep the sign of an improvement and a zero score stays finite;
+ *   - elimination ranks tracks like top-K (advantage desc, NaN last, -0 ties +0, then lower track
+ *     index), keeps a given number of them and lists the survivors in ascending track order.
  */
 #include <math.h>
 #include <stdint.h>
@@ -301,5 +309,58 @@ int oracle_merge(float *run_score, int64_t *run_index, int32_t k,
         run_index[i] = c[i].index;
     }
     free(c);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------------------------- */
+/* Schedule tracks: reward, advantage and adaptive-stopping elimination                         */
+/* ------------------------------------------------------------------------------------------- */
+
+/* One modification step of n schedule tracks.  Track i moved from state s (predicted score
+ * c_prev[i], critic value v_prev[i]) to s' (c_next[i], v_next[i]).  Algorithm 1 rewards the step
+ * with the relative change of the cost model's score, r = (C(s') - C(s)) / C(s), here with the
+ * denominator max(|C(s)|, eps); Eq. 4 gives the advantage A = r + gamma V(s') - V(s).
+ * scale[i] = |r| + |gamma V(s')| + |V(s)| bounds the terms of A (scale-relative tolerance). */
+int oracle_track_advantage(const float *c_prev, const float *c_next, const float *v_prev,
+                           const float *v_next, int64_t n, double gamma, double eps,
+                           double *reward, double *adv, double *scale) {
+    if (n < 0 || !(eps > 0.0)) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        const double c = c_prev[i], cn = c_next[i];
+        const double denom = fabs(c) > eps ? fabs(c) : eps;
+        const double r = (cn - c) / denom;
+        const double g = gamma * (double)v_next[i];
+        const double v = v_prev[i];
+        reward[i] = r;
+        adv[i] = r + g - v;
+        scale[i] = fabs(r) + fabs(g) + fabs(v);
+    }
+    return ORACLE_OK;
+}
+
+/* Adaptive-stopping elimination (Section 5): after a window of steps the tracks are ordered by
+ * advantage and the ones with the lowest advantages stop.  The n_keep tracks ranked first (the
+ * top-K ranking above, on the advantage, track i carrying index i) survive; their indices are
+ * written in ascending order, so the surviving tracks keep their relative order. */
+int oracle_track_eliminate(const float *adv, int64_t n, int64_t n_keep, int32_t *keep_index) {
+    if (n < 0 || n_keep < 0 || n_keep > n || n > INT32_MAX) return ORACLE_EINVAL;
+    cand_t *c = (cand_t *)malloc(sizeof(cand_t) * (size_t)(n > 0 ? n : 1));
+    unsigned char *keep = (unsigned char *)calloc((size_t)(n > 0 ? n : 1), 1);
+    if (!c || !keep) {
+        free(c);
+        free(keep);
+        return ORACLE_ENOMEM;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        c[i].score = adv[i];
+        c[i].index = i;
+    }
+    qsort(c, (size_t)n, sizeof(cand_t), cand_cmp);
+    for (int64_t k = 0; k < n_keep; ++k) keep[c[k].index] = 1;
+    int64_t m = 0;
+    for (int64_t i = 0; i < n; ++i)
+        if (keep[i]) keep_index[m++] = (int32_t)i;
+    free(c);
+    free(keep);
     return ORACLE_OK;
 }

@@ -52,6 +52,20 @@ MUTANTS = {
                          [(pins.test_topk_special_cases, {})]),
     "merge_local_index": ("c[k + i].index = index_base + i;", "c[k + i].index = i;",
                           [(pins.test_merge_equals_topk_of_union_in_any_order, {})]),
+    "reward_signed_denominator": ("fabs(c) > eps ? fabs(c) : eps", "c > eps ? c : eps",
+                                  [(pins.test_reward_advantage_closed_forms, {})]),
+    "reward_no_eps_floor": ("fabs(c) > eps ? fabs(c) : eps", "fabs(c)",
+                            [(pins.test_reward_advantage_closed_forms, {})]),
+    "advantage_discounts_prev": ("const double g = gamma * (double)v_next[i];",
+                                 "const double g = gamma * (double)v_prev[i];",
+                                 [(pins.test_reward_advantage_closed_forms, {})]),
+    "advantage_value_sign": ("adv[i] = r + g - v;", "adv[i] = r + g + v;",
+                             [(pins.test_reward_sign_and_critic_reductions, {})]),
+    "eliminate_keeps_worst": ("keep[c[k].index] = 1;", "keep[c[n - 1 - k].index] = 1;",
+                              [(pins.test_eliminate_special_cases, {})]),
+    "eliminate_rank_order_out": ("if (keep[i]) keep_index[m++] = (int32_t)i;",
+                                 "if (keep[i]) keep_index[m++] = (int32_t)i;\n    for (int64_t k = 0; k < n_keep; ++k) keep_index[k] = (int32_t)c[k].index;",
+                                 [(pins.test_eliminate_ranking_properties_small, {})]),
 }
 
 

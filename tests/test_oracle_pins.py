@@ -2,7 +2,9 @@
 library routines).  Paper anchors: the cost model C scores every new schedule (Algorithm 1; the
 cost model is XGBoost, Section 6.1, Appendix A.2); the actor and critic act on the states
 (Algorithm 1; Section 4.3, Eq. 6); the top-K of the heap H are the K best predicted scores
-(Algorithm 1; Section 4.3, Top-K Selection Phase)."""
+(Algorithm 1; Section 4.3, Top-K Selection Phase); each step of a schedule track is rewarded with
+the relative change of its score (Algorithm 1) and judged by the advantage of Eq. 4, and the
+adaptive-stopping search drops the tracks of lowest advantage (Section 5)."""
 from __future__ import annotations
 
 import numpy as np
@@ -353,3 +355,98 @@ def test_merge_fewer_candidates_than_k_keeps_sentinels():
     rs, ri = oracle.merge(rs, ri, np.array([3.0, -np.inf, 1.0], np.float32), 10)
     assert ri[:3].tolist() == [10, 12, 11]
     assert (ri[3:] == oracle.RESET_INDEX).all() and np.isneginf(rs[3:]).all()
+
+
+# ----------------------------------------------------------------------------------------------
+# schedule tracks: reward, advantage, elimination
+# ----------------------------------------------------------------------------------------------
+def test_reward_advantage_closed_forms():
+    # (c_prev, c_next, v_prev, v_next) -> reward, advantage with gamma = 0.75, eps = 0.25
+    rows = [
+        (2.0, 3.0, 1.0, 2.0, 0.5, 0.5 + 1.5 - 1.0),      # +50 % score, V from 1 to 2
+        (-4.0, -2.0, 0.0, 0.0, 0.5, 0.5),                # negative scores: an improvement is positive
+        (-2.0, -4.0, 0.5, -1.0, -1.0, -1.0 - 0.75 - 0.5),
+        (0.125, 0.375, 0.0, 0.0, 1.0, 1.0),              # |C(s)| below eps: the denominator is eps
+        (0.0, -0.5, 0.25, 1.0, -2.0, -2.0 + 0.75 - 0.25),
+        (3.0, 3.0, -1.0, 1.0, 0.0, 0.0 + 0.75 + 1.0),    # unchanged score: only the critic terms
+    ]
+    c0, c1, v0, v1, r, a = (np.array(x, dtype=np.float64) for x in zip(*rows))
+    got = oracle.track_advantage(c0, c1, v0, v1, gamma=0.75, eps=0.25)
+    np.testing.assert_array_equal(got["reward"], r)
+    np.testing.assert_array_equal(got["adv"], a)
+    np.testing.assert_array_equal(got["scale"], np.abs(r) + np.abs(0.75 * v1) + np.abs(v0))
+
+
+def test_reward_sign_and_critic_reductions():
+    rng = np.random.default_rng(11)
+    n = 5000
+    c0 = (rng.standard_normal(n) * 10).astype(np.float32)
+    c1 = (c0 + rng.standard_normal(n)).astype(np.float32)
+    v0 = rng.standard_normal(n).astype(np.float32)
+    v1 = rng.standard_normal(n).astype(np.float32)
+    got = oracle.track_advantage(c0, c1, v0, v1, gamma=0.0)
+    # the reward has the sign of the score change whatever the sign of the score
+    np.testing.assert_array_equal(np.sign(got["reward"]), np.sign(c1.astype(np.float64) - c0))
+    # gamma = 0: A = r - V(s); gamma = 1 with an unchanged score: A = V(s') - V(s), exact in fp64
+    np.testing.assert_array_equal(got["adv"], got["reward"] - v0)
+    same = oracle.track_advantage(c0, c0, v0, v1, gamma=1.0)
+    np.testing.assert_array_equal(same["reward"], np.zeros(n))
+    np.testing.assert_array_equal(same["adv"], v1.astype(np.float64) - v0)
+    # the discount factor of Section 6.1 enters at its fp32 value
+    dflt = oracle.track_advantage(c0, c0, np.zeros(n), v1)
+    np.testing.assert_array_equal(dflt["adv"], v1.astype(np.float64) * float(np.float32(0.9)))
+
+
+def _elimination_properties(adv, n_keep, keep):
+    """The survivors are the unique set of n_keep tracks such that every survivor ranks ahead of
+    every eliminated track: a larger advantage, or an equal one (-0 == +0) at a lower index; NaN
+    behind every number."""
+    n = adv.size
+    keep = np.asarray(keep)
+    assert keep.size == n_keep
+    assert (np.diff(keep) > 0).all() and (keep >= 0).all() and (keep < n).all()
+    kept = np.zeros(n, bool)
+    kept[keep] = True
+    for i in np.flatnonzero(kept):
+        for j in np.flatnonzero(~kept):
+            ai, aj = adv[i], adv[j]
+            if np.isnan(ai):
+                assert np.isnan(aj) and i < j
+            elif not np.isnan(aj):
+                assert ai > aj or (ai == aj and i < j)
+
+
+def test_eliminate_ranking_properties_small():
+    rng = np.random.default_rng(12)
+    pool = np.array([-1.5, -0.0, 0.0, 0.25, 2.0, np.nan, np.inf, -np.inf], np.float32)
+    for trial in range(40):
+        n = int(rng.integers(1, 12))
+        adv = rng.choice(pool, n).astype(np.float32)
+        for n_keep in range(n + 1):
+            _elimination_properties(adv, n_keep, oracle.track_eliminate(adv, n_keep))
+
+
+def test_eliminate_special_cases():
+    adv = np.array([0.5, -1.0, 3.0, 3.0, np.nan, 0.5, -0.0, 0.0], np.float32)
+    assert oracle.track_eliminate(adv, 8).tolist() == list(range(8))
+    assert oracle.track_eliminate(adv, 0).tolist() == []
+    assert oracle.track_eliminate(adv, 2).tolist() == [2, 3]
+    assert oracle.track_eliminate(adv, 3).tolist() == [0, 2, 3]          # tie at 0.5: lower index
+    assert oracle.track_eliminate(adv, 6).tolist() == [0, 2, 3, 5, 6, 7]  # -0 ties +0
+    assert oracle.track_eliminate(adv, 7).tolist() == [0, 1, 2, 3, 5, 6, 7]  # NaN goes first
+    assert oracle.track_eliminate(np.zeros(10, np.float32), 4).tolist() == [0, 1, 2, 3]
+    # distinct advantages: permuting the tracks permutes the survivors
+    rng = np.random.default_rng(13)
+    a = rng.permutation(1000).astype(np.float32)
+    perm = rng.permutation(1000)
+    base = set(oracle.track_eliminate(a, 300).tolist())
+    moved = set(oracle.track_eliminate(a[perm], 300).tolist())
+    assert {int(perm[i]) for i in moved} == base
+    assert base == set(np.flatnonzero(a >= 700).tolist())
+    with pytest.raises(ValueError):
+        oracle.track_eliminate(adv, 9)
+
+
+def test_eliminate_count_rounds_the_dropped_share_down():
+    assert [oracle.eliminate_count(n) for n in (1, 2, 3, 64, 65, 127, 4096)] == [1, 1, 2, 32, 33, 64, 2048]
+    assert oracle.eliminate_count(100, rho=0.3) == 70
