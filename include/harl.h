@@ -195,6 +195,46 @@ int harl_topk(const float *d_score, int32_t n, int32_t k, int64_t index_base, fl
 /* Fill a running top-k with the empty sentinel (-inf, INT64_MAX) in every slot. */
 int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *stream);
 
+/* ============================================================================================
+ * Schedule tracks between rounds: reward and advantage of a modification step (Algorithm 1,
+ * Eq. 4) and the adaptive-stopping elimination (Section 5).
+ * ============================================================================================ */
+
+/*
+ * Reward and advantage of one modification step of n schedule tracks.  Track i moved from state s
+ * (cost-model score d_c_prev[i], critic value d_v_prev[i]) to s' (d_c_next[i], d_v_next[i]):
+ *   reward     r = (C(s') - C(s)) / max(|C(s)|, eps)     (Algorithm 1's relative score change;
+ *                  the denominator is read as max(|C(s)|, eps) so that signed scores keep the sign
+ *                  of an improvement and a zero score stays finite)
+ *   advantage  A = r + gamma * V(s') - V(s)             (Eq. 4; the paper uses gamma = 0.9)
+ * computed in fp32.  All arrays [n] fp32, 4-byte aligned, device memory; d_reward may be NULL.
+ * NaN inputs propagate.  n == 0 is a no-op; eps must be > 0 and finite.
+ */
+int harl_track_advantage(const float *d_c_prev, const float *d_c_next, const float *d_v_prev,
+                         const float *d_v_next, int32_t n, float gamma, float eps, float *d_reward,
+                         float *d_adv, void *stream);
+
+/* Bytes of device workspace harl_track_eliminate needs for n tracks. */
+size_t harl_track_eliminate_workspace_size(int32_t n);
+
+/*
+ * Adaptive-stopping elimination (Section 5): rank the n tracks by advantage (descending; NaN
+ * behind every number; -0 ties +0; then lower track index) and keep the first n_keep, i.e. drop
+ * the n - n_keep of lowest advantage (the paper drops the proportion rho = 0.5 every lambda = 20
+ * steps while at least 64 tracks remain; the caller chooses n_keep).
+ *   d_adv          [n] fp32 in, 4-byte aligned.
+ *   d_keep_index   [n_keep] int32 out: the surviving tracks' indices in ascending order.
+ *   d_rows         [n][row_bytes] in, or NULL: per-track rows (e.g. the policy states);
+ *   d_rows_out     [n_keep][row_bytes] out, or NULL: the survivors' rows in d_keep_index order
+ *                  (both or neither of d_rows / d_rows_out; row_bytes >= 1; no overlap).
+ *   d_ws, ws_bytes workspace of at least harl_track_eliminate_workspace_size(n) bytes,
+ *                  256-byte aligned; its contents on entry do not matter.
+ * 0 <= n_keep <= n; n_keep == 0 is a no-op.  The result is exact and deterministic.
+ */
+int harl_track_eliminate(const float *d_adv, int32_t n, int32_t n_keep, int32_t *d_keep_index,
+                         const void *d_rows, int64_t row_bytes, void *d_rows_out, void *d_ws,
+                         size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -158,4 +158,49 @@ int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *str
     return harl::topk_reset_launch(d_io_score, d_io_index, k, static_cast<hipStream_t>(stream));
 }
 
+int harl_track_advantage(const float *d_c_prev, const float *d_c_next, const float *d_v_prev, const float *d_v_next,
+                         int32_t n, float gamma, float eps, float *d_reward, float *d_adv, void *stream) {
+    if (n < 0) return fail(HARL_E_INVALID_ARG, "harl_track_advantage: negative size");
+    if (!(eps > 0.f) || !(eps < INFINITY)) return fail(HARL_E_INVALID_ARG, "harl_track_advantage: eps must be > 0 and finite");
+    if (n == 0) return HARL_OK;
+    const float *in[] = {d_c_prev, d_c_next, d_v_prev, d_v_next};
+    for (const float *p : in)
+        if (!p || !aligned(p, 4)) return fail(HARL_E_INVALID_ARG, "harl_track_advantage: null or misaligned input");
+    if (!d_adv || !aligned(d_adv, 4) || (d_reward && !aligned(d_reward, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_track_advantage: null or misaligned output");
+    return harl::track_advantage_launch(d_c_prev, d_c_next, d_v_prev, d_v_next, n, gamma, eps, d_reward, d_adv,
+                                        static_cast<hipStream_t>(stream));
+}
+
+size_t harl_track_eliminate_workspace_size(int32_t n) {
+    if (n < 0) return 0;
+    return harl::track_eliminate_ws_bytes(n);
+}
+
+int harl_track_eliminate(const float *d_adv, int32_t n, int32_t n_keep, int32_t *d_keep_index, const void *d_rows,
+                         int64_t row_bytes, void *d_rows_out, void *d_ws, size_t ws_bytes, void *stream) {
+    if (n < 0 || n_keep < 0 || n_keep > n) return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: need 0 <= n_keep <= n");
+    if ((d_rows == nullptr) != (d_rows_out == nullptr))
+        return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: give both rows and rows_out, or neither");
+    if (d_rows && (row_bytes < 1 || row_bytes > ((int64_t)1 << 40) / (n > 0 ? n : 1)))
+        return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: row_bytes out of range");
+    if (n_keep == 0) return HARL_OK;
+    if (!d_adv || !aligned(d_adv, 4)) return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: null or misaligned advantages");
+    if (!d_keep_index || !aligned(d_keep_index, 4))
+        return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: null or misaligned keep_index");
+    if (d_rows) {
+        const char *a = static_cast<const char *>(d_rows), *b = static_cast<const char *>(d_rows_out);
+        if (a < b + (int64_t)n_keep * row_bytes && b < a + (int64_t)n * row_bytes)
+            return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: rows and rows_out overlap");
+    }
+    if (n_keep < n) {
+        if (!d_ws || !aligned(d_ws, 256))
+            return fail(HARL_E_INVALID_ARG, "harl_track_eliminate: workspace null or not 256-byte aligned");
+        if (ws_bytes < harl::track_eliminate_ws_bytes(n))
+            return fail(HARL_E_WORKSPACE, "harl_track_eliminate: workspace smaller than harl_track_eliminate_workspace_size()");
+    }
+    return harl::track_eliminate_launch(d_adv, n, n_keep, d_keep_index, d_rows, row_bytes, d_rows_out, d_ws,
+                                        static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

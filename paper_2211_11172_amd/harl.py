@@ -28,6 +28,7 @@ EXPORTS = (
     "harl_score_round_workspace_size", "harl_score_round",
     "harl_policy_create", "harl_policy_destroy", "harl_policy_step",
     "harl_topk_workspace_size", "harl_topk", "harl_topk_reset",
+    "harl_track_advantage", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
 )
 
 
@@ -80,6 +81,9 @@ def load():
                 "harl_topk_workspace_size": ([i32, i32], sz),
                 "harl_topk": ([P, i32, i32, i64, P, P, u32, P, sz, P], ctypes.c_int),
                 "harl_topk_reset": ([P, P, i32, P], ctypes.c_int),
+                "harl_track_advantage": ([P, P, P, P, i32, ctypes.c_float, ctypes.c_float, P, P, P], ctypes.c_int),
+                "harl_track_eliminate_workspace_size": ([i32], sz),
+                "harl_track_eliminate": ([P, i32, i32, P, P, i64, P, P, sz, P], ctypes.c_int),
             }
             for name, (args, res) in sig.items():
                 f = getattr(lib, name)
@@ -222,3 +226,27 @@ def harl_topk(score, n: int, k: int, index_base: int, io_score, io_index, flags:
 
 def harl_topk_reset(io_score, io_index, k: int, stream=None):
     _check(load().harl_topk_reset(_ptr(io_score), _ptr(io_index), k, _stream(stream)), "harl_topk_reset")
+
+
+# ------------------------------------------------------------------------------------------------
+# schedule tracks
+# ------------------------------------------------------------------------------------------------
+def harl_track_advantage(c_prev, c_next, v_prev, v_next, n: int, gamma: float, eps: float, reward, adv, stream=None):
+    _check(load().harl_track_advantage(_ptr(c_prev), _ptr(c_next), _ptr(v_prev), _ptr(v_next), n, gamma, eps,
+                                       _ptr(reward), _ptr(adv), _stream(stream)), "harl_track_advantage")
+
+
+def harl_track_eliminate_workspace_size(n: int) -> int:
+    return int(load().harl_track_eliminate_workspace_size(n))
+
+
+def harl_track_eliminate(adv, n: int, n_keep: int, keep_index, rows=None, row_bytes: int = 0, rows_out=None, ws=None,
+                         ws_bytes: int = 0, stream=None):
+    _check(load().harl_track_eliminate(_ptr(adv), n, n_keep, _ptr(keep_index), _ptr(rows), row_bytes, _ptr(rows_out),
+                                       _ptr(ws), ws_bytes, _stream(stream)), "harl_track_eliminate")
+
+
+def eliminate_keep_count(n: int, rho: float = 0.5) -> int:
+    """Tracks left after one adaptive-stopping elimination of proportion rho: floor(rho * n) are
+    dropped."""
+    return n - int(rho * n // 1)

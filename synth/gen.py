@@ -17,6 +17,9 @@ Every array comes from its own numpy PCG64 stream keyed by
   9   policy states               yes
  10   policy weights
  11   policy biases
+ 12   track scores C(s)           yes
+ 13   track score changes         yes
+ 14   track critic values         yes
 ====  ==========================  =========
 
 Nothing here computes a score, an activation or a ranking; both the oracle and the HIP path
@@ -31,7 +34,8 @@ import numpy as np
 from .configs import RoundConfig
 
 S_COUNTS, S_FCAT, S_FMAG, S_SPLITF, S_THRQ, S_DEFDIR, S_LEAF, S_CALIB, S_STATES, S_W, S_B = range(1, 12)
-_BATCH_STREAMS = {S_COUNTS, S_FCAT, S_FMAG, S_STATES}
+S_TRACK_C, S_TRACK_DC, S_TRACK_V = 12, 13, 14
+_BATCH_STREAMS = {S_COUNTS, S_FCAT, S_FMAG, S_STATES, S_TRACK_C, S_TRACK_DC, S_TRACK_V}
 
 
 def _rng(cfg: RoundConfig, stream: int, batch: int = 0) -> np.random.Generator:
@@ -206,6 +210,27 @@ def gen_states(cfg: RoundConfig, batch: int = 0, n: int | None = None) -> np.nda
     else:
         s = r.standard_normal((n, cfg.pol_s)).astype(np.float32)
     return _store(s, cfg.pol_dtype)
+
+
+def gen_track_step(cfg: RoundConfig, batch: int = 0, n: int | None = None) -> dict:
+    """One modification step of n schedule tracks (fp32 arrays [n]): cost-model scores before and
+    after (c_prev ~ N(0, 7^2), the spread of the standard round's program scores; c_next = c_prev
+    + N(0, 1), equal to c_prev for 5 % of the tracks, the dummy action) and critic values
+    v_prev, v_next ~ N(0, 1).  The exact variant draws c_prev = +-2^e (e in -2..3), changes k/8
+    (|k| <= 8) and values k/16, so every reward and advantage (gamma = 0.5) is exact in fp32."""
+    n = cfg.n_prog if n is None else n
+    rc, rd, rv = _rng(cfg, S_TRACK_C, batch), _rng(cfg, S_TRACK_DC, batch), _rng(cfg, S_TRACK_V, batch)
+    if cfg.exact:
+        c0 = (rc.choice([-1.0, 1.0], n) * np.exp2(rc.integers(-2, 3, n, endpoint=True))).astype(np.float32)
+        c1 = (c0 + rd.integers(-8, 8, n, endpoint=True) / 8.0).astype(np.float32)
+        v = (rv.integers(-16, 16, (2, n), endpoint=True) / 16.0).astype(np.float32)
+    else:
+        c0 = (rc.standard_normal(n) * 7.0).astype(np.float32)
+        dc = rd.standard_normal(n)
+        dc[rd.random(n) < 0.05] = 0.0
+        c1 = (c0 + dc).astype(np.float32)
+        v = rv.standard_normal((2, n)).astype(np.float32)
+    return dict(c_prev=c0, c_next=c1, v_prev=v[0].copy(), v_next=v[1].copy())
 
 
 def gen_batch(cfg: RoundConfig, batch: int = 0, ld_pad: int = 0) -> dict:

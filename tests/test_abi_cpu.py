@@ -117,3 +117,24 @@ def test_policy_validation(over):
 
 def test_policy_step_argument_errors():
     assert _status("harl_policy_step", None, None, 4, None, None, None, None, None) == harl.HARL_E_INVALID_ARG
+
+
+def test_track_argument_errors():
+    F = ctypes.c_float
+    adv = lambda *a: _status("harl_track_advantage", *a)
+    assert adv(None, None, None, None, -1, F(0.9), F(1e-6), None, None, None) == harl.HARL_E_INVALID_ARG
+    assert adv(None, None, None, None, 0, F(0.9), F(1e-6), None, None, None) == harl.HARL_OK
+    assert adv(None, None, None, None, 0, F(0.9), F(0.0), None, None, None) == harl.HARL_E_INVALID_ARG  # eps <= 0
+    assert adv(0x1000, 0x1000, 0x1000, None, 4, F(0.9), F(1e-6), None, 0x2000, None) == harl.HARL_E_INVALID_ARG
+    assert adv(0x1000, 0x1000, 0x1000, 0x1000, 4, F(0.9), F(1e-6), 0x2002, 0x2000, None) == harl.HARL_E_INVALID_ARG
+    el = lambda *a: _status("harl_track_eliminate", *a)
+    assert el(None, 10, 11, None, None, 0, None, None, 0, None) == harl.HARL_E_INVALID_ARG       # n_keep > n
+    assert el(None, 10, 0, None, None, 0, None, None, 0, None) == harl.HARL_OK                    # no-op
+    assert el(0x1000, 10, 4, 0x2000, 0x3000, 16, None, 0x4000, 1 << 20, None) == harl.HARL_E_INVALID_ARG  # rows w/o out
+    assert el(0x1000, 10, 4, 0x2000, 0x3000, 0, 0x9000, 0x4000, 1 << 20, None) == harl.HARL_E_INVALID_ARG  # row_bytes 0
+    assert el(0x1000, 10, 4, 0x2000, 0x3000, 64, 0x3100, 0x4000, 1 << 20, None) == harl.HARL_E_INVALID_ARG  # overlap
+    assert el(0x1000, 10, 4, 0x2000, None, 0, None, 0x4000, 8, None) == harl.HARL_E_WORKSPACE
+    assert el(0x1000, 10, 4, 0x2000, None, 0, None, 0x4001, 1 << 20, None) == harl.HARL_E_INVALID_ARG
+    assert el(0x1001, 10, 4, 0x2000, None, 0, None, 0x4000, 1 << 20, None) == harl.HARL_E_INVALID_ARG
+    assert harl.harl_track_eliminate_workspace_size(-1) == 0
+    assert harl.harl_track_eliminate_workspace_size(100000) >= 256 + 25 * 1024
