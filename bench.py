@@ -69,6 +69,10 @@ def parse():
                     help="feature-ingest calibration: harl_score_round over the throughput round's 2.13 M "
                          "statement rows (1.4 GB of features) with shallow ensembles (node visits per row "
                          "<= 16), so that staging the features dominates; prints HBM GB/s and exits")
+    ap.add_argument("--tracks", action="store_true",
+                    help="schedule-track calls between rounds: harl_track_advantage and harl_track_eliminate "
+                         "(drop the lower half, compact the survivors' policy states) on the standard and "
+                         "throughput rounds' track counts; prints one JSON line and exits")
     ap.add_argument("--two-streams", action="store_true",
                     help="run the policy on a second stream after scoring, beside top-K (default: the "
                          "three calls in turn on one stream, which measured faster on the standard round)")
@@ -169,6 +173,88 @@ def ingest_calibration(args):
                       "steps": args.steps, "results": rows}), flush=True)
 
 
+def tracks_bench(args):
+    """Time the calls of one adaptive-stopping elimination point: advantages of every track
+    (Eq. 4), then elimination of the lower half with the survivors' policy states gathered
+    (Section 5).  HIP events around a graph of `steps` back-to-back calls."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2211_11172_amd import harl
+    from synth import gen_states, gen_track_step, get_config
+
+    dev = torch.device("cuda:0")
+    main_stream = torch.cuda.current_stream(dev)
+
+    def timed(fn):
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(args.steps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main_stream)
+        g.replay()
+        e1.record(main_stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps * 1e3
+
+    results = []
+    for name in ("standard", "throughput"):
+        cfg = get_config(name)
+        n = cfg.n_prog
+        step = gen_track_step(cfg)
+        d = {k: torch.from_numpy(v).to(dev) for k, v in step.items()}
+        states = torch.from_numpy(gen_states(cfg)).to(dev)
+        row_bytes = states.shape[1] * states.element_size()
+        n_keep = harl.eliminate_keep_count(n)
+        reward = torch.empty(n, device=dev)
+        adv = torch.empty(n, device=dev)
+        keep = torch.empty(n_keep, dtype=torch.int32, device=dev)
+        rows_out = torch.empty((n_keep, states.shape[1]), dtype=states.dtype, device=dev)
+        wsb = harl.harl_track_eliminate_workspace_size(n)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        adv_us = timed(lambda: harl.harl_track_advantage(d["c_prev"], d["c_next"], d["v_prev"], d["v_next"], n, 0.9,
+                                                         1e-6, reward, adv))
+        elim_us = timed(lambda: harl.harl_track_eliminate(adv, n, n_keep, keep, states, row_bytes, rows_out, ws, wsb))
+        both_us = timed(lambda: (harl.harl_track_advantage(d["c_prev"], d["c_next"], d["v_prev"], d["v_next"], n, 0.9,
+                                                           1e-6, reward, adv),
+                                 harl.harl_track_eliminate(adv, n, n_keep, keep, states, row_bytes, rows_out, ws,
+                                                           wsb)))
+        # algorithmic bytes: advantage 4 x 4 B in + 2 x 4 B out per track; elimination reads the
+        # advantages once and writes 4 B per survivor, the gather moves 2 x row_bytes per survivor
+        adv_bytes = n * 24
+        elim_bytes = n * 4 + n_keep * (4 + 2 * row_bytes)
+        same = bool(np.array_equal(keep.cpu().numpy(), oracle.track_eliminate(adv.cpu().numpy(), n_keep)))
+        entry = {"workload": name, "tracks": n, "kept": n_keep, "row_bytes": row_bytes,
+                 "advantage_us": adv_us, "eliminate_us": elim_us, "both_us": both_us,
+                 "tracks_per_s": n / (both_us * 1e-6),
+                 "advantage_gbs": adv_bytes / (adv_us * 1e-6) / 1e9,
+                 "eliminate_gbs": elim_bytes / (elim_us * 1e-6) / 1e9, "matches_oracle": same}
+        if not args.no_cpu_baseline:
+            a64 = None
+            t0 = time.perf_counter()
+            reps = 0
+            while time.perf_counter() - t0 < 2.0 or reps == 0:
+                a64 = oracle.track_advantage(step["c_prev"], step["c_next"], step["v_prev"], step["v_next"])
+                kk = oracle.track_eliminate(a64["adv"].astype(np.float32), n_keep)
+                _ = step["c_prev"][kk]
+                reps += 1
+            el = time.perf_counter() - t0
+            entry["cpu_baseline"] = {"value": n * reps / el, "unit": "tracks/s", "cores": 1, "kind": "oracle",
+                                     "sample": "%d full elimination points of %d tracks in %.1f s" % (reps, n, el)}
+        print("tracks %s: advantage %.1f us, eliminate+gather %.1f us, both %.1f us" % (name, adv_us, elim_us, both_us),
+              file=sys.stderr, flush=True)
+        results.append(entry)
+    print(json.dumps({"metric": "schedule-track advantage + elimination (one adaptive-stopping point)",
+                      "unit": "us per call", "steps": args.steps, "gamma": 0.9, "rho": 0.5,
+                      "results": results}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -177,6 +263,9 @@ def main():
         sys.exit(2)
     if args.ingest:
         ingest_calibration(args)
+        return
+    if args.tracks:
+        tracks_bench(args)
         return
     import numpy as np
     import torch

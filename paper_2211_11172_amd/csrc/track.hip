@@ -17,7 +17,8 @@
 //    survives, and of the keys equal to T the first `need` in track order: k_elim_count counts both
 //    per block, k_elim_scan turns the counts into block offsets, and k_elim_scatter writes each
 //    survivor's index at its position in track order.  No atomics leave a workgroup, so the result
-//    does not depend on scheduling.
+//    does not depend on scheduling.  Up to kFusedMax tracks, k_elim_fused does all of it in one
+//    workgroup (keys in registers, the histograms in LDS) instead of eleven launches.
 #include <hip/hip_runtime.h>
 
 #include "internal.hpp"
@@ -225,6 +226,93 @@ __global__ __launch_bounds__(kElimThreads) void k_elim_scatter(const float *__re
     }
 }
 
+constexpr int kFusedThreads = 1024, kFusedPer = 16, kFusedMax = kFusedThreads * kFusedPer;
+
+// The whole elimination of n <= kFusedMax tracks in one workgroup: thread t holds the keys of
+// tracks [16t, 16t + 16) in registers; each radix pass histograms the live keys into one of two
+// LDS histograms (the other is cleared meanwhile) and wave 0 picks the digit; the survivors'
+// positions come from one workgroup-wide prefix sum of the per-thread counts.
+__global__ __launch_bounds__(kFusedThreads) void k_elim_fused(const float *__restrict__ adv, int n, int n_keep,
+                                                              int32_t *__restrict__ keep_index) {
+    __shared__ uint32_t hist[2][256];
+    __shared__ uint32_t s_digit, s_above;
+    __shared__ uint64_t wsum[kFusedThreads / 64];
+    const int t = threadIdx.x, lane = t % 64;
+    const int i0 = t * kFusedPer;
+    uint32_t key[kFusedPer];
+#pragma unroll
+    for (int q = 0; q < kFusedPer; ++q) key[q] = i0 + q < n ? order_key(adv[i0 + q]) : 0u;
+    if (t < 512) (&hist[0][0])[t] = 0;
+    __syncthreads();
+    uint32_t prefix = 0, need = (uint32_t)n_keep;
+    int hb = 0;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+#pragma unroll
+        for (int q = 0; q < kFusedPer; ++q) {
+            const bool alive = i0 + q < n && (shift == 24 || ((key[q] ^ prefix) >> (shift + 8)) == 0);
+            const uint32_t bin = (key[q] >> shift) & 255u;
+            const uint64_t live = __ballot(alive);
+            if (live) {
+                const int first = __builtin_ctzll(live);
+                const uint32_t b0 = __builtin_amdgcn_readlane(bin, first);
+                const uint64_t same = __ballot(alive && bin == b0);
+                if (lane == first) atomicAdd(&hist[hb][b0], (uint32_t)__popcll(same));
+                if (alive && bin != b0) atomicAdd(&hist[hb][bin], 1u);
+            }
+        }
+        // the other histogram was last read before the previous pass's final barrier
+        if (t < 256) hist[hb ^ 1][t] = 0;
+        __syncthreads();
+        if (t < 64) {
+            const uint32_t *h = hist[hb];
+            const uint32_t h0 = h[255 - 4 * t], h1 = h[254 - 4 * t], h2 = h[253 - 4 * t], h3 = h[252 - 4 * t];
+            const uint32_t sum = h0 + h1 + h2 + h3;
+            uint32_t incl = sum;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t v = __shfl_up(incl, o, 64);
+                if (t >= o) incl += v;
+            }
+            const uint32_t excl = incl - sum;
+            if (excl < need && incl >= need) {
+                uint32_t above = excl;
+                int d;
+                if (above + h0 >= need) d = 255 - 4 * t;
+                else if (above += h0, above + h1 >= need) d = 254 - 4 * t;
+                else if (above += h1, above + h2 >= need) d = 253 - 4 * t;
+                else { above += h2; d = 252 - 4 * t; }
+                s_digit = (uint32_t)d;
+                s_above = above;
+            }
+        }
+        __syncthreads();
+        prefix |= s_digit << shift;
+        need -= s_above;
+        hb ^= 1;
+    }
+    const uint32_t T = prefix;
+    uint32_t above = 0, eq = 0;
+#pragma unroll
+    for (int q = 0; q < kFusedPer; ++q)
+        if (i0 + q < n) {
+            above += key[q] > T;
+            eq += key[q] == T;
+        }
+    uint64_t total;
+    const uint64_t ex = block_excl_scan<kFusedThreads>((uint64_t)above | ((uint64_t)eq << 32), wsum, total);
+    above = (uint32_t)ex;
+    eq = (uint32_t)(ex >> 32);
+#pragma unroll
+    for (int q = 0; q < kFusedPer; ++q)
+        if (i0 + q < n) {
+            const uint32_t pos = above + (eq < need ? eq : need);
+            const bool keep = key[q] > T || (key[q] == T && eq < need);
+            if (keep && pos < (uint32_t)n_keep) keep_index[pos] = i0 + q;
+            above += key[q] > T;
+            eq += key[q] == T;
+        }
+}
+
 __global__ __launch_bounds__(kGatherThreads) void k_iota(int32_t *__restrict__ out, int n) {
     const int i = blockIdx.x * kGatherThreads + threadIdx.x;
     if (i < n) out[i] = i;
@@ -297,6 +385,9 @@ int track_eliminate_launch(const float *adv, int32_t n, int32_t n_keep, int32_t 
     if (n_keep == n) {
         hipLaunchKernelGGL(k_iota, dim3((unsigned)ceil_div(n, kGatherThreads)), dim3(kGatherThreads), 0, stream,
                            keep_index, n);
+        HARL_HIP_CHECK(hipGetLastError());
+    } else if (n <= kFusedMax) {
+        hipLaunchKernelGGL(k_elim_fused, dim3(1), dim3(kFusedThreads), 0, stream, adv, n, n_keep, keep_index);
         HARL_HIP_CHECK(hipGetLastError());
     } else {
         const ElimLayout L = elim_layout(n);
