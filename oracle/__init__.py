@@ -4,7 +4,8 @@ A ctypes wrapper over ``harl_oracle.c`` (plain C, fp64, optional OpenMP).  It co
 paper's definitions, what the HIP path must reproduce: per-program cost-model scores (GBDT over
 statement rows, summed per program), the actor/critic forward with its argmax action, and the
 top-K / running-heap selection, and for schedule tracks the reward, the advantage and the
-adaptive-stopping elimination.  Only ``tests/``, the package's ``smoke()`` check and
+adaptive-stopping elimination, and the per-modification-type action selection (greedy or sampled
+through a counter-based generator).  Only ``tests/``, the package's ``smoke()`` check and
 ``bench.py``'s ``cpu_baseline`` leg may import this package; the product path never does.
 """
 from __future__ import annotations
@@ -48,12 +49,15 @@ def _bind(lib):
     lib.oracle_merge.argtypes = [P, P, i32, P, i64, i64]
     lib.oracle_track_advantage.argtypes = [P, P, P, P, i64, dbl, dbl, P, P, P]
     lib.oracle_track_eliminate.argtypes = [P, i64, i64, P]
+    lib.oracle_philox4x32.argtypes = [P, P, P]
+    lib.oracle_philox4x32.restype = None
+    lib.oracle_policy_select.argtypes = [P, i64, i32, P, i32, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, P, P, P]
     lib.oracle_max_threads.argtypes = []
     lib.oracle_round_bf16.argtypes = [dbl]
     lib.oracle_round_bf16.restype = dbl
     for f in (lib.oracle_score_round, lib.oracle_policy_step, lib.oracle_topk,
               lib.oracle_merge, lib.oracle_max_threads, lib.oracle_track_advantage,
-              lib.oracle_track_eliminate):
+              lib.oracle_track_eliminate, lib.oracle_policy_select):
         f.restype = ctypes.c_int
     return lib
 
@@ -221,3 +225,31 @@ def eliminate_count(n: int, rho: float = 0.5) -> int:
     """Tracks that survive one elimination of proportion rho (Section 5): the eliminated number
     floor(rho * n) is rounded down."""
     return n - int(np.floor(rho * n))
+
+
+def philox4x32(counter, key) -> list:
+    """Philox4x32-10 of a 4-word counter and a 2-word key (the published generator)."""
+    lib = _load()
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib.oracle_philox4x32(_p(c), _p(k), _p(out))
+    return [int(x) for x in out]
+
+
+def policy_select(logits, seg_offsets, sample: bool = False, seed: int = 0, counter: int = 0) -> dict:
+    """One action per modification type (segment of the logits row): greedy or Gumbel-max sampled;
+    returns action [B][n_seg] int32, logp [B][n_seg] and probs [B][a] (fp64)."""
+    lib = _load()
+    z = _c(logits, np.float32)
+    B, a = z.shape
+    off = _c(seg_offsets, np.int32)
+    n_seg = off.size - 1
+    action = np.zeros((B, n_seg), dtype=np.int32)
+    logp = np.zeros((B, n_seg), dtype=np.float64)
+    probs = np.zeros((B, a), dtype=np.float64)
+    rc = lib.oracle_policy_select(_p(z), B, a, _p(off), n_seg, int(bool(sample)), seed, counter, _p(action),
+                                  _p(logp), _p(probs))
+    if rc != 0:
+        raise ValueError("oracle_policy_select failed (%d)" % rc)
+    return dict(action=action, logp=logp, probs=probs)

@@ -18,7 +18,13 @@
  *   oracle_track_advantage  reward of a modification step (Algorithm 1) and the advantage of
  *                        Eq. 4 for every schedule track;
  *   oracle_track_eliminate  adaptive-stopping elimination of the tracks with the lowest
- *                        advantages (Section 5).
+ *                        advantages (Section 5);
+ *   oracle_policy_select  one action per modification type from the actor's logits (Section 4.3:
+ *                        the best modification of each type; Appendix A.2: num_iters^2 + 1 tile
+ *                        actions and 3 for each other type), greedy or sampled as PPO rollouts
+ *                        do (Section 6.1), with the per-type softmax and log-probability;
+ *   oracle_philox4x32    the counter-based generator the sampling draws from (Salmon, Moraes,
+ *                        Dror, Shaw: "Parallel random numbers: as easy as 1, 2, 3", SC'11).
  *
  * All arithmetic on scores and activations is fp64 over the given fp32 / bf16 input values.
  * Nothing here is blocked, fused or reordered beyond the definitions.  Only tests/, the package's
@@ -37,7 +43,14 @@
  *   - the reward's denominator C(s) is taken as max(|C(s)|, eps): the paper's scores are
  *     positive, signed scores keep the sign of an improvement and a zero score stays finite;
  *   - elimination ranks tracks like top-K (advantage desc, NaN last, -0 ties +0, then lower track
- *     index), keeps a given number of them and lists the survivors in ascending track order.
+ *     index), keeps a given number of them and lists the survivors in ascending track order;
+ *   - the actor's logits are one flat row cut into consecutive segments, one per modification
+ *     type; a segment's action is the lowest index attaining its maximum (of the logits, or of
+ *     logit + Gumbel noise when sampling); NaN logits never win; a segment of only NaN / -inf
+ *     logits picks its first action;
+ *   - the Gumbel noise of logit i of state b is -log(-log(u)), u = (w + 0.5) * 2^-24 from the top
+ *     24 bits w of word i % 4 of Philox4x32-10(counter = (i / 4, b, counter_lo, counter_hi),
+ *     key = (seed_lo, seed_hi)).
  */
 #include <math.h>
 #include <stdint.h>
@@ -362,5 +375,78 @@ int oracle_track_eliminate(const float *adv, int64_t n, int64_t n_keep, int32_t 
         if (keep[i]) keep_index[m++] = (int32_t)i;
     free(c);
     free(keep);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------------------------- */
+/* Per-type action selection                                                                    */
+/* ------------------------------------------------------------------------------------------- */
+
+/* Philox4x32 with 10 rounds, from its published definition: each round multiplies counter words
+ * 0 and 2 by two constants into 64-bit products, and the new counter is
+ * (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0)); the key is advanced by the
+ * Weyl constants between rounds. */
+void oracle_philox4x32(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4]) {
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t c[4] = {ctr_in[0], ctr_in[1], ctr_in[2], ctr_in[3]};
+    uint32_t k[2] = {key_in[0], key_in[1]};
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k[0] += W0;
+            k[1] += W1;
+        }
+        const uint64_t p0 = (uint64_t)M0 * c[0], p1 = (uint64_t)M1 * c[2];
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        const uint32_t n0 = hi1 ^ c[1] ^ k[0], n2 = hi0 ^ c[3] ^ k[1];
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+    }
+    memcpy(out, c, sizeof(c));
+}
+
+/* The Gumbel noise of logit i of state b (see the readings above). */
+static double gumbel_noise(uint64_t seed, uint64_t counter, int64_t b, int32_t i) {
+    const uint32_t ctr[4] = {(uint32_t)(i / 4), (uint32_t)b, (uint32_t)counter, (uint32_t)(counter >> 32)};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t w[4];
+    oracle_philox4x32(ctr, key, w);
+    const double u = ((double)(w[i % 4] >> 8) + 0.5) * (1.0 / 16777216.0);
+    return -log(-log(u));
+}
+
+/* For every state b and segment s = [off[s], off[s+1]) of its a logits: the chosen action (the
+ * lowest index attaining the maximum of z_i, or of z_i + Gumbel noise when `sample`), its
+ * log-probability under the segment's softmax, and the softmax itself (fp64). */
+int oracle_policy_select(const float *logits, int64_t B, int32_t a, const int32_t *off, int32_t n_seg,
+                         int sample, uint64_t seed, uint64_t counter, int32_t *action, double *logp,
+                         double *probs) {
+    if (B < 0 || a < 1 || n_seg < 1 || off[0] != 0 || off[n_seg] != a) return ORACLE_EINVAL;
+    for (int32_t s = 0; s < n_seg; ++s)
+        if (off[s + 1] <= off[s]) return ORACLE_EINVAL;
+    for (int64_t b = 0; b < B; ++b) {
+        const float *z = logits + b * a;
+        for (int32_t s = 0; s < n_seg; ++s) {
+            const int32_t lo = off[s], hi = off[s + 1];
+            double m = -INFINITY, best = -INFINITY;
+            int32_t pick = lo;
+            for (int32_t i = lo; i < hi; ++i) {
+                const double v = z[i];
+                if (v > m) m = v;
+                const double key = sample ? v + gumbel_noise(seed, counter, b, i) : v;
+                if (key > best) {
+                    best = key;
+                    pick = i;
+                }
+            }
+            double sum = 0.0;
+            for (int32_t i = lo; i < hi; ++i) sum += exp((double)z[i] - m);
+            for (int32_t i = lo; i < hi; ++i) probs[b * a + i] = exp((double)z[i] - m) / sum;
+            action[b * n_seg + s] = pick;
+            logp[b * n_seg + s] = (double)z[pick] - m - log(sum);
+        }
+    }
     return ORACLE_OK;
 }

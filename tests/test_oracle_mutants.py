@@ -66,6 +66,20 @@ MUTANTS = {
     "eliminate_rank_order_out": ("if (keep[i]) keep_index[m++] = (int32_t)i;",
                                  "if (keep[i]) keep_index[m++] = (int32_t)i;\n    for (int64_t k = 0; k < n_keep; ++k) keep_index[k] = (int32_t)c[k].index;",
                                  [(pins.test_eliminate_ranking_properties_small, {})]),
+    "philox_multipliers_swapped": ("(uint64_t)M0 * c[0], p1 = (uint64_t)M1 * c[2]",
+                                   "(uint64_t)M1 * c[0], p1 = (uint64_t)M0 * c[2]",
+                                   [(pins.test_philox_known_answers, {})]),
+    "philox_key_bumped_first": ("if (round > 0) {\n            k[0] += W0;", "if (round >= 0) {\n            k[0] += W0;",
+                                [(pins.test_philox_known_answers, {})]),
+    "select_last_tie": ("if (key > best) {", "if (key >= best) {",
+                        [(pins.test_greedy_select_is_per_segment_first_argmax, {})]),
+    "gumbel_sign": ("return -log(-log(u));", "return log(-log(u));",
+                    [(pins.test_sampling_frequencies_follow_the_softmax, {})]),
+    "logp_unnormalised": ("logp[b * n_seg + s] = (double)z[pick] - m - log(sum);",
+                          "logp[b * n_seg + s] = (double)z[pick] - m;",
+                          [(pins.test_select_softmax_and_logp_identities, {})]),
+    "segment_shifted": ("const int32_t lo = off[s], hi = off[s + 1];", "const int32_t lo = off[s], hi = off[s + 1] - (s == 0);",
+                        [(pins.test_greedy_select_is_per_segment_first_argmax, {})]),
 }
 
 

@@ -4,7 +4,8 @@ cost model is XGBoost, Section 6.1, Appendix A.2); the actor and critic act on t
 (Algorithm 1; Section 4.3, Eq. 6); the top-K of the heap H are the K best predicted scores
 (Algorithm 1; Section 4.3, Top-K Selection Phase); each step of a schedule track is rewarded with
 the relative change of its score (Algorithm 1) and judged by the advantage of Eq. 4, and the
-adaptive-stopping search drops the tracks of lowest advantage (Section 5)."""
+adaptive-stopping search drops the tracks of lowest advantage (Section 5); the actor picks the best
+modification of each type (Section 4.3, Appendix A.2), sampled during PPO rollouts (Section 6.1)."""
 from __future__ import annotations
 
 import numpy as np
@@ -450,3 +451,82 @@ def test_eliminate_special_cases():
 def test_eliminate_count_rounds_the_dropped_share_down():
     assert [oracle.eliminate_count(n) for n in (1, 2, 3, 64, 65, 127, 4096)] == [1, 1, 2, 32, 33, 64, 2048]
     assert oracle.eliminate_count(100, rho=0.3) == 70
+
+
+# ----------------------------------------------------------------------------------------------
+# per-type action selection and its random numbers
+# ----------------------------------------------------------------------------------------------
+def test_philox_known_answers():
+    # known-answer values of Philox4x32-10 distributed with the generator's reference
+    # implementation (Salmon et al., SC'11): (counter, key) -> output
+    kat = [
+        ([0, 0, 0, 0], [0, 0], [0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8]),
+        ([0xFFFFFFFF] * 4, [0xFFFFFFFF] * 2, [0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD]),
+        ([0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344], [0xA4093822, 0x299F31D0],
+         [0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1]),
+    ]
+    for ctr, key, want in kat:
+        assert oracle.philox4x32(ctr, key) == want
+
+
+_SEGS = np.array([0, 17, 20, 23, 26], np.int32)   # num_iters = 4: 4 x 4 + 1 tile actions, 3 x 3 others
+
+
+def test_greedy_select_is_per_segment_first_argmax():
+    rng = np.random.default_rng(21)
+    z = rng.integers(-3, 3, (500, 26)).astype(np.float32)     # many ties
+    z[::7, 3] = np.nan
+    z[5, 17:20] = -np.inf
+    z[6, 20:23] = np.nan
+    got = oracle.policy_select(z, _SEGS)
+    for s in range(4):
+        lo, hi = _SEGS[s], _SEGS[s + 1]
+        seg = np.where(np.isnan(z[:, lo:hi]), -np.inf, z[:, lo:hi])
+        np.testing.assert_array_equal(got["action"][:, s], lo + np.argmax(seg, axis=1))
+    assert got["action"][5, 1] == 17 and got["action"][6, 2] == 20
+
+
+def test_select_softmax_and_logp_identities():
+    rng = np.random.default_rng(22)
+    z = (rng.standard_normal((300, 26)) * 3).astype(np.float32)
+    for sample in (False, True):
+        got = oracle.policy_select(z, _SEGS, sample=sample, seed=7, counter=3)
+        for s in range(4):
+            lo, hi = _SEGS[s], _SEGS[s + 1]
+            np.testing.assert_allclose(got["probs"][:, lo:hi].sum(axis=1), 1.0, atol=1e-12)
+            p = got["probs"][np.arange(300), got["action"][:, s]]
+            np.testing.assert_allclose(got["logp"][:, s], np.log(p), rtol=0, atol=1e-12)
+            ratio = got["probs"][:, lo + 1] / got["probs"][:, lo]
+            np.testing.assert_allclose(ratio, np.exp(z[:, lo + 1].astype(np.float64) - z[:, lo]), rtol=1e-12)
+
+
+def test_sampling_frequencies_follow_the_softmax():
+    # Gumbel-max: argmax(z + G) is distributed as softmax(z); 40,000 draws (states) of one row
+    z = np.log(np.array([[0.5, 0.3, 0.2, 0.05, 0.6, 0.35]], np.float64)).astype(np.float32)
+    segs = np.array([0, 3, 6], np.int32)
+    n = 40000
+    got = oracle.policy_select(np.repeat(z, n, axis=0), segs, sample=True, seed=0x1234_5678_9ABC, counter=5)
+    for s, (lo, hi) in enumerate(((0, 3), (3, 6))):
+        p = np.exp(z[0, lo:hi].astype(np.float64))
+        p /= p.sum()
+        freq = np.bincount(got["action"][:, s] - lo, minlength=hi - lo) / n
+        sigma = np.sqrt(p * (1 - p) / n)
+        assert np.all(np.abs(freq - p) < 5 * sigma), (freq, p)
+
+
+def test_sampling_is_a_function_of_seed_counter_state():
+    rng = np.random.default_rng(23)
+    z = rng.standard_normal((2000, 26)).astype(np.float32)
+    a = oracle.policy_select(z, _SEGS, sample=True, seed=11, counter=0)["action"]
+    np.testing.assert_array_equal(a, oracle.policy_select(z, _SEGS, sample=True, seed=11, counter=0)["action"])
+    for other in (dict(seed=12, counter=0), dict(seed=11, counter=1), dict(seed=11 + (1 << 32), counter=0),
+                  dict(seed=11, counter=1 << 32)):
+        b = oracle.policy_select(z, _SEGS, sample=True, **other)["action"]
+        assert (a != b).mean() > 0.3
+    # the noise of state b does not depend on the other states
+    sub = oracle.policy_select(z[:1000], _SEGS, sample=True, seed=11, counter=0)["action"]
+    np.testing.assert_array_equal(sub, a[:1000])
+    # huge logit gaps: sampling agrees with the greedy choice
+    zz = z.copy()
+    zz[:, 0] += 1000.0
+    assert (oracle.policy_select(zz, _SEGS, sample=True, seed=3)["action"][:, 0] == 0).all()
