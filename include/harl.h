@@ -196,6 +196,41 @@ int harl_topk(const float *d_score, int32_t n, int32_t k, int64_t index_base, fl
 int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *stream);
 
 /* ============================================================================================
+ * Per-modification-type action selection (Section 4.3: the best modification of each type;
+ * Appendix A.2: num_iters^2 + 1 tile-size actions and 3 per other type; Section 6.1: PPO rollouts
+ * sample the actions).
+ * ============================================================================================ */
+
+#define HARL_SELECT_MAX_SEGMENTS 32
+/* flags for harl_policy_select */
+#define HARL_SELECT_SAMPLE 1u
+
+/*
+ * One action per modification type from the actor's logits (e.g. the d_logits output of
+ * harl_policy_step).  Each row of a logits is cut into n_seg consecutive segments, one per type:
+ * segment s holds actions [seg_offsets[s], seg_offsets[s + 1]).  Per state and segment:
+ *   action  the lowest index attaining the maximum logit (greedy), or with HARL_SELECT_SAMPLE the
+ *           lowest index attaining the maximum of logit + Gumbel noise, a draw from the segment's
+ *           softmax.  The noise of logit i of state b is -log(-log(u)), u = (w + 0.5) * 2^-24 with
+ *           w the top 24 bits of word i % 4 of Philox4x32-10 (Salmon et al., SC'11) at counter
+ *           (i / 4, b, counter low word, counter high word) and key (seed low word, seed high
+ *           word); noise and comparison are fp64.  NaN logits never win; a segment without a
+ *           number above -inf picks its first action.  Indices are row-global (0 .. a-1).
+ *   logp    the chosen action's log-probability under the segment's softmax (fp32).
+ *   probs   the segment-wise softmax of the row (fp32).
+ *   d_logits       [B][a] fp32 in, 4-byte aligned.
+ *   seg_offsets    HOST array [n_seg + 1]: 0 = o_0 < o_1 < ... < o_n_seg = a.
+ *   d_action       [B][n_seg] int32 out.
+ *   d_logp         [B][n_seg] fp32 out, or NULL.
+ *   d_probs        [B][a] fp32 out, or NULL.
+ * 1 <= n_seg <= HARL_SELECT_MAX_SEGMENTS; 1 <= a <= 65535; B >= 0 (B == 0 is a no-op); the same
+ * (seed, counter) gives the same draws, so a rollout step passes a fresh counter.
+ */
+int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_t *seg_offsets,
+                       int32_t n_seg, uint32_t flags, uint64_t seed, uint64_t counter,
+                       int32_t *d_action, float *d_logp, float *d_probs, void *stream);
+
+/* ============================================================================================
  * Schedule tracks between rounds: reward and advantage of a modification step (Algorithm 1,
  * Eq. 4) and the adaptive-stopping elimination (Section 5).
  * ============================================================================================ */

@@ -158,6 +158,26 @@ int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *str
     return harl::topk_reset_launch(d_io_score, d_io_index, k, static_cast<hipStream_t>(stream));
 }
 
+int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_t *seg_offsets, int32_t n_seg,
+                       uint32_t flags, uint64_t seed, uint64_t counter, int32_t *d_action, float *d_logp, float *d_probs,
+                       void *stream) {
+    if (B < 0 || a < 1 || a > 65535) return fail(HARL_E_INVALID_ARG, "harl_policy_select: need B >= 0 and 1 <= a <= 65535");
+    if (n_seg < 1 || n_seg > HARL_SELECT_MAX_SEGMENTS)
+        return fail(HARL_E_INVALID_ARG, "harl_policy_select: n_seg out of range");
+    if (flags & ~HARL_SELECT_SAMPLE) return fail(HARL_E_INVALID_ARG, "harl_policy_select: unknown flag");
+    if (!seg_offsets || seg_offsets[0] != 0 || seg_offsets[n_seg] != a)
+        return fail(HARL_E_INVALID_ARG, "harl_policy_select: segments must run from 0 to a");
+    for (int s = 0; s < n_seg; ++s)
+        if (seg_offsets[s + 1] <= seg_offsets[s])
+            return fail(HARL_E_INVALID_ARG, "harl_policy_select: segment offsets must increase");
+    if (B == 0) return HARL_OK;
+    if (!d_logits || !aligned(d_logits, 4)) return fail(HARL_E_INVALID_ARG, "harl_policy_select: null or misaligned logits");
+    if (!d_action || !aligned(d_action, 4) || (d_logp && !aligned(d_logp, 4)) || (d_probs && !aligned(d_probs, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_policy_select: null or misaligned output");
+    return harl::policy_select_launch(d_logits, B, a, seg_offsets, n_seg, flags, seed, counter, d_action, d_logp,
+                                      d_probs, static_cast<hipStream_t>(stream));
+}
+
 int harl_track_advantage(const float *d_c_prev, const float *d_c_next, const float *d_v_prev, const float *d_v_next,
                          int32_t n, float gamma, float eps, float *d_reward, float *d_adv, void *stream) {
     if (n < 0) return fail(HARL_E_INVALID_ARG, "harl_track_advantage: negative size");

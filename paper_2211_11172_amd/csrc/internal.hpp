@@ -93,6 +93,9 @@ int topk_reset_launch(float *io_score, int64_t *io_index, int32_t k, hipStream_t
 int track_advantage_launch(const float *c_prev, const float *c_next, const float *v_prev, const float *v_next, int32_t n,
                            float gamma, float eps, float *reward, float *adv, hipStream_t stream);
 size_t track_eliminate_ws_bytes(int32_t n);
+int policy_select_launch(const float *logits, int32_t B, int32_t a, const int32_t *seg_offsets, int32_t n_seg,
+                         uint32_t flags, uint64_t seed, uint64_t counter, int32_t *action, float *logp, float *probs,
+                         hipStream_t stream);
 int track_eliminate_launch(const float *adv, int32_t n, int32_t n_keep, int32_t *keep_index, const void *rows,
                            int64_t row_bytes, void *rows_out, void *ws, hipStream_t stream);
 

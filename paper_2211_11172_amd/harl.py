@@ -20,6 +20,8 @@ HARL_OK, HARL_E_INVALID_ARG, HARL_E_UNSUPPORTED, HARL_E_WORKSPACE, HARL_E_HIP, H
 HARL_F32, HARL_BF16 = 0, 1
 HARL_TOPK_MAX_K = 2048
 HARL_TOPK_MERGE = 1
+HARL_SELECT_MAX_SEGMENTS = 32
+HARL_SELECT_SAMPLE = 1
 
 # every entry point declared in include/harl.h
 EXPORTS = (
@@ -28,6 +30,7 @@ EXPORTS = (
     "harl_score_round_workspace_size", "harl_score_round",
     "harl_policy_create", "harl_policy_destroy", "harl_policy_step",
     "harl_topk_workspace_size", "harl_topk", "harl_topk_reset",
+    "harl_policy_select",
     "harl_track_advantage", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
 )
 
@@ -81,6 +84,8 @@ def load():
                 "harl_topk_workspace_size": ([i32, i32], sz),
                 "harl_topk": ([P, i32, i32, i64, P, P, u32, P, sz, P], ctypes.c_int),
                 "harl_topk_reset": ([P, P, i32, P], ctypes.c_int),
+                "harl_policy_select": ([P, i32, i32, P, i32, u32, ctypes.c_uint64, ctypes.c_uint64, P, P, P, P],
+                                       ctypes.c_int),
                 "harl_track_advantage": ([P, P, P, P, i32, ctypes.c_float, ctypes.c_float, P, P, P], ctypes.c_int),
                 "harl_track_eliminate_workspace_size": ([i32], sz),
                 "harl_track_eliminate": ([P, i32, i32, P, P, i64, P, P, sz, P], ctypes.c_int),
@@ -226,6 +231,14 @@ def harl_topk(score, n: int, k: int, index_base: int, io_score, io_index, flags:
 
 def harl_topk_reset(io_score, io_index, k: int, stream=None):
     _check(load().harl_topk_reset(_ptr(io_score), _ptr(io_index), k, _stream(stream)), "harl_topk_reset")
+
+
+def harl_policy_select(logits, B: int, a: int, seg_offsets, flags: int, seed: int, counter: int, action, logp=None,
+                       probs=None, stream=None):
+    """seg_offsets: host sequence [n_seg + 1] (0 .. a)."""
+    off = np.ascontiguousarray(seg_offsets, np.int32)
+    _check(load().harl_policy_select(_ptr(logits), B, a, off.ctypes.data, off.size - 1, flags, seed, counter,
+                                     _ptr(action), _ptr(logp), _ptr(probs), _stream(stream)), "harl_policy_select")
 
 
 # ------------------------------------------------------------------------------------------------

@@ -138,3 +138,18 @@ def test_track_argument_errors():
     assert el(0x1001, 10, 4, 0x2000, None, 0, None, 0x4000, 1 << 20, None) == harl.HARL_E_INVALID_ARG
     assert harl.harl_track_eliminate_workspace_size(-1) == 0
     assert harl.harl_track_eliminate_workspace_size(100000) >= 256 + 25 * 1024
+
+
+def test_policy_select_argument_errors():
+    sel = lambda B, a, off, flags=0, logits=0x1000, action=0x2000: _status(
+        "harl_policy_select", logits, B, a, np.ascontiguousarray(off, np.int32).ctypes.data, len(off) - 1, flags, 0, 0,
+        action, None, None, None)
+    assert sel(4, 26, [0, 17, 20, 23, 27]) == harl.HARL_E_INVALID_ARG        # does not end at a
+    assert sel(4, 26, [1, 17, 20, 23, 26]) == harl.HARL_E_INVALID_ARG        # does not start at 0
+    assert sel(4, 26, [0, 17, 17, 23, 26]) == harl.HARL_E_INVALID_ARG        # empty segment
+    assert sel(4, 26, [0, 17, 20, 23, 26], flags=2) == harl.HARL_E_INVALID_ARG
+    assert sel(4, 26, [0, 17, 20, 23, 26], logits=0x1002) == harl.HARL_E_INVALID_ARG
+    assert sel(4, 26, [0, 17, 20, 23, 26], action=None) == harl.HARL_E_INVALID_ARG
+    assert sel(4, 66000, [0, 66000]) == harl.HARL_E_INVALID_ARG
+    assert sel(4, 40, list(range(0, 41, 1))) == harl.HARL_E_INVALID_ARG     # 40 segments > 32
+    assert sel(0, 26, [0, 17, 20, 23, 26], logits=None, action=None) == harl.HARL_OK
