@@ -73,6 +73,10 @@ def parse():
                     help="schedule-track calls between rounds: harl_track_advantage and harl_track_eliminate "
                          "(drop the lower half, compact the survivors' policy states) on the standard and "
                          "throughput rounds' track counts; prints one JSON line and exits")
+    ap.add_argument("--select", action="store_true",
+                    help="per-modification-type action selection: harl_policy_step of the standard round's fp32 "
+                         "policy with a 26-action head (17 + 3 + 3 + 3) and harl_policy_select on its logits, greedy "
+                         "and sampled, at 4,096 and 65,536 states; prints one JSON line and exits")
     ap.add_argument("--two-streams", action="store_true",
                     help="run the policy on a second stream after scoring, beside top-K (default: the "
                          "three calls in turn on one stream, which measured faster on the standard round)")
@@ -255,6 +259,70 @@ def tracks_bench(args):
                       "results": results}), flush=True)
 
 
+def select_bench(args):
+    """Time one rollout step's action selection: the actor's logits (harl_policy_step), then one
+    action per modification type, greedy and sampled (harl_policy_select)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2211_11172_amd import harl
+    from synth import gen_policy, gen_states, get_config
+
+    dev = torch.device("cuda:0")
+    main_stream = torch.cuda.current_stream(dev)
+    segs = [0, 17, 20, 23, 26]
+
+    def timed(fn):
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(args.steps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main_stream)
+        g.replay()
+        e1.record(main_stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps * 1e3
+
+    results = []
+    for B in (4096, 65536):
+        cfg = get_config("standard").with_(pol_a=26, n_prog=B)
+        P = harl.harl_policy_create(gen_policy(cfg))
+        st = torch.from_numpy(gen_states(cfg)).to(dev)
+        act = torch.empty(B, dtype=torch.int32, device=dev)
+        val = torch.empty(B, device=dev)
+        logits = torch.empty(B, 26, device=dev)
+        sel = torch.empty(B, 4, dtype=torch.int32, device=dev)
+        logp = torch.empty(B, 4, device=dev)
+        probs = torch.empty(B, 26, device=dev)
+        pol_us = timed(lambda: harl.harl_policy_step(P, st, B, act, val, None, logits))
+        greedy_us = timed(lambda: harl.harl_policy_select(logits, B, 26, segs, 0, 0, 0, sel, logp, probs))
+        ctr = [0]
+
+        def sample():
+            harl.harl_policy_select(logits, B, 26, segs, harl.HARL_SELECT_SAMPLE, 1234, ctr[0], sel, logp, probs)
+        sample_us = timed(sample)
+        harl.harl_policy_select(logits, B, 26, segs, harl.HARL_SELECT_SAMPLE, 1234, 0, sel, logp, probs)
+        torch.cuda.synchronize()
+        want = oracle.policy_select(logits.cpu().numpy(), np.array(segs, np.int32), sample=True, seed=1234, counter=0)
+        same = bool(np.array_equal(sel.cpu().numpy(), want["action"]))
+        # algorithmic bytes: the logits read, probabilities written, 2 x 4 B per (state, type)
+        nbytes = B * (26 * 4 * 2 + 4 * 8)
+        results.append({"states": B, "actions": 26, "types": 4, "policy_step_us": pol_us, "select_greedy_us": greedy_us,
+                        "select_sample_us": sample_us, "select_sample_gbs": nbytes / (sample_us * 1e-6) / 1e9,
+                        "sampled_matches_oracle": same})
+        print("select B=%d: policy %.1f us, greedy %.1f us, sampled %.1f us" % (B, pol_us, greedy_us, sample_us),
+              file=sys.stderr, flush=True)
+        P.close()
+    print(json.dumps({"metric": "per-type action selection (harl_policy_select)", "unit": "us per call",
+                      "segments": segs, "steps": args.steps, "results": results}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -266,6 +334,9 @@ def main():
         return
     if args.tracks:
         tracks_bench(args)
+        return
+    if args.select:
+        select_bench(args)
         return
     import numpy as np
     import torch

@@ -223,7 +223,7 @@ int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *str
  *   d_action       [B][n_seg] int32 out.
  *   d_logp         [B][n_seg] fp32 out, or NULL.
  *   d_probs        [B][a] fp32 out, or NULL.
- * 1 <= n_seg <= HARL_SELECT_MAX_SEGMENTS; 1 <= a <= 65535; B >= 0 (B == 0 is a no-op); the same
+ * 1 <= n_seg <= HARL_SELECT_MAX_SEGMENTS; 1 <= a <= 4096; B >= 0 (B == 0 is a no-op); the same
  * (seed, counter) gives the same draws, so a rollout step passes a fresh counter.
  */
 int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_t *seg_offsets,

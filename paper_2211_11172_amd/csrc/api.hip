@@ -161,7 +161,7 @@ int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *str
 int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_t *seg_offsets, int32_t n_seg,
                        uint32_t flags, uint64_t seed, uint64_t counter, int32_t *d_action, float *d_logp, float *d_probs,
                        void *stream) {
-    if (B < 0 || a < 1 || a > 65535) return fail(HARL_E_INVALID_ARG, "harl_policy_select: need B >= 0 and 1 <= a <= 65535");
+    if (B < 0 || a < 1 || a > 4096) return fail(HARL_E_INVALID_ARG, "harl_policy_select: need B >= 0 and 1 <= a <= 4096");
     if (n_seg < 1 || n_seg > HARL_SELECT_MAX_SEGMENTS)
         return fail(HARL_E_INVALID_ARG, "harl_policy_select: n_seg out of range");
     if (flags & ~HARL_SELECT_SAMPLE) return fail(HARL_E_INVALID_ARG, "harl_policy_select: unknown flag");

@@ -2,7 +2,7 @@
 // modification of each modification type; Appendix A.2: num_iters^2 + 1 tile-size actions and 3
 // for each other type; Section 6.1: PPO, whose rollouts sample the actions).
 //
-// K9 k_policy_select: one thread per (state, segment).  The actor's logits row of a state is cut
+// K9 k_policy_select: one (state, segment) per thread.  The actor's logits row of a state is cut
 // into consecutive segments, one per modification type.  A segment's action is the lowest index
 // attaining the maximum of its logits (greedy) or of logit + Gumbel noise (sampling: the
 // Gumbel-max draw from the segment's softmax).  The noise of logit i of state b is -log(-log u),
@@ -18,6 +18,7 @@ namespace harl {
 namespace {
 
 constexpr int kSelectThreads = 256;
+constexpr int kSelectLdsFloats = 4096;  // logits staged per workgroup (with fp64 keys: 48 KB of LDS)
 
 struct Segments {
     int32_t off[HARL_SELECT_MAX_SEGMENTS + 1];
@@ -39,44 +40,72 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
     return c;
 }
 
+// A workgroup owns R consecutive states: their logits rows (contiguous) are staged in LDS with
+// coalesced loads; with SAMPLE every (row, group of 4 logits) item draws one Philox block and
+// stores the fp64 keys logit + noise; then thread p < R * n_seg takes (row p / n_seg, segment
+// p % n_seg) from LDS, and the softmax rows are written back with coalesced stores.
 template <bool SAMPLE>
 __global__ __launch_bounds__(kSelectThreads) void k_policy_select(const float *__restrict__ logits, int B, int a,
-                                                                  Segments seg, int n_seg, uint64_t seed,
+                                                                  int R, Segments seg, int n_seg, uint64_t seed,
                                                                   uint64_t counter, int32_t *__restrict__ action,
                                                                   float *__restrict__ logp, float *__restrict__ probs) {
-    const int64_t tid = (int64_t)blockIdx.x * kSelectThreads + threadIdx.x;
-    if (tid >= (int64_t)B * n_seg) return;
-    const int64_t b = tid / n_seg;
-    const int s = (int)(tid - b * n_seg);
-    const int lo = seg.off[s], hi = seg.off[s + 1];
-    const float *z = logits + b * a;
-    float m = -INFINITY;
-    double best = -INFINITY;
-    int pick = lo;
-    uint4 w = make_uint4(0, 0, 0, 0);
-    for (int i = lo; i < hi; ++i) {
-        const float v = z[i];
-        m = v > m ? v : m;
-        double key = v;
-        if constexpr (SAMPLE) {
-            if (i == lo || (i & 3) == 0)
-                w = philox4x32_10(make_uint4((uint32_t)(i >> 2), (uint32_t)b, (uint32_t)counter, (uint32_t)(counter >> 32)),
-                                  (uint32_t)seed, (uint32_t)(seed >> 32));
-            const uint32_t word = (i & 3) == 0 ? w.x : (i & 3) == 1 ? w.y : (i & 3) == 2 ? w.z : w.w;
-            const double u = ((double)(word >> 8) + 0.5) * (1.0 / 16777216.0);
-            key += -log(-log(u));
+    extern __shared__ __align__(16) char smem[];
+    double *keys = reinterpret_cast<double *>(smem);                                  // [R][a] (SAMPLE)
+    float *zs = reinterpret_cast<float *>(smem + (SAMPLE ? (size_t)R * a * 8 : 0));  // [R][a]
+    const int t = threadIdx.x;
+    const int64_t b0 = (int64_t)blockIdx.x * R;
+    const int rows = B - b0 < R ? (int)(B - b0) : R;
+    const int n = rows * a;
+    for (int e = t; e < n; e += kSelectThreads) zs[e] = logits[b0 * a + e];
+    __syncthreads();
+    if constexpr (SAMPLE) {
+        const int groups = (a + 3) / 4;
+        for (int q = t; q < rows * groups; q += kSelectThreads) {
+            const int r = q / groups, g = q - r * groups;
+            const uint4 w = philox4x32_10(make_uint4((uint32_t)g, (uint32_t)(b0 + r), (uint32_t)counter,
+                                                     (uint32_t)(counter >> 32)),
+                                          (uint32_t)seed, (uint32_t)(seed >> 32));
+            const uint32_t word[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int i = 4 * g + j;
+                if (i < a) {
+                    const double u = ((double)(word[j] >> 8) + 0.5) * (1.0 / 16777216.0);
+                    keys[r * a + i] = (double)zs[r * a + i] - log(-log(u));
+                }
+            }
         }
-        if (key > best) {
-            best = key;
-            pick = i;
-        }
+        __syncthreads();
     }
-    float sum = 0.f;
-    for (int i = lo; i < hi; ++i) sum += expf(z[i] - m);
-    if (probs)
-        for (int i = lo; i < hi; ++i) probs[b * a + i] = expf(z[i] - m) / sum;
-    action[tid] = pick;
-    if (logp) logp[tid] = (z[pick] - m) - logf(sum);
+    for (int p = t; p < rows * n_seg; p += kSelectThreads) {
+        const int r = p / n_seg, s = p - r * n_seg;
+        const int lo = seg.off[s], hi = seg.off[s + 1];
+        const float *z = zs + r * a;
+        float m = -INFINITY;
+        double best = -INFINITY;
+        int pick = lo;
+        for (int i = lo; i < hi; ++i) {
+            const float v = z[i];
+            m = v > m ? v : m;
+            const double key = SAMPLE ? keys[r * a + i] : (double)v;
+            if (key > best) {
+                best = key;
+                pick = i;
+            }
+        }
+        float sum = 0.f;
+        for (int i = lo; i < hi; ++i) sum += expf(z[i] - m);
+        const int64_t b = b0 + r;
+        action[b * n_seg + s] = pick;
+        if (logp) logp[b * n_seg + s] = (z[pick] - m) - logf(sum);
+        // the segment's softmax replaces its logits in LDS (no other thread reads this segment)
+        if (probs)
+            for (int i = lo; i < hi; ++i) zs[r * a + i] = expf(zs[r * a + i] - m) / sum;
+    }
+    if (probs) {
+        __syncthreads();
+        for (int e = t; e < n; e += kSelectThreads) probs[b0 * a + e] = zs[e];
+    }
 }
 
 }  // namespace
@@ -86,13 +115,24 @@ int policy_select_launch(const float *logits, int32_t B, int32_t a, const int32_
                          hipStream_t stream) {
     Segments seg{};
     for (int s = 0; s <= n_seg; ++s) seg.off[s] = seg_offsets[s];
-    const unsigned grid = (unsigned)ceil_div((int64_t)B * n_seg, kSelectThreads);
-    if (flags & HARL_SELECT_SAMPLE)
-        hipLaunchKernelGGL(k_policy_select<true>, dim3(grid), dim3(kSelectThreads), 0, stream, logits, B, a, seg, n_seg,
-                           seed, counter, action, logp, probs);
+    const bool sample = flags & HARL_SELECT_SAMPLE;
+    // rows per workgroup: at most 64, kSelectLdsFloats logits in all, and few enough that a
+    // batch spreads over about 256 workgroups
+    int64_t R = ceil_div(B, 256);
+    R = R < 1 ? 1 : R > 64 ? 64 : R;
+    if (R * a > kSelectLdsFloats) R = kSelectLdsFloats / a;
+    R = R * n_seg > kSelectThreads ? kSelectThreads / n_seg : R;
+    const size_t lds = (size_t)R * a * (sample ? 12 : 4);
+    const unsigned grid = (unsigned)ceil_div(B, R);
+    const void *kern = sample ? reinterpret_cast<const void *>(k_policy_select<true>)
+                              : reinterpret_cast<const void *>(k_policy_select<false>);
+    if (const int rc = ensure_dynamic_lds(kern, lds)) return rc;
+    if (sample)
+        hipLaunchKernelGGL(k_policy_select<true>, dim3(grid), dim3(kSelectThreads), lds, stream, logits, B, a, (int)R,
+                           seg, n_seg, seed, counter, action, logp, probs);
     else
-        hipLaunchKernelGGL(k_policy_select<false>, dim3(grid), dim3(kSelectThreads), 0, stream, logits, B, a, seg,
-                           n_seg, seed, counter, action, logp, probs);
+        hipLaunchKernelGGL(k_policy_select<false>, dim3(grid), dim3(kSelectThreads), lds, stream, logits, B, a, (int)R,
+                           seg, n_seg, seed, counter, action, logp, probs);
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
 }

@@ -150,6 +150,6 @@ def test_policy_select_argument_errors():
     assert sel(4, 26, [0, 17, 20, 23, 26], flags=2) == harl.HARL_E_INVALID_ARG
     assert sel(4, 26, [0, 17, 20, 23, 26], logits=0x1002) == harl.HARL_E_INVALID_ARG
     assert sel(4, 26, [0, 17, 20, 23, 26], action=None) == harl.HARL_E_INVALID_ARG
-    assert sel(4, 66000, [0, 66000]) == harl.HARL_E_INVALID_ARG
+    assert sel(4, 4097, [0, 4097]) == harl.HARL_E_INVALID_ARG
     assert sel(4, 40, list(range(0, 41, 1))) == harl.HARL_E_INVALID_ARG     # 40 segments > 32
     assert sel(0, 26, [0, 17, 20, 23, 26], logits=None, action=None) == harl.HARL_OK
