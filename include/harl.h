@@ -231,6 +231,53 @@ int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_
                        int32_t *d_action, float *d_logp, float *d_probs, void *stream);
 
 /* ============================================================================================
+ * PPO update of the actor/critic (Algorithm 1: train the actor with the policy gradient of Eq. 3
+ * and the critic with the MSE of the advantage Y; Section 6.1: PPO; Table 8: weights and rates).
+ * ============================================================================================ */
+
+/* Sizes and hyper-parameters of the trained fp32 network (the shared trunk of harl_policy_desc
+ * with the per-type actor head of harl_policy_select and a value head). */
+typedef struct {
+    int32_t s, h1, h2, a;      /* input, hidden and action sizes: 1..1024, 1..4096, 1..4096, 1..4096 */
+    int32_t n_seg;             /* modification types, 1..HARL_SELECT_MAX_SEGMENTS */
+    int32_t seg_offsets[HARL_SELECT_MAX_SEGMENTS + 1];  /* 0 = o_0 < ... < o_n_seg = a */
+    float clip_eps;            /* PPO clip range (0.2) */
+    float w_value, w_entropy;  /* loss weights (0.5, 0.01; Table 8) */
+    float lr_actor, lr_critic; /* Adam rates: trunk + actor head, value head (3e-4, 1e-3; Table 8) */
+    float beta1, beta2, adam_eps;  /* Adam (0.9, 0.999, 1e-8) */
+} harl_ppo_config;
+
+/* Floats of the packed parameters W1 [h1][s], b1, W2 [h2][h1], b2, Wa [a][h2], ba, wv [h2], bv
+ * (PyTorch nn.Linear layout, in that order); also the length of the gradient and Adam moments. */
+size_t harl_ppo_param_count(const harl_ppo_config *cfg);
+/* Bytes of device workspace harl_ppo_update needs for a mini-batch of M transitions. */
+size_t harl_ppo_workspace_size(const harl_ppo_config *cfg, int32_t M);
+
+/*
+ * One PPO update on a mini-batch of M transitions, in fp32 on the device:
+ *   loss = -mean(min(ratio A, clip(ratio, 1 - clip_eps, 1 + clip_eps) A))
+ *          + w_value mean((V(s) - R)^2) - w_entropy mean(H),
+ *   ratio = exp(logp - logp_old), logp = sum over types of the chosen actions' log-softmax,
+ *   H = sum over types of the segment entropies;
+ * then its gradient (backpropagation through the trunk; min passes the gradient to the unclipped
+ * term on equality, clip inside its closed range, ReLU's derivative at 0 is 0) and one Adam step
+ * (bias correction with the 1-based `step`).
+ *   d_params [P] in/out, d_adam_m / d_adam_v [P] in/out (zero before the first step),
+ *   P = harl_ppo_param_count(cfg).
+ *   d_states [M][s] fp32; d_actions [M][n_seg] int32 (row-global indices, each in its segment;
+ *   others are clamped into it); d_logp_old, d_adv, d_ret [M] fp32 (the behaviour policy's
+ *   log-probability, the advantage of Eq. 4 and the critic's target R).
+ *   d_grad   [P] out, or NULL: the gradient of this step.
+ *   d_loss   [4] out, or NULL: total, clipped-surrogate, value-MSE and entropy terms.
+ *   d_ws, ws_bytes: at least harl_ppo_workspace_size(cfg, M) bytes, 256-byte aligned.
+ * All device arrays 4-byte aligned.  M == 0 is a no-op; step >= 1.  Deterministic.
+ */
+int harl_ppo_update(const harl_ppo_config *cfg, float *d_params, float *d_adam_m, float *d_adam_v,
+                    int32_t step, const float *d_states, const int32_t *d_actions,
+                    const float *d_logp_old, const float *d_adv, const float *d_ret, int32_t M,
+                    float *d_grad, float *d_loss, void *d_ws, size_t ws_bytes, void *stream);
+
+/* ============================================================================================
  * Schedule tracks between rounds: reward and advantage of a modification step (Algorithm 1,
  * Eq. 4) and the adaptive-stopping elimination (Section 5).
  * ============================================================================================ */

@@ -93,8 +93,10 @@ def loss(p: dict, batch: dict, segs, clip_eps=0.2, w_v=0.5, w_e=0.01) -> dict:
                 ent=ent, ratio=ratio, logp=logp, s1=s1, s2=s2)
 
 
-def grads(p: dict, batch: dict, segs, clip_eps=0.2, w_v=0.5, w_e=0.01) -> tuple:
-    """Analytic gradient of the PPO objective with respect to every parameter (fp64), and the loss."""
+def grads(p: dict, batch: dict, segs, clip_eps=0.2, w_v=0.5, w_e=0.01, scales: bool = False) -> tuple:
+    """Analytic gradient of the PPO objective with respect to every parameter (fp64), and the loss.
+    With `scales`, L["scale"] holds for every gradient entry the sum of the absolute values of
+    the terms it sums (the basis of a scale-relative tolerance)."""
     L = loss(p, batch, segs, clip_eps, w_v, w_e)
     f = L["fwd"]
     M = f["logits"].shape[0]
@@ -130,7 +132,40 @@ def grads(p: dict, batch: dict, segs, clip_eps=0.2, w_v=0.5, w_e=0.01) -> tuple:
     dz1 = dh1 * (f["z1"] > 0)
     g["w1"] = dz1.T @ X
     g["b1"] = dz1.sum(axis=0)
+    if scales:
+        L["scale"] = _grad_scales(p, X, f, L, g_logp, dlogits, dv, dz2, dz1, segs, w_v, w_e)
     return g, L
+
+
+def _grad_scales(p, X, f, L, g_logp, dlogits, dv, dz2, dz1, segs, w_v, w_e) -> dict:
+    """A running error scale T(q) for every quantity q of the update: q's formula evaluated on the
+    absolute values of its factors and the scales of its inner quantities, carried from the inputs
+    through the forward pass, the objective's gradient at the logits and backpropagation.  An
+    fp32 evaluation of q errs by a small multiple of 2^-24 T(q)."""
+    A = np.abs
+    M = X.shape[0]
+    m1, m2 = (f["z1"] > 0), (f["z2"] > 0)
+    t_h1 = (A(X) @ A(p["w1"]).T + A(p["b1"])) * m1
+    t_h2 = (t_h1 @ A(p["w2"]).T + A(p["b2"])) * m2
+    t_z = t_h2 @ A(p["wa"]).T + A(p["ba"])
+    t_v = (t_h2 @ A(p["wv"]).T)[:, 0] + A(p["bv"][0])
+    probs = np.exp(L["logsm"])
+    t_dl = np.zeros_like(dlogits)
+    for s in range(len(segs) - 1):
+        lo, hi = segs[s], segs[s + 1]
+        ps, ls = probs[:, lo:hi], A(L["logsm"][:, lo:hi])
+        H = L["ent"][:, s:s + 1]
+        own = A(g_logp)[:, None] * (1.0 + ps) + (w_e / M) * ps * (ls + H)
+        # sensitivity to the logits' errors (through the softmax and the ratio of every type)
+        sens = (A(g_logp)[:, None] * (len(segs) - 1) + w_e / M) * (1.0 + ls + H) * t_z.max(axis=1, keepdims=True)
+        t_dl[:, lo:hi] = own + sens
+    t_dv = A(dv) + w_v * 2.0 / M * (t_v + A(f["v"]))
+    t_dz2 = (t_dl @ A(p["wa"]) + t_dv[:, None] * A(p["wv"][0])[None, :]) * m2
+    t_dz1 = (t_dz2 @ A(p["w2"])) * m1
+    return dict(wa=t_dl.T @ A(f["h2"]) + A(dlogits).T @ t_h2, ba=t_dl.sum(axis=0),
+                wv=(t_dv @ A(f["h2"]) + A(dv) @ t_h2)[None, :], bv=np.array([t_dv.sum()]),
+                w2=t_dz2.T @ A(f["h1"]) + A(dz2).T @ t_h1, b2=t_dz2.sum(axis=0),
+                w1=t_dz1.T @ A(X), b1=t_dz1.sum(axis=0))
 
 
 def adam(flat_p, flat_g, m, v, step: int, lr, beta1=0.9, beta2=0.999, eps=1e-8):

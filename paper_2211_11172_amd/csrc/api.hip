@@ -178,6 +178,50 @@ int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_
                                       d_probs, static_cast<hipStream_t>(stream));
 }
 
+static int ppo_check_config(const harl_ppo_config *c) {
+    if (!c) return fail(HARL_E_INVALID_ARG, "harl_ppo: null config");
+    if (c->s < 1 || c->s > 1024 || c->h1 < 1 || c->h1 > 4096 || c->h2 < 1 || c->h2 > 4096 || c->a < 1 || c->a > 4096)
+        return fail(HARL_E_INVALID_ARG, "harl_ppo: sizes out of range");
+    if (c->n_seg < 1 || c->n_seg > HARL_SELECT_MAX_SEGMENTS || c->seg_offsets[0] != 0 || c->seg_offsets[c->n_seg] != c->a)
+        return fail(HARL_E_INVALID_ARG, "harl_ppo: segments must run from 0 to a");
+    for (int s = 0; s < c->n_seg; ++s)
+        if (c->seg_offsets[s + 1] <= c->seg_offsets[s]) return fail(HARL_E_INVALID_ARG, "harl_ppo: segment offsets must increase");
+    if (!(c->clip_eps >= 0.f && c->clip_eps < 1.f) || !(c->beta1 >= 0.f && c->beta1 < 1.f) ||
+        !(c->beta2 >= 0.f && c->beta2 < 1.f) || !(c->adam_eps > 0.f) || !(c->lr_actor >= 0.f) || !(c->lr_critic >= 0.f) ||
+        !(c->w_value >= 0.f) || !(c->w_entropy >= 0.f))
+        return fail(HARL_E_INVALID_ARG, "harl_ppo: hyper-parameter out of range");
+    return HARL_OK;
+}
+
+size_t harl_ppo_param_count(const harl_ppo_config *cfg) {
+    if (ppo_check_config(cfg) != HARL_OK) return 0;
+    return harl::ppo_param_count(cfg);
+}
+
+size_t harl_ppo_workspace_size(const harl_ppo_config *cfg, int32_t M) {
+    if (ppo_check_config(cfg) != HARL_OK || M < 0) return 0;
+    return harl::ppo_ws_bytes(cfg, M);
+}
+
+int harl_ppo_update(const harl_ppo_config *cfg, float *d_params, float *d_adam_m, float *d_adam_v, int32_t step,
+                    const float *d_states, const int32_t *d_actions, const float *d_logp_old, const float *d_adv,
+                    const float *d_ret, int32_t M, float *d_grad, float *d_loss, void *d_ws, size_t ws_bytes,
+                    void *stream) {
+    if (const int rc = ppo_check_config(cfg)) return rc;
+    if (M < 0 || step < 1) return fail(HARL_E_INVALID_ARG, "harl_ppo_update: need M >= 0 and step >= 1");
+    if (M == 0) return HARL_OK;
+    const void *in[] = {d_params, d_adam_m, d_adam_v, d_states, d_actions, d_logp_old, d_adv, d_ret};
+    for (const void *p : in)
+        if (!p || !aligned(p, 4)) return fail(HARL_E_INVALID_ARG, "harl_ppo_update: null or misaligned array");
+    if ((d_grad && !aligned(d_grad, 4)) || (d_loss && !aligned(d_loss, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_ppo_update: misaligned output");
+    if (!d_ws || !aligned(d_ws, 256)) return fail(HARL_E_INVALID_ARG, "harl_ppo_update: workspace null or not 256-byte aligned");
+    if (ws_bytes < harl::ppo_ws_bytes(cfg, M))
+        return fail(HARL_E_WORKSPACE, "harl_ppo_update: workspace smaller than harl_ppo_workspace_size()");
+    return harl::ppo_update_launch(cfg, d_params, d_adam_m, d_adam_v, step, d_states, d_actions, d_logp_old, d_adv, d_ret,
+                                   M, d_grad, d_loss, d_ws, static_cast<hipStream_t>(stream));
+}
+
 int harl_track_advantage(const float *d_c_prev, const float *d_c_next, const float *d_v_prev, const float *d_v_next,
                          int32_t n, float gamma, float eps, float *d_reward, float *d_adv, void *stream) {
     if (n < 0) return fail(HARL_E_INVALID_ARG, "harl_track_advantage: negative size");

@@ -93,6 +93,11 @@ int topk_reset_launch(float *io_score, int64_t *io_index, int32_t k, hipStream_t
 int track_advantage_launch(const float *c_prev, const float *c_next, const float *v_prev, const float *v_next, int32_t n,
                            float gamma, float eps, float *reward, float *adv, hipStream_t stream);
 size_t track_eliminate_ws_bytes(int32_t n);
+size_t ppo_param_count(const harl_ppo_config *c);
+size_t ppo_ws_bytes(const harl_ppo_config *c, int32_t M);
+int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, float *adam_v, int32_t step,
+                      const float *X, const int32_t *actions, const float *logp_old, const float *adv, const float *ret,
+                      int32_t M, float *grad_out, float *loss_out, void *ws, hipStream_t stream);
 int policy_select_launch(const float *logits, int32_t B, int32_t a, const int32_t *seg_offsets, int32_t n_seg,
                          uint32_t flags, uint64_t seed, uint64_t counter, int32_t *action, float *logp, float *probs,
                          hipStream_t stream);

@@ -1,0 +1,449 @@
+// One PPO update of the actor/critic (HARL paper, Algorithm 1: sample a mini-batch from the replay
+// buffer, train the actor with the policy gradient of Eq. 3 and the critic with the MSE of the
+// advantage Y of Eq. 4; Section 6.1: PPO; Table 8: value weight 0.5, entropy weight 0.01, learning
+// rates 3e-4 / 1e-3).
+//
+// The network is the shared trunk of the policy kernels in fp32 (W1, W2 with ReLU) with the
+// per-type actor head of harl_policy_select and a value head.  One update:
+//   forward    h1 = relu(X W1^T + b1), h2 = relu(h1 W2^T + b2), logits = h2 Wa^T + ba,
+//              v = h2 wv^T + bv                                       (k_gemm, fused epilogues)
+//   objective  per row (k_ppo_heads): per-type log-softmax and entropy, logp = sum over types of
+//              the chosen actions' log-probabilities, ratio = exp(logp - logp_old), the clipped
+//              surrogate -min(ratio A, clip(ratio, 1 - eps, 1 + eps) A), w_v (v - R)^2 and the
+//              entropy bonus -w_e H, each averaged over the batch; their gradients with respect to
+//              the logits and v (min passes the gradient to the unclipped term on equality, clip
+//              inside its closed range)
+//   backward   dWa = dlogits^T h2, dwv = dv^T h2, dz2 = (dlogits Wa + dv wv) * [h2 > 0],
+//              dW2 = dz2^T h1, dz1 = (dz2 W2) * [h1 > 0], dW1 = dz1^T X, the bias gradients as
+//              column sums -- weight gradients reduce over the batch in fixed-order split-K
+//   Adam       bias-corrected, the actor's rate for the trunk and actor head, the critic's for the
+//              value head (k_adam)
+// k_gemm: C[i][j] = sum_p A(i, p) B(p, j) with A(i, p) = A[i a_si + p a_sp], B(p, j) = B[p b_sp +
+// j b_sj] (any transpose), fp32 on v_mfma_f32_16x16x4f32: a workgroup of 4 waves owns a 64 x 64
+// tile of C (a wave 32 x 32, 2 x 2 MFMA tiles), K is staged through LDS 16 at a time.  No result
+// depends on scheduling.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "internal.hpp"
+
+namespace harl {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGemmThreads = 256, kTile = 64, kTileK = 16;
+constexpr int kMaxSplits = 16;
+constexpr int kRowThreads = 256;
+
+enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kRank1Mask = 3 };
+
+struct GemmArgs {
+    const float *A;  // null: A(i, p) = 1 (column sums)
+    int64_t a_si, a_sp;
+    const float *B;
+    int64_t b_sp, b_sj;
+    float *C;  // C[i ldc + j], or partial sums [split][I][J] when split
+    int64_t ldc;
+    int I, J, P, p_per_split, split;
+    int epi;
+    const float *bias;            // bias[j]
+    const float *u, *w;           // rank-1 term u[i] w[j]
+    const float *mask;            // multiply by [mask[i ldm + j] > 0]
+    int64_t ldm;
+};
+
+__global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
+    __shared__ float As[kTile][kTileK + 1];
+    __shared__ float Bs[kTileK][kTile + 1];
+    const int t = threadIdx.x, wv = t / 64, l = t % 64;
+    const int i0 = blockIdx.y * kTile, j0 = blockIdx.x * kTile;
+    const int p_begin = blockIdx.z * g.p_per_split;
+    const int p_end = g.P - p_begin < g.p_per_split ? g.P : p_begin + g.p_per_split;
+    const int wi = (wv / 2) * 32, wj = (wv % 2) * 32;
+    const bool a_i_fast = g.a_si == 1, b_p_fast = g.b_sp == 1;
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int p0 = p_begin; p0 < p_end; p0 += kTileK) {
+        // 64 x 16 of A and 16 x 64 of B, 4 elements per thread each; the faster-moving index of
+        // the tile follows the operand's contiguous direction
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = t + kGemmThreads * q;
+            const int ii = a_i_fast ? e % kTile : e / kTileK, pp = a_i_fast ? e / kTile : e % kTileK;
+            const int gi = i0 + ii, gp = p0 + pp;
+            float v = 0.f;
+            if (gi < g.I && gp < p_end) v = g.A ? g.A[(int64_t)gi * g.a_si + (int64_t)gp * g.a_sp] : 1.f;
+            As[ii][pp] = v;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = t + kGemmThreads * q;
+            const int pp = b_p_fast ? e % kTileK : e / kTile, jj = b_p_fast ? e / kTileK : e % kTile;
+            const int gp = p0 + pp, gj = j0 + jj;
+            Bs[pp][jj] = (gp < p_end && gj < g.J) ? g.B[(int64_t)gp * g.b_sp + (int64_t)gj * g.b_sj] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < kTileK; kk += 4) {
+            float a[2], b[2];
+#pragma unroll
+            for (int x = 0; x < 2; ++x) a[x] = As[wi + 16 * x + l % 16][kk + l / 16];
+#pragma unroll
+            for (int y = 0; y < 2; ++y) b[y] = Bs[kk + l / 16][wj + 16 * y + l % 16];
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[x], b[y], acc[x][y], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+    // accumulator register r of tile (x, y) is C[wi + 16x + 4(l/16) + r][wj + 16y + l%16]
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = i0 + wi + 16 * x + 4 * (l / 16) + r, j = j0 + wj + 16 * y + l % 16;
+                if (i >= g.I || j >= g.J) continue;
+                float v = acc[x][y][r];
+                if (g.split) {
+                    g.C[((int64_t)blockIdx.z * g.I + i) * g.J + j] = v;
+                    continue;
+                }
+                if (g.epi == kBias || g.epi == kBiasRelu) v += g.bias[j];
+                if (g.epi == kBiasRelu) v = fmaxf(v, 0.f);
+                if (g.epi == kRank1Mask) {
+                    if (g.u) v += g.u[i] * g.w[j];
+                    v = g.mask[(int64_t)i * g.ldm + j] > 0.f ? v : 0.f;
+                }
+                g.C[(int64_t)i * g.ldc + j] = v;
+            }
+}
+
+// out[i] = sum over splits (in order) of partial[s][i], i < n
+__global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ partial, int splits, int64_t n,
+                                                   float *__restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    float s = 0.f;
+    for (int k = 0; k < splits; ++k) s += partial[(int64_t)k * n + i];
+    out[i] = s;
+}
+
+struct HeadArgs {
+    const float *logits, *v, *logp_old, *adv, *ret;
+    const int32_t *actions;
+    int M, a, n_seg;
+    int32_t off[HARL_SELECT_MAX_SEGMENTS + 1];
+    float clip_eps, w_v, w_e;
+    float *dlogits, *dv, *rows;  // rows: [M][3] (min(s1, s2), (v - R)^2, entropy)
+};
+
+// Log-sum-exp and entropy of segment [lo, hi) of a logits row.
+__device__ __forceinline__ void segment_stats(const float *z, int lo, int hi, float &lse, float &H) {
+    float mx = -INFINITY;
+    for (int i = lo; i < hi; ++i) mx = fmaxf(mx, z[i]);
+    float sum = 0.f;
+    for (int i = lo; i < hi; ++i) sum += expf(z[i] - mx);
+    lse = mx + logf(sum);
+    H = 0.f;
+    for (int i = lo; i < hi; ++i) {
+        const float ls = z[i] - lse;
+        H -= expf(ls) * ls;
+    }
+}
+
+// One row per thread: the clipped surrogate, value and entropy terms and their gradients.  An
+// action outside its segment (a broken device precondition) is clamped into it.
+__global__ __launch_bounds__(kRowThreads) void k_ppo_heads(HeadArgs h) {
+    const int m = blockIdx.x * kRowThreads + threadIdx.x;
+    if (m >= h.M) return;
+    const float *z = h.logits + (int64_t)m * h.a;
+    float *dz = h.dlogits + (int64_t)m * h.a;
+    const int32_t *acts = h.actions + (int64_t)m * h.n_seg;
+    float logp = 0.f, ent = 0.f;
+    for (int s = 0; s < h.n_seg; ++s) {
+        const int lo = h.off[s], hi = h.off[s + 1];
+        float lse, H;
+        segment_stats(z, lo, hi, lse, H);
+        ent += H;
+        logp += z[min(max(acts[s], lo), hi - 1)] - lse;
+    }
+    const float ratio = expf(logp - h.logp_old[m]);
+    const float adv = h.adv[m];
+    const float s1 = ratio * adv;
+    const float rc = fminf(fmaxf(ratio, 1.f - h.clip_eps), 1.f + h.clip_eps);
+    const float s2 = rc * adv;
+    const bool inside = ratio >= 1.f - h.clip_eps && ratio <= 1.f + h.clip_eps;
+    const float active = s1 <= s2 ? 1.f : (inside ? 1.f : 0.f);
+    const float inv_m = 1.f / (float)h.M;
+    const float g_logp = -(adv * ratio * active) * inv_m;
+    const float we = h.w_e * inv_m;
+    for (int s = 0; s < h.n_seg; ++s) {
+        const int lo = h.off[s], hi = h.off[s + 1];
+        const int act = min(max(acts[s], lo), hi - 1);
+        float lse, H;
+        segment_stats(z, lo, hi, lse, H);
+        for (int i = lo; i < hi; ++i) {
+            const float ls = z[i] - lse;
+            const float p = expf(ls);
+            // g_logp (onehot - p) - (w_e / M) dH/dz, with dH/dz = -p (log p + H)
+            dz[i] = g_logp * ((i == act ? 1.f : 0.f) - p) + we * p * (ls + H);
+        }
+    }
+    const float dvv = h.v[m] - h.ret[m];
+    h.dv[m] = h.w_v * 2.f * dvv * inv_m;
+    float *r = h.rows + (int64_t)m * 3;
+    r[0] = fminf(s1, s2);
+    r[1] = dvv * dvv;
+    r[2] = ent;
+}
+
+// loss[0..3] = (total, clip, value, entropy): fixed-order means of the row terms, one workgroup.
+__global__ __launch_bounds__(256) void k_ppo_loss(const float *__restrict__ rows, int M, float w_v, float w_e,
+                                                  float *__restrict__ loss) {
+    __shared__ double part[3][256];
+    const int t = threadIdx.x;
+    double s[3] = {0.0, 0.0, 0.0};
+    for (int m = t; m < M; m += 256)
+#pragma unroll
+        for (int c = 0; c < 3; ++c) s[c] += (double)rows[(int64_t)m * 3 + c];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) part[c][t] = s[c];
+    __syncthreads();
+    if (t == 0) {
+        double tot[3] = {0.0, 0.0, 0.0};
+        for (int k = 0; k < 256; ++k)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) tot[c] += part[c][k];
+        const double clip = -tot[0] / M, value = tot[1] / M, ent = tot[2] / M;
+        loss[0] = (float)(clip + (double)w_v * value - (double)w_e * ent);
+        loss[1] = (float)clip;
+        loss[2] = (float)value;
+        loss[3] = (float)ent;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_adam(float *__restrict__ p, float *__restrict__ m, float *__restrict__ v,
+                                              const float *__restrict__ g, int64_t n, int64_t n_actor, float lr_a,
+                                              float lr_c, float b1, float b2, float bc1, float bc2, float eps) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const float gi = g[i];
+    const float mi = b1 * m[i] + (1.f - b1) * gi;
+    const float vi = b2 * v[i] + (1.f - b2) * gi * gi;
+    m[i] = mi;
+    v[i] = vi;
+    const float lr = i < n_actor ? lr_a : lr_c;
+    p[i] -= lr * (mi / bc1) / (sqrtf(vi / bc2) + eps);
+}
+
+struct Layout {
+    int64_t w1, b1, w2, b2, wa, ba, wv, bv, n, n_actor;
+};
+
+Layout param_layout(const harl_ppo_config *c) {
+    Layout L{};
+    L.w1 = 0;
+    L.b1 = L.w1 + (int64_t)c->h1 * c->s;
+    L.w2 = L.b1 + c->h1;
+    L.b2 = L.w2 + (int64_t)c->h2 * c->h1;
+    L.wa = L.b2 + c->h2;
+    L.ba = L.wa + (int64_t)c->a * c->h2;
+    L.wv = L.ba + c->a;
+    L.bv = L.wv + c->h2;
+    L.n = L.bv + 1;
+    L.n_actor = L.wv;
+    return L;
+}
+
+int splits_for(int P) {
+    int s = (int)ceil_div(P, 256);
+    return s < 1 ? 1 : s > kMaxSplits ? kMaxSplits : s;
+}
+
+struct Ws {
+    float *h1, *h2, *logits, *v, *dlogits, *dv, *dz2, *dz1, *rows, *grad, *partial;
+    size_t bytes;
+};
+
+Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
+    const Layout L = param_layout(c);
+    const int64_t Mp = M > 0 ? M : 1;
+    int64_t off = 0;
+    auto take = [&](int64_t floats) {
+        float *p = base ? reinterpret_cast<float *>(base + off) : nullptr;
+        off += round_up(floats * 4, 256);
+        return p;
+    };
+    Ws w{};
+    w.h1 = take(Mp * c->h1);
+    w.h2 = take(Mp * c->h2);
+    w.logits = take(Mp * c->a);
+    w.v = take(Mp);
+    w.dlogits = take(Mp * c->a);
+    w.dv = take(Mp);
+    w.dz2 = take(Mp * c->h2);
+    w.dz1 = take(Mp * c->h1);
+    w.rows = take(Mp * 3);
+    w.grad = take(L.n);
+    const int64_t big = std::max<int64_t>(std::max<int64_t>((int64_t)c->h1 * c->s, (int64_t)c->h2 * c->h1),
+                                          std::max<int64_t>((int64_t)c->a * c->h2, std::max(c->h1, c->h2)));
+    w.partial = take((int64_t)kMaxSplits * big);
+    w.bytes = (size_t)off;
+    return w;
+}
+
+int gemm(const GemmArgs &g0, float *partial, hipStream_t stream) {
+    GemmArgs g = g0;
+    const unsigned gx = (unsigned)ceil_div(g.J, kTile), gy = (unsigned)ceil_div(g.I, kTile);
+    if (g.split) {
+        const int splits = splits_for(g.P);
+        g.p_per_split = (int)round_up(ceil_div(g.P, splits), kTileK);
+        const int used = (int)ceil_div(g.P, g.p_per_split);
+        float *out = g.C;
+        g.C = partial;
+        hipLaunchKernelGGL(k_gemm, dim3(gx, gy, used), dim3(kGemmThreads), 0, stream, g);
+        HARL_HIP_CHECK(hipGetLastError());
+        const int64_t n = (int64_t)g.I * g.J;  // out is contiguous [I][J]
+        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, stream, partial, used, n, out);
+    } else {
+        g.p_per_split = (int)round_up(g.P, kTileK);
+        hipLaunchKernelGGL(k_gemm, dim3(gx, gy, 1), dim3(kGemmThreads), 0, stream, g);
+    }
+    HARL_HIP_CHECK(hipGetLastError());
+    return HARL_OK;
+}
+
+GemmArgs ga(const float *A, int64_t a_si, int64_t a_sp, const float *B, int64_t b_sp, int64_t b_sj, float *C,
+            int64_t ldc, int I, int J, int P) {
+    GemmArgs g{};
+    g.A = A;
+    g.a_si = a_si;
+    g.a_sp = a_sp;
+    g.B = B;
+    g.b_sp = b_sp;
+    g.b_sj = b_sj;
+    g.C = C;
+    g.ldc = ldc;
+    g.I = I;
+    g.J = J;
+    g.P = P;
+    return g;
+}
+
+}  // namespace
+
+size_t ppo_param_count(const harl_ppo_config *c) { return (size_t)param_layout(c).n; }
+
+size_t ppo_ws_bytes(const harl_ppo_config *c, int32_t M) { return ws_layout(c, M, nullptr).bytes; }
+
+int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, float *adam_v, int32_t step,
+                      const float *X, const int32_t *actions, const float *logp_old, const float *adv, const float *ret,
+                      int32_t M, float *grad_out, float *loss_out, void *ws, hipStream_t stream) {
+    const Layout L = param_layout(c);
+    const Ws w = ws_layout(c, M, static_cast<char *>(ws));
+    float *grad = grad_out ? grad_out : w.grad;
+    const int s = c->s, h1 = c->h1, h2 = c->h2, a = c->a;
+    const float *W1 = params + L.w1, *W2 = params + L.w2, *Wa = params + L.wa, *wv = params + L.wv;
+    int rc;
+    // ---- forward ----
+    GemmArgs g = ga(X, s, 1, W1, 1, s, w.h1, h1, M, h1, s);
+    g.epi = kBiasRelu;
+    g.bias = params + L.b1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(w.h1, h1, 1, W2, 1, h1, w.h2, h2, M, h2, h1);
+    g.epi = kBiasRelu;
+    g.bias = params + L.b2;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(w.h2, h2, 1, Wa, 1, h2, w.logits, a, M, a, h2);
+    g.epi = kBias;
+    g.bias = params + L.ba;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(w.h2, h2, 1, wv, 1, 0, w.v, 1, M, 1, h2);
+    g.epi = kBias;
+    g.bias = params + L.bv;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    // ---- objective and its gradient at the logits and the value ----
+    HeadArgs h{};
+    h.logits = w.logits;
+    h.v = w.v;
+    h.logp_old = logp_old;
+    h.adv = adv;
+    h.ret = ret;
+    h.actions = actions;
+    h.M = M;
+    h.a = a;
+    h.n_seg = c->n_seg;
+    for (int k = 0; k <= c->n_seg; ++k) h.off[k] = c->seg_offsets[k];
+    h.clip_eps = c->clip_eps;
+    h.w_v = c->w_value;
+    h.w_e = c->w_entropy;
+    h.dlogits = w.dlogits;
+    h.dv = w.dv;
+    h.rows = w.rows;
+    hipLaunchKernelGGL(k_ppo_heads, dim3((unsigned)ceil_div(M, kRowThreads)), dim3(kRowThreads), 0, stream, h);
+    HARL_HIP_CHECK(hipGetLastError());
+    if (loss_out) {
+        hipLaunchKernelGGL(k_ppo_loss, dim3(1), dim3(256), 0, stream, w.rows, M, c->w_value, c->w_entropy, loss_out);
+        HARL_HIP_CHECK(hipGetLastError());
+    }
+    // ---- backward: heads ----
+    g = ga(w.dlogits, 1, a, w.h2, h2, 1, grad + L.wa, h2, a, h2, M);  // dWa = dlogits^T h2
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(nullptr, 0, 0, w.dlogits, a, 1, grad + L.ba, a, 1, a, M);  // dba = column sums
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(w.dv, 0, 1, w.h2, h2, 1, grad + L.wv, h2, 1, h2, M);  // dwv = dv^T h2
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(nullptr, 0, 0, w.dv, 1, 0, grad + L.bv, 1, 1, 1, M);  // dbv = sum dv
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    // dz2 = (dlogits Wa + dv wv) * [h2 > 0]
+    g = ga(w.dlogits, a, 1, Wa, h2, 1, w.dz2, h2, M, h2, a);
+    g.epi = kRank1Mask;
+    g.u = w.dv;
+    g.w = wv;
+    g.mask = w.h2;
+    g.ldm = h2;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    // ---- backward: layer 2 ----
+    g = ga(w.dz2, 1, h2, w.h1, h1, 1, grad + L.w2, h1, h2, h1, M);  // dW2 = dz2^T h1
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(nullptr, 0, 0, w.dz2, h2, 1, grad + L.b2, h2, 1, h2, M);
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    // dz1 = (dz2 W2) * [h1 > 0]
+    g = ga(w.dz2, h2, 1, W2, h1, 1, w.dz1, h1, M, h1, h2);
+    g.epi = kRank1Mask;
+    g.u = nullptr;
+    g.mask = w.h1;
+    g.ldm = h1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    // ---- backward: layer 1 ----
+    g = ga(w.dz1, 1, h1, X, s, 1, grad + L.w1, s, h1, s, M);  // dW1 = dz1^T X
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    g = ga(nullptr, 0, 0, w.dz1, h1, 1, grad + L.b1, h1, 1, h1, M);
+    g.split = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
+    // ---- Adam ----
+    const double bc1 = 1.0 - std::pow((double)c->beta1, step), bc2 = 1.0 - std::pow((double)c->beta2, step);
+    hipLaunchKernelGGL(k_adam, dim3((unsigned)ceil_div(L.n, 256)), dim3(256), 0, stream, params, adam_m, adam_v, grad,
+                       L.n, L.n_actor, c->lr_actor, c->lr_critic, c->beta1, c->beta2, (float)bc1, (float)bc2,
+                       c->adam_eps);
+    HARL_HIP_CHECK(hipGetLastError());
+    return HARL_OK;
+}
+
+}  // namespace harl

@@ -31,8 +31,28 @@ EXPORTS = (
     "harl_policy_create", "harl_policy_destroy", "harl_policy_step",
     "harl_topk_workspace_size", "harl_topk", "harl_topk_reset",
     "harl_policy_select",
+    "harl_ppo_param_count", "harl_ppo_workspace_size", "harl_ppo_update",
     "harl_track_advantage", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
 )
+
+
+class PpoConfig(ctypes.Structure):
+    _fields_ = [("s", ctypes.c_int32), ("h1", ctypes.c_int32), ("h2", ctypes.c_int32), ("a", ctypes.c_int32),
+                ("n_seg", ctypes.c_int32), ("seg_offsets", ctypes.c_int32 * (HARL_SELECT_MAX_SEGMENTS + 1)),
+                ("clip_eps", ctypes.c_float), ("w_value", ctypes.c_float), ("w_entropy", ctypes.c_float),
+                ("lr_actor", ctypes.c_float), ("lr_critic", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("adam_eps", ctypes.c_float)]
+
+
+def ppo_config(s: int, h1: int, h2: int, a: int, segs, clip_eps=0.2, w_value=0.5, w_entropy=0.01, lr_actor=3e-4,
+               lr_critic=1e-3, beta1=0.9, beta2=0.999, adam_eps=1e-8) -> PpoConfig:
+    c = PpoConfig()
+    c.s, c.h1, c.h2, c.a, c.n_seg = s, h1, h2, a, len(segs) - 1
+    for i, o in enumerate(segs):
+        c.seg_offsets[i] = int(o)
+    c.clip_eps, c.w_value, c.w_entropy = clip_eps, w_value, w_entropy
+    c.lr_actor, c.lr_critic, c.beta1, c.beta2, c.adam_eps = lr_actor, lr_critic, beta1, beta2, adam_eps
+    return c
 
 
 class HarlError(RuntimeError):
@@ -84,6 +104,9 @@ def load():
                 "harl_topk_workspace_size": ([i32, i32], sz),
                 "harl_topk": ([P, i32, i32, i64, P, P, u32, P, sz, P], ctypes.c_int),
                 "harl_topk_reset": ([P, P, i32, P], ctypes.c_int),
+                "harl_ppo_param_count": ([P], sz),
+                "harl_ppo_workspace_size": ([P, i32], sz),
+                "harl_ppo_update": ([P, P, P, P, i32, P, P, P, P, P, i32, P, P, P, sz, P], ctypes.c_int),
                 "harl_policy_select": ([P, i32, i32, P, i32, u32, ctypes.c_uint64, ctypes.c_uint64, P, P, P, P],
                                        ctypes.c_int),
                 "harl_track_advantage": ([P, P, P, P, i32, ctypes.c_float, ctypes.c_float, P, P, P], ctypes.c_int),
@@ -239,6 +262,21 @@ def harl_policy_select(logits, B: int, a: int, seg_offsets, flags: int, seed: in
     off = np.ascontiguousarray(seg_offsets, np.int32)
     _check(load().harl_policy_select(_ptr(logits), B, a, off.ctypes.data, off.size - 1, flags, seed, counter,
                                      _ptr(action), _ptr(logp), _ptr(probs), _stream(stream)), "harl_policy_select")
+
+
+def harl_ppo_param_count(cfg: PpoConfig) -> int:
+    return int(load().harl_ppo_param_count(ctypes.byref(cfg)))
+
+
+def harl_ppo_workspace_size(cfg: PpoConfig, M: int) -> int:
+    return int(load().harl_ppo_workspace_size(ctypes.byref(cfg), M))
+
+
+def harl_ppo_update(cfg: PpoConfig, params, adam_m, adam_v, step: int, states, actions, logp_old, adv, ret, M: int,
+                    grad=None, loss=None, ws=None, ws_bytes: int = 0, stream=None):
+    _check(load().harl_ppo_update(ctypes.byref(cfg), _ptr(params), _ptr(adam_m), _ptr(adam_v), step, _ptr(states),
+                                  _ptr(actions), _ptr(logp_old), _ptr(adv), _ptr(ret), M, _ptr(grad), _ptr(loss),
+                                  _ptr(ws), ws_bytes, _stream(stream)), "harl_ppo_update")
 
 
 # ------------------------------------------------------------------------------------------------

@@ -153,3 +153,23 @@ def test_policy_select_argument_errors():
     assert sel(4, 4097, [0, 4097]) == harl.HARL_E_INVALID_ARG
     assert sel(4, 40, list(range(0, 41, 1))) == harl.HARL_E_INVALID_ARG     # 40 segments > 32
     assert sel(0, 26, [0, 17, 20, 23, 26], logits=None, action=None) == harl.HARL_OK
+
+
+def test_ppo_argument_errors():
+    cfg = harl.ppo_config(64, 256, 256, 26, [0, 17, 20, 23, 26])
+    n = harl.harl_ppo_param_count(cfg)
+    assert n == 256 * 64 + 256 + 256 * 256 + 256 + 26 * 256 + 26 + 256 + 1
+    assert harl.harl_ppo_workspace_size(cfg, 4096) > 4096 * (256 * 4 + 26 * 2) * 4
+    bad = harl.ppo_config(64, 256, 256, 26, [0, 17, 20, 23, 27])
+    assert harl.harl_ppo_param_count(bad) == 0
+    up = lambda c, step=1, M=4, ws=0x5000, wsb=1 << 30, params=0x1000: _status(
+        "harl_ppo_update", ctypes.byref(c), params, 0x2000, 0x3000, step, 0x4000, 0x4000, 0x4000, 0x4000, 0x4000, M,
+        None, None, ws, wsb, None)
+    assert up(bad) == harl.HARL_E_INVALID_ARG
+    assert up(cfg, step=0) == harl.HARL_E_INVALID_ARG
+    assert up(cfg, M=0) == harl.HARL_OK
+    assert up(cfg, params=None) == harl.HARL_E_INVALID_ARG
+    assert up(cfg, ws=0x5001) == harl.HARL_E_INVALID_ARG
+    assert up(cfg, wsb=64) == harl.HARL_E_WORKSPACE
+    lr = harl.ppo_config(64, 256, 256, 26, [0, 26], beta1=1.0)
+    assert up(lr) == harl.HARL_E_INVALID_ARG
