@@ -77,6 +77,9 @@ def parse():
                     help="per-modification-type action selection: harl_policy_step of the standard round's fp32 "
                          "policy with a 26-action head (17 + 3 + 3 + 3) and harl_policy_select on its logits, greedy "
                          "and sampled, at 4,096 and 65,536 states; prints one JSON line and exits")
+    ap.add_argument("--ppo", action="store_true",
+                    help="one PPO update (harl_ppo_update) of the standard round's fp32 network with a 26-action "
+                         "per-type head on 4,096 and 65,536 transitions; prints one JSON line and exits")
     ap.add_argument("--two-streams", action="store_true",
                     help="run the policy on a second stream after scoring, beside top-K (default: the "
                          "three calls in turn on one stream, which measured faster on the standard round)")
@@ -323,6 +326,85 @@ def select_bench(args):
                       "segments": segs, "steps": args.steps, "results": results}), flush=True)
 
 
+def ppo_bench(args):
+    """Time one PPO update: forward with saved activations, clipped objective, backward, Adam."""
+    import numpy as np
+    import torch
+
+    from oracle import ppo as oppo
+    from paper_2211_11172_amd import harl
+    from synth import gen_policy, gen_states, get_config
+
+    dev = torch.device("cuda:0")
+    main_stream = torch.cuda.current_stream(dev)
+    segs = [0, 17, 20, 23, 26]
+    s_, h1, h2, a = 64, 256, 256, 26
+    results = []
+    for M in (4096, 65536):
+        cfg = get_config("standard").with_(pol_a=a, n_prog=M)
+        pol = gen_policy(cfg)
+        flat = oppo.pack(dict(w1=pol["w1"], b1=pol["b1"], w2=pol["w2"], b2=pol["b2"], wa=pol["wa"], ba=pol["ba"],
+                              wv=np.asarray(pol["wv"]).reshape(1, h2), bv=np.asarray(pol["bv"]).reshape(1)))
+        rng = np.random.default_rng(0)
+        X = gen_states(cfg)
+        acts = np.stack([rng.integers(segs[i], segs[i + 1], M) for i in range(4)], axis=1).astype(np.int32)
+        c = harl.ppo_config(s_, h1, h2, a, segs)
+        n = harl.harl_ppo_param_count(c)
+        d = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+        P, Mm, Vv = d(flat.astype(np.float32)), torch.zeros(n, device=dev), torch.zeros(n, device=dev)
+        st, ac = d(X), d(acts)
+        lpo = d((rng.standard_normal(M) * 0.1 - 7.0).astype(np.float32))
+        adv, ret = d(rng.standard_normal(M).astype(np.float32)), d(rng.standard_normal(M).astype(np.float32))
+        wsb = harl.harl_ppo_workspace_size(c, M)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        loss = torch.empty(4, device=dev)
+        fn = lambda: harl.harl_ppo_update(c, P, Mm, Vv, 1, st, ac, lpo, adv, ret, M, None, loss, ws, wsb)
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(args.steps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main_stream)
+        g.replay()
+        e1.record(main_stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / args.steps * 1e3
+        # algorithmic flops: forward 2M(s h1 + h1 h2 + h2 (a + 1)); backward: the weight gradients
+        # (the same again) and the data gradients of the heads and layer 2
+        fwd = 2 * M * (s_ * h1 + h1 * h2 + h2 * (a + 1))
+        flops = 2 * fwd + 2 * M * (h2 * (a + 1) + h1 * h2)
+        tf = flops / (us * 1e-6) / 1e12
+        entry = {"transitions": M, "us_per_update": us, "gflop": flops / 1e9, "achieved_tflops": tf,
+                 "peak_tflops": PEAK_MFMA_TFLOPS["f32"], "frac": tf / PEAK_MFMA_TFLOPS["f32"]}
+        if not args.no_cpu_baseline:
+            batch = dict(states=X, actions=acts, logp_old=lpo.cpu().numpy(), adv=adv.cpu().numpy(), ret=ret.cpu().numpy())
+            sub = min(M, 4096)
+            bs = {k: v[:sub] for k, v in batch.items()}
+            t0 = time.perf_counter()
+            reps = 0
+            while time.perf_counter() - t0 < 3.0 or reps == 0:
+                oppo.update(flat, np.zeros(n), np.zeros(n), 1, bs, segs, (s_, h1, h2, a))
+                reps += 1
+            el = time.perf_counter() - t0
+            entry["cpu_baseline"] = {"value": sub * reps / el, "unit": "transitions/s", "cores": oracle_threads(),
+                                     "kind": "oracle", "sample": "%d updates of %d transitions in %.1f s" % (reps, sub, el)}
+        entry["transitions_per_s"] = M / (us * 1e-6)
+        print("ppo M=%d: %.1f us per update, %.1f TFLOP/s" % (M, us, tf), file=sys.stderr, flush=True)
+        results.append(entry)
+    print(json.dumps({"metric": "PPO update of the actor/critic (harl_ppo_update)", "unit": "us per update",
+                      "network": "fp32 64-256-256 -> 26 (4 types) + 1", "steps": args.steps, "results": results}),
+          flush=True)
+
+
+def oracle_threads():
+    """Threads numpy's BLAS may use for the fp64 oracle of the PPO update."""
+    return len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -337,6 +419,9 @@ def main():
         return
     if args.select:
         select_bench(args)
+        return
+    if args.ppo:
+        ppo_bench(args)
         return
     import numpy as np
     import torch

@@ -15,13 +15,13 @@
 //              inside its closed range)
 //   backward   dWa = dlogits^T h2, dwv = dv^T h2, dz2 = (dlogits Wa + dv wv) * [h2 > 0],
 //              dW2 = dz2^T h1, dz1 = (dz2 W2) * [h1 > 0], dW1 = dz1^T X, the bias gradients as
-//              column sums -- weight gradients reduce over the batch in fixed-order split-K
+//              column sums (k_colsum) -- all reductions over the batch in fixed-order chunks
 //   Adam       bias-corrected, the actor's rate for the trunk and actor head, the critic's for the
 //              value head (k_adam)
 // k_gemm: C[i][j] = sum_p A(i, p) B(p, j) with A(i, p) = A[i a_si + p a_sp], B(p, j) = B[p b_sp +
 // j b_sj] (any transpose), fp32 on v_mfma_f32_16x16x4f32: a workgroup of 4 waves owns a 64 x 64
-// tile of C (a wave 32 x 32, 2 x 2 MFMA tiles), K is staged through LDS 16 at a time.  No result
-// depends on scheduling.
+// tile of C (a wave 32 x 32, 2 x 2 MFMA tiles), K is staged through LDS 32 at a time while the next
+// 32 are loaded into registers.  No result depends on scheduling.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -34,9 +34,11 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGemmThreads = 256, kTile = 64, kTileK = 16;
-constexpr int kMaxSplits = 16;
-constexpr int kRowThreads = 256;
+constexpr int kGemmThreads = 256, kTile = 64, kTileK = 32;
+constexpr int kPer = kTile * kTileK / kGemmThreads;  // operand elements per thread per K step
+constexpr int kMaxSplits = 32;
+constexpr int kColChunks = 64;  // row chunks of a column sum
+constexpr int kRowThreads = 64;
 
 enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kRank1Mask = 3 };
 
@@ -55,6 +57,26 @@ struct GemmArgs {
     int64_t ldm;
 };
 
+// Operand elements of the K step starting at p0 for this thread: A's 64 x 32 and B's 32 x 64
+// tiles, the tile index moving fastest along the operand's contiguous direction.
+__device__ __forceinline__ void gemm_fetch(const GemmArgs &g, int i0, int j0, int p0, int p_end, float (&ra)[kPer],
+                                           float (&rb)[kPer]) {
+    const int t = threadIdx.x;
+    const bool a_i_fast = g.a_si == 1, b_p_fast = g.b_sp == 1;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int e = t + kGemmThreads * q;
+        const int ii = a_i_fast ? e % kTile : e / kTileK, pp = a_i_fast ? e / kTile : e % kTileK;
+        const int gi = i0 + ii, gp = p0 + pp;
+        float v = 0.f;
+        if (gi < g.I && gp < p_end) v = g.A ? g.A[(int64_t)gi * g.a_si + (int64_t)gp * g.a_sp] : 1.f;
+        ra[q] = v;
+        const int pb = b_p_fast ? e % kTileK : e / kTile, jb = b_p_fast ? e / kTileK : e % kTile;
+        const int gpb = p0 + pb, gj = j0 + jb;
+        rb[q] = (gpb < p_end && gj < g.J) ? g.B[(int64_t)gpb * g.b_sp + (int64_t)gj * g.b_sj] : 0.f;
+    }
+}
+
 __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
     __shared__ float As[kTile][kTileK + 1];
     __shared__ float Bs[kTileK][kTile + 1];
@@ -69,26 +91,20 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
     for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float ra[kPer], rb[kPer];
+    if (p_begin < p_end) gemm_fetch(g, i0, j0, p_begin, p_end, ra, rb);
     for (int p0 = p_begin; p0 < p_end; p0 += kTileK) {
-        // 64 x 16 of A and 16 x 64 of B, 4 elements per thread each; the faster-moving index of
-        // the tile follows the operand's contiguous direction
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < kPer; ++q) {
             const int e = t + kGemmThreads * q;
             const int ii = a_i_fast ? e % kTile : e / kTileK, pp = a_i_fast ? e / kTile : e % kTileK;
-            const int gi = i0 + ii, gp = p0 + pp;
-            float v = 0.f;
-            if (gi < g.I && gp < p_end) v = g.A ? g.A[(int64_t)gi * g.a_si + (int64_t)gp * g.a_sp] : 1.f;
-            As[ii][pp] = v;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = t + kGemmThreads * q;
-            const int pp = b_p_fast ? e % kTileK : e / kTile, jj = b_p_fast ? e / kTileK : e % kTile;
-            const int gp = p0 + pp, gj = j0 + jj;
-            Bs[pp][jj] = (gp < p_end && gj < g.J) ? g.B[(int64_t)gp * g.b_sp + (int64_t)gj * g.b_sj] : 0.f;
+            As[ii][pp] = ra[q];
+            const int pb = b_p_fast ? e % kTileK : e / kTile, jb = b_p_fast ? e / kTileK : e % kTile;
+            Bs[pb][jb] = rb[q];
         }
         __syncthreads();
+        // the next K step's operands are loaded while this one runs on the matrix cores
+        if (p0 + kTileK < p_end) gemm_fetch(g, i0, j0, p0 + kTileK, p_end, ra, rb);
 #pragma unroll
         for (int kk = 0; kk < kTileK; kk += 4) {
             float a[2], b[2];
@@ -133,8 +149,43 @@ __global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ par
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     float s = 0.f;
-    for (int k = 0; k < splits; ++k) s += partial[(int64_t)k * n + i];
+    int k = 0;
+    for (; k + 8 <= splits; k += 8) {  // eight loads in flight, added in split order
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = partial[(int64_t)(k + u) * n + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; k < splits; ++k) s += partial[(int64_t)k * n + i];
     out[i] = s;
+}
+
+// Column sums of Y [rows][J] (row stride ldy), each row weighted by w[row] when w is given:
+// partial[c][j] = sum over chunk c's rows of w Y, 4 row phases per column summed in order.
+__global__ __launch_bounds__(256) void k_colsum(const float *__restrict__ Y, int64_t ldy, int rows, int J,
+                                                const float *__restrict__ w, int rows_per_chunk,
+                                                float *__restrict__ partial) {
+    __shared__ float part[4][64];
+    const int jj = threadIdx.x % 64, q = threadIdx.x / 64;
+    const int j = blockIdx.x * 64 + jj;
+    const int r0 = blockIdx.y * rows_per_chunk;
+    const int r1 = rows - r0 < rows_per_chunk ? rows : r0 + rows_per_chunk;
+    float s = 0.f;
+    if (j < J) {
+        int r = r0 + q;
+        for (; r + 12 < r1; r += 16) {  // four rows of this phase in flight, added in row order
+            float v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = (w ? w[r + 4 * u] : 1.f) * Y[(int64_t)(r + 4 * u) * ldy + j];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) s += v[u];
+        }
+        for (; r < r1; r += 4) s += (w ? w[r] : 1.f) * Y[(int64_t)r * ldy + j];
+    }
+    part[q][jj] = s;
+    __syncthreads();
+    if (q == 0 && j < J) partial[(int64_t)blockIdx.y * J + j] = ((part[0][jj] + part[1][jj]) + part[2][jj]) + part[3][jj];
 }
 
 struct HeadArgs {
@@ -212,7 +263,19 @@ __global__ __launch_bounds__(256) void k_ppo_loss(const float *__restrict__ rows
     __shared__ double part[3][256];
     const int t = threadIdx.x;
     double s[3] = {0.0, 0.0, 0.0};
-    for (int m = t; m < M; m += 256)
+    int m = t;
+    for (; m + 768 < M; m += 1024) {  // four rows of this thread in flight, added in row order
+        float v[4][3];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) v[u][c] = rows[(int64_t)(m + 256 * u) * 3 + c];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) s[c] += (double)v[u][c];
+    }
+    for (; m < M; m += 256)
 #pragma unroll
         for (int c = 0; c < 3; ++c) s[c] += (double)rows[(int64_t)m * 3 + c];
 #pragma unroll
@@ -265,8 +328,22 @@ Layout param_layout(const harl_ppo_config *c) {
 }
 
 int splits_for(int P) {
-    int s = (int)ceil_div(P, 256);
+    int s = (int)ceil_div(P, 128);
     return s < 1 ? 1 : s > kMaxSplits ? kMaxSplits : s;
+}
+
+// out[j] = sum over rows of (w[r]) Y[r][j], fixed order (chunks, then their sums in chunk order)
+int colsum(const float *Y, int64_t ldy, int rows, int J, const float *w, float *partial, float *out,
+           hipStream_t stream) {
+    const int chunks = (int)std::min<int64_t>(kColChunks, ceil_div(rows, 64));
+    const int per = (int)ceil_div(rows, chunks);
+    hipLaunchKernelGGL(k_colsum, dim3((unsigned)ceil_div(J, 64), (unsigned)chunks), dim3(256), 0, stream, Y, ldy, rows,
+                       J, w, per, partial);
+    HARL_HIP_CHECK(hipGetLastError());
+    hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(J, 256)), dim3(256), 0, stream, partial, chunks, (int64_t)J,
+                       out);
+    HARL_HIP_CHECK(hipGetLastError());
+    return HARL_OK;
 }
 
 struct Ws {
@@ -295,8 +372,9 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
     w.rows = take(Mp * 3);
     w.grad = take(L.n);
     const int64_t big = std::max<int64_t>(std::max<int64_t>((int64_t)c->h1 * c->s, (int64_t)c->h2 * c->h1),
-                                          std::max<int64_t>((int64_t)c->a * c->h2, std::max(c->h1, c->h2)));
-    w.partial = take((int64_t)kMaxSplits * big);
+                                          (int64_t)c->a * c->h2);
+    const int64_t cols = std::max<int64_t>(std::max(c->h1, c->h2), c->a);
+    w.partial = take(std::max<int64_t>((int64_t)kMaxSplits * big, (int64_t)kColChunks * cols));
     w.bytes = (size_t)off;
     return w;
 }
@@ -399,15 +477,9 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g = ga(w.dlogits, 1, a, w.h2, h2, 1, grad + L.wa, h2, a, h2, M);  // dWa = dlogits^T h2
     g.split = 1;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(nullptr, 0, 0, w.dlogits, a, 1, grad + L.ba, a, 1, a, M);  // dba = column sums
-    g.split = 1;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(w.dv, 0, 1, w.h2, h2, 1, grad + L.wv, h2, 1, h2, M);  // dwv = dv^T h2
-    g.split = 1;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(nullptr, 0, 0, w.dv, 1, 0, grad + L.bv, 1, 1, 1, M);  // dbv = sum dv
-    g.split = 1;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
+    if ((rc = colsum(w.dlogits, a, M, a, nullptr, w.partial, grad + L.ba, stream))) return rc;  // dba
+    if ((rc = colsum(w.h2, h2, M, h2, w.dv, w.partial, grad + L.wv, stream))) return rc;       // dwv = dv^T h2
+    if ((rc = colsum(w.dv, 1, M, 1, nullptr, w.partial, grad + L.bv, stream))) return rc;      // dbv
     // dz2 = (dlogits Wa + dv wv) * [h2 > 0]
     g = ga(w.dlogits, a, 1, Wa, h2, 1, w.dz2, h2, M, h2, a);
     g.epi = kRank1Mask;
@@ -420,9 +492,7 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g = ga(w.dz2, 1, h2, w.h1, h1, 1, grad + L.w2, h1, h2, h1, M);  // dW2 = dz2^T h1
     g.split = 1;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(nullptr, 0, 0, w.dz2, h2, 1, grad + L.b2, h2, 1, h2, M);
-    g.split = 1;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
+    if ((rc = colsum(w.dz2, h2, M, h2, nullptr, w.partial, grad + L.b2, stream))) return rc;
     // dz1 = (dz2 W2) * [h1 > 0]
     g = ga(w.dz2, h2, 1, W2, h1, 1, w.dz1, h1, M, h1, h2);
     g.epi = kRank1Mask;
@@ -434,9 +504,7 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g = ga(w.dz1, 1, h1, X, s, 1, grad + L.w1, s, h1, s, M);  // dW1 = dz1^T X
     g.split = 1;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(nullptr, 0, 0, w.dz1, h1, 1, grad + L.b1, h1, 1, h1, M);
-    g.split = 1;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
+    if ((rc = colsum(w.dz1, h1, M, h1, nullptr, w.partial, grad + L.b1, stream))) return rc;
     // ---- Adam ----
     const double bc1 = 1.0 - std::pow((double)c->beta1, step), bc2 = 1.0 - std::pow((double)c->beta2, step);
     hipLaunchKernelGGL(k_adam, dim3((unsigned)ceil_div(L.n, 256)), dim3(256), 0, stream, params, adam_m, adam_v, grad,
