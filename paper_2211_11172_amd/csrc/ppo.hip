@@ -20,7 +20,7 @@
 //              value head (k_adam)
 // k_gemm: C[i][j] = sum_p A(i, p) B(p, j) with A(i, p) = A[i a_si + p a_sp], B(p, j) = B[p b_sp +
 // j b_sj] (any transpose), fp32 on v_mfma_f32_16x16x4f32: a workgroup of 4 waves owns a 64 x 64
-// tile of C (a wave 32 x 32, 2 x 2 MFMA tiles), K is staged through LDS 32 at a time while the next
+// tile of C (a wave 32 x 32, 2 x 2 MFMA tiles; 32 x 64 when the grid would be small), K is staged through LDS 32 at a time while the next
 // 32 are loaded into registers.  No result depends on scheduling.
 #include <hip/hip_runtime.h>
 
@@ -38,7 +38,6 @@ constexpr int kGemmThreads = 256, kTile = 64, kTileK = 32;
 constexpr int kPer = kTile * kTileK / kGemmThreads;  // operand elements per thread per K step
 constexpr int kMaxSplits = 32;
 constexpr int kColChunks = 64;  // row chunks of a column sum
-constexpr int kRowThreads = 64;
 
 enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kRank1Mask = 3 };
 
@@ -57,63 +56,77 @@ struct GemmArgs {
     int64_t ldm;
 };
 
-// Operand elements of the K step starting at p0 for this thread: A's 64 x 32 and B's 32 x 64
+// Operand elements of the K step starting at p0 for this thread: A's TI x 32 and B's 32 x 64
 // tiles, the tile index moving fastest along the operand's contiguous direction.
-__device__ __forceinline__ void gemm_fetch(const GemmArgs &g, int i0, int j0, int p0, int p_end, float (&ra)[kPer],
-                                           float (&rb)[kPer]) {
+template <int TI>
+__device__ __forceinline__ void gemm_fetch(const GemmArgs &g, int i0, int j0, int p0, int p_end,
+                                           float (&ra)[TI * kTileK / kGemmThreads], float (&rb)[kPer]) {
+    constexpr int PA = TI * kTileK / kGemmThreads;
     const int t = threadIdx.x;
     const bool a_i_fast = g.a_si == 1, b_p_fast = g.b_sp == 1;
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
+    for (int q = 0; q < PA; ++q) {
         const int e = t + kGemmThreads * q;
-        const int ii = a_i_fast ? e % kTile : e / kTileK, pp = a_i_fast ? e / kTile : e % kTileK;
+        const int ii = a_i_fast ? e % TI : e / kTileK, pp = a_i_fast ? e / TI : e % kTileK;
         const int gi = i0 + ii, gp = p0 + pp;
         float v = 0.f;
         if (gi < g.I && gp < p_end) v = g.A ? g.A[(int64_t)gi * g.a_si + (int64_t)gp * g.a_sp] : 1.f;
         ra[q] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int e = t + kGemmThreads * q;
         const int pb = b_p_fast ? e % kTileK : e / kTile, jb = b_p_fast ? e / kTileK : e % kTile;
         const int gpb = p0 + pb, gj = j0 + jb;
         rb[q] = (gpb < p_end && gj < g.J) ? g.B[(int64_t)gpb * g.b_sp + (int64_t)gj * g.b_sj] : 0.f;
     }
 }
 
+// TI rows (64 or 32) by 64 columns of C per workgroup; wave w owns rows (w / 2) TI / 2 .. and
+// columns (w % 2) 32 ..
+template <int TI>
 __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
-    __shared__ float As[kTile][kTileK + 1];
+    constexpr int XT = TI / 32, PA = TI * kTileK / kGemmThreads;
+    __shared__ float As[TI][kTileK + 1];
     __shared__ float Bs[kTileK][kTile + 1];
     const int t = threadIdx.x, wv = t / 64, l = t % 64;
-    const int i0 = blockIdx.y * kTile, j0 = blockIdx.x * kTile;
+    const int i0 = blockIdx.y * TI, j0 = blockIdx.x * kTile;
     const int p_begin = blockIdx.z * g.p_per_split;
     const int p_end = g.P - p_begin < g.p_per_split ? g.P : p_begin + g.p_per_split;
-    const int wi = (wv / 2) * 32, wj = (wv % 2) * 32;
+    const int wi = (wv / 2) * (16 * XT), wj = (wv % 2) * 32;
     const bool a_i_fast = g.a_si == 1, b_p_fast = g.b_sp == 1;
-    f32x4 acc[2][2];
+    f32x4 acc[XT][2];
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < XT; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float ra[kPer], rb[kPer];
-    if (p_begin < p_end) gemm_fetch(g, i0, j0, p_begin, p_end, ra, rb);
+    float ra[PA], rb[kPer];
+    if (p_begin < p_end) gemm_fetch<TI>(g, i0, j0, p_begin, p_end, ra, rb);
     for (int p0 = p_begin; p0 < p_end; p0 += kTileK) {
+#pragma unroll
+        for (int q = 0; q < PA; ++q) {
+            const int e = t + kGemmThreads * q;
+            const int ii = a_i_fast ? e % TI : e / kTileK, pp = a_i_fast ? e / TI : e % kTileK;
+            As[ii][pp] = ra[q];
+        }
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
             const int e = t + kGemmThreads * q;
-            const int ii = a_i_fast ? e % kTile : e / kTileK, pp = a_i_fast ? e / kTile : e % kTileK;
-            As[ii][pp] = ra[q];
             const int pb = b_p_fast ? e % kTileK : e / kTile, jb = b_p_fast ? e / kTileK : e % kTile;
             Bs[pb][jb] = rb[q];
         }
         __syncthreads();
         // the next K step's operands are loaded while this one runs on the matrix cores
-        if (p0 + kTileK < p_end) gemm_fetch(g, i0, j0, p0 + kTileK, p_end, ra, rb);
+        if (p0 + kTileK < p_end) gemm_fetch<TI>(g, i0, j0, p0 + kTileK, p_end, ra, rb);
 #pragma unroll
         for (int kk = 0; kk < kTileK; kk += 4) {
-            float a[2], b[2];
+            float a[XT], b[2];
 #pragma unroll
-            for (int x = 0; x < 2; ++x) a[x] = As[wi + 16 * x + l % 16][kk + l / 16];
+            for (int x = 0; x < XT; ++x) a[x] = As[wi + 16 * x + l % 16][kk + l / 16];
 #pragma unroll
             for (int y = 0; y < 2; ++y) b[y] = Bs[kk + l / 16][wj + 16 * y + l % 16];
 #pragma unroll
-            for (int x = 0; x < 2; ++x)
+            for (int x = 0; x < XT; ++x)
 #pragma unroll
                 for (int y = 0; y < 2; ++y) acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[x], b[y], acc[x][y], 0, 0, 0);
         }
@@ -121,7 +134,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
     }
     // accumulator register r of tile (x, y) is C[wi + 16x + 4(l/16) + r][wj + 16y + l%16]
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < XT; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y)
 #pragma unroll
@@ -211,50 +224,73 @@ __device__ __forceinline__ void segment_stats(const float *z, int lo, int hi, fl
     }
 }
 
-// One row per thread: the clipped surrogate, value and entropy terms and their gradients.  An
-// action outside its segment (a broken device precondition) is clamped into it.
-__global__ __launch_bounds__(kRowThreads) void k_ppo_heads(HeadArgs h) {
-    const int m = blockIdx.x * kRowThreads + threadIdx.x;
-    if (m >= h.M) return;
-    const float *z = h.logits + (int64_t)m * h.a;
-    float *dz = h.dlogits + (int64_t)m * h.a;
-    const int32_t *acts = h.actions + (int64_t)m * h.n_seg;
-    float logp = 0.f, ent = 0.f;
-    for (int s = 0; s < h.n_seg; ++s) {
-        const int lo = h.off[s], hi = h.off[s + 1];
+// A workgroup owns R consecutive rows, staged in LDS with coalesced loads.  Thread (row, segment)
+// takes the segment's log-sum-exp, entropy and chosen log-probability; thread (row) adds them over
+// the segments in order and forms the clipped surrogate, value and entropy terms; thread (row,
+// segment) then overwrites the segment's logits with their gradient, and the rows are stored
+// coalesced.  An action outside its segment (a broken device precondition) is clamped into it.
+constexpr int kHeadThreads = 256, kHeadLdsFloats = 4096;
+
+__global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
+    __shared__ float zs[kHeadLdsFloats];
+    __shared__ float s_lse[kHeadThreads], s_H[kHeadThreads], s_lp[kHeadThreads], s_gl[kHeadThreads];
+    const int t = threadIdx.x, a = h.a, ns = h.n_seg;
+    const int64_t m0 = (int64_t)blockIdx.x * R;
+    const int rows = h.M - m0 < R ? (int)(h.M - m0) : R;
+    const int n = rows * a;
+    for (int e = t; e < n; e += kHeadThreads) zs[e] = h.logits[m0 * a + e];
+    __syncthreads();
+    const int p = t, r = p / ns, sg = p - r * ns;
+    const bool own = p < rows * ns;
+    int lo = 0, hi = 0, act = 0;
+    if (own) {
+        lo = h.off[sg];
+        hi = h.off[sg + 1];
+        act = min(max(h.actions[(m0 + r) * ns + sg], lo), hi - 1);
         float lse, H;
-        segment_stats(z, lo, hi, lse, H);
-        ent += H;
-        logp += z[min(max(acts[s], lo), hi - 1)] - lse;
+        segment_stats(zs + r * a, lo, hi, lse, H);
+        s_lse[p] = lse;
+        s_H[p] = H;
+        s_lp[p] = zs[r * a + act] - lse;
     }
-    const float ratio = expf(logp - h.logp_old[m]);
-    const float adv = h.adv[m];
-    const float s1 = ratio * adv;
-    const float rc = fminf(fmaxf(ratio, 1.f - h.clip_eps), 1.f + h.clip_eps);
-    const float s2 = rc * adv;
-    const bool inside = ratio >= 1.f - h.clip_eps && ratio <= 1.f + h.clip_eps;
-    const float active = s1 <= s2 ? 1.f : (inside ? 1.f : 0.f);
-    const float inv_m = 1.f / (float)h.M;
-    const float g_logp = -(adv * ratio * active) * inv_m;
-    const float we = h.w_e * inv_m;
-    for (int s = 0; s < h.n_seg; ++s) {
-        const int lo = h.off[s], hi = h.off[s + 1];
-        const int act = min(max(acts[s], lo), hi - 1);
-        float lse, H;
-        segment_stats(z, lo, hi, lse, H);
+    __syncthreads();
+    if (t < rows) {
+        const int64_t m = m0 + t;
+        float logp = 0.f, ent = 0.f;
+        for (int k = 0; k < ns; ++k) {
+            ent += s_H[t * ns + k];
+            logp += s_lp[t * ns + k];
+        }
+        const float ratio = expf(logp - h.logp_old[m]);
+        const float adv = h.adv[m];
+        const float s1 = ratio * adv;
+        const float rc = fminf(fmaxf(ratio, 1.f - h.clip_eps), 1.f + h.clip_eps);
+        const float s2 = rc * adv;
+        const bool inside = ratio >= 1.f - h.clip_eps && ratio <= 1.f + h.clip_eps;
+        const float active = s1 <= s2 ? 1.f : (inside ? 1.f : 0.f);
+        const float inv_m = 1.f / (float)h.M;
+        s_gl[t] = -(adv * ratio * active) * inv_m;
+        const float dvv = h.v[m] - h.ret[m];
+        h.dv[m] = h.w_v * 2.f * dvv * inv_m;
+        float *rw = h.rows + m * 3;
+        rw[0] = fminf(s1, s2);
+        rw[1] = dvv * dvv;
+        rw[2] = ent;
+    }
+    __syncthreads();
+    if (own) {
+        const float g_logp = s_gl[r], lse = s_lse[p], H = s_H[p];
+        const float we = h.w_e * (1.f / (float)h.M);
+        float *z = zs + r * a;
         for (int i = lo; i < hi; ++i) {
             const float ls = z[i] - lse;
-            const float p = expf(ls);
+            const float pr = expf(ls);
             // g_logp (onehot - p) - (w_e / M) dH/dz, with dH/dz = -p (log p + H)
-            dz[i] = g_logp * ((i == act ? 1.f : 0.f) - p) + we * p * (ls + H);
+            z[i] = g_logp * ((i == act ? 1.f : 0.f) - pr) + we * pr * (ls + H);
         }
     }
-    const float dvv = h.v[m] - h.ret[m];
-    h.dv[m] = h.w_v * 2.f * dvv * inv_m;
-    float *r = h.rows + (int64_t)m * 3;
-    r[0] = fminf(s1, s2);
-    r[1] = dvv * dvv;
-    r[2] = ent;
+    __syncthreads();
+    for (int e = t; e < n; e += kHeadThreads) h.dlogits[m0 * a + e] = zs[e];
 }
 
 // loss[0..3] = (total, clip, value, entropy): fixed-order means of the row terms, one workgroup.
@@ -381,20 +417,27 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
 
 int gemm(const GemmArgs &g0, float *partial, hipStream_t stream) {
     GemmArgs g = g0;
-    const unsigned gx = (unsigned)ceil_div(g.J, kTile), gy = (unsigned)ceil_div(g.I, kTile);
+    const unsigned gx = (unsigned)ceil_div(g.J, kTile);
+    int used = 1;
     if (g.split) {
         const int splits = splits_for(g.P);
         g.p_per_split = (int)round_up(ceil_div(g.P, splits), kTileK);
-        const int used = (int)ceil_div(g.P, g.p_per_split);
-        float *out = g.C;
-        g.C = partial;
-        hipLaunchKernelGGL(k_gemm, dim3(gx, gy, used), dim3(kGemmThreads), 0, stream, g);
-        HARL_HIP_CHECK(hipGetLastError());
-        const int64_t n = (int64_t)g.I * g.J;  // out is contiguous [I][J]
-        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, stream, partial, used, n, out);
+        used = (int)ceil_div(g.P, g.p_per_split);
     } else {
         g.p_per_split = (int)round_up(g.P, kTileK);
-        hipLaunchKernelGGL(k_gemm, dim3(gx, gy, 1), dim3(kGemmThreads), 0, stream, g);
+    }
+    float *out = g.C;
+    if (g.split) g.C = partial;
+    // 32-row tiles when 64-row tiles would leave the machine short of workgroups
+    const bool small = (int64_t)gx * ceil_div(g.I, 64) * used < 1024 && g.I > 32;
+    if (small)
+        hipLaunchKernelGGL(k_gemm<32>, dim3(gx, (unsigned)ceil_div(g.I, 32), used), dim3(kGemmThreads), 0, stream, g);
+    else
+        hipLaunchKernelGGL(k_gemm<64>, dim3(gx, (unsigned)ceil_div(g.I, 64), used), dim3(kGemmThreads), 0, stream, g);
+    HARL_HIP_CHECK(hipGetLastError());
+    if (g.split) {
+        const int64_t n = (int64_t)g.I * g.J;  // out is contiguous [I][J]
+        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, stream, partial, used, n, out);
     }
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
@@ -467,7 +510,13 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     h.dlogits = w.dlogits;
     h.dv = w.dv;
     h.rows = w.rows;
-    hipLaunchKernelGGL(k_ppo_heads, dim3((unsigned)ceil_div(M, kRowThreads)), dim3(kRowThreads), 0, stream, h);
+    {
+        // rows per workgroup: enough workgroups to cover the machine, at most kHeadLdsFloats logits
+        // and kHeadThreads (row, segment) pairs
+        int64_t R = ceil_div(M, 512);
+        R = std::max<int64_t>(1, std::min<int64_t>({R, kHeadLdsFloats / a, kHeadThreads / c->n_seg}));
+        hipLaunchKernelGGL(k_ppo_heads, dim3((unsigned)ceil_div(M, R)), dim3(kHeadThreads), 0, stream, h, (int)R);
+    }
     HARL_HIP_CHECK(hipGetLastError());
     if (loss_out) {
         hipLaunchKernelGGL(k_ppo_loss, dim3(1), dim3(256), 0, stream, w.rows, M, c->w_value, c->w_entropy, loss_out);
