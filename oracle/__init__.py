@@ -4,8 +4,9 @@ A ctypes wrapper over ``harl_oracle.c`` (plain C, fp64, optional OpenMP).  It co
 paper's definitions, what the HIP path must reproduce: per-program cost-model scores (GBDT over
 statement rows, summed per program), the actor/critic forward with its argmax action, and the
 top-K / running-heap selection, and for schedule tracks the reward, the advantage and the
-adaptive-stopping elimination, and the per-modification-type action selection (greedy or sampled
-through a counter-based generator).  Only ``tests/``, the package's ``smoke()`` check and
+adaptive-stopping elimination, the per-modification-type action selection (greedy or sampled
+through a counter-based generator) and one boosting round of the cost model's refit on measured
+programs.  Only ``tests/``, the package's ``smoke()`` check and
 ``bench.py``'s ``cpu_baseline`` leg may import this package; the product path never does.
 """
 from __future__ import annotations
@@ -23,7 +24,7 @@ _LIB_PATH = os.path.join(_HERE, "_liboracle.so")
 _lock = threading.Lock()
 _lib = None
 
-CFLAGS = ["-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-fno-fast-math", "-Wall", "-Wextra"]
+CFLAGS = ["-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-fno-fast-math", "-ffp-contract=off", "-Wall", "-Wextra"]
 
 
 def build(force: bool = True) -> str:
@@ -52,12 +53,15 @@ def _bind(lib):
     lib.oracle_philox4x32.argtypes = [P, P, P]
     lib.oracle_philox4x32.restype = None
     lib.oracle_policy_select.argtypes = [P, i64, i32, P, i32, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, P, P, P]
+    lib.oracle_gbdt_bin.argtypes = [P, i64, i32, i64, P, i32, P, i64, P]
+    lib.oracle_gbdt_round.argtypes = [P, i64, i32, i64, P, i32, P, P, i64, P, P, dbl, i32, dbl, dbl, dbl, dbl,
+                                      P, P, P, P, P, P, P, P]
     lib.oracle_max_threads.argtypes = []
     lib.oracle_round_bf16.argtypes = [dbl]
     lib.oracle_round_bf16.restype = dbl
     for f in (lib.oracle_score_round, lib.oracle_policy_step, lib.oracle_topk,
               lib.oracle_merge, lib.oracle_max_threads, lib.oracle_track_advantage,
-              lib.oracle_track_eliminate, lib.oracle_policy_select):
+              lib.oracle_track_eliminate, lib.oracle_policy_select, lib.oracle_gbdt_bin, lib.oracle_gbdt_round):
         f.restype = ctypes.c_int
     return lib
 
@@ -253,3 +257,55 @@ def policy_select(logits, seg_offsets, sample: bool = False, seed: int = 0, coun
     if rc != 0:
         raise ValueError("oracle_policy_select failed (%d)" % rc)
     return dict(action=action, logp=logp, probs=probs)
+
+
+# Ansor's XGBoost settings for the cost model (eta, max_depth, gamma, min_child_weight) with
+# XGBoost's default L2 regularisation lambda = 1.
+GBDT_DEFAULTS = dict(max_depth=10, eta=0.2, reg_lambda=1.0, gamma=0.001, min_child_weight=0.0, base_score=0.0)
+
+
+def gbdt_bin(x_fm, n_rows: int, cuts, n_cuts, ld: int) -> np.ndarray:
+    """Bins [n_rows][ld] uint8 of feature-major values x_fm [F][ldx]: the number of cut points of
+    the feature that are <= x, 255 for NaN, padding bytes 0."""
+    lib = _load()
+    x = _c(x_fm, np.float32)
+    F, ldx = x.shape
+    cu = _c(cuts, np.float32)
+    nc = _c(n_cuts, np.int32)
+    out = np.zeros((n_rows, ld), dtype=np.uint8)
+    rc = lib.oracle_gbdt_bin(_p(x), n_rows, F, ldx, _p(cu), cu.shape[1], _p(nc), ld, _p(out))
+    if rc != 0:
+        raise ValueError("oracle_gbdt_bin failed (%d)" % rc)
+    return out
+
+
+def gbdt_round(bins, F: int, cuts, n_cuts, prog_ptr, label, weight, margin, max_depth=10, eta=0.2,
+               reg_lambda=1.0, gamma=0.001, min_child_weight=0.0, base_score=0.0) -> dict:
+    """One boosting round under the pack-sum squared error; returns the tree (heap-numbered node
+    arrays), the updated margins and the fixed-point exponents."""
+    lib = _load()
+    b = _c(bins, np.uint8)
+    N, ld = b.shape
+    cu = _c(cuts, np.float32)
+    nc = _c(n_cuts, np.int32)
+    pp = _c(prog_ptr, np.int32)
+    P = pp.size - 1
+    y = _c(label, np.float32)
+    w = _c(weight, np.float32)
+    m = np.array(margin, dtype=np.float32, copy=True)
+    n_nodes = (1 << (max_depth + 1)) - 1
+    feature = np.zeros(n_nodes, np.int32)
+    threshold = np.zeros(n_nodes, np.float32)
+    left = np.zeros(n_nodes, np.int32)
+    right = np.zeros(n_nodes, np.int32)
+    dl = np.zeros(n_nodes, np.uint8)
+    leaf = np.zeros(n_nodes, np.float32)
+    exps = np.zeros(2, np.int32)
+    rc = lib.oracle_gbdt_round(_p(b), N, F, ld, _p(cu), cu.shape[1], _p(nc), _p(pp), P, _p(y), _p(w),
+                               float(base_score), int(max_depth), float(eta), float(reg_lambda), float(gamma),
+                               float(min_child_weight), _p(m), _p(feature), _p(threshold), _p(left), _p(right),
+                               _p(dl), _p(leaf), _p(exps))
+    if rc != 0:
+        raise ValueError("oracle_gbdt_round failed (%d)" % rc)
+    return dict(feature=feature, threshold=threshold, left=left, right=right, default_left=dl, leaf_value=leaf,
+                margin=m, exps=exps)

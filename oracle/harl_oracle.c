@@ -450,3 +450,230 @@ int oracle_policy_select(const float *logits, int64_t B, int32_t a, const int32_
     }
     return ORACLE_OK;
 }
+
+/* ------------------------------------------------------------------------------------------- */
+/* Refit of the cost model on measured programs (Algorithm 1, its last steps: the top-K states
+ * are measured and the cost model is trained on (S^, P); Section 6.1 and Appendix A.2: XGBoost
+ * with Ansor's settings).  One boosting round of histogram-based gradient boosting (Chen and
+ * Guestrin, KDD'16, Section 3: the second-order gain and the optimal leaf weight; Section 3.4:
+ * the sparsity-aware default direction) under the pack-sum squared error: a program's prediction
+ * is base_score plus the sum of its statements' margins, the objective is
+ * 1/2 sum_p w_p (s_p - y_p)^2, so every statement row of program p carries the gradient
+ * w_p (s_p - y_p) and the hessian w_p.
+ *
+ * Readings (each also listed in the design doc):
+ *   - features are binned per feature by caller-given increasing cut points: bin(x) = the number
+ *     of cut points <= x (0 .. n_cuts), 255 for NaN (missing);
+ *   - a candidate split (f, t, dir) sends bins < t left, t in 1 .. n_cuts[f], and the missing
+ *     rows left (dir = 1) or right (dir = 0); its node test is x < cuts[f][t - 1];
+ *   - gradients and hessians are summed exactly: each program's value is rounded once to a
+ *     fixed-point grid 2^-e (e chosen from the largest magnitude and the row count so that no
+ *     sum can exceed 2^62) and summed as 64-bit integers;
+ *   - gain = GL^2 / (HL + lambda) + GR^2 / (HR + lambda) - G^2 / (H + lambda) in fp64, the node
+ *     splits iff the best gain exceeds gamma (pre-pruning) and both children's hessians reach
+ *     min_child_weight; the best is the largest gain, ties to the lowest feature, then the lowest
+ *     t, then missing-left before missing-right;
+ *   - the tree grows depth-wise to max_depth in heap numbering (children of node k are 2k + 1
+ *     and 2k + 2); a leaf holds -(G / (H + lambda)) eta rounded to fp32;
+ *   - the margins are updated in fp32: margin[r] += leaf value of the row's leaf. */
+
+/* bins[r * ld + f] for statement row r and feature f < F (bytes F .. ld - 1 are zero) from the
+ * feature-major values x[f * ldx + r] and the cut points cuts[f * cut_stride + i], i < n_cuts[f]. */
+int oracle_gbdt_bin(const float *x, int64_t N, int32_t F, int64_t ldx, const float *cuts,
+                    int32_t cut_stride, const int32_t *n_cuts, int64_t ld, uint8_t *bins) {
+    if (N < 0 || F < 1 || ld < F || ldx < N || cut_stride < 1) return ORACLE_EINVAL;
+    for (int32_t f = 0; f < F; ++f)
+        if (n_cuts[f] < 0 || n_cuts[f] > 254 || n_cuts[f] > cut_stride) return ORACLE_EINVAL;
+    for (int64_t r = 0; r < N; ++r) {
+        for (int64_t f = 0; f < ld; ++f) {
+            uint8_t b = 0;
+            if (f < F) {
+                const float v = x[f * ldx + r];
+                if (isnan(v)) {
+                    b = 255;
+                } else {
+                    int c = 0;
+                    for (int32_t i = 0; i < n_cuts[f]; ++i)
+                        if (cuts[f * cut_stride + i] <= v) ++c;
+                    b = (uint8_t)c;
+                }
+            }
+            bins[r * ld + f] = b;
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* Smallest c with 2^c >= n (n >= 1). */
+static int ceil_log2_i64(int64_t n) {
+    int c = 0;
+    while (((int64_t)1 << c) < n) ++c;
+    return c;
+}
+
+/* The fixed-point exponent e for values of largest magnitude amax summed over n rows:
+ * amax < 2^E (frexp), |v 2^e| <= 2^(62 - ceil_log2(n)). */
+static int fixed_exponent(double amax, int64_t n) {
+    if (!(amax > 0.0)) return 0;
+    int E;
+    frexp(amax, &E);
+    return 62 - ceil_log2_i64(n > 0 ? n : 1) - E;
+}
+
+typedef struct {
+    const uint8_t *bins;
+    int32_t F;
+    int64_t ld;
+    const float *cuts;
+    int32_t cut_stride;
+    const int32_t *n_cuts;
+    const int64_t *qg, *qh;  /* per row */
+    int eg, eh;
+    int32_t max_depth;
+    double eta, lambda, gamma, mcw;
+    float *margin;
+    int32_t *feature;
+    float *threshold;
+    int32_t *left, *right;
+    uint8_t *default_left;
+    float *leaf_value;
+} gbdt_ctx;
+
+static double node_score(double G, double H, double lambda) { return (G * G) / (H + lambda); }
+
+static int grow(const gbdt_ctx *c, int64_t k, int32_t depth, const int64_t *rows, int64_t n) {
+    int64_t Gi = 0, Hi = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        Gi += c->qg[rows[i]];
+        Hi += c->qh[rows[i]];
+    }
+    const double G = ldexp((double)Gi, -c->eg), H = ldexp((double)Hi, -c->eh);
+    int found = 0, bf = 0, bt = 0, bdir = 0;
+    double best = 0.0;
+    if (depth < c->max_depth) {
+        const double parent = node_score(G, H, c->lambda);
+        for (int32_t f = 0; f < c->F; ++f) {
+            int64_t hg[256], hh[256];
+            memset(hg, 0, sizeof hg);
+            memset(hh, 0, sizeof hh);
+            for (int64_t i = 0; i < n; ++i) {
+                const uint8_t b = c->bins[rows[i] * c->ld + f];
+                hg[b] += c->qg[rows[i]];
+                hh[b] += c->qh[rows[i]];
+            }
+            int64_t GLi = 0, HLi = 0;
+            for (int32_t t = 1; t <= c->n_cuts[f]; ++t) {
+                GLi += hg[t - 1];
+                HLi += hh[t - 1];
+                for (int dir = 1; dir >= 0; --dir) { /* missing-left first */
+                    const int64_t gl = GLi + (dir ? hg[255] : 0), hl = HLi + (dir ? hh[255] : 0);
+                    const double GL = ldexp((double)gl, -c->eg), HL = ldexp((double)hl, -c->eh);
+                    const double GR = ldexp((double)(Gi - gl), -c->eg), HR = ldexp((double)(Hi - hl), -c->eh);
+                    if (!(HL >= c->mcw) || !(HR >= c->mcw)) continue;
+                    const double gain = (node_score(GL, HL, c->lambda) + node_score(GR, HR, c->lambda)) - parent;
+                    if (!found || gain > best) {
+                        found = 1;
+                        best = gain;
+                        bf = f;
+                        bt = t;
+                        bdir = dir;
+                    }
+                }
+            }
+        }
+    }
+    if (found && best > c->gamma) {
+        c->feature[k] = bf;
+        c->threshold[k] = c->cuts[(int64_t)bf * c->cut_stride + bt - 1];
+        c->left[k] = (int32_t)(2 * k + 1);
+        c->right[k] = (int32_t)(2 * k + 2);
+        c->default_left[k] = (uint8_t)bdir;
+        c->leaf_value[k] = 0.0f;
+        int64_t *lr = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+        int64_t *rr = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+        if (!lr || !rr) {
+            free(lr);
+            free(rr);
+            return ORACLE_ENOMEM;
+        }
+        int64_t nl = 0, nr = 0;
+        for (int64_t i = 0; i < n; ++i) {
+            const uint8_t b = c->bins[rows[i] * c->ld + bf];
+            const int go_left = b == 255 ? bdir : b < bt;
+            if (go_left) lr[nl++] = rows[i];
+            else rr[nr++] = rows[i];
+        }
+        int rc = grow(c, 2 * k + 1, depth + 1, lr, nl);
+        if (rc == ORACLE_OK) rc = grow(c, 2 * k + 2, depth + 1, rr, nr);
+        free(lr);
+        free(rr);
+        return rc;
+    }
+    const float w = (float)(-(G / (H + c->lambda)) * c->eta);
+    c->feature[k] = -1;
+    c->leaf_value[k] = w;
+    for (int64_t i = 0; i < n; ++i) c->margin[rows[i]] = c->margin[rows[i]] + w;
+    return ORACLE_OK;
+}
+
+/* One boosting round.  bins [N][ld] as oracle_gbdt_bin writes them; program p owns rows
+ * [prog_ptr[p], prog_ptr[p + 1]); label, weight [P]; margin [N] in/out.  The tree is written to
+ * node arrays of 2^(max_depth + 1) - 1 entries in heap numbering; nodes the tree does not reach
+ * hold feature -1, leaf value 0.  exps (optional) receives the fixed-point exponents (e_g, e_h). */
+int oracle_gbdt_round(const uint8_t *bins, int64_t N, int32_t F, int64_t ld, const float *cuts,
+                      int32_t cut_stride, const int32_t *n_cuts, const int32_t *prog_ptr, int64_t P,
+                      const float *label, const float *weight, double base_score, int32_t max_depth,
+                      double eta, double lambda, double gamma, double min_child_weight, float *margin,
+                      int32_t *feature, float *threshold, int32_t *left, int32_t *right,
+                      uint8_t *default_left, float *leaf_value, int32_t *exps) {
+    if (N < 0 || P < 0 || F < 1 || ld < F || max_depth < 1 || max_depth > 12 || !(lambda > 0.0) ||
+        !(gamma >= 0.0) || !(min_child_weight >= 0.0) || cut_stride < 1)
+        return ORACLE_EINVAL;
+    if (prog_ptr[0] != 0 || prog_ptr[P] != N) return ORACLE_EINVAL;
+    const int64_t n_nodes = ((int64_t)1 << (max_depth + 1)) - 1;
+    for (int64_t k = 0; k < n_nodes; ++k) {
+        feature[k] = -1;
+        threshold[k] = 0.0f;
+        left[k] = right[k] = 0;
+        default_left[k] = 0;
+        leaf_value[k] = 0.0f;
+    }
+    /* pack-sum gradient and hessian per program */
+    double *g = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+    double *h = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+    int64_t *qg = (int64_t *)malloc(sizeof(int64_t) * (size_t)(N > 0 ? N : 1));
+    int64_t *qh = (int64_t *)malloc(sizeof(int64_t) * (size_t)(N > 0 ? N : 1));
+    int64_t *rows = (int64_t *)malloc(sizeof(int64_t) * (size_t)(N > 0 ? N : 1));
+    if (!g || !h || !qg || !qh || !rows) {
+        free(g); free(h); free(qg); free(qh); free(rows);
+        return ORACLE_ENOMEM;
+    }
+    double gmax = 0.0, hmax = 0.0;
+    for (int64_t p = 0; p < P; ++p) {
+        double s = base_score;
+        for (int32_t r = prog_ptr[p]; r < prog_ptr[p + 1]; ++r) s += (double)margin[r];
+        g[p] = (double)weight[p] * (s - (double)label[p]);
+        h[p] = (double)weight[p];
+        if (prog_ptr[p + 1] > prog_ptr[p]) {
+            if (fabs(g[p]) > gmax) gmax = fabs(g[p]);
+            if (fabs(h[p]) > hmax) hmax = fabs(h[p]);
+        }
+    }
+    const int eg = fixed_exponent(gmax, N), eh = fixed_exponent(hmax, N);
+    for (int64_t p = 0; p < P; ++p)
+        for (int32_t r = prog_ptr[p]; r < prog_ptr[p + 1]; ++r) {
+            qg[r] = (int64_t)rint(ldexp(g[p], eg));
+            qh[r] = (int64_t)rint(ldexp(h[p], eh));
+        }
+    if (exps) {
+        exps[0] = eg;
+        exps[1] = eh;
+    }
+    for (int64_t r = 0; r < N; ++r) rows[r] = r;
+    const gbdt_ctx c = {bins, F, ld, cuts, cut_stride, n_cuts, qg, qh, eg, eh, max_depth, eta, lambda,
+                        gamma, min_child_weight, margin, feature, threshold, left, right, default_left,
+                        leaf_value};
+    const int rc = grow(&c, 0, 0, rows, N);
+    free(g); free(h); free(qg); free(qh); free(rows);
+    return rc;
+}

@@ -99,3 +99,67 @@ def lexsort_topk(score, k: int, index_base: int = 0):
     nan_last = np.isnan(s).astype(np.int8)
     order = np.lexsort((idx, neg, nan_last))
     return s[order[:k]].astype(np.float32), order[:k] + index_base
+
+
+def brute_gbdt_tree(bins, F, cuts, n_cuts, prog_ptr, label, weight, margin, max_depth, eta, lam, gamma, mcw,
+                    base_score=0.0):
+    """Depth-wise greedy tree of one boosting round under the pack-sum squared error, from sets of
+    rows and exact rational arithmetic: every candidate (feature f, threshold index t, missing
+    direction) is scored by summing the rows' gradients directly.  Returns (nodes, margins, gaps):
+    nodes maps heap index -> ("split", f, t, default_left) or ("leaf", value as Fraction); gaps
+    lists, per split decision, the relative distance between the best and the next distinct gain
+    (a decision closer than fp64 rounding cannot be pinned)."""
+    from fractions import Fraction as Fr
+    P = len(prog_ptr) - 1
+    g, h = {}, {}
+    for p in range(P):
+        s = Fr(base_score)
+        for r in range(prog_ptr[p], prog_ptr[p + 1]):
+            s += Fr(float(margin[r]))
+        for r in range(prog_ptr[p], prog_ptr[p + 1]):
+            g[r] = Fr(float(weight[p])) * (s - Fr(float(label[p])))
+            h[r] = Fr(float(weight[p]))
+    lam, eta, gamma, mcw = Fr(lam), Fr(eta), Fr(gamma), Fr(mcw)
+    nodes, gaps = {}, []
+    new_margin = np.array(margin, dtype=np.float32, copy=True)
+
+    def score(G, H):
+        return G * G / (H + lam)
+
+    def grow(k, depth, rows):
+        G = sum((g[r] for r in rows), Fr(0))
+        H = sum((h[r] for r in rows), Fr(0))
+        cands = []
+        if depth < max_depth:
+            for f in range(F):
+                for t in range(1, int(n_cuts[f]) + 1):
+                    for dleft in (1, 0):
+                        L = [r for r in rows if (bins[r, f] == 255 and dleft) or (bins[r, f] != 255 and bins[r, f] < t)]
+                        GL = sum((g[r] for r in L), Fr(0))
+                        HL = sum((h[r] for r in L), Fr(0))
+                        if HL < mcw or H - HL < mcw:
+                            continue
+                        cands.append((score(GL, HL) + score(G - GL, H - HL) - score(G, H), f, t, dleft))
+        if cands:
+            best = max(c[0] for c in cands)
+            first = next(c for c in cands if c[0] == best)
+            others = [c[0] for c in cands if c[0] != best]
+            if others:
+                gaps.append(float((best - max(others)) / max(abs(best), Fr(1, 10**30))))
+            if best > gamma:
+                gaps.append(float(abs(best - gamma) / max(abs(best), Fr(1, 10**30))))
+                _, f, t, dleft = first
+                nodes[k] = ("split", f, t, dleft)
+                L = [r for r in rows if (bins[r, f] == 255 and dleft) or (bins[r, f] != 255 and bins[r, f] < t)]
+                R = [r for r in rows if r not in set(L)]
+                grow(2 * k + 1, depth + 1, L)
+                grow(2 * k + 2, depth + 1, R)
+                return
+            gaps.append(float(abs(best - gamma) / max(abs(best), Fr(1, 10**30))))
+        w = -(G / (H + lam)) * eta
+        nodes[k] = ("leaf", w)
+        for r in rows:
+            new_margin[r] = np.float32(new_margin[r] + np.float32(float(w)))
+
+    grow(0, 0, list(range(int(prog_ptr[-1]))))
+    return nodes, new_margin, gaps

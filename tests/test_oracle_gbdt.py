@@ -1,0 +1,259 @@
+"""Pins of the oracle's cost-model refit (one boosting round; Algorithm 1, the training of the cost
+model on the measured top-K; Section 6.1 and Appendix A.2: XGBoost with Ansor's settings; the gain,
+leaf weight and default direction of Chen and Guestrin, KDD'16, Sections 3 and 3.4) against
+things other than the oracle: numpy's searchsorted, an exact rational brute force over every
+candidate split, closed forms of isolated programs and of a step function, and the scoring
+oracle, which routes rows by the produced tree's thresholds instead of by bins."""
+from __future__ import annotations
+
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import brute
+
+
+def _dyadic(rng, n, lo=-8, hi=8, den=16):
+    return (rng.integers(lo * den, hi * den, size=n) / den).astype(np.float32)
+
+
+def _problem(seed, P=7, s_max=3, F=3, n_cuts=5, p_nan=0.0, dyadic=True, structured=False):
+    rng = np.random.default_rng(seed)
+    counts = rng.integers(1, s_max + 1, size=P)
+    prog_ptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    N = int(prog_ptr[-1])
+    cuts = np.sort(rng.choice(np.arange(-20, 20, dtype=np.float32) / 4, size=(F, n_cuts), replace=True), axis=1)
+    cuts = np.stack([np.unique(c)[:n_cuts] for c in cuts]) if all(np.unique(c).size >= n_cuts for c in cuts) else \
+        np.stack([np.linspace(-4, 4, n_cuts, dtype=np.float32)] * F)
+    nc = np.full(F, n_cuts, np.int32)
+    x = (rng.integers(-24, 24, size=(F, N)) / 4).astype(np.float32)
+    x[rng.random(size=x.shape) < p_nan] = np.nan
+    label = _dyadic(rng, P, 0, 4) if dyadic else rng.uniform(0, 4, P).astype(np.float32)
+    if structured:  # labels that the features explain in part, as measured run times are
+        xz = np.nan_to_num(x, nan=0.0)
+        row_y = 2.0 * (xz[0] > 0) + 1.0 * (xz[1 % F] > 1.0) - 1.5 * (xz[2 % F] < -2.0)
+        label = (label / 4 + np.array([row_y[prog_ptr[p]:prog_ptr[p + 1]].sum() for p in range(P)])).astype(np.float32)
+    weight = (rng.integers(1, 8, size=P) / 4).astype(np.float32)
+    margin = _dyadic(rng, N, -1, 1)
+    return dict(x=x, cuts=cuts.astype(np.float32), n_cuts=nc, prog_ptr=prog_ptr, label=label, weight=weight,
+                margin=margin, N=N, F=F)
+
+
+def _compare_to_brute(pb, max_depth, lam=1.0, gamma=0.001, mcw=0.0, eta=0.2, base=0.0):
+    bins = oracle.gbdt_bin(pb["x"], pb["N"], pb["cuts"], pb["n_cuts"], 8)
+    got = oracle.gbdt_round(bins, pb["F"], pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"], pb["weight"],
+                            pb["margin"], max_depth=max_depth, eta=eta, reg_lambda=lam, gamma=gamma,
+                            min_child_weight=mcw, base_score=base)
+    nodes, margin, gaps = brute.brute_gbdt_tree(bins, pb["F"], pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"],
+                                                pb["weight"], pb["margin"], max_depth, eta, lam, gamma, mcw, base)
+    assert min(gaps, default=1.0) > 1e-9, "decision too close to a tie for an fp64 pin; pick another seed"
+    n_nodes = (1 << (max_depth + 1)) - 1
+    for k in range(n_nodes):
+        if k not in nodes:
+            assert got["feature"][k] == -1 and got["leaf_value"][k] == 0.0
+            continue
+        if nodes[k][0] == "split":
+            _, f, t, dleft = nodes[k]
+            assert got["feature"][k] == f, (k, got["feature"][k], f)
+            assert got["threshold"][k] == pb["cuts"][f, t - 1]
+            assert got["default_left"][k] == dleft
+            assert got["left"][k] == 2 * k + 1 and got["right"][k] == 2 * k + 2
+        else:
+            want = np.float32(float(nodes[k][1]))
+            assert got["feature"][k] == -1
+            assert abs(int(np.float32(got["leaf_value"][k]).view(np.int32)) - int(want.view(np.int32))) <= 1, \
+                (k, got["leaf_value"][k], want)
+    np.testing.assert_allclose(got["margin"], margin, rtol=1e-6, atol=1e-6)
+    return got, nodes
+
+
+def test_bins_are_searchsorted_counts():
+    rng = np.random.default_rng(3)
+    F, N = 5, 300
+    cuts = np.sort(rng.normal(size=(F, 20)).astype(np.float32), axis=1)
+    n_cuts = np.array([20, 0, 7, 1, 13], np.int32)
+    x = rng.normal(size=(F, N + 9)).astype(np.float32)
+    x[:, :20] = cuts[:, :20]  # values equal to a cut point count it
+    x[:, 20] = np.nan
+    x[:, 21] = np.inf
+    x[:, 22] = -np.inf
+    x[:, 23] = np.nextafter(cuts[:, 0], -np.inf)
+    bins = oracle.gbdt_bin(x, N, cuts, n_cuts, 16)
+    for f in range(F):
+        want = np.searchsorted(cuts[f, :n_cuts[f]], x[f, :N], side="right")
+        want[np.isnan(x[f, :N])] = 255
+        assert (bins[:, f] == want).all(), f
+    assert (bins[:, F:] == 0).all()
+
+
+@pytest.mark.parametrize("seed,depth,p_nan,lam", [(1, 1, 0.0, 1.0), (2, 2, 0.0, 0.5), (4, 3, 0.2, 0.25),
+                                                  (5, 2, 0.3, 1.0), (8, 4, 0.1, 0.125), (9, 3, 0.0, 1.0)])
+def test_tree_matches_exact_brute_force(seed, depth, p_nan, lam):
+    for s in range(seed * 100, seed * 100 + 50):  # first seed whose decisions are not near-ties
+        pb = _problem(s, P=14, p_nan=p_nan, structured=True)
+        try:
+            got, nodes = _compare_to_brute(pb, depth, lam=lam)
+            assert sum(v[0] == "split" for v in nodes.values()) >= min(depth, 2)
+            return
+        except AssertionError as e:
+            if "near-ties" in str(e) or "too close" in str(e):
+                continue
+            raise
+    pytest.fail("no seed without near-ties")
+
+
+def test_step_function_single_split_closed_form():
+    """Programs of one statement each, label 1 below c and 3 from c on, margins 0: the root splits
+    at c, each side's leaf is eta n y / (n + lambda) (g = -y, h = 1), missing-left on the tie."""
+    N = 10
+    x = np.array([[0.0, 1, 2, 3, 4, 5, 6, 7, 8, 9]], np.float32)
+    cuts = np.array([[2.5, 3.5, 6.5]], np.float32)
+    y = np.where(x[0] < 3.5, 1.0, 3.0).astype(np.float32)
+    pp = np.arange(N + 1, dtype=np.int32)
+    bins = oracle.gbdt_bin(x, N, cuts, np.array([3], np.int32), 8)
+    r = oracle.gbdt_round(bins, 1, cuts, np.array([3], np.int32), pp, y, np.ones(N, np.float32),
+                          np.zeros(N, np.float32), max_depth=1, eta=0.2, reg_lambda=1.0, gamma=0.0)
+    assert r["feature"][0] == 0 and r["threshold"][0] == np.float32(3.5) and r["default_left"][0] == 1
+    assert r["leaf_value"][1] == np.float32(0.2 * 4 * 1.0 / 5) and r["leaf_value"][2] == np.float32(0.2 * 6 * 3.0 / 7)
+    np.testing.assert_array_equal(r["margin"], np.where(x[0] < 3.5, r["leaf_value"][1], r["leaf_value"][2]))
+
+
+def test_isolated_programs_closed_form():
+    """Feature 0 names the program, deep enough to isolate every program, gamma 0, lambda small (a
+    large lambda can make a split of two programs lose): each row of
+    program p gets -eta n_p w_p (s_p - y_p) / (n_p w_p + lambda), s_p = base + its margins."""
+    rng = np.random.default_rng(11)
+    P = 6
+    counts = np.array([1, 3, 2, 4, 1, 2])
+    pp = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    N = int(pp[-1])
+    x = np.repeat(np.arange(P, dtype=np.float32), counts)[None, :]
+    cuts = (np.arange(1, P, dtype=np.float32) - 0.5)[None, :]
+    y = np.array([3.0, -1.0, 0.5, 2.0, 7.0, -4.0], np.float32)
+    w = np.array([1.0, 0.5, 2.0, 1.5, 0.25, 1.0], np.float32)
+    m = _dyadic(rng, N, -1, 1)
+    base, lam, eta = 0.75, 1e-3, 0.3  # a small lambda: a split of distinct residuals always gains
+    bins = oracle.gbdt_bin(x, N, cuts, np.array([P - 1], np.int32), 8)
+    r = oracle.gbdt_round(bins, 1, cuts, np.array([P - 1], np.int32), pp, y, w, m, max_depth=P - 1, eta=eta,
+                          reg_lambda=lam, gamma=0.0, base_score=base)
+    for p in range(P):
+        n = counts[p]
+        s = base + float(np.sum(m[pp[p]:pp[p + 1]].astype(np.float64)))
+        leaf = np.float32(-eta * n * w[p] * (s - y[p]) / (n * w[p] + lam))
+        want = (m[pp[p]:pp[p + 1]] + leaf).astype(np.float32)
+        np.testing.assert_allclose(r["margin"][pp[p]:pp[p + 1]], want, rtol=2e-7, atol=1e-7)
+
+
+def test_missing_rows_follow_the_learned_direction():
+    """Rows whose feature is missing carry the labels of one side; the default direction sends them
+    there, and they receive that side's leaf."""
+    for nan_like_low in (True, False):
+        N = 12
+        xv = np.array([0, 1, 2, 3, 4, 5, 6, 7, np.nan, np.nan, np.nan, np.nan], np.float32)
+        y = np.where(xv < 3.5, 1.0, 5.0).astype(np.float32)
+        y[8:] = 1.0 if nan_like_low else 5.0
+        cuts = np.array([[3.5]], np.float32)
+        pp = np.arange(N + 1, dtype=np.int32)
+        bins = oracle.gbdt_bin(xv[None, :], N, cuts, np.array([1], np.int32), 8)
+        r = oracle.gbdt_round(bins, 1, cuts, np.array([1], np.int32), pp, y, np.ones(N, np.float32),
+                              np.zeros(N, np.float32), max_depth=1, gamma=0.0)
+        assert r["feature"][0] == 0
+        assert r["default_left"][0] == (1 if nan_like_low else 0)
+        side = r["leaf_value"][1] if nan_like_low else r["leaf_value"][2]
+        assert (r["margin"][8:] == side).all()
+
+
+def test_gamma_prunes_at_the_best_gain():
+    pb = _problem(31, P=9)
+    bins = oracle.gbdt_bin(pb["x"], pb["N"], pb["cuts"], pb["n_cuts"], 8)
+    nodes, _, gaps = brute.brute_gbdt_tree(bins, pb["F"], pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"],
+                                           pb["weight"], pb["margin"], 1, 0.2, 1.0, 0.0, 0.0)
+    assert nodes[0][0] == "split"
+    # the root's best gain, exactly
+    from fractions import Fraction as Fr
+    f, t, dleft = nodes[0][1:]
+    P = len(pb["prog_ptr"]) - 1
+    g, h = {}, {}
+    for p in range(P):
+        s = sum((Fr(float(pb["margin"][r])) for r in range(pb["prog_ptr"][p], pb["prog_ptr"][p + 1])), Fr(0))
+        for r in range(pb["prog_ptr"][p], pb["prog_ptr"][p + 1]):
+            g[r] = Fr(float(pb["weight"][p])) * (s - Fr(float(pb["label"][p])))
+            h[r] = Fr(float(pb["weight"][p]))
+    rows = range(pb["N"])
+    L = [r for r in rows if (bins[r, f] == 255 and dleft) or (bins[r, f] != 255 and bins[r, f] < t)]
+    G, H = sum(g.values(), Fr(0)), sum(h.values(), Fr(0))
+    GL, HL = sum((g[r] for r in L), Fr(0)), sum((h[r] for r in L), Fr(0))
+    sc = lambda a, b: a * a / (b + 1)
+    best = float(sc(GL, HL) + sc(G - GL, H - HL) - sc(G, H))
+    for gamma, split in ((best * (1 - 1e-9), True), (best * (1 + 1e-9), False)):
+        r = oracle.gbdt_round(bins, pb["F"], pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"], pb["weight"],
+                              pb["margin"], max_depth=1, gamma=gamma)
+        assert (r["feature"][0] >= 0) == split, gamma
+        if not split:
+            assert r["leaf_value"][0] == np.float32(float(-(G / (H + 1)) * Fraction(0.2)))
+
+
+def test_ties_go_to_the_lowest_feature_and_threshold():
+    pb = _problem(41, F=2)
+    pb["x"] = np.stack([pb["x"][1], pb["x"][1], pb["x"][1]])  # three identical features
+    pb["cuts"] = np.stack([pb["cuts"][1]] * 3)
+    pb["n_cuts"] = np.full(3, pb["n_cuts"][1], np.int32)
+    pb["F"] = 3
+    bins = oracle.gbdt_bin(pb["x"], pb["N"], pb["cuts"], pb["n_cuts"], 8)
+    r = oracle.gbdt_round(bins, 3, pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"], pb["weight"], pb["margin"],
+                          max_depth=3, gamma=0.0)
+    internal = r["feature"][r["feature"] >= 0]
+    assert internal.size > 0 and (internal == 0).all()
+    # mirror-symmetric labels: the splits at 1.5 and 3.5 gain exactly the same; the lower t wins
+    x = np.arange(6, dtype=np.float32)[None, :]
+    y = np.array([1, 1, 3, 3, 1, 1], np.float32)
+    cuts = np.array([[1.5, 3.5]], np.float32)
+    bins = oracle.gbdt_bin(x, 6, cuts, np.array([2], np.int32), 8)
+    r = oracle.gbdt_round(bins, 1, cuts, np.array([2], np.int32), np.arange(7, dtype=np.int32), y,
+                          np.ones(6, np.float32), np.zeros(6, np.float32), max_depth=1, gamma=0.0, reg_lambda=1e-3)
+    assert r["feature"][0] == 0 and r["threshold"][0] == np.float32(1.5)
+
+
+def test_min_child_weight_blocks_light_children():
+    pb = _problem(51, P=8)
+    bins = oracle.gbdt_bin(pb["x"], pb["N"], pb["cuts"], pb["n_cuts"], 8)
+    H = float(sum(pb["weight"][p] * (pb["prog_ptr"][p + 1] - pb["prog_ptr"][p]) for p in range(8)))
+    r = oracle.gbdt_round(bins, pb["F"], pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"], pb["weight"],
+                          pb["margin"], max_depth=2, gamma=0.0, min_child_weight=H / 2 + 0.01)
+    assert r["feature"][0] == -1
+    _compare_to_brute(pb, 2, gamma=0.0, mcw=1.0)
+
+
+def test_fixed_point_exponent_rule():
+    """e = 62 - ceil(log2 N) - E with max |g| = m 2^E, 1/2 <= m < 1 (no sum of N rows overflows)."""
+    N = 40
+    x = np.zeros((1, N), np.float32)
+    cuts = np.array([[0.5]], np.float32)
+    pp = np.array([0, 10, 40], np.int32)
+    y = np.array([3.0, 1.0], np.float32)  # g = -3 and -1: max 3 = 0.75 * 2^2
+    w = np.array([1.0, 0.75], np.float32)  # h max 1 = 0.5 * 2^1
+    bins = oracle.gbdt_bin(x, N, cuts, np.array([1], np.int32), 8)
+    r = oracle.gbdt_round(bins, 1, cuts, np.array([1], np.int32), pp, y, w, np.zeros(N, np.float32), max_depth=1)
+    assert list(r["exps"]) == [62 - 6 - 2, 62 - 6 - 1]
+
+
+def test_new_tree_scores_like_the_margin_update():
+    """The tree, routed by its thresholds on the raw features (the scoring oracle), adds to each row
+    exactly what the round added to its margin: thresholds, bins and default directions agree."""
+    pb = _problem(61, P=40, s_max=5, F=4, n_cuts=6, p_nan=0.15, dyadic=False)
+    x = np.nan_to_num(pb["x"], nan=0.0)
+    row_y = 2.0 * (x[0] > 0) + (x[1] > 1.0) - 1.5 * (x[2] < -2.0)
+    pp = pb["prog_ptr"]
+    pb["label"] = np.array([row_y[pp[p]:pp[p + 1]].sum() for p in range(pp.size - 1)], np.float32)
+    bins = oracle.gbdt_bin(pb["x"], pb["N"], pb["cuts"], pb["n_cuts"], 8)
+    zero = np.zeros(pb["N"], np.float32)
+    r = oracle.gbdt_round(bins, pb["F"], pb["cuts"], pb["n_cuts"], pb["prog_ptr"], pb["label"], pb["weight"], zero,
+                          max_depth=4, gamma=0.0)
+    assert (r["feature"] >= 0).sum() >= 3
+    ens = dict(n_trees=1, n_features=pb["F"], root=np.zeros(1, np.int32), feature=r["feature"],
+               threshold=r["threshold"], left=r["left"], right=r["right"], default_left=r["default_left"],
+               leaf_value=r["leaf_value"], base_score=0.0)
+    sc = oracle.score_round(ens, pb["x"], pb["prog_ptr"])
+    np.testing.assert_array_equal(sc["stmt32"], r["margin"])

@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 
 import oracle
+from tests import test_oracle_gbdt as gb
 from tests import test_oracle_pins as pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "harl_oracle.c")
@@ -80,6 +81,39 @@ MUTANTS = {
                           [(pins.test_select_softmax_and_logp_identities, {})]),
     "segment_shifted": ("const int32_t lo = off[s], hi = off[s + 1];", "const int32_t lo = off[s], hi = off[s + 1] - (s == 0);",
                         [(pins.test_greedy_select_is_per_segment_first_argmax, {})]),
+    "gbdt_bin_strict": ("if (cuts[f * cut_stride + i] <= v) ++c;", "if (cuts[f * cut_stride + i] < v) ++c;",
+                        [(gb.test_bins_are_searchsorted_counts, {})]),
+    "gbdt_threshold_next_cut": ("c->cuts[(int64_t)bf * c->cut_stride + bt - 1]", "c->cuts[(int64_t)bf * c->cut_stride + bt]",
+                                [(gb.test_step_function_single_split_closed_form, {})]),
+    "gbdt_lambda_dropped": ("return (G * G) / (H + lambda);", "return (G * G) / (H + 1e-300);",
+                            [(gb.test_tree_matches_exact_brute_force, dict(seed=2, depth=2, p_nan=0.0, lam=0.5))]),
+    "gbdt_leaf_sign": ("const float w = (float)(-(G / (H + c->lambda)) * c->eta);",
+                       "const float w = (float)((G / (H + c->lambda)) * c->eta);",
+                       [(gb.test_step_function_single_split_closed_form, {})]),
+    "gbdt_eta_dropped": ("const float w = (float)(-(G / (H + c->lambda)) * c->eta);",
+                         "const float w = (float)(-(G / (H + c->lambda)));",
+                         [(gb.test_isolated_programs_closed_form, {})]),
+    "gbdt_hessian_one": ("h[p] = (double)weight[p];", "h[p] = 1.0;", [(gb.test_isolated_programs_closed_form, {})]),
+    "gbdt_base_ignored": ("double s = base_score;", "double s = 0.0;", [(gb.test_isolated_programs_closed_form, {})]),
+    "gbdt_pack_mean": ("g[p] = (double)weight[p] * (s - (double)label[p]);",
+                       "g[p] = (double)weight[p] * (s / (prog_ptr[p + 1] - prog_ptr[p] + (prog_ptr[p + 1] == prog_ptr[p])) - (double)label[p]);",
+                       [(gb.test_isolated_programs_closed_form, {})]),
+    "gbdt_missing_right_first": ("for (int dir = 1; dir >= 0; --dir)", "for (int dir = 0; dir <= 1; ++dir)",
+                                 [(gb.test_step_function_single_split_closed_form, {})]),
+    "gbdt_missing_not_routed": ("const int go_left = b == 255 ? bdir : b < bt;", "const int go_left = b < bt;",
+                                [(gb.test_missing_rows_follow_the_learned_direction, {})]),
+    "gbdt_tie_last_feature": ("if (!found || gain > best) {", "if (!found || gain >= best) {",
+                              [(gb.test_ties_go_to_the_lowest_feature_and_threshold, {})]),
+    "gbdt_parent_not_subtracted": ("(node_score(GL, HL, c->lambda) + node_score(GR, HR, c->lambda)) - parent",
+                                   "(node_score(GL, HL, c->lambda) + node_score(GR, HR, c->lambda))",
+                                   [(gb.test_gamma_prunes_at_the_best_gain, {})]),
+    "gbdt_mcw_ignored": ("if (!(HL >= c->mcw) || !(HR >= c->mcw)) continue;", "",
+                         [(gb.test_min_child_weight_blocks_light_children, {})]),
+    "gbdt_exponent_off": ("return 62 - ceil_log2_i64(n > 0 ? n : 1) - E;", "return 62 - ceil_log2_i64(n > 0 ? n : 1) - E + 1;",
+                          [(gb.test_fixed_point_exponent_rule, {})]),
+    "gbdt_children_swapped": ("int rc = grow(c, 2 * k + 1, depth + 1, lr, nl);\n        if (rc == ORACLE_OK) rc = grow(c, 2 * k + 2, depth + 1, rr, nr);",
+                              "int rc = grow(c, 2 * k + 1, depth + 1, rr, nr);\n        if (rc == ORACLE_OK) rc = grow(c, 2 * k + 2, depth + 1, lr, nl);",
+                              [(gb.test_new_tree_scores_like_the_margin_update, {})]),
 }
 
 
