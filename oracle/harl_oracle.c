@@ -489,14 +489,10 @@ int oracle_gbdt_bin(const float *x, int64_t N, int32_t F, int64_t ldx, const flo
             uint8_t b = 0;
             if (f < F) {
                 const float v = x[f * ldx + r];
-                if (isnan(v)) {
-                    b = 255;
-                } else {
-                    int c = 0;
-                    for (int32_t i = 0; i < n_cuts[f]; ++i)
-                        if (cuts[f * cut_stride + i] <= v) ++c;
-                    b = (uint8_t)c;
-                }
+                int c = 0;
+                for (int32_t i = 0; i < n_cuts[f]; ++i)
+                    if (cuts[f * cut_stride + i] <= v) ++c;
+                b = isnan(v) ? (uint8_t)255 : (uint8_t)c;
             }
             bins[r * ld + f] = b;
         }
