@@ -317,6 +317,81 @@ int harl_track_eliminate(const float *d_adv, int32_t n, int32_t n_keep, int32_t 
                          const void *d_rows, int64_t row_bytes, void *d_rows_out, void *d_ws,
                          size_t ws_bytes, void *stream);
 
+/* ============================================================================================
+ * Refit of the cost model on measured programs (Algorithm 1: the top-K states are measured and
+ * the cost model is trained on (S^, P); Section 6.1 and Appendix A.2: XGBoost with Ansor's
+ * settings).  Histogram-based gradient boosting (Chen and Guestrin, KDD'16, Sections 3 and 3.4).
+ * ============================================================================================ */
+
+#define HARL_GBDT_MAX_DEPTH 12
+#define HARL_GBDT_MAX_CUTS 254
+#define HARL_GBDT_MAX_FEATURES 4096
+
+/*
+ * Feature binning.  Feature f of statement row r is d_feat[f*ld_feat + r] (the feature-major
+ * layout harl_score_round reads); its cut points are d_cuts[f*cut_stride + i], i < d_n_cuts[f]
+ * (strictly increasing, finite; d_n_cuts[f] is clamped to [0, min(254, cut_stride)]).
+ *   d_bins [n_rows][ld_bins] uint8 out: byte f < n_features is the number of cut points <= x,
+ *          255 for NaN (missing); bytes n_features .. ld_bins-1 are 0.
+ * ld_bins % 8 == 0, ld_bins >= n_features, d_bins 8-byte aligned; other arrays 4-byte aligned.
+ * n_rows == 0 is a no-op.  Exact.
+ */
+int harl_gbdt_bin(const float *d_feat, int64_t ld_feat, int32_t n_features, int32_t n_rows,
+                  const float *d_cuts, int32_t cut_stride, const int32_t *d_n_cuts, uint8_t *d_bins,
+                  int64_t ld_bins, void *stream);
+
+/* Boosting hyper-parameters (Ansor's cost model: max_depth 10, eta 0.2, gamma 0.001,
+ * min_child_weight 0; XGBoost's default reg_lambda 1). */
+typedef struct {
+    int32_t max_depth;       /* 1 .. HARL_GBDT_MAX_DEPTH                          */
+    double eta;              /* learning rate (shrinkage of the leaf weights)     */
+    double reg_lambda;       /* L2 regularisation of the leaf weights, > 0        */
+    double gamma;            /* minimum gain of a split, >= 0                      */
+    double min_child_weight; /* minimum hessian sum of a child, >= 0               */
+    double base_score;       /* added once to every program's prediction          */
+} harl_gbdt_params;
+
+/* Bytes of device workspace harl_gbdt_round needs. */
+size_t harl_gbdt_round_workspace_size(const harl_gbdt_params *prm, int32_t n_features, int32_t n_rows,
+                                      int32_t n_prog);
+
+/*
+ * One boosting round on measured programs under the pack-sum squared error: program p's
+ * prediction is s_p = base_score + the sum of its statements' margins, the objective
+ * 1/2 sum_p w_p (s_p - y_p)^2, so each statement row of p carries gradient w_p (s_p - y_p) and
+ * hessian w_p.  The tree grows depth-wise: a node takes the split (feature f, threshold index t
+ * in 1 .. n_cuts[f], missing direction) of largest gain
+ *   GL^2/(HL + lambda) + GR^2/(HR + lambda) - G^2/(H + lambda)
+ * (ties: lowest f, then lowest t, then missing-left) among those whose children's hessian sums
+ * reach min_child_weight, and splits iff that gain exceeds gamma; a leaf holds
+ * -(G / (H + lambda)) * eta.  Gradient and hessian sums are exact: each program's value is rounded
+ * once to the grid 2^-e, e = 62 - ceil(log2 n_rows) - E for the largest magnitude m 2^E
+ * (1/2 <= m < 1), and summed as 64-bit integers; gains are fp64.  The result does not depend on
+ * scheduling.
+ *   d_bins     [n_rows][ld_bins] from harl_gbdt_bin (bytes <= n_cuts or 255); 8-byte aligned,
+ *              ld_bins % 8 == 0.
+ *   d_cuts, cut_stride, d_n_cuts   the cut points the bins were made with (thresholds).
+ *   d_prog_ptr [n_prog+1] int32: program p owns rows [d_prog_ptr[p], d_prog_ptr[p+1]),
+ *              0 = d_prog_ptr[0] <= ... <= d_prog_ptr[n_prog] = n_rows.
+ *   d_label, d_weight [n_prog] fp32: measured target and weight (finite, weight >= 0).
+ *   d_margin   [n_rows] fp32 in/out: each row's sum over the trees so far; the new tree's leaf
+ *              value is added (fp32).
+ *   d_feature, d_threshold, d_left, d_right, d_default_left, d_leaf_value: the new tree, node
+ *              arrays of 2^(max_depth+1) - 1 entries (the harl_ensemble_desc fields), children of
+ *              node k at 2k+1 and 2k+2; a split node sends x < threshold left; nodes the tree does
+ *              not reach hold feature -1 and leaf value 0.
+ *   d_ws, ws_bytes: at least harl_gbdt_round_workspace_size() bytes, 256-byte aligned; contents
+ *              on entry do not matter.
+ * n_rows == 0 gives a single leaf of value -0.  Errors: HARL_E_INVALID_ARG for sizes, parameters
+ * or alignment out of range, HARL_E_WORKSPACE for a short workspace.
+ */
+int harl_gbdt_round(const harl_gbdt_params *prm, const uint8_t *d_bins, int64_t ld_bins,
+                    int32_t n_features, int32_t n_rows, const float *d_cuts, int32_t cut_stride,
+                    const int32_t *d_n_cuts, const int32_t *d_prog_ptr, int32_t n_prog,
+                    const float *d_label, const float *d_weight, float *d_margin, int32_t *d_feature,
+                    float *d_threshold, int32_t *d_left, int32_t *d_right, uint8_t *d_default_left,
+                    float *d_leaf_value, void *d_ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,6 +6,8 @@
 #include <mutex>
 #include <string>
 
+#include <cmath>
+
 #include "internal.hpp"
 
 namespace harl {
@@ -265,6 +267,66 @@ int harl_track_eliminate(const float *d_adv, int32_t n, int32_t n_keep, int32_t 
     }
     return harl::track_eliminate_launch(d_adv, n, n_keep, d_keep_index, d_rows, row_bytes, d_rows_out, d_ws,
                                         static_cast<hipStream_t>(stream));
+}
+
+static int gbdt_check_params(const harl_gbdt_params *p) {
+    if (!p) return fail(HARL_E_INVALID_ARG, "harl_gbdt: null parameters");
+    if (p->max_depth < 1 || p->max_depth > HARL_GBDT_MAX_DEPTH)
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt: max_depth out of range");
+    if (!(p->reg_lambda > 0.0) || !(p->gamma >= 0.0) || !(p->min_child_weight >= 0.0) || !std::isfinite(p->eta) ||
+        !std::isfinite(p->reg_lambda) || !std::isfinite(p->gamma) || !std::isfinite(p->min_child_weight) ||
+        !std::isfinite(p->base_score))
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt: hyper-parameter out of range");
+    return HARL_OK;
+}
+
+static bool gbdt_sizes_ok(int32_t F, int32_t N, int32_t P) {
+    return F >= 1 && F <= HARL_GBDT_MAX_FEATURES && N >= 0 && N <= (1 << 30) && P >= 0 && P <= (1 << 30);
+}
+
+int harl_gbdt_bin(const float *d_feat, int64_t ld_feat, int32_t n_features, int32_t n_rows, const float *d_cuts,
+                  int32_t cut_stride, const int32_t *d_n_cuts, uint8_t *d_bins, int64_t ld_bins, void *stream) {
+    if (!gbdt_sizes_ok(n_features, n_rows, 0)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: sizes out of range");
+    if (ld_feat < n_rows || ld_bins < n_features || ld_bins % 8 != 0 || cut_stride < 1)
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: need ld_feat >= n_rows, ld_bins >= n_features, ld_bins % 8 == 0, cut_stride >= 1");
+    if (n_rows == 0) return HARL_OK;
+    if (!d_feat || !aligned(d_feat, 4) || !d_cuts || !aligned(d_cuts, 4) || !d_n_cuts || !aligned(d_n_cuts, 4))
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: null or misaligned input");
+    if (!d_bins || !aligned(d_bins, 8)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: bins null or not 8-byte aligned");
+    return harl::gbdt_bin_launch(d_feat, ld_feat, n_features, n_rows, d_cuts, cut_stride, d_n_cuts, d_bins, ld_bins,
+                                 static_cast<hipStream_t>(stream));
+}
+
+size_t harl_gbdt_round_workspace_size(const harl_gbdt_params *prm, int32_t n_features, int32_t n_rows, int32_t n_prog) {
+    if (gbdt_check_params(prm) != HARL_OK || !gbdt_sizes_ok(n_features, n_rows, n_prog)) return 0;
+    return harl::gbdt_ws_bytes(n_features, n_rows, n_prog, prm->max_depth);
+}
+
+int harl_gbdt_round(const harl_gbdt_params *prm, const uint8_t *d_bins, int64_t ld_bins, int32_t n_features,
+                    int32_t n_rows, const float *d_cuts, int32_t cut_stride, const int32_t *d_n_cuts,
+                    const int32_t *d_prog_ptr, int32_t n_prog, const float *d_label, const float *d_weight,
+                    float *d_margin, int32_t *d_feature, float *d_threshold, int32_t *d_left, int32_t *d_right,
+                    uint8_t *d_default_left, float *d_leaf_value, void *d_ws, size_t ws_bytes, void *stream) {
+    if (const int rc = gbdt_check_params(prm)) return rc;
+    if (!gbdt_sizes_ok(n_features, n_rows, n_prog)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: sizes out of range");
+    if (ld_bins < n_features || ld_bins % 8 != 0 || cut_stride < 1)
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: need ld_bins >= n_features, ld_bins % 8 == 0, cut_stride >= 1");
+    if (n_rows > 0 && (!d_bins || !aligned(d_bins, 8)))
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: bins null or not 8-byte aligned");
+    const void *in4[] = {d_cuts, d_n_cuts, d_prog_ptr, d_feature, d_threshold, d_left, d_right, d_leaf_value};
+    for (const void *p : in4)
+        if (!p || !aligned(p, 4)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: null or misaligned array");
+    if (!d_default_left) return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: null default_left");
+    if (n_prog > 0 && (!d_label || !aligned(d_label, 4) || !d_weight || !aligned(d_weight, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: null or misaligned label / weight");
+    if (n_rows > 0 && (!d_margin || !aligned(d_margin, 4)))
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: null or misaligned margin");
+    if (!d_ws || !aligned(d_ws, 256)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: workspace null or not 256-byte aligned");
+    if (ws_bytes < harl::gbdt_ws_bytes(n_features, n_rows, n_prog, prm->max_depth))
+        return fail(HARL_E_WORKSPACE, "harl_gbdt_round: workspace smaller than harl_gbdt_round_workspace_size()");
+    return harl::gbdt_round_launch(prm, d_bins, ld_bins, n_features, n_rows, d_cuts, cut_stride, d_n_cuts, d_prog_ptr,
+                                   n_prog, d_label, d_weight, d_margin, d_feature, d_threshold, d_left, d_right,
+                                   d_default_left, d_leaf_value, d_ws, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

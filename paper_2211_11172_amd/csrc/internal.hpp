@@ -104,4 +104,13 @@ int policy_select_launch(const float *logits, int32_t B, int32_t a, const int32_
 int track_eliminate_launch(const float *adv, int32_t n, int32_t n_keep, int32_t *keep_index, const void *rows,
                            int64_t row_bytes, void *rows_out, void *ws, hipStream_t stream);
 
+size_t gbdt_ws_bytes(int32_t F, int32_t N, int32_t P, int32_t depth);
+int gbdt_bin_launch(const float *x, int64_t ldx, int32_t F, int32_t N, const float *cuts, int32_t cut_stride,
+                    const int32_t *n_cuts, uint8_t *bins, int64_t ld, hipStream_t stream);
+int gbdt_round_launch(const harl_gbdt_params *prm, const uint8_t *bins, int64_t ld, int32_t F, int32_t N,
+                      const float *cuts, int32_t cut_stride, const int32_t *n_cuts, const int32_t *prog_ptr,
+                      int32_t P, const float *label, const float *weight, float *margin, int32_t *feature,
+                      float *threshold, int32_t *left, int32_t *right, uint8_t *default_left, float *leaf_value,
+                      void *ws, hipStream_t stream);
+
 }  // namespace harl

@@ -33,7 +33,11 @@ EXPORTS = (
     "harl_policy_select",
     "harl_ppo_param_count", "harl_ppo_workspace_size", "harl_ppo_update",
     "harl_track_advantage", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
+    "harl_gbdt_bin", "harl_gbdt_round_workspace_size", "harl_gbdt_round",
 )
+HARL_GBDT_MAX_DEPTH = 12
+HARL_GBDT_MAX_CUTS = 254
+HARL_GBDT_MAX_FEATURES = 4096
 
 
 class PpoConfig(ctypes.Structure):
@@ -53,6 +57,19 @@ def ppo_config(s: int, h1: int, h2: int, a: int, segs, clip_eps=0.2, w_value=0.5
     c.clip_eps, c.w_value, c.w_entropy = clip_eps, w_value, w_entropy
     c.lr_actor, c.lr_critic, c.beta1, c.beta2, c.adam_eps = lr_actor, lr_critic, beta1, beta2, adam_eps
     return c
+
+
+class GbdtParams(ctypes.Structure):
+    _fields_ = [("max_depth", ctypes.c_int32), ("eta", ctypes.c_double), ("reg_lambda", ctypes.c_double),
+                ("gamma", ctypes.c_double), ("min_child_weight", ctypes.c_double), ("base_score", ctypes.c_double)]
+
+
+def gbdt_params(max_depth=10, eta=0.2, reg_lambda=1.0, gamma=0.001, min_child_weight=0.0, base_score=0.0) -> GbdtParams:
+    """Boosting hyper-parameters; the defaults are Ansor's cost-model settings with XGBoost's lambda."""
+    p = GbdtParams()
+    p.max_depth, p.eta, p.reg_lambda, p.gamma, p.min_child_weight, p.base_score = (
+        max_depth, eta, reg_lambda, gamma, min_child_weight, base_score)
+    return p
 
 
 class HarlError(RuntimeError):
@@ -112,6 +129,10 @@ def load():
                 "harl_track_advantage": ([P, P, P, P, i32, ctypes.c_float, ctypes.c_float, P, P, P], ctypes.c_int),
                 "harl_track_eliminate_workspace_size": ([i32], sz),
                 "harl_track_eliminate": ([P, i32, i32, P, P, i64, P, P, sz, P], ctypes.c_int),
+                "harl_gbdt_bin": ([P, i64, i32, i32, P, i32, P, P, i64, P], ctypes.c_int),
+                "harl_gbdt_round_workspace_size": ([P, i32, i32, i32], sz),
+                "harl_gbdt_round": ([P, P, i64, i32, i32, P, i32, P, P, i32, P, P, P, P, P, P, P, P, P, P, sz, P],
+                                    ctypes.c_int),
             }
             for name, (args, res) in sig.items():
                 f = getattr(lib, name)
@@ -301,3 +322,25 @@ def eliminate_keep_count(n: int, rho: float = 0.5) -> int:
     """Tracks left after one adaptive-stopping elimination of proportion rho: floor(rho * n) are
     dropped."""
     return n - int(rho * n // 1)
+
+
+# ------------------------------------------------------------------------------------------------
+# cost-model refit
+# ------------------------------------------------------------------------------------------------
+def harl_gbdt_bin(feat, ld_feat: int, n_features: int, n_rows: int, cuts, cut_stride: int, n_cuts, bins,
+                  ld_bins: int, stream=None):
+    _check(load().harl_gbdt_bin(_ptr(feat), ld_feat, n_features, n_rows, _ptr(cuts), cut_stride, _ptr(n_cuts),
+                                _ptr(bins), ld_bins, _stream(stream)), "harl_gbdt_bin")
+
+
+def harl_gbdt_round_workspace_size(prm: GbdtParams, n_features: int, n_rows: int, n_prog: int) -> int:
+    return int(load().harl_gbdt_round_workspace_size(ctypes.byref(prm), n_features, n_rows, n_prog))
+
+
+def harl_gbdt_round(prm: GbdtParams, bins, ld_bins: int, n_features: int, n_rows: int, cuts, cut_stride: int, n_cuts,
+                    prog_ptr, n_prog: int, label, weight, margin, feature, threshold, left, right, default_left,
+                    leaf_value, ws, ws_bytes: int, stream=None):
+    _check(load().harl_gbdt_round(ctypes.byref(prm), _ptr(bins), ld_bins, n_features, n_rows, _ptr(cuts), cut_stride,
+                                  _ptr(n_cuts), _ptr(prog_ptr), n_prog, _ptr(label), _ptr(weight), _ptr(margin),
+                                  _ptr(feature), _ptr(threshold), _ptr(left), _ptr(right), _ptr(default_left),
+                                  _ptr(leaf_value), _ptr(ws), ws_bytes, _stream(stream)), "harl_gbdt_round")

@@ -11,6 +11,7 @@ from .gen import (  # noqa: F401
     gen_policy,
     gen_states,
     gen_track_step,
+    gen_measured,
     gen_features,
     gen_prog_ptr,
     bf16_bits_from_f32,

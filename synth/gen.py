@@ -20,6 +20,8 @@ Every array comes from its own numpy PCG64 stream keyed by
  12   track scores C(s)           yes
  13   track score changes         yes
  14   track critic values         yes
+ 15   measured-run noise          yes
+ 16   cut-point calibration rows
 ====  ==========================  =========
 
 Nothing here computes a score, an activation or a ranking; both the oracle and the HIP path
@@ -35,7 +37,8 @@ from .configs import RoundConfig
 
 S_COUNTS, S_FCAT, S_FMAG, S_SPLITF, S_THRQ, S_DEFDIR, S_LEAF, S_CALIB, S_STATES, S_W, S_B = range(1, 12)
 S_TRACK_C, S_TRACK_DC, S_TRACK_V = 12, 13, 14
-_BATCH_STREAMS = {S_COUNTS, S_FCAT, S_FMAG, S_STATES, S_TRACK_C, S_TRACK_DC, S_TRACK_V}
+S_MEAS_NOISE, S_MEAS_CUTS = 15, 16
+_BATCH_STREAMS = {S_COUNTS, S_FCAT, S_FMAG, S_STATES, S_TRACK_C, S_TRACK_DC, S_TRACK_V, S_MEAS_NOISE}
 
 
 def _rng(cfg: RoundConfig, stream: int, batch: int = 0) -> np.random.Generator:
@@ -231,6 +234,43 @@ def gen_track_step(cfg: RoundConfig, batch: int = 0, n: int | None = None) -> di
         c1 = (c0 + dc).astype(np.float32)
         v = rv.standard_normal((2, n)).astype(np.float32)
     return dict(c_prev=c0, c_next=c1, v_prev=v[0].copy(), v_next=v[1].copy())
+
+
+def gen_measured(cfg: RoundConfig, n_cuts: int = 254, batch: int = 0) -> dict:
+    """Measured programs for a refit of the cost model: the batch's programs and statement features
+    (as gen_batch: prog_ptr, features [F][n_rows]), a measured throughput per program and per-feature
+    cut points.
+
+    A statement's synthetic run time is 0.1 + log10(1 + |x3|) + 0.5 [x17 > 1] + 0.25 log10(1 + |x101|)
+    (missing values count 0; feature ids taken modulo F), a program's is the sum over its statements
+    times a log-normal factor exp(N(0, 0.1^2)); label = throughput / the largest throughput, and
+    weight = label (Ansor weights each program's squared error by its normalised throughput).
+    Cut points: per feature, the distinct values at n_cuts + 1 equally spaced ranks of a sorted
+    calibration sample of non-missing values (at most n_cuts of them, strictly increasing), in
+    cuts [F][n_cuts] (unused tail 0) with counts n_cuts_f [F]."""
+    ptr = gen_prog_ptr(cfg, batch)
+    n_rows = int(ptr[-1])
+    X = gen_features(cfg, n_rows, batch)
+    F = cfg.n_features
+    xz = np.nan_to_num(X.astype(np.float64), nan=0.0)
+    row_t = 0.1 + np.log10(1 + np.abs(xz[3 % F])) + 0.5 * (xz[17 % F] > 1) + 0.25 * np.log10(1 + np.abs(xz[101 % F]))
+    prog_t = np.add.reduceat(row_t, ptr[:-1]) if n_rows else np.zeros(cfg.n_prog)
+    prog_t[np.diff(ptr) == 0] = 0.1
+    prog_t *= np.exp(_rng(cfg, S_MEAS_NOISE, batch).normal(0.0, 0.1, cfg.n_prog))
+    thr = 1.0 / prog_t
+    label = (thr / thr.max()).astype(np.float32)
+    rcal = _rng(cfg, S_MEAS_CUTS)
+    cal_cfg = cfg.with_(p_nan=0.0)
+    calib = _draw_values(rcal.random((F, cfg.n_calib)), rcal.random((F, cfg.n_calib)), cal_cfg)
+    cuts = np.zeros((F, max(n_cuts, 1)), np.float32)
+    counts = np.zeros(F, np.int32)
+    ranks = (np.arange(1, n_cuts + 1) * cfg.n_calib) // (n_cuts + 1)
+    for f in range(F):
+        v = np.unique(np.sort(calib[f])[ranks])
+        counts[f] = v.size
+        cuts[f, :v.size] = v
+    return dict(prog_ptr=ptr, n_rows=n_rows, features=X, label=label, weight=label.copy(), cuts=cuts,
+                n_cuts=counts)
 
 
 def gen_batch(cfg: RoundConfig, batch: int = 0, ld_pad: int = 0) -> dict:

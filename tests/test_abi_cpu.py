@@ -173,3 +173,29 @@ def test_ppo_argument_errors():
     assert up(cfg, wsb=64) == harl.HARL_E_WORKSPACE
     lr = harl.ppo_config(64, 256, 256, 26, [0, 26], beta1=1.0)
     assert up(lr) == harl.HARL_E_INVALID_ARG
+
+
+def test_gbdt_argument_errors():
+    prm = harl.gbdt_params()
+    assert harl.harl_gbdt_round_workspace_size(prm, 164, 65536, 2048) > 65536 * 40
+    for bad in (harl.gbdt_params(max_depth=0), harl.gbdt_params(max_depth=13), harl.gbdt_params(reg_lambda=0.0),
+                harl.gbdt_params(gamma=-1.0), harl.gbdt_params(min_child_weight=float("nan"))):
+        assert harl.harl_gbdt_round_workspace_size(bad, 164, 100, 10) == 0
+    assert harl.harl_gbdt_round_workspace_size(prm, 0, 100, 10) == 0
+    b = lambda ldf=100, F=164, N=100, ldb=168, bins=0x1000, stride=16: _status(
+        "harl_gbdt_bin", 0x2000, ldf, F, N, 0x3000, stride, 0x4000, bins, ldb, None)
+    assert b(ldf=99) == harl.HARL_E_INVALID_ARG
+    assert b(ldb=164) == harl.HARL_E_INVALID_ARG  # not a multiple of 8
+    assert b(ldb=160) == harl.HARL_E_INVALID_ARG  # shorter than a row
+    assert b(bins=0x1004) == harl.HARL_E_INVALID_ARG
+    assert b(stride=0) == harl.HARL_E_INVALID_ARG
+    assert b(N=0) == harl.HARL_OK
+    r = lambda p=prm, ldb=168, bins=0x1000, ws=0x5000, wsb=1 << 30, N=100, P=10, label=0x6000: _status(
+        "harl_gbdt_round", ctypes.byref(p), bins, ldb, 164, N, 0x3000, 16, 0x4000, 0x7000, P, label, 0x6000, 0x8000,
+        0x9000, 0x9000, 0x9000, 0x9000, 0x9000, 0x9000, ws, wsb, None)
+    assert r(p=harl.gbdt_params(max_depth=13)) == harl.HARL_E_INVALID_ARG
+    assert r(ldb=164) == harl.HARL_E_INVALID_ARG
+    assert r(bins=0x1004) == harl.HARL_E_INVALID_ARG
+    assert r(label=None) == harl.HARL_E_INVALID_ARG
+    assert r(ws=0x5001) == harl.HARL_E_INVALID_ARG
+    assert r(wsb=64) == harl.HARL_E_WORKSPACE
