@@ -80,6 +80,11 @@ def parse():
     ap.add_argument("--ppo", action="store_true",
                     help="one PPO update (harl_ppo_update) of the standard round's fp32 network with a 26-action "
                          "per-type head on 4,096 and 65,536 transitions; prints one JSON line and exits")
+    ap.add_argument("--refit", action="store_true",
+                    help="one boosting round of the cost-model refit (harl_gbdt_round, Ansor's settings: depth 10, "
+                         "eta 0.2, gamma 0.001) on 4,096 measured programs (the standard round's statements, 66,923 "
+                         "rows) and on 65,536 (the throughput round's, 2.13 M rows), 164 features binned to at most "
+                         "255 bins (harl_gbdt_bin, timed on its own); prints one JSON line and exits")
     ap.add_argument("--two-streams", action="store_true",
                     help="run the policy on a second stream after scoring, beside top-K (default: the "
                          "three calls in turn on one stream, which measured faster on the standard round)")
@@ -400,6 +405,85 @@ def ppo_bench(args):
           flush=True)
 
 
+def refit_bench(args):
+    """Time harl_gbdt_bin and one harl_gbdt_round (graphs of `steps` calls, HIP events)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2211_11172_amd import harl
+    from synth import gen_measured, get_config
+
+    dev = torch.device("cuda:0")
+    main_stream = torch.cuda.current_stream(dev)
+    prm = harl.gbdt_params(**{k: v for k, v in oracle.GBDT_DEFAULTS.items()})
+    results = []
+    for name in ("standard", "throughput"):
+        m = gen_measured(get_config(name), n_cuts=254)
+        N, P, F = m["n_rows"], len(m["prog_ptr"]) - 1, 164
+        n_fg, ld = (F + 7) // 8, m["n_rows"]
+        d = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+        X, cuts, nc, ptr = d(m["features"]), d(m["cuts"]), d(m["n_cuts"]), d(m["prog_ptr"])
+        lab, wt = d(m["label"]), d(m["weight"])
+        bins = torch.empty((n_fg, ld, 8), dtype=torch.uint8, device=dev)
+        margin = torch.zeros(N, device=dev)
+        n_nodes = (1 << (prm.max_depth + 1)) - 1
+        tree = [torch.empty(n_nodes, dtype=t, device=dev) for t in
+                (torch.int32, torch.float32, torch.int32, torch.int32, torch.uint8, torch.float32)]
+        wsb = harl.harl_gbdt_round_workspace_size(prm, F, N, P)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        fbin = lambda: harl.harl_gbdt_bin(X, N, F, N, cuts, cuts.shape[1], nc, bins, ld)
+        fround = lambda: harl.harl_gbdt_round(prm, bins, ld, F, N, cuts, cuts.shape[1], nc, ptr, P, lab, wt, margin,
+                                              *tree, ws, wsb)
+
+        def timed(fn, steps):
+            for _ in range(max(args.warmup, 1)):
+                fn()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(steps):
+                    fn()
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(main_stream)
+            g.replay()
+            e1.record(main_stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / steps * 1e3
+
+        steps = max(1, min(args.steps, 20 if N < 1_000_000 else 5))
+        us_bin = timed(fbin, steps)
+        us_round = timed(fround, steps)
+        splits = int((tree[0] >= 0).sum().item())
+        # bytes every depth level must stream at least once: the rows' bins, integer gradient pair
+        # and position (N (ld + 16 + 4)); plus the binning's read of the features and write of the bins
+        level_bytes = N * (n_fg * 8 + 16 + 4)
+        entry = {"measured_programs": P, "rows": N, "us_per_round": us_round, "us_bin": us_bin, "splits": splits,
+                 "rows_per_s": N / (us_round * 1e-6), "level_bytes": level_bytes,
+                 "stream_GBps": prm.max_depth * level_bytes / (us_round * 1e-6) / 1e9,
+                 "bin_GBps": (N * F * 4 + N * n_fg * 8) / (us_bin * 1e-6) / 1e9}
+        if not args.no_cpu_baseline and name == "standard":
+            hb = bins.cpu().numpy().transpose(1, 0, 2).reshape(N, n_fg * 8)  # the oracle's row-major layout
+            t0 = time.perf_counter()
+            reps = 0
+            while time.perf_counter() - t0 < 3.0 or reps == 0:
+                oracle.gbdt_round(hb, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"],
+                                  np.zeros(N, np.float32), **oracle.GBDT_DEFAULTS)
+                reps += 1
+            el = time.perf_counter() - t0
+            entry["cpu_baseline"] = {"value": el / reps * 1e6, "unit": "us per round", "cores": 1, "kind": "oracle",
+                                     "sample": "%d rounds of the %d-row set in %.1f s" % (reps, N, el)}
+        print("refit %s: %d rows, bin %.1f us, round %.1f us (%d splits)" % (name, N, us_bin, us_round, splits),
+              file=sys.stderr, flush=True)
+        results.append(entry)
+        del X, bins, ws
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "cost-model refit: one boosting round (harl_gbdt_round)", "unit": "us per round",
+                      "settings": "depth 10, eta 0.2, gamma 0.001, lambda 1, 164 features, <= 255 bins",
+                      "steps": args.steps, "results": results}), flush=True)
+
+
 def oracle_threads():
     """Threads numpy's BLAS may use for the fp64 oracle of the PPO update."""
     return len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
@@ -422,6 +506,9 @@ def main():
         return
     if args.ppo:
         ppo_bench(args)
+        return
+    if args.refit:
+        refit_bench(args)
         return
     import numpy as np
     import torch

@@ -331,10 +331,13 @@ int harl_track_eliminate(const float *d_adv, int32_t n, int32_t n_keep, int32_t 
  * Feature binning.  Feature f of statement row r is d_feat[f*ld_feat + r] (the feature-major
  * layout harl_score_round reads); its cut points are d_cuts[f*cut_stride + i], i < d_n_cuts[f]
  * (strictly increasing, finite; d_n_cuts[f] is clamped to [0, min(254, cut_stride)]).
- *   d_bins [n_rows][ld_bins] uint8 out: byte f < n_features is the number of cut points <= x,
- *          255 for NaN (missing); bytes n_features .. ld_bins-1 are 0.
- * ld_bins % 8 == 0, ld_bins >= n_features, d_bins 8-byte aligned; other arrays 4-byte aligned.
- * n_rows == 0 is a no-op.  Exact.
+ *   d_bins  out, in groups of 8 features: the bin of feature f of row r is the byte
+ *           d_bins[((f/8)*ld_bins + r)*8 + f%8], the number of cut points <= x, or 255 for NaN
+ *           (missing); the bytes of features n_features .. 8*ceil(n_features/8)-1 are 0.  The
+ *           array holds ceil(n_features/8) planes of ld_bins rows of 8 bytes; rows >= n_rows are
+ *           not written.
+ * ld_bins >= n_rows; d_bins 8-byte aligned; other arrays 4-byte aligned.  n_rows == 0 is a
+ * no-op.  Exact.
  */
 int harl_gbdt_bin(const float *d_feat, int64_t ld_feat, int32_t n_features, int32_t n_rows,
                   const float *d_cuts, int32_t cut_stride, const int32_t *d_n_cuts, uint8_t *d_bins,
@@ -368,8 +371,8 @@ size_t harl_gbdt_round_workspace_size(const harl_gbdt_params *prm, int32_t n_fea
  * once to the grid 2^-e, e = 62 - ceil(log2 n_rows) - E for the largest magnitude m 2^E
  * (1/2 <= m < 1), and summed as 64-bit integers; gains are fp64.  The result does not depend on
  * scheduling.
- *   d_bins     [n_rows][ld_bins] from harl_gbdt_bin (bytes <= n_cuts or 255); 8-byte aligned,
- *              ld_bins % 8 == 0.
+ *   d_bins, ld_bins  the bins in harl_gbdt_bin's layout (each byte <= its feature's n_cuts, or
+ *              255); 8-byte aligned, ld_bins >= n_rows.
  *   d_cuts, cut_stride, d_n_cuts   the cut points the bins were made with (thresholds).
  *   d_prog_ptr [n_prog+1] int32: program p owns rows [d_prog_ptr[p], d_prog_ptr[p+1]),
  *              0 = d_prog_ptr[0] <= ... <= d_prog_ptr[n_prog] = n_rows.

@@ -287,8 +287,8 @@ static bool gbdt_sizes_ok(int32_t F, int32_t N, int32_t P) {
 int harl_gbdt_bin(const float *d_feat, int64_t ld_feat, int32_t n_features, int32_t n_rows, const float *d_cuts,
                   int32_t cut_stride, const int32_t *d_n_cuts, uint8_t *d_bins, int64_t ld_bins, void *stream) {
     if (!gbdt_sizes_ok(n_features, n_rows, 0)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: sizes out of range");
-    if (ld_feat < n_rows || ld_bins < n_features || ld_bins % 8 != 0 || cut_stride < 1)
-        return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: need ld_feat >= n_rows, ld_bins >= n_features, ld_bins % 8 == 0, cut_stride >= 1");
+    if (ld_feat < n_rows || ld_bins < n_rows || cut_stride < 1)
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: need ld_feat >= n_rows, ld_bins >= n_rows, cut_stride >= 1");
     if (n_rows == 0) return HARL_OK;
     if (!d_feat || !aligned(d_feat, 4) || !d_cuts || !aligned(d_cuts, 4) || !d_n_cuts || !aligned(d_n_cuts, 4))
         return fail(HARL_E_INVALID_ARG, "harl_gbdt_bin: null or misaligned input");
@@ -309,8 +309,8 @@ int harl_gbdt_round(const harl_gbdt_params *prm, const uint8_t *d_bins, int64_t 
                     uint8_t *d_default_left, float *d_leaf_value, void *d_ws, size_t ws_bytes, void *stream) {
     if (const int rc = gbdt_check_params(prm)) return rc;
     if (!gbdt_sizes_ok(n_features, n_rows, n_prog)) return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: sizes out of range");
-    if (ld_bins < n_features || ld_bins % 8 != 0 || cut_stride < 1)
-        return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: need ld_bins >= n_features, ld_bins % 8 == 0, cut_stride >= 1");
+    if (ld_bins < n_rows || cut_stride < 1)
+        return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: need ld_bins >= n_rows, cut_stride >= 1");
     if (n_rows > 0 && (!d_bins || !aligned(d_bins, 8)))
         return fail(HARL_E_INVALID_ARG, "harl_gbdt_round: bins null or not 8-byte aligned");
     const void *in4[] = {d_cuts, d_n_cuts, d_prog_ptr, d_feature, d_threshold, d_left, d_right, d_leaf_value};

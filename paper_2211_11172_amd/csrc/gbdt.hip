@@ -5,7 +5,9 @@
 // gain, leaf weight and learned missing direction follow Chen and Guestrin (KDD'16, Sections 3
 // and 3.4).
 //
-//   k_gb_bin        bins[r][f] = number of cut points <= x (upper bound), 255 for NaN
+//   k_gb_bin        bin of feature f of row r = number of cut points <= x (upper bound), 255 for NaN,
+//                   stored in 8-feature groups: byte ((f / 8) ld + r) 8 + f % 8, so that a
+//                   workgroup of one group reads its rows' 8 bytes from one contiguous plane
 //   k_gb_prog_grad  per program: s_p (fp64, statements in order), g_p = w_p (s_p - y_p), h_p = w_p,
 //                   per-block maxima of |g|, |h|
 //   k_gb_exps       the fixed-point exponents: |v 2^e| <= 2^(62 - ceil(log2 N)), so sums of N rows
@@ -13,14 +15,17 @@
 //   k_gb_row_q      each statement row's integer gradient and hessian; rows start in the root
 //   per depth d < max_depth (rows kept grouped by node in `order`):
 //     k_gb_level    one workgroup: node ranges from the parent's partition, the chunk list
-//                   (kChunk rows per chunk) and the shared-histogram slots of multi-chunk nodes
+//                   (2048 rows per chunk, more for large sets) and the shared-histogram slots
+//                   of multi-chunk nodes
 //     k_gb_hist     workgroup = (chunk, 8 features): a [2][8][256] int64 histogram in LDS (ds_add
-//                   of integers); a one-chunk node evaluates its splits at once, a larger one adds
-//                   its histogram into the node's slot (integer atomics: the sum is exact)
-//     k_gb_split    the slot nodes' split evaluation from the shared histograms
+//                   of integers; the lanes of one add instruction are spread over the 8 features,
+//                   so at most 8 meet on one bin; the bin of 0.0 is the total minus the others); a
+//                   one-chunk node evaluates its splits at once, a larger one stores its partial
+//     k_gb_reduce   a multi-chunk node's histogram: its partials summed in chunk order
+//     k_gb_split    the multi-chunk nodes' split evaluation
 //     k_gb_decide   per node: best over feature groups, split or leaf, tree arrays, children sums
 //     k_gb_flags / scan / k_gb_scatter   stable partition of each split node's rows
-//   k_gb_leaves     the last level's leaves;  k_gb_margin  margin[r] += leaf of the row
+//   k_gb_finish     the last level's leaves and margin[r] += the weight of the row's leaf
 //
 // Split evaluation (thread = (feature, 8 consecutive bins)): an int64 prefix over bins gives GL,
 // HL for every threshold index t; the gain GL^2/(HL+l) + GR^2/(HR+l) - G^2/(H+l) is fp64 with
@@ -43,7 +48,10 @@ constexpr int kThreads = 256;
 constexpr int kChunk = 2048;        // rows per histogram workgroup
 constexpr int kGroup = 8;           // features per histogram workgroup (one 8-byte load per row)
 constexpr int kBins = 256;          // bin 255 holds the missing values
-constexpr int kScanBlock = 2048;    // flags per scan block
+constexpr int kBinStride = 257;     // int64 words per (feature, G|H) histogram row: odd, so that
+                                    // the 8 features' rows fall on different LDS banks
+constexpr int kHistWords = 2 * kGroup * kBinStride;
+constexpr int kScanBlock = kThreads; // flags per scan block (one per thread)
 
 struct Params {
     double eta, lambda, gamma, mcw, base;
@@ -65,8 +73,12 @@ struct Ws {
     int32_t *start, *cnt, *alive, *sf, *st, *sd;             // per heap node
     int64_t *Gt, *Ht;                                        // per heap node
     int32_t *cp, *slot, *slot_node, *lvl;                    // level: [L+1], [L], [S], {chunks, slots}
+    int32_t *zb;                                             // [F] the bin of 0.0 per feature
+    int32_t *pbase;                                          // [L] first partial of a multi-chunk node
+    int64_t *part;                                           // [Pmax][n_fg][2][8][kBinStride]
+    int pmax;
     Best *best;                                              // [L][n_fg]
-    int64_t *hist;                                           // [S][n_fg][2][8][256]
+    int64_t *hist;                                           // [S][n_fg][2][8][kBinStride]
 };
 
 __device__ __forceinline__ int ceil_log2(int64_t n) {
@@ -119,7 +131,7 @@ __global__ __launch_bounds__(kThreads) void k_gb_bin(const float *__restrict__ x
         const uint64_t b = v != v ? 255u : (uint64_t)lo;
         word |= b << (8 * j);
     }
-    *reinterpret_cast<uint64_t *>(bins + (int64_t)r * ld + (int64_t)g * kGroup) = word;
+    *reinterpret_cast<uint64_t *>(bins + ((int64_t)g * ld + r) * kGroup) = word;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -202,9 +214,10 @@ __global__ __launch_bounds__(kThreads) void k_gb_row_q(const int32_t *__restrict
 }
 
 // tree arrays to unreached-node defaults, node state cleared, rows in the root
-__global__ __launch_bounds__(kThreads) void k_gb_init(Ws w, int n_nodes, int N, int32_t *feature, float *threshold,
-                                                      int32_t *left, int32_t *right, uint8_t *default_left,
-                                                      float *leaf_value) {
+__global__ __launch_bounds__(kThreads) void k_gb_init(Ws w, int n_nodes, int N, int F, const float *__restrict__ cuts,
+                                                      int cut_stride, const int32_t *__restrict__ n_cuts,
+                                                      int32_t *feature, float *threshold, int32_t *left,
+                                                      int32_t *right, uint8_t *default_left, float *leaf_value) {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i < n_nodes) {
         feature[i] = -1;
@@ -224,6 +237,16 @@ __global__ __launch_bounds__(kThreads) void k_gb_init(Ws w, int n_nodes, int N, 
         w.order[i] = (int32_t)i;
         w.nid[i] = 0;
     }
+    if (i < F) {  // the bin of 0.0: the number of cut points <= 0
+        const float *cf = cuts + i * cut_stride;
+        int lo = 0, hi = clamp_cuts(n_cuts, (int)i, cut_stride);
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (cf[mid] <= 0.f) lo = mid + 1;
+            else hi = mid;
+        }
+        w.zb[i] = lo;
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -232,12 +255,12 @@ __global__ __launch_bounds__(kThreads) void k_gb_init(Ws w, int n_nodes, int N, 
 
 // Node ranges of level d from the parents' partition (X is the previous level's scan), the chunk
 // list and the slots of nodes that span several chunks.  One workgroup.
-__global__ __launch_bounds__(1024) void k_gb_level(Ws w, int d, int max_slots) {
-    __shared__ int32_t sc[1024], ss[1024];
+__global__ __launch_bounds__(1024) void k_gb_level(Ws w, int d, int max_slots, int chunk) {
+    __shared__ int32_t sc[1024], ss[1024], sp[1024];
     const int L = 1 << d, base = L - 1;
     const int per = (L + 1023) / 1024;  // consecutive nodes per thread
     const int t = threadIdx.x;
-    int chunks = 0, slots = 0;
+    int chunks = 0, slots = 0, parts = 0;
     for (int q = 0; q < per; ++q) {
         const int j = t * per + q;
         if (j >= L) break;
@@ -254,34 +277,40 @@ __global__ __launch_bounds__(1024) void k_gb_level(Ws w, int d, int max_slots) {
                 w.cnt[k] = n - nl;
             }
         }
-        const int c = w.alive[k] ? max(1, (w.cnt[k] + kChunk - 1) / kChunk) : 0;
+        const int c = w.alive[k] ? max(1, (w.cnt[k] + chunk - 1) / chunk) : 0;
         chunks += c;
         slots += c > 1;
+        parts += c > 1 ? c : 0;
     }
     sc[t] = chunks;
     ss[t] = slots;
+    sp[t] = parts;
     __syncthreads();
     for (int off = 1; off < 1024; off <<= 1) {  // inclusive scans
-        const int a = t >= off ? sc[t - off] : 0, b = t >= off ? ss[t - off] : 0;
+        const int a = t >= off ? sc[t - off] : 0, b = t >= off ? ss[t - off] : 0, e = t >= off ? sp[t - off] : 0;
         __syncthreads();
         sc[t] += a;
         ss[t] += b;
+        sp[t] += e;
         __syncthreads();
     }
-    int c0 = sc[t] - chunks, s0 = ss[t] - slots;
+    int c0 = sc[t] - chunks, s0 = ss[t] - slots, p0 = sp[t] - parts;
     for (int q = 0; q < per; ++q) {
         const int j = t * per + q;
         if (j >= L) break;
         const int k = base + j;
-        const int c = w.alive[k] ? max(1, (w.cnt[k] + kChunk - 1) / kChunk) : 0;
+        const int c = w.alive[k] ? max(1, (w.cnt[k] + chunk - 1) / chunk) : 0;
         w.cp[j] = c0;
         w.slot[j] = -1;
-        if (c > 1 && s0 < max_slots) {
+        w.pbase[j] = -1;
+        if (c > 1 && s0 < max_slots && p0 + c <= w.pmax) {
             w.slot[j] = s0;
             w.slot_node[s0] = j;
+            w.pbase[j] = p0;
         }
         c0 += c;
         s0 += c > 1;
+        p0 += c > 1 ? c : 0;
     }
     if (t == 1023) {
         w.cp[L] = sc[1023];
@@ -290,23 +319,16 @@ __global__ __launch_bounds__(1024) void k_gb_level(Ws w, int d, int max_slots) {
     }
 }
 
-__global__ __launch_bounds__(kThreads) void k_gb_zero_slots(Ws w, int n_fg) {
-    const int64_t per_slot = (int64_t)n_fg * 2 * kGroup * kBins;
-    const int64_t n = (int64_t)w.lvl[1] * per_slot;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads)
-        w.hist[i] = 0;
-}
-
-// Evaluate the splits of features f0 .. f0 + 7 of one node from its histogram h[2][8][256] (LDS
-// or global memory); thread = (feature j = t / 32, bins 8 (t % 32) ..).  Result in *out.
-__device__ void evaluate(const int64_t *h, int f0, int F, const float *cuts, int cut_stride,
+// Evaluate the splits of features f0 .. f0 + 7 of one node from its histogram h[2][8][kBinStride]
+// (LDS or global memory); thread = (feature j = t / 32, bins 8 (t % 32) ..).  Result in *out.
+__device__ __forceinline__ void evaluate(const int64_t *h, int f0, int F, const float *cuts, int cut_stride,
                          const int32_t *n_cuts, const Params &prm, int eg, int eh, Best *out, Best *red) {
     const int t = threadIdx.x, j = t / 32, q = t % 32, f = f0 + j;
     int64_t pg[8], ph[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        pg[e] = h[(0 * kGroup + j) * kBins + 8 * q + e];
-        ph[e] = h[(1 * kGroup + j) * kBins + 8 * q + e];
+        pg[e] = h[(0 * kGroup + j) * kBinStride + 8 * q + e];
+        ph[e] = h[(1 * kGroup + j) * kBinStride + 8 * q + e];
     }
     const int64_t mg = pg[7], mh = ph[7];  // bin 8q + 7 (bin 255 on lane 31)
 #pragma unroll
@@ -326,13 +348,10 @@ __device__ void evaluate(const int64_t *h, int f0, int F, const float *cuts, int
     const int64_t xg = ig - pg[7], xh = ih - ph[7];
     const int64_t Gi = __shfl(ig, 31, 32), Hi = __shfl(ih, 31, 32);
     const int64_t Gm = __shfl(mg, 31, 32), Hm = __shfl(mh, 31, 32);
-    Best b;
-    b.valid = 0;
-    b.gain = 0.0;
-    b.key = 0;
-    b.GL = b.HL = 0;
-    b.G = Gi;
-    b.H = Hi;
+    // this lane's best candidate, kept in scalars (a struct copied under a condition spills)
+    int bv = 0, bk = 0;
+    double bg = 0.0;
+    int64_t bGL = 0, bHL = 0;
     if (f < F) {
         const int nc = clamp_cuts(n_cuts, f, cut_stride);
         const double G = ldexp((double)Gi, -eg), H = ldexp((double)Hi, -eh);
@@ -347,45 +366,59 @@ __device__ void evaluate(const int64_t *h, int f0, int F, const float *cuts, int
                 const double GR = ldexp((double)(Gi - gl), -eg), HR = ldexp((double)(Hi - hl), -eh);
                 if (!(HL >= prm.mcw) || !(HR >= prm.mcw)) continue;
                 const double gain = (node_score(GL, HL, prm.lambda) + node_score(GR, HR, prm.lambda)) - parent;
-                if (!b.valid || gain > b.gain) {
-                    b.valid = 1;
-                    b.gain = gain;
-                    b.key = (f * 256 + tt) * 2 + (1 - dir);
-                    b.GL = gl;
-                    b.HL = hl;
+                if (!bv || gain > bg) {
+                    bv = 1;
+                    bg = gain;
+                    bk = (f * 256 + tt) * 2 + (1 - dir);
+                    bGL = gl;
+                    bHL = hl;
                 }
             }
         }
     }
-    // best over the 32 lanes of the feature
+    // best over the 32 lanes of the feature: larger gain, then smaller key
 #pragma unroll
     for (int off = 16; off > 0; off >>= 1) {
-        Best o;
-        o.gain = __shfl_xor(b.gain, off, 32);
-        o.key = __shfl_xor(b.key, off, 32);
-        o.valid = __shfl_xor(b.valid, off, 32);
-        o.GL = __shfl_xor(b.GL, off, 32);
-        o.HL = __shfl_xor(b.HL, off, 32);
-        o.G = b.G;
-        o.H = b.H;
-        if (better(o, b)) b = o;
+        const double og = __shfl_xor(bg, off, 32);
+        const int ok = __shfl_xor(bk, off, 32), ov = __shfl_xor(bv, off, 32);
+        const int64_t oGL = __shfl_xor(bGL, off, 32), oHL = __shfl_xor(bHL, off, 32);
+        const bool take = ov && (!bv || og > bg || (og == bg && ok < bk));
+        if (take) {
+            bv = ov;
+            bg = og;
+            bk = ok;
+            bGL = oGL;
+            bHL = oHL;
+        }
     }
-    if (q == 0) red[j] = b;
+    if (q == 0) {
+        red[j].valid = bv;
+        red[j].gain = bg;
+        red[j].key = bk;
+        red[j].GL = bGL;
+        red[j].HL = bHL;
+        red[j].G = Gi;
+        red[j].H = Hi;
+    }
     __syncthreads();
     if (t == 0) {
-        Best r = red[0];
+        int ri = 0;
         for (int i = 1; i < kGroup; ++i)
-            if (better(red[i], r)) r = red[i];
-        r.G = red[0].G;
-        r.H = red[0].H;
-        *out = r;
+            if (better(red[i], red[ri])) ri = i;
+        out->valid = red[ri].valid;
+        out->gain = red[ri].gain;
+        out->key = red[ri].key;
+        out->GL = red[ri].GL;
+        out->HL = red[ri].HL;
+        out->G = red[0].G;
+        out->H = red[0].H;
     }
 }
 
 struct HistArgs {
     const uint8_t *bins;
     int64_t ld;
-    int F, n_fg, d;
+    int F, n_fg, d, chunk;
     const float *cuts;
     int cut_stride;
     const int32_t *n_cuts;
@@ -393,7 +426,8 @@ struct HistArgs {
 };
 
 __global__ __launch_bounds__(kThreads) void k_gb_hist(HistArgs a, Ws w) {
-    __shared__ int64_t h[2 * kGroup * kBins];  // 32 KB
+    __shared__ int64_t h[kHistWords];  // 32.1 KB
+    __shared__ int64_t tot[2][kThreads];
     __shared__ Best red[kGroup];
     const int c = blockIdx.x, fg = blockIdx.y, t = threadIdx.x;
     if (c >= w.lvl[0]) return;
@@ -407,20 +441,81 @@ __global__ __launch_bounds__(kThreads) void k_gb_hist(HistArgs a, Ws w) {
     const int j = lo, k = base + j;
     const int nch = w.cp[j + 1] - w.cp[j];
     const int s = w.start[k], n = w.cnt[k];
-    const int i0 = s + (c - w.cp[j]) * kChunk, i1 = std::min(s + n, i0 + kChunk);
-    for (int e = t; e < 2 * kGroup * kBins; e += kThreads) h[e] = 0;
-    __syncthreads();
+    const int i0 = s + (c - w.cp[j]) * a.chunk, i1 = std::min(s + n, i0 + a.chunk);
+    for (int e = t; e < kHistWords; e += kThreads) h[e] = 0;
     const int f0 = fg * kGroup;
     const int nf = std::min(kGroup, a.F - f0);
-    for (int i = i0 + t; i < i1; i += kThreads) {
-        const int r = w.order[i];
-        const uint64_t word = *reinterpret_cast<const uint64_t *>(a.bins + (int64_t)r * a.ld + f0);
-        const unsigned long long qg = (unsigned long long)w.qg[r], qh = (unsigned long long)w.qh[r];
-        for (int jj = 0; jj < nf; ++jj) {
-            const int b = (int)((word >> (8 * jj)) & 255u);
-            atomicAdd(reinterpret_cast<unsigned long long *>(&h[(0 * kGroup + jj) * kBins + b]), qg);
-            atomicAdd(reinterpret_cast<unsigned long long *>(&h[(1 * kGroup + jj) * kBins + b]), qh);
+    // the bin of 0.0 (statement features are mostly zeros) is not added row by row: it is the
+    // chunk's total minus the other bins, exact in integers.  At add step e lane l adds feature
+    // (e + l) % 8, so one instruction spreads its lanes over the 8 features and at most 8 of
+    // them can meet on one bin.
+    int zb[kGroup];
+#pragma unroll
+    for (int e = 0; e < kGroup; ++e) {
+        const int jj = (e + t) % kGroup;
+        zb[e] = jj < nf ? w.zb[f0 + jj] : -1;
+    }
+    __syncthreads();
+    int64_t sg = 0, sh = 0;
+    constexpr int U = kChunk / kThreads;
+    for (int b0 = i0; b0 < i1; b0 += kChunk) {  // 2048 rows at a time, every load issued before the adds
+        int rr[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = b0 + t + kThreads * u;
+            rr[u] = i < i1 ? w.order[i] : -1;
         }
+        uint64_t word[U];
+        int64_t qg[U], qh[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int r = rr[u] < 0 ? 0 : rr[u];
+            word[u] = *reinterpret_cast<const uint64_t *>(a.bins + ((int64_t)fg * a.ld + r) * kGroup);
+            qg[u] = w.qg[r];
+            qh[u] = w.qh[r];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (rr[u] < 0) break;
+            sg += qg[u];
+            sh += qh[u];
+#pragma unroll
+            for (int e = 0; e < kGroup; ++e) {
+                const int jj = (e + t) % kGroup;
+                const int b = (int)((word[u] >> (8 * jj)) & 255u);
+                if (zb[e] >= 0 && b != zb[e]) {
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&h[(0 * kGroup + jj) * kBinStride + b]),
+                              (unsigned long long)qg[u]);
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&h[(1 * kGroup + jj) * kBinStride + b]),
+                              (unsigned long long)qh[u]);
+                }
+            }
+        }
+    }
+    tot[0][t] = sg;
+    tot[1][t] = sh;
+    __syncthreads();
+    for (int off = kThreads / 2; off > 0; off >>= 1) {
+        if (t < off) {
+            tot[0][t] += tot[0][t + off];
+            tot[1][t] += tot[1][t + off];
+        }
+        __syncthreads();
+    }
+    {  // zero bin = total - the other bins: 16 threads per (G|H, feature) row, 16 bins each
+        const int row = t / 16, part = t % 16, gh = row / kGroup, jj = row % kGroup;
+        const int b0 = jj < nf ? w.zb[f0 + jj] : -1;
+        int64_t *hr = &h[(gh * kGroup + jj) * kBinStride];
+        int64_t rest = 0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int b = part * 16 + e;
+            rest += b == b0 ? 0 : hr[b];
+        }
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) rest += __shfl_xor(rest, off, 16);
+        __syncthreads();
+        if (part == 0 && b0 >= 0) hr[b0] = tot[gh][0] - rest;
     }
     __syncthreads();
     if (nch == 1) {
@@ -428,11 +523,34 @@ __global__ __launch_bounds__(kThreads) void k_gb_hist(HistArgs a, Ws w) {
                  &w.best[(int64_t)j * a.n_fg + fg], red);
         return;
     }
-    if (w.slot[j] < 0) return;  // cannot happen: every multi-chunk node has a slot
-    int64_t *g = w.hist + ((int64_t)w.slot[j] * a.n_fg + fg) * (2 * kGroup * kBins);
-    for (int e = t; e < 2 * kGroup * kBins; e += kThreads) {
-        const int64_t v = h[e];
-        if (v != 0) atomicAdd(reinterpret_cast<unsigned long long *>(&g[e]), (unsigned long long)v);
+    if (w.pbase[j] < 0) return;  // cannot happen: every multi-chunk node has its partials
+    int64_t *g = w.part + ((int64_t)(w.pbase[j] + c - w.cp[j]) * a.n_fg + fg) * kHistWords;
+    for (int e = t; e < kHistWords; e += kThreads) g[e] = h[e];
+}
+
+// The histogram of a multi-chunk node: the sum of its chunks' partial histograms, in chunk
+// order (integers: exact).  Workgroup = (slot, feature group, 1/8 of the words).
+__global__ __launch_bounds__(kThreads) void k_gb_reduce(HistArgs a, Ws w) {
+    const int sidx = blockIdx.x, fg = blockIdx.y;
+    if (sidx >= w.lvl[1]) return;
+    const int j = w.slot_node[sidx];
+    const int nch = w.cp[j + 1] - w.cp[j], pb = w.pbase[j];
+    const int64_t stride = (int64_t)a.n_fg * kHistWords;
+    const int64_t *src = w.part + ((int64_t)pb * a.n_fg + fg) * kHistWords;
+    int64_t *dst = w.hist + ((int64_t)sidx * a.n_fg + fg) * kHistWords;
+    constexpr int per = (kHistWords + 7) / 8;
+    for (int e = blockIdx.z * per + threadIdx.x; e < std::min(kHistWords, (int)(blockIdx.z + 1) * per); e += kThreads) {
+        int64_t acc = 0;
+        int q = 0;
+        for (; q + 8 <= nch; q += 8) {  // eight loads in flight, added in chunk order
+            int64_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = src[(int64_t)(q + u) * stride + e];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc += v[u];
+        }
+        for (; q < nch; ++q) acc += src[(int64_t)q * stride + e];
+        dst[e] = acc;
     }
 }
 
@@ -441,7 +559,7 @@ __global__ __launch_bounds__(kThreads) void k_gb_split(HistArgs a, Ws w) {
     const int sidx = blockIdx.x, fg = blockIdx.y;
     if (sidx >= w.lvl[1]) return;
     const int j = w.slot_node[sidx];
-    const int64_t *g = w.hist + ((int64_t)sidx * a.n_fg + fg) * (2 * kGroup * kBins);
+    const int64_t *g = w.hist + ((int64_t)sidx * a.n_fg + fg) * kHistWords;
     evaluate(g, fg * kGroup, a.F, a.cuts, a.cut_stride, a.n_cuts, a.prm, w.exps[0], w.exps[1],
              &w.best[(int64_t)j * a.n_fg + fg], red);
 }
@@ -493,30 +611,27 @@ __global__ __launch_bounds__(kThreads) void k_gb_decide(Ws w, int d, int n_fg, c
     }
 }
 
+// Direction of every row of a node split at this level (left = 1; rows of other nodes stay, as
+// "left"), the row's new node, and the number of lefts per block of kScanBlock positions.
 __global__ __launch_bounds__(kThreads) void k_gb_flags(Ws w, int N, const uint8_t *__restrict__ bins, int64_t ld) {
-    const int i = blockIdx.x * kThreads + threadIdx.x;
-    if (i >= N) return;
-    const int r = w.order[i], k = w.nid[r];
-    const int f = w.sf[k];
-    if (f < 0) {
-        w.flag[i] = 1;
-        w.spn[i] = -1;
-        return;
-    }
-    const int b = bins[(int64_t)r * ld + f];
-    const int go_left = b == 255 ? w.sd[k] : b < w.st[k];
-    w.nid[r] = go_left ? 2 * k + 1 : 2 * k + 2;
-    w.flag[i] = go_left;
-    w.spn[i] = k;
-}
-
-// exclusive scan of flag[0..N) into X[0..N]: block sums, a one-workgroup scan of them, the final pass
-__global__ __launch_bounds__(kThreads) void k_gb_scan_sum(Ws w, int N) {
     __shared__ int32_t s[kThreads];
-    const int b0 = blockIdx.x * kScanBlock;
-    int acc = 0;
-    for (int i = b0 + threadIdx.x; i < std::min(N, b0 + kScanBlock); i += kThreads) acc += w.flag[i];
-    s[threadIdx.x] = acc;
+    const int i = blockIdx.x * kScanBlock + threadIdx.x;
+    int go_left = 0;
+    if (i < N) {
+        const int r = w.order[i], k = w.nid[r];
+        const int f = w.sf[k];
+        int sp = -1;
+        go_left = 1;
+        if (f >= 0) {
+            const int b = bins[((int64_t)(f / kGroup) * ld + r) * kGroup + f % kGroup];
+            go_left = b == 255 ? w.sd[k] : b < w.st[k];
+            w.nid[r] = go_left ? 2 * k + 1 : 2 * k + 2;
+            sp = k;
+        }
+        w.flag[i] = go_left;
+        w.spn[i] = sp;
+    }
+    s[threadIdx.x] = go_left;
     __syncthreads();
     for (int off = kThreads / 2; off > 0; off >>= 1) {
         if (threadIdx.x < off) s[threadIdx.x] += s[threadIdx.x + off];
@@ -525,6 +640,8 @@ __global__ __launch_bounds__(kThreads) void k_gb_scan_sum(Ws w, int N) {
     if (threadIdx.x == 0) w.bsum[blockIdx.x] = s[0];
 }
 
+// exclusive scan of flag[0..N) into X[0..N]: block sums (k_gb_flags), a one-workgroup scan of
+// them, the final pass
 __global__ __launch_bounds__(1024) void k_gb_scan_top(Ws w, int nb) {
     __shared__ int32_t s[1024];
     __shared__ int32_t carry;
@@ -551,16 +668,9 @@ __global__ __launch_bounds__(1024) void k_gb_scan_top(Ws w, int nb) {
 
 __global__ __launch_bounds__(kThreads) void k_gb_scan_final(Ws w, int N, int nb) {
     __shared__ int32_t s[kThreads];
-    const int b0 = blockIdx.x * kScanBlock;
-    constexpr int per = kScanBlock / kThreads;  // 8 consecutive flags per thread
-    const int i0 = b0 + threadIdx.x * per;
-    int v[per], acc = 0;
-#pragma unroll
-    for (int e = 0; e < per; ++e) {
-        v[e] = i0 + e < N ? w.flag[i0 + e] : 0;
-        acc += v[e];
-    }
-    s[threadIdx.x] = acc;
+    const int i = blockIdx.x * kScanBlock + threadIdx.x;
+    const int v = i < N ? w.flag[i] : 0;
+    s[threadIdx.x] = v;
     __syncthreads();
     for (int off = 1; off < kThreads; off <<= 1) {
         const int a = threadIdx.x >= off ? s[threadIdx.x - off] : 0;
@@ -568,12 +678,7 @@ __global__ __launch_bounds__(kThreads) void k_gb_scan_final(Ws w, int N, int nb)
         s[threadIdx.x] += a;
         __syncthreads();
     }
-    int run = w.bsum[blockIdx.x] + s[threadIdx.x] - acc;
-#pragma unroll
-    for (int e = 0; e < per; ++e) {
-        if (i0 + e < N) w.X[i0 + e] = run;
-        run += v[e];
-    }
+    if (i < N) w.X[i] = w.bsum[blockIdx.x] + s[threadIdx.x] - v;
     if (blockIdx.x == nb - 1 && threadIdx.x == 0) w.X[N] = w.bsum[nb];
 }
 
@@ -591,19 +696,18 @@ __global__ __launch_bounds__(kThreads) void k_gb_scatter(Ws w, int N) {
     w.order2[pos] = w.order[i];
 }
 
-__global__ __launch_bounds__(kThreads) void k_gb_leaves(Ws w, int d, Params prm, float *leaf_value) {
-    const int j = blockIdx.x * kThreads + threadIdx.x, L = 1 << d;
-    if (j >= L) return;
-    const int k = L - 1 + j;
-    if (!w.alive[k]) return;
-    leaf_value[k] = leaf_weight(w.Gt[k], w.Ht[k], w.exps[0], w.exps[1], prm);
-}
-
-__global__ __launch_bounds__(kThreads) void k_gb_margin(Ws w, int N, const float *__restrict__ leaf_value,
+// The last level's leaves (threads j < 2^D) and every row's margin update (threads r < N): a row in
+// a last-level leaf takes that leaf's weight directly, a row in an earlier leaf reads it.
+__global__ __launch_bounds__(kThreads) void k_gb_finish(Ws w, int D, Params prm, int N, float *leaf_value,
                                                         float *__restrict__ margin) {
-    const int r = blockIdx.x * kThreads + threadIdx.x;
-    if (r >= N) return;
-    margin[r] = margin[r] + leaf_value[w.nid[r]];
+    const int i = blockIdx.x * kThreads + threadIdx.x, L = 1 << D;
+    const int eg = w.exps[0], eh = w.exps[1];
+    if (i < L && w.alive[L - 1 + i]) leaf_value[L - 1 + i] = leaf_weight(w.Gt[L - 1 + i], w.Ht[L - 1 + i], eg, eh, prm);
+    if (i < N) {
+        const int k = w.nid[i];
+        const float v = k >= L - 1 ? leaf_weight(w.Gt[k], w.Ht[k], eg, eh, prm) : leaf_value[k];
+        margin[i] = margin[i] + v;
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -614,8 +718,16 @@ struct Layout {
     size_t total;
 };
 
-int max_slots_for(int N, int depth) {
-    const int64_t by_rows = (int64_t)N / (kChunk + 1);
+// Rows per histogram workgroup: 2048, or a multiple of it for large sets, so that a level launches
+// about 4,096 (chunk, feature group) workgroups and flushes that many partial histograms at most.
+int chunk_rows(int N, int F) {
+    const int n_fg = (F + kGroup - 1) / kGroup;
+    const int64_t m = (int64_t)N * n_fg / ((int64_t)4096 * kChunk);
+    return kChunk * (int)std::max<int64_t>(1, std::min<int64_t>(m, 64));
+}
+
+int max_slots_for(int N, int F, int depth) {
+    const int64_t by_rows = (int64_t)N / (chunk_rows(N, F) + 1);
     const int64_t by_nodes = (int64_t)1 << (depth - 1);
     return (int)std::min(by_rows, by_nodes);
 }
@@ -626,7 +738,7 @@ Ws carve(void *base, int F, int N, int P, int depth, size_t *total) {
     const int64_t Lmax = (int64_t)1 << (depth - 1);  // widest level that builds histograms
     const int64_t nblk = ceil_div(std::max(P, 1), kThreads);
     const int64_t nb = ceil_div(std::max(N, 1), kScanBlock);
-    const int S = max_slots_for(N, depth);
+    const int S = max_slots_for(N, F, depth);
     char *p = static_cast<char *>(base);
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -660,8 +772,13 @@ Ws carve(void *base, int F, int N, int P, int depth, size_t *total) {
     w.slot = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * Lmax));
     w.slot_node = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * std::max(S, 1)));
     w.lvl = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 2));
+    w.zb = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * F));
+    w.pbase = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * Lmax));
+    // a multi-chunk node of n > CH rows has ceil(n / CH) < 2 n / CH chunks: fewer than 2 N / CH in all
+    w.pmax = (int)(2 * ceil_div(std::max(N, 1), chunk_rows(N, F)));
+    w.part = reinterpret_cast<int64_t *>(take(sizeof(int64_t) * (size_t)w.pmax * n_fg * kHistWords));
     w.best = reinterpret_cast<Best *>(take(sizeof(Best) * Lmax * n_fg));
-    w.hist = reinterpret_cast<int64_t *>(take(sizeof(int64_t) * (size_t)std::max(S, 1) * n_fg * 2 * kGroup * kBins));
+    w.hist = reinterpret_cast<int64_t *>(take(sizeof(int64_t) * (size_t)std::max(S, 1) * n_fg * kHistWords));
     *total = o;
     return w;
 }
@@ -677,8 +794,8 @@ size_t gbdt_ws_bytes(int32_t F, int32_t N, int32_t P, int32_t depth) {
 int gbdt_bin_launch(const float *x, int64_t ldx, int32_t F, int32_t N, const float *cuts, int32_t cut_stride,
                     const int32_t *n_cuts, uint8_t *bins, int64_t ld, hipStream_t stream) {
     if (N == 0) return HARL_OK;
-    // padding bytes of the row: groups past F write zeros (every lane of a group past F skips)
-    const dim3 grid((unsigned)ceil_div(N, kThreads), (unsigned)(ld / kGroup));
+    // bytes of features past F in the last group are written as zeros
+    const dim3 grid((unsigned)ceil_div(N, kThreads), (unsigned)ceil_div(F, kGroup));
     hipLaunchKernelGGL(k_gb_bin, grid, dim3(kThreads), 0, stream, x, ldx, F, N, cuts, cut_stride, n_cuts, bins, ld);
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
@@ -696,39 +813,36 @@ int gbdt_round_launch(const harl_gbdt_params *prm_in, const uint8_t *bins, int64
     const int n_nodes = (1 << (D + 1)) - 1;
     size_t total = 0;
     Ws w = carve(ws, F, N, P, D, &total);
-    const int S = max_slots_for(N, D);
+    const int S = max_slots_for(N, F, D);
+    const int CH = chunk_rows(N, F);
     TreeOut tr{feature, threshold, left, right, default_left, leaf_value};
-    const int init_n = std::max(n_nodes, N);
+    const int init_n = std::max(std::max(n_nodes, N), F);
     hipLaunchKernelGGL(k_gb_init, dim3((unsigned)ceil_div(init_n, kThreads)), dim3(kThreads), 0, stream, w, n_nodes, N,
-                       feature, threshold, left, right, default_left, leaf_value);
+                       F, cuts, cut_stride, n_cuts, feature, threshold, left, right, default_left, leaf_value);
     const int nblk = (int)ceil_div(std::max(P, 1), kThreads);
     hipLaunchKernelGGL(k_gb_prog_grad, dim3(nblk), dim3(kThreads), 0, stream, margin, prog_ptr, P, label, weight,
                        prm.base, w);
     hipLaunchKernelGGL(k_gb_exps, dim3(1), dim3(kThreads), 0, stream, w, nblk, (int64_t)N);
     hipLaunchKernelGGL(k_gb_row_q, dim3(nblk), dim3(kThreads), 0, stream, prog_ptr, P, w);
     HARL_HIP_CHECK(hipGetLastError());
-    HistArgs ha{bins, ld, F, n_fg, 0, cuts, cut_stride, n_cuts, prm};
+    HistArgs ha{bins, ld, F, n_fg, 0, CH, cuts, cut_stride, n_cuts, prm};
     const unsigned rows_grid = (unsigned)ceil_div(std::max(N, 1), kThreads);
     const int nb = (int)ceil_div(std::max(N, 1), kScanBlock);
     for (int d = 0; d < D; ++d) {
         const int L = 1 << d;
-        hipLaunchKernelGGL(k_gb_level, dim3(1), dim3(1024), 0, stream, w, d, S);
+        hipLaunchKernelGGL(k_gb_level, dim3(1), dim3(1024), 0, stream, w, d, S, CH);
         const int slots = std::min(S, L);
-        if (slots > 0) {
-            const int64_t words = (int64_t)slots * n_fg * 2 * kGroup * kBins;
-            const unsigned zg = (unsigned)std::min<int64_t>(ceil_div(words, kThreads), 4096);
-            hipLaunchKernelGGL(k_gb_zero_slots, dim3(zg), dim3(kThreads), 0, stream, w, n_fg);
-        }
         ha.d = d;
-        const unsigned chunk_bound = (unsigned)(ceil_div(N, kChunk) + L);
+        const unsigned chunk_bound = (unsigned)(ceil_div(N, CH) + L);
         hipLaunchKernelGGL(k_gb_hist, dim3(chunk_bound, (unsigned)n_fg), dim3(kThreads), 0, stream, ha, w);
-        if (slots > 0)
+        if (slots > 0) {
+            hipLaunchKernelGGL(k_gb_reduce, dim3((unsigned)slots, (unsigned)n_fg, 8), dim3(kThreads), 0, stream, ha, w);
             hipLaunchKernelGGL(k_gb_split, dim3((unsigned)slots, (unsigned)n_fg), dim3(kThreads), 0, stream, ha, w);
+        }
         hipLaunchKernelGGL(k_gb_decide, dim3((unsigned)ceil_div(L, kThreads)), dim3(kThreads), 0, stream, w, d, n_fg,
                            cuts, cut_stride, prm, tr);
         if (N > 0) {
-            hipLaunchKernelGGL(k_gb_flags, dim3(rows_grid), dim3(kThreads), 0, stream, w, N, bins, ld);
-            hipLaunchKernelGGL(k_gb_scan_sum, dim3((unsigned)nb), dim3(kThreads), 0, stream, w, N);
+            hipLaunchKernelGGL(k_gb_flags, dim3((unsigned)nb), dim3(kThreads), 0, stream, w, N, bins, ld);
             hipLaunchKernelGGL(k_gb_scan_top, dim3(1), dim3(1024), 0, stream, w, nb);
             hipLaunchKernelGGL(k_gb_scan_final, dim3((unsigned)nb), dim3(kThreads), 0, stream, w, N, nb);
             hipLaunchKernelGGL(k_gb_scatter, dim3(rows_grid), dim3(kThreads), 0, stream, w, N);
@@ -736,10 +850,8 @@ int gbdt_round_launch(const harl_gbdt_params *prm_in, const uint8_t *bins, int64
         }
         HARL_HIP_CHECK(hipGetLastError());
     }
-    hipLaunchKernelGGL(k_gb_leaves, dim3((unsigned)ceil_div(1 << D, kThreads)), dim3(kThreads), 0, stream, w, D, prm,
-                       leaf_value);
-    if (N > 0)
-        hipLaunchKernelGGL(k_gb_margin, dim3(rows_grid), dim3(kThreads), 0, stream, w, N, leaf_value, margin);
+    hipLaunchKernelGGL(k_gb_finish, dim3((unsigned)ceil_div(std::max(1 << D, N), kThreads)), dim3(kThreads), 0, stream,
+                       w, D, prm, N, leaf_value, margin);
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
 }

@@ -182,19 +182,18 @@ def test_gbdt_argument_errors():
                 harl.gbdt_params(gamma=-1.0), harl.gbdt_params(min_child_weight=float("nan"))):
         assert harl.harl_gbdt_round_workspace_size(bad, 164, 100, 10) == 0
     assert harl.harl_gbdt_round_workspace_size(prm, 0, 100, 10) == 0
-    b = lambda ldf=100, F=164, N=100, ldb=168, bins=0x1000, stride=16: _status(
+    b = lambda ldf=100, F=164, N=100, ldb=100, bins=0x1000, stride=16: _status(
         "harl_gbdt_bin", 0x2000, ldf, F, N, 0x3000, stride, 0x4000, bins, ldb, None)
     assert b(ldf=99) == harl.HARL_E_INVALID_ARG
-    assert b(ldb=164) == harl.HARL_E_INVALID_ARG  # not a multiple of 8
-    assert b(ldb=160) == harl.HARL_E_INVALID_ARG  # shorter than a row
+    assert b(ldb=99) == harl.HARL_E_INVALID_ARG  # planes shorter than the rows
     assert b(bins=0x1004) == harl.HARL_E_INVALID_ARG
     assert b(stride=0) == harl.HARL_E_INVALID_ARG
     assert b(N=0) == harl.HARL_OK
-    r = lambda p=prm, ldb=168, bins=0x1000, ws=0x5000, wsb=1 << 30, N=100, P=10, label=0x6000: _status(
+    r = lambda p=prm, ldb=100, bins=0x1000, ws=0x5000, wsb=1 << 30, N=100, P=10, label=0x6000: _status(
         "harl_gbdt_round", ctypes.byref(p), bins, ldb, 164, N, 0x3000, 16, 0x4000, 0x7000, P, label, 0x6000, 0x8000,
         0x9000, 0x9000, 0x9000, 0x9000, 0x9000, 0x9000, ws, wsb, None)
     assert r(p=harl.gbdt_params(max_depth=13)) == harl.HARL_E_INVALID_ARG
-    assert r(ldb=164) == harl.HARL_E_INVALID_ARG
+    assert r(ldb=99) == harl.HARL_E_INVALID_ARG
     assert r(bins=0x1004) == harl.HARL_E_INVALID_ARG
     assert r(label=None) == harl.HARL_E_INVALID_ARG
     assert r(ws=0x5001) == harl.HARL_E_INVALID_ARG

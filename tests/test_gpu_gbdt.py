@@ -24,14 +24,33 @@ def _dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_bin(X, n_rows, cuts, n_cuts, ld_bins):
+def to_groups(bins_rows, F, ld_rows):
+    """Row-major bins [N][>= F] (the oracle's layout) -> the library's planes [ceil(F/8)][ld_rows][8]
+    (a relayout only)."""
+    N = bins_rows.shape[0]
+    n_fg = (F + 7) // 8
+    padded = np.zeros((N, n_fg * 8), np.uint8)
+    padded[:, :F] = bins_rows[:, :F]
+    out = np.zeros((n_fg, ld_rows, 8), np.uint8)
+    out[:, :N, :] = padded.reshape(N, n_fg, 8).transpose(1, 0, 2)
+    return out
+
+
+def from_groups(planes, F, N):
+    n_fg = planes.shape[0]
+    return planes[:, :N, :].transpose(1, 0, 2).reshape(N, n_fg * 8)[:, :F]
+
+
+def gpu_bin(X, n_rows, cuts, n_cuts, ld_rows):
+    """harl_gbdt_bin; returns the planes [ceil(F/8)][ld_rows][8]."""
     import torch
     from paper_2211_11172_amd import harl
     F = X.shape[0]
-    bins = torch.full((max(n_rows, 1), ld_bins), 0xAB, dtype=torch.uint8, device="cuda")
-    harl.harl_gbdt_bin(_dev(X), X.shape[1], F, n_rows, _dev(cuts), cuts.shape[1], _dev(n_cuts), bins, ld_bins)
+    n_fg = (F + 7) // 8
+    bins = torch.full((n_fg, max(ld_rows, 1), 8), 0xAB, dtype=torch.uint8, device="cuda")
+    harl.harl_gbdt_bin(_dev(X), X.shape[1], F, n_rows, _dev(cuts), cuts.shape[1], _dev(n_cuts), bins, ld_rows)
     torch.cuda.synchronize()
-    return bins.cpu().numpy()[:n_rows]
+    return bins.cpu().numpy()
 
 
 def gpu_rounds(bins, F, cuts, n_cuts, prog_ptr, label, weight, margin, rounds=1, **kw):
@@ -40,10 +59,11 @@ def gpu_rounds(bins, F, cuts, n_cuts, prog_ptr, label, weight, margin, rounds=1,
     import torch
     from paper_2211_11172_amd import harl
     prm = harl.gbdt_params(**kw)
-    N, ld = bins.shape
+    N = bins.shape[0]
+    ld = N + 3  # ragged plane stride
     P = len(prog_ptr) - 1
     n_nodes = (1 << (prm.max_depth + 1)) - 1
-    d_bins = _dev(bins) if N else torch.zeros((1, ld), dtype=torch.uint8, device="cuda")
+    d_bins = _dev(to_groups(bins, F, ld))
     d_margin = _dev(np.asarray(margin, np.float32)) if N else torch.zeros(1, dtype=torch.float32, device="cuda")
     d_label = _dev(np.asarray(label, np.float32)) if P else torch.zeros(1, device="cuda")
     d_weight = _dev(np.asarray(weight, np.float32)) if P else torch.zeros(1, device="cuda")
@@ -108,11 +128,15 @@ def test_bins_bit_exact(F, n_cuts, p_nan):
     X[:, 6] = -np.inf
     Xp = np.full((F, m["n_rows"] + 5), np.nan, np.float32)
     Xp[:, :m["n_rows"]] = X
-    ldb = _ld(F) + 8
+    ldr = m["n_rows"] + 9
     log("gbdt bin parity: F=%d n_cuts=%d rows=%d" % (F, n_cuts, m["n_rows"]))
-    got = gpu_bin(Xp, m["n_rows"], m["cuts"], m["n_cuts"], ldb)
-    want = oracle.gbdt_bin(Xp, m["n_rows"], m["cuts"], m["n_cuts"], ldb)
-    np.testing.assert_array_equal(got, want)
+    planes = gpu_bin(Xp, m["n_rows"], m["cuts"], m["n_cuts"], ldr)
+    want = oracle.gbdt_bin(Xp, m["n_rows"], m["cuts"], m["n_cuts"], _ld(F))
+    np.testing.assert_array_equal(from_groups(planes, F, m["n_rows"]), want[:, :F])
+    n_fg = planes.shape[0]
+    tail = planes[:, :m["n_rows"], :].transpose(1, 0, 2).reshape(m["n_rows"], n_fg * 8)[:, F:]
+    assert (tail == 0).all(), "bytes of features past F must be 0"
+    assert (planes[:, m["n_rows"]:, :] == 0xAB).all(), "rows past n_rows must not be written"
 
 
 @pytest.mark.parametrize("name,n_prog,s_max,F,depth,p_nan,rounds", [
