@@ -14,6 +14,12 @@
  *                     Section 4.3, Top-K Selection Phase), optionally merged into a running top-K
  *                     that plays the heap H accumulating candidates across steps (Algorithm 1).
  *
+ * Around the round: harl_track_advantage / harl_track_eliminate (reward, advantage and the
+ * adaptive-stopping elimination of schedule tracks; Eq. 4, Section 5), harl_policy_select (one
+ * action per modification type, greedy or sampled; Section 4.3), harl_ppo_update (the actor/critic's
+ * training step; Section 6.1) and harl_gbdt_bin / harl_gbdt_round (the cost model's refit on
+ * measured programs; Algorithm 1, Section 6.1).
+ *
  * Conventions for every call:
  *   - Return value is a harl_status; nothing else signals an error and no C++ exception crosses
  *     this interface.  harl_last_error() gives the message of the calling thread's last failure.

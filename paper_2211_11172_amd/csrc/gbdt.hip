@@ -140,12 +140,13 @@ __global__ __launch_bounds__(kThreads) void k_gb_bin(const float *__restrict__ x
 __global__ __launch_bounds__(kThreads) void k_gb_prog_grad(const float *__restrict__ margin,
                                                            const int32_t *__restrict__ prog_ptr, int P,
                                                            const float *__restrict__ label,
-                                                           const float *__restrict__ weight, double base, Ws w) {
+                                                           const float *__restrict__ weight, double base, int N,
+                                                           Ws w) {
     __shared__ double sg[kThreads], sh[kThreads];
     const int p = blockIdx.x * kThreads + threadIdx.x;
     double ag = 0.0, ah = 0.0;
     if (p < P) {
-        const int r0 = prog_ptr[p], r1 = prog_ptr[p + 1];
+        const int r0 = min(max(prog_ptr[p], 0), N), r1 = min(max(prog_ptr[p + 1], r0), N);
         double s = base;
         for (int r = r0; r < r1; ++r) s += (double)margin[r];
         const double g = (double)weight[p] * (s - (double)label[p]);
@@ -202,12 +203,13 @@ __global__ __launch_bounds__(kThreads) void k_gb_exps(Ws w, int nblk, int64_t N)
     }
 }
 
-__global__ __launch_bounds__(kThreads) void k_gb_row_q(const int32_t *__restrict__ prog_ptr, int P, Ws w) {
+__global__ __launch_bounds__(kThreads) void k_gb_row_q(const int32_t *__restrict__ prog_ptr, int P, int N, Ws w) {
     const int p = blockIdx.x * kThreads + threadIdx.x;
     if (p >= P) return;
     const int eg = w.exps[0], eh = w.exps[1];
     const int64_t qg = (int64_t)rint(ldexp(w.gp[p], eg)), qh = (int64_t)rint(ldexp(w.hp[p], eh));
-    for (int r = prog_ptr[p]; r < prog_ptr[p + 1]; ++r) {
+    const int r0 = min(max(prog_ptr[p], 0), N), r1 = min(max(prog_ptr[p + 1], r0), N);  // clamped
+    for (int r = r0; r < r1; ++r) {
         w.qg[r] = qg;
         w.qh[r] = qh;
     }
@@ -821,9 +823,9 @@ int gbdt_round_launch(const harl_gbdt_params *prm_in, const uint8_t *bins, int64
                        F, cuts, cut_stride, n_cuts, feature, threshold, left, right, default_left, leaf_value);
     const int nblk = (int)ceil_div(std::max(P, 1), kThreads);
     hipLaunchKernelGGL(k_gb_prog_grad, dim3(nblk), dim3(kThreads), 0, stream, margin, prog_ptr, P, label, weight,
-                       prm.base, w);
+                       prm.base, N, w);
     hipLaunchKernelGGL(k_gb_exps, dim3(1), dim3(kThreads), 0, stream, w, nblk, (int64_t)N);
-    hipLaunchKernelGGL(k_gb_row_q, dim3(nblk), dim3(kThreads), 0, stream, prog_ptr, P, w);
+    hipLaunchKernelGGL(k_gb_row_q, dim3(nblk), dim3(kThreads), 0, stream, prog_ptr, P, N, w);
     HARL_HIP_CHECK(hipGetLastError());
     HistArgs ha{bins, ld, F, n_fg, 0, CH, cuts, cut_stride, n_cuts, prm};
     const unsigned rows_grid = (unsigned)ceil_div(std::max(N, 1), kThreads);
