@@ -216,3 +216,40 @@ def test_degenerate_cases_bit_exact(case):
     want, wm = oracle_rounds(bins, 11, m["cuts"], m["n_cuts"], ptr, label, weight, m0, 1, **kw)
     assert_trees_equal(got, want, case)
     np.testing.assert_array_equal(gm.view(np.uint32), wm.view(np.uint32))
+
+
+def test_throughput_measured_set_full_size():
+    """65,536 measured programs (2,134,518 rows), the benchmark's launch configuration (Ansor's
+    settings, depth 10): bins bit-exact on every row; a depth-1 round bit-exact against the oracle
+    (the root's decision over all rows); the depth-10 round's margin change on 4,096 sampled rows
+    equal to the leaf the scoring oracle reaches by routing the raw features through the GPU's tree
+    (thresholds, default directions and leaves agree with the bins the tree was grown on)."""
+    require_gpu()
+    import torch
+    m = _case(get_config("throughput"), 254)
+    N, F = m["n_rows"], 164
+    log("gbdt full size: %d rows; oracle binning" % N)
+    want_bins = oracle.gbdt_bin_np(m["features"], N, m["cuts"], m["n_cuts"], 168)
+    planes = gpu_bin(m["features"], N, m["cuts"], m["n_cuts"], N)
+    np.testing.assert_array_equal(from_groups(planes, F, N), want_bins[:, :F])
+    del planes
+    m0 = np.zeros(N, np.float32)
+    log("gbdt full size: depth-1 round")
+    got, gm = gpu_rounds(want_bins, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"], m0, 1,
+                         max_depth=1)
+    want, wm = oracle_rounds(want_bins, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"], m0, 1,
+                             **dict(oracle.GBDT_DEFAULTS, max_depth=1))
+    assert_trees_equal(got, want, "full size depth 1")
+    np.testing.assert_array_equal(gm.view(np.uint32), wm.view(np.uint32))
+    log("gbdt full size: depth-10 round")
+    got, gm = gpu_rounds(want_bins, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"], m0, 1)
+    tree = got[0]
+    assert (tree["feature"] >= 0).sum() >= 8
+    rows = np.sort(np.random.default_rng(5).choice(N, 4096, replace=False))
+    ens = dict(n_trees=1, n_features=F, root=np.zeros(1, np.int32), feature=tree["feature"],
+               threshold=tree["threshold"], left=tree["left"], right=tree["right"],
+               default_left=tree["default_left"], leaf_value=tree["leaf_value"], base_score=0.0)
+    sc = oracle.score_round(ens, np.ascontiguousarray(m["features"][:, rows]),
+                            np.arange(rows.size + 1, dtype=np.int32))
+    np.testing.assert_array_equal(gm[rows], sc["stmt32"])
+    torch.cuda.empty_cache()

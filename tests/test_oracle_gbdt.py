@@ -257,3 +257,14 @@ def test_new_tree_scores_like_the_margin_update():
                leaf_value=r["leaf_value"], base_score=0.0)
     sc = oracle.score_round(ens, pb["x"], pb["prog_ptr"])
     np.testing.assert_array_equal(sc["stmt32"], r["margin"])
+
+
+def test_numpy_binning_equals_the_c_count():
+    rng = np.random.default_rng(17)
+    F, N = 6, 2000
+    cuts = np.sort(rng.normal(size=(F, 40)).astype(np.float32), axis=1)
+    n_cuts = np.array([40, 0, 1, 17, 39, 25], np.int32)
+    x = rng.normal(size=(F, N)).astype(np.float32)
+    x[:, ::7] = cuts[:, :1]
+    x[:, 3::11] = np.nan
+    np.testing.assert_array_equal(oracle.gbdt_bin_np(x, N, cuts, n_cuts, 8), oracle.gbdt_bin(x, N, cuts, n_cuts, 8))
