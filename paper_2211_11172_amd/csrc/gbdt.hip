@@ -108,24 +108,34 @@ __device__ __forceinline__ bool better(const Best &a, const Best &b) {
 // ------------------------------------------------------------------------------------------
 // binning
 // ------------------------------------------------------------------------------------------
+// Thread = (row, 8-feature group); the group's cut points are staged in LDS first, so the binary
+// searches run on LDS.
 __global__ __launch_bounds__(kThreads) void k_gb_bin(const float *__restrict__ x, int64_t ldx, int F, int N,
                                                      const float *__restrict__ cuts, int cut_stride,
                                                      const int32_t *__restrict__ n_cuts, uint8_t *__restrict__ bins,
                                                      int64_t ld) {
-    const int r = blockIdx.x * kThreads + threadIdx.x;
+    __shared__ float sc[kGroup][256];
+    __shared__ int snc[kGroup];
+    const int g = blockIdx.y, t = threadIdx.x;
+    if (t < kGroup) snc[t] = g * kGroup + t < F ? clamp_cuts(n_cuts, g * kGroup + t, cut_stride) : 0;
+    __syncthreads();
+    for (int e = t; e < kGroup * 256; e += kThreads) {
+        const int j = e / 256, i = e % 256;
+        if (i < snc[j]) sc[j][i] = cuts[(int64_t)(g * kGroup + j) * cut_stride + i];
+    }
+    __syncthreads();
+    const int r = blockIdx.x * kThreads + t;
     if (r >= N) return;
-    const int g = blockIdx.y;
     uint64_t word = 0;
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) {
         const int f = g * kGroup + j;
         if (f >= F) break;
         const float v = x[(int64_t)f * ldx + r];
-        const float *c = cuts + (int64_t)f * cut_stride;
-        int lo = 0, hi = clamp_cuts(n_cuts, f, cut_stride);
+        int lo = 0, hi = snc[j];
         while (lo < hi) {  // number of cut points <= v
             const int mid = (lo + hi) >> 1;
-            if (c[mid] <= v) lo = mid + 1;
+            if (sc[j][mid] <= v) lo = mid + 1;
             else hi = mid;
         }
         const uint64_t b = v != v ? 255u : (uint64_t)lo;
@@ -579,21 +589,47 @@ struct TreeOut {
     float *leaf_value;
 };
 
+// One wave per node: lane i < n_fg holds feature group i's record; the best (larger gain, then the
+// smaller key, as in the evaluation) is found by a shuffle reduction, then lane 0 writes.
 __global__ __launch_bounds__(kThreads) void k_gb_decide(Ws w, int d, int n_fg, const float *__restrict__ cuts,
                                                         int cut_stride, Params prm, TreeOut tr) {
-    const int j = blockIdx.x * kThreads + threadIdx.x, L = 1 << d;
+    const int j = blockIdx.x * (kThreads / 64) + threadIdx.x / 64, lane = threadIdx.x % 64, L = 1 << d;
     if (j >= L) return;
     const int k = L - 1 + j;
     if (!w.alive[k]) return;
     const Best *bs = w.best + (int64_t)j * n_fg;
-    Best b = bs[0];
-    for (int i = 1; i < n_fg; ++i)
-        if (better(bs[i], b)) b = bs[i];
+    int bv = 0, bk = 0;
+    double bg = 0.0;
+    int64_t bGL = 0, bHL = 0;
+    for (int i = lane; i < n_fg; i += 64) {  // n_fg <= 512: records i, i + 64, ... in order
+        const Best &o = bs[i];
+        if (o.valid && (!bv || o.gain > bg || (o.gain == bg && o.key < bk))) {
+            bv = 1;
+            bg = o.gain;
+            bk = o.key;
+            bGL = o.GL;
+            bHL = o.HL;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const double og = __shfl_xor(bg, off);
+        const int ok = __shfl_xor(bk, off), ov = __shfl_xor(bv, off);
+        const int64_t oGL = __shfl_xor(bGL, off), oHL = __shfl_xor(bHL, off);
+        if (ov && (!bv || og > bg || (og == bg && ok < bk))) {
+            bv = ov;
+            bg = og;
+            bk = ok;
+            bGL = oGL;
+            bHL = oHL;
+        }
+    }
+    if (lane != 0) return;
     const int64_t G = bs[0].G, H = bs[0].H;
     w.Gt[k] = G;
     w.Ht[k] = H;
-    if (b.valid && b.gain > prm.gamma) {
-        const int f = b.key / 512, tt = (b.key / 2) % 256, dir = 1 - (b.key & 1);
+    if (bv && bg > prm.gamma) {
+        const int f = bk / 512, tt = (bk / 2) % 256, dir = 1 - (bk & 1);
         tr.feature[k] = f;
         tr.threshold[k] = cuts[(int64_t)f * cut_stride + tt - 1];
         tr.left[k] = 2 * k + 1;
@@ -604,10 +640,10 @@ __global__ __launch_bounds__(kThreads) void k_gb_decide(Ws w, int d, int n_fg, c
         w.sd[k] = dir;
         w.alive[2 * k + 1] = 1;
         w.alive[2 * k + 2] = 1;
-        w.Gt[2 * k + 1] = b.GL;
-        w.Ht[2 * k + 1] = b.HL;
-        w.Gt[2 * k + 2] = G - b.GL;
-        w.Ht[2 * k + 2] = H - b.HL;
+        w.Gt[2 * k + 1] = bGL;
+        w.Ht[2 * k + 1] = bHL;
+        w.Gt[2 * k + 2] = G - bGL;
+        w.Ht[2 * k + 2] = H - bHL;
     } else {
         tr.leaf_value[k] = leaf_weight(G, H, w.exps[0], w.exps[1], prm);
     }
@@ -841,7 +877,7 @@ int gbdt_round_launch(const harl_gbdt_params *prm_in, const uint8_t *bins, int64
             hipLaunchKernelGGL(k_gb_reduce, dim3((unsigned)slots, (unsigned)n_fg, 8), dim3(kThreads), 0, stream, ha, w);
             hipLaunchKernelGGL(k_gb_split, dim3((unsigned)slots, (unsigned)n_fg), dim3(kThreads), 0, stream, ha, w);
         }
-        hipLaunchKernelGGL(k_gb_decide, dim3((unsigned)ceil_div(L, kThreads)), dim3(kThreads), 0, stream, w, d, n_fg,
+        hipLaunchKernelGGL(k_gb_decide, dim3((unsigned)ceil_div(L, kThreads / 64)), dim3(kThreads), 0, stream, w, d, n_fg,
                            cuts, cut_stride, prm, tr);
         if (N > 0) {
             hipLaunchKernelGGL(k_gb_flags, dim3((unsigned)nb), dim3(kThreads), 0, stream, w, N, bins, ld);
