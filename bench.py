@@ -246,7 +246,10 @@ def tracks_bench(args):
                  "advantage_us": adv_us, "eliminate_us": elim_us, "both_us": both_us,
                  "tracks_per_s": n / (both_us * 1e-6),
                  "advantage_gbs": adv_bytes / (adv_us * 1e-6) / 1e9,
-                 "eliminate_gbs": elim_bytes / (elim_us * 1e-6) / 1e9, "matches_oracle": same}
+                 "eliminate_gbs": elim_bytes / (elim_us * 1e-6) / 1e9, "matches_oracle": same,
+                 "roofline": {"bound": "hbm", "kernel": "harl_track_eliminate (+ row gather)",
+                              "achieved": elim_bytes / (elim_us * 1e-6) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                              "frac": elim_bytes / (elim_us * 1e-6) / 1e9 / PEAK_HBM_GBS, "traffic": None}}
         if not args.no_cpu_baseline:
             a64 = None
             t0 = time.perf_counter()
@@ -321,9 +324,23 @@ def select_bench(args):
         same = bool(np.array_equal(sel.cpu().numpy(), want["action"]))
         # algorithmic bytes: the logits read, probabilities written, 2 x 4 B per (state, type)
         nbytes = B * (26 * 4 * 2 + 4 * 8)
-        results.append({"states": B, "actions": 26, "types": 4, "policy_step_us": pol_us, "select_greedy_us": greedy_us,
-                        "select_sample_us": sample_us, "select_sample_gbs": nbytes / (sample_us * 1e-6) / 1e9,
-                        "sampled_matches_oracle": same})
+        gbs = nbytes / (sample_us * 1e-6) / 1e9
+        entry = {"states": B, "actions": 26, "types": 4, "policy_step_us": pol_us, "select_greedy_us": greedy_us,
+                 "select_sample_us": sample_us, "select_sample_gbs": gbs, "sampled_matches_oracle": same,
+                 "roofline": {"bound": "hbm", "kernel": "k_policy_select<true> via harl_policy_select (sampled)",
+                              "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+                              "traffic": None}}
+        if not args.no_cpu_baseline:
+            zl = logits.cpu().numpy()[:4096]
+            t0 = time.perf_counter()
+            reps = 0
+            while time.perf_counter() - t0 < 2.0 or reps == 0:
+                oracle.policy_select(zl, np.array(segs, np.int32), sample=True, seed=1234, counter=reps)
+                reps += 1
+            el = time.perf_counter() - t0
+            entry["cpu_baseline"] = {"value": zl.shape[0] * reps / el, "unit": "states/s", "cores": 1, "kind": "oracle",
+                                     "sample": "%d sampled selections of 4096 states in %.1f s" % (reps, el)}
+        results.append(entry)
         print("select B=%d: policy %.1f us, greedy %.1f us, sampled %.1f us" % (B, pol_us, greedy_us, sample_us),
               file=sys.stderr, flush=True)
         P.close()
@@ -384,7 +401,10 @@ def ppo_bench(args):
         flops = 2 * fwd + 2 * M * (h2 * (a + 1) + h1 * h2)
         tf = flops / (us * 1e-6) / 1e12
         entry = {"transitions": M, "us_per_update": us, "gflop": flops / 1e9, "achieved_tflops": tf,
-                 "peak_tflops": PEAK_MFMA_TFLOPS["f32"], "frac": tf / PEAK_MFMA_TFLOPS["f32"]}
+                 "peak_tflops": PEAK_MFMA_TFLOPS["f32"], "frac": tf / PEAK_MFMA_TFLOPS["f32"],
+                 "roofline": {"bound": "mfma", "kernel": "harl_ppo_update (k_gemm and the objective kernels)",
+                              "achieved": tf, "peak": PEAK_MFMA_TFLOPS["f32"], "unit": "TFLOP/s",
+                              "frac": tf / PEAK_MFMA_TFLOPS["f32"], "traffic": None}}
         if not args.no_cpu_baseline:
             batch = dict(states=X, actions=acts, logp_old=lpo.cpu().numpy(), adv=adv.cpu().numpy(), ret=ret.cpu().numpy())
             sub = min(M, 4096)
@@ -463,6 +483,10 @@ def refit_bench(args):
                  "rows_per_s": N / (us_round * 1e-6), "level_bytes": level_bytes,
                  "stream_GBps": prm.max_depth * level_bytes / (us_round * 1e-6) / 1e9,
                  "bin_GBps": (N * F * 4 + N * n_fg * 8) / (us_bin * 1e-6) / 1e9}
+        gbs = prm.max_depth * level_bytes / (us_round * 1e-6) / 1e9
+        entry["roofline"] = {"bound": "hbm", "kernel": "harl_gbdt_round (k_gb_hist and the per-level kernels)",
+                             "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+                             "traffic": None}
         if not args.no_cpu_baseline and name == "standard":
             hb = bins.cpu().numpy().transpose(1, 0, 2).reshape(N, n_fg * 8)  # the oracle's row-major layout
             t0 = time.perf_counter()
