@@ -14,8 +14,9 @@
 //              the logits and v (min passes the gradient to the unclipped term on equality, clip
 //              inside its closed range)
 //   backward   dWa = dlogits^T h2, dwv = dv^T h2, dz2 = (dlogits Wa + dv wv) * [h2 > 0],
-//              dW2 = dz2^T h1, dz1 = (dz2 W2) * [h1 > 0], dW1 = dz1^T X, the bias gradients as
-//              column sums (k_colsum) -- all reductions over the batch in fixed-order chunks
+//              dW2 = dz2^T h1, dz1 = (dz2 W2) * [h1 > 0], dW1 = dz1^T X; each bias gradient is
+//              the last column of its weight gradient's GEMM against [B | 1] -- all reductions over
+//              the batch in fixed-order split-K pieces summed in order
 //   Adam       bias-corrected, the actor's rate for the trunk and actor head, the critic's for the
 //              value head (k_adam)
 // k_gemm: C[i][j] = sum_p A(i, p) B(p, j) with A(i, p) = A[i a_si + p a_sp], B(p, j) = B[p b_sp +
@@ -35,9 +36,7 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGemmThreads = 256, kTile = 64, kTileK = 32;
-constexpr int kPer = kTile * kTileK / kGemmThreads;  // operand elements per thread per K step
 constexpr int kMaxSplits = 32;
-constexpr int kColChunks = 64;  // row chunks of a column sum
 
 enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kRank1Mask = 3 };
 
@@ -54,41 +53,74 @@ struct GemmArgs {
     const float *u, *w;           // rank-1 term u[i] w[j]
     const float *mask;            // multiply by [mask[i ldm + j] > 0]
     int64_t ldm;
+    int ones;                     // C's last column (j = J - 1) is A's row sums (B has J - 1 columns)
+    float *bias_out;              // split only: column J - 1 of the sum goes to bias_out[i]
 };
 
-// Operand elements of the K step starting at p0 for this thread: A's TI x 32 and B's 32 x 64
-// tiles, the tile index moving fastest along the operand's contiguous direction.
-template <int TI>
-__device__ __forceinline__ void gemm_fetch(const GemmArgs &g, int i0, int j0, int p0, int p_end,
-                                           float (&ra)[TI * kTileK / kGemmThreads], float (&rb)[kPer]) {
-    constexpr int PA = TI * kTileK / kGemmThreads;
+// Operand elements of the K step starting at p0 for this thread: A's TI x TK and B's TK x 64
+// tiles, the tile index moving fastest along the operand's contiguous direction.  VEC: 16-byte
+// loads of 4 elements consecutive along that direction (the host checks that every such group is
+// wholly inside or wholly outside the operand and 16-byte aligned); otherwise one element per load.
+template <int TI, int TK, bool VEC>
+struct Frag {
+    static constexpr int W = VEC ? 4 : 1;
+    static constexpr int NA = TI * TK / (kGemmThreads * W), NB = kTile * TK / (kGemmThreads * W);
+    float a[NA][W], b[NB][W];
+};
+
+template <int TI, int TK, bool VEC>
+__device__ __forceinline__ void gemm_fetch(const GemmArgs &g, int i0, int j0, int p0, int p_end, Frag<TI, TK, VEC> &f) {
+    using F = Frag<TI, TK, VEC>;
+    constexpr int W = F::W;
     const int t = threadIdx.x;
     const bool a_i_fast = g.a_si == 1, b_p_fast = g.b_sp == 1;
 #pragma unroll
-    for (int q = 0; q < PA; ++q) {
+    for (int q = 0; q < F::NA; ++q) {
         const int e = t + kGemmThreads * q;
-        const int ii = a_i_fast ? e % TI : e / kTileK, pp = a_i_fast ? e / TI : e % kTileK;
+        // element (ii, pp) is the first of the group
+        const int ii = a_i_fast ? (e % (TI / W)) * W : e / (TK / W), pp = a_i_fast ? e / (TI / W) : (e % (TK / W)) * W;
         const int gi = i0 + ii, gp = p0 + pp;
-        float v = 0.f;
-        if (gi < g.I && gp < p_end) v = g.A ? g.A[(int64_t)gi * g.a_si + (int64_t)gp * g.a_sp] : 1.f;
-        ra[q] = v;
+        if constexpr (VEC) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (gi < g.I && gp < p_end) v = *reinterpret_cast<const float4 *>(g.A + (int64_t)gi * g.a_si + (int64_t)gp * g.a_sp);
+            f.a[q][0] = v.x;
+            f.a[q][1] = v.y;
+            f.a[q][2] = v.z;
+            f.a[q][3] = v.w;
+        } else {
+            float v = 0.f;
+            if (gi < g.I && gp < p_end) v = g.A ? g.A[(int64_t)gi * g.a_si + (int64_t)gp * g.a_sp] : 1.f;
+            f.a[q][0] = v;
+        }
     }
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
+    for (int q = 0; q < F::NB; ++q) {
         const int e = t + kGemmThreads * q;
-        const int pb = b_p_fast ? e % kTileK : e / kTile, jb = b_p_fast ? e / kTileK : e % kTile;
+        const int pb = b_p_fast ? (e % (TK / W)) * W : e / (kTile / W), jb = b_p_fast ? e / (TK / W) : (e % (kTile / W)) * W;
         const int gpb = p0 + pb, gj = j0 + jb;
-        rb[q] = (gpb < p_end && gj < g.J) ? g.B[(int64_t)gpb * g.b_sp + (int64_t)gj * g.b_sj] : 0.f;
+        const int J0 = g.J - g.ones;  // B's columns
+        if constexpr (VEC) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (gpb < p_end && gj < J0)
+                v = *reinterpret_cast<const float4 *>(g.B + (int64_t)gpb * g.b_sp + (int64_t)gj * g.b_sj);
+            f.b[q][0] = v.x;
+            f.b[q][1] = v.y;
+            f.b[q][2] = v.z;
+            f.b[q][3] = v.w;
+        } else {
+            f.b[q][0] = (gpb < p_end && gj < J0) ? g.B[(int64_t)gpb * g.b_sp + (int64_t)gj * g.b_sj] : 0.f;
+        }
     }
 }
 
 // TI rows (64 or 32) by 64 columns of C per workgroup; wave w owns rows (w / 2) TI / 2 .. and
 // columns (w % 2) 32 ..
-template <int TI>
+template <int TI, int TK, bool VEC>
 __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
-    constexpr int XT = TI / 32, PA = TI * kTileK / kGemmThreads;
-    __shared__ float As[TI][kTileK + 1];
-    __shared__ float Bs[kTileK][kTile + 1];
+    using F = Frag<TI, TK, VEC>;
+    constexpr int XT = TI / 32, W = F::W;
+    __shared__ float As[TI][TK + 1];
+    __shared__ float Bs[TK][kTile + 1];
     const int t = threadIdx.x, wv = t / 64, l = t % 64;
     const int i0 = blockIdx.y * TI, j0 = blockIdx.x * kTile;
     const int p_begin = blockIdx.z * g.p_per_split;
@@ -100,26 +132,34 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
     for (int x = 0; x < XT; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float ra[PA], rb[kPer];
-    if (p_begin < p_end) gemm_fetch<TI>(g, i0, j0, p_begin, p_end, ra, rb);
-    for (int p0 = p_begin; p0 < p_end; p0 += kTileK) {
+    F fr;
+    // the column-0 workgroups of a GEMM with g.ones also sum A's rows: thread t < TI, row t
+    const bool rowsum = g.ones && blockIdx.x == 0 && t < TI;
+    float rs = 0.f;
+    if (p_begin < p_end) gemm_fetch<TI, TK, VEC>(g, i0, j0, p_begin, p_end, fr);
+    for (int p0 = p_begin; p0 < p_end; p0 += TK) {
 #pragma unroll
-        for (int q = 0; q < PA; ++q) {
+        for (int q = 0; q < F::NA; ++q) {
             const int e = t + kGemmThreads * q;
-            const int ii = a_i_fast ? e % TI : e / kTileK, pp = a_i_fast ? e / TI : e % kTileK;
-            As[ii][pp] = ra[q];
+            const int ii = a_i_fast ? (e % (TI / W)) * W : e / (TK / W), pp = a_i_fast ? e / (TI / W) : (e % (TK / W)) * W;
+#pragma unroll
+            for (int u = 0; u < W; ++u) As[ii + (a_i_fast ? u : 0)][pp + (a_i_fast ? 0 : u)] = fr.a[q][u];
         }
 #pragma unroll
-        for (int q = 0; q < kPer; ++q) {
+        for (int q = 0; q < F::NB; ++q) {
             const int e = t + kGemmThreads * q;
-            const int pb = b_p_fast ? e % kTileK : e / kTile, jb = b_p_fast ? e / kTileK : e % kTile;
-            Bs[pb][jb] = rb[q];
+            const int pb = b_p_fast ? (e % (TK / W)) * W : e / (kTile / W), jb = b_p_fast ? e / (TK / W) : (e % (kTile / W)) * W;
+#pragma unroll
+            for (int u = 0; u < W; ++u) Bs[pb + (b_p_fast ? u : 0)][jb + (b_p_fast ? 0 : u)] = fr.b[q][u];
         }
         __syncthreads();
         // the next K step's operands are loaded while this one runs on the matrix cores
-        if (p0 + kTileK < p_end) gemm_fetch<TI>(g, i0, j0, p0 + kTileK, p_end, ra, rb);
+        if (p0 + TK < p_end) gemm_fetch<TI, TK, VEC>(g, i0, j0, p0 + TK, p_end, fr);
+        if (rowsum)
+#pragma unroll 8
+            for (int kk = 0; kk < TK; ++kk) rs += As[t][kk];  // in p order; staged zeros past p_end
 #pragma unroll
-        for (int kk = 0; kk < kTileK; kk += 4) {
+        for (int kk = 0; kk < TK; kk += 4) {
             float a[XT], b[2];
 #pragma unroll
             for (int x = 0; x < XT; ++x) a[x] = As[wi + 16 * x + l % 16][kk + l / 16];
@@ -132,6 +172,11 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
         }
         __syncthreads();
     }
+    if (rowsum && i0 + t < g.I) {
+        const int i = i0 + t;
+        if (g.split) g.C[((int64_t)blockIdx.z * g.I + i) * g.J + g.J - 1] = rs;
+        else g.C[(int64_t)i * g.ldc + g.J - 1] = rs;
+    }
     // accumulator register r of tile (x, y) is C[wi + 16x + 4(l/16) + r][wj + 16y + l%16]
 #pragma unroll
     for (int x = 0; x < XT; ++x)
@@ -140,7 +185,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int i = i0 + wi + 16 * x + 4 * (l / 16) + r, j = j0 + wj + 16 * y + l % 16;
-                if (i >= g.I || j >= g.J) continue;
+                if (i >= g.I || j >= g.J - g.ones) continue;
                 float v = acc[x][y][r];
                 if (g.split) {
                     g.C[((int64_t)blockIdx.z * g.I + i) * g.J + j] = v;
@@ -156,9 +201,10 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
             }
 }
 
-// out[i] = sum over splits (in order) of partial[s][i], i < n
+// The sum over splits (in order) of partial[s][e], e < n = I J: to out[e], or, with bias_out, column
+// J - 1 to bias_out[e / J] and the others to out[(e / J)(J - 1) + e % J].
 __global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ partial, int splits, int64_t n,
-                                                   float *__restrict__ out) {
+                                                   float *__restrict__ out, int J, float *__restrict__ bias_out) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     float s = 0.f;
@@ -171,35 +217,16 @@ __global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ par
         for (int u = 0; u < 8; ++u) s += v[u];
     }
     for (; k < splits; ++k) s += partial[(int64_t)k * n + i];
-    out[i] = s;
+    if (!bias_out) {
+        out[i] = s;
+        return;
+    }
+    const int64_t r = i / J, c = i - r * J;
+    if (c == J - 1) bias_out[r] = s;
+    else out[r * (J - 1) + c] = s;
 }
 
 // Column sums of Y [rows][J] (row stride ldy), each row weighted by w[row] when w is given:
-// partial[c][j] = sum over chunk c's rows of w Y, 4 row phases per column summed in order.
-__global__ __launch_bounds__(256) void k_colsum(const float *__restrict__ Y, int64_t ldy, int rows, int J,
-                                                const float *__restrict__ w, int rows_per_chunk,
-                                                float *__restrict__ partial) {
-    __shared__ float part[4][64];
-    const int jj = threadIdx.x % 64, q = threadIdx.x / 64;
-    const int j = blockIdx.x * 64 + jj;
-    const int r0 = blockIdx.y * rows_per_chunk;
-    const int r1 = rows - r0 < rows_per_chunk ? rows : r0 + rows_per_chunk;
-    float s = 0.f;
-    if (j < J) {
-        int r = r0 + q;
-        for (; r + 12 < r1; r += 16) {  // four rows of this phase in flight, added in row order
-            float v[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = (w ? w[r + 4 * u] : 1.f) * Y[(int64_t)(r + 4 * u) * ldy + j];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) s += v[u];
-        }
-        for (; r < r1; r += 4) s += (w ? w[r] : 1.f) * Y[(int64_t)r * ldy + j];
-    }
-    part[q][jj] = s;
-    __syncthreads();
-    if (q == 0 && j < J) partial[(int64_t)blockIdx.y * J + j] = ((part[0][jj] + part[1][jj]) + part[2][jj]) + part[3][jj];
-}
 
 struct HeadArgs {
     const float *logits, *v, *logp_old, *adv, *ret;
@@ -368,19 +395,6 @@ int splits_for(int P) {
     return s < 1 ? 1 : s > kMaxSplits ? kMaxSplits : s;
 }
 
-// out[j] = sum over rows of (w[r]) Y[r][j], fixed order (chunks, then their sums in chunk order)
-int colsum(const float *Y, int64_t ldy, int rows, int J, const float *w, float *partial, float *out,
-           hipStream_t stream) {
-    const int chunks = (int)std::min<int64_t>(kColChunks, ceil_div(rows, 64));
-    const int per = (int)ceil_div(rows, chunks);
-    hipLaunchKernelGGL(k_colsum, dim3((unsigned)ceil_div(J, 64), (unsigned)chunks), dim3(256), 0, stream, Y, ldy, rows,
-                       J, w, per, partial);
-    HARL_HIP_CHECK(hipGetLastError());
-    hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(J, 256)), dim3(256), 0, stream, partial, chunks, (int64_t)J,
-                       out);
-    HARL_HIP_CHECK(hipGetLastError());
-    return HARL_OK;
-}
 
 struct Ws {
     float *h1, *h2, *logits, *v, *dlogits, *dv, *dz2, *dz1, *rows, *grad, *partial;
@@ -407,37 +421,60 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
     w.dz1 = take(Mp * c->h1);
     w.rows = take(Mp * 3);
     w.grad = take(L.n);
-    const int64_t big = std::max<int64_t>(std::max<int64_t>((int64_t)c->h1 * c->s, (int64_t)c->h2 * c->h1),
-                                          (int64_t)c->a * c->h2);
-    const int64_t cols = std::max<int64_t>(std::max(c->h1, c->h2), c->a);
-    w.partial = take(std::max<int64_t>((int64_t)kMaxSplits * big, (int64_t)kColChunks * cols));
+    // split-K partials of the weight-gradient GEMMs, each with its bias column
+    const int64_t big = std::max<int64_t>(std::max<int64_t>((int64_t)c->h1 * (c->s + 1), (int64_t)c->h2 * (c->h1 + 1)),
+                                          (int64_t)(c->a + 1) * (c->h2 + 1));
+    w.partial = take((int64_t)kMaxSplits * big);
     w.bytes = (size_t)off;
     return w;
 }
 
-int gemm(const GemmArgs &g0, float *partial, hipStream_t stream) {
-    GemmArgs g = g0;
-    const unsigned gx = (unsigned)ceil_div(g.J, kTile);
-    int used = 1;
-    if (g.split) {
-        const int splits = splits_for(g.P);
-        g.p_per_split = (int)round_up(ceil_div(g.P, splits), kTileK);
-        used = (int)ceil_div(g.P, g.p_per_split);
-    } else {
-        g.p_per_split = (int)round_up(g.P, kTileK);
-    }
-    float *out = g.C;
-    if (g.split) g.C = partial;
+// 16-byte operand loads are safe when each operand's contiguous dimension and other stride are
+// multiples of 4 and its base is 16-byte aligned (then a group of 4 is wholly in or out of range).
+bool vec_ok(const GemmArgs &g) {
+    if (!g.A || !aligned(g.A, 16) || !aligned(g.B, 16)) return false;
+    const bool a_ok = g.a_si == 1 ? (g.I % 4 == 0 && g.a_sp % 4 == 0) : (g.a_sp == 1 && g.P % 4 == 0 && g.a_si % 4 == 0);
+    const int J0 = g.J - g.ones;  // B's columns
+    const bool b_ok = g.b_sp == 1 ? (g.P % 4 == 0 && g.b_sj % 4 == 0) : (g.b_sj == 1 && J0 % 4 == 0 && g.b_sp % 4 == 0);
+    return a_ok && b_ok;
+}
+
+template <int TK, bool VEC>
+void launch_gemm(const GemmArgs &g, unsigned gx, int used, hipStream_t stream) {
     // 32-row tiles when 64-row tiles would leave the machine short of workgroups
     const bool small = (int64_t)gx * ceil_div(g.I, 64) * used < 1024 && g.I > 32;
     if (small)
-        hipLaunchKernelGGL(k_gemm<32>, dim3(gx, (unsigned)ceil_div(g.I, 32), used), dim3(kGemmThreads), 0, stream, g);
+        hipLaunchKernelGGL((k_gemm<32, TK, VEC>), dim3(gx, (unsigned)ceil_div(g.I, 32), used), dim3(kGemmThreads), 0,
+                           stream, g);
     else
-        hipLaunchKernelGGL(k_gemm<64>, dim3(gx, (unsigned)ceil_div(g.I, 64), used), dim3(kGemmThreads), 0, stream, g);
+        hipLaunchKernelGGL((k_gemm<64, TK, VEC>), dim3(gx, (unsigned)ceil_div(g.I, 64), used), dim3(kGemmThreads), 0,
+                           stream, g);
+}
+
+int gemm(const GemmArgs &g0, float *partial, hipStream_t stream) {
+    GemmArgs g = g0;
+    const unsigned gx = (unsigned)ceil_div(g.J - g.ones, kTile);
+    const bool vec = vec_ok(g);
+    const int tk = vec ? 2 * kTileK : kTileK;  // 64-deep K stages with 16-byte loads, else 32
+    int used = 1;
+    if (g.split) {
+        const int splits = splits_for(g.P);
+        g.p_per_split = (int)round_up(ceil_div(g.P, splits), tk);
+        used = (int)ceil_div(g.P, g.p_per_split);
+    } else {
+        g.p_per_split = (int)round_up(g.P, tk);
+    }
+    float *out = g.C;
+    if (g.split) g.C = partial;
+    if (vec)
+        launch_gemm<2 * kTileK, true>(g, gx, used, stream);
+    else
+        launch_gemm<kTileK, false>(g, gx, used, stream);
     HARL_HIP_CHECK(hipGetLastError());
     if (g.split) {
         const int64_t n = (int64_t)g.I * g.J;  // out is contiguous [I][J]
-        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, stream, partial, used, n, out);
+        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, stream, partial, used, n, out,
+                           g.J, g.bias_out);
     }
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
@@ -523,12 +560,17 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
         HARL_HIP_CHECK(hipGetLastError());
     }
     // ---- backward: heads ----
-    g = ga(w.dlogits, 1, a, w.h2, h2, 1, grad + L.wa, h2, a, h2, M);  // dWa = dlogits^T h2
+    // Each weight gradient's GEMM also returns the row sums of A in a last column of C (the
+    // bias gradient): the column-0 workgroups add up the A tiles they stage.
+    g = ga(w.dlogits, 1, a, w.h2, h2, 1, grad + L.wa, h2, a, h2 + 1, M);  // [dWa | dba] = dlogits^T [h2 | 1]
     g.split = 1;
+    g.ones = 1;
+    g.bias_out = grad + L.ba;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    if ((rc = colsum(w.dlogits, a, M, a, nullptr, w.partial, grad + L.ba, stream))) return rc;  // dba
-    if ((rc = colsum(w.h2, h2, M, h2, w.dv, w.partial, grad + L.wv, stream))) return rc;       // dwv = dv^T h2
-    if ((rc = colsum(w.dv, 1, M, 1, nullptr, w.partial, grad + L.bv, stream))) return rc;      // dbv
+    g = ga(w.dv, 0, 1, w.h2, h2, 1, grad + L.wv, h2 + 1, 1, h2 + 1, M);  // [dwv | dbv] = dv^T [h2 | 1] (wv, bv adjacent)
+    g.split = 1;
+    g.ones = 1;
+    if ((rc = gemm(g, w.partial, stream))) return rc;
     // dz2 = (dlogits Wa + dv wv) * [h2 > 0]
     g = ga(w.dlogits, a, 1, Wa, h2, 1, w.dz2, h2, M, h2, a);
     g.epi = kRank1Mask;
@@ -538,10 +580,11 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g.ldm = h2;
     if ((rc = gemm(g, w.partial, stream))) return rc;
     // ---- backward: layer 2 ----
-    g = ga(w.dz2, 1, h2, w.h1, h1, 1, grad + L.w2, h1, h2, h1, M);  // dW2 = dz2^T h1
+    g = ga(w.dz2, 1, h2, w.h1, h1, 1, grad + L.w2, h1, h2, h1 + 1, M);  // [dW2 | db2] = dz2^T [h1 | 1]
     g.split = 1;
+    g.ones = 1;
+    g.bias_out = grad + L.b2;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    if ((rc = colsum(w.dz2, h2, M, h2, nullptr, w.partial, grad + L.b2, stream))) return rc;
     // dz1 = (dz2 W2) * [h1 > 0]
     g = ga(w.dz2, h2, 1, W2, h1, 1, w.dz1, h1, M, h1, h2);
     g.epi = kRank1Mask;
@@ -550,10 +593,11 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g.ldm = h1;
     if ((rc = gemm(g, w.partial, stream))) return rc;
     // ---- backward: layer 1 ----
-    g = ga(w.dz1, 1, h1, X, s, 1, grad + L.w1, s, h1, s, M);  // dW1 = dz1^T X
+    g = ga(w.dz1, 1, h1, X, s, 1, grad + L.w1, s, h1, s + 1, M);  // [dW1 | db1] = dz1^T [X | 1]
     g.split = 1;
+    g.ones = 1;
+    g.bias_out = grad + L.b1;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    if ((rc = colsum(w.dz1, h1, M, h1, nullptr, w.partial, grad + L.b1, stream))) return rc;
     // ---- Adam ----
     const double bc1 = 1.0 - std::pow((double)c->beta1, step), bc2 = 1.0 - std::pow((double)c->beta2, step);
     hipLaunchKernelGGL(k_adam, dim3((unsigned)ceil_div(L.n, 256)), dim3(256), 0, stream, params, adam_m, adam_v, grad,
