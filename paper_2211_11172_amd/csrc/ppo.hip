@@ -5,9 +5,9 @@
 //
 // The network is the shared trunk of the policy kernels in fp32 (W1, W2 with ReLU) with the
 // per-type actor head of harl_policy_select and a value head.  One update:
-//   forward    h1 = relu(X W1^T + b1), h2 = relu(h1 W2^T + b2), logits = h2 Wa^T + ba,
-//              v = h2 wv^T + bv                                       (k_gemm, fused epilogues)
-//   objective  per row (k_ppo_heads): per-type log-softmax and entropy, logp = sum over types of
+//   forward    h1 = relu(X W1^T + b1), h2 = relu(h1 W2^T + b2), logits = h2 Wa^T + ba
+//                                                                      (k_gemm, fused epilogues)
+//   objective  per row (k_ppo_heads): v = h2 wv^T + bv, per-type log-softmax and entropy, logp = sum over types of
 //              the chosen actions' log-probabilities, ratio = exp(logp - logp_old), the clipped
 //              surrogate -min(ratio A, clip(ratio, 1 - eps, 1 + eps) A), w_v (v - R)^2 and the
 //              entropy bonus -w_e H, each averaged over the batch; their gradients with respect to
@@ -229,7 +229,9 @@ __global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ par
 // Column sums of Y [rows][J] (row stride ldy), each row weighted by w[row] when w is given:
 
 struct HeadArgs {
-    const float *logits, *v, *logp_old, *adv, *ret;
+    const float *logits, *logp_old, *adv, *ret;
+    const float *h2, *wv, *bv;  // the value head v = h2 . wv + bv is evaluated here
+    int h2n;
     const int32_t *actions;
     int M, a, n_seg;
     int32_t off[HARL_SELECT_MAX_SEGMENTS + 1];
@@ -261,11 +263,25 @@ constexpr int kHeadThreads = 256, kHeadLdsFloats = 4096;
 __global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
     __shared__ float zs[kHeadLdsFloats];
     __shared__ float s_lse[kHeadThreads], s_H[kHeadThreads], s_lp[kHeadThreads], s_gl[kHeadThreads];
+    __shared__ float s_v[kHeadThreads];
     const int t = threadIdx.x, a = h.a, ns = h.n_seg;
     const int64_t m0 = (int64_t)blockIdx.x * R;
     const int rows = h.M - m0 < R ? (int)(h.M - m0) : R;
     const int n = rows * a;
     for (int e = t; e < n; e += kHeadThreads) zs[e] = h.logits[m0 * a + e];
+    {  // value head: tpr threads per row (a power of two, within one wave), strided partial dot
+       // products combined by a butterfly of shuffles (fixed order)
+        int tpr = 64;
+        while (tpr * R > kHeadThreads) tpr >>= 1;
+        const int row = t / tpr, sub = t % tpr;
+        float acc = 0.f;
+        if (row < rows) {
+            const float *x = h.h2 + (m0 + row) * h.h2n;
+            for (int k = sub; k < h.h2n; k += tpr) acc += x[k] * h.wv[k];
+        }
+        for (int off = tpr / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, tpr);
+        if (sub == 0 && row < rows) s_v[row] = acc + h.bv[0];
+    }
     __syncthreads();
     const int p = t, r = p / ns, sg = p - r * ns;
     const bool own = p < rows * ns;
@@ -297,7 +313,7 @@ __global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
         const float active = s1 <= s2 ? 1.f : (inside ? 1.f : 0.f);
         const float inv_m = 1.f / (float)h.M;
         s_gl[t] = -(adv * ratio * active) * inv_m;
-        const float dvv = h.v[m] - h.ret[m];
+        const float dvv = s_v[t] - h.ret[m];
         h.dv[m] = h.w_v * 2.f * dvv * inv_m;
         float *rw = h.rows + m * 3;
         rw[0] = fminf(s1, s2);
@@ -397,7 +413,7 @@ int splits_for(int P) {
 
 
 struct Ws {
-    float *h1, *h2, *logits, *v, *dlogits, *dv, *dz2, *dz1, *rows, *grad, *partial;
+    float *h1, *h2, *logits, *dlogits, *dv, *dz2, *dz1, *rows, *grad, *partial;
     size_t bytes;
 };
 
@@ -414,7 +430,6 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
     w.h1 = take(Mp * c->h1);
     w.h2 = take(Mp * c->h2);
     w.logits = take(Mp * c->a);
-    w.v = take(Mp);
     w.dlogits = take(Mp * c->a);
     w.dv = take(Mp);
     w.dz2 = take(Mp * c->h2);
@@ -525,14 +540,13 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g.epi = kBias;
     g.bias = params + L.ba;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(w.h2, h2, 1, wv, 1, 0, w.v, 1, M, 1, h2);
-    g.epi = kBias;
-    g.bias = params + L.bv;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
     // ---- objective and its gradient at the logits and the value ----
     HeadArgs h{};
     h.logits = w.logits;
-    h.v = w.v;
+    h.h2 = w.h2;
+    h.wv = wv;
+    h.bv = params + L.bv;
+    h.h2n = h2;
     h.logp_old = logp_old;
     h.adv = adv;
     h.ret = ret;
