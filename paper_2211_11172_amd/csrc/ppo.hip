@@ -53,8 +53,11 @@ struct GemmArgs {
     const float *u, *w;           // rank-1 term u[i] w[j]
     const float *mask;            // multiply by [mask[i ldm + j] > 0]
     int64_t ldm;
+    int64_t u_si;                 // stride of u (0 = 1)
     int ones;                     // C's last column (j = J - 1) is A's row sums (B has J - 1 columns)
-    float *bias_out;              // split only: column J - 1 of the sum goes to bias_out[i]
+    float *bias_out;              // split only: column J - 1 of rows i < rows_w goes to bias_out[i]
+    int rows_w;                   // split only: rows i < rows_w go to C / bias_out (0 = all rows);
+    float *last_out;              //   row rows_w, if last_out, to last_out[j]; later rows nowhere
 };
 
 // Operand elements of the K step starting at p0 for this thread: A's TI x TK and B's TK x 64
@@ -194,17 +197,20 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
                 if (g.epi == kBias || g.epi == kBiasRelu) v += g.bias[j];
                 if (g.epi == kBiasRelu) v = fmaxf(v, 0.f);
                 if (g.epi == kRank1Mask) {
-                    if (g.u) v += g.u[i] * g.w[j];
+                    if (g.u) v += g.u[(int64_t)i * (g.u_si ? g.u_si : 1)] * g.w[j];
                     v = g.mask[(int64_t)i * g.ldm + j] > 0.f ? v : 0.f;
                 }
                 g.C[(int64_t)i * g.ldc + j] = v;
             }
 }
 
-// The sum over splits (in order) of partial[s][e], e < n = I J: to out[e], or, with bias_out, column
-// J - 1 to bias_out[e / J] and the others to out[(e / J)(J - 1) + e % J].
+// The sum over splits (in order) of partial[s][e], e < n = I J, row r = e / J, column c = e % J:
+// without bias_out to out[e]; with it, rows r < rows_w send column J - 1 to bias_out[r] and the
+// others to out[r (J - 1) + c], row rows_w goes to last_out[c] when last_out is given, and later
+// rows are dropped.
 __global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ partial, int splits, int64_t n,
-                                                   float *__restrict__ out, int J, float *__restrict__ bias_out) {
+                                                   float *__restrict__ out, int J, float *__restrict__ bias_out,
+                                                   int rows_w, float *__restrict__ last_out) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     float s = 0.f;
@@ -222,8 +228,13 @@ __global__ __launch_bounds__(256) void k_split_sum(const float *__restrict__ par
         return;
     }
     const int64_t r = i / J, c = i - r * J;
-    if (c == J - 1) bias_out[r] = s;
-    else out[r * (J - 1) + c] = s;
+    if (r >= rows_w) {
+        if (r == rows_w && last_out) last_out[c] = s;
+    } else if (c == J - 1) {
+        bias_out[r] = s;
+    } else {
+        out[r * (J - 1) + c] = s;
+    }
 }
 
 // Column sums of Y [rows][J] (row stride ldy), each row weighted by w[row] when w is given:
@@ -236,7 +247,8 @@ struct HeadArgs {
     int M, a, n_seg;
     int32_t off[HARL_SELECT_MAX_SEGMENTS + 1];
     float clip_eps, w_v, w_e;
-    float *dlogits, *dv, *rows;  // rows: [M][3] (min(s1, s2), (v - R)^2, entropy)
+    float *dlogits, *rows;  // dlogits: [M][ldd], dv in column a, zeros after; rows: [M][3] (min(s1, s2), (v - R)^2, entropy)
+    int ldd;
 };
 
 // Log-sum-exp and entropy of segment [lo, hi) of a logits row.
@@ -263,7 +275,7 @@ constexpr int kHeadThreads = 256, kHeadLdsFloats = 4096;
 __global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
     __shared__ float zs[kHeadLdsFloats];
     __shared__ float s_lse[kHeadThreads], s_H[kHeadThreads], s_lp[kHeadThreads], s_gl[kHeadThreads];
-    __shared__ float s_v[kHeadThreads];
+    __shared__ float s_v[kHeadThreads], s_dv[kHeadThreads];
     const int t = threadIdx.x, a = h.a, ns = h.n_seg;
     const int64_t m0 = (int64_t)blockIdx.x * R;
     const int rows = h.M - m0 < R ? (int)(h.M - m0) : R;
@@ -314,7 +326,7 @@ __global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
         const float inv_m = 1.f / (float)h.M;
         s_gl[t] = -(adv * ratio * active) * inv_m;
         const float dvv = s_v[t] - h.ret[m];
-        h.dv[m] = h.w_v * 2.f * dvv * inv_m;
+        s_dv[t] = h.w_v * 2.f * dvv * inv_m;
         float *rw = h.rows + m * 3;
         rw[0] = fminf(s1, s2);
         rw[1] = dvv * dvv;
@@ -333,7 +345,10 @@ __global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
         }
     }
     __syncthreads();
-    for (int e = t; e < n; e += kHeadThreads) h.dlogits[m0 * a + e] = zs[e];
+    for (int e = t; e < rows * h.ldd; e += kHeadThreads) {
+        const int r2 = e / h.ldd, c = e - r2 * h.ldd;
+        h.dlogits[m0 * h.ldd + e] = c < a ? zs[r2 * a + c] : (c == a ? s_dv[r2] : 0.f);
+    }
 }
 
 // loss[0..3] = (total, clip, value, entropy): fixed-order means of the row terms, one workgroup.
@@ -413,7 +428,7 @@ int splits_for(int P) {
 
 
 struct Ws {
-    float *h1, *h2, *logits, *dlogits, *dv, *dz2, *dz1, *rows, *grad, *partial;
+    float *h1, *h2, *logits, *dlogits, *dz2, *dz1, *rows, *grad, *partial;
     size_t bytes;
 };
 
@@ -430,15 +445,14 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
     w.h1 = take(Mp * c->h1);
     w.h2 = take(Mp * c->h2);
     w.logits = take(Mp * c->a);
-    w.dlogits = take(Mp * c->a);
-    w.dv = take(Mp);
+    w.dlogits = take(Mp * round_up(c->a + 1, 4));  // [M][a + 1 rounded to 4]: dlogits, dv, zeros
     w.dz2 = take(Mp * c->h2);
     w.dz1 = take(Mp * c->h1);
     w.rows = take(Mp * 3);
     w.grad = take(L.n);
     // split-K partials of the weight-gradient GEMMs, each with its bias column
     const int64_t big = std::max<int64_t>(std::max<int64_t>((int64_t)c->h1 * (c->s + 1), (int64_t)c->h2 * (c->h1 + 1)),
-                                          (int64_t)(c->a + 1) * (c->h2 + 1));
+                                          (int64_t)round_up(c->a + 1, 4) * (c->h2 + 1));
     w.partial = take((int64_t)kMaxSplits * big);
     w.bytes = (size_t)off;
     return w;
@@ -489,7 +503,7 @@ int gemm(const GemmArgs &g0, float *partial, hipStream_t stream) {
     if (g.split) {
         const int64_t n = (int64_t)g.I * g.J;  // out is contiguous [I][J]
         hipLaunchKernelGGL(k_split_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, stream, partial, used, n, out,
-                           g.J, g.bias_out);
+                           g.J, g.bias_out, g.rows_w ? g.rows_w : g.I, g.last_out);
     }
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
@@ -559,7 +573,7 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     h.w_v = c->w_value;
     h.w_e = c->w_entropy;
     h.dlogits = w.dlogits;
-    h.dv = w.dv;
+    h.ldd = (int)round_up(a + 1, 4);
     h.rows = w.rows;
     {
         // rows per workgroup: enough workgroups to cover the machine, at most kHeadLdsFloats logits
@@ -576,19 +590,21 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     // ---- backward: heads ----
     // Each weight gradient's GEMM also returns the row sums of A in a last column of C (the
     // bias gradient): the column-0 workgroups add up the A tiles they stage.
-    g = ga(w.dlogits, 1, a, w.h2, h2, 1, grad + L.wa, h2, a, h2 + 1, M);  // [dWa | dba] = dlogits^T [h2 | 1]
+    // [dWa | dba; dwv | dbv] = [dlogits, dv, 0]^T [h2 | 1]: rows < a to Wa's and ba's gradients,
+    // row a to wv's and bv's (adjacent in the parameter layout), the zero rows nowhere
+    const int ldd = (int)round_up(a + 1, 4);
+    g = ga(w.dlogits, 1, ldd, w.h2, h2, 1, grad + L.wa, h2, ldd, h2 + 1, M);
     g.split = 1;
     g.ones = 1;
     g.bias_out = grad + L.ba;
-    if ((rc = gemm(g, w.partial, stream))) return rc;
-    g = ga(w.dv, 0, 1, w.h2, h2, 1, grad + L.wv, h2 + 1, 1, h2 + 1, M);  // [dwv | dbv] = dv^T [h2 | 1] (wv, bv adjacent)
-    g.split = 1;
-    g.ones = 1;
+    g.rows_w = a;
+    g.last_out = grad + L.wv;
     if ((rc = gemm(g, w.partial, stream))) return rc;
     // dz2 = (dlogits Wa + dv wv) * [h2 > 0]
-    g = ga(w.dlogits, a, 1, Wa, h2, 1, w.dz2, h2, M, h2, a);
+    g = ga(w.dlogits, ldd, 1, Wa, h2, 1, w.dz2, h2, M, h2, a);
     g.epi = kRank1Mask;
-    g.u = w.dv;
+    g.u = w.dlogits + a;  // dv, column a
+    g.u_si = ldd;
     g.w = wv;
     g.mask = w.h2;
     g.ldm = h2;
