@@ -516,8 +516,8 @@ def oracle_threads():
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (candidates shard with "
-              "one all-gather of the top-k; see DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU only: there is no multi-GPU path here (candidates would shard by "
+              "program range, with one all-gather of each GPU's top-k)", file=sys.stderr)
         sys.exit(2)
     if args.ingest:
         ingest_calibration(args)

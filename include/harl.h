@@ -49,7 +49,7 @@ extern "C" {
 typedef enum {
     HARL_OK = 0,
     HARL_E_INVALID_ARG = -1, /* a null pointer, bad size, bad alignment or malformed model      */
-    HARL_E_UNSUPPORTED = -2, /* a valid request outside what this build implements               */
+    HARL_E_UNSUPPORTED = -2, /* a valid request outside what the library implements             */
     HARL_E_WORKSPACE = -3,   /* the workspace is smaller than the matching *_workspace_size()   */
     HARL_E_HIP = -4,         /* a HIP runtime call or kernel launch failed                      */
     HARL_E_NOMEM = -5        /* a device allocation failed (create calls only)                  */
