@@ -253,3 +253,28 @@ def test_throughput_measured_set_full_size():
                             np.arange(rows.size + 1, dtype=np.int32))
     np.testing.assert_array_equal(gm[rows], sc["stmt32"])
     torch.cuda.empty_cache()
+
+
+def test_refit_tree_scores_through_the_scoring_path():
+    """The GPU's refit tree, packed by harl_ensemble_create and evaluated by harl_score_round (an
+    independent kernel path) on the same statement rows, gives every row exactly the margin change
+    of the round (single tree, margins starting at 0) and every program the sum of its rows: the tree
+    arrays are a valid ensemble and thresholds, default directions and leaves agree with the bins."""
+    require_gpu()
+    from tests.gpu_util import gpu_score
+    m = _case(get_config("standard"), 254)
+    N, F = m["n_rows"], 164
+    bins = oracle.gbdt_bin_np(m["features"], N, m["cuts"], m["n_cuts"], 168)
+    got, gm = gpu_rounds(bins, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"],
+                         np.zeros(N, np.float32), 1, gamma=0.0)
+    tree = got[0]
+    assert (tree["feature"] >= 0).sum() >= 20
+    ens = dict(n_trees=1, n_features=F, n_nodes=tree["feature"].size, root=np.zeros(1, np.int32),
+               feature=tree["feature"], threshold=tree["threshold"], left=tree["left"], right=tree["right"],
+               default_left=tree["default_left"], leaf_value=tree["leaf_value"], base_score=0.0)
+    log("refit tree through harl_score_round: %d rows, %d splits" % (N, int((tree["feature"] >= 0).sum())))
+    prog, stmt = gpu_score(ens, m["features"], m["prog_ptr"])
+    np.testing.assert_array_equal(stmt, gm)
+    want_prog = np.array([gm[m["prog_ptr"][p]:m["prog_ptr"][p + 1]].astype(np.float64).sum()
+                          for p in range(len(m["prog_ptr"]) - 1)])
+    np.testing.assert_allclose(prog, want_prog, rtol=1e-6, atol=1e-7)
