@@ -36,7 +36,8 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGemmThreads = 256, kTile = 64, kTileK = 32;
-constexpr int kMaxSplits = 32;
+constexpr int kMaxSplits = 128;
+constexpr int kLossChunk = 4096;  // rows per loss partial (large batches)
 
 enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kRank1Mask = 3 };
 
@@ -249,6 +250,8 @@ struct HeadArgs {
     float clip_eps, w_v, w_e;
     float *dlogits, *rows;  // dlogits: [M][ldd], dv in column a, zeros after; rows: [M][3] (min(s1, s2), (v - R)^2, entropy)
     int ldd;
+    const float *wa;        // [a][h2n]: with wv, copied (a row per workgroup) into
+    float *wext;            // [ldd][h2n] = [Wa; wv; 0], the B operand of dz2 = [dlogits, dv, 0] wext
 };
 
 // Log-sum-exp and entropy of segment [lo, hi) of a logits row.
@@ -349,16 +352,19 @@ __global__ __launch_bounds__(kHeadThreads) void k_ppo_heads(HeadArgs h, int R) {
         const int r2 = e / h.ldd, c = e - r2 * h.ldd;
         h.dlogits[m0 * h.ldd + e] = c < a ? zs[r2 * a + c] : (c == a ? s_dv[r2] : 0.f);
     }
+    for (int r2 = blockIdx.x; r2 < h.ldd; r2 += gridDim.x)  // row r2 of [Wa; wv; 0] by workgroup r2
+        for (int c = t; c < h.h2n; c += kHeadThreads)
+            h.wext[(int64_t)r2 * h.h2n + c] = r2 < a ? h.wa[(int64_t)r2 * h.h2n + c] : (r2 == a ? h.wv[c] : 0.f);
 }
 
-// loss[0..3] = (total, clip, value, entropy): fixed-order means of the row terms, one workgroup.
-__global__ __launch_bounds__(256) void k_ppo_loss(const float *__restrict__ rows, int M, float w_v, float w_e,
-                                                  float *__restrict__ loss) {
+// Sums of the row terms over rows [r0, r1) by one workgroup: thread-strided in row order, then the
+// 256 thread sums in order.  Result in out (thread 0).
+__device__ void loss_rows(const float *__restrict__ rows, int r0, int r1, double (&out)[3]) {
     __shared__ double part[3][256];
     const int t = threadIdx.x;
     double s[3] = {0.0, 0.0, 0.0};
-    int m = t;
-    for (; m + 768 < M; m += 1024) {  // four rows of this thread in flight, added in row order
+    int m = r0 + t;
+    for (; m + 768 < r1; m += 1024) {  // four rows of this thread in flight, added in row order
         float v[4][3];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
@@ -369,17 +375,42 @@ __global__ __launch_bounds__(256) void k_ppo_loss(const float *__restrict__ rows
 #pragma unroll
             for (int c = 0; c < 3; ++c) s[c] += (double)v[u][c];
     }
-    for (; m < M; m += 256)
+    for (; m < r1; m += 256)
 #pragma unroll
         for (int c = 0; c < 3; ++c) s[c] += (double)rows[(int64_t)m * 3 + c];
 #pragma unroll
     for (int c = 0; c < 3; ++c) part[c][t] = s[c];
     __syncthreads();
     if (t == 0) {
-        double tot[3] = {0.0, 0.0, 0.0};
+        out[0] = out[1] = out[2] = 0.0;
         for (int k = 0; k < 256; ++k)
 #pragma unroll
-            for (int c = 0; c < 3; ++c) tot[c] += part[c][k];
+            for (int c = 0; c < 3; ++c) out[c] += part[c][k];
+    }
+}
+
+// Large batches: workgroup b sums rows [b kLossChunk, (b + 1) kLossChunk).
+__global__ __launch_bounds__(256) void k_ppo_loss_part(const float *__restrict__ rows, int M, double *__restrict__ lpart) {
+    double tot[3];
+    const int r0 = blockIdx.x * kLossChunk;
+    loss_rows(rows, r0, std::min(M, r0 + kLossChunk), tot);
+    if (threadIdx.x == 0)
+        for (int c = 0; c < 3; ++c) lpart[blockIdx.x * 3 + c] = tot[c];
+}
+
+// loss[0..3] = (total, clip, value, entropy): the means of the row terms; with lpart, the sums of
+// n_part chunk sums in chunk order, else the rows summed here.
+__global__ __launch_bounds__(256) void k_ppo_loss(const float *__restrict__ rows, int M, const double *__restrict__ lpart,
+                                                  int n_part, float w_v, float w_e, float *__restrict__ loss) {
+    double tot[3] = {0.0, 0.0, 0.0};
+    if (lpart) {
+        if (threadIdx.x != 0) return;
+        for (int b = 0; b < n_part; ++b)
+            for (int c = 0; c < 3; ++c) tot[c] += lpart[b * 3 + c];
+    } else {
+        loss_rows(rows, 0, M, tot);
+    }
+    if (threadIdx.x == 0) {
         const double clip = -tot[0] / M, value = tot[1] / M, ent = tot[2] / M;
         loss[0] = (float)(clip + (double)w_v * value - (double)w_e * ent);
         loss[1] = (float)clip;
@@ -421,14 +452,19 @@ Layout param_layout(const harl_ppo_config *c) {
     return L;
 }
 
-int splits_for(int P) {
-    int s = (int)ceil_div(P, 128);
-    return s < 1 ? 1 : s > kMaxSplits ? kMaxSplits : s;
+// Split-K pieces of a weight-gradient GEMM: enough for about 1,024 workgroups of 64 x 64 tiles, at
+// least 128 rows of the batch per piece, at most kMaxSplits.
+int splits_for(int P, int I, int J) {
+    const int64_t tiles = ceil_div(J, 64) * ceil_div(I, 64);
+    int64_t s = ceil_div(1024, tiles);
+    s = std::min<int64_t>(s, ceil_div(P, 128));
+    return (int)std::max<int64_t>(1, std::min<int64_t>(s, kMaxSplits));
 }
 
 
 struct Ws {
-    float *h1, *h2, *logits, *dlogits, *dz2, *dz1, *rows, *grad, *partial;
+    float *h1, *h2, *logits, *dlogits, *wext, *dz2, *dz1, *rows, *grad, *partial;
+    double *lpart;  // loss partials of row chunks (large batches)
     size_t bytes;
 };
 
@@ -446,6 +482,8 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
     w.h2 = take(Mp * c->h2);
     w.logits = take(Mp * c->a);
     w.dlogits = take(Mp * round_up(c->a + 1, 4));  // [M][a + 1 rounded to 4]: dlogits, dv, zeros
+    w.wext = take(round_up(c->a + 1, 4) * c->h2);
+    w.lpart = reinterpret_cast<double *>(take(2 * 3 * ceil_div(Mp, kLossChunk)));
     w.dz2 = take(Mp * c->h2);
     w.dz1 = take(Mp * c->h1);
     w.rows = take(Mp * 3);
@@ -487,7 +525,7 @@ int gemm(const GemmArgs &g0, float *partial, hipStream_t stream) {
     const int tk = vec ? 2 * kTileK : kTileK;  // 64-deep K stages with 16-byte loads, else 32
     int used = 1;
     if (g.split) {
-        const int splits = splits_for(g.P);
+        const int splits = splits_for(g.P, g.I, g.J - g.ones);
         g.p_per_split = (int)round_up(ceil_div(g.P, splits), tk);
         used = (int)ceil_div(g.P, g.p_per_split);
     } else {
@@ -574,6 +612,8 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     h.w_e = c->w_entropy;
     h.dlogits = w.dlogits;
     h.ldd = (int)round_up(a + 1, 4);
+    h.wa = Wa;
+    h.wext = w.wext;
     h.rows = w.rows;
     {
         // rows per workgroup: enough workgroups to cover the machine, at most kHeadLdsFloats logits
@@ -584,7 +624,15 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     }
     HARL_HIP_CHECK(hipGetLastError());
     if (loss_out) {
-        hipLaunchKernelGGL(k_ppo_loss, dim3(1), dim3(256), 0, stream, w.rows, M, c->w_value, c->w_entropy, loss_out);
+        if (M > 4 * kLossChunk) {  // one workgroup per chunk of rows, then the chunk sums in order
+            const int nb = (int)ceil_div(M, kLossChunk);
+            hipLaunchKernelGGL(k_ppo_loss_part, dim3((unsigned)nb), dim3(256), 0, stream, w.rows, M, w.lpart);
+            hipLaunchKernelGGL(k_ppo_loss, dim3(1), dim3(256), 0, stream, w.rows, M, w.lpart, nb, c->w_value,
+                               c->w_entropy, loss_out);
+        } else {
+            hipLaunchKernelGGL(k_ppo_loss, dim3(1), dim3(256), 0, stream, w.rows, M, nullptr, 0, c->w_value,
+                               c->w_entropy, loss_out);
+        }
         HARL_HIP_CHECK(hipGetLastError());
     }
     // ---- backward: heads ----
@@ -600,11 +648,10 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     g.rows_w = a;
     g.last_out = grad + L.wv;
     if ((rc = gemm(g, w.partial, stream))) return rc;
-    // dz2 = (dlogits Wa + dv wv) * [h2 > 0]
-    g = ga(w.dlogits, ldd, 1, Wa, h2, 1, w.dz2, h2, M, h2, a);
+    // dz2 = (dlogits Wa + dv wv) * [h2 > 0], one contraction over the padded columns
+    g = ga(w.dlogits, ldd, 1, w.wext, h2, 1, w.dz2, h2, M, h2, ldd);  // [dlogits, dv, 0] [Wa; wv; 0]
     g.epi = kRank1Mask;
-    g.u = w.dlogits + a;  // dv, column a
-    g.u_si = ldd;
+    g.u = nullptr;
     g.w = wv;
     g.mask = w.h2;
     g.ldm = h2;
