@@ -94,7 +94,7 @@ def _check_step(flat_before, m0, v0, step, batch, got, dims, segs):
     return m1, v1
 
 
-@pytest.mark.parametrize("M", [1, 70, 1000, 4096])
+@pytest.mark.parametrize("M", [1, 70, 1000, 4096, 20000, 65536])  # 20,000+: two-stage loss, up to 128 split pieces
 def test_ppo_update_matches_oracle(M):
     require_gpu()
     dims = (64, 256, 256, 26)
