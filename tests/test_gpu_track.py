@@ -103,7 +103,7 @@ def _adv_values(n, kind, seed):
     raise ValueError(kind)
 
 
-@pytest.mark.parametrize("n", [2, 3, 100, 4095, 4096, 4097, 65536, 100003])
+@pytest.mark.parametrize("n", [2, 3, 100, 4095, 4096, 4097, 16384, 16385, 40001, 65536, 65537, 100003])
 @pytest.mark.parametrize("kind", ["normal", "ties", "quantised"])
 def test_eliminate_matches_oracle(n, kind):
     require_gpu()
