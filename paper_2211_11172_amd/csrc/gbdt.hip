@@ -52,6 +52,7 @@ constexpr int kBinStride = 257;     // int64 words per (feature, G|H) histogram 
                                     // the 8 features' rows fall on different LDS banks
 constexpr int kHistWords = 2 * kGroup * kBinStride;
 constexpr int kScanBlock = kThreads; // flags per scan block (one per thread)
+constexpr int kBinRowBlocks = 8;     // at most this many 256-row blocks per binning workgroup
 
 struct Params {
     double eta, lambda, gamma, mcw, base;
@@ -109,11 +110,11 @@ __device__ __forceinline__ bool better(const Best &a, const Best &b) {
 // binning
 // ------------------------------------------------------------------------------------------
 // Thread = (row, 8-feature group); the group's cut points are staged in LDS first, so the binary
-// searches run on LDS.
+// searches run on LDS, and each workgroup then bins rb_per blocks of 256 rows with them.
 __global__ __launch_bounds__(kThreads) void k_gb_bin(const float *__restrict__ x, int64_t ldx, int F, int N,
                                                      const float *__restrict__ cuts, int cut_stride,
                                                      const int32_t *__restrict__ n_cuts, uint8_t *__restrict__ bins,
-                                                     int64_t ld) {
+                                                     int64_t ld, int rb_per) {
     __shared__ float sc[kGroup][256];
     __shared__ int snc[kGroup];
     const int g = blockIdx.y, t = threadIdx.x;
@@ -124,24 +125,26 @@ __global__ __launch_bounds__(kThreads) void k_gb_bin(const float *__restrict__ x
         if (i < snc[j]) sc[j][i] = cuts[(int64_t)(g * kGroup + j) * cut_stride + i];
     }
     __syncthreads();
-    const int r = blockIdx.x * kThreads + t;
-    if (r >= N) return;
-    uint64_t word = 0;
+    for (int rb = 0; rb < rb_per; ++rb) {
+        const int r = (blockIdx.x * rb_per + rb) * kThreads + t;
+        if (r >= N) return;
+        uint64_t word = 0;
 #pragma unroll
-    for (int j = 0; j < kGroup; ++j) {
-        const int f = g * kGroup + j;
-        if (f >= F) break;
-        const float v = x[(int64_t)f * ldx + r];
-        int lo = 0, hi = snc[j];
-        while (lo < hi) {  // number of cut points <= v
-            const int mid = (lo + hi) >> 1;
-            if (sc[j][mid] <= v) lo = mid + 1;
-            else hi = mid;
+        for (int j = 0; j < kGroup; ++j) {
+            const int f = g * kGroup + j;
+            if (f >= F) break;
+            const float v = x[(int64_t)f * ldx + r];
+            int lo = 0, hi = snc[j];
+            while (lo < hi) {  // number of cut points <= v
+                const int mid = (lo + hi) >> 1;
+                if (sc[j][mid] <= v) lo = mid + 1;
+                else hi = mid;
+            }
+            const uint64_t b = v != v ? 255u : (uint64_t)lo;
+            word |= b << (8 * j);
         }
-        const uint64_t b = v != v ? 255u : (uint64_t)lo;
-        word |= b << (8 * j);
+        *reinterpret_cast<uint64_t *>(bins + ((int64_t)g * ld + r) * kGroup) = word;
     }
-    *reinterpret_cast<uint64_t *>(bins + ((int64_t)g * ld + r) * kGroup) = word;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -835,8 +838,12 @@ int gbdt_bin_launch(const float *x, int64_t ldx, int32_t F, int32_t N, const flo
                     const int32_t *n_cuts, uint8_t *bins, int64_t ld, hipStream_t stream) {
     if (N == 0) return HARL_OK;
     // bytes of features past F in the last group are written as zeros
-    const dim3 grid((unsigned)ceil_div(N, kThreads), (unsigned)ceil_div(F, kGroup));
-    hipLaunchKernelGGL(k_gb_bin, grid, dim3(kThreads), 0, stream, x, ldx, F, N, cuts, cut_stride, n_cuts, bins, ld);
+    // several row blocks per cut staging on large sets, while keeping about 2,048 workgroups
+    const int64_t n_g = ceil_div(F, kGroup);
+    const int rb_per = (int)std::max<int64_t>(1, std::min<int64_t>(kBinRowBlocks, ceil_div(N, kThreads) * n_g / 2048));
+    const dim3 grid((unsigned)ceil_div(N, kThreads * rb_per), (unsigned)n_g);
+    hipLaunchKernelGGL(k_gb_bin, grid, dim3(kThreads), 0, stream, x, ldx, F, N, cuts, cut_stride, n_cuts, bins, ld,
+                       rb_per);
     HARL_HIP_CHECK(hipGetLastError());
     return HARL_OK;
 }
