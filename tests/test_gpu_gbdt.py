@@ -178,7 +178,7 @@ def test_standard_measured_set_bit_exact():
 
 
 @pytest.mark.parametrize("case", ["no rows", "one program", "constant features", "zero weights", "heavy mcw",
-                                  "huge gamma", "all missing", "empty programs"])
+                                  "huge gamma", "all missing", "empty programs", "extreme scales", "base score"])
 def test_degenerate_cases_bit_exact(case):
     require_gpu()
     cfg = mini_config(n_prog=200, s_max=5, n_features=11, p_nan=0.1)
@@ -203,6 +203,13 @@ def test_degenerate_cases_bit_exact(case):
         kw["gamma"] = 1e30
     elif case == "all missing":
         X = np.full_like(X, np.nan)
+    elif case == "extreme scales":  # fixed-point exponents far from 0
+        label = (label * np.float32(1e15)).astype(np.float32)
+        weight = (weight * np.float32(1e-12)).astype(np.float32)
+        kw["gamma"] = 0.0
+        kw["reg_lambda"] = 1e-20  # on the hessians' scale, so that splits still gain
+    elif case == "base score":
+        kw["base_score"] = -0.75
     elif case == "empty programs":
         counts = np.diff(ptr)
         counts[::3] = 0
