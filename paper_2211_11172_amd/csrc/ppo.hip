@@ -39,7 +39,7 @@ constexpr int kGemmThreads = 256, kTile = 64, kTileK = 32;
 constexpr int kMaxSplits = 128;
 constexpr int kLossChunk = 4096;  // rows per loss partial (large batches)
 
-enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kRank1Mask = 3 };
+enum Epilogue : int { kPlain = 0, kBias = 1, kBiasRelu = 2, kReluMask = 3 };
 
 struct GemmArgs {
     const float *A;  // null: A(i, p) = 1 (column sums)
@@ -51,10 +51,8 @@ struct GemmArgs {
     int I, J, P, p_per_split, split;
     int epi;
     const float *bias;            // bias[j]
-    const float *u, *w;           // rank-1 term u[i] w[j]
     const float *mask;            // multiply by [mask[i ldm + j] > 0]
     int64_t ldm;
-    int64_t u_si;                 // stride of u (0 = 1)
     int ones;                     // C's last column (j = J - 1) is A's row sums (B has J - 1 columns)
     float *bias_out;              // split only: column J - 1 of rows i < rows_w goes to bias_out[i]
     int rows_w;                   // split only: rows i < rows_w go to C / bias_out (0 = all rows);
@@ -197,10 +195,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(GemmArgs g) {
                 }
                 if (g.epi == kBias || g.epi == kBiasRelu) v += g.bias[j];
                 if (g.epi == kBiasRelu) v = fmaxf(v, 0.f);
-                if (g.epi == kRank1Mask) {
-                    if (g.u) v += g.u[(int64_t)i * (g.u_si ? g.u_si : 1)] * g.w[j];
-                    v = g.mask[(int64_t)i * g.ldm + j] > 0.f ? v : 0.f;
-                }
+                if (g.epi == kReluMask) v = g.mask[(int64_t)i * g.ldm + j] > 0.f ? v : 0.f;
                 g.C[(int64_t)i * g.ldc + j] = v;
             }
 }
@@ -650,9 +645,7 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     if ((rc = gemm(g, w.partial, stream))) return rc;
     // dz2 = (dlogits Wa + dv wv) * [h2 > 0], one contraction over the padded columns
     g = ga(w.dlogits, ldd, 1, w.wext, h2, 1, w.dz2, h2, M, h2, ldd);  // [dlogits, dv, 0] [Wa; wv; 0]
-    g.epi = kRank1Mask;
-    g.u = nullptr;
-    g.w = wv;
+    g.epi = kReluMask;
     g.mask = w.h2;
     g.ldm = h2;
     if ((rc = gemm(g, w.partial, stream))) return rc;
@@ -664,8 +657,7 @@ int ppo_update_launch(const harl_ppo_config *c, float *params, float *adam_m, fl
     if ((rc = gemm(g, w.partial, stream))) return rc;
     // dz1 = (dz2 W2) * [h1 > 0]
     g = ga(w.dz2, h2, 1, W2, h1, 1, w.dz1, h1, M, h1, h2);
-    g.epi = kRank1Mask;
-    g.u = nullptr;
+    g.epi = kReluMask;
     g.mask = w.h1;
     g.ldm = h1;
     if ((rc = gemm(g, w.partial, stream))) return rc;
