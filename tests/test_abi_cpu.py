@@ -198,3 +198,20 @@ def test_gbdt_argument_errors():
     assert r(label=None) == harl.HARL_E_INVALID_ARG
     assert r(ws=0x5001) == harl.HARL_E_INVALID_ARG
     assert r(wsb=64) == harl.HARL_E_WORKSPACE
+
+
+def test_header_is_plain_c():
+    """include/harl.h compiles on its own as C99 (pedantic) and as C++: a C ABI with no torch or HIP
+    types."""
+    import shutil
+    import subprocess
+    hdr = os.path.join(ROOT, "include", "harl.h")
+    for cc, args in (("gcc", ["-std=c99", "-pedantic", "-x", "c"]), ("g++", ["-std=c++11", "-x", "c++"])):
+        if shutil.which(cc) is None:
+            pytest.skip("%s not available" % cc)
+        r = subprocess.run([cc, *args, "-Wall", "-Wextra", "-Werror", "-fsyntax-only", hdr], capture_output=True,
+                           text=True)
+        assert r.returncode == 0, r.stderr
+    src = open(hdr).read()
+    for banned in ("torch", "hip_runtime", "at::", "c10::"):
+        assert banned not in src, banned
