@@ -483,10 +483,11 @@ Ws ws_layout(const harl_ppo_config *c, int32_t M, char *base) {
     w.dz1 = take(Mp * c->h1);
     w.rows = take(Mp * 3);
     w.grad = take(L.n);
-    // split-K partials of the weight-gradient GEMMs, each with its bias column
-    const int64_t big = std::max<int64_t>(std::max<int64_t>((int64_t)c->h1 * (c->s + 1), (int64_t)c->h2 * (c->h1 + 1)),
-                                          (int64_t)round_up(c->a + 1, 4) * (c->h2 + 1));
-    w.partial = take((int64_t)kMaxSplits * big);
+    // split-K partials of the weight-gradient GEMMs (each with its bias column), for the piece
+    // counts those GEMMs use at this batch size
+    const int ldd = (int)round_up(c->a + 1, 4);
+    auto need = [&](int I, int J0) { return (int64_t)splits_for((int)Mp, I, J0) * I * (J0 + 1); };
+    w.partial = take(std::max(std::max(need(ldd, c->h2), need(c->h2, c->h1)), need(c->h1, c->s)));
     w.bytes = (size_t)off;
     return w;
 }
