@@ -8,14 +8,14 @@
  *   harl_policy_step  the actor pi_theta(M|S) picks each candidate's next modification and the
  *                     critic V(S) gives its value (Algorithm 1, action selection; Eq. 6);
  *   harl_score_round  the cost model C(S') scores every candidate: a gradient-boosted tree
- *                     ensemble (XGBoost in the paper, Section 6.1, Appendix A.2) applied to each
+ *                     ensemble (XGBoost in the paper, Section 6.1, Appendix A.1) applied to each
  *                     statement's feature row and summed over the program's statements;
  *   harl_topk         the top-K candidates by predicted score (Algorithm 1, top-K phase;
  *                     Section 4.3, Top-K Selection Phase), optionally merged into a running top-K
  *                     that plays the heap H accumulating candidates across steps (Algorithm 1).
  *
  * Around the round: harl_track_advantage / harl_track_eliminate (reward, advantage and the
- * adaptive-stopping elimination of schedule tracks; Eq. 4, Section 5), harl_policy_select (one
+ * adaptive-stopping elimination of schedule tracks; Eq. 6, Section 5), harl_policy_select (one
  * action per modification type, greedy or sampled; Section 4.3), harl_ppo_update (the actor/critic's
  * training step; Section 6.1) and harl_gbdt_bin / harl_gbdt_round (the cost model's refit on
  * measured programs; Algorithm 1, Section 6.1).
@@ -64,7 +64,7 @@ const char *harl_last_error(void);
 const char *harl_version(void);
 
 /* ============================================================================================
- * Cost model: a GBDT ensemble (Section 6.1 and Appendix A.2: XGBoost with Ansor's settings).
+ * Cost model: a GBDT ensemble (Section 6.1 and Appendix A.1: XGBoost with Ansor's settings).
  * ============================================================================================ */
 
 /*
@@ -203,7 +203,7 @@ int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *str
 
 /* ============================================================================================
  * Per-modification-type action selection (Section 4.3: the best modification of each type;
- * Appendix A.2: num_iters^2 + 1 tile-size actions and 3 per other type; Section 6.1: PPO rollouts
+ * Appendix A.1: num_iters^2 + 1 tile-size actions and 3 per other type; Section 6.1: PPO rollouts
  * sample the actions).
  * ============================================================================================ */
 
@@ -237,8 +237,8 @@ int harl_policy_select(const float *d_logits, int32_t B, int32_t a, const int32_
                        int32_t *d_action, float *d_logp, float *d_probs, void *stream);
 
 /* ============================================================================================
- * PPO update of the actor/critic (Algorithm 1: train the actor with the policy gradient of Eq. 3
- * and the critic with the MSE of the advantage Y; Section 6.1: PPO; Table 8: weights and rates).
+ * PPO update of the actor/critic (Algorithm 1: train the actor with the policy gradient of Eq. 5
+ * and the critic with the MSE of the advantage Y; Section 6.1: PPO; Table 5: weights and rates).
  * ============================================================================================ */
 
 /* Sizes and hyper-parameters of the trained fp32 network (the shared trunk of harl_policy_desc
@@ -248,8 +248,8 @@ typedef struct {
     int32_t n_seg;             /* modification types, 1..HARL_SELECT_MAX_SEGMENTS */
     int32_t seg_offsets[HARL_SELECT_MAX_SEGMENTS + 1];  /* 0 = o_0 < ... < o_n_seg = a */
     float clip_eps;            /* PPO clip range (0.2) */
-    float w_value, w_entropy;  /* loss weights (0.5, 0.01; Table 8) */
-    float lr_actor, lr_critic; /* Adam rates: trunk + actor head, value head (3e-4, 1e-3; Table 8) */
+    float w_value, w_entropy;  /* loss weights (0.5, 0.01; Table 5) */
+    float lr_actor, lr_critic; /* Adam rates: trunk + actor head, value head (3e-4, 1e-3; Table 5) */
     float beta1, beta2, adam_eps;  /* Adam (0.9, 0.999, 1e-8) */
 } harl_ppo_config;
 
@@ -272,7 +272,7 @@ size_t harl_ppo_workspace_size(const harl_ppo_config *cfg, int32_t M);
  *   P = harl_ppo_param_count(cfg).
  *   d_states [M][s] fp32; d_actions [M][n_seg] int32 (row-global indices, each in its segment;
  *   others are clamped into it); d_logp_old, d_adv, d_ret [M] fp32 (the behaviour policy's
- *   log-probability, the advantage of Eq. 4 and the critic's target R).
+ *   log-probability, the advantage of Eq. 6 and the critic's target R).
  *   d_grad   [P] out, or NULL: the gradient of this step.
  *   d_loss   [4] out, or NULL: total, clipped-surrogate, value-MSE and entropy terms.
  *   d_ws, ws_bytes: at least harl_ppo_workspace_size(cfg, M) bytes, 256-byte aligned.
@@ -285,7 +285,7 @@ int harl_ppo_update(const harl_ppo_config *cfg, float *d_params, float *d_adam_m
 
 /* ============================================================================================
  * Schedule tracks between rounds: reward and advantage of a modification step (Algorithm 1,
- * Eq. 4) and the adaptive-stopping elimination (Section 5).
+ * Eq. 6) and the adaptive-stopping elimination (Section 5).
  * ============================================================================================ */
 
 /*
@@ -294,13 +294,21 @@ int harl_ppo_update(const harl_ppo_config *cfg, float *d_params, float *d_adam_m
  *   reward     r = (C(s') - C(s)) / max(|C(s)|, eps)     (Algorithm 1's relative score change;
  *                  the denominator is read as max(|C(s)|, eps) so that signed scores keep the sign
  *                  of an improvement and a zero score stays finite)
- *   advantage  A = r + gamma * V(s') - V(s)             (Eq. 4; the paper uses gamma = 0.9)
+ *   advantage  A = r + gamma * V(s') - V(s)             (Eq. 6; the paper uses gamma = 0.9)
  * computed in fp32.  All arrays [n] fp32, 4-byte aligned, device memory; d_reward may be NULL.
  * NaN inputs propagate.  n == 0 is a no-op; eps must be > 0 and finite.
  */
 int harl_track_advantage(const float *d_c_prev, const float *d_c_next, const float *d_v_prev,
                          const float *d_v_next, int32_t n, float gamma, float eps, float *d_reward,
                          float *d_adv, void *stream);
+
+/*
+ * Tracks kept by one adaptive-stopping elimination (Section 5: after every window of lambda steps
+ * the proportion rho of the tracks with the lowest advantage is eliminated): the eliminated count
+ * is floor(rho * n), computed in double precision, so *n_keep = n - floor(rho * n).  Host-only
+ * arithmetic (no device call); 0 <= rho <= 1 (the paper uses rho = 0.5), n >= 0.
+ */
+int harl_track_keep_count(int32_t n, double rho, int32_t *n_keep);
 
 /* Bytes of device workspace harl_track_eliminate needs for n tracks. */
 size_t harl_track_eliminate_workspace_size(int32_t n);
@@ -325,7 +333,7 @@ int harl_track_eliminate(const float *d_adv, int32_t n, int32_t n_keep, int32_t 
 
 /* ============================================================================================
  * Refit of the cost model on measured programs (Algorithm 1: the top-K states are measured and
- * the cost model is trained on (S^, P); Section 6.1 and Appendix A.2: XGBoost with Ansor's
+ * the cost model is trained on (S^, P); Section 6.1 and Appendix A.1: XGBoost with Ansor's
  * settings).  Histogram-based gradient boosting (Chen and Guestrin, KDD'16, Sections 3 and 3.4).
  * ============================================================================================ */
 

@@ -196,7 +196,7 @@ def merge(run_score: np.ndarray, run_index: np.ndarray, score: np.ndarray, index
 
 
 def track_advantage(c_prev, c_next, v_prev, v_next, gamma: float = 0.9, eps: float = 1e-6) -> dict:
-    """Reward (Algorithm 1, denominator max(|C(s)|, eps)) and advantage (Eq. 4) of one step of
+    """Reward (Algorithm 1, denominator max(|C(s)|, eps)) and advantage (Eq. 6) of one step of
     every schedule track, fp64 over the fp32 inputs; ``scale`` = |r| + |gamma V(s')| + |V(s)|.
     ``gamma`` and ``eps`` are taken at their fp32 values (the values the GPU path computes with)."""
     lib = _load()

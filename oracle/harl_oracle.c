@@ -7,7 +7,7 @@
  *
  *   oracle_score_round   cost-model prediction C(S') of every candidate (Algorithm 1, the reward
  *                        step and the heap-insert step; Section 4.3; the cost model is XGBoost,
- *                        Section 6.1 and Appendix A.2), here a GBDT applied to each statement's
+ *                        Section 6.1 and Appendix A.1), here a GBDT applied to each statement's
  *                        feature row and summed over the statements of a program;
  *   oracle_policy_step   actor pi_theta(M|S) and critic V(S) forward (Algorithm 1, action
  *                        selection; Eq. 6 for the critic's role; Section 4.3), a shared ReLU
@@ -16,11 +16,11 @@
  *                        Section 4.3, Top-K Selection Phase): the K best predicted scores;
  *   oracle_merge         the heap H accumulating candidates across steps (Algorithm 1);
  *   oracle_track_advantage  reward of a modification step (Algorithm 1) and the advantage of
- *                        Eq. 4 for every schedule track;
+ *                        Eq. 6 for every schedule track;
  *   oracle_track_eliminate  adaptive-stopping elimination of the tracks with the lowest
  *                        advantages (Section 5);
  *   oracle_policy_select  one action per modification type from the actor's logits (Section 4.3:
- *                        the best modification of each type; Appendix A.2: num_iters^2 + 1 tile
+ *                        the best modification of each type; Appendix A.1: num_iters^2 + 1 tile
  *                        actions and 3 for each other type), greedy or sampled as PPO rollouts
  *                        do (Section 6.1), with the per-type softmax and log-probability;
  *   oracle_philox4x32    the counter-based generator the sampling draws from (Salmon, Moraes,
@@ -31,7 +31,7 @@
  * smoke check and bench.py's CPU-baseline leg may load this library; the HIP path shares no code
  * with it.  Built with plain -O2 (never -ffast-math: NaN tests must survive).
  *
- * Readings where the paper is silent (each also listed in the design doc):
+ * Readings where the paper is silent:
  *   - a split sends x left iff x < threshold (strict), x == threshold goes right;
  *   - only NaN is missing; a missing value follows the node's default direction;
  *   - a program's score is base_score + the sum of its statements' scores;
@@ -332,7 +332,7 @@ int oracle_merge(float *run_score, int64_t *run_index, int32_t k,
 /* One modification step of n schedule tracks.  Track i moved from state s (predicted score
  * c_prev[i], critic value v_prev[i]) to s' (c_next[i], v_next[i]).  Algorithm 1 rewards the step
  * with the relative change of the cost model's score, r = (C(s') - C(s)) / C(s), here with the
- * denominator max(|C(s)|, eps); Eq. 4 gives the advantage A = r + gamma V(s') - V(s).
+ * denominator max(|C(s)|, eps); Eq. 6 gives the advantage A = r + gamma V(s') - V(s).
  * scale[i] = |r| + |gamma V(s')| + |V(s)| bounds the terms of A (scale-relative tolerance). */
 int oracle_track_advantage(const float *c_prev, const float *c_next, const float *v_prev,
                            const float *v_next, int64_t n, double gamma, double eps,
@@ -453,7 +453,7 @@ int oracle_policy_select(const float *logits, int64_t B, int32_t a, const int32_
 
 /* ------------------------------------------------------------------------------------------- */
 /* Refit of the cost model on measured programs (Algorithm 1, its last steps: the top-K states
- * are measured and the cost model is trained on (S^, P); Section 6.1 and Appendix A.2: XGBoost
+ * are measured and the cost model is trained on (S^, P); Section 6.1 and Appendix A.1: XGBoost
  * with Ansor's settings).  One boosting round of histogram-based gradient boosting (Chen and
  * Guestrin, KDD'16, Section 3: the second-order gain and the optimal leaf weight; Section 3.4:
  * the sparsity-aware default direction) under the pack-sum squared error: a program's prediction
@@ -461,7 +461,7 @@ int oracle_policy_select(const float *logits, int64_t B, int32_t a, const int32_
  * 1/2 sum_p w_p (s_p - y_p)^2, so every statement row of program p carries the gradient
  * w_p (s_p - y_p) and the hessian w_p.
  *
- * Readings (each also listed in the design doc):
+ * Readings where the paper is silent:
  *   - features are binned per feature by caller-given increasing cut points: bin(x) = the number
  *     of cut points <= x (0 .. n_cuts), 255 for NaN (missing);
  *   - a candidate split (f, t, dir) sends bins < t left, t in 1 .. n_cuts[f], and the missing

@@ -2,11 +2,11 @@
 
 The paper trains its actor and critic with PPO (Section 6.1, after Schulman et al., "Proximal
 Policy Optimization Algorithms", 2017): Algorithm 1 samples a mini-batch from the replay buffer,
-trains the actor with the policy gradient of Eq. 3 (in PPO's clipped form) and the critic with the
-MSE of the advantage Y (Eq. 4); Table 8 gives the weights 0.5 (value MSE) and 0.01 (entropy) and the
+trains the actor with the policy gradient of Eq. 5 (in PPO's clipped form) and the critic with the
+MSE of the advantage Y (Eq. 6); Table 5 gives the weights 0.5 (value MSE) and 0.01 (entropy) and the
 learning rates 3e-4 (actor) and 1e-3 (critic).
 
-Readings (each also listed in the design doc):
+Readings where the paper is silent:
   - network: the shared trunk s -> h1 -> h2 (ReLU) with a linear actor head (the per-type
     segments of harl_policy_select) and a linear value head; parameters in PyTorch nn.Linear
     layout, packed W1, b1, W2, b2, Wa, ba, wv, bv;
@@ -15,7 +15,7 @@ Readings (each also listed in the design doc):
   - loss = -mean(min(ratio A, clip(ratio, 1 - eps, 1 + eps) A)) + w_v mean((V(s) - R)^2)
     - w_e mean(entropy), ratio = exp(logp - logp_old), eps = 0.2 (PPO's default; the paper gives
     none); R = r + gamma V(s') is the critic's target, held fixed (minimising the squared
-    advantage of Eq. 4);
+    advantage of Eq. 6);
   - derivatives at the kinks follow the reference framework's conventions: min passes the
     gradient to the unclipped term when the two are equal, clip passes it for
     1 - eps <= ratio <= 1 + eps, ReLU's derivative at 0 is 0;

@@ -238,6 +238,13 @@ int harl_track_advantage(const float *d_c_prev, const float *d_c_next, const flo
                                         static_cast<hipStream_t>(stream));
 }
 
+int harl_track_keep_count(int32_t n, double rho, int32_t *n_keep) {
+    if (!n_keep) return fail(HARL_E_INVALID_ARG, "harl_track_keep_count: null n_keep");
+    if (n < 0 || !(rho >= 0.0 && rho <= 1.0)) return fail(HARL_E_INVALID_ARG, "harl_track_keep_count: need n >= 0, 0 <= rho <= 1");
+    *n_keep = n - (int32_t)std::floor(rho * (double)n);
+    return HARL_OK;
+}
+
 size_t harl_track_eliminate_workspace_size(int32_t n) {
     if (n < 0) return 0;
     return harl::track_eliminate_ws_bytes(n);

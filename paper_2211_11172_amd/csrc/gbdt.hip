@@ -1,5 +1,5 @@
 // Refit of the cost model on measured programs (Algorithm 1: the top-K states are measured and
-// the cost model is trained on (S^, P); Section 6.1 and Appendix A.2: XGBoost with Ansor's
+// the cost model is trained on (S^, P); Section 6.1 and Appendix A.1: XGBoost with Ansor's
 // settings).  One boosting round of histogram-based gradient boosting under the pack-sum squared
 // error 1/2 sum_p w_p (s_p - y_p)^2, s_p = base + the sum of program p's statement margins; the
 // gain, leaf weight and learned missing direction follow Chen and Guestrin (KDD'16, Sections 3

@@ -523,13 +523,6 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     // use 16 states per workgroup so that they still spread over every CU.
     int nsg = B >= 16 * 1024 ? (bf ? 4 : 2) : 1;
     int u = nsg == 4 ? 4 : 8;
-    if (const char *env = std::getenv("HARL_POLICY_CFG")) {  // "nsg,u" (tuning sweeps)
-        int e_nsg = 0, e_u = 0;
-        if (std::sscanf(env, "%d,%d", &e_nsg, &e_u) == 2) {
-            nsg = e_nsg;
-            u = e_u;
-        }
-    }
     if (policy_lds_bytes(P, nsg, u) > 160 * 1024) {
         nsg = 1;
         u = 8;

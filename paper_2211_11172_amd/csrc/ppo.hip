@@ -1,6 +1,6 @@
 // One PPO update of the actor/critic (HARL paper, Algorithm 1: sample a mini-batch from the replay
-// buffer, train the actor with the policy gradient of Eq. 3 and the critic with the MSE of the
-// advantage Y of Eq. 4; Section 6.1: PPO; Table 8: value weight 0.5, entropy weight 0.01, learning
+// buffer, train the actor with the policy gradient of Eq. 5 and the critic with the MSE of the
+// advantage Y of Eq. 6; Section 6.1: PPO; Table 5: value weight 0.5, entropy weight 0.01, learning
 // rates 3e-4 / 1e-3).
 //
 // The network is the shared trunk of the policy kernels in fp32 (W1, W2 with ReLU) with the

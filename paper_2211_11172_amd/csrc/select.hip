@@ -1,5 +1,5 @@
 // Per-modification-type action selection (HARL paper, Section 4.3: the actor returns the best
-// modification of each modification type; Appendix A.2: num_iters^2 + 1 tile-size actions and 3
+// modification of each modification type; Appendix A.1: num_iters^2 + 1 tile-size actions and 3
 // for each other type; Section 6.1: PPO, whose rollouts sample the actions).
 //
 // K9 k_policy_select: one (state, segment) per thread.  The actor's logits row of a state is cut

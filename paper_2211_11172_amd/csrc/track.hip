@@ -1,11 +1,11 @@
 // Schedule tracks between rounds (HARL paper, Algorithm 1 and Section 5): the reward of a
-// modification step, its advantage (Eq. 4), and the adaptive-stopping elimination of the tracks
+// modification step, its advantage (Eq. 6), and the adaptive-stopping elimination of the tracks
 // with the lowest advantages.
 //
 // K7 k_track_advantage: one thread per track, fp32:
 //      r = (C(s') - C(s)) / max(|C(s)|, eps)   -- Algorithm 1's relative score change, with the
 //                                                 denominator read as max(|C(s)|, eps)
-//      A = r + gamma V(s') - V(s)              -- Eq. 4
+//      A = r + gamma V(s') - V(s)              -- Eq. 6
 // K8 elimination: the n_keep tracks ranked first by (advantage desc, NaN last, -0 ties +0, lower
 //    track index first) survive; their indices are written in ascending order (the live set is
 //    compacted in place order), optionally with their rows of a per-track matrix.

@@ -32,7 +32,7 @@ EXPORTS = (
     "harl_topk_workspace_size", "harl_topk", "harl_topk_reset",
     "harl_policy_select",
     "harl_ppo_param_count", "harl_ppo_workspace_size", "harl_ppo_update",
-    "harl_track_advantage", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
+    "harl_track_advantage", "harl_track_keep_count", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
     "harl_gbdt_bin", "harl_gbdt_round_workspace_size", "harl_gbdt_round",
 )
 HARL_GBDT_MAX_DEPTH = 12
@@ -127,6 +127,7 @@ def load():
                 "harl_policy_select": ([P, i32, i32, P, i32, u32, ctypes.c_uint64, ctypes.c_uint64, P, P, P, P],
                                        ctypes.c_int),
                 "harl_track_advantage": ([P, P, P, P, i32, ctypes.c_float, ctypes.c_float, P, P, P], ctypes.c_int),
+                "harl_track_keep_count": ([i32, ctypes.c_double, P], ctypes.c_int),
                 "harl_track_eliminate_workspace_size": ([i32], sz),
                 "harl_track_eliminate": ([P, i32, i32, P, P, i64, P, P, sz, P], ctypes.c_int),
                 "harl_gbdt_bin": ([P, i64, i32, i32, P, i32, P, P, i64, P], ctypes.c_int),
@@ -318,10 +319,10 @@ def harl_track_eliminate(adv, n: int, n_keep: int, keep_index, rows=None, row_by
                                        _ptr(ws), ws_bytes, _stream(stream)), "harl_track_eliminate")
 
 
-def eliminate_keep_count(n: int, rho: float = 0.5) -> int:
-    """Tracks left after one adaptive-stopping elimination of proportion rho: floor(rho * n) are
-    dropped."""
-    return n - int(rho * n // 1)
+def harl_track_keep_count(n: int, rho: float = 0.5) -> int:
+    out = ctypes.c_int32(0)
+    _check(load().harl_track_keep_count(n, ctypes.c_double(rho), ctypes.byref(out)), "harl_track_keep_count")
+    return int(out.value)
 
 
 # ------------------------------------------------------------------------------------------------

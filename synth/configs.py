@@ -7,8 +7,8 @@ statement is one row of ``n_features`` fp32 features.  The cost model is a compl
 an actor head of ``pol_a`` logits and a one-unit value head.
 
 The paper prints none of these sizes (its cost model follows Ansor's XGBoost setup, Section 6.1 and
-Appendix A.2; its actor/critic follows an external PPO code base).  The sizes below are the
-workloads this implementation is measured on; the design doc lists them with their recipe.
+Appendix A.1; its actor/critic follows an external PPO code base).  The sizes below are the
+workloads this implementation is measured on, each with its generation recipe in `synth.gen`.
 """
 from __future__ import annotations
 

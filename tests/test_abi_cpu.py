@@ -38,6 +38,20 @@ def _status(fn, *args):
     return getattr(harl.load(), fn)(*args)
 
 
+def test_track_keep_count_matches_the_oracle_rule():
+    """Host-only arithmetic behind the ABI: n - floor(rho n) tracks survive (Section 5)."""
+    import oracle
+    for n in (0, 1, 2, 3, 7, 64, 65, 100, 4095, 4096, 65537, 1048653, 2**31 - 1):
+        for rho in (0.0, 0.25, 0.3, 0.5, 0.75, 0.999, 1.0):
+            assert harl.harl_track_keep_count(n, rho) == oracle.eliminate_count(n, rho), (n, rho)
+    out = ctypes.c_int32(0)
+    lib = harl.load()
+    assert lib.harl_track_keep_count(-1, ctypes.c_double(0.5), ctypes.byref(out)) == harl.HARL_E_INVALID_ARG
+    assert lib.harl_track_keep_count(10, ctypes.c_double(1.5), ctypes.byref(out)) == harl.HARL_E_INVALID_ARG
+    assert lib.harl_track_keep_count(10, ctypes.c_double(float("nan")), ctypes.byref(out)) == harl.HARL_E_INVALID_ARG
+    assert lib.harl_track_keep_count(10, ctypes.c_double(0.5), None) == harl.HARL_E_INVALID_ARG
+
+
 def test_topk_argument_errors():
     assert _status("harl_topk", None, 10, 11, 0, None, None, 0, None, 0, None) == harl.HARL_E_INVALID_ARG
     assert "k > n" in harl.harl_last_error()

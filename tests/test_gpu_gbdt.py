@@ -1,5 +1,5 @@
 """GPU parity of the cost-model refit (Algorithm 1: the cost model is trained on the measured
-top-K; Section 6.1 and Appendix A.2: XGBoost with Ansor's settings) against the oracle.
+top-K; Section 6.1 and Appendix A.1: XGBoost with Ansor's settings) against the oracle.
 
 Bar: bit-exact.  Binning is integer work; the tree is a sequence of decisions taken on exact
 64-bit integer sums and on fp64 gains evaluated by the same expressions in the same order on both

@@ -1,5 +1,5 @@
 """GPU parity of harl_ppo_update (one PPO update of the actor/critic: Algorithm 1's training step,
-Eq. 3 in PPO's clipped form, the critic's MSE of Eq. 4's advantage; Section 6.1; Table 8) against
+Eq. 5 in PPO's clipped form, the critic's MSE of Eq. 6's advantage; Section 6.1; Table 5) against
 the fp64 oracle (oracle/ppo.py).
 
 Bars: loss terms within 1e-4 relative; every gradient entry within 1e-5 of its running error scale

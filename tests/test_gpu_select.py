@@ -1,5 +1,5 @@
 """GPU parity of harl_policy_select (one action per modification type, Section 4.3 and Appendix
-A.2; sampled as in PPO rollouts, Section 6.1) against the oracle.
+A.1; sampled as in PPO rollouts, Section 6.1) against the oracle.
 
 Bars: greedy actions bit-exact on the same fp32 logits; sampled actions equal to the oracle's on the
 same logits (the noise and the decision are fp64 on both sides, so only two candidates within a

@@ -1,5 +1,5 @@
 """GPU parity of the schedule-track calls against the oracle: reward and advantage of a step
-(Algorithm 1, Eq. 4) and the adaptive-stopping elimination (Section 5).
+(Algorithm 1, Eq. 6) and the adaptive-stopping elimination (Section 5).
 
 Bars: advantages and rewards within 1e-6 of their oracle scale (|r| + |gamma V(s')| + |V(s)| for
 the advantage, |r| for the reward) -- a handful of fp32 roundings; the exact variant bit-exact;

@@ -1,5 +1,5 @@
 """Pins of the oracle's cost-model refit (one boosting round; Algorithm 1, the training of the cost
-model on the measured top-K; Section 6.1 and Appendix A.2: XGBoost with Ansor's settings; the gain,
+model on the measured top-K; Section 6.1 and Appendix A.1: XGBoost with Ansor's settings; the gain,
 leaf weight and default direction of Chen and Guestrin, KDD'16, Sections 3 and 3.4) against
 things other than the oracle: numpy's searchsorted, an exact rational brute force over every
 candidate split, closed forms of isolated programs and of a step function, and the scoring

@@ -1,11 +1,11 @@
 """Pins of the CPU oracle against things other than itself (brute force, closed forms, invariants,
 library routines).  Paper anchors: the cost model C scores every new schedule (Algorithm 1; the
-cost model is XGBoost, Section 6.1, Appendix A.2); the actor and critic act on the states
+cost model is XGBoost, Section 6.1, Appendix A.1); the actor and critic act on the states
 (Algorithm 1; Section 4.3, Eq. 6); the top-K of the heap H are the K best predicted scores
 (Algorithm 1; Section 4.3, Top-K Selection Phase); each step of a schedule track is rewarded with
-the relative change of its score (Algorithm 1) and judged by the advantage of Eq. 4, and the
+the relative change of its score (Algorithm 1) and judged by the advantage of Eq. 6, and the
 adaptive-stopping search drops the tracks of lowest advantage (Section 5); the actor picks the best
-modification of each type (Section 4.3, Appendix A.2), sampled during PPO rollouts (Section 6.1)."""
+modification of each type (Section 4.3, Appendix A.1), sampled during PPO rollouts (Section 6.1)."""
 from __future__ import annotations
 
 import numpy as np
