@@ -56,9 +56,8 @@ int harl_ensemble_create(const harl_ensemble_desc *desc, harl_ensemble **out, vo
 
 int harl_ensemble_destroy(harl_ensemble *ens) {
     if (!ens) return HARL_OK;
-    hipError_t e = hipFree(ens->d_trees);
-    delete ens;
-    return e == hipSuccess ? HARL_OK : harl::hip_fail(e, "harl_ensemble_destroy");
+    harl::free_ensemble(ens);
+    return HARL_OK;
 }
 
 int harl_ensemble_info(const harl_ensemble *ens, int32_t *n_trees, int32_t *depth, int32_t *n_features) {

@@ -6,6 +6,7 @@
 #include <cstddef>
 #include <cstdint>
 #include <string>
+#include <vector>
 
 #include "../../include/harl.h"
 
@@ -38,6 +39,7 @@ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 // ------------------------------------------------------------------------------------------
 constexpr int kMaxDepth = 12;
 constexpr int kMaxFeatures = 448;
+constexpr int kMinB16Depth = 9, kMaxB16Depth = 10;  // ensemble depths the binned path (score_bin.hip) walks
 
 }  // namespace harl
 
@@ -49,6 +51,19 @@ struct harl_ensemble {
     float base_score;
     int device;
     void *d_trees;        // n_trees * tree_stride bytes
+    // launch shape of the fp32 walk, chosen once at create
+    int32_t cfg_wp, cfg_a, cfg_b, cfg_c;
+    // tree groups forced at create (HARL_SCORE_TREE_GROUPS, for tests of the grouped layout); 0 = automatic
+    int32_t tree_groups_override;
+    // binned path (score_bin.hip), or null when the ensemble does not qualify: packed trees of
+    // b16_stride bytes, per-feature distinct thresholds (offsets and counts per feature)
+    void *d_trees_b16;
+    float *d_thr_b16;                         // per feature: sorted thresholds + NaN padding
+    int32_t *d_thr_off_b16, *d_thr_len_b16;   // their offsets and lengths (padding included)
+    int32_t *d_steps_b16;                     // binary-search probes per feature
+    uint16_t *d_lut_b16;                      // per feature: thresholds below each of 4,096 key buckets
+    float *d_leaves_b16;                      // [n_trees][2^depth] leaves
+    int32_t b16_stride, tree_groups_b16;
 };
 
 // ------------------------------------------------------------------------------------------
@@ -76,6 +91,15 @@ int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32
                        void *ws, size_t ws_bytes, hipStream_t stream);
 size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows);
 int pack_ensemble(const harl_ensemble_desc *desc, harl_ensemble **out, hipStream_t stream);
+void free_ensemble(harl_ensemble *E);
+// binned path (score_bin.hip)
+int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vector<float> &thr,
+             const std::vector<uint8_t> &dleft, const std::vector<float> &leaf, hipStream_t stream);
+void free_b16(harl_ensemble *E);
+bool score_b16_usable(const harl_ensemble *E);
+size_t score_b16_ws_bytes(const harl_ensemble *E, int32_t n_rows);
+int score_b16_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows, float **partial_out,
+                     int *groups_out, int *tiles_out, int *nbg_out, void *ws, size_t ws_bytes, hipStream_t stream);
 
 int pack_policy(const harl_policy_desc *desc, harl_policy **out, hipStream_t stream);
 bool policy_x32_eligible(const harl_policy_desc *desc);

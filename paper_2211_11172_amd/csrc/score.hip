@@ -1,5 +1,5 @@
 // Cost-model scoring of one search round: C(S') for every candidate (Algorithm 1 of the HARL
-// paper; the cost model is an XGBoost ensemble, Section 6.1 and Appendix A.2).  A candidate is a
+// paper; the cost model is an XGBoost ensemble, Section 6.1 and Appendix A.1).  A candidate is a
 // program of statements; each statement row has F fp32 features; the program score is the base
 // score plus the sum over its statements of the ensemble's leaf sum.
 //
@@ -912,15 +912,9 @@ ScoreCfg make_cfg(const harl_ensemble *E, bool wp, int a, int b, int n) {
     return c;
 }
 
-// Preferred shapes, best first; the first whose LDS fits is used.  HARL_SCORE_CFG="wp,RPL,TW,NTW"
-// or "ch,TW,ILP" puts a shape first (tuning sweeps).
+// Preferred shapes, best first; the first whose LDS fits is used.
 ScoreCfg choose_cfg(const harl_ensemble *E) {
     std::vector<ScoreCfg> cands;
-    if (const char *env = std::getenv("HARL_SCORE_CFG")) {
-        char kind[3] = {0, 0, 0};
-        int a = 0, b = 0, n = 1;
-        if (std::sscanf(env, "%2[a-z],%d,%d,%d", kind, &a, &b, &n) >= 3) cands.push_back(make_cfg(E, kind[0] == 'w', a, b, n));
-    }
     const int wp_pref[][3] = {{2, 16, 1}, {2, 12, 2}, {2, 12, 1}, {2, 8, 1}, {2, 6, 1}, {2, 4, 1},
                               {1, 16, 2}, {1, 8, 1}, {1, 4, 1}};
     for (auto &p : wp_pref) cands.push_back(make_cfg(E, true, p[0], p[1], p[2]));
@@ -930,6 +924,9 @@ ScoreCfg choose_cfg(const harl_ensemble *E) {
         if (c.kern && c.lds <= (size_t)kLdsBytes) return c;
     return cands.back();  // nothing fits: the launch reports HARL_E_UNSUPPORTED
 }
+
+// The shape chosen at create.
+ScoreCfg stored_cfg(const harl_ensemble *E) { return make_cfg(E, E->cfg_wp != 0, E->cfg_a, E->cfg_b, E->cfg_c); }
 
 int device_cus(int device) {
     static int cached[64] = {0};
@@ -951,15 +948,12 @@ struct WpSplit {
 };
 
 // Tree groups: the fewest (a power of 2 up to 8) whose share of the packed ensemble fits in about
-// 3 MB of an XCD's 4 MB L2.  HARL_SCORE_TREE_GROUPS overrides.
+// 3 MB of an XCD's 4 MB L2 (or the count forced at create).
 int tree_groups(const harl_ensemble *E) {
     int G = 1;
     const int64_t bytes = (int64_t)E->n_trees * E->tree_stride;
     while (G < 8 && 2 * G <= E->n_trees && bytes / G > (3 << 20)) G *= 2;
-    if (const char *env = std::getenv("HARL_SCORE_TREE_GROUPS")) {
-        const int o = std::atoi(env);
-        if ((o == 1 || o == 2 || o == 4 || o == 8) && o <= E->n_trees) G = o;
-    }
+    if (E->tree_groups_override > 0 && E->tree_groups_override <= E->n_trees) G = E->tree_groups_override;
     return G;
 }
 
@@ -980,7 +974,7 @@ WpSplit wp_split(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows) {
 // Number of tree groups G of the grid kernel.  Each group's share of the ensemble should stay
 // L2-resident (about 2 MB per XCD), and the work items (row tile x group) should fill whole waves
 // of the machine: G minimises (rounds of co-resident workgroups) x (walk time + staging time per
-// item).  HARL_SCORE_GROUPS overrides.
+// item).
 int choose_groups(const harl_ensemble *E, int32_t n_rows, const ScoreCfg &c) {
     const int64_t tiles = ceil_div(n_rows > 0 ? n_rows : 1, c.rows_per_tile);
     const int64_t bytes = (int64_t)E->n_trees * E->tree_stride;
@@ -997,10 +991,6 @@ int choose_groups(const harl_ensemble *E, int32_t n_rows, const ScoreCfg &c) {
             best_cost = cost;
             best = g;
         }
-    }
-    if (const char *env = std::getenv("HARL_SCORE_GROUPS")) {
-        const int o = std::atoi(env);
-        if (o >= 1 && o <= E->n_trees && o <= 64) best = o;
     }
     return best;
 }
@@ -1019,21 +1009,31 @@ size_t partial_floats(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows)
 }  // namespace
 
 size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows) {
-    const ScoreCfg c = choose_cfg(E);
+    if (score_b16_usable(E)) return score_b16_ws_bytes(E, n_rows);
+    const ScoreCfg c = stored_cfg(E);
     return partial_floats(E, c, n_rows) * sizeof(float) + 256;
 }
 
 int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows,
                        const int32_t *prog_ptr, int32_t n_prog, float *prog_score, float *stmt_score,
                        void *ws, size_t ws_bytes, hipStream_t stream) {
-    const ScoreCfg c = choose_cfg(E);
+    const bool b16 = score_b16_usable(E);
+    const ScoreCfg c = stored_cfg(E);
     const int64_t ldp = round_up(n_rows > 0 ? n_rows : 1, 64);
-    if (ws_bytes < partial_floats(E, c, n_rows) * sizeof(float))
-        return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
+    if (ws_bytes < score_round_ws_bytes(E, n_rows)) return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
     float *partial = static_cast<float *>(ws);
     if (n_prog <= 0) return HARL_OK;
     const int ppw = segsum_ppw(n_prog);
     const unsigned seg_grid = (unsigned)ceil_div(n_prog, ppw);
+    if (n_rows > 0 && b16) {
+        int groups = 0, tiles = 0, nbg = 0;
+        if (const int rc = score_b16_launch(E, X, ld, n_rows, &partial, &groups, &tiles, &nbg, ws, ws_bytes, stream))
+            return rc;
+        hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(kSegThreads), 0, stream, partial, ldp, 8, E->n_trees, 1,
+                           groups, tiles, nbg, prog_ptr, n_prog, n_rows, ppw, E->base_score, prog_score, stmt_score);
+        HARL_HIP_CHECK(hipGetLastError());
+        return HARL_OK;
+    }
     if (n_rows == 0) {
         hipLaunchKernelGGL(k_segsum, dim3(seg_grid), dim3(kSegThreads), 0, stream, partial, ldp, 6, 1, 0, 0, 1, 8,
                            prog_ptr, n_prog, 0, ppw, E->base_score, prog_score, stmt_score);
@@ -1115,6 +1115,11 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
     std::vector<uint8_t> host((size_t)T * stride, 0);
     std::vector<int32_t> map(2 * (size_t)M);      // complete-tree slot (1-based) -> original node
     std::vector<uint32_t> code(M), thr_bits(M);   // per internal slot 1 .. M-1
+    // the complete-tree form of every tree, for the binned packing: per split slot its feature (-1
+    // for a dummy split below an early leaf), threshold and missing direction; per leaf slot its value
+    std::vector<int32_t> c_feat((size_t)T * M, -1);
+    std::vector<float> c_thr((size_t)T * M, 0.f), c_leaf((size_t)T * M, 0.f);
+    std::vector<uint8_t> c_dl((size_t)T * M, 0);
     auto put = [](uint8_t *dst, uint32_t w) { std::memcpy(dst, &w, 4); };
     for (int t = 0; t < T; ++t) {
         uint8_t *tb = host.data() + (size_t)t * stride;
@@ -1126,6 +1131,9 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
             if (d->feature[n] >= 0) {
                 code[s] = (uint32_t)d->feature[n] | (d->default_left[n] ? kCodeDefaultLeft : 0u);
                 thr = d->threshold[n];
+                c_feat[(size_t)t * M + s] = d->feature[n];
+                c_thr[(size_t)t * M + s] = thr;
+                c_dl[(size_t)t * M + s] = d->default_left[n] ? 1 : 0;
                 if (std::isnan(thr)) thr = -INFINITY;   // no value is < NaN: everything present goes right
                 map[2 * s] = d->left[n];
                 map[2 * s + 1] = d->right[n];
@@ -1135,6 +1143,7 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
             }
             std::memcpy(&thr_bits[s], &thr, 4);
         }
+        for (int j = 0; j < M; ++j) c_leaf[(size_t)t * M + j] = d->leaf_value[map[M + j]];
         put(tb + 4, code[1]);
         for (int s = 1; s < M / 2; ++s) {
             put(tb + 8 * s, thr_bits[s]);
@@ -1155,6 +1164,19 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
     E->depth = D;
     E->tree_stride = stride;
     E->base_score = d->base_score;
+    // the tree-group count may be forced (a power of 2 up to 8) to test the grouped layout on small
+    // ensembles; read once here, so that every call on the handle uses the same layout
+    if (const char *env = std::getenv("HARL_SCORE_TREE_GROUPS")) {
+        const int o = std::atoi(env);
+        if ((o == 1 || o == 2 || o == 4 || o == 8) && o <= T) E->tree_groups_override = o;
+    }
+    {
+        const ScoreCfg c = choose_cfg(E);
+        E->cfg_wp = c.wp ? 1 : 0;
+        E->cfg_a = c.a;
+        E->cfg_b = c.b;
+        E->cfg_c = c.c;
+    }
     if (hipGetDevice(&E->device) != hipSuccess) {
         delete E;
         return fail(HARL_E_HIP, "harl_ensemble_create: hipGetDevice failed");
@@ -1170,8 +1192,19 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
         delete E;
         return hip_fail(e, "harl_ensemble_create: upload");
     }
+    if (const int rc = pack_b16(E, c_feat, c_thr, c_dl, c_leaf, stream)) {
+        (void)hipFree(E->d_trees);
+        delete E;
+        return rc;
+    }
     *out = E;
     return HARL_OK;
+}
+
+void free_ensemble(harl_ensemble *E) {
+    free_b16(E);
+    (void)hipFree(E->d_trees);
+    delete E;
 }
 
 }  // namespace harl

@@ -1,0 +1,747 @@
+// Cost-model scoring on binned feature codes: the path harl_score_round takes for deep ensembles (9
+// or 10 split levels) of up to 256 features with at most 65,534 distinct thresholds per feature
+// (Algorithm 1's cost model C(S'), an XGBoost ensemble: Section 6.1 and Appendix A.1).  Shallower
+// ensembles use the fp32 walk of score.hip, whose 3 KB depth-8 trees already leave room for 16
+// waves per CU; at depth 10 its 12 KB trees leave room for 6.
+//
+// A split sends x left iff x < threshold, so a node's decision depends only on where x falls among
+// the thresholds its feature is split on.  With t_f[0] < ... < t_f[m_f - 1] the distinct thresholds
+// of feature f over the whole ensemble, a present value gets the code
+//     b(x) = #{ j : t_f[j] <= x }        (IEEE compares, so -0 and +0 are one value)
+// and for a node splitting f at t_f[j]:  x < t_f[j]  <=>  b(x) <= j  <=>  b(x) < theta, theta = j + 1.
+// A missing value (NaN) gets the code 0xFFFF.  Each node stores theta and U = 0xFFFF - theta when
+// missing values go right, 0xFFFE - theta when they go left; a code c goes right iff
+// (c - theta) mod 2^32 <= U.  This reproduces the fp32 comparison exactly, missing values included,
+// with one subtraction and one compare per node visit.  A NaN threshold (every present value goes
+// right) gets theta = 0.
+//
+// K0 k_bin16: one pass over the round's fp32 features [F][ld] writes the codes into the workspace:
+//   per 256-row tile and feature, 128 dwords {code(row p), code(row p + 128)}.
+// K1 k_tree_score_b16: persistent workgroups over slices of the (row tile, tree) space as the fp32
+//   walk (XCD-aware slices, tree groups that stay L2-resident, per-wave tree slots streamed through
+//   registers).  A tile holds 256 rows, 512 bytes per feature (84 KB for 164 features, the size of
+//   a 128-row fp32 tile); each lane walks 4 rows of every tree: twice the row-tree chains per wave
+//   of the fp32 walk, and half the tree bytes streamed per row.
+//
+// Tile in LDS: row group g (rows 64g .. 64g + 63 and 128 + 64g .. 191 + 64g) at byte 65536 g, its
+// feature f at 65536 g + 256 f: dword l = {code(row 64g + l), code(row 128 + 64g + l)}.  The code of
+// lane l's row 64j + l for feature f is then at byte 65536 (j & 1) + 256 f + 4 l + 2 (j >> 1): the
+// lane and row bits of the address never change, and a decision writes the child's feature straight
+// into its second byte.  Lanes read distinct banks whatever features their nodes ask for.  Tree
+// slots fill the LDS around the two row groups.
+//
+// Packed tree (D split levels, M = 2^D leaves, nodes numbered breadth-first from 1), 6M bytes:
+//   [0, 4M)        8-byte records: record 0 = {feature(1), 0}; record i, 1 <= i < M/2 (levels
+//                  0 .. D-2) = {theta(i) | U(i) << 16, feature(2i) | feature(2i+1) << 8}
+//   [4M, 6M)       last split level, node i = M/2 + k: {theta(i) | U(i) << 16} at 4M + 4k
+// and the leaves in global memory ([T][M] fp32, L2-resident with the trees), node i = M/2 + k's at
+// 2k and 2k + 1.  A level of a walk reads the current node's code and record together (one LDS round
+// trip); the record carries both children's features, so the child's code is read with the child's
+// record.  Without the leaves a depth-10 slot is 6 KB, and 12 waves fit beside the tile; each
+// chain's leaf is loaded at the end of a tree's walk and added after the next tree's.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <vector>
+
+#include "internal.hpp"
+
+namespace harl {
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kLdsBytes = 160 * 1024;
+constexpr int kRT = 256;                        // rows per tile
+constexpr int kRPL = 4;                         // rows per lane
+constexpr uint32_t kRowBytes = kRT * 2;         // bytes per feature row of a tile
+constexpr int kTileU4 = kRowBytes / 16;         // uint4 per feature row of a tile (32)
+constexpr int kPrefetchFeatures = 192;          // features per tile held in the register prefetch
+constexpr uint32_t kMissing = 0xFFFFu;
+constexpr uint32_t kGroupStride = 65536;        // LDS bytes between the tile's two row groups
+
+// LDS accesses by absolute byte address.
+__device__ __forceinline__ uint32_t lds_u16(uint32_t a) {
+    return *(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)a;
+}
+__device__ __forceinline__ uint32_t lds_b32(uint32_t a) {
+    return *(const __attribute__((address_space(3))) uint32_t *)(uintptr_t)a;
+}
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint2 lds_b64(uint32_t a) {
+    const u32x2 v = *(const __attribute__((address_space(3))) u32x2 *)(uintptr_t)a;
+    return make_uint2(v.x, v.y);
+}
+typedef __attribute__((address_space(3))) char lds_char;
+__device__ __forceinline__ uint32_t lds_addr(const char *p) { return (uint32_t)(uintptr_t)(const lds_char *)p; }
+
+// An opaque VGPR copy of a wave-uniform value (so that one v_cndmask can select between two).
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
+// One inner decision: code c at a node with word w = theta | U << 16 and child features p (byte 0
+// left, byte 1 right).  Writes the child's feature into byte 1 of the code address xa (the other
+// bytes, the lane's row, are kept) and returns sel = go right ? r : l.  The compare writes VCC and
+// the SDWA select reads it (two wait states between them).
+__device__ __forceinline__ void decide(uint32_t c, uint32_t w, uint32_t p, uint32_t l, uint32_t r, uint32_t &xa,
+                                       uint32_t &sel) {
+    uint32_t d;
+    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
+        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
+        "s_nop 1\n\t"
+        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 src1_sel:BYTE_1\n\t"
+        "v_cndmask_b32 %[s], %[l], %[r], vcc"
+        : [d] "=&v"(d), [xa] "+v"(xa), [s] "=&v"(sel)
+        : [c] "v"(c), [w] "v"(w), [p] "v"(p), [l] "v"(l), [r] "v"(r)
+        : "vcc");
+}
+
+// Last level: byte offset of the leaf reached, o0 + (go right ? 4 : 0).
+__device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t o0, uint32_t o1) {
+    uint32_t d, out;
+    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
+        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
+        "s_nop 1\n\t"
+        "v_cndmask_b32 %[o], %[a], %[b], vcc"
+        : [d] "=&v"(d), [o] "=&v"(out)
+        : [c] "v"(c), [w] "v"(w), [a] "v"(o0), [b] "v"(o1)
+        : "vcc");
+    return out;
+}
+
+struct Head {
+    uint32_t f, w, p;  // root feature, root word, root's children's features (D >= 2)
+};
+
+// Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows;
+// xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each level rewrites.  The
+// rows are independent chains: each takes its step of a level in turn, so the reads of the others
+// are in flight while one decides.  The tree's leaves are at gl (M floats); each chain's leaf is
+// loaded into pend[] after the previous tree's pending leaf has been added to acc[].
+__device__ __forceinline__ void walk(uint32_t tb, int D, const Head &h, uint32_t (&xa)[kRPL], double (&acc)[kRPL],
+                                     const float *__restrict__ gl, float (&pend)[kRPL]) {
+    const uint32_t M = 1u << D;
+    uint32_t x[kRPL], a[kRPL], lw[kRPL];
+    uint2 rec[kRPL];
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) {
+        xa[c] = (xa[c] & 0xFFFF00FFu) | (h.f << 8);
+        x[c] = lds_u16(xa[c]);
+    }
+    const uint32_t hw = in_vgpr(h.w), hp = in_vgpr(h.p);
+    const uint32_t l0 = in_vgpr(tb + 16u), r0 = in_vgpr(tb + 24u);
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) {
+        uint32_t s;
+        decide(x[c], hw, hp, l0, r0, xa[c], s);
+        x[c] = lds_u16(xa[c]);
+        a[c] = s;
+        rec[c] = lds_b64(s);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // levels 1 .. D-3: record address of child 2n + g = 2a - tb + 8g
+    const uint32_t li = in_vgpr(0u - tb), ri = in_vgpr(8u - tb);
+    for (int lvl = 1; lvl + 2 < D; ++lvl) {
+#pragma unroll
+        for (int c = 0; c < kRPL; ++c) {
+            uint32_t s;
+            decide(x[c], rec[c].x, rec[c].y, li, ri, xa[c], s);
+            x[c] = lds_u16(xa[c]);
+            a[c] = 2u * a[c] + s;
+            rec[c] = lds_b64(a[c]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    // level D-2 into the last level: the child's word at as + 2M, as = a + 4g
+    const uint32_t lt = in_vgpr(0u), rt = in_vgpr(4u), k2m = 2u * M;
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) {
+        uint32_t s;
+        decide(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
+        x[c] = lds_u16(xa[c]);
+        a[c] = a[c] + s;
+        lw[c] = lds_b32(a[c] + k2m);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // last-level node k = (as - tb - 2M) / 4; its leaves at byte 8k of the tree's leaves
+    const uint32_t kb2 = 0u - 2u * tb - 4u * M;
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) {
+        const uint32_t o0 = 2u * a[c] + kb2;
+        const uint32_t o = leaf_off(x[c], lw[c], o0, o0 + 4u);
+        acc[c] += (double)pend[c];
+        pend[c] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(gl) + o);
+    }
+}
+
+// ---- K0: codes of every (row, feature) ----
+// The order-preserving 32-bit key of a present value is its bit pattern with the sign bit set for
+// +-values >= +0 and all bits inverted for negatives; its top 12 bits select one of 4,096 buckets.
+// Per feature, lut[b] = number of thresholds whose key lies in a lower bucket, and every bucket
+// holds fewer than 2^steps thresholds.  A value in bucket b has a code between lut[b] and
+// lut[b] + 2^steps - 1: a branch-free binary search of `steps` probes, starting at lut[b], finds
+// it.  Probes past the bucket land on larger thresholds (or on the table's NaN padding), which
+// never compare <= x, so no bound check is needed; -0 and +0 compare equal, and the thresholds hold
+// one zero (+0), which a -0 in the bucket below reaches in the same way.
+// Workgroup (feature f, range of tiles): stages lut and the thresholds of f in LDS (or searches
+// them in global memory when they do not fit), then each thread codes 4 row pairs (p, p + 128) of
+// its tiles at a time.  Rows at or past n_rows get code 0 (never summed).
+constexpr int kBinThreads = 256;
+constexpr int kLutBuckets = 4096;
+constexpr int kLutStride = 4104;                  // u16 per feature's lut (4,097 used), 16-byte rows
+constexpr int kBinLdsThresholds = 10240;          // 40 KB, padding included
+constexpr int kBinPairs = 4;                      // row pairs per thread and iteration
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
+
+// Codes of N values at once: the probes of the N searches are independent and overlap.
+template <int N>
+__device__ __forceinline__ void codes_of(const float (&x)[N], uint32_t (&c)[N], const uint16_t *lut, const float *tf,
+                                         int steps) {
+#pragma unroll
+    for (int e = 0; e < N; ++e) c[e] = lut[order_key(x[e]) >> 20];
+    for (int k = steps - 1; k >= 0; --k) {
+        const uint32_t s = 1u << k;
+#pragma unroll
+        for (int e = 0; e < N; ++e)
+            if (tf[c[e] + s - 1] <= x[e]) c[e] += s;
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+        if (x[e] != x[e]) c[e] = kMissing;
+}
+
+__global__ __launch_bounds__(kBinThreads) void k_bin16(const float *__restrict__ X, int64_t ld, int n_rows,
+                                                       const float *__restrict__ thr, const int32_t *__restrict__ t_off,
+                                                       const int32_t *__restrict__ t_len,
+                                                       const uint16_t *__restrict__ luts,
+                                                       const int32_t *__restrict__ steps_f, uint32_t *__restrict__ codes,
+                                                       int64_t ldw, int tiles, int tiles_per_block, int blocks_per_f) {
+    __shared__ float st[kBinLdsThresholds];
+    __shared__ uint16_t sl[kLutStride];
+    const int f = blockIdx.x / blocks_per_f;
+    const int tile0 = (blockIdx.x % blocks_per_f) * tiles_per_block;
+    const int tile1 = min(tiles, tile0 + tiles_per_block);
+    if (tile0 >= tile1) return;  // whole workgroup
+    const int len = t_len[f], steps = steps_f[f];
+    const float *__restrict__ tg = thr + t_off[f];
+    const bool in_lds = len <= kBinLdsThresholds;
+    {
+        const uint4 *src = reinterpret_cast<const uint4 *>(luts + (int64_t)f * kLutStride);
+        uint4 *dst = reinterpret_cast<uint4 *>(sl);
+        for (int i = threadIdx.x; i < kLutStride / 8; i += kBinThreads) dst[i] = src[i];
+        if (in_lds)
+            for (int i = threadIdx.x; i < len; i += kBinThreads) st[i] = tg[i];
+    }
+    __syncthreads();
+    const float *__restrict__ xf = X + (int64_t)f * ld;
+    uint32_t *__restrict__ out = codes + (int64_t)f * ldw;
+    const int n_pairs = (tile1 - tile0) * (kRT / 2);
+    for (int i0 = threadIdx.x; i0 < n_pairs; i0 += kBinPairs * kBinThreads) {
+        float x[2 * kBinPairs];
+        int at[kBinPairs];
+#pragma unroll
+        for (int j = 0; j < kBinPairs; ++j) {
+            const int i = i0 + j * kBinThreads;
+            const int t = tile0 + i / (kRT / 2), p = i % (kRT / 2);
+            const int r0 = t * kRT + p, r1 = r0 + kRT / 2;
+            at[j] = i < n_pairs ? t * (kRT / 2) + p : -1;
+            x[2 * j] = i < n_pairs && r0 < n_rows ? xf[r0] : 0.f;
+            x[2 * j + 1] = i < n_pairs && r1 < n_rows ? xf[r1] : 0.f;
+        }
+        uint32_t c[2 * kBinPairs];
+        if (in_lds)
+            codes_of<2 * kBinPairs>(x, c, sl, st, steps);
+        else
+            codes_of<2 * kBinPairs>(x, c, sl, tg, steps);
+#pragma unroll
+        for (int j = 0; j < kBinPairs; ++j) {
+            const int i = i0 + j * kBinThreads;
+            const int t = tile0 + i / (kRT / 2), p = i % (kRT / 2);
+            if (at[j] >= 0) {
+                const uint32_t lo = t * kRT + p < n_rows ? c[2 * j] : 0u;
+                const uint32_t hi = t * kRT + p + kRT / 2 < n_rows ? c[2 * j + 1] : 0u;
+                out[at[j]] = lo | hi << 16;
+            }
+        }
+    }
+}
+
+// ---- K1 ----
+// Slices of the (tile, tree) space, XCD-aware: workgroup b runs on XCD b % 8, walks tree group
+// (b % 8) % G and slice ((b % 8) / G) * (nb / 8) + b / 8 of that group; consecutive slices share
+// their boundary tile and stage it at about the same time, on one XCD (even slices walk their tiles
+// last to first, odd ones first to last).
+__device__ __forceinline__ void block_slice(int b, int nb, int G, int &g, int &r) {
+    const int x = b % 8, j = b / 8;  // nb is a multiple of 8
+    g = x % G;
+    r = (x / G) * (nb / 8) + j;
+}
+__host__ __device__ __forceinline__ int group_trees(int T, int G, int g) {
+    const int tg = (T + G - 1) / G;
+    return T - g * tg < tg ? T - g * tg : tg;
+}
+__host__ __device__ __forceinline__ int64_t group_slice_len(int64_t tiles, int tc, int nbg) {
+    return (tiles * tc + nbg - 1) / nbg;
+}
+
+// A wave's tree: lane l moves uint4 j*64 + l (S16 uint4 per tree, PF per lane at most; EXACT: the
+// tree is exactly PF * 64 uint4, and the loads need no guard).
+template <int PF, bool EXACT>
+__device__ __forceinline__ void tree_fetch(uint4 (&pf)[PF], const uint4 *__restrict__ src, int S16, int lane) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j)
+        if (EXACT || j * kWave + lane < S16) pf[j] = src[j * kWave + lane];
+}
+template <int PF, bool EXACT>
+__device__ __forceinline__ void tree_commit(const uint4 (&pf)[PF], uint4 *dst, int S16, int lane, Head &h) {
+#pragma unroll
+    for (int j = 0; j < PF; ++j)
+        if (EXACT || j * kWave + lane < S16) dst[j * kWave + lane] = pf[j];
+    h.f = __builtin_amdgcn_readlane(pf[0].x, 0);
+    h.w = __builtin_amdgcn_readlane(pf[0].z, 0);
+    h.p = __builtin_amdgcn_readlane(pf[0].w, 0);
+}
+
+// Tile staging.  uint4 i of a tile is part i % 32 of feature i / 32 in the codes (global: feature
+// f's 128 dwords of tile t at f * ldw + 128 t) and goes to LDS uint4 4096 g + 16 f + q, where
+// (g, q) = (part / 16, part % 16): row group g, dwords 4q .. 4q + 3.  With NT a multiple of 32,
+// thread t holds parts t % 32 of features t / 32 + j * NT / 32.
+__device__ __forceinline__ int tile_lds_index(int i) {
+    const int part = i % kTileU4;
+    return (part / 16) * (int)(kGroupStride / 16) + (i / kTileU4) * 16 + part % 16;
+}
+template <int NT, int NPX>
+__device__ __forceinline__ void tile_fetch(uint4 (&xf)[NPX], const uint4 *__restrict__ codes, int64_t ldw4, int F,
+                                           int tile) {
+    const int total = F * kTileU4;
+    const uint4 *p = codes + (int64_t)(threadIdx.x / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + threadIdx.x % kTileU4;
+    const int64_t step = (int64_t)(NT / kTileU4) * ldw4;
+#pragma unroll
+    for (int j = 0; j < NPX; ++j) {
+        if ((int)threadIdx.x + j * NT < total) xf[j] = *p;
+        p += step;
+    }
+}
+template <int NT, int NPX>
+__device__ __forceinline__ void tile_commit(const uint4 (&xf)[NPX], uint4 *tile_lds, int F) {
+    const int total = F * kTileU4;
+    uint4 *dst = tile_lds + tile_lds_index(threadIdx.x);
+#pragma unroll
+    for (int j = 0; j < NPX; ++j)
+        if ((int)threadIdx.x + j * NT < total) dst[j * (NT / kTileU4) * 16] = xf[j];
+}
+// Direct staging (tiles too wide for the register prefetch), 4 loads in flight per thread.
+template <int NT>
+__device__ __forceinline__ void tile_stage(uint4 *tile_lds, const uint4 *__restrict__ codes, int64_t ldw4, int F,
+                                           int tile) {
+    const int total = F * kTileU4;
+    for (int i0 = threadIdx.x; i0 < total; i0 += 4 * NT) {
+        uint4 v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = i0 + j * NT;
+            if (i < total) v[j] = codes[(int64_t)(i / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + (i % kTileU4)];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (i0 + j * NT < total) tile_lds[tile_lds_index(i0 + j * NT)] = v[j];
+    }
+}
+
+// LDS placement of a workgroup's tree slots: n_a slots of `sb` bytes after row group 0 (from byte
+// 256 F up to 65536), the rest after row group 1 (from 65536 + 256 F); the row sums of a piece
+// reuse the second area, and two progress counters follow whichever of slots and sums is longer.
+struct SlotPlan {
+    int n_a;
+    uint32_t a0, b0, progress, lds;
+};
+__host__ __device__ __forceinline__ SlotPlan slot_plan(int F, int tw, uint32_t sb) {
+    SlotPlan p{};
+    p.a0 = 256u * (uint32_t)F;
+    p.b0 = kGroupStride + 256u * (uint32_t)F;
+    const int fit_a = (int)((kGroupStride - p.a0) / sb);
+    p.n_a = fit_a < tw ? fit_a : tw;
+    const uint32_t slots_b = (uint32_t)(tw - p.n_a) * sb, red = (uint32_t)tw * kRT * 8u;
+    p.progress = p.b0 + (slots_b > red ? slots_b : red);
+    p.lds = p.progress + 16u;
+    return p;
+}
+
+template <int TW, int PF>
+__global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restrict__ codes, int64_t ldw4, int n_rows,
+                                                           int F, const uint4 *__restrict__ trees_all, int S16, int D,
+                                                           int T_all, int G, int tiles, float *__restrict__ partial_all,
+                                                           const float *__restrict__ leaves_all) {
+    constexpr int NT = 64 * TW;
+    constexpr int NPX = (kPrefetchFeatures * kTileU4 + NT - 1) / NT;
+    extern __shared__ __align__(16) char smem[];
+    int g, s;
+    block_slice(blockIdx.x, gridDim.x, G, g, s);
+    const int nbg = gridDim.x / G;
+    const int T = group_trees(T_all, G, g);
+    if (T <= 0) return;  // whole workgroup
+    const int64_t g_tree0 = (int64_t)g * ((T_all + G - 1) / G);
+    const uint4 *__restrict__ trees = trees_all + g_tree0 * S16;
+    const int M = 1 << D;
+    const float *__restrict__ leaves = leaves_all + g_tree0 * M;
+    float *__restrict__ partial = partial_all + (int64_t)g * (tiles + nbg) * kRT;
+    const int64_t V = (int64_t)tiles * T, L = group_slice_len(tiles, T, nbg);
+    const int64_t v_begin = (int64_t)s * L;
+    const int64_t v_end = v_begin + L < V ? v_begin + L : V;
+    if (v_begin >= v_end) return;  // whole workgroup: no barrier is skipped by part of it
+    const int tile_first = (int)(v_begin / T), tile_last = (int)((v_end - 1) / T);
+    const int dir = (s & 1) ? 1 : -1;
+    const int n_pieces = tile_last - tile_first + 1;
+    auto piece_lo = [&](int i) { return (int)(v_begin - (int64_t)i * T > 0 ? v_begin - (int64_t)i * T : 0); };
+    auto piece_hi = [&](int i) { return (int)(v_end - (int64_t)i * T < T ? v_end - (int64_t)i * T : T); };
+
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const uint32_t sb = (uint32_t)S16 * 16u;
+    const SlotPlan plan = slot_plan(F, TW, sb);
+    const uint32_t slot_off = wid < plan.n_a ? plan.a0 + (uint32_t)wid * sb : plan.b0 + (uint32_t)(wid - plan.n_a) * sb;
+    uint4 *const slot = reinterpret_cast<uint4 *>(smem + slot_off);
+    unsigned int *const progress = reinterpret_cast<unsigned int *>(smem + plan.progress);
+    if (threadIdx.x == 0) progress[0] = progress[1] = 0;
+
+    // the dynamic LDS starts at address 0 (the kernel has no static LDS), so the code addresses
+    // carry the row bits alone outside byte 1
+    const uint32_t tb = lds_addr(smem) + slot_off;
+    uint32_t xa[kRPL];
+#pragma unroll
+    for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
+
+    constexpr bool EXACT = true;  // a slot is 6M bytes, exactly PF * 64 uint4 (host-checked)
+    uint4 pf[PF];
+#pragma unroll
+    for (int j = 0; j < PF; ++j) pf[j] = make_uint4(0, 0, 0, 0);
+    Head hd{0, 0, 0};
+    float pend[kRPL];
+#pragma unroll
+    for (int r = 0; r < kRPL; ++r) pend[r] = 0.f;
+    const bool x_regs = F <= kPrefetchFeatures;
+    uint4 xf[NPX];
+    uint4 *const tile_lds = reinterpret_cast<uint4 *>(smem);
+    double *const red = reinterpret_cast<double *>(smem + plan.b0);
+
+    int tile = dir > 0 ? tile_first : tile_last;
+    int t1 = piece_hi(tile);
+    int t = piece_lo(tile) + wid;
+    if (t < t1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)t * S16, S16, lane);   // overlaps the tile staging
+    if (x_regs) {
+        tile_fetch<NT, NPX>(xf, codes, ldw4, F, tile);
+        tile_commit<NT, NPX>(xf, tile_lds, F);
+        __syncthreads();
+        if (n_pieces > 1) tile_fetch<NT, NPX>(xf, codes, ldw4, F, tile + dir);
+    } else {
+        tile_stage<NT>(tile_lds, codes, ldw4, F, tile);
+        __syncthreads();
+    }
+    for (int piece = 0;; ++piece) {
+        const int row0 = tile * kRT;
+        if (threadIdx.x == 0) progress[(piece + 1) & 1] = 0;
+        uint32_t my_done = 0;
+        if (t < t1) tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);
+        if (t + TW < t1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(t + TW) * S16, S16, lane);
+        const bool next = piece + 1 < n_pieces;
+        const int ntile = tile + dir;
+        double acc[kRPL];
+#pragma unroll
+        for (int r = 0; r < kRPL; ++r) acc[r] = 0.0;
+        for (; t < t1; t += TW) {
+            walk(tb, D, hd, xa, acc, leaves + (int64_t)t * M, pend);
+            if (t + TW < t1) {
+                tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);   // LDS operations of a wave run in order
+                if (t + 2 * TW < t1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(t + 2 * TW) * S16, S16, lane);
+            }
+            // fair progress: a wave behind its workgroup's average takes the top issue priority
+            my_done += 1;
+            uint32_t total = 0;
+            if (lane == 0) total = atomicAdd(progress + (piece & 1), 1u) + 1u;
+            total = __builtin_amdgcn_readfirstlane(total);
+            if (my_done * TW < total)
+                __builtin_amdgcn_s_setprio(3);
+            else
+                __builtin_amdgcn_s_setprio(0);
+        }
+        __builtin_amdgcn_s_setprio(0);
+#pragma unroll
+        for (int r = 0; r < kRPL; ++r) {
+            acc[r] += (double)pend[r];
+            pend[r] = 0.f;
+        }
+        const int nt0 = next ? piece_lo(ntile) : 0, nt1 = next ? piece_hi(ntile) : 0;
+        if (next && nt0 + wid < nt1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(nt0 + wid) * S16, S16, lane);
+        __syncthreads();  // B1: every wave is done with the tile and its slot
+#pragma unroll
+        for (int r = 0; r < kRPL; ++r) red[wid * kRT + r * 64 + lane] = acc[r];
+        if (next && x_regs) {
+            tile_commit<NT, NPX>(xf, tile_lds, F);
+            if (piece + 2 < n_pieces) tile_fetch<NT, NPX>(xf, codes, ldw4, F, ntile + dir);
+        }
+        __syncthreads();  // B2: row sums (and the next tile) are in LDS
+        float *__restrict__ out = partial + ((int64_t)tile + s) * kRT;
+        for (int r = threadIdx.x; r < kRT; r += NT) {
+            double sum = 0.0;
+#pragma unroll
+            for (int w = 0; w < TW; ++w) sum += red[w * kRT + r];
+            if (row0 + r < n_rows) out[r] = (float)sum;
+        }
+        if (!next) break;
+        __syncthreads();  // B3: the sums are read before the next trees overwrite the slots
+        if (!x_regs) {
+            tile_stage<NT>(tile_lds, codes, ldw4, F, ntile);
+            __syncthreads();
+        }
+        tile = ntile;
+        t1 = nt1;
+        t = nt0 + wid;
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+// launch configuration
+// ---------------------------------------------------------------------------------------------
+using B16Kernel = void (*)(const uint4 *, int64_t, int, int, const uint4 *, int, int, int, int, int, float *,
+                           const float *);
+
+struct B16Shape {
+    int tw, pf;
+    B16Kernel kern;
+};
+// Shapes, most waves first: the first whose tree prefetch is exactly one tree per lane group and
+// whose slots fit beside the tile is used (depth 9: 3 KB slots, 3 uint4 per lane; depth 10: 6 KB, 6).
+const B16Shape kShapes[] = {
+    {16, 3, k_tree_score_b16<16, 3>}, {8, 3, k_tree_score_b16<8, 3>},  {4, 3, k_tree_score_b16<4, 3>},
+    {12, 6, k_tree_score_b16<12, 6>}, {8, 6, k_tree_score_b16<8, 6>},  {4, 6, k_tree_score_b16<4, 6>},
+    {2, 6, k_tree_score_b16<2, 6>},
+};
+
+size_t b16_lds(const harl_ensemble *E, int tw) { return slot_plan(E->n_features, tw, (uint32_t)E->b16_stride).lds; }
+
+const B16Shape *b16_shape(const harl_ensemble *E) {
+    const int s16 = E->b16_stride / 16;
+    for (const B16Shape &sh : kShapes)
+        if (sh.pf * kWave == s16 && b16_lds(E, sh.tw) <= (size_t)kLdsBytes) return &sh;
+    return nullptr;
+}
+
+int device_cus_b16(int device) {
+    static int cached[64] = {0};
+    if (device < 0 || device >= 64) return 256;
+    if (!cached[device]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || n <= 0) n = 256;
+        cached[device] = n;
+    }
+    return cached[device];
+}
+
+struct B16Split {
+    int64_t tiles;
+    int nb, G;
+};
+
+B16Split b16_split(const harl_ensemble *E, const B16Shape &sh, int32_t n_rows) {
+    B16Split w{};
+    w.tiles = ceil_div(n_rows > 0 ? n_rows : 1, kRT);
+    w.G = E->tree_groups_b16;
+    int64_t nb = device_cus_b16(E->device);  // one workgroup per CU (the tile and slots fill the LDS)
+    const int64_t min_l = 2LL * sh.tw;        // at least 2 trees per wave per slice
+    const int64_t vg = w.tiles * ceil_div(E->n_trees, w.G);
+    if (ceil_div(vg, nb / w.G > 0 ? nb / w.G : 1) < min_l) nb = ceil_div(vg, min_l) * w.G;
+    w.nb = (int)round_up(nb < 8 ? 8 : nb, 8);
+    return w;
+}
+
+int bin_tiles_per_block(int64_t tiles) { return tiles >= 128 ? 128 : (int)tiles; }
+
+}  // namespace
+
+// Workspace: the codes ([F][tiles * 128] dwords, 256-byte aligned) followed by the partial sums.
+size_t score_b16_ws_bytes(const harl_ensemble *E, int32_t n_rows) {
+    const B16Shape *sh = b16_shape(E);
+    if (!sh) return 0;
+    const B16Split w = b16_split(E, *sh, n_rows);
+    const size_t codes = (size_t)E->n_features * (size_t)w.tiles * kRowBytes;
+    const size_t partial = (size_t)w.G * (size_t)(w.tiles + w.nb / w.G) * kRT * sizeof(float);
+    return round_up((int64_t)codes, 256) + partial + 256;
+}
+
+bool score_b16_usable(const harl_ensemble *E) { return E->d_trees_b16 != nullptr && b16_shape(E) != nullptr; }
+
+int score_b16_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows, float **partial_out,
+                     int *groups_out, int *tiles_out, int *nbg_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+    const B16Shape *sh = b16_shape(E);
+    if (!sh) return fail(HARL_E_UNSUPPORTED, "harl_score_round: no binned kernel shape fits this ensemble");
+    const B16Split w = b16_split(E, *sh, n_rows);
+    if (ws_bytes < score_b16_ws_bytes(E, n_rows)) return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
+    const size_t codes_bytes = round_up((int64_t)E->n_features * w.tiles * kRowBytes, 256);
+    uint32_t *codes = static_cast<uint32_t *>(ws);
+    float *partial = reinterpret_cast<float *>(static_cast<char *>(ws) + codes_bytes);
+    const int64_t ldw = w.tiles * (kRT / 2);
+    const int tpb = bin_tiles_per_block(w.tiles);
+    const int bpf = (int)ceil_div(w.tiles, tpb);
+    hipLaunchKernelGGL(k_bin16, dim3((unsigned)(E->n_features * bpf)), dim3(kBinThreads), 0, stream, X, ld, n_rows,
+                       E->d_thr_b16, E->d_thr_off_b16, E->d_thr_len_b16, E->d_lut_b16, E->d_steps_b16, codes, ldw,
+                       (int)w.tiles, tpb, bpf);
+    HARL_HIP_CHECK(hipGetLastError());
+    const size_t lds = b16_lds(E, sh->tw);
+    if (const int rc = ensure_dynamic_lds(reinterpret_cast<const void *>(sh->kern), lds)) return rc;
+    hipLaunchKernelGGL(sh->kern, dim3((unsigned)w.nb), dim3(64 * sh->tw), lds, stream,
+                       reinterpret_cast<const uint4 *>(codes), ldw / 4, n_rows, E->n_features,
+                       static_cast<const uint4 *>(E->d_trees_b16), E->b16_stride / 16, E->depth, E->n_trees, w.G,
+                       (int)w.tiles, partial, E->d_leaves_b16);
+    HARL_HIP_CHECK(hipGetLastError());
+    *partial_out = partial;
+    *groups_out = w.G;
+    *tiles_out = (int)w.tiles;
+    *nbg_out = w.nb / w.G;
+    return HARL_OK;
+}
+
+// ---------------------------------------------------------------------------------------------
+// packing (host): threshold tables and the binned tree format, from the complete-tree form
+// ---------------------------------------------------------------------------------------------
+// `feat`, `thr`, `dleft` per complete-tree slot 1 .. M-1 of every tree (T x M, slot 0 unused;
+// feature -1 marks a dummy split below an early leaf), `leaf` per leaf slot (T x M).  Returns
+// HARL_OK with E's binned fields set, or HARL_OK with them left empty when the ensemble does not
+// qualify (the fp32 path is then used).
+int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vector<float> &thr,
+             const std::vector<uint8_t> &dleft, const std::vector<float> &leaf, hipStream_t stream) {
+    const int T = E->n_trees, F = E->n_features, D = E->depth;
+    if (F > 256 || D < kMinB16Depth || D > kMaxB16Depth) return HARL_OK;
+    const int M = 1 << D;
+    // distinct thresholds per feature (NaN thresholds need none: theta = 0), with -0 stored as +0
+    std::vector<std::vector<float>> tab(F);
+    for (int t = 0; t < T; ++t)
+        for (int s = 1; s < M; ++s) {
+            const int32_t f = feat[(size_t)t * M + s];
+            const float v = thr[(size_t)t * M + s];
+            if (f >= 0 && !std::isnan(v)) tab[f].push_back(v == 0.f ? 0.f : v);
+        }
+    auto key_of = [](float v) {
+        uint32_t u;
+        std::memcpy(&u, &v, 4);
+        return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+    };
+    // per feature: the sorted thresholds padded with 2^steps NaNs, the bucket table and the probe count
+    std::vector<int32_t> off(F), len(F), steps(F);
+    std::vector<uint16_t> lut((size_t)F * kLutStride, 0);
+    std::vector<float> flat;
+    for (int f = 0; f < F; ++f) {
+        auto &v = tab[f];
+        std::sort(v.begin(), v.end());
+        v.erase(std::unique(v.begin(), v.end()), v.end());
+        if (v.size() > 65534) return HARL_OK;
+        std::vector<int32_t> per(kLutBuckets, 0);
+        for (float t : v) ++per[key_of(t) >> 20];
+        int max_b = 0, run = 0;
+        uint16_t *lf = lut.data() + (size_t)f * kLutStride;
+        for (int b = 0; b < kLutBuckets; ++b) {
+            lf[b] = (uint16_t)run;
+            run += per[b];
+            max_b = per[b] > max_b ? per[b] : max_b;
+        }
+        lf[kLutBuckets] = (uint16_t)run;
+        int st = 0;
+        while ((1 << st) < max_b + 2) ++st;   // a -0 in the bucket below +0 may count one more
+        off[f] = (int32_t)flat.size();
+        flat.insert(flat.end(), v.begin(), v.end());
+        flat.insert(flat.end(), (size_t)1 << st, std::numeric_limits<float>::quiet_NaN());
+        len[f] = (int32_t)(flat.size() - off[f]);
+        steps[f] = st;
+    }
+    auto word = [&](int32_t f, float v, uint8_t dl) -> uint32_t {
+        uint32_t theta = 0;  // dummy split (f < 0) or NaN threshold: every present value goes right
+        if (f >= 0 && !std::isnan(v)) {
+            const auto &tv = tab[f];
+            theta = (uint32_t)(std::lower_bound(tv.begin(), tv.end(), v == 0.f ? 0.f : v) - tv.begin()) + 1u;
+        }
+        const uint32_t U = (f >= 0 && dl ? 0xFFFEu : 0xFFFFu) - theta;
+        return theta | U << 16;
+    };
+    const int stride = 6 * M;
+    std::vector<uint8_t> host((size_t)T * stride, 0);
+    std::vector<float> gleaves((size_t)T * M, 0.f);
+    auto put = [](uint8_t *dst, uint32_t w) { std::memcpy(dst, &w, 4); };
+    for (int t = 0; t < T; ++t) {
+        uint8_t *tb = host.data() + (size_t)t * stride;
+        const int32_t *ft = feat.data() + (size_t)t * M;
+        const float *th = thr.data() + (size_t)t * M;
+        const uint8_t *dl = dleft.data() + (size_t)t * M;
+        const float *lf = leaf.data() + (size_t)t * M;
+        auto fcode = [&](int s) { return (uint32_t)(ft[s] >= 0 ? ft[s] : 0); };
+        put(tb, fcode(1));
+        for (int s = 1; s < M / 2; ++s) {
+            put(tb + 8 * s, word(ft[s], th[s], dl[s]));
+            put(tb + 8 * s + 4, fcode(2 * s) | fcode(2 * s + 1) << 8);
+        }
+        for (int s = M / 2; s < M; ++s) {
+            const int k = s - M / 2;
+            put(tb + 4 * M + 4 * k, word(ft[s], th[s], dl[s]));
+            gleaves[(size_t)t * M + 2 * k] = lf[2 * s - M];
+            gleaves[(size_t)t * M + 2 * k + 1] = lf[2 * s + 1 - M];
+        }
+    }
+    // tree groups: the fewest (a power of 2 up to 8) whose share of the packed trees fits in about
+    // 3 MB of an XCD's 4 MB L2
+    int G = 1;
+    while (G < 8 && 2 * G <= T && (int64_t)T * stride / G > (3 << 20)) G *= 2;
+    if (E->tree_groups_override > 0 && E->tree_groups_override <= T) G = E->tree_groups_override;
+    void *d_trees = nullptr, *d_thr = nullptr, *d_off = nullptr, *d_len = nullptr, *d_steps = nullptr, *d_lut = nullptr,
+         *d_gl = nullptr;
+    auto cleanup = [&]() {
+        for (void *p : {d_trees, d_thr, d_off, d_len, d_steps, d_lut, d_gl})
+            if (p) (void)hipFree(p);
+    };
+    if (hipMalloc(&d_trees, host.size()) != hipSuccess || hipMalloc(&d_thr, flat.size() * 4) != hipSuccess ||
+        hipMalloc(&d_off, (size_t)F * 4) != hipSuccess || hipMalloc(&d_len, (size_t)F * 4) != hipSuccess ||
+        hipMalloc(&d_steps, (size_t)F * 4) != hipSuccess || hipMalloc(&d_lut, lut.size() * 2) != hipSuccess ||
+        hipMalloc(&d_gl, gleaves.size() * 4) != hipSuccess) {
+        cleanup();
+        return fail(HARL_E_NOMEM, "harl_ensemble_create: device allocation failed");
+    }
+    hipError_t e = hipMemcpyAsync(d_trees, host.data(), host.size(), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_thr, flat.data(), flat.size() * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_off, off.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_len, len.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_steps, steps.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_lut, lut.data(), lut.size() * 2, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_gl, gleaves.data(), gleaves.size() * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) {
+        cleanup();
+        return hip_fail(e, "harl_ensemble_create: upload");
+    }
+    E->d_trees_b16 = d_trees;
+    E->d_thr_b16 = static_cast<float *>(d_thr);
+    E->d_thr_off_b16 = static_cast<int32_t *>(d_off);
+    E->d_thr_len_b16 = static_cast<int32_t *>(d_len);
+    E->d_steps_b16 = static_cast<int32_t *>(d_steps);
+    E->d_lut_b16 = static_cast<uint16_t *>(d_lut);
+    E->d_leaves_b16 = static_cast<float *>(d_gl);
+    E->b16_stride = stride;
+    E->tree_groups_b16 = G;
+    return HARL_OK;
+}
+
+void free_b16(harl_ensemble *E) {
+    for (void *p : {E->d_trees_b16, (void *)E->d_thr_b16, (void *)E->d_thr_off_b16, (void *)E->d_thr_len_b16,
+                    (void *)E->d_steps_b16, (void *)E->d_lut_b16, (void *)E->d_leaves_b16})
+        if (p) (void)hipFree(p);
+    E->d_trees_b16 = nullptr;
+    E->d_leaves_b16 = nullptr;
+    E->d_thr_b16 = nullptr;
+    E->d_thr_off_b16 = E->d_thr_len_b16 = E->d_steps_b16 = nullptr;
+    E->d_lut_b16 = nullptr;
+}
+
+}  // namespace harl

@@ -131,3 +131,100 @@ def test_deterministic_repeat():
     a1, s1 = gpu_score(ens, b["features"], b["prog_ptr"])
     a2, s2 = gpu_score(ens, b["features"], b["prog_ptr"])
     assert a1.tobytes() == a2.tobytes() and s1.tobytes() == s2.tobytes()
+
+
+# ---- the binned path (ensembles of depth 9 or 10, <= 256 features, <= 65,534 distinct thresholds
+# per feature) and the fp32 walks that remain for the others ----
+def _exact_leaves(ens):
+    return {**ens, "leaf_value": (np.round(ens["leaf_value"] * 4096) / 4096).astype(np.float32)}
+
+
+@pytest.mark.parametrize("depth,n_prog", [(9, 611), (10, 611), (10, 37), (9, 5)])
+def test_binned_depths_exact(depth, n_prog):
+    """The binned walk at both of its depths, 15 % missing values, a ragged last tile and rounds of
+    fewer rows than one tile: bit-exact against the oracle."""
+    cfg = get_config("tiny", exact=True).with_(depth=depth, n_trees=23, n_prog=n_prog, s_max=9, p_nan=0.15,
+                                               name="binned-d%d-p%d" % (depth, n_prog))
+    _check(cfg)
+
+
+@pytest.mark.parametrize("groups", [2, 4, 8])
+def test_binned_tree_groups_exact(groups, monkeypatch):
+    monkeypatch.setenv("HARL_SCORE_TREE_GROUPS", str(groups))
+    cfg = get_config("tiny", exact=True).with_(depth=10, n_trees=45, n_prog=900, p_nan=0.1,
+                                               name="binned-groups%d" % groups)
+    _check(cfg)
+
+
+def test_binned_irregular_trees():
+    """Trees with early leaves (packed with dummy splits below them), depth 10."""
+    rng = np.random.default_rng(19)
+    cfg = mini_config(p_nan=0.1, n_features=12, n_prog=400, s_max=9)
+    b = gen_batch(cfg)
+    pool = np.unique(b["features"][~np.isnan(b["features"])])
+    ens = _irregular_ensemble(rng, n_trees=19, n_features=12, max_depth=10, thr_pool=pool)
+
+    def depth(n):
+        return 0 if ens["feature"][n] < 0 else 1 + max(depth(ens["left"][n]), depth(ens["right"][n]))
+    assert max(depth(r) for r in ens["root"]) == 10
+    _check(cfg, ens=_exact_leaves(ens), b=b, exact=True)
+
+
+def test_binned_special_thresholds_and_values():
+    """Thresholds NaN, +-inf, -0.0, +0.0 and denormals; feature values equal to thresholds, their
+    fp32 neighbours, +-inf, +-0 and NaN: the codes order every value exactly as the fp32 compare."""
+    rng = np.random.default_rng(5)
+    cfg = get_config("tiny", exact=True).with_(depth=9, n_trees=40, n_prog=400, s_max=8, p_nan=0.1,
+                                               n_features=24, name="binned-special")
+    ens = gen_ensemble(cfg)
+    internal = np.nonzero(ens["feature"] >= 0)[0]
+    special = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, 1e-45, -1e-45, 1e-40], np.float32)
+    pick = rng.choice(internal, size=internal.size // 4, replace=False)
+    ens["threshold"] = ens["threshold"].copy()
+    ens["threshold"][pick] = rng.choice(special, size=pick.size)
+    b = gen_batch(cfg)
+    X = b["features"].copy()
+    n = b["n_rows"]
+    vals = np.concatenate([special, np.nextafter(special[1:], np.float32(0))]).astype(np.float32)
+    for r in range(0, n, 2):
+        for nd in rng.choice(internal, 6, replace=False):
+            f, th = ens["feature"][nd], np.float32(ens["threshold"][nd])
+            X[f, r] = rng.choice([th, np.nextafter(th, np.float32(-np.inf)), np.nextafter(th, np.float32(np.inf)),
+                                  rng.choice(vals)])
+    b["features"] = X
+    _check(cfg, ens=_exact_leaves(ens), b=b)
+
+
+@pytest.mark.parametrize("n_features", [193, 256])
+def test_binned_wide_tiles_staged_directly(n_features):
+    """Tiles of more than 192 features are staged without the register prefetch; 256 is the widest
+    binned ensemble."""
+    cfg = get_config("tiny", exact=True).with_(depth=10, n_trees=37, n_prog=500, s_max=12, p_nan=0.1,
+                                               n_features=n_features, name="binned-f%d" % n_features)
+    _check(cfg)
+
+
+@pytest.mark.parametrize("depth", [8, 10])
+def test_fp32_walk_wide_ensembles(depth):
+    """More than 256 features: the fp32 walk (16-bit feature codes) scores the round."""
+    cfg = get_config("tiny", exact=True).with_(depth=depth, n_trees=21, n_prog=300, s_max=8, p_nan=0.1,
+                                               n_features=300, name="fp32-wide-d%d" % depth)
+    _check(cfg)
+
+
+def test_fp32_walk_many_distinct_thresholds():
+    """One feature split at more than 65,534 distinct thresholds does not fit 16-bit codes: the fp32
+    walk scores the round, bit-exact."""
+    rng = np.random.default_rng(11)
+    cfg = get_config("tiny", exact=True).with_(depth=10, n_trees=70, n_prog=200, s_max=6, p_nan=0.1,
+                                               n_features=8, name="fp32-many-thr")
+    ens = gen_ensemble(cfg)
+    internal = np.nonzero(ens["feature"] >= 0)[0]
+    ens["feature"] = ens["feature"].copy()
+    ens["threshold"] = ens["threshold"].copy()
+    ens["feature"][internal] = 0
+    thr = np.unique(np.float32(10.0) ** rng.uniform(-3, 3, size=internal.size * 2).astype(np.float32))
+    assert thr.size > 65534
+    ens["threshold"][internal] = rng.permutation(thr)[:internal.size]
+    assert np.unique(ens["threshold"][internal]).size > 65534
+    _check(cfg, ens=ens)
