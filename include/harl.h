@@ -201,6 +201,21 @@ int harl_topk(const float *d_score, int32_t n, int32_t k, int64_t index_base, fl
 /* Fill a running top-k with the empty sentinel (-inf, INT64_MAX) in every slot. */
 int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *stream);
 
+/*
+ * For callers that cannot allocate device memory (work recorded under stream or graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): harl_topk without a workspace argument.
+ * Its candidate buffers are a library-owned device array of HARL_TOPK_STATIC_SCRATCH_BYTES per
+ * device, held from the first call on that device until the process ends; the call itself
+ * allocates nothing.  Arguments, results and errors as harl_topk, plus HARL_E_UNSUPPORTED when
+ * harl_topk_workspace_size(n, k) exceeds HARL_TOPK_STATIC_SCRATCH_BYTES (k = 2048 allows
+ * n <= 2,088,960; k = 1024, n <= 4,186,112; k = 128, n <= 33,546,240).  Every call on one device shares that device's
+ * array: calls that may overlap on one device (other streams, other host threads) race and must be
+ * ordered by the caller; each call writes the buffers before it reads them, so nothing carries over.
+ */
+#define HARL_TOPK_STATIC_SCRATCH_BYTES (8u << 20)
+int harl_topk_static(const float *d_score, int32_t n, int32_t k, int64_t index_base, float *d_io_score,
+                     int64_t *d_io_index, uint32_t flags, void *stream);
+
 /* ============================================================================================
  * Per-modification-type action selection (Section 4.3: the best modification of each type;
  * Appendix A.1: num_iters^2 + 1 tile-size actions and 3 per other type; Section 6.1: PPO rollouts

@@ -131,24 +131,59 @@ size_t harl_topk_workspace_size(int32_t n, int32_t k) {
     return harl::topk_ws_bytes(n, k);
 }
 
+// Checks shared by harl_topk and harl_topk_static (everything but the workspace); *done is set
+// when the call is a valid no-op.
+static int topk_check(const char *who, const float *d_score, int32_t n, int32_t k, int64_t index_base,
+                      const float *d_io_score, const int64_t *d_io_index, uint32_t flags, bool *done) {
+    *done = false;
+    const std::string w(who);
+    if (n < 0 || k < 0) return fail(HARL_E_INVALID_ARG, w + ": negative size");
+    if (k > HARL_TOPK_MAX_K) return fail(HARL_E_UNSUPPORTED, w + ": k above HARL_TOPK_MAX_K");
+    if (flags & ~HARL_TOPK_MERGE) return fail(HARL_E_INVALID_ARG, w + ": unknown flag");
+    if (!(flags & HARL_TOPK_MERGE) && k > n) return fail(HARL_E_INVALID_ARG, w + ": k > n without HARL_TOPK_MERGE");
+    if (index_base < 0 || index_base > ((int64_t)1 << 62) - 1 - n)
+        return fail(HARL_E_INVALID_ARG, w + ": index_base out of range");
+    if (k == 0) {
+        *done = true;
+        return HARL_OK;
+    }
+    if (!d_io_score || !d_io_index) return fail(HARL_E_INVALID_ARG, w + ": null output");
+    if (!aligned(d_io_score, 4) || !aligned(d_io_index, 8)) return fail(HARL_E_INVALID_ARG, w + ": misaligned output");
+    if (n == 0) {  // only reachable with MERGE: nothing to merge
+        *done = true;
+        return HARL_OK;
+    }
+    if (!d_score || !aligned(d_score, 4)) return fail(HARL_E_INVALID_ARG, w + ": null or misaligned scores");
+    return HARL_OK;
+}
+
 int harl_topk(const float *d_score, int32_t n, int32_t k, int64_t index_base, float *d_io_score, int64_t *d_io_index,
               uint32_t flags, void *d_ws, size_t ws_bytes, void *stream) {
-    if (n < 0 || k < 0) return fail(HARL_E_INVALID_ARG, "harl_topk: negative size");
-    if (k > HARL_TOPK_MAX_K) return fail(HARL_E_UNSUPPORTED, "harl_topk: k above HARL_TOPK_MAX_K");
-    if (flags & ~HARL_TOPK_MERGE) return fail(HARL_E_INVALID_ARG, "harl_topk: unknown flag");
-    if (!(flags & HARL_TOPK_MERGE) && k > n) return fail(HARL_E_INVALID_ARG, "harl_topk: k > n without HARL_TOPK_MERGE");
-    if (index_base < 0 || index_base > ((int64_t)1 << 62) - 1 - n)
-        return fail(HARL_E_INVALID_ARG, "harl_topk: index_base out of range");
-    if (k == 0) return HARL_OK;
-    if (!d_io_score || !d_io_index) return fail(HARL_E_INVALID_ARG, "harl_topk: null output");
-    if (!aligned(d_io_score, 4) || !aligned(d_io_index, 8)) return fail(HARL_E_INVALID_ARG, "harl_topk: misaligned output");
-    if (n == 0) return HARL_OK;  // only reachable with MERGE: nothing to merge
-    if (!d_score || !aligned(d_score, 4)) return fail(HARL_E_INVALID_ARG, "harl_topk: null or misaligned scores");
+    bool done = false;
+    if (const int rc = topk_check("harl_topk", d_score, n, k, index_base, d_io_score, d_io_index, flags, &done)) return rc;
+    if (done) return HARL_OK;
     if (!d_ws || !aligned(d_ws, 256)) return fail(HARL_E_INVALID_ARG, "harl_topk: workspace null or not 256-byte aligned");
     if (ws_bytes < harl::topk_ws_bytes(n, k))
         return fail(HARL_E_WORKSPACE, "harl_topk: workspace smaller than harl_topk_workspace_size()");
     return harl::topk_launch(d_score, n, k, index_base, d_io_score, d_io_index, flags, d_ws, ws_bytes,
                              static_cast<hipStream_t>(stream));
+}
+
+int harl_topk_static(const float *d_score, int32_t n, int32_t k, int64_t index_base, float *d_io_score,
+                     int64_t *d_io_index, uint32_t flags, void *stream) {
+    bool done = false;
+    if (const int rc = topk_check("harl_topk_static", d_score, n, k, index_base, d_io_score, d_io_index, flags, &done))
+        return rc;
+    if (done) return HARL_OK;
+    const size_t need = harl::topk_ws_bytes(n, k);
+    if (need > (size_t)HARL_TOPK_STATIC_SCRATCH_BYTES)
+        return fail(HARL_E_UNSUPPORTED, "harl_topk_static: n and k need " + std::to_string(need) +
+                                            " bytes of scratch, above HARL_TOPK_STATIC_SCRATCH_BYTES (" +
+                                            std::to_string((size_t)HARL_TOPK_STATIC_SCRATCH_BYTES) + "); use harl_topk");
+    void *ws = nullptr;
+    if (const int rc = harl::topk_scratch(&ws)) return rc;
+    return harl::topk_launch(d_score, n, k, index_base, d_io_score, d_io_index, flags, ws,
+                             (size_t)HARL_TOPK_STATIC_SCRATCH_BYTES, static_cast<hipStream_t>(stream));
 }
 
 int harl_topk_reset(float *d_io_score, int64_t *d_io_index, int32_t k, void *stream) {

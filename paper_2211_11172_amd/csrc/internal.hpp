@@ -113,6 +113,7 @@ size_t topk_ws_bytes(int32_t n, int32_t k);
 int topk_launch(const float *score, int32_t n, int32_t k, int64_t index_base, float *io_score,
                 int64_t *io_index, uint32_t flags, void *ws, size_t ws_bytes, hipStream_t stream);
 int topk_reset_launch(float *io_score, int64_t *io_index, int32_t k, hipStream_t stream);
+int topk_scratch(void **out);
 
 int track_advantage_launch(const float *c_prev, const float *c_next, const float *v_prev, const float *v_next, int32_t n,
                            float gamma, float eps, float *reward, float *adv, hipStream_t stream);

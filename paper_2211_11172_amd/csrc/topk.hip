@@ -22,10 +22,18 @@
 //    other list that rank ahead of it).
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "internal.hpp"
 
 namespace harl {
 namespace {
+
+// The candidate buffers of harl_topk_static: a file-scope device array instead of a caller
+// workspace.  Every device that runs the library holds its own copy until the process ends.  In host
+// code its name is only a host-side stand-in: kernels get the device address that
+// hipGetSymbolAddress returns for the current device (topk_scratch below), never the name itself.
+static __device__ __align__(256) unsigned char scratch[HARL_TOPK_STATIC_SCRATCH_BYTES];
 
 constexpr int kSelThreads = 1024;
 constexpr int kPerThread = 8;
@@ -356,6 +364,25 @@ int topk_launch(const float *score, int32_t n, int32_t k, int64_t index_base, fl
                            io_index, k);
         HARL_HIP_CHECK(hipGetLastError());
     }
+    return HARL_OK;
+}
+
+// Device address of this device's `scratch`, looked up once per device (with that device current)
+// and kept.
+int topk_scratch(void **out) {
+    static std::mutex mu;
+    static void *addr[64] = {nullptr};
+    int dev = 0;
+    HARL_HIP_CHECK(hipGetDevice(&dev));
+    if (dev < 0 || dev >= 64) return fail(HARL_E_UNSUPPORTED, "harl_topk_static: device index above 63");
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "harl_topk_static: scratch address");
+        addr[dev] = p;
+    }
+    *out = addr[dev];
     return HARL_OK;
 }
 

@@ -29,7 +29,7 @@ EXPORTS = (
     "harl_ensemble_create", "harl_ensemble_destroy", "harl_ensemble_info",
     "harl_score_round_workspace_size", "harl_score_round",
     "harl_policy_create", "harl_policy_destroy", "harl_policy_step",
-    "harl_topk_workspace_size", "harl_topk", "harl_topk_reset",
+    "harl_topk_workspace_size", "harl_topk", "harl_topk_reset", "harl_topk_static",
     "harl_policy_select",
     "harl_ppo_param_count", "harl_ppo_workspace_size", "harl_ppo_update",
     "harl_track_advantage", "harl_track_keep_count", "harl_track_eliminate_workspace_size", "harl_track_eliminate",
@@ -121,6 +121,7 @@ def load():
                 "harl_topk_workspace_size": ([i32, i32], sz),
                 "harl_topk": ([P, i32, i32, i64, P, P, u32, P, sz, P], ctypes.c_int),
                 "harl_topk_reset": ([P, P, i32, P], ctypes.c_int),
+                "harl_topk_static": ([P, i32, i32, i64, P, P, u32, P], ctypes.c_int),
                 "harl_ppo_param_count": ([P], sz),
                 "harl_ppo_workspace_size": ([P, i32], sz),
                 "harl_ppo_update": ([P, P, P, P, i32, P, P, P, P, P, i32, P, P, P, sz, P], ctypes.c_int),
@@ -272,6 +273,14 @@ def harl_topk_workspace_size(n: int, k: int) -> int:
 def harl_topk(score, n: int, k: int, index_base: int, io_score, io_index, flags: int, ws, ws_bytes: int, stream=None):
     _check(load().harl_topk(_ptr(score), n, k, index_base, _ptr(io_score), _ptr(io_index), flags, _ptr(ws), ws_bytes,
                             _stream(stream)), "harl_topk")
+
+
+def harl_topk_static(score, n: int, k: int, index_base: int, io_score, io_index, flags: int, stream=None):
+    _check(load().harl_topk_static(_ptr(score), n, k, index_base, _ptr(io_score), _ptr(io_index), flags,
+                                   _stream(stream)), "harl_topk_static")
+
+
+HARL_TOPK_STATIC_SCRATCH_BYTES = 8 << 20
 
 
 def harl_topk_reset(io_score, io_index, k: int, stream=None):
