@@ -227,8 +227,8 @@ def test_degenerate_cases_bit_exact(case):
 
 def test_throughput_measured_set_full_size():
     """65,536 measured programs (2,134,518 rows), the benchmark's launch configuration (Ansor's
-    settings, depth 10): bins bit-exact on every row; a depth-1 round bit-exact against the oracle
-    (the root's decision over all rows); the depth-10 round's margin change on 4,096 sampled rows
+    settings, depth 10): bins bit-exact on every row; a depth-1 and the depth-10 round bit-exact
+    against the oracle (every node field, leaf value and margin); the depth-10 round's margin change on 4,096 sampled rows
     equal to the leaf the scoring oracle reaches by routing the raw features through the GPU's tree
     (thresholds, default directions and leaves agree with the bins the tree was grown on)."""
     require_gpu()
@@ -252,6 +252,11 @@ def test_throughput_measured_set_full_size():
     got, gm = gpu_rounds(want_bins, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"], m0, 1)
     tree = got[0]
     assert (tree["feature"] >= 0).sum() >= 8
+    log("gbdt full size: the oracle's depth-10 round on all rows")
+    want, wm = oracle_rounds(want_bins, F, m["cuts"], m["n_cuts"], m["prog_ptr"], m["label"], m["weight"], m0, 1,
+                             **oracle.GBDT_DEFAULTS)
+    assert_trees_equal(got, want, "full size depth 10")
+    np.testing.assert_array_equal(gm.view(np.uint32), wm.view(np.uint32))
     rows = np.sort(np.random.default_rng(5).choice(N, 4096, replace=False))
     ens = dict(n_trees=1, n_features=F, root=np.zeros(1, np.int32), feature=tree["feature"],
                threshold=tree["threshold"], left=tree["left"], right=tree["right"],
