@@ -26,32 +26,38 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 N_CU, CLOCK_GHZ = 256, 2.4
-# Node-visit ceiling of tree traversal: a visit must read at least 12 bytes from LDS (an 8-byte
-# node and a 4-byte feature); the LDS read rate measured on MI355X with 16-byte reads is
-# 152 B/clk/CU (100 B/clk/CU with 4- and 8-byte reads).
-LDS_BYTES_PER_CLK = 152.0
-LDS_BYTES_PER_VISIT = 12.0
-PEAK_GVISITS = N_CU * CLOCK_GHZ * LDS_BYTES_PER_CLK / LDS_BYTES_PER_VISIT  # G visits / s
+# Node-visit ceiling of tree traversal, from the chip's unit counts: 256 CUs x 4 SIMDs x 16 lanes x
+# 2.4 GHz = 39.3 T VALU lane-instructions/s, and a visit of the walk needs at least 5 VALU
+# instructions (a subtraction and a compare that decide the child, two selects for the child's
+# feature and record, one address update) -> 7.86 T visits/s.  The LDS gives the same figure: a
+# visit reads 10 bytes (an 8-byte node record, a 2-byte feature code) at 128 B/clk/CU.
+VALU_LANES_PER_CLK = 4 * 16
+VALU_PER_VISIT = 5
+PEAK_GVISITS = N_CU * CLOCK_GHZ * VALU_LANES_PER_CLK / VALU_PER_VISIT  # G visits / s
 
 # HBM bytes of one harl_score_round call (tree walk + segmented sum), measured with rocprofv3 --pmc
 # FETCH_SIZE and WRITE_SIZE over 3 eager calls and scaled by what the same counters read for a
 # 256 MiB device-to-device copy (x2.000 for FETCH_SIZE, x1.000 for WRITE_SIZE).  Keyed by workload
-# and by the SHA-256 of the scoring source the counters were taken with: any other source reports
-# null.
+# and by the SHA-256 of the scoring sources (score.hip, score_bin.hip, walk_b16.hpp) the counters were
+# taken with: any other source reports null.
 SCORE_TRAFFIC_BYTES = {
-    ("standard", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 58.93e6,
-    ("ingest-16x1", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 1.4612e9,
-    ("ingest-4x4", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 1.4608e9,
-    ("ingest-2x8", "cd57195dd9d7ff2ca0f7410ee41890d37447d87b3372aaa3db81ff4de8fc7a39"): 1.4702e9,
 }
 
 
-def score_traffic(cfg_name):
+SCORE_SOURCES = ("score.hip", "score_bin.hip", "walk_b16.hpp")
+
+
+def score_digest():
     import hashlib
-    src = os.path.join(ROOT, "paper_2211_11172_amd", "csrc", "score.hip")
-    with open(src, "rb") as f:
-        digest = hashlib.sha256(f.read()).hexdigest()
-    return SCORE_TRAFFIC_BYTES.get((cfg_name, digest))
+    h = hashlib.sha256()
+    for name in SCORE_SOURCES:
+        with open(os.path.join(ROOT, "paper_2211_11172_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def score_traffic(cfg_name):
+    return SCORE_TRAFFIC_BYTES.get((cfg_name, score_digest()))
 
 
 def parse():
@@ -92,6 +98,9 @@ def parse():
                          "eta 0.2, gamma 0.001) on 4,096 measured programs (the standard round's statements, 66,923 "
                          "rows) and on 65,536 (the throughput round's, 2.13 M rows), 164 features binned to at most "
                          "255 bins (harl_gbdt_bin, timed on its own); prints one JSON line and exits")
+    ap.add_argument("--visit-probe", action="store_true",
+                    help="visit-loop microbenchmark: the binned walk with its tile and trees resident in LDS "
+                         "(libharl_probe.so), node visits/s for 1 .. 16 waves per CU; prints one JSON line and exits")
     ap.add_argument("--two-streams", action="store_true",
                     help="run the policy on a second stream after scoring, beside top-K (default: the "
                          "three calls in turn on one stream, which measured faster on the standard round)")
@@ -234,6 +243,78 @@ def ingest_calibration(args):
     print(json.dumps({"metric": "feature ingest HBM bandwidth (harl_score_round, shallow ensembles)",
                       "rows": n_rows, "algorithmic_bytes": alg_bytes, "peak_gbs": PEAK_HBM_GBS,
                       "steps": args.steps, "results": rows}), flush=True)
+
+
+def visit_probe(args):
+    """The walk of the binned scoring kernel with its code tile and every wave's tree resident in LDS
+    (libharl_probe.so, the same walk code): node visits/s for 1 .. 12 waves per CU at depth 10 (the
+    streamed workload's trees; 12 waves is the scoring kernel's shape) and 16 at depth 9, random
+    codes (10 % missing) and random trees over 164 features.  The depth-10, 12-wave rate is the
+    ceiling of the scoring kernel's walk without staging, streaming and reductions."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2211_11172_amd", "libharl_probe.so"))
+    P = ctypes.c_void_p
+    lib.harl_probe_visits.argtypes = [ctypes.c_int] * 5 + [P, P, ctypes.c_int, P, P, P]
+    lib.harl_probe_visits.restype = ctypes.c_int
+    F, n_trees, n_blocks = 164, 64, N_CU
+    rng = np.random.default_rng(7)
+    codes = rng.integers(0, 2600, size=(2, F, 64, 2)).astype(np.uint16)
+    codes[rng.random(codes.shape) < 0.1] = 0xFFFF
+    d_codes = torch.from_numpy(codes.view(np.uint32).reshape(-1).copy()).cuda()
+    out = torch.empty(n_blocks * 64 * 16, dtype=torch.float64, device="cuda")
+    results = []
+    for depth, waves in ((10, 1), (10, 2), (10, 4), (10, 8), (10, 12), (9, 16)):
+        M = 1 << depth
+        trees = np.zeros((n_trees, 6 * M), np.uint8)
+        words = trees.view(np.uint32)                         # [n_trees][6M / 4]
+        theta = rng.integers(0, 2600, size=(n_trees, M)).astype(np.uint32)
+        U = (0xFFFF - theta - (rng.random((n_trees, M)) < 0.5)).astype(np.uint32)
+        feats = rng.integers(0, F, size=(n_trees, M)).astype(np.uint32)
+        words[:, 0] = feats[:, 1]
+        i = np.arange(1, M // 2)
+        words[:, 2 * i] = theta[:, i] | U[:, i] << 16                 # record i at byte 8i
+        words[:, 2 * i + 1] = feats[:, 2 * i] | feats[:, 2 * i + 1] << 8
+        k = np.arange(M // 2)
+        words[:, M + k] = theta[:, M // 2 + k] | U[:, M // 2 + k] << 16  # last level at byte 4M + 4k
+        d_trees = torch.from_numpy(trees.reshape(-1).copy()).cuda()
+        d_leaves = torch.from_numpy(rng.standard_normal((n_trees, M)).astype(np.float32)).cuda()
+
+        def run(reps):
+            rc = lib.harl_probe_visits(waves, depth, reps, F, n_blocks, d_codes.data_ptr(), d_trees.data_ptr(), n_trees,
+                                       d_leaves.data_ptr(), out.data_ptr(), None)
+            if rc != 0:
+                raise RuntimeError("harl_probe_visits failed (%d)" % rc)
+        run(2)
+        torch.cuda.synchronize()
+        reps = 8
+        while True:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            run(reps)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            if ms > 20 or reps > 1 << 16:
+                break
+            reps *= 4
+        chains = waves * 4                                    # per CU: 4 rows per lane per wave
+        visits = n_blocks * waves * 64 * 4 * reps * depth
+        rate = visits / (ms * 1e-3)
+        # cycles per tree level of one row-chain: a CU holds `chains` wave-chains of 64 lanes
+        cyc = N_CU * CLOCK_GHZ * 1e9 * chains * 64 / rate
+        results.append({"depth": depth, "waves_per_cu": waves, "chains_per_cu": chains, "reps": reps, "ms": ms,
+                        "gvisits": rate / 1e9, "cycles_per_level_per_chain": cyc})
+        print("probe depth %d, %d waves: %.0f Gvisit/s, %.0f cycles per level per chain" % (depth, waves, rate / 1e9, cyc),
+              file=sys.stderr, flush=True)
+    ceiling = [r for r in results if r["depth"] == 10 and r["waves_per_cu"] == 12][0]["gvisits"]
+    print(json.dumps({"metric": "visit-loop probe: node visits/s of the binned walk with every operand resident in LDS",
+                      "unit": "Gvisit/s", "n_features": F, "workgroups": n_blocks,
+                      "ceiling_depth10_12waves_gvisits": ceiling, "valu_derived_peak_gvisits": PEAK_GVISITS,
+                      "results": results}), flush=True)
 
 
 def tracks_bench(args):
@@ -773,7 +854,7 @@ def main():
               "program range, with one all-gather of each GPU's top-k)", file=sys.stderr)
         sys.exit(2)
     modes = {"ingest": ingest_calibration, "tracks": tracks_bench, "select": select_bench, "ppo": ppo_bench,
-             "refit": refit_bench}
+             "refit": refit_bench, "visit_probe": visit_probe}
     for name, fn in modes.items():
         if getattr(args, name):
             fn(args)

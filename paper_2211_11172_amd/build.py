@@ -1,7 +1,8 @@
 """Build libharl.so (the HIP kernels and the C ABI) for gfx950 with hipcc, in-tree.
 
 Usage: ``python -m paper_2211_11172_amd.build`` (or ``build()`` from Python).  Objects go to
-``paper_2211_11172_amd/_build``; the library to ``paper_2211_11172_amd/libharl.so``.
+``paper_2211_11172_amd/_build``; the library to ``paper_2211_11172_amd/libharl.so``, and the
+visit-loop microbenchmark (``probe/``) to ``paper_2211_11172_amd/libharl_probe.so``.
 """
 from __future__ import annotations
 
@@ -54,6 +55,14 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (r.stdout, r.stderr))
     os.replace(tmp, LIB)
+    # the visit-loop microbenchmark (probe/): a separate library only the benchmark loads
+    for src in sorted(glob.glob(os.path.join(PKG, "probe", "*.hip"))):
+        out = os.path.join(PKG, "lib" + "harl_probe" + ".so")
+        tmp = out + ".tmp%d" % os.getpid()
+        r = subprocess.run([hipcc(), *CXXFLAGS, "-shared", src, "-o", tmp], capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, r.stdout, r.stderr))
+        os.replace(tmp, out)
     if verbose:
         print("built", LIB)
     return LIB

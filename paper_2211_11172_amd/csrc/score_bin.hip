@@ -48,135 +48,14 @@
 #include <vector>
 
 #include "internal.hpp"
+#include "walk_b16.hpp"
 
 namespace harl {
 namespace {
 
-constexpr int kWave = 64;
+using namespace b16;
 constexpr int kLdsBytes = 160 * 1024;
-constexpr int kRT = 256;                        // rows per tile
-constexpr int kRPL = 4;                         // rows per lane
-constexpr uint32_t kRowBytes = kRT * 2;         // bytes per feature row of a tile
-constexpr int kTileU4 = kRowBytes / 16;         // uint4 per feature row of a tile (32)
 constexpr int kPrefetchFeatures = 192;          // features per tile held in the register prefetch
-constexpr uint32_t kMissing = 0xFFFFu;
-constexpr uint32_t kGroupStride = 65536;        // LDS bytes between the tile's two row groups
-
-// LDS accesses by absolute byte address.
-__device__ __forceinline__ uint32_t lds_u16(uint32_t a) {
-    return *(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)a;
-}
-__device__ __forceinline__ uint32_t lds_b32(uint32_t a) {
-    return *(const __attribute__((address_space(3))) uint32_t *)(uintptr_t)a;
-}
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint2 lds_b64(uint32_t a) {
-    const u32x2 v = *(const __attribute__((address_space(3))) u32x2 *)(uintptr_t)a;
-    return make_uint2(v.x, v.y);
-}
-typedef __attribute__((address_space(3))) char lds_char;
-__device__ __forceinline__ uint32_t lds_addr(const char *p) { return (uint32_t)(uintptr_t)(const lds_char *)p; }
-
-// An opaque VGPR copy of a wave-uniform value (so that one v_cndmask can select between two).
-__device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
-    asm("" : "+v"(v));
-    return v;
-}
-
-// One inner decision: code c at a node with word w = theta | U << 16 and child features p (byte 0
-// left, byte 1 right).  Writes the child's feature into byte 1 of the code address xa (the other
-// bytes, the lane's row, are kept) and returns sel = go right ? r : l.  The compare writes VCC and
-// the SDWA select reads it (two wait states between them).
-__device__ __forceinline__ void decide(uint32_t c, uint32_t w, uint32_t p, uint32_t l, uint32_t r, uint32_t &xa,
-                                       uint32_t &sel) {
-    uint32_t d;
-    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
-        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
-        "s_nop 1\n\t"
-        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 src1_sel:BYTE_1\n\t"
-        "v_cndmask_b32 %[s], %[l], %[r], vcc"
-        : [d] "=&v"(d), [xa] "+v"(xa), [s] "=&v"(sel)
-        : [c] "v"(c), [w] "v"(w), [p] "v"(p), [l] "v"(l), [r] "v"(r)
-        : "vcc");
-}
-
-// Last level: byte offset of the leaf reached, o0 + (go right ? 4 : 0).
-__device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t o0, uint32_t o1) {
-    uint32_t d, out;
-    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
-        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
-        "s_nop 1\n\t"
-        "v_cndmask_b32 %[o], %[a], %[b], vcc"
-        : [d] "=&v"(d), [o] "=&v"(out)
-        : [c] "v"(c), [w] "v"(w), [a] "v"(o0), [b] "v"(o1)
-        : "vcc");
-    return out;
-}
-
-struct Head {
-    uint32_t f, w, p;  // root feature, root word, root's children's features (D >= 2)
-};
-
-// Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows;
-// xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each level rewrites.  The
-// rows are independent chains: each takes its step of a level in turn, so the reads of the others
-// are in flight while one decides.  The tree's leaves are at gl (M floats); each chain's leaf is
-// loaded into pend[] after the previous tree's pending leaf has been added to acc[].
-__device__ __forceinline__ void walk(uint32_t tb, int D, const Head &h, uint32_t (&xa)[kRPL], double (&acc)[kRPL],
-                                     const float *__restrict__ gl, float (&pend)[kRPL]) {
-    const uint32_t M = 1u << D;
-    uint32_t x[kRPL], a[kRPL], lw[kRPL];
-    uint2 rec[kRPL];
-#pragma unroll
-    for (int c = 0; c < kRPL; ++c) {
-        xa[c] = (xa[c] & 0xFFFF00FFu) | (h.f << 8);
-        x[c] = lds_u16(xa[c]);
-    }
-    const uint32_t hw = in_vgpr(h.w), hp = in_vgpr(h.p);
-    const uint32_t l0 = in_vgpr(tb + 16u), r0 = in_vgpr(tb + 24u);
-#pragma unroll
-    for (int c = 0; c < kRPL; ++c) {
-        uint32_t s;
-        decide(x[c], hw, hp, l0, r0, xa[c], s);
-        x[c] = lds_u16(xa[c]);
-        a[c] = s;
-        rec[c] = lds_b64(s);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    // levels 1 .. D-3: record address of child 2n + g = 2a - tb + 8g
-    const uint32_t li = in_vgpr(0u - tb), ri = in_vgpr(8u - tb);
-    for (int lvl = 1; lvl + 2 < D; ++lvl) {
-#pragma unroll
-        for (int c = 0; c < kRPL; ++c) {
-            uint32_t s;
-            decide(x[c], rec[c].x, rec[c].y, li, ri, xa[c], s);
-            x[c] = lds_u16(xa[c]);
-            a[c] = 2u * a[c] + s;
-            rec[c] = lds_b64(a[c]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    }
-    // level D-2 into the last level: the child's word at as + 2M, as = a + 4g
-    const uint32_t lt = in_vgpr(0u), rt = in_vgpr(4u), k2m = 2u * M;
-#pragma unroll
-    for (int c = 0; c < kRPL; ++c) {
-        uint32_t s;
-        decide(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
-        x[c] = lds_u16(xa[c]);
-        a[c] = a[c] + s;
-        lw[c] = lds_b32(a[c] + k2m);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    // last-level node k = (as - tb - 2M) / 4; its leaves at byte 8k of the tree's leaves
-    const uint32_t kb2 = 0u - 2u * tb - 4u * M;
-#pragma unroll
-    for (int c = 0; c < kRPL; ++c) {
-        const uint32_t o0 = 2u * a[c] + kb2;
-        const uint32_t o = leaf_off(x[c], lw[c], o0, o0 + 4u);
-        acc[c] += (double)pend[c];
-        pend[c] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(gl) + o);
-    }
-}
 
 // ---- K0: codes of every (row, feature) ----
 // The order-preserving 32-bit key of a present value is its bit pattern with the sign bit set for
@@ -324,9 +203,10 @@ __device__ __forceinline__ void tile_fetch(uint4 (&xf)[NPX], const uint4 *__rest
     const int total = F * kTileU4;
     const uint4 *p = codes + (int64_t)(threadIdx.x / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + threadIdx.x % kTileU4;
     const int64_t step = (int64_t)(NT / kTileU4) * ldw4;
+    // every element is assigned (a guarded assignment would leave xf to the stack)
 #pragma unroll
     for (int j = 0; j < NPX; ++j) {
-        if ((int)threadIdx.x + j * NT < total) xf[j] = *p;
+        xf[j] = (int)threadIdx.x + j * NT < total ? *p : make_uint4(0, 0, 0, 0);
         p += step;
     }
 }
@@ -348,31 +228,13 @@ __device__ __forceinline__ void tile_stage(uint4 *tile_lds, const uint4 *__restr
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int i = i0 + j * NT;
-            if (i < total) v[j] = codes[(int64_t)(i / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + (i % kTileU4)];
+            v[j] = i < total ? codes[(int64_t)(i / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + (i % kTileU4)]
+                             : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             if (i0 + j * NT < total) tile_lds[tile_lds_index(i0 + j * NT)] = v[j];
     }
-}
-
-// LDS placement of a workgroup's tree slots: n_a slots of `sb` bytes after row group 0 (from byte
-// 256 F up to 65536), the rest after row group 1 (from 65536 + 256 F); the row sums of a piece
-// reuse the second area, and two progress counters follow whichever of slots and sums is longer.
-struct SlotPlan {
-    int n_a;
-    uint32_t a0, b0, progress, lds;
-};
-__host__ __device__ __forceinline__ SlotPlan slot_plan(int F, int tw, uint32_t sb) {
-    SlotPlan p{};
-    p.a0 = 256u * (uint32_t)F;
-    p.b0 = kGroupStride + 256u * (uint32_t)F;
-    const int fit_a = (int)((kGroupStride - p.a0) / sb);
-    p.n_a = fit_a < tw ? fit_a : tw;
-    const uint32_t slots_b = (uint32_t)(tw - p.n_a) * sb, red = (uint32_t)tw * kRT * 8u;
-    p.progress = p.b0 + (slots_b > red ? slots_b : red);
-    p.lds = p.progress + 16u;
-    return p;
 }
 
 template <int TW, int PF>
