@@ -17,4 +17,7 @@ def pytest_configure(config):
 def _oracle_built():
     import oracle
     oracle.build(force=False)
+    # a differently built copy of the oracle (the sanitizer run points the pins at one)
+    if os.environ.get("HARL_ORACLE_LIBRARY"):
+        oracle.use_library(os.environ["HARL_ORACLE_LIBRARY"])
     yield

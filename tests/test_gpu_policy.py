@@ -59,7 +59,9 @@ def test_policy_heavy_bf16_small_batch():
 
 
 def test_bf16_large_batch_path():
-    # at >= 16384 states the kernel shares weight fragments among 4 state groups
+    # from 16,384 states bf16 policies run on the large-batch kernel (k_policy_x32: 128 states per
+    # workgroup, 32x32x16 MFMA tiles, weights streamed into LDS in chunks); 37 states in a ragged
+    # last workgroup
     _check(get_config("policy_heavy", exact=True), B=16384 + 37)
 
 
