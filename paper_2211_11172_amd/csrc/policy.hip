@@ -6,24 +6,36 @@
 // K4 k_policy: the three dense contractions run on MFMA, transposed so that states are the MFMA
 // N dimension (H^T = W X^T).  A workgroup holds 16*NSG states and U waves; a wave computes its
 // share of each layer's 16-unit tiles in groups of TP tiles.
-//   phase 0  the states are staged into LDS ([state][unit], padded rows);
+//   start    every wave issues the global loads its first tile groups need up front (states,
+//            biases, the first W1 fragments into a register ring, the first head fragments; the
+//            first W2 fragments into a second ring right after phase 0), so that the kernel waits
+//            on memory latency about once rather than once per phase;
+//   phase 0  the biases and the states are staged into LDS (activation layout below);
 //   phase 1  each wave computes its 1/U of h1's tiles for all states, TP tiles at a time (A =
-//            W1 fragments streamed from global memory through a kRing-deep register ring, B =
-//            states from LDS, read one k-group ahead), applies bias + ReLU (+ bf16 rounding) and
-//            stores the tiles to LDS;
+//            W1 fragments streamed from global memory through the register ring, B = states
+//            from LDS, read one k-group ahead), applies bias + ReLU (+ bf16 rounding) and stores
+//            the tiles to LDS;
 //   phase 2  each wave computes its 1/U of h2's tiles the same way (B = h1 from LDS; every A
 //            fragment feeds NSG state groups) and feeds each finished tile straight from its
 //            accumulator registers into the head contraction: the MFMA result layout of a tile is
 //            re-used as the B operand layout, with the head weights pre-permuted to match;
 //   phase 3  the U per-wave partial heads are summed in a fixed order; bias, argmax, softmax
-//            and value are computed per state and written out.
+//            and value are computed per state (one wave per state at a time) and written out.
 // fp32 policies use v_mfma_f32_16x16x4_f32, bf16 policies v_mfma_f32_16x16x32_bf16 (fp32
 // accumulation; h1, h2 rounded to bf16, nearest even).  Weights are pre-tiled at create time so
 // that a lane's operand for one "k-group" is 16 contiguous bytes:
 //   fp32: a k-group is 16 input units = 4 MFMAs; lane l, slot j (j < 4) holds unit 16g + 4(l/16) + j
 //   bf16: a k-group is 32 input units = 1 MFMA;  lane l, slot j (j < 8) holds unit 32g + 8(l/16) + j
-// so an activation row in LDS ([state][unit]) gives the B operand of k-group g at byte offset
-// 64g + 16(l/16) for either dtype.
+// Fragments are stored k-group-major ([g][tile][lane] x 16 B): the waves of a workgroup, which own
+// different tiles, read one contiguous stretch of the layer's weights at a time, spread evenly over
+// the cache channels.
+//
+// Activations in LDS are kept as 16-byte "unit blocks" (4 fp32 or 8 bf16 consecutive units of one
+// state), stored [unit block][state]: unit u of state s is at byte ((u / UB) NS + s) 16 + (u % UB) EL
+// (UB units per block, NS states per workgroup, EL bytes per element).  The B operand of k-group g
+// for the state group sg is then unit block 4g + l/16 of state 16 sg + l%16, so the 64 lanes read
+// 1 KB of consecutive bytes (no bank conflicts), and the finished h1 tiles are written back the same
+// way.
 //
 // MFMA operand layouts (lane l of 64; i indexes the 4 accumulator registers):
 //   16x16x4  f32 : A[m = l%16][k = l/16],          B[k = l/16][n = l%16]
@@ -35,6 +47,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 #include <vector>
 
 #include "internal.hpp"
@@ -43,7 +56,7 @@ namespace harl {
 namespace {
 
 constexpr int kMaxU = 8;      // waves per workgroup (at most)
-constexpr int kRing = 4;      // k-groups of weight fragments in flight per wave
+constexpr int kRing = 4;      // k-groups of W1 fragments in flight per wave (W2: the launch table)
 constexpr int kHiddenPad = 256;  // hidden widths padded to whole tile groups of every kernel shape
 constexpr int kX32MinBatch = 16384;  // bf16 batches from this size use k_policy_x32 (policy_x32.hip)
 
@@ -61,6 +74,80 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
     bf16x8 r;
     __builtin_memcpy(&r, &v, 16);
     return r;
+}
+
+// Reductions over groups of 16, 32 or 64 lanes without LDS round trips: DPP moves pair the lanes of
+// each row of 16 (xor 1, xor 2, half-row mirror, row mirror), then the gfx950 row swaps pair rows
+// 2k and 2k+1 (v_permlane16_swap) and the two halves of the wave (v_permlane32_swap).  Every step
+// pairs each lane with one partner and both combine the same two values in the same order, so all
+// lanes of a group end with the same bits.
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp(unsigned v) {
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+// (value, index) with the larger value, the lower index among equal values; NaN values never win
+__device__ __forceinline__ void argmax_step(float &best, int &best_i, float ov, int oi) {
+    const bool take = (ov > best) | ((ov == best) & (oi < best_i));
+    best = take ? ov : best;
+    best_i = take ? oi : best_i;
+}
+
+// the two values a lane sees after the row swap of span 16 or 32: the lower group's, the upper's
+template <int SPAN>
+__device__ __forceinline__ void swap_pair(unsigned v, unsigned &lo, unsigned &hi) {
+    const auto r = SPAN == 16 ? __builtin_amdgcn_permlane16_swap(v, v, false, false)
+                              : __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    lo = r[0];
+    hi = r[1];
+}
+
+template <int CTRL>
+__device__ __forceinline__ void argmax_dpp(float &best, int &best_i) {
+    argmax_step(best, best_i, __uint_as_float(dpp<CTRL>(__float_as_uint(best))), (int)dpp<CTRL>((unsigned)best_i));
+}
+
+template <int SPAN>
+__device__ __forceinline__ void argmax_swap(float &best, int &best_i) {
+    unsigned vl, vh, il, ih;
+    swap_pair<SPAN>(__float_as_uint(best), vl, vh);
+    swap_pair<SPAN>((unsigned)best_i, il, ih);
+    best = __uint_as_float(vl);
+    best_i = (int)il;
+    argmax_step(best, best_i, __uint_as_float(vh), (int)ih);
+}
+
+// lowest-index maximum over each group of `width` lanes (16, 32 or 64; uniform)
+__device__ __forceinline__ void group_argmax(float &best, int &best_i, int width) {
+    argmax_dpp<kDppXor1>(best, best_i);
+    argmax_dpp<kDppXor2>(best, best_i);
+    argmax_dpp<kDppHalfMirror>(best, best_i);
+    argmax_dpp<kDppMirror>(best, best_i);
+    if (width >= 32) argmax_swap<16>(best, best_i);
+    if (width >= 64) argmax_swap<32>(best, best_i);
+}
+
+template <int SPAN>
+__device__ __forceinline__ float sum_swap(float x) {
+    unsigned lo, hi;
+    swap_pair<SPAN>(__float_as_uint(x), lo, hi);
+    return __uint_as_float(lo) + __uint_as_float(hi);
+}
+
+// sum over each group of `width` lanes (16, 32 or 64; uniform)
+__device__ __forceinline__ float group_sum(float x, int width) {
+    x += __uint_as_float(dpp<kDppXor1>(__float_as_uint(x)));
+    x += __uint_as_float(dpp<kDppXor2>(__float_as_uint(x)));
+    x += __uint_as_float(dpp<kDppHalfMirror>(__float_as_uint(x)));
+    x += __uint_as_float(dpp<kDppMirror>(__float_as_uint(x)));
+    if (width >= 32) x = sum_swap<16>(x);
+    if (width >= 64) x = sum_swap<32>(x);
+    return x;
+}
+
+__device__ __forceinline__ float word(const uint4 &v, int q) {
+    return __uint_as_float(q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w);
 }
 
 template <bool BF16>
@@ -85,23 +172,21 @@ struct PolicyArgs {
     float *value, *probs, *logits;
 };
 
-// The A fragments of a layer's first RING iterations (see dense_layer), loaded before the layer
-// starts so that their latency overlaps the work before it.
+// The weight loads of the layer loops are unconditional (a layer's last round is a separate copy
+// that issues none, and the head fragments of absent head tiles are read from a valid tile and
+// never used): the compiler then knows how many loads follow each one and waits for exactly the
+// one it needs, instead of draining every load in flight.
+
+// The A fragments of a layer's first RING iterations (k-groups 0 .. RING - 1 of the wave's first
+// tile group; RING <= KG), loaded before the layer starts so that their latency overlaps the work
+// before it.
 template <int TP, int RING>
-__device__ __forceinline__ void ring_fill(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int t0, int n_tiles,
-                                          int KG, int l) {
-    const int NIT = n_tiles / TP * KG;
-    const int64_t tstride = (int64_t)KG * 64;
+__device__ __forceinline__ void ring_fill(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int NT, int t0, int l) {
 #pragma unroll
     for (int r = 0; r < RING; ++r) {
-        if (r < NIT) {
-            const uint4 *src = A + (int64_t)(t0 + TP * (r / KG)) * tstride + (int64_t)(r % KG) * 64 + l;
+        const uint4 *src = A + ((int64_t)r * NT + t0) * 64 + l;
 #pragma unroll
-            for (int j = 0; j < TP; ++j) ring[r][j] = src[j * tstride];
-        } else {
-#pragma unroll
-            for (int j = 0; j < TP; ++j) ring[r][j] = make_uint4(0, 0, 0, 0);
-        }
+        for (int j = 0; j < TP; ++j) ring[r][j] = src[j * 64];
     }
 }
 
@@ -109,108 +194,205 @@ __device__ __forceinline__ void ring_fill(uint4 (&ring)[RING][TP], const uint4 *
 // sum over KG k-groups (KG a multiple of RING), computed TP tiles at a time (TP independent
 // accumulator chains sharing every B fragment).  The wave's iterations (tile group, k-group) run
 // in order; `ring` holds the A fragments of the first RING iterations (ring_fill), and those of
-// iteration it + RING are loaded from `A` (packed [tile][g][lane] x 16 B) into ring slot it % RING
-// as soon as iteration it has issued its MFMAs; the B fragments of the next k-group are read from
-// the LDS activation rows `in` (row stride `in_stride` bytes) into the other half of a double
+// iteration it + RING are loaded from `A` (packed [g][tile][lane] x 16 B, NT tiles per k-group)
+// into ring slot it % RING as soon as iteration it has issued its MFMAs; the B fragments of the
+// next k-group are read from the LDS activation blocks `in` into the other half of a double
 // buffer.  done(first_tile, acc[TP][NSG]) consumes each finished group.
-template <bool BF16, int NSG, int TP, int RING, typename Done>
-__device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int t0, int n_tiles,
-                                            int KG, const char *in, int in_stride, int ln, int lq, int l, Done done) {
+template <bool BF16, int NSG, int TP, int RING, bool ONE_ROUND_COPY, typename Done>
+__device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int NT, int t0,
+                                            int n_tiles, int KG, const char *in, int ln, int lq, int l, Done done) {
     static_assert(RING % 2 == 0, "the B double buffer alternates with the ring slot");
+    constexpr int NS = 16 * NSG;
     const int n_groups = n_tiles / TP;
-    const int NIT = n_groups * KG;
-    const int64_t tstride = (int64_t)KG * 64;  // uint4 between the same k-group of consecutive tiles
-    auto a_src = [&](int it) {
-        return A + (int64_t)(t0 + TP * (it / KG)) * tstride + (int64_t)(it % KG) * 64 + l;
-    };
     auto b_load = [&](int g, uint4 (&b)[NSG]) {
 #pragma unroll
         for (int sg = 0; sg < NSG; ++sg)
-            b[sg] = *reinterpret_cast<const uint4 *>(in + (sg * 16 + ln) * in_stride + g * 64 + lq * 16);
+            b[sg] = *reinterpret_cast<const uint4 *>(in + ((g * 4 + lq) * NS + sg * 16 + ln) * 16);
     };
     uint4 b[2][NSG];
     b_load(0, b[0]);
-    for (int grp = 0; grp < n_groups; ++grp) {
-        f32x4 acc[TP][NSG];
+    f32x4 acc[TP][NSG];
+    // One round: RING iterations (k-groups g0 .. g0 + RING - 1 of tile group grp).  Every round but
+    // the layer's last refills its ring slots with the fragments of the next round (k-groups
+    // g0 + RING + r, or r of the next tile group: KG is a multiple of RING) and reads the B
+    // fragments one k-group ahead; the last round issues neither, so that no load is left in
+    // flight when the layer ends.  The two cases are separate copies of the round, so that every
+    // load in either is unconditional and the compiler knows exactly which one each use waits for.
+    auto round = [&](int grp, int g0, auto refill_tag) {
+        constexpr bool REFILL = decltype(refill_tag)::value;
+        const bool wrap = g0 + RING >= KG;
+        const uint4 *rsrc = A + ((int64_t)(wrap ? 0 : g0 + RING) * NT + t0 + TP * (grp + wrap)) * 64 + l;
+#pragma unroll
+        for (int r = 0; r < RING; ++r) {
+            const int g = g0 + r;
+            if (REFILL || r + 1 < RING) b_load(g + 1 == KG ? 0 : g + 1, b[(r + 1) & 1]);
+            if constexpr (BF16) {
+#pragma unroll
+                for (int sg = 0; sg < NSG; ++sg)
+#pragma unroll
+                    for (int j = 0; j < TP; ++j) mfma_group<true>(ring[r][j], b[r & 1][sg], acc[j][sg]);
+            } else {
+                // the 4 k-steps outermost: consecutive MFMAs feed different accumulators
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int sg = 0; sg < NSG; ++sg)
+#pragma unroll
+                        for (int j = 0; j < TP; ++j)
+                            acc[j][sg] = __builtin_amdgcn_mfma_f32_16x16x4f32(word(ring[r][j], q), word(b[r & 1][sg], q),
+                                                                              acc[j][sg], 0, 0, 0);
+            }
+            if constexpr (REFILL) {
+                const uint4 *src = rsrc + (int64_t)r * NT * 64;
+#pragma unroll
+                for (int j = 0; j < TP; ++j) ring[r][j] = src[j * 64];
+            }
+            // keep each refill right behind the MFMAs of its slot (left alone, the scheduler sinks
+            // all refills of a round to its end, and the next round then waits on them at once)
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    auto zero = [&]() {
 #pragma unroll
         for (int h = 0; h < TP; ++h)
 #pragma unroll
             for (int sg = 0; sg < NSG; ++sg) acc[h][sg] = f32x4{0, 0, 0, 0};
-        for (int g0 = 0; g0 < KG; g0 += RING) {
-#pragma unroll
-            for (int r = 0; r < RING; ++r) {
-                const int g = g0 + r;
-                const int it = grp * KG + g;
-                if (it + 1 < NIT) b_load(g + 1 == KG ? 0 : g + 1, b[(r + 1) & 1]);
-#pragma unroll
-                for (int sg = 0; sg < NSG; ++sg)
-#pragma unroll
-                    for (int j = 0; j < TP; ++j) mfma_group<BF16>(ring[r][j], b[r & 1][sg], acc[j][sg]);
-                if (it + RING < NIT) {
-                    const uint4 *src = a_src(it + RING);
-#pragma unroll
-                    for (int j = 0; j < TP; ++j) ring[r][j] = src[j * tstride];
-                }
-            }
-        }
-        done(t0 + grp * TP, acc);
+    };
+    zero();
+    const int n_rounds = n_groups * (KG / RING);
+    if (ONE_ROUND_COPY && n_rounds == 1) {
+        // a layer of one round gets a copy of its own, whose waits count the loads issued before
+        // the layer (after the merge with the loop below, the compiler would assume the fewest and
+        // wait for loads issued after the layer's own, such as the next layer's first fragments)
+        round(0, 0, std::false_type{});
+        done(t0, acc);
+        return;
     }
+    // all rounds but the last in one loop, the last one peeled off after it
+    int grp = 0, g0 = 0;
+    for (int rr = n_rounds - 1; rr > 0; --rr) {
+        round(grp, g0, std::true_type{});
+        g0 += RING;
+        if (g0 == KG) {
+            done(t0 + grp * TP, acc);
+            zero();
+            g0 = 0;
+            ++grp;
+        }
+    }
+    round(grp, g0, std::false_type{});
+    done(t0 + grp * TP, acc);
 }
 
-// U waves per workgroup, 16*NSG states; HTM >= head tiles; layers in groups of TP tiles per wave.
-template <bool BF16, int NSG, int HTM, int U, int TP, int RING>
+// U waves per workgroup, 16*NSG states; HTM >= head tiles; layers in groups of TP tiles per wave;
+// R1 (R2) k-groups of W1 (W2) fragments in flight per wave.
+template <bool BF16, int NSG, int HTM, int U, int TP, int R1, int R2>
 __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     extern __shared__ __align__(16) char smem[];
     constexpr int EL = BF16 ? 2 : 4;        // bytes per activation element
-    constexpr int UPG = BF16 ? 32 : 16;     // input units per k-group
+    constexpr int UB = 16 / EL;             // units per 16-byte unit block
+    constexpr int UPG = 4 * UB;             // input units per k-group
     constexpr int NTH = 64 * U;
     const int wid = threadIdx.x / 64, l = threadIdx.x % 64;
     const int ln = l % 16, lq = l / 16;
     const int s0 = blockIdx.x * 16 * NSG;
     constexpr int NS = 16 * NSG;
-    const int xs_stride = p.sp * EL + 16;   // bytes per state row (padded against bank conflicts)
-    const int h1_stride = p.h1p * EL + 16;
-    char *xs = smem;
-    char *h1 = smem + NS * xs_stride;
+    // LDS: the biases (b1, b2, heads), then the activations (states, h1), whose space the partial
+    // heads take over in phase 3
+    float *b1s = reinterpret_cast<float *>(smem);
+    float *b2s = b1s + p.h1p;
+    float *bhs = b2s + p.h2p;
+    char *acts = smem + (p.h1p + p.h2p + p.hap) * 4;
+    char *xs = acts;
+    char *h1 = acts + NS * p.sp * EL;
     const int HT = p.hap / 16;
-    // the first W1 fragments are loaded while the states are staged
-    const int mt1 = p.h1p / 16 / U, mt2 = p.h2p / 16 / U;
-    uint4 ring[RING][TP];
-    ring_fill<TP, RING>(ring, p.w1, wid * mt1, mt1, p.sp / UPG, l);
-
-    // ---------------- phase 0: states -> LDS [state][unit] (zero beyond S and B) ----------------
-    {
-        const int row_elems = p.sp;
-        for (int e = threadIdx.x; e < NS * row_elems; e += NTH) {
-            const int r = e / row_elems, c = e % row_elems;
-            const int st = s0 + r;
-            if constexpr (BF16) {
-                uint16_t v = 0;
-                if (st < p.B && c < p.S) v = static_cast<const uint16_t *>(p.states)[(int64_t)st * p.S + c];
-                *reinterpret_cast<uint16_t *>(xs + r * xs_stride + c * 2) = v;
-            } else {
-                float v = 0.f;
-                if (st < p.B && c < p.S) v = static_cast<const float *>(p.states)[(int64_t)st * p.S + c];
-                *reinterpret_cast<float *>(xs + r * xs_stride + c * 4) = v;
+    const int NT1 = p.h1p / 16, NT2 = p.h2p / 16;
+    const int mt1 = NT1 / U, mt2 = NT2 / U;
+    // The global loads the first tile groups need are issued up front, so that the kernel waits
+    // for memory about once: the states and biases (staged by phase 0; issued first, so that phase
+    // 0 waits for them alone), the first W1 fragments (register ring) and the first head fragments
+    // now, the first W2 fragments as soon as the states are staged (they stream during phase 1).
+    constexpr int PRE = 4;   // state elements per thread loaded up front (the rest: phase 0 loop)
+    constexpr int PREB = 2;  // bias float4s per thread loaded up front
+    using SE = typename std::conditional<BF16, uint16_t, float>::type;
+    const SE *states = static_cast<const SE *>(p.states);
+    const int n_st = NS * p.sp;
+    SE sv[PRE];
+#pragma unroll
+    for (int k = 0; k < PRE; ++k) {
+        const int e = threadIdx.x + k * NTH;
+        const int r = e % NS, c = e / NS;
+        const bool ok = e < n_st && s0 + r < p.B && c < p.S;
+        sv[k] = states[ok ? (int64_t)(s0 + r) * p.S + c : 0];
+    }
+    const int nb4 = (p.h1p + p.h2p + p.hap) / 4;
+    auto bias_src = [&](int e4) {
+        e4 = e4 < nb4 ? e4 : nb4 - 1;
+        const int q1 = p.h1p / 4, q2 = q1 + p.h2p / 4;
+        const float *src = e4 < q1 ? p.b1 + 4 * e4 : e4 < q2 ? p.b2 + 4 * (e4 - q1) : p.bh + 4 * (e4 - q2);
+        return *reinterpret_cast<const float4 *>(src);
+    };
+    float4 bv4[PREB];
+#pragma unroll
+    for (int k = 0; k < PREB; ++k) bv4[k] = bias_src(threadIdx.x + k * NTH);
+    uint4 ring1[R1][TP], ring2[R2][TP];
+    ring_fill<TP, R1>(ring1, p.w1, NT1, wid * mt1, l);
+    // head fragments: fp32 one k-group per h2 tile, bf16 one per pair of tiles
+    const int HKG = BF16 ? p.h2p / 32 : p.h2p / 16;
+    constexpr int HPG = BF16 ? TP / 2 : TP;  // head k-groups per group of TP tiles
+    uint4 hpf[HPG][HTM];
+    auto head_fetch = [&](int tile) {
+        const int hk0 = BF16 ? tile / 2 : tile;
+#pragma unroll
+        for (int q = 0; q < HPG; ++q)
+#pragma unroll
+            for (int ht = 0; ht < HTM; ++ht) {
+                const int hk = hk0 + q < HKG ? hk0 + q : HKG - 1, hs = ht < HT ? ht : HT - 1;
+                hpf[q][ht] = p.wh[((int64_t)hs * HKG + hk) * 64 + l];
             }
-        }
+    };
+    head_fetch(wid * mt2);
+
+    // ------ phase 0: biases -> LDS; states -> LDS unit blocks (zero beyond S and B), state fastest ------
+#pragma unroll
+    for (int k = 0; k < PREB; ++k) {
+        const int e4 = threadIdx.x + k * NTH;
+        if (e4 < nb4) reinterpret_cast<float4 *>(b1s)[e4] = bv4[k];
+    }
+    for (int e4 = threadIdx.x + PREB * NTH; e4 < nb4; e4 += NTH) reinterpret_cast<float4 *>(b1s)[e4] = bias_src(e4);
+    auto put_state = [&](int e, SE v) {
+        const int r = e % NS, c = e / NS;
+        *reinterpret_cast<SE *>(xs + ((c / UB) * NS + r) * 16 + (c % UB) * EL) = v;
+    };
+#pragma unroll
+    for (int k = 0; k < PRE; ++k) {
+        const int e = threadIdx.x + k * NTH;
+        const int r = e % NS, c = e / NS;
+        if (e < n_st) put_state(e, s0 + r < p.B && c < p.S ? sv[k] : SE(0));
+    }
+    for (int e = threadIdx.x + PRE * NTH; e < n_st; e += NTH) {
+        const int r = e % NS, c = e / NS;
+        put_state(e, s0 + r < p.B && c < p.S ? states[(int64_t)(s0 + r) * p.S + c] : SE(0));
     }
     __syncthreads();
+    ring_fill<TP, R2>(ring2, p.w2, NT2, wid * mt2, l);
 
     // ---------------- phase 1: h1 = act(W1 s + b1), this wave's share of the tiles ----------------
     {
         const int mt_per = mt1;
-        dense_layer<BF16, NSG, TP, RING>(ring, p.w1, wid * mt_per, mt_per, p.sp / UPG, xs, xs_stride, ln, lq, l,
+        dense_layer<BF16, NSG, TP, R1, true>(ring1, p.w1, NT1, wid * mt_per, mt_per, p.sp / UPG, xs, ln, lq, l,
                                          [&](int mt0, f32x4 (&acc)[TP][NSG]) {
 #pragma unroll
                                              for (int h = 0; h < TP; ++h) {
                                                  const int u0 = (mt0 + h) * 16 + lq * 4;
+                                                 const float4 bias = *reinterpret_cast<const float4 *>(b1s + u0);
+                                                 const float bv[4] = {bias.x, bias.y, bias.z, bias.w};
 #pragma unroll
                                                  for (int sg = 0; sg < NSG; ++sg) {
                                                      float v[4];
 #pragma unroll
-                                                     for (int i = 0; i < 4; ++i) v[i] = fmaxf(acc[h][sg][i] + p.b1[u0 + i], 0.f);
-                                                     char *dst = h1 + (sg * 16 + ln) * h1_stride + u0 * EL;
+                                                     for (int i = 0; i < 4; ++i) v[i] = fmaxf(acc[h][sg][i] + bv[i], 0.f);
+                                                     char *dst = h1 + ((u0 / UB) * NS + sg * 16 + ln) * 16 + (u0 % UB) * EL;
                                                      if constexpr (BF16) {
                                                          *reinterpret_cast<uint2 *>(dst) =
                                                              make_uint2(bf16_rne(v[0]) | (bf16_rne(v[1]) << 16),
@@ -222,8 +404,6 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                                              }
                                          });
     }
-    // the first W2 fragments are loaded before the barrier that publishes h1
-    ring_fill<TP, RING>(ring, p.w2, wid * mt2, mt2, p.h1p / UPG, l);
     __syncthreads();
 
     // ------- phase 2: h2 tile groups of this wave, chained into the partial heads (registers) -------
@@ -235,28 +415,14 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     {
         const int mt_per = mt2;
         const int mt_first = wid * mt_per;
-        // head fragments: fp32 one k-group per h2 tile, bf16 one per pair of tiles
-        const int HKG = BF16 ? p.h2p / 32 : p.h2p / 16;
-        constexpr int HPG = BF16 ? TP / 2 : TP;  // head k-groups per group of TP tiles
-        uint4 hpf[HPG][HTM];
-        auto head_fetch = [&](int tile) {
-            const int hk0 = BF16 ? tile / 2 : tile;
-#pragma unroll
-            for (int q = 0; q < HPG; ++q)
-#pragma unroll
-                for (int ht = 0; ht < HTM; ++ht) {
-                    const int hk = hk0 + q;
-                    if (ht < HT && hk < HKG) hpf[q][ht] = p.wh[((int64_t)ht * HKG + hk) * 64 + l];
-                }
-        };
-        head_fetch(mt_first);
-        dense_layer<BF16, NSG, TP, RING>(
-            ring, p.w2, mt_first, mt_per, p.h1p / UPG, h1, h1_stride, ln, lq, l, [&](int mt0, f32x4 (&acc)[TP][NSG]) {
+        dense_layer<BF16, NSG, TP, R2, false>(
+            ring2, p.w2, NT2, mt_first, mt_per, p.h1p / UPG, h1, ln, lq, l, [&](int mt0, f32x4 (&acc)[TP][NSG]) {
                 float bias[TP][4];
 #pragma unroll
-                for (int h = 0; h < TP; ++h)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) bias[h][i] = p.b2[(mt0 + h) * 16 + lq * 4 + i];
+                for (int h = 0; h < TP; ++h) {
+                    const float4 b = *reinterpret_cast<const float4 *>(b2s + (mt0 + h) * 16 + lq * 4);
+                    bias[h][0] = b.x; bias[h][1] = b.y; bias[h][2] = b.z; bias[h][3] = b.w;
+                }
 #pragma unroll
                 for (int sg = 0; sg < NSG; ++sg) {
                     float v[TP][4];
@@ -288,16 +454,21 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                         }
                     }
                 }
-                head_fetch(mt0 + TP);
+                if (mt0 + TP < mt_first + mt_per) head_fetch(mt0 + TP);
             });
     }
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
 
     // ---------------- phase 3: fixed-order sum of the U partial heads, epilogue ----------------
-    // Every thread sums some of the NSG*hap*16 head values over the U waves (in wave order, then
-    // the bias) into zs; the waves of the state groups then take argmax, softmax and the value.
-    float *part = reinterpret_cast<float *>(smem);  // [U][NSG][hap][16]
-    float *zs = part + (int64_t)U * NSG * p.hap * 16;  // [NSG][hap][16]
+    // The partial heads are stored in accumulator order ([U][NSG][head tile][register][lane], so
+    // every store and load is 64 consecutive floats); every thread sums some of the NSG*hap*16 head
+    // values over the U waves (in wave order, then the bias) into zr ([state][row], rows padded to
+    // hap + 1 against bank conflicts).  The waves then take whole states: argmax and the softmax
+    // sum are reductions over the lanes of a state.
+    float *part = reinterpret_cast<float *>(acts);
+    const int nz = NSG * p.hap * 16;
+    const int zst = p.hap + 1;
+    float *zr = part + (int64_t)U * nz;
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
@@ -305,79 +476,56 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
             if (ht < HT)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    part[(((int64_t)wid * NSG + sg) * p.hap + ht * 16 + lq * 4 + i) * 16 + ln] = hacc[sg][ht][i];
+                    part[(int64_t)wid * nz + ((sg * HT + ht) * 4 + i) * 64 + l] = hacc[sg][ht][i];
     __syncthreads();
-    {
-        const int nz = NSG * p.hap * 16;
-        for (int v = threadIdx.x; v < nz; v += NTH) {
-            const int row = (v / 16) % p.hap;
-            float s = 0.f;
+    for (int v = threadIdx.x; v < nz; v += NTH) {
+        const int sg = v / (HT * 256), ht = (v / 256) % HT, i = (v / 64) % 4, vl = v % 64;
+        const int row = ht * 16 + (vl / 16) * 4 + i;
+        float s = 0.f;
 #pragma unroll
-            for (int w = 0; w < U; ++w) s += part[(int64_t)w * nz + v];
-            zs[v] = s + p.bh[row];
-        }
+        for (int w = 0; w < U; ++w) s += part[(int64_t)w * nz + v];
+        zr[(sg * 16 + vl % 16) * zst + row] = s + bhs[row];
     }
     __syncthreads();
-    for (int sg = wid; sg < NSG; sg += U) {
-        const int st = s0 + sg * 16 + ln;
+    // Each pass of a wave takes 64 / W states, W = 16, 32 or 64 lanes per state (the head rows
+    // rounded up): lane l holds rows l % W (and l % W + 64 when a state has more than 64 rows).
+    constexpr int RC = (HTM * 16 + 63) / 64;  // row chunks of 64 per state
+    const int rw = p.hap <= 16 ? 16 : p.hap <= 32 ? 32 : 64;
+    const int spp = 64 / rw;
+    for (int sb = wid * spp; sb < NS; sb += U * spp) {
+        const int sl = sb + l / rw, lr = l % rw;
+        const int st = s0 + sl;
+        float z[RC];
         float best = -INFINITY;
         int best_i = 0x7FFFFFFF;
-        float val = 0.f;
-        float z[HTM][4];  // rows owned by this lane: 16*ht + 4*lq + i
 #pragma unroll
-        for (int ht = 0; ht < HTM; ++ht)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                z[ht][i] = 0.f;
-                if (ht >= HT) continue;
-                const int row = ht * 16 + lq * 4 + i;
-                const float s = zs[((int64_t)sg * p.hap + row) * 16 + ln];
-                z[ht][i] = s;
-                if (row < p.a && (s > best || (s == best && row < best_i))) {
-                    best = s;
-                    best_i = row;
-                }
-                if (row == p.a) val = s;
-            }
-        // combine over the 4 lanes of this state (xor 16, xor 32)
-#pragma unroll
-        for (int m = 16; m <= 32; m <<= 1) {
-            const float ob = __shfl_xor(best, m, 64);
-            const int oi = __shfl_xor(best_i, m, 64);
-            if (ob > best || (ob == best && oi < best_i)) {
-                best = ob;
-                best_i = oi;
-            }
-            val += __shfl_xor(val, m, 64);
+        for (int c = 0; c < RC; ++c) {
+            const int row = c * 64 + lr;
+            z[c] = row < p.hap ? zr[sl * zst + row] : 0.f;
+            if (row < p.a) argmax_step(best, best_i, z[c], row);
         }
+        group_argmax(best, best_i, rw);
         if (best_i == 0x7FFFFFFF) best_i = 0;  // only NaN logits: no maximum exists
-        float sum = 0.f;
+        float e[RC] = {}, sum = 0.f;
         if (p.probs) {
 #pragma unroll
-            for (int ht = 0; ht < HTM; ++ht)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = ht * 16 + lq * 4 + i;
-                    if (ht < HT && row < p.a) sum += expf(z[ht][i] - best);
-                }
-            sum += __shfl_xor(sum, 16, 64);
-            sum += __shfl_xor(sum, 32, 64);
+            for (int c = 0; c < RC; ++c) {
+                e[c] = c * 64 + lr < p.a ? expf(z[c] - best) : 0.f;
+                sum += e[c];
+            }
+            sum = group_sum(sum, rw);
         }
         if (st < p.B) {
 #pragma unroll
-            for (int ht = 0; ht < HTM; ++ht)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = ht * 16 + lq * 4 + i;
-                    if (ht < HT && row < p.a) {
-                        if (p.logits) p.logits[(int64_t)st * p.a + row] = z[ht][i];
-                        if (p.probs) p.probs[(int64_t)st * p.a + row] = expf(z[ht][i] - best) / sum;
-                    }
+            for (int c = 0; c < RC; ++c) {
+                const int row = c * 64 + lr;
+                if (row < p.a) {
+                    if (p.logits) p.logits[(int64_t)st * p.a + row] = z[c];
+                    if (p.probs) p.probs[(int64_t)st * p.a + row] = e[c] / sum;
                 }
-            if (lq == 0) {
-                p.action[st] = best_i;
-                p.value[st] = val;
+                if (row == p.a) p.value[st] = z[c];
             }
+            if (lr == 0) p.action[st] = best_i;
         }
     }
 }
@@ -386,28 +534,31 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
 // host: weight pre-tiling
 // ---------------------------------------------------------------------------------------------
 // Pack the A operand of a [rows x K] row-major weight (fp32 values or bf16 bits) into 16-byte
-// per-lane fragments, order [tile][g][lane]: lane l, slot j of k-group g of tile mt holds
-// W[16 mt + l%16][kmap(g, l/16, j)], zero outside the matrix.
+// per-lane fragments: lane l, slot j of k-group g of tile mt holds W[16 mt + l%16][kmap(g, l/16, j)],
+// zero outside the matrix.  Order [g][tile][lane] (k-group-major, the layer weights) or
+// [tile][g][lane] (the heads).
 template <typename KMap>
-std::vector<uint32_t> pack_frags(const void *W, bool bf, int rows, int K, int rows_p, int n_g, KMap kmap) {
+std::vector<uint32_t> pack_frags(const void *W, bool bf, int rows, int K, int rows_p, int n_g, bool g_major,
+                                 KMap kmap) {
     const int per = bf ? 8 : 4;
+    const int n_t = rows_p / 16;
     std::vector<uint32_t> out;
-    out.reserve((size_t)rows_p / 16 * n_g * 64 * 4);
-    for (int mt = 0; mt < rows_p / 16; ++mt)
-        for (int g = 0; g < n_g; ++g)
-            for (int l = 0; l < 64; ++l) {
-                uint32_t slot[8] = {};
-                for (int j = 0; j < per; ++j) {
-                    const int r = mt * 16 + l % 16, k = kmap(g, l / 16, j);
-                    if (r >= rows || k < 0 || k >= K) continue;
-                    if (bf) slot[j] = static_cast<const uint16_t *>(W)[(int64_t)r * K + k];
-                    else std::memcpy(&slot[j], static_cast<const float *>(W) + (int64_t)r * K + k, 4);
-                }
-                if (bf)
-                    for (int w = 0; w < 4; ++w) out.push_back(slot[2 * w] | (slot[2 * w + 1] << 16));
-                else
-                    for (int w = 0; w < 4; ++w) out.push_back(slot[w]);
+    out.reserve((size_t)n_t * n_g * 64 * 4);
+    for (int o = 0; o < n_t * n_g; ++o)
+        for (int l = 0; l < 64; ++l) {
+            const int mt = g_major ? o % n_t : o / n_g, g = g_major ? o / n_t : o % n_g;
+            uint32_t slot[8] = {};
+            for (int j = 0; j < per; ++j) {
+                const int r = mt * 16 + l % 16, k = kmap(g, l / 16, j);
+                if (r >= rows || k < 0 || k >= K) continue;
+                if (bf) slot[j] = static_cast<const uint16_t *>(W)[(int64_t)r * K + k];
+                else std::memcpy(&slot[j], static_cast<const float *>(W) + (int64_t)r * K + k, 4);
             }
+            if (bf)
+                for (int w = 0; w < 4; ++w) out.push_back(slot[2 * w] | (slot[2 * w + 1] << 16));
+            else
+                for (int w = 0; w < 4; ++w) out.push_back(slot[w]);
+        }
     return out;
 }
 
@@ -422,9 +573,10 @@ size_t policy_lds_bytes(const harl_policy *P, int nsg, int u) {
     const bool bf = P->dtype == HARL_BF16;
     const size_t el = bf ? 2 : 4;
     const size_t ns = 16 * (size_t)nsg;
-    const size_t acts = ns * (P->sp * el + 16) + ns * (P->h1p * el + 16);
-    const size_t part = (size_t)(u + 1) * nsg * P->hap * 16 * 4;  // partial heads and their sums
-    return acts > part ? acts : part;
+    const size_t acts = ns * P->sp * el + ns * P->h1p * el;
+    const size_t part = ((size_t)u * nsg * P->hap * 16 + ns * (P->hap + 1)) * 4;  // partial heads, their sums
+    const size_t bias = ((size_t)P->h1p + P->h2p + P->hap) * 4;
+    return bias + (acts > part ? acts : part);
 }
 
 }  // namespace
@@ -449,19 +601,19 @@ int pack_policy(const harl_policy_desc *d, harl_policy **out, hipStream_t stream
     std::vector<uint32_t> w1, w2, whp;
     if (bf) {
         auto kstd = [](int g, int q, int j) { return g * 32 + q * 8 + j; };
-        w1 = pack_frags(d->w1, true, d->h1, d->s, h1p, sp / 32, kstd);
-        w2 = pack_frags(d->w2, true, d->h2, d->h1, h2p, h1p / 32, kstd);
+        w1 = pack_frags(d->w1, true, d->h1, d->s, h1p, sp / 32, true, kstd);
+        w2 = pack_frags(d->w2, true, d->h2, d->h1, h2p, h1p / 32, true, kstd);
         // head k-group p consumes h2 tiles 2p (slots 0..3) and 2p+1 (slots 4..7), each from the
         // accumulator layout: unit 16 t + 4 q + i
         auto khead = [](int pr, int q, int j) { return pr * 32 + (j / 4) * 16 + q * 4 + (j % 4); };
-        whp = pack_frags(wh.data(), true, d->a + 1, d->h2, hap, h2p / 32, khead);
+        whp = pack_frags(wh.data(), true, d->a + 1, d->h2, hap, h2p / 32, false, khead);
     } else {
         auto kstd = [](int g, int q, int j) { return g * 16 + q * 4 + j; };
-        w1 = pack_frags(d->w1, false, d->h1, d->s, h1p, sp / 16, kstd);
-        w2 = pack_frags(d->w2, false, d->h2, d->h1, h2p, h1p / 16, kstd);
+        w1 = pack_frags(d->w1, false, d->h1, d->s, h1p, sp / 16, true, kstd);
+        w2 = pack_frags(d->w2, false, d->h2, d->h1, h2p, h1p / 16, true, kstd);
         // head k-group t consumes h2 tile t from the accumulator layout (unit 16 t + 4 q + j): the
         // same map as the standard one
-        whp = pack_frags(wh.data(), false, d->a + 1, d->h2, hap, h2p / 16, kstd);
+        whp = pack_frags(wh.data(), false, d->a + 1, d->h2, hap, h2p / 16, false, kstd);
     }
     std::vector<float> b1(h1p, 0.f), b2(h2p, 0.f), bh(hap, 0.f);
     std::memcpy(b1.data(), d->b1, (size_t)d->h1 * 4);
@@ -532,13 +684,15 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     const int ht = P->hap / 16;
     const int htm = ht <= 2 ? 2 : ht <= 5 ? 5 : 8;
     const void *kern = nullptr;
-#define HARL_POL(BF, NSG, HTM, U, TP)                  \
+    // R2 = 8 k-groups of W2 in flight, 4 for the 64-state bf16 shapes (TP = 4 tiles per group
+    // already hold 4 x 4 fragments per k-group, and more would spill)
+#define HARL_POL(BF, NSG, HTM, U, TP, R2)              \
     if (bf == BF && nsg == NSG && htm == HTM && u == U) \
-        kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM, U, TP, kRing>);
-    HARL_POL(false, 1, 2, 8, 2) HARL_POL(false, 1, 5, 8, 2) HARL_POL(false, 1, 8, 8, 2)
-    HARL_POL(false, 2, 2, 8, 2) HARL_POL(false, 2, 5, 8, 2) HARL_POL(false, 2, 8, 8, 2)
-    HARL_POL(true, 1, 2, 8, 2) HARL_POL(true, 1, 5, 8, 2) HARL_POL(true, 1, 8, 8, 2)
-    HARL_POL(true, 4, 2, 4, 4) HARL_POL(true, 4, 5, 4, 4) HARL_POL(true, 4, 8, 4, 4)
+        kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM, U, TP, kRing, R2>);
+    HARL_POL(false, 1, 2, 8, 2, 8) HARL_POL(false, 1, 5, 8, 2, 8) HARL_POL(false, 1, 8, 8, 2, 8)
+    HARL_POL(false, 2, 2, 8, 2, 8) HARL_POL(false, 2, 5, 8, 2, 8) HARL_POL(false, 2, 8, 8, 2, 8)
+    HARL_POL(true, 1, 2, 8, 2, 8) HARL_POL(true, 1, 5, 8, 2, 8) HARL_POL(true, 1, 8, 8, 2, 8)
+    HARL_POL(true, 4, 2, 4, 4, 4) HARL_POL(true, 4, 5, 4, 4, 4) HARL_POL(true, 4, 8, 4, 4, 4)
 #undef HARL_POL
     if (!kern) return fail(HARL_E_UNSUPPORTED, "harl_policy_step: no kernel for this policy shape");
     if (const int rc = ensure_dynamic_lds(kern, lds)) return rc;
