@@ -7,9 +7,9 @@
 // N dimension (H^T = W X^T).  A workgroup holds 16*NSG states and U waves; a wave computes its
 // share of each layer's 16-unit tiles in groups of TP tiles.
 //   start    every wave issues the global loads its first tile groups need up front (states,
-//            biases, the first W1 fragments into a register ring, the first head fragments; the
-//            first W2 fragments into a second ring right after phase 0), so that the kernel waits
-//            on memory latency about once rather than once per phase;
+//            biases, the first W1 fragments into a register ring; the first W2 fragments into a
+//            second ring right after phase 0), so that the kernel waits on memory latency about
+//            once rather than once per phase;
 //   phase 0  the biases and the states are staged into LDS (activation layout below);
 //   phase 1  each wave computes its 1/U of h1's tiles for all states, TP tiles at a time (A =
 //            W1 fragments streamed from global memory through the register ring, B = states
@@ -226,6 +226,8 @@ __device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4
         for (int r = 0; r < RING; ++r) {
             const int g = g0 + r;
             if (REFILL || r + 1 < RING) b_load(g + 1 == KG ? 0 : g + 1, b[(r + 1) & 1]);
+            // the next k-group's B read stays ahead of this k-group's MFMAs (the double buffer)
+            __builtin_amdgcn_sched_barrier(0);
             if constexpr (BF16) {
 #pragma unroll
                 for (int sg = 0; sg < NSG; ++sg)
@@ -310,8 +312,9 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     const int mt1 = NT1 / U, mt2 = NT2 / U;
     // The global loads the first tile groups need are issued up front, so that the kernel waits
     // for memory about once: the states and biases (staged by phase 0; issued first, so that phase
-    // 0 waits for them alone), the first W1 fragments (register ring) and the first head fragments
-    // now, the first W2 fragments as soon as the states are staged (they stream during phase 1).
+    // 0 waits for them alone) and the first W1 fragments (register ring) now, the first W2
+    // fragments as soon as the states are staged (they stream during phase 1), the first head
+    // fragments when phase 2 starts (they are needed when its first tile group ends).
     constexpr int PRE = 4;   // state elements per thread loaded up front (the rest: phase 0 loop)
     constexpr int PREB = 2;  // bias float4s per thread loaded up front
     using SE = typename std::conditional<BF16, uint16_t, float>::type;
@@ -351,7 +354,6 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                 hpf[q][ht] = p.wh[((int64_t)hs * HKG + hk) * 64 + l];
             }
     };
-    head_fetch(wid * mt2);
 
     // ------ phase 0: biases -> LDS; states -> LDS unit blocks (zero beyond S and B), state fastest ------
 #pragma unroll
@@ -415,6 +417,7 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     {
         const int mt_per = mt2;
         const int mt_first = wid * mt_per;
+        head_fetch(mt_first);
         dense_layer<BF16, NSG, TP, R2, false>(
             ring2, p.w2, NT2, mt_first, mt_per, p.h1p / UPG, h1, ln, lq, l, [&](int mt0, f32x4 (&acc)[TP][NSG]) {
                 float bias[TP][4];
@@ -684,13 +687,14 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     const int ht = P->hap / 16;
     const int htm = ht <= 2 ? 2 : ht <= 5 ? 5 : 8;
     const void *kern = nullptr;
-    // R2 = 8 k-groups of W2 in flight, 4 for the 64-state bf16 shapes (TP = 4 tiles per group
-    // already hold 4 x 4 fragments per k-group, and more would spill)
+    // R2 = 8 k-groups of W2 in flight; 4 for the 64-state bf16 shapes (TP = 4 tiles per group
+    // already hold 4 x 4 fragments per k-group) and for 32-state fp32 with 8 head tiles, where
+    // more would spill
 #define HARL_POL(BF, NSG, HTM, U, TP, R2)              \
     if (bf == BF && nsg == NSG && htm == HTM && u == U) \
         kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM, U, TP, kRing, R2>);
     HARL_POL(false, 1, 2, 8, 2, 8) HARL_POL(false, 1, 5, 8, 2, 8) HARL_POL(false, 1, 8, 8, 2, 8)
-    HARL_POL(false, 2, 2, 8, 2, 8) HARL_POL(false, 2, 5, 8, 2, 8) HARL_POL(false, 2, 8, 8, 2, 8)
+    HARL_POL(false, 2, 2, 8, 2, 8) HARL_POL(false, 2, 5, 8, 2, 8) HARL_POL(false, 2, 8, 8, 2, 4)
     HARL_POL(true, 1, 2, 8, 2, 8) HARL_POL(true, 1, 5, 8, 2, 8) HARL_POL(true, 1, 8, 8, 2, 8)
     HARL_POL(true, 4, 2, 4, 4, 4) HARL_POL(true, 4, 5, 4, 4, 4) HARL_POL(true, 4, 8, 4, 4, 4)
 #undef HARL_POL
