@@ -197,6 +197,13 @@ __device__ __forceinline__ int tile_lds_index(int i) {
     const int part = i % kTileU4;
     return (part / 16) * (int)(kGroupStride / 16) + (i / kTileU4) * 16 + part % 16;
 }
+// A code tile is read once per tree group and not again soon: a streaming (non-temporal) load, so
+// that the code stream does not push the ensemble's node records out of the L2.
+typedef unsigned u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
+    const u32x4_nt v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 template <int NT, int NPX>
 __device__ __forceinline__ void tile_fetch(uint4 (&xf)[NPX], const uint4 *__restrict__ codes, int64_t ldw4, int F,
                                            int tile) {
@@ -206,7 +213,7 @@ __device__ __forceinline__ void tile_fetch(uint4 (&xf)[NPX], const uint4 *__rest
     // every element is assigned (a guarded assignment would leave xf to the stack)
 #pragma unroll
     for (int j = 0; j < NPX; ++j) {
-        xf[j] = (int)threadIdx.x + j * NT < total ? *p : make_uint4(0, 0, 0, 0);
+        xf[j] = (int)threadIdx.x + j * NT < total ? load_stream(p) : make_uint4(0, 0, 0, 0);
         p += step;
     }
 }
@@ -228,7 +235,7 @@ __device__ __forceinline__ void tile_stage(uint4 *tile_lds, const uint4 *__restr
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int i = i0 + j * NT;
-            v[j] = i < total ? codes[(int64_t)(i / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + (i % kTileU4)]
+            v[j] = i < total ? load_stream(codes + (int64_t)(i / kTileU4) * ldw4 + (int64_t)tile * kTileU4 + (i % kTileU4))
                              : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
