@@ -41,6 +41,9 @@ PEAK_GVISITS = N_CU * CLOCK_GHZ * VALU_LANES_PER_CLK / VALU_PER_VISIT  # G visit
 # and by the SHA-256 of the scoring sources (score.hip, score_bin.hip, walk_b16.hpp) the counters were
 # taken with: any other source reports null.
 SCORE_TRAFFIC_BYTES = {
+    # streamed batch 0 (2,124,965 rows): k_bin16 1,382,698 + 680,682 KiB, k_tree_score_b16<12,6>
+    # 2,792,173 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
+    ("streamed", "dec2f7c0089b1b51bd95ab0f8988d687ca6e6e0bf6400acf5f207145954f2c99"): 5007653990,
 }
 
 
@@ -793,7 +796,8 @@ def round_bench(args):
     pol_tflops = n_prog * flops_per_state / (pol_mean_us * 1e-6) / 1e12
     ms_per_step = el * 1e3 / args.steps
     hbm_gbs = alg_bytes / (score_mean_us * 1e-6) / 1e9
-    roof = {"bound": "alu", "kernel": "k_tree_score (+k_segsum) via harl_score_round",
+    kern = ("k_bin16 + k_tree_score_b16 + k_segsum" if 9 <= cfg.depth <= 10 else "k_tree_score + k_segsum")
+    roof = {"bound": "alu", "kernel": kern + " via harl_score_round",
             "achieved": gvisits, "peak": PEAK_GVISITS, "unit": "Gvisit/s", "frac": gvisits / PEAK_GVISITS,
             "traffic": score_traffic(cfg.name), "traffic_unit": "HBM bytes per launch",
             "algorithmic_units_per_launch": visits, "us_per_launch": score_mean_us,
