@@ -687,14 +687,15 @@ int policy_step_launch(const harl_policy *P, const void *states, int32_t B, int3
     const int ht = P->hap / 16;
     const int htm = ht <= 2 ? 2 : ht <= 5 ? 5 : 8;
     const void *kern = nullptr;
-    // R2 = 8 k-groups of W2 in flight; 4 for the 64-state bf16 shapes (TP = 4 tiles per group
-    // already hold 4 x 4 fragments per k-group) and for 32-state fp32 with 8 head tiles, where
-    // more would spill
+    // R2 = 8 k-groups of W2 in flight for 16-state workgroups (one per CU on small batches, where
+    // each workgroup's memory waits are the kernel's); 4 for the 32- and 64-state shapes of large
+    // batches, whose workgroups follow each other on a CU (8 measured 3 % slower at 65,536 fp32
+    // states, and more registers spill at 8 head tiles)
 #define HARL_POL(BF, NSG, HTM, U, TP, R2)              \
     if (bf == BF && nsg == NSG && htm == HTM && u == U) \
         kern = reinterpret_cast<const void *>(k_policy<BF, NSG, HTM, U, TP, kRing, R2>);
     HARL_POL(false, 1, 2, 8, 2, 8) HARL_POL(false, 1, 5, 8, 2, 8) HARL_POL(false, 1, 8, 8, 2, 8)
-    HARL_POL(false, 2, 2, 8, 2, 8) HARL_POL(false, 2, 5, 8, 2, 8) HARL_POL(false, 2, 8, 8, 2, 4)
+    HARL_POL(false, 2, 2, 8, 2, 4) HARL_POL(false, 2, 5, 8, 2, 4) HARL_POL(false, 2, 8, 8, 2, 4)
     HARL_POL(true, 1, 2, 8, 2, 8) HARL_POL(true, 1, 5, 8, 2, 8) HARL_POL(true, 1, 8, 8, 2, 8)
     HARL_POL(true, 4, 2, 4, 4, 4) HARL_POL(true, 4, 5, 4, 4, 4) HARL_POL(true, 4, 8, 4, 4, 4)
 #undef HARL_POL
