@@ -8,8 +8,8 @@
 // share of each layer's 16-unit tiles in groups of TP tiles.
 //   start    every wave issues the global loads its first tile groups need up front (states,
 //            biases, the first W1 fragments into a register ring; the first W2 fragments into a
-//            second ring right after phase 0), so that the kernel waits on memory latency about
-//            once rather than once per phase;
+//            second ring during phase 1, behind its MFMAs), so that the kernel waits on memory
+//            latency about once rather than once per phase;
 //   phase 0  the biases and the states are staged into LDS (activation layout below);
 //   phase 1  each wave computes its 1/U of h1's tiles for all states, TP tiles at a time (A =
 //            W1 fragments streamed from global memory through the register ring, B = states
@@ -197,10 +197,15 @@ __device__ __forceinline__ void ring_fill(uint4 (&ring)[RING][TP], const uint4 *
 // iteration it + RING are loaded from `A` (packed [g][tile][lane] x 16 B, NT tiles per k-group)
 // into ring slot it % RING as soon as iteration it has issued its MFMAs; the B fragments of the
 // next k-group are read from the LDS activation blocks `in` into the other half of a double
-// buffer.  done(first_tile, acc[TP][NSG]) consumes each finished group.
-template <bool BF16, int NSG, int TP, int RING, bool ONE_ROUND_COPY, typename Done>
+// buffer.  done(first_tile, acc[TP][NSG]) consumes each finished group.  side(r) issues part r
+// (r < RING) of loads meant for later work: a layer of one round issues part r right behind the
+// MFMAs of its iteration r, so that the loads drain through the memory pipeline while the MFMAs run
+// (issued all at once, they held the waves' instruction issue back for about 0.8 us); any other
+// layer issues all parts before its first round.
+template <bool BF16, int NSG, int TP, int RING, bool ONE_ROUND_COPY, typename Done, typename Side>
 __device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4 *__restrict__ A, int NT, int t0,
-                                            int n_tiles, int KG, const char *in, int ln, int lq, int l, Done done) {
+                                            int n_tiles, int KG, const char *in, int ln, int lq, int l, Done done,
+                                            Side side) {
     static_assert(RING % 2 == 0, "the B double buffer alternates with the ring slot");
     constexpr int NS = 16 * NSG;
     const int n_groups = n_tiles / TP;
@@ -218,8 +223,9 @@ __device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4
     // fragments one k-group ahead; the last round issues neither, so that no load is left in
     // flight when the layer ends.  The two cases are separate copies of the round, so that every
     // load in either is unconditional and the compiler knows exactly which one each use waits for.
-    auto round = [&](int grp, int g0, auto refill_tag) {
+    auto round = [&](int grp, int g0, auto refill_tag, auto side_tag) {
         constexpr bool REFILL = decltype(refill_tag)::value;
+        constexpr bool SIDE = decltype(side_tag)::value;
         const bool wrap = g0 + RING >= KG;
         const uint4 *rsrc = A + ((int64_t)(wrap ? 0 : g0 + RING) * NT + t0 + TP * (grp + wrap)) * 64 + l;
 #pragma unroll
@@ -249,6 +255,7 @@ __device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4
 #pragma unroll
                 for (int j = 0; j < TP; ++j) ring[r][j] = src[j * 64];
             }
+            if constexpr (SIDE) side(r);
             // keep each refill right behind the MFMAs of its slot (left alone, the scheduler sinks
             // all refills of a round to its end, and the next round then waits on them at once)
             __builtin_amdgcn_sched_barrier(0);
@@ -266,14 +273,16 @@ __device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4
         // a layer of one round gets a copy of its own, whose waits count the loads issued before
         // the layer (after the merge with the loop below, the compiler would assume the fewest and
         // wait for loads issued after the layer's own, such as the next layer's first fragments)
-        round(0, 0, std::false_type{});
+        round(0, 0, std::false_type{}, std::true_type{});
         done(t0, acc);
         return;
     }
+#pragma unroll
+    for (int r = 0; r < RING; ++r) side(r);
     // all rounds but the last in one loop, the last one peeled off after it
     int grp = 0, g0 = 0;
     for (int rr = n_rounds - 1; rr > 0; --rr) {
-        round(grp, g0, std::true_type{});
+        round(grp, g0, std::true_type{}, std::false_type{});
         g0 += RING;
         if (g0 == KG) {
             done(t0 + grp * TP, acc);
@@ -282,7 +291,7 @@ __device__ __forceinline__ void dense_layer(uint4 (&ring)[RING][TP], const uint4
             ++grp;
         }
     }
-    round(grp, g0, std::false_type{});
+    round(grp, g0, std::false_type{}, std::false_type{});
     done(t0 + grp * TP, acc);
 }
 
@@ -313,8 +322,8 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     // The global loads the first tile groups need are issued up front, so that the kernel waits
     // for memory about once: the states and biases (staged by phase 0; issued first, so that phase
     // 0 waits for them alone) and the first W1 fragments (register ring) now, the first W2
-    // fragments as soon as the states are staged (they stream during phase 1), the first head
-    // fragments when phase 2 starts (they are needed when its first tile group ends).
+    // fragments during phase 1 (see dense_layer's side loads), the first head fragments when phase
+    // 2 starts (they are needed when its first tile group ends).
     constexpr int PRE = 4;   // state elements per thread loaded up front (the rest: phase 0 loop)
     constexpr int PREB = 2;  // bias float4s per thread loaded up front
     using SE = typename std::conditional<BF16, uint16_t, float>::type;
@@ -377,7 +386,6 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
         put_state(e, s0 + r < p.B && c < p.S ? states[(int64_t)(s0 + r) * p.S + c] : SE(0));
     }
     __syncthreads();
-    ring_fill<TP, R2>(ring2, p.w2, NT2, wid * mt2, l);
 
     // ---------------- phase 1: h1 = act(W1 s + b1), this wave's share of the tiles ----------------
     {
@@ -403,6 +411,17 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                                                          *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
                                                      }
                                                  }
+                                             }
+                                         },
+                                         // the first W2 fragments, issued during layer 1
+                                         [&](int r) {
+                                             static_assert(R2 % R1 == 0, "W2 ring slots per layer-1 iteration");
+#pragma unroll
+                                             for (int q = 0; q < R2 / R1; ++q) {
+                                                 const int slot = r * (R2 / R1) + q;
+                                                 const uint4 *src = p.w2 + ((int64_t)slot * NT2 + wid * mt2) * 64 + l;
+#pragma unroll
+                                                 for (int j = 0; j < TP; ++j) ring2[slot][j] = src[j * 64];
                                              }
                                          });
     }
@@ -458,7 +477,8 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
                     }
                 }
                 if (mt0 + TP < mt_first + mt_per) head_fetch(mt0 + TP);
-            });
+            },
+            [](int) {});
     }
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
 
