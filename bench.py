@@ -43,7 +43,7 @@ PEAK_GVISITS = N_CU * CLOCK_GHZ * VALU_LANES_PER_CLK / VALU_PER_VISIT  # G visit
 SCORE_TRAFFIC_BYTES = {
     # streamed batch 0 (2,124,965 rows): k_bin16 1,382,698 + 680,682 KiB, k_tree_score_b16<12,6>
     # 2,792,173 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
-    ("streamed", "dec2f7c0089b1b51bd95ab0f8988d687ca6e6e0bf6400acf5f207145954f2c99"): 5007653990,
+    ("streamed", "b6d9dffda451f214387d2b6b66d086fa7f9b84c0a2ea60952297f7c64c921a11"): 5007653990,
 }
 
 

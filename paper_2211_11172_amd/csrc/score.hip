@@ -18,7 +18,10 @@
 //   k_tree_score_ch (deeper trees, whose 2^depth-node trees are too big for per-wave slots): the
 //     workgroup stages chunks of TW*ILP trees shared by all waves, the next chunk fetched into
 //     registers during the walk of the current one.
-// K2 k_segsum: one wave per program sums its rows' partial slots in a fixed order (fp64).
+// K2 k_segsum: a workgroup owns consecutive programs; every thread forms its rows' sums from their
+//     slice partials, and one thread per program adds its rows in row order (fp64, fixed order).
+// Ensembles of 9 or 10 split levels (at most 256 features, 65,534 distinct thresholds per feature)
+// are scored on 16-bit bin codes instead (score_bin.hip); K2 then sums that path's partials.
 //
 // Grid mapping is XCD-aware: workgroup b takes tree group b % G and row tile b / G; workgroups
 // are dealt to the 8 XCDs round-robin, so with G in {2,4,8} every XCD's L2 only ever holds its
