@@ -19,8 +19,8 @@
 //            fragment feeds NSG state groups) and feeds each finished tile straight from its
 //            accumulator registers into the head contraction: the MFMA result layout of a tile is
 //            re-used as the B operand layout, with the head weights pre-permuted to match;
-//   phase 3  the U per-wave partial heads are summed in a fixed order; bias, argmax, softmax
-//            and value are computed per state (one wave per state at a time) and written out.
+//   phase 3  each wave takes whole states: the U per-wave partial heads of a state are summed in
+//            a fixed order with the bias, and argmax, softmax and value computed and written out.
 // fp32 policies use v_mfma_f32_16x16x4_f32, bf16 policies v_mfma_f32_16x16x32_bf16 (fp32
 // accumulation; h1, h2 rounded to bf16, nearest even).  Weights are pre-tiled at create time so
 // that a lane's operand for one "k-group" is 16 contiguous bytes:
@@ -483,15 +483,14 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
 
     // ---------------- phase 3: fixed-order sum of the U partial heads, epilogue ----------------
-    // The partial heads are stored in accumulator order ([U][NSG][head tile][register][lane], so
-    // every store and load is 64 consecutive floats); every thread sums some of the NSG*hap*16 head
-    // values over the U waves (in wave order, then the bias) into zr ([state][row], rows padded to
-    // hap + 1 against bank conflicts).  The waves then take whole states: argmax and the softmax
-    // sum are reductions over the lanes of a state.
+    // The partial heads are stored [U][state][row], rows padded to hap + 1 floats against bank
+    // conflicts.  The waves then take whole states: each pass of a wave takes 64 / W states, W =
+    // 16, 32 or 64 lanes per state (the head rows rounded up); lane l sums row l % W (and l % W + 64
+    // when a state has more than 64 rows) over the U waves in wave order, adds the bias, and argmax
+    // and the softmax sum are reductions over the lanes of a state.
     float *part = reinterpret_cast<float *>(acts);
-    const int nz = NSG * p.hap * 16;
-    const int zst = p.hap + 1;
-    float *zr = part + (int64_t)U * nz;
+    const int rs = p.hap + 1;
+    const int nz = NS * rs;
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
@@ -499,19 +498,8 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
             if (ht < HT)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    part[(int64_t)wid * nz + ((sg * HT + ht) * 4 + i) * 64 + l] = hacc[sg][ht][i];
+                    part[(int64_t)wid * nz + (sg * 16 + ln) * rs + ht * 16 + lq * 4 + i] = hacc[sg][ht][i];
     __syncthreads();
-    for (int v = threadIdx.x; v < nz; v += NTH) {
-        const int sg = v / (HT * 256), ht = (v / 256) % HT, i = (v / 64) % 4, vl = v % 64;
-        const int row = ht * 16 + (vl / 16) * 4 + i;
-        float s = 0.f;
-#pragma unroll
-        for (int w = 0; w < U; ++w) s += part[(int64_t)w * nz + v];
-        zr[(sg * 16 + vl % 16) * zst + row] = s + bhs[row];
-    }
-    __syncthreads();
-    // Each pass of a wave takes 64 / W states, W = 16, 32 or 64 lanes per state (the head rows
-    // rounded up): lane l holds rows l % W (and l % W + 64 when a state has more than 64 rows).
     constexpr int RC = (HTM * 16 + 63) / 64;  // row chunks of 64 per state
     const int rw = p.hap <= 16 ? 16 : p.hap <= 32 ? 32 : 64;
     const int spp = 64 / rw;
@@ -524,7 +512,14 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
 #pragma unroll
         for (int c = 0; c < RC; ++c) {
             const int row = c * 64 + lr;
-            z[c] = row < p.hap ? zr[sl * zst + row] : 0.f;
+            z[c] = 0.f;
+            if (row < p.hap) {
+                const int v = sl * rs + row;
+                float s = 0.f;
+#pragma unroll
+                for (int w = 0; w < U; ++w) s += part[(int64_t)w * nz + v];
+                z[c] = s + bhs[row];
+            }
             if (row < p.a) argmax_step(best, best_i, z[c], row);
         }
         group_argmax(best, best_i, rw);
@@ -597,7 +592,7 @@ size_t policy_lds_bytes(const harl_policy *P, int nsg, int u) {
     const size_t el = bf ? 2 : 4;
     const size_t ns = 16 * (size_t)nsg;
     const size_t acts = ns * P->sp * el + ns * P->h1p * el;
-    const size_t part = ((size_t)u * nsg * P->hap * 16 + ns * (P->hap + 1)) * 4;  // partial heads, their sums
+    const size_t part = (size_t)u * ns * (P->hap + 1) * 4;  // partial heads
     const size_t bias = ((size_t)P->h1p + P->h2p + P->hap) * 4;
     return bias + (acts > part ? acts : part);
 }
