@@ -107,3 +107,18 @@ def test_large_fp32_batch(exact):
 def test_large_batch_policy_heavy_values():
     # the policy-heavy network with its own (non-integer) weights and states
     _check(get_config("policy_heavy"), B=_LARGE + 129)
+
+
+@pytest.mark.parametrize("dtype,a,B", [
+    ("f32", 6, 333),              # 16 head rows: four states per wave pass
+    ("f32", 40, 333),             # 48 rows, five head tiles: one state per pass, a second 64-row chunk
+    ("f32", 63, 333),             # 64 rows: the value in the last row of the first chunk
+    ("bf16", 40, 200),            # the same on the bf16 general kernel
+    ("f32", 60, _LARGE + 45),     # 32-state workgroups with five head tiles
+    ("f32", 10, _LARGE + 45),     # 32-state workgroups, four states per pass
+])
+def test_epilogue_widths(dtype, a, B):
+    # the general kernel's epilogue takes 64 / W states per wave pass, W = 16, 32 or 64 lanes per
+    # state: every width, with one and two row chunks, on 16- and 32-state workgroups
+    for exact in (True, False):
+        _check(mini_config(pol_dtype=dtype, pol_s=64, pol_h1=256, pol_h2=200, pol_a=a, exact=exact), B=B)
