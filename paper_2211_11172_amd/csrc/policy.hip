@@ -483,22 +483,22 @@ __global__ __launch_bounds__(64 * U) void k_policy(PolicyArgs p) {
     __syncthreads();  // h1 no longer needed: its LDS takes the partial heads
 
     // ---------------- phase 3: fixed-order sum of the U partial heads, epilogue ----------------
-    // The partial heads are stored [U][state][row], rows padded to hap + 1 floats against bank
-    // conflicts.  The waves then take whole states: each pass of a wave takes 64 / W states, W =
+    // The partial heads are stored [U][state][row], rows padded to hap + 4 floats: a lane writes
+    // its 4 rows of a head tile as one 16-byte store, and the 16 lanes of a store cycle (16
+    // states, stride (hap + 4) / 4 an odd number of 16-byte units) hit disjoint banks.  The waves then take whole states: each pass of a wave takes 64 / W states, W =
     // 16, 32 or 64 lanes per state (the head rows rounded up); lane l sums row l % W (and l % W + 64
     // when a state has more than 64 rows) over the U waves in wave order, adds the bias, and argmax
     // and the softmax sum are reductions over the lanes of a state.
     float *part = reinterpret_cast<float *>(acts);
-    const int rs = p.hap + 1;
+    const int rs = p.hap + 4;
     const int nz = NS * rs;
 #pragma unroll
     for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
         for (int ht = 0; ht < HTM; ++ht)
             if (ht < HT)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    part[(int64_t)wid * nz + (sg * 16 + ln) * rs + ht * 16 + lq * 4 + i] = hacc[sg][ht][i];
+                *reinterpret_cast<float4 *>(part + (int64_t)wid * nz + (sg * 16 + ln) * rs + ht * 16 + lq * 4) =
+                    make_float4(hacc[sg][ht][0], hacc[sg][ht][1], hacc[sg][ht][2], hacc[sg][ht][3]);
     __syncthreads();
     constexpr int RC = (HTM * 16 + 63) / 64;  // row chunks of 64 per state
     const int rw = p.hap <= 16 ? 16 : p.hap <= 32 ? 32 : 64;
@@ -592,7 +592,7 @@ size_t policy_lds_bytes(const harl_policy *P, int nsg, int u) {
     const size_t el = bf ? 2 : 4;
     const size_t ns = 16 * (size_t)nsg;
     const size_t acts = ns * P->sp * el + ns * P->h1p * el;
-    const size_t part = (size_t)u * ns * (P->hap + 1) * 4;  // partial heads
+    const size_t part = (size_t)u * ns * (P->hap + 4) * 4;  // partial heads
     const size_t bias = ((size_t)P->h1p + P->h2p + P->hap) * 4;
     return bias + (acts > part ? acts : part);
 }
