@@ -283,6 +283,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     // the dynamic LDS starts at address 0 (the kernel has no static LDS), so the code addresses
     // carry the row bits alone outside byte 1
     const uint32_t tb = lds_addr(smem) + slot_off;
+    const SlotConsts sk = slot_consts(tb, D);
     uint32_t xa[kRPL];
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
@@ -321,36 +322,40 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
         if (t + TW < t1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(t + TW) * S16, S16, lane);
         const bool next = piece + 1 < n_pieces;
         const int ntile = tile + dir;
-        double acc[kRPL];
+        float acc[kRPL];  // this wave's trees of the piece (at most ~100 leaves per row)
 #pragma unroll
-        for (int r = 0; r < kRPL; ++r) acc[r] = 0.0;
+        for (int r = 0; r < kRPL; ++r) acc[r] = 0.f;
         for (; t < t1; t += TW) {
-            walk(tb, D, hd, xa, acc, leaves + (int64_t)t * M, pend);
-            if (t + TW < t1) {
-                tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);   // LDS operations of a wave run in order
-                if (t + 2 * TW < t1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(t + 2 * TW) * S16, S16, lane);
-            }
-            // fair progress: a wave behind its workgroup's average takes the top issue priority
+            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * M, pend);
+            if (t + TW < t1) tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);  // LDS operations of a wave run in order
+            // unconditional, past the piece's last tree clamped to it: every pass issues the same
+            // loads, so the wait for a pending leaf counts only what was issued after it (with the
+            // fetch conditional, the compiler's count assumed no fetch and waited for this one)
+            tree_fetch<PF, EXACT>(pf, trees + (int64_t)min(t + 2 * TW, t1 - 1) * S16, S16, lane);
+            // fair progress, every second tree: a wave behind its workgroup's average takes the top
+            // issue priority
             my_done += 1;
-            uint32_t total = 0;
-            if (lane == 0) total = atomicAdd(progress + (piece & 1), 1u) + 1u;
-            total = __builtin_amdgcn_readfirstlane(total);
-            if (my_done * TW < total)
-                __builtin_amdgcn_s_setprio(3);
-            else
-                __builtin_amdgcn_s_setprio(0);
+            if (!(my_done & 1)) {
+                uint32_t total = 0;
+                if (lane == 0) total = atomicAdd(progress + (piece & 1), 2u) + 2u;
+                total = __builtin_amdgcn_readfirstlane(total);
+                if (my_done * TW < total)
+                    __builtin_amdgcn_s_setprio(3);
+                else
+                    __builtin_amdgcn_s_setprio(0);
+            }
         }
         __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) {
-            acc[r] += (double)pend[r];
+            acc[r] += pend[r];
             pend[r] = 0.f;
         }
         const int nt0 = next ? piece_lo(ntile) : 0, nt1 = next ? piece_hi(ntile) : 0;
         if (next && nt0 + wid < nt1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(nt0 + wid) * S16, S16, lane);
         __syncthreads();  // B1: every wave is done with the tile and its slot
 #pragma unroll
-        for (int r = 0; r < kRPL; ++r) red[wid * kRT + r * 64 + lane] = acc[r];
+        for (int r = 0; r < kRPL; ++r) red[wid * kRT + r * 64 + lane] = (double)acc[r];
         if (next && x_regs) {
             tile_commit<NT, NPX>(xf, tile_lds, F);
             if (piece + 2 < n_pieces) tile_fetch<NT, NPX>(xf, codes, ldw4, F, ntile + dir);

@@ -57,81 +57,109 @@ __device__ __forceinline__ void decide(uint32_t c, uint32_t w, uint32_t p, uint3
         : "vcc");
 }
 
-// Last level: byte offset of the leaf reached, o0 + (go right ? 4 : 0).
-__device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t o0, uint32_t o1) {
-    uint32_t d, out;
+// acc + leaf, kept where it stands (before the next leaf load into the same register): moved to the
+// end of a tree's walk, it kept the previous leaf alive past the new load, and the register copy at
+// the loop's back edge then waited for every load in flight, the next trees' prefetch included.
+__device__ __forceinline__ float add_pinned(float acc, float leaf) {
+    float r;
+    asm volatile("v_add_f32 %0, %1, %2" : "=v"(r) : "v"(acc), "v"(leaf));
+    return r;
+}
+
+// Writes feature fv (its byte 0) into byte 1 of the code address xa, keeping the row bits.
+__device__ __forceinline__ void set_feature(uint32_t &xa, uint32_t fv) {
+    asm("v_mov_b32_sdwa %[xa], %[f] dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0" : [xa] "+v"(xa)
+        : [f] "v"(fv));
+}
+
+// Last level: 2 a + (go right ? 4 : 0), where a is the LDS address of the last-level node's word.
+__device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t a) {
+    uint32_t d, s;
     asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
         "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
         "s_nop 1\n\t"
-        "v_cndmask_b32 %[o], %[a], %[b], vcc"
-        : [d] "=&v"(d), [o] "=&v"(out)
-        : [c] "v"(c), [w] "v"(w), [a] "v"(o0), [b] "v"(o1)
+        "v_cndmask_b32_e64 %[s], 0, 4, vcc"
+        : [d] "=&v"(d), [s] "=&v"(s)
+        : [c] "v"(c), [w] "v"(w)
         : "vcc");
-    return out;
+    return 2u * a + s;
 }
 
 struct Head {
     uint32_t f, w, p;  // root feature, root word, root's children's features (D >= 2)
 };
 
+// Address constants of a wave's slot (tb) for trees of depth D, as VGPR copies made once per kernel
+// (the walk's v_cndmask selects between two of them): the root's children's records at tb + 16 and
+// tb + 24; child 2n + g of a record at a is at 2a - tb + 8g; the last-level word of the child g of a
+// level D-2 record is at a + 4g + 2M.
+struct SlotConsts {
+    uint32_t l0, r0, li, ri, lt, rt;
+};
+__device__ __forceinline__ SlotConsts slot_consts(uint32_t tb, int D) {
+    const uint32_t M = 1u << D;
+    return SlotConsts{in_vgpr(tb + 16u), in_vgpr(tb + 24u), in_vgpr(0u - tb), in_vgpr(8u - tb), in_vgpr(2u * M),
+                      in_vgpr(2u * M + 4u)};
+}
+
 // Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows;
 // xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each level rewrites.  The
 // rows are independent chains: each takes its step of a level in turn, so the reads of the others
 // are in flight while one decides.  The tree's leaves are at gl (M floats); each chain's leaf is
 // loaded into pend[] after the previous tree's pending leaf has been added to acc[].
-__device__ __forceinline__ void walk(uint32_t tb, int D, const Head &h, uint32_t (&xa)[kRPL], double (&acc)[kRPL],
+__device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, const Head &h, uint32_t (&xa)[kRPL],
+                                     float (&acc)[kRPL],
                                      const float *__restrict__ gl, float (&pend)[kRPL]) {
     const uint32_t M = 1u << D;
     uint32_t x[kRPL], a[kRPL], lw[kRPL];
     uint2 rec[kRPL];
+    const uint32_t hf = in_vgpr(h.f);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
-        xa[c] = (xa[c] & 0xFFFF00FFu) | (h.f << 8);
+        set_feature(xa[c], hf);
         x[c] = lds_u16(xa[c]);
     }
     const uint32_t hw = in_vgpr(h.w), hp = in_vgpr(h.p);
-    const uint32_t l0 = in_vgpr(tb + 16u), r0 = in_vgpr(tb + 24u);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
-        decide(x[c], hw, hp, l0, r0, xa[c], s);
+        decide(x[c], hw, hp, k.l0, k.r0, xa[c], s);
         x[c] = lds_u16(xa[c]);
         a[c] = s;
         rec[c] = lds_b64(s);
         __builtin_amdgcn_sched_barrier(0);
     }
-    // levels 1 .. D-3: record address of child 2n + g = 2a - tb + 8g
-    const uint32_t li = in_vgpr(0u - tb), ri = in_vgpr(8u - tb);
+    // levels 1 .. D-3
     for (int lvl = 1; lvl + 2 < D; ++lvl) {
 #pragma unroll
         for (int c = 0; c < kRPL; ++c) {
             uint32_t s;
-            decide(x[c], rec[c].x, rec[c].y, li, ri, xa[c], s);
+            decide(x[c], rec[c].x, rec[c].y, k.li, k.ri, xa[c], s);
             x[c] = lds_u16(xa[c]);
             a[c] = 2u * a[c] + s;
             rec[c] = lds_b64(a[c]);
             __builtin_amdgcn_sched_barrier(0);
         }
     }
-    // level D-2 into the last level: the child's word at as + 2M, as = a + 4g
-    const uint32_t lt = in_vgpr(0u), rt = in_vgpr(4u), k2m = 2u * M;
+    // level D-2 into the last level (node M/2 + j's word at tb + 4M + 4j)
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
-        decide(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
+        decide(x[c], rec[c].x, rec[c].y, k.lt, k.rt, xa[c], s);
         x[c] = lds_u16(xa[c]);
         a[c] = a[c] + s;
-        lw[c] = lds_b32(a[c] + k2m);
+        lw[c] = lds_b32(a[c]);
         __builtin_amdgcn_sched_barrier(0);
     }
-    // last-level node k = (as - tb - 2M) / 4; its leaves at byte 8k of the tree's leaves
-    const uint32_t kb2 = 0u - 2u * tb - 4u * M;
+    // last-level node M/2 + j's leaves are at byte 8j of the tree's leaves, and 2 (tb + 4M + 4j) - 8j
+    // is the same for every j: leaf byte = lb + 2a + 4g
+    const char *__restrict__ lb = reinterpret_cast<const char *>(gl) - (2u * tb + 8u * M);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
-        const uint32_t o0 = 2u * a[c] + kb2;
-        const uint32_t o = leaf_off(x[c], lw[c], o0, o0 + 4u);
-        acc[c] += (double)pend[c];
-        pend[c] = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(gl) + o);
+        const uint32_t o = leaf_off(x[c], lw[c], a[c]);
+        acc[c] = add_pinned(acc[c], pend[c]);
+        __builtin_amdgcn_sched_barrier(0);
+        pend[c] = *reinterpret_cast<const float *>(lb + o);
     }
 }
 

@@ -38,13 +38,14 @@ __global__ __launch_bounds__(64 * TW) void k_visit_probe(const uint4 *__restrict
     uint32_t xa[kRPL];
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
-    double acc[kRPL] = {0.0, 0.0, 0.0, 0.0};
+    float acc[kRPL] = {0.f, 0.f, 0.f, 0.f};
     float pend[kRPL] = {0.f, 0.f, 0.f, 0.f};
     const float *gl = leaves + (int64_t)tree * (1 << D);
-    for (int r = 0; r < reps; ++r) walk(tb, D, hd, xa, acc, gl, pend);
+    const SlotConsts sk = slot_consts(tb, D);
+    for (int r = 0; r < reps; ++r) walk(tb, D, sk, hd, xa, acc, gl, pend);
     double s = 0.0;
 #pragma unroll
-    for (int j = 0; j < kRPL; ++j) s += acc[j] + (double)pend[j];
+    for (int j = 0; j < kRPL; ++j) s += (double)acc[j] + (double)pend[j];
     out[(int64_t)blockIdx.x * 64 * TW + threadIdx.x] = s;
 }
 
