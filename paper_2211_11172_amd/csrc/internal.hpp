@@ -60,7 +60,7 @@ struct harl_ensemble {
     void *d_trees_b16;
     float *d_thr_b16;                         // per feature: sorted thresholds + NaN padding
     int32_t *d_thr_off_b16, *d_thr_len_b16;   // their offsets and lengths (padding included)
-    int32_t *d_steps_b16;                     // binary-search probes per feature
+    int32_t *d_search_b16;                    // per feature: {probes | key shift << 8, bucket base}
     uint16_t *d_lut_b16;                      // per feature: thresholds below each of 4,096 key buckets
     float *d_leaves_b16;                      // [n_trees][2^depth] leaves
     int32_t b16_stride, tree_groups_b16;

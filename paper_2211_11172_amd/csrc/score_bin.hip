@@ -59,21 +59,28 @@ constexpr int kPrefetchFeatures = 192;          // features per tile held in the
 
 // ---- K0: codes of every (row, feature) ----
 // The order-preserving 32-bit key of a present value is its bit pattern with the sign bit set for
-// +-values >= +0 and all bits inverted for negatives; its top 12 bits select one of 4,096 buckets.
-// Per feature, lut[b] = number of thresholds whose key lies in a lower bucket, and every bucket
-// holds fewer than 2^steps thresholds.  A value in bucket b has a code between lut[b] and
-// lut[b] + 2^steps - 1: a branch-free binary search of `steps` probes, starting at lut[b], finds
-// it.  Probes past the bucket land on larger thresholds (or on the table's NaN padding), which
-// never compare <= x, so no bound check is needed; -0 and +0 compare equal, and the thresholds hold
-// one zero (+0), which a -0 in the bucket below reaches in the same way.
+// +-values >= +0 and all bits inverted for negatives.  Per feature, a window of keys is cut into
+// 4,094 buckets of 2^sh keys (sh >= 1): bucket b = clamp((key >> sh) - base, 0, 4095), so keys
+// below the window fall in bucket 0 and keys above it in bucket 4095.  The window (and sh) is chosen
+// when the ensemble is packed to cover the feature's thresholds, but for up to three outliers at
+// either end, with the fewest thresholds in the fullest bucket.  lut[b] = number of thresholds in
+// lower buckets, and every bucket holds fewer than 2^steps - 1 thresholds.  A value in bucket b has a
+// code between lut[b] and lut[b] + 2^steps - 1: a branch-free binary search of `steps` probes,
+// starting at lut[b], finds it.  Probes past the bucket land on larger thresholds (or on the table's
+// NaN padding), which never compare <= x, so no bound check is needed; -0 and +0 compare equal, and
+// the thresholds hold one zero (+0), which a -0 in the bucket below reaches in the same way (hence
+// the one threshold of slack).
 // Workgroup (feature f, range of tiles): stages lut and the thresholds of f in LDS (or searches
-// them in global memory when they do not fit), then each thread codes 4 row pairs (p, p + 128) of
-// its tiles at a time.  Rows at or past n_rows get code 0 (never summed).
+// them in global memory when they do not fit), then each thread codes two row quads of a tile at a
+// time: rows 4q .. 4q + 3 and 128 + 4q .. 131 + 4q, read as two 16-byte loads when the feature
+// rows are 16-byte aligned (VEC), written as one 16-byte store.  Rows at or past n_rows get code 0
+// (never summed).
 constexpr int kBinThreads = 256;
 constexpr int kLutBuckets = 4096;
 constexpr int kLutStride = 4104;                  // u16 per feature's lut (4,097 used), 16-byte rows
 constexpr int kBinLdsThresholds = 10240;          // 40 KB, padding included
-constexpr int kBinPairs = 4;                      // row pairs per thread and iteration
+constexpr int kBinQuads = 2;                      // row quads per thread and iteration
+constexpr int kQuadsPerTile = kRT / 8;            // 32
 
 __device__ __forceinline__ uint32_t order_key(float x) {
     const uint32_t u = __float_as_uint(x);
@@ -83,9 +90,13 @@ __device__ __forceinline__ uint32_t order_key(float x) {
 // Codes of N values at once: the probes of the N searches are independent and overlap.
 template <int N>
 __device__ __forceinline__ void codes_of(const float (&x)[N], uint32_t (&c)[N], const uint16_t *lut, const float *tf,
-                                         int steps) {
+                                         int steps, int sh, uint32_t base) {
 #pragma unroll
-    for (int e = 0; e < N; ++e) c[e] = lut[order_key(x[e]) >> 20];
+    for (int e = 0; e < N; ++e) {
+        int b = (int)((order_key(x[e]) >> sh) - base);
+        b = b < 0 ? 0 : (b > kLutBuckets - 1 ? kLutBuckets - 1 : b);
+        c[e] = lut[b];
+    }
     for (int k = steps - 1; k >= 0; --k) {
         const uint32_t s = 1u << k;
 #pragma unroll
@@ -97,11 +108,12 @@ __device__ __forceinline__ void codes_of(const float (&x)[N], uint32_t (&c)[N], 
         if (x[e] != x[e]) c[e] = kMissing;
 }
 
+template <bool VEC>
 __global__ __launch_bounds__(kBinThreads) void k_bin16(const float *__restrict__ X, int64_t ld, int n_rows,
                                                        const float *__restrict__ thr, const int32_t *__restrict__ t_off,
                                                        const int32_t *__restrict__ t_len,
                                                        const uint16_t *__restrict__ luts,
-                                                       const int32_t *__restrict__ steps_f, uint32_t *__restrict__ codes,
+                                                       const int32_t *__restrict__ search_f, uint32_t *__restrict__ codes,
                                                        int64_t ldw, int tiles, int tiles_per_block, int blocks_per_f) {
     __shared__ float st[kBinLdsThresholds];
     __shared__ uint16_t sl[kLutStride];
@@ -109,7 +121,8 @@ __global__ __launch_bounds__(kBinThreads) void k_bin16(const float *__restrict__
     const int tile0 = (blockIdx.x % blocks_per_f) * tiles_per_block;
     const int tile1 = min(tiles, tile0 + tiles_per_block);
     if (tile0 >= tile1) return;  // whole workgroup
-    const int len = t_len[f], steps = steps_f[f];
+    const int len = t_len[f], steps = search_f[2 * f] & 0xFF, sh = search_f[2 * f] >> 8;
+    const uint32_t base = (uint32_t)search_f[2 * f + 1];
     const float *__restrict__ tg = thr + t_off[f];
     const bool in_lds = len <= kBinLdsThresholds;
     {
@@ -122,33 +135,48 @@ __global__ __launch_bounds__(kBinThreads) void k_bin16(const float *__restrict__
     __syncthreads();
     const float *__restrict__ xf = X + (int64_t)f * ld;
     uint32_t *__restrict__ out = codes + (int64_t)f * ldw;
-    const int n_pairs = (tile1 - tile0) * (kRT / 2);
-    for (int i0 = threadIdx.x; i0 < n_pairs; i0 += kBinPairs * kBinThreads) {
-        float x[2 * kBinPairs];
-        int at[kBinPairs];
+    const int n_quads = (tile1 - tile0) * kQuadsPerTile;
+    for (int i0 = threadIdx.x; i0 < n_quads; i0 += kBinQuads * kBinThreads) {
+        float x[8 * kBinQuads];
+        int row[kBinQuads];  // first row of the quad pair, -1 past the range
 #pragma unroll
-        for (int j = 0; j < kBinPairs; ++j) {
+        for (int j = 0; j < kBinQuads; ++j) {
             const int i = i0 + j * kBinThreads;
-            const int t = tile0 + i / (kRT / 2), p = i % (kRT / 2);
-            const int r0 = t * kRT + p, r1 = r0 + kRT / 2;
-            at[j] = i < n_pairs ? t * (kRT / 2) + p : -1;
-            x[2 * j] = i < n_pairs && r0 < n_rows ? xf[r0] : 0.f;
-            x[2 * j + 1] = i < n_pairs && r1 < n_rows ? xf[r1] : 0.f;
-        }
-        uint32_t c[2 * kBinPairs];
-        if (in_lds)
-            codes_of<2 * kBinPairs>(x, c, sl, st, steps);
-        else
-            codes_of<2 * kBinPairs>(x, c, sl, tg, steps);
+            const int t = tile0 + i / kQuadsPerTile, q = i % kQuadsPerTile;
+            const int r = i < n_quads ? t * kRT + 4 * q : -1;
+            row[j] = r;
+            if (VEC && r >= 0 && r + kRT / 2 + 3 < n_rows) {
+                const float4 a = *reinterpret_cast<const float4 *>(xf + r);
+                const float4 b = *reinterpret_cast<const float4 *>(xf + r + kRT / 2);
+                x[8 * j + 0] = a.x, x[8 * j + 1] = a.y, x[8 * j + 2] = a.z, x[8 * j + 3] = a.w;
+                x[8 * j + 4] = b.x, x[8 * j + 5] = b.y, x[8 * j + 6] = b.z, x[8 * j + 7] = b.w;
+            } else {  // the last tile's quads (n_rows >= 1): clamped loads, rows past the end read as 0
 #pragma unroll
-        for (int j = 0; j < kBinPairs; ++j) {
-            const int i = i0 + j * kBinThreads;
-            const int t = tile0 + i / (kRT / 2), p = i % (kRT / 2);
-            if (at[j] >= 0) {
-                const uint32_t lo = t * kRT + p < n_rows ? c[2 * j] : 0u;
-                const uint32_t hi = t * kRT + p + kRT / 2 < n_rows ? c[2 * j + 1] : 0u;
-                out[at[j]] = lo | hi << 16;
+                for (int e = 0; e < 8; ++e) {
+                    const int rr = r + (e & 3) + (e >> 2) * (kRT / 2);
+                    const float v = xf[rr < 0 ? 0 : (rr < n_rows ? rr : n_rows - 1)];
+                    x[8 * j + e] = r >= 0 && rr < n_rows ? v : 0.f;
+                }
             }
+        }
+        uint32_t c[8 * kBinQuads];
+        if (in_lds)
+            codes_of<8 * kBinQuads>(x, c, sl, st, steps, sh, base);
+        else
+            codes_of<8 * kBinQuads>(x, c, sl, tg, steps, sh, base);
+#pragma unroll
+        for (int j = 0; j < kBinQuads; ++j) {
+            const int r = row[j];
+            if (r < 0) continue;
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t lo = r + e < n_rows ? c[8 * j + e] : 0u;
+                const uint32_t hi = r + kRT / 2 + e < n_rows ? c[8 * j + 4 + e] : 0u;
+                w[e] = lo | hi << 16;
+            }
+            // dwords (tile, p .. p + 3): tile r / 256, p = r % 256
+            *reinterpret_cast<uint4 *>(out + (int64_t)(r / kRT) * (kRT / 2) + r % kRT) = make_uint4(w[0], w[1], w[2], w[3]);
         }
     }
 }
@@ -463,9 +491,11 @@ int score_b16_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t
     const int64_t ldw = w.tiles * (kRT / 2);
     const int tpb = bin_tiles_per_block(w.tiles);
     const int bpf = (int)ceil_div(w.tiles, tpb);
-    hipLaunchKernelGGL(k_bin16, dim3((unsigned)(E->n_features * bpf)), dim3(kBinThreads), 0, stream, X, ld, n_rows,
-                       E->d_thr_b16, E->d_thr_off_b16, E->d_thr_len_b16, E->d_lut_b16, E->d_steps_b16, codes, ldw,
-                       (int)w.tiles, tpb, bpf);
+    // 16-byte feature loads when every feature row starts on a 16-byte boundary
+    const bool vec = (reinterpret_cast<uintptr_t>(X) % 16) == 0 && ld % 4 == 0;
+    hipLaunchKernelGGL(vec ? k_bin16<true> : k_bin16<false>, dim3((unsigned)(E->n_features * bpf)), dim3(kBinThreads),
+                       0, stream, X, ld, n_rows, E->d_thr_b16, E->d_thr_off_b16, E->d_thr_len_b16, E->d_lut_b16,
+                       E->d_search_b16, codes, ldw, (int)w.tiles, tpb, bpf);
     HARL_HIP_CHECK(hipGetLastError());
     const size_t lds = b16_lds(E, sh->tw);
     if (const int rc = ensure_dynamic_lds(reinterpret_cast<const void *>(sh->kern), lds)) return rc;
@@ -506,32 +536,58 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
         std::memcpy(&u, &v, 4);
         return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
     };
-    // per feature: the sorted thresholds padded with 2^steps NaNs, the bucket table and the probe count
-    std::vector<int32_t> off(F), len(F), steps(F);
+    // per feature: the sorted thresholds padded with 2^steps NaNs, the bucket window and table, and
+    // the probe count
+    std::vector<int32_t> off(F), len(F), search(2 * (size_t)F);
     std::vector<uint16_t> lut((size_t)F * kLutStride, 0);
     std::vector<float> flat;
+    std::vector<int32_t> per(kLutBuckets);
     for (int f = 0; f < F; ++f) {
         auto &v = tab[f];
         std::sort(v.begin(), v.end());
         v.erase(std::unique(v.begin(), v.end()), v.end());
         if (v.size() > 65534) return HARL_OK;
-        std::vector<int32_t> per(kLutBuckets, 0);
-        for (float t : v) ++per[key_of(t) >> 20];
-        int max_b = 0, run = 0;
+        const int n = (int)v.size();
+        std::vector<uint32_t> k(n);
+        for (int i = 0; i < n; ++i) k[i] = key_of(v[i]);
+        auto bucket = [](uint32_t key, int sh, uint32_t base) {
+            const int b = (int)((key >> sh) - base);
+            return b < 0 ? 0 : (b > kLutBuckets - 1 ? kLutBuckets - 1 : b);
+        };
+        // window [k[lo], k[n - 1 - hi]] in buckets 1 .. 4094; the fewest probes, then the fewest outliers
+        int best_steps = 99, best_sh = 1;
+        uint32_t best_base = 0;
+        for (int drop = 0; drop <= 6; ++drop)
+            for (int lo = 0; lo <= drop && lo <= 3; ++lo) {
+                const int hi = drop - lo;
+                if (hi > 3 || lo + hi >= n) continue;
+                const uint32_t klo = k[lo], khi = k[n - 1 - hi];
+                int sh = 1;
+                while (sh < 31 && (khi >> sh) - (klo >> sh) > (uint32_t)(kLutBuckets - 3)) ++sh;
+                const uint32_t base = (klo >> sh) - 1u;
+                std::fill(per.begin(), per.end(), 0);
+                int max_b = 0;
+                for (int i = 0; i < n; ++i) max_b = std::max(max_b, ++per[bucket(k[i], sh, base)]);
+                int st = 0;
+                while ((1 << st) < max_b + 2) ++st;  // a -0 in the bucket below +0 may count one more
+                if (st < best_steps) best_steps = st, best_sh = sh, best_base = base;
+            }
+        if (n == 0) best_steps = 1, best_sh = 1, best_base = 0;
+        std::fill(per.begin(), per.end(), 0);
+        for (int i = 0; i < n; ++i) ++per[bucket(k[i], best_sh, best_base)];
         uint16_t *lf = lut.data() + (size_t)f * kLutStride;
+        int run = 0;
         for (int b = 0; b < kLutBuckets; ++b) {
             lf[b] = (uint16_t)run;
             run += per[b];
-            max_b = per[b] > max_b ? per[b] : max_b;
         }
         lf[kLutBuckets] = (uint16_t)run;
-        int st = 0;
-        while ((1 << st) < max_b + 2) ++st;   // a -0 in the bucket below +0 may count one more
         off[f] = (int32_t)flat.size();
         flat.insert(flat.end(), v.begin(), v.end());
-        flat.insert(flat.end(), (size_t)1 << st, std::numeric_limits<float>::quiet_NaN());
+        flat.insert(flat.end(), (size_t)1 << best_steps, std::numeric_limits<float>::quiet_NaN());
         len[f] = (int32_t)(flat.size() - off[f]);
-        steps[f] = st;
+        search[2 * f] = best_steps | best_sh << 8;
+        search[2 * f + 1] = (int32_t)best_base;
     }
     auto word = [&](int32_t f, float v, uint8_t dl) -> uint32_t {
         uint32_t theta = 0;  // dummy split (f < 0) or NaN threshold: every present value goes right
@@ -570,15 +626,15 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     int G = 1;
     while (G < 8 && 2 * G <= T && (int64_t)T * stride / G > (3 << 20)) G *= 2;
     if (E->tree_groups_override > 0 && E->tree_groups_override <= T) G = E->tree_groups_override;
-    void *d_trees = nullptr, *d_thr = nullptr, *d_off = nullptr, *d_len = nullptr, *d_steps = nullptr, *d_lut = nullptr,
+    void *d_trees = nullptr, *d_thr = nullptr, *d_off = nullptr, *d_len = nullptr, *d_search = nullptr, *d_lut = nullptr,
          *d_gl = nullptr;
     auto cleanup = [&]() {
-        for (void *p : {d_trees, d_thr, d_off, d_len, d_steps, d_lut, d_gl})
+        for (void *p : {d_trees, d_thr, d_off, d_len, d_search, d_lut, d_gl})
             if (p) (void)hipFree(p);
     };
     if (hipMalloc(&d_trees, host.size()) != hipSuccess || hipMalloc(&d_thr, flat.size() * 4) != hipSuccess ||
         hipMalloc(&d_off, (size_t)F * 4) != hipSuccess || hipMalloc(&d_len, (size_t)F * 4) != hipSuccess ||
-        hipMalloc(&d_steps, (size_t)F * 4) != hipSuccess || hipMalloc(&d_lut, lut.size() * 2) != hipSuccess ||
+        hipMalloc(&d_search, search.size() * 4) != hipSuccess || hipMalloc(&d_lut, lut.size() * 2) != hipSuccess ||
         hipMalloc(&d_gl, gleaves.size() * 4) != hipSuccess) {
         cleanup();
         return fail(HARL_E_NOMEM, "harl_ensemble_create: device allocation failed");
@@ -587,7 +643,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     if (e == hipSuccess) e = hipMemcpyAsync(d_thr, flat.data(), flat.size() * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(d_off, off.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(d_len, len.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
-    if (e == hipSuccess) e = hipMemcpyAsync(d_steps, steps.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_search, search.data(), search.size() * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(d_lut, lut.data(), lut.size() * 2, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(d_gl, gleaves.data(), gleaves.size() * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
@@ -599,7 +655,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     E->d_thr_b16 = static_cast<float *>(d_thr);
     E->d_thr_off_b16 = static_cast<int32_t *>(d_off);
     E->d_thr_len_b16 = static_cast<int32_t *>(d_len);
-    E->d_steps_b16 = static_cast<int32_t *>(d_steps);
+    E->d_search_b16 = static_cast<int32_t *>(d_search);
     E->d_lut_b16 = static_cast<uint16_t *>(d_lut);
     E->d_leaves_b16 = static_cast<float *>(d_gl);
     E->b16_stride = stride;
@@ -609,12 +665,12 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
 
 void free_b16(harl_ensemble *E) {
     for (void *p : {E->d_trees_b16, (void *)E->d_thr_b16, (void *)E->d_thr_off_b16, (void *)E->d_thr_len_b16,
-                    (void *)E->d_steps_b16, (void *)E->d_lut_b16, (void *)E->d_leaves_b16})
+                    (void *)E->d_search_b16, (void *)E->d_lut_b16, (void *)E->d_leaves_b16})
         if (p) (void)hipFree(p);
     E->d_trees_b16 = nullptr;
     E->d_leaves_b16 = nullptr;
     E->d_thr_b16 = nullptr;
-    E->d_thr_off_b16 = E->d_thr_len_b16 = E->d_steps_b16 = nullptr;
+    E->d_thr_off_b16 = E->d_thr_len_b16 = E->d_search_b16 = nullptr;
     E->d_lut_b16 = nullptr;
 }
 
