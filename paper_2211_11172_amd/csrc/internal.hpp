@@ -64,6 +64,7 @@ struct harl_ensemble {
     uint16_t *d_lut_b16;                      // per feature: thresholds below each of 4,096 key buckets
     float *d_leaves_b16;                      // [n_trees][2^depth] leaves
     int32_t b16_stride, tree_groups_b16;
+    int32_t b16_common_steps;                 // the probe count of the most features
 };
 
 // ------------------------------------------------------------------------------------------

@@ -71,10 +71,10 @@ constexpr int kPrefetchFeatures = 192;          // features per tile held in the
 // the thresholds hold one zero (+0), which a -0 in the bucket below reaches in the same way (hence
 // the one threshold of slack).
 // Workgroup (feature f, range of tiles): stages lut and the thresholds of f in LDS (or searches
-// them in global memory when they do not fit), then each thread codes two row quads of a tile at a
-// time: rows 4q .. 4q + 3 and 128 + 4q .. 131 + 4q, read as two 16-byte loads when the feature
-// rows are 16-byte aligned (VEC), written as one 16-byte store.  Rows at or past n_rows get code 0
-// (never summed).
+// them in global memory when they do not fit), then each thread codes two row quads at a time: rows
+// 4q .. 4q + 3 and 128 + 4q .. 131 + 4q of a tile, read as two 16-byte loads when the feature rows
+// are 16-byte aligned (VEC), written as one 16-byte store.  Rows at or past n_rows get code 0 (never
+// summed).
 constexpr int kBinThreads = 256;
 constexpr int kLutBuckets = 4096;
 constexpr int kLutStride = 4104;                  // u16 per feature's lut (4,097 used), 16-byte rows
@@ -87,28 +87,51 @@ __device__ __forceinline__ uint32_t order_key(float x) {
     return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
 }
 
-// Codes of N values at once: the probes of the N searches are independent and overlap.
-template <int N>
+__device__ __forceinline__ int key_bucket(float x, int sh, uint32_t base) {
+    const int b = (int)((order_key(x) >> sh) - base);
+    return b < 0 ? 0 : (b > kLutBuckets - 1 ? kLutBuckets - 1 : b);
+}
+
+// Codes of N values at once: the probes of the N searches are independent and overlap.  With the
+// probe count a compile-time STEPS and the thresholds in LDS, each search carries a pointer whose
+// probe offsets are immediates of the LDS reads; otherwise (STEPS = 0) an index and `steps` probes.
+typedef __attribute__((address_space(3))) const float lds_float;
+template <int N, int STEPS>
 __device__ __forceinline__ void codes_of(const float (&x)[N], uint32_t (&c)[N], const uint16_t *lut, const float *tf,
                                          int steps, int sh, uint32_t base) {
+    if constexpr (STEPS > 0) {
+        lds_float *const t0 = (lds_float *)tf;  // tf points into LDS on this path
+        lds_float *p[N];
 #pragma unroll
-    for (int e = 0; e < N; ++e) {
-        int b = (int)((order_key(x[e]) >> sh) - base);
-        b = b < 0 ? 0 : (b > kLutBuckets - 1 ? kLutBuckets - 1 : b);
-        c[e] = lut[b];
-    }
-    for (int k = steps - 1; k >= 0; --k) {
-        const uint32_t s = 1u << k;
+        for (int e = 0; e < N; ++e) p[e] = t0 + lut[key_bucket(x[e], sh, base)];
 #pragma unroll
-        for (int e = 0; e < N; ++e)
-            if (tf[c[e] + s - 1] <= x[e]) c[e] += s;
+        for (int k = STEPS - 1; k >= 0; --k) {
+            float t[N];
+#pragma unroll
+            for (int e = 0; e < N; ++e) t[e] = p[e][(1 << k) - 1];
+            __builtin_amdgcn_sched_barrier(0);  // all N reads in flight before the first compare
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                if (t[e] <= x[e]) p[e] += 1 << k;
+        }
+#pragma unroll
+        for (int e = 0; e < N; ++e) c[e] = (uint32_t)(p[e] - t0);
+    } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) c[e] = lut[key_bucket(x[e], sh, base)];
+        for (int k = steps - 1; k >= 0; --k) {
+            const uint32_t s = 1u << k;
+#pragma unroll
+            for (int e = 0; e < N; ++e)
+                if (tf[c[e] + s - 1] <= x[e]) c[e] += s;
+        }
     }
 #pragma unroll
     for (int e = 0; e < N; ++e)
         if (x[e] != x[e]) c[e] = kMissing;
 }
 
-template <bool VEC>
+template <bool VEC, int STEPS>
 __global__ __launch_bounds__(kBinThreads) void k_bin16(const float *__restrict__ X, int64_t ld, int n_rows,
                                                        const float *__restrict__ thr, const int32_t *__restrict__ t_off,
                                                        const int32_t *__restrict__ t_len,
@@ -135,48 +158,80 @@ __global__ __launch_bounds__(kBinThreads) void k_bin16(const float *__restrict__
     __syncthreads();
     const float *__restrict__ xf = X + (int64_t)f * ld;
     uint32_t *__restrict__ out = codes + (int64_t)f * ldw;
+    constexpr int kPass = kBinQuads * kBinThreads;  // quads per pass: 16 tiles
     const int n_quads = (tile1 - tile0) * kQuadsPerTile;
-    for (int i0 = threadIdx.x; i0 < n_quads; i0 += kBinQuads * kBinThreads) {
-        float x[8 * kBinQuads];
-        int row[kBinQuads];  // first row of the quad pair, -1 past the range
+    auto code = [&](const float (&x)[8 * kBinQuads], uint32_t (&c)[8 * kBinQuads]) {
+        if (STEPS > 0 && in_lds && steps == STEPS)
+            codes_of<8 * kBinQuads, STEPS>(x, c, sl, st, steps, sh, base);
+        else if (in_lds)
+            codes_of<8 * kBinQuads, 0>(x, c, sl, st, steps, sh, base);
+        else
+            codes_of<8 * kBinQuads, 0>(x, c, sl, tg, steps, sh, base);
+    };
+    // quad i of the range: rows 4q .. 4q + 3 and 128 + 4q .. 131 + 4q of tile tile0 + i / 32, whose codes
+    // go to dwords 4q .. 4q + 3 of that tile
+    auto quad_row = [&](int i) { return (tile0 + i / kQuadsPerTile) * kRT + 4 * (i % kQuadsPerTile); };
+    auto store = [&](int r, const uint32_t *c) {
+        *reinterpret_cast<uint4 *>(out + (int64_t)(r / kRT) * (kRT / 2) + r % kRT) =
+            make_uint4(c[0] | c[4] << 16, c[1] | c[5] << 16, c[2] | c[6] << 16, c[3] | c[7] << 16);
+    };
+    // Passes over whole tiles of rows below n_rows need no bounds checks; their features are read one
+    // pass ahead, so that the next pass's loads are in flight while this one is coded (every pass
+    // issues the same loads and stores, the last one re-reading its own features, so the wait for the
+    // features counts only the stores issued after them).
+    const int full_tiles = min(tile1, n_rows / kRT) - tile0;
+    const int n_full = VEC && full_tiles > 0 ? full_tiles * kQuadsPerTile / kPass : 0;
+    if (n_full > 0) {
+        auto load = [&](int pass, float (&x)[8 * kBinQuads]) {
 #pragma unroll
-        for (int j = 0; j < kBinQuads; ++j) {
-            const int i = i0 + j * kBinThreads;
-            const int t = tile0 + i / kQuadsPerTile, q = i % kQuadsPerTile;
-            const int r = i < n_quads ? t * kRT + 4 * q : -1;
-            row[j] = r;
-            if (VEC && r >= 0 && r + kRT / 2 + 3 < n_rows) {
+            for (int j = 0; j < kBinQuads; ++j) {
+                const int r = quad_row(pass * kPass + j * kBinThreads + threadIdx.x);
                 const float4 a = *reinterpret_cast<const float4 *>(xf + r);
                 const float4 b = *reinterpret_cast<const float4 *>(xf + r + kRT / 2);
                 x[8 * j + 0] = a.x, x[8 * j + 1] = a.y, x[8 * j + 2] = a.z, x[8 * j + 3] = a.w;
                 x[8 * j + 4] = b.x, x[8 * j + 5] = b.y, x[8 * j + 6] = b.z, x[8 * j + 7] = b.w;
-            } else {  // the last tile's quads (n_rows >= 1): clamped loads, rows past the end read as 0
+            }
+        };
+        float xn[8 * kBinQuads];
+        load(0, xn);
+        for (int pass = 0; pass < n_full; ++pass) {
+            float x[8 * kBinQuads];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int rr = r + (e & 3) + (e >> 2) * (kRT / 2);
-                    const float v = xf[rr < 0 ? 0 : (rr < n_rows ? rr : n_rows - 1)];
-                    x[8 * j + e] = r >= 0 && rr < n_rows ? v : 0.f;
-                }
+            for (int e = 0; e < 8 * kBinQuads; ++e) x[e] = xn[e];
+            load(min(pass + 1, n_full - 1), xn);
+            uint32_t c[8 * kBinQuads];
+            code(x, c);
+#pragma unroll
+            for (int j = 0; j < kBinQuads; ++j) store(quad_row(pass * kPass + j * kBinThreads + threadIdx.x), c + 8 * j);
+        }
+    }
+    // the rest of the range (its last tiles, a partial last tile): bounds-checked, rows at or past
+    // n_rows read as 0 and coded 0
+    for (int i0 = n_full * kPass + threadIdx.x; i0 < n_quads; i0 += kPass) {
+        float x[8 * kBinQuads];
+        int row[kBinQuads];
+#pragma unroll
+        for (int j = 0; j < kBinQuads; ++j) {
+            const int i = i0 + j * kBinThreads;
+            const int r = i < n_quads ? quad_row(i) : -1;
+            row[j] = r;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int rr = r + (e & 3) + (e >> 2) * (kRT / 2);
+                const float v = xf[rr < 0 ? 0 : (rr < n_rows ? rr : n_rows - 1)];  // n_rows >= 1
+                x[8 * j + e] = r >= 0 && rr < n_rows ? v : 0.f;
             }
         }
         uint32_t c[8 * kBinQuads];
-        if (in_lds)
-            codes_of<8 * kBinQuads>(x, c, sl, st, steps, sh, base);
-        else
-            codes_of<8 * kBinQuads>(x, c, sl, tg, steps, sh, base);
+        code(x, c);
 #pragma unroll
         for (int j = 0; j < kBinQuads; ++j) {
             const int r = row[j];
             if (r < 0) continue;
-            uint32_t w[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t lo = r + e < n_rows ? c[8 * j + e] : 0u;
-                const uint32_t hi = r + kRT / 2 + e < n_rows ? c[8 * j + 4 + e] : 0u;
-                w[e] = lo | hi << 16;
-            }
-            // dwords (tile, p .. p + 3): tile r / 256, p = r % 256
-            *reinterpret_cast<uint4 *>(out + (int64_t)(r / kRT) * (kRT / 2) + r % kRT) = make_uint4(w[0], w[1], w[2], w[3]);
+            for (int e = 0; e < 8; ++e)
+                if (r + (e & 3) + (e >> 2) * (kRT / 2) >= n_rows) c[8 * j + e] = 0u;
+            store(r, c + 8 * j);
         }
     }
 }
@@ -491,11 +546,18 @@ int score_b16_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t
     const int64_t ldw = w.tiles * (kRT / 2);
     const int tpb = bin_tiles_per_block(w.tiles);
     const int bpf = (int)ceil_div(w.tiles, tpb);
-    // 16-byte feature loads when every feature row starts on a 16-byte boundary
+    // 16-byte feature loads when every feature row starts on a 16-byte boundary; probe offsets as
+    // immediates for the workgroups of features searched with the ensemble's most common probe count
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16) == 0 && ld % 4 == 0;
-    hipLaunchKernelGGL(vec ? k_bin16<true> : k_bin16<false>, dim3((unsigned)(E->n_features * bpf)), dim3(kBinThreads),
-                       0, stream, X, ld, n_rows, E->d_thr_b16, E->d_thr_off_b16, E->d_thr_len_b16, E->d_lut_b16,
-                       E->d_search_b16, codes, ldw, (int)w.tiles, tpb, bpf);
+    using BinKernel = void (*)(const float *, int64_t, int, const float *, const int32_t *, const int32_t *,
+                               const uint16_t *, const int32_t *, uint32_t *, int64_t, int, int, int);
+    static const BinKernel kBin[2][6] = {
+        {k_bin16<false, 0>, k_bin16<false, 1>, k_bin16<false, 2>, k_bin16<false, 3>, k_bin16<false, 4>, k_bin16<false, 5>},
+        {k_bin16<true, 0>, k_bin16<true, 1>, k_bin16<true, 2>, k_bin16<true, 3>, k_bin16<true, 4>, k_bin16<true, 5>}};
+    const int ms = E->b16_common_steps >= 1 && E->b16_common_steps <= 5 ? E->b16_common_steps : 0;
+    hipLaunchKernelGGL(kBin[vec ? 1 : 0][ms], dim3((unsigned)(E->n_features * bpf)), dim3(kBinThreads), 0, stream, X,
+                       ld, n_rows, E->d_thr_b16, E->d_thr_off_b16, E->d_thr_len_b16, E->d_lut_b16, E->d_search_b16,
+                       codes, ldw, (int)w.tiles, tpb, bpf);
     HARL_HIP_CHECK(hipGetLastError());
     const size_t lds = b16_lds(E, sh->tw);
     if (const int rc = ensure_dynamic_lds(reinterpret_cast<const void *>(sh->kern), lds)) return rc;
@@ -589,6 +651,13 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
         search[2 * f] = best_steps | best_sh << 8;
         search[2 * f + 1] = (int32_t)best_base;
     }
+    int common_steps = 0;
+    {
+        int count[17] = {0};
+        for (int f = 0; f < F; ++f) ++count[std::min(search[2 * f] & 0xFF, 16)];
+        for (int st = 1; st <= 16; ++st)
+            if (count[st] > count[common_steps]) common_steps = st;
+    }
     auto word = [&](int32_t f, float v, uint8_t dl) -> uint32_t {
         uint32_t theta = 0;  // dummy split (f < 0) or NaN threshold: every present value goes right
         if (f >= 0 && !std::isnan(v)) {
@@ -660,6 +729,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     E->d_leaves_b16 = static_cast<float *>(d_gl);
     E->b16_stride = stride;
     E->tree_groups_b16 = G;
+    E->b16_common_steps = common_steps;
     return HARL_OK;
 }
 
