@@ -41,9 +41,9 @@ PEAK_GVISITS = N_CU * CLOCK_GHZ * VALU_LANES_PER_CLK / VALU_PER_VISIT  # G visit
 # and by the SHA-256 of the scoring sources (score.hip, score_bin.hip, walk_b16.hpp) the counters were
 # taken with: any other source reports null.
 SCORE_TRAFFIC_BYTES = {
-    # streamed batch 0 (2,124,965 rows): k_bin16 1,382,698 + 680,682 KiB, k_tree_score_b16<12,6>
-    # 2,792,173 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
-    ("streamed", "b6d9dffda451f214387d2b6b66d086fa7f9b84c0a2ea60952297f7c64c921a11"): 5007653990,
+    # streamed batch 0 (2,124,965 rows): k_bin16 1,385,234 + 680,682 KiB, k_tree_score_b16<12,6>
+    # 4,300,361 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
+    ("streamed", "2abb492041fb57fbfeb341abc646a30aa907fbe648916e0e3d47741a5d66ec8f"): 6554635776,
 }
 
 
