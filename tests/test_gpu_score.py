@@ -204,6 +204,48 @@ def test_binned_wide_tiles_staged_directly(n_features):
     _check(cfg)
 
 
+@pytest.mark.parametrize("aligned", [True, False])
+def test_binned_whole_tile_passes_exact(aligned):
+    """More than 16 whole tiles of rows: the bin kernel's unchecked passes (16 tiles each, features
+    read one pass ahead) and its bounds-checked rest, with 16-byte feature loads when the leading
+    dimension is a multiple of 4 floats and element loads when it is not."""
+    cfg = get_config("tiny", exact=True).with_(depth=10, n_trees=23, n_prog=3000, s_max=9, p_nan=0.1,
+                                               name="binned-passes-%s" % ("vec" if aligned else "scalar"))
+    n_rows = gen_batch(cfg)["n_rows"]
+    assert n_rows > 3 * 16 * 256 and n_rows % 256 != 0
+    pad = (-n_rows) % 4 if aligned else (1 if (n_rows + 1) % 4 else 2)
+    b = gen_batch(cfg, ld_pad=pad)
+    assert (b["ld"] % 4 == 0) == aligned
+    _check(cfg, b=b)
+
+
+def test_binned_probe_counts_and_global_search():
+    """Features searched with different probe counts (the bin kernel is specialised for the most
+    common one, the others take its general loop), a feature with one distinct threshold, one that
+    no node splits on, and one with more thresholds than the LDS table holds (searched in global
+    memory)."""
+    rng = np.random.default_rng(23)
+    cfg = get_config("tiny", exact=True).with_(depth=10, n_trees=60, n_prog=700, s_max=8, p_nan=0.1,
+                                               n_features=8, name="binned-probes")
+    ens = gen_ensemble(cfg)
+    b = gen_batch(cfg)
+    internal = np.nonzero(ens["feature"] >= 0)[0]
+    feat = ens["feature"].copy()
+    thr = ens["threshold"].copy()
+    feat[feat == 7] = 6                                   # feature 7: no split
+    on0 = internal[feat[internal] == 0]
+    many = np.unique(np.float32(10.0) ** rng.uniform(-3, 3, size=4 * on0.size).astype(np.float32))
+    on0 = np.concatenate([on0, internal[feat[internal] == 5][: 22000 - on0.size]])
+    feat[on0] = 0                                         # feature 0: > 10,240 distinct thresholds
+    thr[on0] = rng.permutation(many)[: on0.size]
+    thr[internal[feat[internal] == 1]] = np.float32(0.5)  # feature 1: one threshold
+    on2 = internal[feat[internal] == 2]
+    thr[on2] = rng.choice(np.float32(10.0) ** np.linspace(-2, 2, 40).astype(np.float32), size=on2.size)
+    ens = _exact_leaves({**ens, "feature": feat, "threshold": thr})
+    assert np.unique(thr[internal[feat[internal] == 0]]).size > 10240
+    _check(cfg, ens=ens, b=b)
+
+
 @pytest.mark.parametrize("depth", [8, 10])
 def test_fp32_walk_wide_ensembles(depth):
     """More than 256 features: the fp32 walk (16-bit feature codes) scores the round."""
