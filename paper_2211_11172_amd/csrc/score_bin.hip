@@ -405,9 +405,12 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
         if (t + TW < t1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(t + TW) * S16, S16, lane);
         const bool next = piece + 1 < n_pieces;
         const int ntile = tile + dir;
-        float acc[kRPL];  // this wave's trees of the piece (at most ~100 leaves per row)
+        // this wave's leaves of the piece per row: at most 16 summed in fp32 (acc), then added to
+        // the fp64 row sum (acc64)
+        float acc[kRPL];
+        double acc64[kRPL];
 #pragma unroll
-        for (int r = 0; r < kRPL; ++r) acc[r] = 0.f;
+        for (int r = 0; r < kRPL; ++r) acc[r] = 0.f, acc64[r] = 0.0;
         for (; t < t1; t += TW) {
             walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * M, pend);
             if (t + TW < t1) tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);  // LDS operations of a wave run in order
@@ -418,6 +421,10 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
             // fair progress, every second tree: a wave behind its workgroup's average takes the top
             // issue priority
             my_done += 1;
+            if (!(my_done & 15)) {
+#pragma unroll
+                for (int r = 0; r < kRPL; ++r) acc64[r] += (double)acc[r], acc[r] = 0.f;
+            }
             if (!(my_done & 1)) {
                 uint32_t total = 0;
                 if (lane == 0) total = atomicAdd(progress + (piece & 1), 2u) + 2u;
@@ -431,14 +438,14 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
         __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) {
-            acc[r] += pend[r];
+            acc64[r] += (double)(acc[r] + pend[r]);
             pend[r] = 0.f;
         }
         const int nt0 = next ? piece_lo(ntile) : 0, nt1 = next ? piece_hi(ntile) : 0;
         if (next && nt0 + wid < nt1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(nt0 + wid) * S16, S16, lane);
         __syncthreads();  // B1: every wave is done with the tile and its slot
 #pragma unroll
-        for (int r = 0; r < kRPL; ++r) red[wid * kRT + r * 64 + lane] = (double)acc[r];
+        for (int r = 0; r < kRPL; ++r) red[wid * kRT + r * 64 + lane] = acc64[r];
         if (next && x_regs) {
             tile_commit<NT, NPX>(xf, tile_lds, F);
             if (piece + 2 < n_pieces) tile_fetch<NT, NPX>(xf, codes, ldw4, F, ntile + dir);
