@@ -12,11 +12,12 @@
 //    per-wave LDS histograms, early exit once a digit bucket holds exactly the ranks still needed;
 //    a segment of at most kk candidates keeps them all) finds the segment's kk best; they are
 //    compacted into LDS and sorted (kk <= 128: each key's slot is its rank, counted against all
-//    others by several threads per key; larger kk: bitonic).  Lanes of one LDS atomic that hit
+//    others by several threads per key; larger kk: bitonic, in the last round only).  Lanes of one LDS atomic that hit
 //    the same address are serialised, so histogram updates and compaction slots are aggregated per
 //    wave first.
-//    Segments run in parallel; their sorted outputs form the next round's candidates until one
-//    segment is left, whose workgroup writes the final top-k directly.
+//    Segments run in parallel; their selections (unsorted: the next round selects again) form the
+//    next round's candidates until one segment is left, whose workgroup writes the final top-k
+//    directly (or, sorted, for the merge).
 // K5 k_topk_merge: merges the sorted top-k of this call into the sorted running top-k by rank
 //    computation (an element's output slot is its own index plus the number of elements of the
 //    other list that rank ahead of it).
@@ -62,11 +63,13 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
 
 // FROM_SCORES: round 0 reads fp32 scores (candidate = position); later rounds read composites.
 // emit: this is the last round and its (single) workgroup writes io_score / io_index directly.
+// sort_out: the kk selected composites are written in rank order (the last round, whose list is
+// emitted or merged); the rounds before it feed another selection, which needs no order.
 template <bool FROM_SCORES>
 __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__restrict__ score, const uint64_t *__restrict__ cin,
                                                              int64_t count, int kk, uint64_t *__restrict__ cout, int emit,
-                                                             int n, int64_t index_base, float *__restrict__ out_score,
-                                                             int64_t *__restrict__ out_index) {
+                                                             int sort_out, int n, int64_t index_base,
+                                                             float *__restrict__ out_score, int64_t *__restrict__ out_index) {
     __shared__ uint32_t hist[2][256];  // digit histograms of consecutive passes (one is cleared meanwhile)
     __shared__ uint64_t sel[HARL_TOPK_MAX_K > kRankSortMax ? HARL_TOPK_MAX_K : kRankSortMax];
     __shared__ uint64_t ranked[kRankSortMax];
@@ -208,6 +211,8 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         if (part == 0 && i < kk) ranked[rank] = v;
         __syncthreads();
         out_keys = ranked;
+    } else if (!sort_out) {
+        __syncthreads();  // the selected composites, in compaction order
     } else {
         int P = 1;
         while (P < kk) P <<= 1;
@@ -347,14 +352,15 @@ int topk_launch(const float *score, int32_t n, int32_t k, int64_t index_base, fl
     for (int r = 0; r < p.rounds; ++r) {
         const int64_t c = p.counts[r];
         const unsigned segs = (unsigned)ceil_div(c, kSeg);
-        const int emit = (r == p.rounds - 1 && !merge) ? 1 : 0;
+        const int last = r == p.rounds - 1 ? 1 : 0;
+        const int emit = last && !merge ? 1 : 0;
         uint64_t *dst = buf[r & 1];
         if (r == 0)
             hipLaunchKernelGGL(k_topk_select<true>, dim3(segs), dim3(kSelThreads), 0, stream, score, nullptr, c, k, dst,
-                               emit, n, index_base, io_score, io_index);
+                               emit, last, n, index_base, io_score, io_index);
         else
             hipLaunchKernelGGL(k_topk_select<false>, dim3(segs), dim3(kSelThreads), 0, stream, score, src, c, k, dst,
-                               emit, n, index_base, io_score, io_index);
+                               emit, last, n, index_base, io_score, io_index);
         HARL_HIP_CHECK(hipGetLastError());
         src = dst;
     }
