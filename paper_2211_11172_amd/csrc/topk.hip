@@ -12,7 +12,8 @@
 //    per-wave LDS histograms, early exit once a digit bucket holds exactly the ranks still needed;
 //    a segment of at most kk candidates keeps them all) finds the segment's kk best; they are
 //    compacted into LDS and sorted (kk <= 128: each key's slot is its rank, counted against all
-//    others by several threads per key; larger kk: bitonic, in the last round only).  Lanes of one LDS atomic that hit
+//    others by several threads per key; larger kk: bitonic, in the last round only, in registers
+//    and lane shuffles up to one key per thread).  Lanes of one LDS atomic that hit
 //    the same address are serialised, so histogram updates and compaction slots are aggregated per
 //    wave first.
 //    Segments run in parallel; their selections (unsorted: the next round selects again) form the
@@ -213,6 +214,34 @@ __global__ __launch_bounds__(kSelThreads) void k_topk_select(const float *__rest
         out_keys = ranked;
     } else if (!sort_out) {
         __syncthreads();  // the selected composites, in compaction order
+    } else if (kk <= kSelThreads) {
+        // bitonic sort, descending, of the kk selected composites padded with zeros to P (a power of
+        // 2, at most one per thread): a thread holds one key; partners fewer than 64 positions away
+        // are in its wave and exchange by lane shuffles, the others through LDS (two barriers)
+        int P = 1;
+        while (P < kk) P <<= 1;
+        for (int i = kk + t; i < P; i += kSelThreads) sel[i] = 0;
+        __syncthreads();
+        uint64_t key = t < P ? sel[t] : 0;
+        for (int size = 2; size <= P; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                uint64_t other;
+                if (stride >= 64) {
+                    __syncthreads();  // the previous exchange's reads are done
+                    if (t < P) sel[t] = key;
+                    __syncthreads();
+                    other = t < P ? sel[t ^ stride] : 0;
+                } else {
+                    other = __shfl_xor(key, stride, 64);
+                }
+                // the lower position of a pair keeps the larger key in a descending block
+                const bool keep_max = ((t & stride) == 0) == ((t & size) == 0);
+                key = keep_max == (key > other) ? key : other;
+            }
+        }
+        __syncthreads();
+        if (t < P) sel[t] = key;
+        __syncthreads();
     } else {
         int P = 1;
         while (P < kk) P <<= 1;

@@ -20,8 +20,9 @@ def _scores(n, rng, ties=True):
     return s
 
 
-@pytest.mark.parametrize("n,k", [(1, 1), (7, 7), (100, 1), (4096, 128), (4097, 128), (65536, 512),
-                                 (65536, 2048), (70001, 1024), (300000, 64), (9000, 2048)])
+@pytest.mark.parametrize("n,k", [(1, 1), (7, 7), (100, 1), (4096, 128), (4097, 128), (3000, 129), (20000, 300),
+                                 (8193, 1000), (65536, 512), (65536, 2048), (70001, 1024), (300000, 64),
+                                 (9000, 2048)])
 def test_topk_matches_oracle(n, k):
     require_gpu()
     rng = np.random.default_rng(n + k)
