@@ -250,9 +250,9 @@ def ingest_calibration(args):
 
 def visit_probe(args):
     """The walk of the binned scoring kernel with its code tile and every wave's tree resident in LDS
-    (libharl_probe.so, the same walk code): node visits/s for 1 .. 12 waves per CU at depth 10 (the
-    streamed workload's trees; 12 waves is the scoring kernel's shape) and 16 at depth 9, random
-    codes (10 % missing) and random trees over 164 features.  The depth-10, 12-wave rate is the
+    (libharl_probe.so, the same walk code): node visits/s for 1 .. 16 waves per CU at depth 10 (the
+    streamed workload's trees; 16 waves is the scoring kernel's shape) and 16 at depth 9, random
+    codes (10 % missing) and random trees over 164 features.  The depth-10, 16-wave rate is the
     ceiling of the scoring kernel's walk without staging, streaming and reductions."""
     import ctypes
 
@@ -270,10 +270,10 @@ def visit_probe(args):
     d_codes = torch.from_numpy(codes.view(np.uint32).reshape(-1).copy()).cuda()
     out = torch.empty(n_blocks * 64 * 16, dtype=torch.float64, device="cuda")
     results = []
-    for depth, waves in ((10, 1), (10, 2), (10, 4), (10, 8), (10, 12), (9, 16)):
+    for depth, waves in ((10, 1), (10, 2), (10, 4), (10, 8), (10, 12), (10, 16), (9, 16)):
         M = 1 << depth
-        trees = np.zeros((n_trees, 6 * M), np.uint8)
-        words = trees.view(np.uint32)                         # [n_trees][6M / 4]
+        trees = np.zeros((n_trees, 4 * M), np.uint8)
+        words = trees.view(np.uint32)                         # [n_trees][M]: the records
         theta = rng.integers(0, 2600, size=(n_trees, M)).astype(np.uint32)
         U = (0xFFFF - theta - (rng.random((n_trees, M)) < 0.5)).astype(np.uint32)
         feats = rng.integers(0, F, size=(n_trees, M)).astype(np.uint32)
@@ -281,10 +281,12 @@ def visit_probe(args):
         i = np.arange(1, M // 2)
         words[:, 2 * i] = theta[:, i] | U[:, i] << 16                 # record i at byte 8i
         words[:, 2 * i + 1] = feats[:, 2 * i] | feats[:, 2 * i + 1] << 8
+        tails = np.zeros((n_trees, 3 * M // 2), np.uint32)           # last-level words, then leaves
         k = np.arange(M // 2)
-        words[:, M + k] = theta[:, M // 2 + k] | U[:, M // 2 + k] << 16  # last level at byte 4M + 4k
+        tails[:, k] = theta[:, M // 2 + k] | U[:, M // 2 + k] << 16
+        tails[:, M // 2:] = rng.standard_normal((n_trees, M)).astype(np.float32).view(np.uint32)
         d_trees = torch.from_numpy(trees.reshape(-1).copy()).cuda()
-        d_leaves = torch.from_numpy(rng.standard_normal((n_trees, M)).astype(np.float32)).cuda()
+        d_leaves = torch.from_numpy(tails.reshape(-1).copy()).cuda()
 
         def run(reps):
             rc = lib.harl_probe_visits(waves, depth, reps, F, n_blocks, d_codes.data_ptr(), d_trees.data_ptr(), n_trees,
@@ -313,10 +315,10 @@ def visit_probe(args):
                         "gvisits": rate / 1e9, "cycles_per_level_per_chain": cyc})
         print("probe depth %d, %d waves: %.0f Gvisit/s, %.0f cycles per level per chain" % (depth, waves, rate / 1e9, cyc),
               file=sys.stderr, flush=True)
-    ceiling = [r for r in results if r["depth"] == 10 and r["waves_per_cu"] == 12][0]["gvisits"]
+    ceiling = [r for r in results if r["depth"] == 10 and r["waves_per_cu"] == 16][0]["gvisits"]
     print(json.dumps({"metric": "visit-loop probe: node visits/s of the binned walk with every operand resident in LDS",
                       "unit": "Gvisit/s", "n_features": F, "workgroups": n_blocks,
-                      "ceiling_depth10_12waves_gvisits": ceiling, "valu_derived_peak_gvisits": PEAK_GVISITS,
+                      "ceiling_depth10_16waves_gvisits": ceiling, "valu_derived_peak_gvisits": PEAK_GVISITS,
                       "results": results}), flush=True)
 
 

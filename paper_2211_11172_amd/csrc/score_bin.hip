@@ -30,15 +30,15 @@
 // into its second byte.  Lanes read distinct banks whatever features their nodes ask for.  Tree
 // slots fill the LDS around the two row groups.
 //
-// Packed tree (D split levels, M = 2^D leaves, nodes numbered breadth-first from 1), 6M bytes:
-//   [0, 4M)        8-byte records: record 0 = {feature(1), 0}; record i, 1 <= i < M/2 (levels
-//                  0 .. D-2) = {theta(i) | U(i) << 16, feature(2i) | feature(2i+1) << 8}
-//   [4M, 6M)       last split level, node i = M/2 + k: {theta(i) | U(i) << 16} at 4M + 4k
-// and the leaves in global memory ([T][M] fp32, L2-resident with the trees), node i = M/2 + k's at
-// 2k and 2k + 1.  A level of a walk reads the current node's code and record together (one LDS round
-// trip); the record carries both children's features, so the child's code is read with the child's
-// record.  Without the leaves a depth-10 slot is 6 KB, and 12 waves fit beside the tile; each
-// chain's leaf is loaded at the end of a tree's walk and added after the next tree's.
+// Packed tree (D split levels, M = 2^D leaves, nodes numbered breadth-first from 1), 4M bytes: the
+// 8-byte records of levels 0 .. D-2, record 0 = {feature(1), 0}, record i (1 <= i < M/2) =
+// {theta(i) | U(i) << 16, feature(2i) | feature(2i+1) << 8}.  Its tail in global memory, 6M bytes
+// per tree (L2-resident with the trees): the last split level's words, node i = M/2 + k's
+// {theta(i) | U(i) << 16} at 4k, then the leaves, node M/2 + k's at 2M + 8k and 2M + 8k + 4.  A
+// level of a walk reads the current node's code and record together (one LDS round trip); the
+// record carries both children's features, so the child's code is read with the child's record.
+// A depth-10 slot is 4 KB, and 16 waves fit beside the tile; a chain reads its last-level word from
+// the tail, and its leaf is loaded at the end of a tree's walk and added after the next tree's.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     const int64_t g_tree0 = (int64_t)g * ((T_all + G - 1) / G);
     const uint4 *__restrict__ trees = trees_all + g_tree0 * S16;
     const int M = 1 << D;
-    const float *__restrict__ leaves = leaves_all + g_tree0 * M;
+    const float *__restrict__ leaves = leaves_all + g_tree0 * (3 * M / 2);  // tails
     float *__restrict__ partial = partial_all + (int64_t)g * (tiles + nbg) * kRT;
     const int64_t V = (int64_t)tiles * T, L = group_slice_len(tiles, T, nbg);
     const int64_t v_begin = (int64_t)s * L;
@@ -366,7 +366,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     // the dynamic LDS starts at address 0 (the kernel has no static LDS), so the code addresses
     // carry the row bits alone outside byte 1
     const uint32_t tb = lds_addr(smem) + slot_off;
-    const SlotConsts sk = slot_consts(tb, D);
+    const SlotConsts sk = slot_consts(tb);
     uint32_t xa[kRPL];
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
@@ -412,7 +412,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) acc[r] = 0.f, acc64[r] = 0.0;
         for (; t < t1; t += TW) {
-            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * M, pend);
+            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * (3 * M / 2), pend);
             if (t + TW < t1) tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);  // LDS operations of a wave run in order
             // unconditional, past the piece's last tree clamped to it: every pass issues the same
             // loads, so the wait for a pending leaf counts only what was issued after it (with the
@@ -481,11 +481,11 @@ struct B16Shape {
     B16Kernel kern;
 };
 // Shapes, most waves first: the first whose tree prefetch is exactly one tree per lane group and
-// whose slots fit beside the tile is used (depth 9: 3 KB slots, 3 uint4 per lane; depth 10: 6 KB, 6).
+// whose slots fit beside the tile is used (depth 9: 2 KB slots, 2 uint4 per lane; depth 10: 4 KB, 4).
 const B16Shape kShapes[] = {
-    {16, 3, k_tree_score_b16<16, 3>}, {8, 3, k_tree_score_b16<8, 3>},  {4, 3, k_tree_score_b16<4, 3>},
-    {12, 6, k_tree_score_b16<12, 6>}, {8, 6, k_tree_score_b16<8, 6>},  {4, 6, k_tree_score_b16<4, 6>},
-    {2, 6, k_tree_score_b16<2, 6>},
+    {16, 2, k_tree_score_b16<16, 2>}, {8, 2, k_tree_score_b16<8, 2>},   {4, 2, k_tree_score_b16<4, 2>},
+    {16, 4, k_tree_score_b16<16, 4>}, {12, 4, k_tree_score_b16<12, 4>}, {8, 4, k_tree_score_b16<8, 4>},
+    {4, 4, k_tree_score_b16<4, 4>},   {2, 4, k_tree_score_b16<2, 4>},
 };
 
 size_t b16_lds(const harl_ensemble *E, int tw) { return slot_plan(E->n_features, tw, (uint32_t)E->b16_stride).lds; }
@@ -674,9 +674,9 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
         const uint32_t U = (f >= 0 && dl ? 0xFFFEu : 0xFFFFu) - theta;
         return theta | U << 16;
     };
-    const int stride = 6 * M;
+    const int stride = 4 * M;  // the slot: records only
     std::vector<uint8_t> host((size_t)T * stride, 0);
-    std::vector<float> gleaves((size_t)T * M, 0.f);
+    std::vector<float> gleaves((size_t)T * (3 * M / 2), 0.f);  // tails: last-level words, leaves
     auto put = [](uint8_t *dst, uint32_t w) { std::memcpy(dst, &w, 4); };
     for (int t = 0; t < T; ++t) {
         uint8_t *tb = host.data() + (size_t)t * stride;
@@ -692,9 +692,11 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
         }
         for (int s = M / 2; s < M; ++s) {
             const int k = s - M / 2;
-            put(tb + 4 * M + 4 * k, word(ft[s], th[s], dl[s]));
-            gleaves[(size_t)t * M + 2 * k] = lf[2 * s - M];
-            gleaves[(size_t)t * M + 2 * k + 1] = lf[2 * s + 1 - M];
+            float *tail = gleaves.data() + (size_t)t * (3 * M / 2);
+            const uint32_t w = word(ft[s], th[s], dl[s]);
+            std::memcpy(tail + k, &w, 4);
+            tail[M / 2 + 2 * k] = lf[2 * s - M];
+            tail[M / 2 + 2 * k + 1] = lf[2 * s + 1 - M];
         }
     }
     // tree groups: the fewest (a power of 2 up to 8) whose share of the packed trees fits in about

@@ -91,22 +91,21 @@ struct Head {
 
 // Address constants of a wave's slot (tb) for trees of depth D, as VGPR copies made once per kernel
 // (the walk's v_cndmask selects between two of them): the root's children's records at tb + 16 and
-// tb + 24; child 2n + g of a record at a is at 2a - tb + 8g; the last-level word of the child g of a
-// level D-2 record is at a + 4g + 2M.
+// tb + 24; child 2n + g of a record at a is at 2a - tb + 8g; the last-level word of the child g of
+// the level D-2 record at a is at byte a + 4g of the tree's tail shifted back by tb + 2M.
 struct SlotConsts {
     uint32_t l0, r0, li, ri, lt, rt;
 };
-__device__ __forceinline__ SlotConsts slot_consts(uint32_t tb, int D) {
-    const uint32_t M = 1u << D;
-    return SlotConsts{in_vgpr(tb + 16u), in_vgpr(tb + 24u), in_vgpr(0u - tb), in_vgpr(8u - tb), in_vgpr(2u * M),
-                      in_vgpr(2u * M + 4u)};
+__device__ __forceinline__ SlotConsts slot_consts(uint32_t tb) {
+    return SlotConsts{in_vgpr(tb + 16u), in_vgpr(tb + 24u), in_vgpr(0u - tb), in_vgpr(8u - tb), in_vgpr(0u), in_vgpr(4u)};
 }
 
 // Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows;
 // xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each level rewrites.  The
 // rows are independent chains: each takes its step of a level in turn, so the reads of the others
-// are in flight while one decides.  The tree's leaves are at gl (M floats); each chain's leaf is
-// loaded into pend[] after the previous tree's pending leaf has been added to acc[].
+// are in flight while one decides.  The tree's tail is at gl (the M/2 last-level words, then the M
+// leaves); each chain's leaf is loaded into pend[] after the previous tree's pending leaf has been
+// added to acc[].
 __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, const Head &h, uint32_t (&xa)[kRPL],
                                      float (&acc)[kRPL],
                                      const float *__restrict__ gl, float (&pend)[kRPL]) {
@@ -141,19 +140,21 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
             __builtin_amdgcn_sched_barrier(0);
         }
     }
-    // level D-2 into the last level (node M/2 + j's word at tb + 4M + 4j)
+    // level D-2 into the last level: the D-2 record of node i at a = tb + 8i, its child M/2 + j
+    // (j = 2i + g - M/2) has its word at tail byte 4j = a + 4g - tb - 2M
+    const char *__restrict__ wb = reinterpret_cast<const char *>(gl) - (tb + 2u * M);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
         decide(x[c], rec[c].x, rec[c].y, k.lt, k.rt, xa[c], s);
         x[c] = lds_u16(xa[c]);
         a[c] = a[c] + s;
-        lw[c] = lds_b32(a[c]);
+        lw[c] = *reinterpret_cast<const uint32_t *>(wb + a[c]);
         __builtin_amdgcn_sched_barrier(0);
     }
-    // last-level node M/2 + j's leaves are at byte 8j of the tree's leaves, and 2 (tb + 4M + 4j) - 8j
-    // is the same for every j: leaf byte = lb + 2a + 4g
-    const char *__restrict__ lb = reinterpret_cast<const char *>(gl) - (2u * tb + 8u * M);
+    // last-level node M/2 + j's leaves are at tail byte 2M + 8j, and 2 (a + 4g) = 8j + 2tb + 4M:
+    // leaf byte = lb + 2 (a + 4g) + 4g' with lb = tail - 2tb - 2M
+    const char *__restrict__ lb = reinterpret_cast<const char *>(gl) - (2u * tb + 2u * M);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         const uint32_t o = leaf_off(x[c], lw[c], a[c]);
