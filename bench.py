@@ -286,7 +286,7 @@ def visit_probe(args):
         tails[:, k] = theta[:, M // 2 + k] | U[:, M // 2 + k] << 16
         tails[:, M // 2:] = rng.standard_normal((n_trees, M)).astype(np.float32).view(np.uint32)
         d_trees = torch.from_numpy(trees.reshape(-1).copy()).cuda()
-        d_leaves = torch.from_numpy(tails.reshape(-1).copy()).cuda()
+        d_leaves = torch.from_numpy(np.concatenate([tails.reshape(-1), np.zeros(1, np.uint32)])).cuda()  # then a 0
 
         def run(reps):
             rc = lib.harl_probe_visits(waves, depth, reps, F, n_blocks, d_codes.data_ptr(), d_trees.data_ptr(), n_trees,

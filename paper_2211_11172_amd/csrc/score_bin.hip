@@ -344,6 +344,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     const uint4 *__restrict__ trees = trees_all + g_tree0 * S16;
     const int M = 1 << D;
     const float *__restrict__ leaves = leaves_all + g_tree0 * (3 * M / 2);  // tails
+    const float *const zero = leaves_all + (int64_t)T_all * (3 * M / 2);     // a 0 after them
     float *__restrict__ partial = partial_all + (int64_t)g * (tiles + nbg) * kRT;
     const int64_t V = (int64_t)tiles * T, L = group_slice_len(tiles, T, nbg);
     const int64_t v_begin = (int64_t)s * L;
@@ -371,7 +372,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
 
-    constexpr bool EXACT = true;  // a slot is 6M bytes, exactly PF * 64 uint4 (host-checked)
+    constexpr bool EXACT = true;  // a slot is 4M bytes, exactly PF * 64 uint4 (host-checked)
     uint4 pf[PF];
 #pragma unroll
     for (int j = 0; j < PF; ++j) pf[j] = make_uint4(0, 0, 0, 0);
@@ -411,8 +412,10 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
         double acc64[kRPL];
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) acc[r] = 0.f, acc64[r] = 0.0;
+        LastLevel last;
+        no_last_level(last, zero);
         for (; t < t1; t += TW) {
-            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * (3 * M / 2), pend);
+            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * (3 * M / 2), pend, last);
             if (t + TW < t1) tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);  // LDS operations of a wave run in order
             // unconditional, past the piece's last tree clamped to it: every pass issues the same
             // loads, so the wait for a pending leaf counts only what was issued after it (with the
@@ -436,6 +439,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
             }
         }
         __builtin_amdgcn_s_setprio(0);
+        finish(last, acc, pend);
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) {
             acc64[r] += (double)(acc[r] + pend[r]);
@@ -676,7 +680,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     };
     const int stride = 4 * M;  // the slot: records only
     std::vector<uint8_t> host((size_t)T * stride, 0);
-    std::vector<float> gleaves((size_t)T * (3 * M / 2), 0.f);  // tails: last-level words, leaves
+    std::vector<float> gleaves((size_t)T * (3 * M / 2) + 1, 0.f);  // tails: last-level words, leaves; then a 0
     auto put = [](uint8_t *dst, uint32_t w) { std::memcpy(dst, &w, 4); };
     for (int t = 0; t < T; ++t) {
         uint8_t *tb = host.data() + (size_t)t * stride;

@@ -100,17 +100,45 @@ __device__ __forceinline__ SlotConsts slot_consts(uint32_t tb) {
     return SlotConsts{in_vgpr(tb + 16u), in_vgpr(tb + 24u), in_vgpr(0u - tb), in_vgpr(8u - tb), in_vgpr(0u), in_vgpr(4u)};
 }
 
-// Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows;
-// xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each level rewrites.  The
-// rows are independent chains: each takes its step of a level in turn, so the reads of the others
-// are in flight while one decides.  The tree's tail is at gl (the M/2 last-level words, then the M
-// leaves); each chain's leaf is loaded into pend[] after the previous tree's pending leaf has been
-// added to acc[].
+// A tree's last level, left for the next walk: per chain the code of the last-level node, its word
+// (loaded from the tail, in flight) and 2 x its word's tail offset plus shift; lb locates the leaves.
+struct LastLevel {
+    uint32_t x[kRPL], w[kRPL], a[kRPL];
+    const char *lb;
+};
+
+// A last level that loads the float at `zero` (which holds 0) for every chain: the one left before
+// a piece's first tree.
+__device__ __forceinline__ void no_last_level(LastLevel &d, const float *zero) {
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) d.x[c] = 0u, d.w[c] = 1u, d.a[c] = 0u;  // code 0 < theta 1: offset 0
+    d.lb = reinterpret_cast<const char *>(zero);
+}
+
+// The last level of tree d: each chain's leaf is loaded into pend[] after the leaf pending from the
+// tree before has been added to acc[].
+__device__ __forceinline__ void finish(const LastLevel &d, float (&acc)[kRPL], float (&pend)[kRPL]) {
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) {
+        const uint32_t o = leaf_off(d.x[c], d.w[c], d.a[c]);
+        acc[c] = add_pinned(acc[c], pend[c]);
+        __builtin_amdgcn_sched_barrier(0);
+        pend[c] = *reinterpret_cast<const float *>(d.lb + o);
+    }
+}
+
+// Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows, down
+// to its last split level; xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each
+// level rewrites.  The rows are independent chains: each takes its step of a level in turn, so the
+// reads of the others are in flight while one decides.  The tree's tail is at gl (the M/2 last-level
+// words, then the M leaves).  The last level's words are loaded from the tail and the level itself
+// is left in d: the walk first finishes the previous tree's (or no_last_level's), after its own
+// root level, so that the words have a whole walk to arrive.
 __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, const Head &h, uint32_t (&xa)[kRPL],
-                                     float (&acc)[kRPL],
-                                     const float *__restrict__ gl, float (&pend)[kRPL]) {
+                                     float (&acc)[kRPL], const float *__restrict__ gl, float (&pend)[kRPL],
+                                     LastLevel &d) {
     const uint32_t M = 1u << D;
-    uint32_t x[kRPL], a[kRPL], lw[kRPL];
+    uint32_t x[kRPL], a[kRPL];
     uint2 rec[kRPL];
     const uint32_t hf = in_vgpr(h.f);
 #pragma unroll
@@ -128,6 +156,7 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
         rec[c] = lds_b64(s);
         __builtin_amdgcn_sched_barrier(0);
     }
+    finish(d, acc, pend);
     // levels 1 .. D-3
     for (int lvl = 1; lvl + 2 < D; ++lvl) {
 #pragma unroll
@@ -147,21 +176,14 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
         decide(x[c], rec[c].x, rec[c].y, k.lt, k.rt, xa[c], s);
-        x[c] = lds_u16(xa[c]);
-        a[c] = a[c] + s;
-        lw[c] = *reinterpret_cast<const uint32_t *>(wb + a[c]);
+        d.x[c] = lds_u16(xa[c]);
+        d.a[c] = a[c] + s;
+        d.w[c] = *reinterpret_cast<const uint32_t *>(wb + d.a[c]);
         __builtin_amdgcn_sched_barrier(0);
     }
     // last-level node M/2 + j's leaves are at tail byte 2M + 8j, and 2 (a + 4g) = 8j + 2tb + 4M:
     // leaf byte = lb + 2 (a + 4g) + 4g' with lb = tail - 2tb - 2M
-    const char *__restrict__ lb = reinterpret_cast<const char *>(gl) - (2u * tb + 2u * M);
-#pragma unroll
-    for (int c = 0; c < kRPL; ++c) {
-        const uint32_t o = leaf_off(x[c], lw[c], a[c]);
-        acc[c] = add_pinned(acc[c], pend[c]);
-        __builtin_amdgcn_sched_barrier(0);
-        pend[c] = *reinterpret_cast<const float *>(lb + o);
-    }
+    d.lb = reinterpret_cast<const char *>(gl) - (2u * tb + 2u * M);
 }
 
 // LDS placement of a workgroup's tree slots: n_a slots of `sb` bytes after row group 0 (from byte

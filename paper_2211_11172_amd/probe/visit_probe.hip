@@ -42,7 +42,10 @@ __global__ __launch_bounds__(64 * TW) void k_visit_probe(const uint4 *__restrict
     float pend[kRPL] = {0.f, 0.f, 0.f, 0.f};
     const float *gl = leaves + (int64_t)tree * (3 << D) / 2;  // the tree's tail
     const SlotConsts sk = slot_consts(tb);
-    for (int r = 0; r < reps; ++r) walk(tb, D, sk, hd, xa, acc, gl, pend);
+    LastLevel last;
+    no_last_level(last, leaves + (int64_t)n_trees * (3 << D) / 2);
+    for (int r = 0; r < reps; ++r) walk(tb, D, sk, hd, xa, acc, gl, pend, last);
+    finish(last, acc, pend);
     double s = 0.0;
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) s += (double)acc[j] + (double)pend[j];
@@ -74,7 +77,7 @@ extern "C" {
 // d_trees ([n_trees][4 * 2^depth] bytes of records, the binned layout, depth 9 or 10; wave w of
 // block b walks tree (b * waves + w) % n_trees) over the code tile d_codes ([2][n_features][64]
 // dwords, row group major) with the trees' tails d_leaves ([n_trees][3 * 2^depth / 2] dwords: the
-// last level's words, then the leaves as fp32); d_out [n_blocks * 64 * waves] receives each
+// last level's words, then the leaves as fp32; then one 0.0f); d_out [n_blocks * 64 * waves] receives each
 // thread's sum (to keep the work).  Returns 0, -1 on bad arguments, -2 when the tile and slots do not
 // fit in LDS, -4 on a launch failure.
 int harl_probe_visits(int waves, int depth, int reps, int n_features, int n_blocks, const void *d_codes,
