@@ -41,9 +41,9 @@ PEAK_GVISITS = N_CU * CLOCK_GHZ * VALU_LANES_PER_CLK / VALU_PER_VISIT  # G visit
 # and by the SHA-256 of the scoring sources (score.hip, score_bin.hip, walk_b16.hpp) the counters were
 # taken with: any other source reports null.
 SCORE_TRAFFIC_BYTES = {
-    # streamed batch 0 (2,124,965 rows): k_bin16 1,385,153 + 680,682 KiB, k_tree_score_b16<12,6>
-    # 4,406,273 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
-    ("streamed", "36a995d0e6b0eb0f78610e51957d5ec7b0866b458563b4c08a2c98f9e5f45f46"): 6663006720,
+    # streamed batch 0 (2,124,965 rows): k_bin16 1,385,070 + 680,682 KiB, k_tree_score_b16<16,4>
+    # 2,161,902 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
+    ("streamed", "e8105f2efb7fcbd9ac4199a1401a863df0163f18e7d1ed161c08350f46bb19c9"): 4364685005,
 }
 
 
