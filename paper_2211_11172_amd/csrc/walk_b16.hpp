@@ -72,7 +72,8 @@ __device__ __forceinline__ void set_feature(uint32_t &xa, uint32_t fv) {
         : [f] "v"(fv));
 }
 
-// Last level: 2 a + (go right ? 4 : 0), where a is the LDS address of the last-level node's word.
+// Last level: 2 a + (go right ? 4 : 0) for the last-level node whose word is at tail byte
+// a - tb - 2M (walk).
 __device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t a) {
     uint32_t d, s;
     asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
@@ -101,7 +102,8 @@ __device__ __forceinline__ SlotConsts slot_consts(uint32_t tb) {
 }
 
 // A tree's last level, left for the next walk: per chain the code of the last-level node, its word
-// (loaded from the tail, in flight) and 2 x its word's tail offset plus shift; lb locates the leaves.
+// (loaded from the tail, in flight) and a, its word's tail byte plus tb + 2M; lb locates the
+// leaves (leaf byte lb + 2a + 4g).
 struct LastLevel {
     uint32_t x[kRPL], w[kRPL], a[kRPL];
     const char *lb;
