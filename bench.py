@@ -272,21 +272,26 @@ def visit_probe(args):
     results = []
     for depth, waves in ((10, 1), (10, 2), (10, 4), (10, 8), (10, 12), (10, 16), (9, 16)):
         M = 1 << depth
-        trees = np.zeros((n_trees, 4 * M), np.uint8)
-        words = trees.view(np.uint32)                         # [n_trees][M]: the records
+        trees = np.zeros((n_trees, 2 * M), np.uint8)
+        words = trees.view(np.uint32)                         # [n_trees][M / 2]: the records
         theta = rng.integers(0, 2600, size=(n_trees, M)).astype(np.uint32)
         U = (0xFFFF - theta - (rng.random((n_trees, M)) < 0.5)).astype(np.uint32)
         feats = rng.integers(0, F, size=(n_trees, M)).astype(np.uint32)
+        node_word = theta | U << 16
         words[:, 0] = feats[:, 1]
-        i = np.arange(1, M // 2)
-        words[:, 2 * i] = theta[:, i] | U[:, i] << 16                 # record i at byte 8i
+        i = np.arange(1, M // 4)
+        words[:, 2 * i] = node_word[:, i]                      # record i at byte 8i
         words[:, 2 * i + 1] = feats[:, 2 * i] | feats[:, 2 * i + 1] << 8
-        tails = np.zeros((n_trees, 3 * M // 2), np.uint32)           # last-level words, then leaves
-        k = np.arange(M // 2)
-        tails[:, k] = theta[:, M // 2 + k] | U[:, M // 2 + k] << 16
-        tails[:, M // 2:] = rng.standard_normal((n_trees, M)).astype(np.float32).view(np.uint32)
+        tails = np.zeros((n_trees, 2 * M), np.uint32)          # level depth-2's records, then leaves
+        k = np.arange(M // 4)
+        s2 = M // 4 + k
+        tails[:, 4 * k] = node_word[:, s2]
+        tails[:, 4 * k + 1] = feats[:, 2 * s2] | feats[:, 2 * s2 + 1] << 8
+        tails[:, 4 * k + 2] = node_word[:, 2 * s2]
+        tails[:, 4 * k + 3] = node_word[:, 2 * s2 + 1]
+        tails[:, M:] = rng.standard_normal((n_trees, M)).astype(np.float32).view(np.uint32)
         d_trees = torch.from_numpy(trees.reshape(-1).copy()).cuda()
-        d_leaves = torch.from_numpy(np.concatenate([tails.reshape(-1), np.zeros(1, np.uint32)])).cuda()  # then a 0
+        d_leaves = torch.from_numpy(np.concatenate([tails.reshape(-1), np.zeros(2, np.uint32)])).cuda()  # then two 0s
 
         def run(reps):
             rc = lib.harl_probe_visits(waves, depth, reps, F, n_blocks, d_codes.data_ptr(), d_trees.data_ptr(), n_trees,

@@ -62,7 +62,7 @@ struct harl_ensemble {
     int32_t *d_thr_off_b16, *d_thr_len_b16;   // their offsets and lengths (padding included)
     int32_t *d_search_b16;                    // per feature: {probes | key shift << 8, bucket base}
     uint16_t *d_lut_b16;                      // per feature: thresholds below each of 4,096 key buckets
-    float *d_leaves_b16;                      // [n_trees][2^depth] leaves
+    float *d_leaves_b16;                      // tails: per tree level D-2's records and the leaves
     int32_t b16_stride, tree_groups_b16;
     int32_t b16_common_steps;                 // the probe count of the most features
 };

@@ -30,15 +30,18 @@
 // into its second byte.  Lanes read distinct banks whatever features their nodes ask for.  Tree
 // slots fill the LDS around the two row groups.
 //
-// Packed tree (D split levels, M = 2^D leaves, nodes numbered breadth-first from 1), 4M bytes: the
-// 8-byte records of levels 0 .. D-2, record 0 = {feature(1), 0}, record i (1 <= i < M/2) =
-// {theta(i) | U(i) << 16, feature(2i) | feature(2i+1) << 8}.  Its tail in global memory, 6M bytes
-// per tree (L2-resident with the trees): the last split level's words, node i = M/2 + k's
-// {theta(i) | U(i) << 16} at 4k, then the leaves, node M/2 + k's at 2M + 8k and 2M + 8k + 4.  A
-// level of a walk reads the current node's code and record together (one LDS round trip); the
-// record carries both children's features, so the child's code is read with the child's record.
-// A depth-10 slot is 4 KB, and 16 waves fit beside the tile; a chain reads its last-level word from
-// the tail, and its leaf is loaded at the end of a tree's walk and added after the next tree's.
+// Packed tree (D split levels, M = 2^D leaves, nodes numbered breadth-first from 1), 2M bytes: the
+// 8-byte records of levels 0 .. D-3, record 0 = {feature(1), 0}, record i (1 <= i < M/4) =
+// {theta(i) | U(i) << 16, feature(2i) | feature(2i+1) << 8}.  Its tail in global memory, 8M bytes
+// per tree (L2-resident with the trees): the 16-byte records of level D-2, node i = M/4 + k's
+// {theta(i) | U(i) << 16, feature(2i) | feature(2i+1) << 8, word(2i), word(2i+1)} at 16k (word(n)
+// = theta(n) | U(n) << 16 of a last-level node n), then the leaves, node M/2 + k's at 4M + 8k and
+// 4M + 8k + 4.  A level of a walk reads the current node's code and record together (one LDS round
+// trip); the record carries both children's features, so the child's code is read with the child's
+// record.  A depth-10 slot is 2 KB, and 16 waves fit beside the tile.  A chain loads its level D-2
+// record from the tail at the end of a tree's walk and takes that level during the next tree's walk,
+// after the root level, and the last level (whose word came with the record) after level 1; its leaf
+// is added during the walk after that.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -343,8 +346,8 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     const int64_t g_tree0 = (int64_t)g * ((T_all + G - 1) / G);
     const uint4 *__restrict__ trees = trees_all + g_tree0 * S16;
     const int M = 1 << D;
-    const float *__restrict__ leaves = leaves_all + g_tree0 * (3 * M / 2);  // tails
-    const float *const zero = leaves_all + (int64_t)T_all * (3 * M / 2);     // a 0 after them
+    const float *__restrict__ leaves = leaves_all + g_tree0 * (2 * M);  // tails
+    const float *const zero = leaves_all + (int64_t)T_all * (2 * M);     // two 0s after them
     float *__restrict__ partial = partial_all + (int64_t)g * (tiles + nbg) * kRT;
     const int64_t V = (int64_t)tiles * T, L = group_slice_len(tiles, T, nbg);
     const int64_t v_begin = (int64_t)s * L;
@@ -367,12 +370,12 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     // the dynamic LDS starts at address 0 (the kernel has no static LDS), so the code addresses
     // carry the row bits alone outside byte 1
     const uint32_t tb = lds_addr(smem) + slot_off;
-    const SlotConsts sk = slot_consts(tb);
+    const SlotConsts sk = slot_consts(tb, (uint32_t)M);
     uint32_t xa[kRPL];
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
 
-    constexpr bool EXACT = true;  // a slot is 4M bytes, exactly PF * 64 uint4 (host-checked)
+    constexpr bool EXACT = true;  // a slot is 2M bytes, exactly PF * 64 uint4 (host-checked)
     uint4 pf[PF];
 #pragma unroll
     for (int j = 0; j < PF; ++j) pf[j] = make_uint4(0, 0, 0, 0);
@@ -412,10 +415,10 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
         double acc64[kRPL];
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) acc[r] = 0.f, acc64[r] = 0.0;
-        LastLevel last;
-        no_last_level(last, zero);
+        Deferred last;
+        no_deferred(last, zero);
         for (; t < t1; t += TW) {
-            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * (3 * M / 2), pend, last);
+            walk(tb, D, sk, hd, xa, acc, leaves + (int64_t)t * (2 * M), pend, last);
             if (t + TW < t1) tree_commit<PF, EXACT>(pf, slot, S16, lane, hd);  // LDS operations of a wave run in order
             // unconditional, past the piece's last tree clamped to it: every pass issues the same
             // loads, so the wait for a pending leaf counts only what was issued after it (with the
@@ -439,7 +442,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
             }
         }
         __builtin_amdgcn_s_setprio(0);
-        finish(last, acc, pend);
+        finish(last, xa, acc, pend);
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) {
             acc64[r] += (double)(acc[r] + pend[r]);
@@ -485,11 +488,10 @@ struct B16Shape {
     B16Kernel kern;
 };
 // Shapes, most waves first: the first whose tree prefetch is exactly one tree per lane group and
-// whose slots fit beside the tile is used (depth 9: 2 KB slots, 2 uint4 per lane; depth 10: 4 KB, 4).
+// whose slots fit beside the tile is used (depth 9: 1 KB slots, 1 uint4 per lane; depth 10: 2 KB, 2).
 const B16Shape kShapes[] = {
-    {16, 2, k_tree_score_b16<16, 2>}, {8, 2, k_tree_score_b16<8, 2>},   {4, 2, k_tree_score_b16<4, 2>},
-    {16, 4, k_tree_score_b16<16, 4>}, {12, 4, k_tree_score_b16<12, 4>}, {8, 4, k_tree_score_b16<8, 4>},
-    {4, 4, k_tree_score_b16<4, 4>},   {2, 4, k_tree_score_b16<2, 4>},
+    {16, 1, k_tree_score_b16<16, 1>}, {8, 1, k_tree_score_b16<8, 1>}, {4, 1, k_tree_score_b16<4, 1>},
+    {16, 2, k_tree_score_b16<16, 2>}, {8, 2, k_tree_score_b16<8, 2>}, {4, 2, k_tree_score_b16<4, 2>},
 };
 
 size_t b16_lds(const harl_ensemble *E, int tw) { return slot_plan(E->n_features, tw, (uint32_t)E->b16_stride).lds; }
@@ -678,35 +680,41 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
         const uint32_t U = (f >= 0 && dl ? 0xFFFEu : 0xFFFFu) - theta;
         return theta | U << 16;
     };
-    const int stride = 4 * M;  // the slot: records only
+    const int stride = 2 * M;  // the slot: records of levels 0 .. D-3
     std::vector<uint8_t> host((size_t)T * stride, 0);
-    std::vector<float> gleaves((size_t)T * (3 * M / 2) + 1, 0.f);  // tails: last-level words, leaves; then a 0
+    std::vector<uint32_t> tails((size_t)T * (2 * M) + 2, 0u);  // level D-2 records, leaves; then two 0s
     auto put = [](uint8_t *dst, uint32_t w) { std::memcpy(dst, &w, 4); };
     for (int t = 0; t < T; ++t) {
         uint8_t *tb = host.data() + (size_t)t * stride;
+        uint32_t *tail = tails.data() + (size_t)t * (2 * M);
         const int32_t *ft = feat.data() + (size_t)t * M;
         const float *th = thr.data() + (size_t)t * M;
         const uint8_t *dl = dleft.data() + (size_t)t * M;
         const float *lf = leaf.data() + (size_t)t * M;
         auto fcode = [&](int s) { return (uint32_t)(ft[s] >= 0 ? ft[s] : 0); };
         put(tb, fcode(1));
-        for (int s = 1; s < M / 2; ++s) {
+        for (int s = 1; s < M / 4; ++s) {
             put(tb + 8 * s, word(ft[s], th[s], dl[s]));
             put(tb + 8 * s + 4, fcode(2 * s) | fcode(2 * s + 1) << 8);
         }
+        for (int s = M / 4; s < M / 2; ++s) {
+            uint32_t *r = tail + 4 * (s - M / 4);
+            r[0] = word(ft[s], th[s], dl[s]);
+            r[1] = fcode(2 * s) | fcode(2 * s + 1) << 8;
+            r[2] = word(ft[2 * s], th[2 * s], dl[2 * s]);
+            r[3] = word(ft[2 * s + 1], th[2 * s + 1], dl[2 * s + 1]);
+        }
         for (int s = M / 2; s < M; ++s) {
             const int k = s - M / 2;
-            float *tail = gleaves.data() + (size_t)t * (3 * M / 2);
-            const uint32_t w = word(ft[s], th[s], dl[s]);
-            std::memcpy(tail + k, &w, 4);
-            tail[M / 2 + 2 * k] = lf[2 * s - M];
-            tail[M / 2 + 2 * k + 1] = lf[2 * s + 1 - M];
+            std::memcpy(tail + M + 2 * k, lf + (2 * s - M), 4);
+            std::memcpy(tail + M + 2 * k + 1, lf + (2 * s + 1 - M), 4);
         }
     }
-    // tree groups: the fewest (a power of 2 up to 8) whose share of the packed trees fits in about
-    // 3 MB of an XCD's 4 MB L2
+    // tree groups: the fewest (a power of 2 up to 8) whose share of the records a tile walk reads
+    // (the slots and the level D-2 records, 6M bytes per tree) fits in about 4.5 MB, a little over an
+    // XCD's 4 MB L2
     int G = 1;
-    while (G < 8 && 2 * G <= T && (int64_t)T * stride / G > (3 << 20)) G *= 2;
+    while (G < 8 && 2 * G <= T && (int64_t)T * 6 * M / G > (9 << 19)) G *= 2;
     if (E->tree_groups_override > 0 && E->tree_groups_override <= T) G = E->tree_groups_override;
     void *d_trees = nullptr, *d_thr = nullptr, *d_off = nullptr, *d_len = nullptr, *d_search = nullptr, *d_lut = nullptr,
          *d_gl = nullptr;
@@ -717,7 +725,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     if (hipMalloc(&d_trees, host.size()) != hipSuccess || hipMalloc(&d_thr, flat.size() * 4) != hipSuccess ||
         hipMalloc(&d_off, (size_t)F * 4) != hipSuccess || hipMalloc(&d_len, (size_t)F * 4) != hipSuccess ||
         hipMalloc(&d_search, search.size() * 4) != hipSuccess || hipMalloc(&d_lut, lut.size() * 2) != hipSuccess ||
-        hipMalloc(&d_gl, gleaves.size() * 4) != hipSuccess) {
+        hipMalloc(&d_gl, tails.size() * 4) != hipSuccess) {
         cleanup();
         return fail(HARL_E_NOMEM, "harl_ensemble_create: device allocation failed");
     }
@@ -727,7 +735,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     if (e == hipSuccess) e = hipMemcpyAsync(d_len, len.data(), (size_t)F * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(d_search, search.data(), search.size() * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(d_lut, lut.data(), lut.size() * 2, hipMemcpyHostToDevice, stream);
-    if (e == hipSuccess) e = hipMemcpyAsync(d_gl, gleaves.data(), gleaves.size() * 4, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(d_gl, tails.data(), tails.size() * 4, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) {
         cleanup();

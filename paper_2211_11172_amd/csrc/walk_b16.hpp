@@ -72,9 +72,27 @@ __device__ __forceinline__ void set_feature(uint32_t &xa, uint32_t fv) {
         : [f] "v"(fv));
 }
 
-// Last level: 2 a + (go right ? 4 : 0) for the last-level node whose word is at tail byte
-// a - tb - 2M (walk).
-__device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t a) {
+// The decision at a node of level D-2 from its tail record r = {word, children's features, left
+// child's word, right child's word}: writes the child's feature into byte 1 of xa, returns the
+// child's word in cw and j' = jj + (go right) in cj (jj = 2j for the level D-2 node j, so that j' is
+// the child's index in the last level).  The carry of the add is the decision itself.
+__device__ __forceinline__ void decide_d2(uint32_t c, const uint4 &r, uint32_t jj, uint32_t &xa, uint32_t &cw,
+                                          uint32_t &cj) {
+    uint32_t d;
+    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
+        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
+        "s_nop 1\n\t"
+        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 src1_sel:BYTE_1\n\t"
+        "v_cndmask_b32 %[cw], %[l], %[r], vcc\n\t"
+        "v_addc_co_u32 %[cj], vcc, 0, %[jj], vcc"
+        : [d] "=&v"(d), [xa] "+v"(xa), [cw] "=&v"(cw), [cj] "=&v"(cj)
+        : [c] "v"(c), [w] "v"(r.x), [p] "v"(r.y), [l] "v"(r.z), [r] "v"(r.w), [jj] "v"(jj)
+        : "vcc");
+}
+
+// Last level: 8 j + (go right ? 4 : 0), the byte offset of the leaf reached from last-level node j
+// (code c, word w) among the tree's leaves.
+__device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t j) {
     uint32_t d, s;
     asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
         "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
@@ -83,62 +101,91 @@ __device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t a)
         : [d] "=&v"(d), [s] "=&v"(s)
         : [c] "v"(c), [w] "v"(w)
         : "vcc");
-    return 2u * a + s;
+    return 8u * j + s;
 }
 
 struct Head {
     uint32_t f, w, p;  // root feature, root word, root's children's features (D >= 2)
 };
 
-// Address constants of a wave's slot (tb) for trees of depth D, as VGPR copies made once per kernel
-// (the walk's v_cndmask selects between two of them): the root's children's records at tb + 16 and
-// tb + 24; child 2n + g of a record at a is at 2a - tb + 8g; the last-level word of the child g of
-// the level D-2 record at a is at byte a + 4g of the tree's tail shifted back by tb + 2M.
+// Address constants of a wave's slot (tb) for trees of depth D (M = 2^D): the root's children's
+// records at tb + 16 and tb + 24; child 2n + g of a record at a is at 2a - tb + 8g; the tail record of
+// child g of the level D-3 record at a is at tail byte 4a + 16g - 4 (tb + M).  The walk's v_cndmask
+// selects between two VGPR copies: those of the inner levels are made once per kernel, the others
+// where they are used (fewer registers live through the walk).
 struct SlotConsts {
-    uint32_t l0, r0, li, ri, lt, rt;
+    uint32_t tb, lt, li, ri;
 };
-__device__ __forceinline__ SlotConsts slot_consts(uint32_t tb) {
-    return SlotConsts{in_vgpr(tb + 16u), in_vgpr(tb + 24u), in_vgpr(0u - tb), in_vgpr(8u - tb), in_vgpr(0u), in_vgpr(4u)};
+__device__ __forceinline__ SlotConsts slot_consts(uint32_t tb, uint32_t M) {
+    return SlotConsts{tb, 0u - 4u * (tb + M), in_vgpr(0u - tb), in_vgpr(8u - tb)};
 }
 
-// A tree's last level, left for the next walk: per chain the code of the last-level node, its word
-// (loaded from the tail, in flight) and a, its word's tail byte plus tb + 2M; lb locates the
-// leaves (leaf byte lb + 2a + 4g).
-struct LastLevel {
-    uint32_t x[kRPL], w[kRPL], a[kRPL];
+// A tree's last two levels, left for the next walk: per chain the code of its level D-2 node, that
+// node's tail record (loaded from global memory, in flight) and jj = 2j for the node's index j in
+// its level; lb locates the tree's leaves.
+struct Deferred {
+    uint32_t x[kRPL], jj[kRPL];
+    uint4 r[kRPL];
     const char *lb;
 };
 
-// A last level that loads the float at `zero` (which holds 0) for every chain: the one left before
-// a piece's first tree.
-__device__ __forceinline__ void no_last_level(LastLevel &d, const float *zero) {
+// A deferred tree whose leaves are the two floats at `zero` (both 0): the one left before a piece's
+// first tree.  Its record {theta 1, U 0 | features 0 | two such words} sends code 0 left, and the
+// last level's word sends any code to leaf 0 or 1.
+__device__ __forceinline__ void no_deferred(Deferred &d, const float *zero) {
 #pragma unroll
-    for (int c = 0; c < kRPL; ++c) d.x[c] = 0u, d.w[c] = 1u, d.a[c] = 0u;  // code 0 < theta 1: offset 0
+    for (int c = 0; c < kRPL; ++c) d.x[c] = 0u, d.jj[c] = 0u, d.r[c] = make_uint4(1u, 0u, 1u, 1u);
     d.lb = reinterpret_cast<const char *>(zero);
 }
 
-// The last level of tree d: each chain's leaf is loaded into pend[] after the leaf pending from the
-// tree before has been added to acc[].
-__device__ __forceinline__ void finish(const LastLevel &d, float (&acc)[kRPL], float (&pend)[kRPL]) {
+// The last level of a deferred tree, as left by step_d2: per chain the code and word of its last
+// level node and that node's index.
+struct LastLevel {
+    uint32_t x[kRPL], w[kRPL], j[kRPL];
+};
+
+// Level D-2 of the deferred tree d: each chain decides with its record and reads the code of its
+// last-level node.
+__device__ __forceinline__ void step_d2(const Deferred &d, uint32_t (&xa)[kRPL], LastLevel &e) {
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
-        const uint32_t o = leaf_off(d.x[c], d.w[c], d.a[c]);
-        acc[c] = add_pinned(acc[c], pend[c]);
+        decide_d2(d.x[c], d.r[c], d.jj[c], xa[c], e.w[c], e.j[c]);
+        e.x[c] = lds_u16(xa[c]);
         __builtin_amdgcn_sched_barrier(0);
-        pend[c] = *reinterpret_cast<const float *>(d.lb + o);
     }
 }
 
-// Walk one tree (slot at LDS address tb, depth D >= 3 at run time) for this lane's kRPL rows, down
-// to its last split level; xa[j] is the LDS address of row j's code, whose byte 1 (the feature) each
-// level rewrites.  The rows are independent chains: each takes its step of a level in turn, so the
-// reads of the others are in flight while one decides.  The tree's tail is at gl (the M/2 last-level
-// words, then the M leaves).  The last level's words are loaded from the tail and the level itself
-// is left in d: the walk first finishes the previous tree's (or no_last_level's), after its own
-// root level, so that the words have a whole walk to arrive.
+// The last level: each chain's leaf (leaves at lb) is loaded into pend[] after the leaf pending from
+// the tree before has been added to acc[].
+__device__ __forceinline__ void step_leaf(const LastLevel &e, const char *lb, float (&acc)[kRPL], float (&pend)[kRPL]) {
+#pragma unroll
+    for (int c = 0; c < kRPL; ++c) {
+        const uint32_t o = leaf_off(e.x[c], e.w[c], e.j[c]);
+        acc[c] = add_pinned(acc[c], pend[c]);
+        __builtin_amdgcn_sched_barrier(0);
+        pend[c] = *reinterpret_cast<const float *>(lb + o);
+    }
+}
+
+// Finish the deferred tree d (the last one of a piece): its last two levels.
+__device__ __forceinline__ void finish(const Deferred &d, uint32_t (&xa)[kRPL], float (&acc)[kRPL],
+                                       float (&pend)[kRPL]) {
+    LastLevel e;
+    step_d2(d, xa, e);
+    step_leaf(e, d.lb, acc, pend);
+}
+
+// Walk one tree (slot at LDS address tb, depth D >= 5 at run time) for this lane's kRPL rows, down
+// to level D-3, the last level whose records the slot holds; xa[j] is the LDS address of row j's
+// code, whose byte 1 (the feature) each level rewrites.  The rows are independent chains: each takes
+// its step of a level in turn, so the reads of the others are in flight while one decides.  The
+// tree's tail is at gl: M/4 records of 16 bytes for level D-2, then the M leaves.  Level D-2 and the
+// last level are left in d for the next walk: it first takes the previous tree's (or
+// no_deferred's) level D-2 after its own root level and that tree's last level after its own level
+// 1, so that the records and leaves loaded from the tails have a whole walk to arrive.
 __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, const Head &h, uint32_t (&xa)[kRPL],
                                      float (&acc)[kRPL], const float *__restrict__ gl, float (&pend)[kRPL],
-                                     LastLevel &d) {
+                                     Deferred &d) {
     const uint32_t M = 1u << D;
     uint32_t x[kRPL], a[kRPL];
     uint2 rec[kRPL];
@@ -148,19 +195,20 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
         set_feature(xa[c], hf);
         x[c] = lds_u16(xa[c]);
     }
-    const uint32_t hw = in_vgpr(h.w), hp = in_vgpr(h.p);
+    const uint32_t hw = in_vgpr(h.w), hp = in_vgpr(h.p), l0 = in_vgpr(k.tb + 16u), r0 = in_vgpr(k.tb + 24u);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
-        decide(x[c], hw, hp, k.l0, k.r0, xa[c], s);
+        decide(x[c], hw, hp, l0, r0, xa[c], s);
         x[c] = lds_u16(xa[c]);
         a[c] = s;
         rec[c] = lds_b64(s);
         __builtin_amdgcn_sched_barrier(0);
     }
-    finish(d, acc, pend);
-    // levels 1 .. D-3
-    for (int lvl = 1; lvl + 2 < D; ++lvl) {
+    LastLevel e;
+    step_d2(d, xa, e);
+    // levels 1 .. D-4, the previous tree's last level after level 1
+    auto inner = [&]() {
 #pragma unroll
         for (int c = 0; c < kRPL; ++c) {
             uint32_t s;
@@ -170,22 +218,25 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
             rec[c] = lds_b64(a[c]);
             __builtin_amdgcn_sched_barrier(0);
         }
-    }
-    // level D-2 into the last level: the D-2 record of node i at a = tb + 8i, its child M/2 + j
-    // (j = 2i + g - M/2) has its word at tail byte 4j = a + 4g - tb - 2M
-    const char *__restrict__ wb = reinterpret_cast<const char *>(gl) - (tb + 2u * M);
+    };
+    inner();
+    step_leaf(e, d.lb, acc, pend);
+    for (int lvl = 2; lvl + 3 < D; ++lvl) inner();
+    // level D-3 into level D-2: the D-3 record of node m at a = tb + 8m, its child n = 2m + g has its
+    // tail record at byte 16 (n - M/4) = 4a + 16g - 4 (tb + M)
+    const char *__restrict__ tail = reinterpret_cast<const char *>(gl);
+    const uint32_t lt = in_vgpr(k.lt), rt = in_vgpr(k.lt + 16u);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
-        decide(x[c], rec[c].x, rec[c].y, k.lt, k.rt, xa[c], s);
+        decide(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
         d.x[c] = lds_u16(xa[c]);
-        d.a[c] = a[c] + s;
-        d.w[c] = *reinterpret_cast<const uint32_t *>(wb + d.a[c]);
+        const uint32_t o = 4u * a[c] + s;
+        d.r[c] = *reinterpret_cast<const uint4 *>(tail + o);
+        d.jj[c] = o >> 3;
         __builtin_amdgcn_sched_barrier(0);
     }
-    // last-level node M/2 + j's leaves are at tail byte 2M + 8j, and 2 (a + 4g) = 8j + 2tb + 4M:
-    // leaf byte = lb + 2 (a + 4g) + 4g' with lb = tail - 2tb - 2M
-    d.lb = reinterpret_cast<const char *>(gl) - (2u * tb + 2u * M);
+    d.lb = tail + 4u * M;  // the leaves follow the M/4 records of 16 bytes
 }
 
 // LDS placement of a workgroup's tree slots: n_a slots of `sb` bytes after row group 0 (from byte

@@ -40,12 +40,12 @@ __global__ __launch_bounds__(64 * TW) void k_visit_probe(const uint4 *__restrict
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
     float acc[kRPL] = {0.f, 0.f, 0.f, 0.f};
     float pend[kRPL] = {0.f, 0.f, 0.f, 0.f};
-    const float *gl = leaves + (int64_t)tree * (3 << D) / 2;  // the tree's tail
-    const SlotConsts sk = slot_consts(tb);
-    LastLevel last;
-    no_last_level(last, leaves + (int64_t)n_trees * (3 << D) / 2);
+    const float *gl = leaves + (int64_t)tree * (2 << D);  // the tree's tail
+    const SlotConsts sk = slot_consts(tb, 1u << D);
+    Deferred last;
+    no_deferred(last, leaves + (int64_t)n_trees * (2 << D));
     for (int r = 0; r < reps; ++r) walk(tb, D, sk, hd, xa, acc, gl, pend, last);
-    finish(last, acc, pend);
+    finish(last, xa, acc, pend);
     double s = 0.0;
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) s += (double)acc[j] + (double)pend[j];
@@ -74,18 +74,18 @@ int launch(int F, const void *codes, const void *trees, int n_trees, int S16, in
 extern "C" {
 
 // Walk `reps` times, in n_blocks workgroups of `waves` waves (1, 2, 4, 8, 12 or 16), the packed trees
-// d_trees ([n_trees][4 * 2^depth] bytes of records, the binned layout, depth 9 or 10; wave w of
+// d_trees ([n_trees][2 * 2^depth] bytes of records, the binned layout, depth 9 or 10; wave w of
 // block b walks tree (b * waves + w) % n_trees) over the code tile d_codes ([2][n_features][64]
-// dwords, row group major) with the trees' tails d_leaves ([n_trees][3 * 2^depth / 2] dwords: the
-// last level's words, then the leaves as fp32; then one 0.0f); d_out [n_blocks * 64 * waves] receives each
-// thread's sum (to keep the work).  Returns 0, -1 on bad arguments, -2 when the tile and slots do not
+// dwords, row group major) with the trees' tails d_leaves ([n_trees][2 * 2^depth] dwords: level
+// depth-2's 16-byte records, then the leaves as fp32; then two 0.0f); d_out [n_blocks * 64 * waves]
+// receives each thread's sum (to keep the work).  Returns 0, -1 on bad arguments, -2 when the tile and slots do not
 // fit in LDS, -4 on a launch failure.
 int harl_probe_visits(int waves, int depth, int reps, int n_features, int n_blocks, const void *d_codes,
                       const void *d_trees, int n_trees, const float *d_leaves, double *d_out, void *stream) {
     if (depth < 9 || depth > 10 || reps < 1 || n_features < 1 || n_features > 256 || n_blocks < 1 || n_trees < 1 ||
         !d_codes || !d_trees || !d_leaves || !d_out)
         return -1;
-    const int S16 = (4 << depth) / 16;  // the slot: records only
+    const int S16 = (2 << depth) / 16;  // the slot: records of levels 0 .. depth-3
     hipStream_t s = static_cast<hipStream_t>(stream);
     switch (waves) {
     case 1: return launch<1>(n_features, d_codes, d_trees, n_trees, S16, depth, d_leaves, reps, n_blocks, d_out, s);
