@@ -43,19 +43,30 @@ __device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
 // One inner decision: code c at a node with word w = theta | U << 16 and child features p (byte 0
 // left, byte 1 right).  Writes the child's feature into byte 1 of the code address xa (the other
 // bytes, the lane's row, are kept) and returns sel = go right ? r : l.  The compare writes VCC and
-// the SDWA select reads it (two wait states between them).
+// the SDWA select reads it (two wait states between them).  CSEL picks the code from c: the whole
+// register (0), or its low (1) or high (2) half, for two rows' codes read as one dword.
+#define HARL_B16_DECIDE(CSEL)                                                                                       \
+    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:" CSEL " src1_sel:WORD_0\n\t" \
+        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"                                     \
+        "s_nop 1\n\t"                                                                                               \
+        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 "      \
+        "src1_sel:BYTE_1\n\t"                                                                                       \
+        "v_cndmask_b32 %[s], %[l], %[r], vcc"                                                                       \
+        : [d] "=&v"(d), [xa] "+v"(xa), [s] "=&v"(sel)                                                               \
+        : [c] "v"(c), [w] "v"(w), [p] "v"(p), [l] "v"(l), [r] "v"(r)                                                \
+        : "vcc")
+template <int CSEL = 0>
 __device__ __forceinline__ void decide(uint32_t c, uint32_t w, uint32_t p, uint32_t l, uint32_t r, uint32_t &xa,
                                        uint32_t &sel) {
     uint32_t d;
-    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
-        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
-        "s_nop 1\n\t"
-        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 src1_sel:BYTE_1\n\t"
-        "v_cndmask_b32 %[s], %[l], %[r], vcc"
-        : [d] "=&v"(d), [xa] "+v"(xa), [s] "=&v"(sel)
-        : [c] "v"(c), [w] "v"(w), [p] "v"(p), [l] "v"(l), [r] "v"(r)
-        : "vcc");
+    if constexpr (CSEL == 0)
+        HARL_B16_DECIDE("DWORD");
+    else if constexpr (CSEL == 1)
+        HARL_B16_DECIDE("WORD_0");
+    else
+        HARL_B16_DECIDE("WORD_1");
 }
+#undef HARL_B16_DECIDE
 
 // acc + leaf, kept where it stands (before the next leaf load into the same register): moved to the
 // end of a tree's walk, it kept the previous leaf alive past the new load, and the register copy at
@@ -189,17 +200,23 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
     const uint32_t M = 1u << D;
     uint32_t x[kRPL], a[kRPL];
     uint2 rec[kRPL];
+    // the root: rows j and j + 2 (chains j, j + 2) have adjacent codes of the root's feature, one
+    // dword read (xa[j] for j < 2 is 4-byte aligned)
     const uint32_t hf = in_vgpr(h.f);
+    uint32_t x01[2];
 #pragma unroll
-    for (int c = 0; c < kRPL; ++c) {
+    for (int c = 0; c < 2; ++c) {
         set_feature(xa[c], hf);
-        x[c] = lds_u16(xa[c]);
+        x01[c] = lds_b32(xa[c]);
     }
     const uint32_t hw = in_vgpr(h.w), hp = in_vgpr(h.p), l0 = in_vgpr(k.tb + 16u), r0 = in_vgpr(k.tb + 24u);
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
-        decide(x[c], hw, hp, l0, r0, xa[c], s);
+        if (c < 2)
+            decide<1>(x01[c & 1], hw, hp, l0, r0, xa[c], s);
+        else
+            decide<2>(x01[c & 1], hw, hp, l0, r0, xa[c], s);
         x[c] = lds_u16(xa[c]);
         a[c] = s;
         rec[c] = lds_b64(s);
