@@ -25,10 +25,11 @@
 //
 // Tile in LDS: row group g (rows 64g .. 64g + 63 and 128 + 64g .. 191 + 64g) at byte 65536 g, its
 // feature f at 65536 g + 256 f: dword l = {code(row 64g + l), code(row 128 + 64g + l)}.  The code of
-// lane l's row 64j + l for feature f is then at byte 65536 (j & 1) + 256 f + 4 l + 2 (j >> 1): the
-// lane and row bits of the address never change, and a decision writes the child's feature straight
-// into its second byte.  Lanes read distinct banks whatever features their nodes ask for.  Tree
-// slots fill the LDS around the two row groups.
+// lane l's row 64j + l for feature f is then half j >> 1 of the dword at byte 65536 (j & 1) + 256 f
+// + 4 l, which a walk reads whole (a decision takes the half by an SDWA select): the lane and row
+// bits of the address never change, and a decision writes the child's feature straight into its
+// second byte.  Lanes read distinct banks whatever features their nodes ask for.  Tree slots fill
+// the LDS around the two row groups.
 //
 // Packed tree (D split levels, M = 2^D leaves, nodes numbered breadth-first from 1), 2M bytes: the
 // 8-byte records of levels 0 .. D-3, record 0 = {feature(1), 0}, record i (1 <= i < M/4) =
@@ -373,7 +374,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
     const SlotConsts sk = slot_consts(tb, (uint32_t)M);
     uint32_t xa[kRPL];
 #pragma unroll
-    for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
+    for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane;
 
     constexpr bool EXACT = true;  // a slot is 2M bytes, exactly PF * 64 uint4 (host-checked)
     uint4 pf[PF];

@@ -20,9 +20,6 @@ constexpr uint32_t kMissing = 0xFFFFu;
 constexpr uint32_t kGroupStride = 65536;        // LDS bytes between the tile's two row groups
 
 // LDS accesses by absolute byte address.
-__device__ __forceinline__ uint32_t lds_u16(uint32_t a) {
-    return *(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)a;
-}
 __device__ __forceinline__ uint32_t lds_b32(uint32_t a) {
     return *(const __attribute__((address_space(3))) uint32_t *)(uintptr_t)a;
 }
@@ -86,34 +83,50 @@ __device__ __forceinline__ void set_feature(uint32_t &xa, uint32_t fv) {
 // The decision at a node of level D-2 from its tail record r = {word, children's features, left
 // child's word, right child's word}: writes the child's feature into byte 1 of xa, returns the
 // child's word in cw and j' = jj + (go right) in cj (jj = 2j for the level D-2 node j, so that j' is
-// the child's index in the last level).  The carry of the add is the decision itself.
+// the child's index in the last level).  The carry of the add is the decision itself.  CSEL as for
+// decide.
+#define HARL_B16_DECIDE_D2(CSEL)                                                                                    \
+    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:" CSEL " src1_sel:WORD_0\n\t" \
+        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"                                     \
+        "s_nop 1\n\t"                                                                                               \
+        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 "      \
+        "src1_sel:BYTE_1\n\t"                                                                                       \
+        "v_cndmask_b32 %[cw], %[l], %[r], vcc\n\t"                                                                  \
+        "v_addc_co_u32 %[cj], vcc, 0, %[jj], vcc"                                                                   \
+        : [d] "=&v"(d), [xa] "+v"(xa), [cw] "=&v"(cw), [cj] "=&v"(cj)                                               \
+        : [c] "v"(c), [w] "v"(r.x), [p] "v"(r.y), [l] "v"(r.z), [r] "v"(r.w), [jj] "v"(jj)                          \
+        : "vcc")
+template <int CSEL>
 __device__ __forceinline__ void decide_d2(uint32_t c, const uint4 &r, uint32_t jj, uint32_t &xa, uint32_t &cw,
                                           uint32_t &cj) {
     uint32_t d;
-    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
-        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
-        "s_nop 1\n\t"
-        "v_cndmask_b32_sdwa %[xa], %[p], %[p], vcc dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_0 src1_sel:BYTE_1\n\t"
-        "v_cndmask_b32 %[cw], %[l], %[r], vcc\n\t"
-        "v_addc_co_u32 %[cj], vcc, 0, %[jj], vcc"
-        : [d] "=&v"(d), [xa] "+v"(xa), [cw] "=&v"(cw), [cj] "=&v"(cj)
-        : [c] "v"(c), [w] "v"(r.x), [p] "v"(r.y), [l] "v"(r.z), [r] "v"(r.w), [jj] "v"(jj)
-        : "vcc");
+    if constexpr (CSEL == 1)
+        HARL_B16_DECIDE_D2("WORD_0");
+    else
+        HARL_B16_DECIDE_D2("WORD_1");
 }
+#undef HARL_B16_DECIDE_D2
 
 // Last level: 8 j + (go right ? 4 : 0), the byte offset of the leaf reached from last-level node j
-// (code c, word w) among the tree's leaves.
+// (code c, word w) among the tree's leaves.  CSEL as for decide.
+#define HARL_B16_LEAF(CSEL)                                                                                         \
+    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:" CSEL " src1_sel:WORD_0\n\t" \
+        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"                                     \
+        "s_nop 1\n\t"                                                                                               \
+        "v_cndmask_b32_e64 %[s], 0, 4, vcc"                                                                         \
+        : [d] "=&v"(d), [s] "=&v"(s)                                                                                \
+        : [c] "v"(c), [w] "v"(w)                                                                                    \
+        : "vcc")
+template <int CSEL>
 __device__ __forceinline__ uint32_t leaf_off(uint32_t c, uint32_t w, uint32_t j) {
     uint32_t d, s;
-    asm("v_sub_u32_sdwa %[d], %[c], %[w] dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:WORD_0\n\t"
-        "v_cmp_le_u32_sdwa vcc, %[d], %[w] src0_sel:DWORD src1_sel:WORD_1\n\t"
-        "s_nop 1\n\t"
-        "v_cndmask_b32_e64 %[s], 0, 4, vcc"
-        : [d] "=&v"(d), [s] "=&v"(s)
-        : [c] "v"(c), [w] "v"(w)
-        : "vcc");
+    if constexpr (CSEL == 1)
+        HARL_B16_LEAF("WORD_0");
+    else
+        HARL_B16_LEAF("WORD_1");
     return 8u * j + s;
 }
+#undef HARL_B16_LEAF
 
 struct Head {
     uint32_t f, w, p;  // root feature, root word, root's children's features (D >= 2)
@@ -160,8 +173,11 @@ struct LastLevel {
 __device__ __forceinline__ void step_d2(const Deferred &d, uint32_t (&xa)[kRPL], LastLevel &e) {
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
-        decide_d2(d.x[c], d.r[c], d.jj[c], xa[c], e.w[c], e.j[c]);
-        e.x[c] = lds_u16(xa[c]);
+        if (c < 2)
+            decide_d2<1>(d.x[c], d.r[c], d.jj[c], xa[c], e.w[c], e.j[c]);
+        else
+            decide_d2<2>(d.x[c], d.r[c], d.jj[c], xa[c], e.w[c], e.j[c]);
+        e.x[c] = lds_b32(xa[c]);
         __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -171,7 +187,7 @@ __device__ __forceinline__ void step_d2(const Deferred &d, uint32_t (&xa)[kRPL],
 __device__ __forceinline__ void step_leaf(const LastLevel &e, const char *lb, float (&acc)[kRPL], float (&pend)[kRPL]) {
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
-        const uint32_t o = leaf_off(e.x[c], e.w[c], e.j[c]);
+        const uint32_t o = c < 2 ? leaf_off<1>(e.x[c], e.w[c], e.j[c]) : leaf_off<2>(e.x[c], e.w[c], e.j[c]);
         acc[c] = add_pinned(acc[c], pend[c]);
         __builtin_amdgcn_sched_barrier(0);
         pend[c] = *reinterpret_cast<const float *>(lb + o);
@@ -187,8 +203,9 @@ __device__ __forceinline__ void finish(const Deferred &d, uint32_t (&xa)[kRPL], 
 }
 
 // Walk one tree (slot at LDS address tb, depth D >= 5 at run time) for this lane's kRPL rows, down
-// to level D-3, the last level whose records the slot holds; xa[j] is the LDS address of row j's
-// code, whose byte 1 (the feature) each level rewrites.  The rows are independent chains: each takes
+// to level D-3, the last level whose records the slot holds; xa[j] is the LDS address of the dword
+// that holds row j's code (its low half for j < 2, its high half for j >= 2), whose byte 1 (the
+// feature) each level rewrites.  The rows are independent chains: each takes
 // its step of a level in turn, so the reads of the others are in flight while one decides.  The
 // tree's tail is at gl: M/4 records of 16 bytes for level D-2, then the M leaves.  Level D-2 and the
 // last level are left in d for the next walk: it first takes the previous tree's (or
@@ -200,8 +217,7 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
     const uint32_t M = 1u << D;
     uint32_t x[kRPL], a[kRPL];
     uint2 rec[kRPL];
-    // the root: rows j and j + 2 (chains j, j + 2) have adjacent codes of the root's feature, one
-    // dword read (xa[j] for j < 2 is 4-byte aligned)
+    // the root: chains j and j + 2 read the two halves of one dword of the root's feature
     const uint32_t hf = in_vgpr(h.f);
     uint32_t x01[2];
 #pragma unroll
@@ -217,7 +233,7 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
             decide<1>(x01[c & 1], hw, hp, l0, r0, xa[c], s);
         else
             decide<2>(x01[c & 1], hw, hp, l0, r0, xa[c], s);
-        x[c] = lds_u16(xa[c]);
+        x[c] = lds_b32(xa[c]);
         a[c] = s;
         rec[c] = lds_b64(s);
         __builtin_amdgcn_sched_barrier(0);
@@ -229,8 +245,11 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
 #pragma unroll
         for (int c = 0; c < kRPL; ++c) {
             uint32_t s;
-            decide(x[c], rec[c].x, rec[c].y, k.li, k.ri, xa[c], s);
-            x[c] = lds_u16(xa[c]);
+            if (c < 2)
+                decide<1>(x[c], rec[c].x, rec[c].y, k.li, k.ri, xa[c], s);
+            else
+                decide<2>(x[c], rec[c].x, rec[c].y, k.li, k.ri, xa[c], s);
+            x[c] = lds_b32(xa[c]);
             a[c] = 2u * a[c] + s;
             rec[c] = lds_b64(a[c]);
             __builtin_amdgcn_sched_barrier(0);
@@ -246,8 +265,11 @@ __device__ __forceinline__ void walk(uint32_t tb, int D, const SlotConsts &k, co
 #pragma unroll
     for (int c = 0; c < kRPL; ++c) {
         uint32_t s;
-        decide(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
-        d.x[c] = lds_u16(xa[c]);
+        if (c < 2)
+            decide<1>(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
+        else
+            decide<2>(x[c], rec[c].x, rec[c].y, lt, rt, xa[c], s);
+        d.x[c] = lds_b32(xa[c]);
         const uint32_t o = 4u * a[c] + s;
         d.r[c] = *reinterpret_cast<const uint4 *>(tail + o);
         d.jj[c] = o >> 3;

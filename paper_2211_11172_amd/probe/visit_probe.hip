@@ -37,7 +37,7 @@ __global__ __launch_bounds__(64 * TW) void k_visit_probe(const uint4 *__restrict
     const uint32_t tb = lds_addr(smem) + slot_off;
     uint32_t xa[kRPL];
 #pragma unroll
-    for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane + 2u * (j >> 1);
+    for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane;
     float acc[kRPL] = {0.f, 0.f, 0.f, 0.f};
     float pend[kRPL] = {0.f, 0.f, 0.f, 0.f};
     const float *gl = leaves + (int64_t)tree * (2 << D);  // the tree's tail
