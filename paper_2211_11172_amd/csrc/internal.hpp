@@ -39,7 +39,10 @@ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 // ------------------------------------------------------------------------------------------
 constexpr int kMaxDepth = 12;
 constexpr int kMaxFeatures = 448;
-constexpr int kMinB16Depth = 9, kMaxB16Depth = 10;  // ensemble depths the binned path (score_bin.hip) walks
+constexpr int kMinB16Depth = 8, kMaxB16Depth = 10;  // ensemble depths the binned path (score_bin.hip) walks
+// Statement rows from which a depth-8 ensemble is scored on the binned path (its binning pass costs
+// more than it saves on smaller rounds); deeper ensembles take it at any size.
+constexpr int32_t kB16MinRowsDepth8 = 1 << 17;
 
 }  // namespace harl
 
@@ -55,6 +58,8 @@ struct harl_ensemble {
     int32_t cfg_wp, cfg_a, cfg_b, cfg_c;
     // tree groups forced at create (HARL_SCORE_TREE_GROUPS, for tests of the grouped layout); 0 = automatic
     int32_t tree_groups_override;
+    // binned-path row threshold forced at create (HARL_SCORE_BINNED_MIN_ROWS, for tests); -1 = automatic
+    int32_t b16_min_rows_override;
     // binned path (score_bin.hip), or null when the ensemble does not qualify: packed trees of
     // b16_stride bytes, per-feature distinct thresholds (offsets and counts per feature)
     void *d_trees_b16;
@@ -65,6 +70,7 @@ struct harl_ensemble {
     float *d_leaves_b16;                      // tails: per tree level D-2's records and the leaves
     int32_t b16_stride, tree_groups_b16;
     int32_t b16_common_steps;                 // the probe count of the most features
+    int32_t b16_min_rows;                     // rounds of fewer statement rows take the fp32 walk
 };
 
 // ------------------------------------------------------------------------------------------
@@ -97,7 +103,8 @@ void free_ensemble(harl_ensemble *E);
 int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vector<float> &thr,
              const std::vector<uint8_t> &dleft, const std::vector<float> &leaf, hipStream_t stream);
 void free_b16(harl_ensemble *E);
-bool score_b16_usable(const harl_ensemble *E);
+bool score_b16_packed(const harl_ensemble *E);
+bool score_b16_usable(const harl_ensemble *E, int32_t n_rows);
 size_t score_b16_ws_bytes(const harl_ensemble *E, int32_t n_rows);
 int score_b16_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows, float **partial_out,
                      int *groups_out, int *tiles_out, int *nbg_out, void *ws, size_t ws_bytes, hipStream_t stream);

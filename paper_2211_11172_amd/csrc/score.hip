@@ -28,6 +28,8 @@
 // own share of the ensemble.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -1012,15 +1014,18 @@ size_t partial_floats(const harl_ensemble *E, const ScoreCfg &c, int32_t n_rows)
 }  // namespace
 
 size_t score_round_ws_bytes(const harl_ensemble *E, int32_t n_rows) {
-    if (score_b16_usable(E)) return score_b16_ws_bytes(E, n_rows);
     const ScoreCfg c = stored_cfg(E);
-    return partial_floats(E, c, n_rows) * sizeof(float) + 256;
+    const size_t fp32 = partial_floats(E, c, n_rows) * sizeof(float) + 256;
+    // an ensemble with both forms takes either walk by the round's size: enough for both, so that a
+    // workspace sized for n_rows serves every smaller round too
+    if (score_b16_packed(E)) return std::max(fp32, score_b16_ws_bytes(E, n_rows));
+    return fp32;
 }
 
 int score_round_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows,
                        const int32_t *prog_ptr, int32_t n_prog, float *prog_score, float *stmt_score,
                        void *ws, size_t ws_bytes, hipStream_t stream) {
-    const bool b16 = score_b16_usable(E);
+    const bool b16 = score_b16_usable(E, n_rows);
     const ScoreCfg c = stored_cfg(E);
     const int64_t ldp = round_up(n_rows > 0 ? n_rows : 1, 64);
     if (ws_bytes < score_round_ws_bytes(E, n_rows)) return fail(HARL_E_WORKSPACE, "harl_score_round: workspace too small");
@@ -1172,6 +1177,12 @@ int pack_ensemble(const harl_ensemble_desc *d, harl_ensemble **out, hipStream_t 
     if (const char *env = std::getenv("HARL_SCORE_TREE_GROUPS")) {
         const int o = std::atoi(env);
         if ((o == 1 || o == 2 || o == 4 || o == 8) && o <= T) E->tree_groups_override = o;
+    }
+    // likewise the row count from which a depth-8 ensemble takes the binned walk
+    E->b16_min_rows_override = -1;
+    if (const char *env = std::getenv("HARL_SCORE_BINNED_MIN_ROWS")) {
+        const long o = std::atol(env);
+        if (o >= 0 && o <= INT32_MAX) E->b16_min_rows_override = (int32_t)o;
     }
     {
         const ScoreCfg c = choose_cfg(E);

@@ -1,8 +1,9 @@
-// Cost-model scoring on binned feature codes: the path harl_score_round takes for deep ensembles (9
-// or 10 split levels) of up to 256 features with at most 65,534 distinct thresholds per feature
-// (Algorithm 1's cost model C(S'), an XGBoost ensemble: Section 6.1 and Appendix A.1).  Shallower
-// ensembles use the fp32 walk of score.hip, whose 3 KB depth-8 trees already leave room for 16
-// waves per CU; at depth 10 its 12 KB trees leave room for 6.
+// Cost-model scoring on binned feature codes: the path harl_score_round takes for ensembles of 9 or
+// 10 split levels, and of 8 on rounds of at least kB16MinRowsDepth8 statement rows, of up to 256
+// features with at most 65,534 distinct thresholds per feature (Algorithm 1's cost model C(S'), an
+// XGBoost ensemble: Section 6.1 and Appendix A.1).  Other rounds use the fp32 walk of score.hip,
+// whose 3 KB depth-8 trees leave room for 16 waves per CU (at depth 10 its 12 KB trees leave room
+// for 6); on small depth-8 rounds the binning pass costs more than the binned walk saves.
 //
 // A split sends x left iff x < threshold, so a node's decision depends only on where x falls among
 // the thresholds its feature is split on.  With t_f[0] < ... < t_f[m_f - 1] the distinct thresholds
@@ -331,7 +332,7 @@ __device__ __forceinline__ void tile_stage(uint4 *tile_lds, const uint4 *__restr
     }
 }
 
-template <int TW, int PF>
+template <int TW, int PF, bool EXACT>
 __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restrict__ codes, int64_t ldw4, int n_rows,
                                                            int F, const uint4 *__restrict__ trees_all, int S16, int D,
                                                            int T_all, int G, int tiles, float *__restrict__ partial_all,
@@ -376,7 +377,7 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
 #pragma unroll
     for (int j = 0; j < kRPL; ++j) xa[j] = lds_addr(smem) + kGroupStride * (j & 1) + 4u * (uint32_t)lane;
 
-    constexpr bool EXACT = true;  // a slot is 2M bytes, exactly PF * 64 uint4 (host-checked)
+    // EXACT: a slot (2M bytes) is exactly PF * 64 uint4 (host-checked); else (depth 8) fewer
     uint4 pf[PF];
 #pragma unroll
     for (int j = 0; j < PF; ++j) pf[j] = make_uint4(0, 0, 0, 0);
@@ -486,13 +487,17 @@ using B16Kernel = void (*)(const uint4 *, int64_t, int, int, const uint4 *, int,
 
 struct B16Shape {
     int tw, pf;
+    bool exact;
     B16Kernel kern;
 };
-// Shapes, most waves first: the first whose tree prefetch is exactly one tree per lane group and
-// whose slots fit beside the tile is used (depth 9: 1 KB slots, 1 uint4 per lane; depth 10: 2 KB, 2).
+// Shapes, most waves first: the first whose tree prefetch is one tree per lane group (exactly, or
+// half of it at depth 8) and whose slots fit beside the tile is used (depth 8: 512 B slots; depth 9:
+// 1 KB, 1 uint4 per lane; depth 10: 2 KB, 2).
 const B16Shape kShapes[] = {
-    {16, 1, k_tree_score_b16<16, 1>}, {8, 1, k_tree_score_b16<8, 1>}, {4, 1, k_tree_score_b16<4, 1>},
-    {16, 2, k_tree_score_b16<16, 2>}, {8, 2, k_tree_score_b16<8, 2>}, {4, 2, k_tree_score_b16<4, 2>},
+    {16, 1, false, k_tree_score_b16<16, 1, false>}, {8, 1, false, k_tree_score_b16<8, 1, false>},
+    {16, 1, true, k_tree_score_b16<16, 1, true>},   {8, 1, true, k_tree_score_b16<8, 1, true>},
+    {4, 1, true, k_tree_score_b16<4, 1, true>},     {16, 2, true, k_tree_score_b16<16, 2, true>},
+    {8, 2, true, k_tree_score_b16<8, 2, true>},     {4, 2, true, k_tree_score_b16<4, 2, true>},
 };
 
 size_t b16_lds(const harl_ensemble *E, int tw) { return slot_plan(E->n_features, tw, (uint32_t)E->b16_stride).lds; }
@@ -500,7 +505,8 @@ size_t b16_lds(const harl_ensemble *E, int tw) { return slot_plan(E->n_features,
 const B16Shape *b16_shape(const harl_ensemble *E) {
     const int s16 = E->b16_stride / 16;
     for (const B16Shape &sh : kShapes)
-        if (sh.pf * kWave == s16 && b16_lds(E, sh.tw) <= (size_t)kLdsBytes) return &sh;
+        if ((sh.exact ? sh.pf * kWave == s16 : 2 * s16 == sh.pf * kWave) && b16_lds(E, sh.tw) <= (size_t)kLdsBytes)
+            return &sh;
     return nullptr;
 }
 
@@ -546,7 +552,8 @@ size_t score_b16_ws_bytes(const harl_ensemble *E, int32_t n_rows) {
     return round_up((int64_t)codes, 256) + partial + 256;
 }
 
-bool score_b16_usable(const harl_ensemble *E) { return E->d_trees_b16 != nullptr && b16_shape(E) != nullptr; }
+bool score_b16_packed(const harl_ensemble *E) { return E->d_trees_b16 != nullptr && b16_shape(E) != nullptr; }
+bool score_b16_usable(const harl_ensemble *E, int32_t n_rows) { return score_b16_packed(E) && n_rows >= E->b16_min_rows; }
 
 int score_b16_launch(const harl_ensemble *E, const float *X, int64_t ld, int32_t n_rows, float **partial_out,
                      int *groups_out, int *tiles_out, int *nbg_out, void *ws, size_t ws_bytes, hipStream_t stream) {
@@ -752,6 +759,7 @@ int pack_b16(harl_ensemble *E, const std::vector<int32_t> &feat, const std::vect
     E->b16_stride = stride;
     E->tree_groups_b16 = G;
     E->b16_common_steps = common_steps;
+    E->b16_min_rows = E->b16_min_rows_override >= 0 ? E->b16_min_rows_override : (D <= 8 ? kB16MinRowsDepth8 : 0);
     return HARL_OK;
 }
 

@@ -133,8 +133,9 @@ def test_deterministic_repeat():
     assert a1.tobytes() == a2.tobytes() and s1.tobytes() == s2.tobytes()
 
 
-# ---- the binned path (ensembles of depth 9 or 10, <= 256 features, <= 65,534 distinct thresholds
-# per feature) and the fp32 walks that remain for the others ----
+# ---- the binned path (ensembles of depth 9 or 10, and of depth 8 on rounds of at least 2^17
+# statement rows; <= 256 features, <= 65,534 distinct thresholds per feature) and the fp32 walks
+# that remain for the others ----
 def _exact_leaves(ens):
     return {**ens, "leaf_value": (np.round(ens["leaf_value"] * 4096) / 4096).astype(np.float32)}
 
@@ -146,6 +147,44 @@ def test_binned_depths_exact(depth, n_prog):
     cfg = get_config("tiny", exact=True).with_(depth=depth, n_trees=23, n_prog=n_prog, s_max=9, p_nan=0.15,
                                                name="binned-d%d-p%d" % (depth, n_prog))
     _check(cfg)
+
+
+@pytest.mark.parametrize("n_prog,groups", [(611, 0), (5, 0), (900, 2), (900, 4)])
+def test_binned_depth8_exact(n_prog, groups, monkeypatch):
+    """Depth 8 on the binned walk (its slots are half a prefetch wide), forced below the row count
+    from which it is taken by default, with tree groups: bit-exact against the oracle."""
+    monkeypatch.setenv("HARL_SCORE_BINNED_MIN_ROWS", "0")
+    if groups:
+        monkeypatch.setenv("HARL_SCORE_TREE_GROUPS", str(groups))
+    cfg = get_config("tiny", exact=True).with_(depth=8, n_trees=31, n_prog=n_prog, s_max=9, p_nan=0.15,
+                                               name="binned-d8-p%d-g%d" % (n_prog, groups))
+    _check(cfg)
+
+
+@pytest.mark.parametrize("above", [True, False])
+def test_depth8_route_by_round_size_exact(above, monkeypatch):
+    """A depth-8 ensemble takes the binned walk from a row count on and the fp32 walk below it; both
+    routes, on the same ensemble and batch, are bit-exact against the oracle."""
+    cfg = get_config("tiny", exact=True).with_(depth=8, n_trees=29, n_prog=300, s_max=9, p_nan=0.1,
+                                               name="route-d8")
+    n_rows = gen_batch(cfg)["n_rows"]
+    monkeypatch.setenv("HARL_SCORE_BINNED_MIN_ROWS", str(n_rows if above else n_rows + 1))
+    _check(cfg)
+
+
+def test_binned_depth8_irregular_trees(monkeypatch):
+    """Early leaves (dummy splits below them) at depth 8 on the binned walk."""
+    monkeypatch.setenv("HARL_SCORE_BINNED_MIN_ROWS", "0")
+    rng = np.random.default_rng(29)
+    cfg = mini_config(p_nan=0.1, n_features=12, n_prog=400, s_max=9)
+    b = gen_batch(cfg)
+    pool = np.unique(b["features"][~np.isnan(b["features"])])
+    ens = _irregular_ensemble(rng, n_trees=21, n_features=12, max_depth=8, thr_pool=pool)
+
+    def depth(n):
+        return 0 if ens["feature"][n] < 0 else 1 + max(depth(ens["left"][n]), depth(ens["right"][n]))
+    assert max(depth(r) for r in ens["root"]) == 8
+    _check(cfg, ens=_exact_leaves(ens), b=b, exact=True)
 
 
 @pytest.mark.parametrize("groups", [2, 4, 8])
