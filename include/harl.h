@@ -119,8 +119,9 @@ size_t harl_score_round_workspace_size(const harl_ensemble *ens, int32_t n_rows,
  *   d_stmt_score [n_rows] fp32 out, or NULL: each statement row's ensemble sum.
  *   d_ws, ws_bytes  device workspace of at least harl_score_round_workspace_size() bytes,
  *               256-byte aligned; its contents on entry are ignored.
- * Sums over trees and over a program's statements are accumulated in fp64 in a fixed order and
- * rounded once to fp32.  n_prog == 0 is a no-op.
+ * Sums over trees (on the binned path of 8- to 10-level ensembles in fp32 over at most 16 trees
+ * at a time, then in fp64) and over a program's statements (fp64) are accumulated in a fixed order
+ * and rounded once to fp32.  n_prog == 0 is a no-op.
  */
 int harl_score_round(const harl_ensemble *ens, const float *d_feat, int64_t ld, int32_t n_rows,
                      const int32_t *d_prog_ptr, int32_t n_prog, float *d_prog_score,
