@@ -172,6 +172,41 @@ def test_depth8_route_by_round_size_exact(above, monkeypatch):
     _check(cfg)
 
 
+def test_depth8_workspace_serves_smaller_rounds_exact(monkeypatch):
+    """A workspace sized for a round that takes the binned walk serves a smaller round of the same
+    depth-8 ensemble on the fp32 walk (and the other way round): both calls, on one workspace of the
+    larger round's size, are bit-exact against the oracle."""
+    require_gpu()
+    import torch
+    from paper_2211_11172_amd import harl
+    cfg = get_config("tiny", exact=True).with_(depth=8, n_trees=27, n_prog=600, s_max=9, p_nan=0.1,
+                                               name="ws-d8")
+    ens, b = gen_ensemble(cfg), gen_batch(cfg)
+    ptr_all = b["prog_ptr"]
+    small = 150                                           # programs of the smaller round
+    n_small, n_big = int(ptr_all[small]), int(ptr_all[-1])
+    monkeypatch.setenv("HARL_SCORE_BINNED_MIN_ROWS", str(n_small + 1))   # big: binned, small: fp32
+    E = harl.harl_ensemble_create(ens)
+    try:
+        ws_small = harl.harl_score_round_workspace_size(E, n_small, small)
+        wsb = harl.harl_score_round_workspace_size(E, n_big, len(ptr_all) - 1)
+        assert wsb >= ws_small
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        for n_prog in (len(ptr_all) - 1, small):
+            ptr = ptr_all[: n_prog + 1]
+            n_rows = int(ptr[-1])
+            X = np.ascontiguousarray(b["features"][:, :n_rows])
+            want = oracle.score_round(ens, X, ptr)
+            Xd = torch.from_numpy(X).cuda()
+            ptr_d = torch.from_numpy(np.ascontiguousarray(ptr, np.int32)).cuda()
+            ps = torch.full((n_prog,), np.nan, dtype=torch.float32, device="cuda")
+            harl.harl_score_round(E, Xd, X.shape[1], n_rows, ptr_d, n_prog, ps, None, ws, wsb)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(ps.cpu().numpy(), want["prog32"])
+    finally:
+        E.close()
+
+
 def test_binned_depth8_irregular_trees(monkeypatch):
     """Early leaves (dummy splits below them) at depth 8 on the binned walk."""
     monkeypatch.setenv("HARL_SCORE_BINNED_MIN_ROWS", "0")
