@@ -30,7 +30,7 @@ N_CU, CLOCK_GHZ = 256, 2.4
 # 2.4 GHz = 39.3 T VALU lane-instructions/s, and a visit of the walk needs at least 5 VALU
 # instructions (a subtraction and a compare that decide the child, two selects for the child's
 # feature and record, one address update) -> 7.86 T visits/s.  The LDS allows a similar figure: at
-# 128 B/clk/CU a wave's 2-byte code reads take 2 clocks (a dword's bank slot each) and its 8-byte
+# 128 B/clk/CU a wave's code reads take 2 clocks (a dword that holds the row's code) and its 8-byte
 # node-record reads 4, and the binned walk reads records from LDS on 7 of its 10 levels (about 5.1
 # clocks per visit: 7.7 T visits/s).
 VALU_LANES_PER_CLK = 4 * 16
