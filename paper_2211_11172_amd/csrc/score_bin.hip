@@ -445,16 +445,19 @@ __global__ __launch_bounds__(64 * TW) void k_tree_score_b16(const uint4 *__restr
         }
         __builtin_amdgcn_s_setprio(0);
         finish(last, xa, acc, pend);
+        const int nt0 = next ? piece_lo(ntile) : 0, nt1 = next ? piece_hi(ntile) : 0;
+        // the next piece's first tree, fetched unconditionally (clamped to a tree of the group; a wave
+        // with no tree there never commits it), so that the wait for the last leaves counts the same
+        // loads on every path: with the fetch conditional, the compiler's count waited for it too.
+        // The leaves are added after B1, their loads in flight meanwhile.
+        tree_fetch<PF, EXACT>(pf, trees + (int64_t)min(nt0 + wid, T - 1) * S16, S16, lane);
+        __syncthreads();  // B1: every wave is done with the tile and its slot
 #pragma unroll
         for (int r = 0; r < kRPL; ++r) {
             acc64[r] += (double)(acc[r] + pend[r]);
             pend[r] = 0.f;
+            red[wid * kRT + r * 64 + lane] = acc64[r];
         }
-        const int nt0 = next ? piece_lo(ntile) : 0, nt1 = next ? piece_hi(ntile) : 0;
-        if (next && nt0 + wid < nt1) tree_fetch<PF, EXACT>(pf, trees + (int64_t)(nt0 + wid) * S16, S16, lane);
-        __syncthreads();  // B1: every wave is done with the tile and its slot
-#pragma unroll
-        for (int r = 0; r < kRPL; ++r) red[wid * kRT + r * 64 + lane] = acc64[r];
         if (next && x_regs) {
             tile_commit<NT, NPX>(xf, tile_lds, F);
             if (piece + 2 < n_pieces) tile_fetch<NT, NPX>(xf, codes, ldw4, F, ntile + dir);
