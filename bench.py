@@ -43,9 +43,9 @@ PEAK_GVISITS = N_CU * CLOCK_GHZ * VALU_LANES_PER_CLK / VALU_PER_VISIT  # G visit
 # and by the SHA-256 of the scoring sources (score.hip, score_bin.hip, walk_b16.hpp) the counters were
 # taken with: any other source reports null.
 SCORE_TRAFFIC_BYTES = {
-    # streamed batch 0 (2,124,965 rows): k_bin16 1,385,079 + 680,682 KiB, k_tree_score_b16<16,2,true>
-    # 1,461,307 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
-    ("streamed", "dd30f8dd9e458f3bcbc42e19f48f589e76fef141217974207653a72ecc657404"): 3647285227,
+    # streamed batch 0 (2,124,965 rows): k_bin16 1,385,001 + 680,682 KiB, k_tree_score_b16<16,2,true>
+    # 1,459,893 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
+    ("streamed", "4742154bfc00676184204f6d616e8f8b1f28895528ddcbcc8e6d96f9ced7e6ac"): 3645757120,
 }
 
 
