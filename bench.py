@@ -46,6 +46,9 @@ SCORE_TRAFFIC_BYTES = {
     # streamed batch 0 (2,124,965 rows): k_bin16 1,385,001 + 680,682 KiB, k_tree_score_b16<16,2,true>
     # 1,459,893 + 16,855 KiB, k_segsum 17,623 + 256 KiB (read + written)
     ("streamed", "4742154bfc00676184204f6d616e8f8b1f28895528ddcbcc8e6d96f9ced7e6ac"): 3645757120,
+    # throughput round (2,134,518 rows, depth 8 on the binned walk): k_bin16 1,384,007 + 683,716 KiB,
+    # k_tree_score_b16<16,1,false> 698,301 + 8,592 KiB, k_segsum 9,235 + 256 KiB
+    ("throughput", "4742154bfc00676184204f6d616e8f8b1f28895528ddcbcc8e6d96f9ced7e6ac"): 2850925363,
 }
 
 
