@@ -809,7 +809,9 @@ def round_bench(args):
     pol_tflops = n_prog * flops_per_state / (pol_mean_us * 1e-6) / 1e12
     ms_per_step = el * 1e3 / args.steps
     hbm_gbs = alg_bytes / (score_mean_us * 1e-6) / 1e9
-    kern = ("k_bin16 + k_tree_score_b16 + k_segsum" if 9 <= cfg.depth <= 10 else "k_tree_score + k_segsum")
+    # the library's route: the binned walk for depth 9-10, and for depth 8 from 2^17 statement rows
+    binned = 9 <= cfg.depth <= 10 or (cfg.depth == 8 and n_rows >= 1 << 17)
+    kern = "k_bin16 + k_tree_score_b16 + k_segsum" if binned else "k_tree_score_wp + k_segsum"
     roof = {"bound": "alu", "kernel": kern + " via harl_score_round",
             "achieved": gvisits, "peak": PEAK_GVISITS, "unit": "Gvisit/s", "frac": gvisits / PEAK_GVISITS,
             "traffic": score_traffic(cfg.name), "traffic_unit": "HBM bytes per launch",
